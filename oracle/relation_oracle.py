@@ -1,0 +1,259 @@
+"""fp64 CPU oracle for the causal Full Relation operator (Self-Exchange Relation).
+
+TEST INFRASTRUCTURE. Only the tests, the smoke check and the benchmark's CPU
+baseline leg may import this module. The product path (the HIP library and its
+Python binding) never calls it, and it shares no code with that path.
+
+What it computes: the plain definition of one Relation head, written out in
+fp64 with the T x T matrices materialised, following the paper:
+  * pairwise evidence  U_ij = p1_i . p2_j / sqrt(d_h)                 (eq. 1)
+  * Self map           S_i  = sigmoid(U_ii / tau_S), tau_S = 2        (eq. 2)
+  * Exchange map       E_ij = SiLU(U_ij)                              (eq. 2)
+  * causal Relation    R_ii = S_i; R_ij = E_ij - lambda log i (j < i);
+                       R_ij = -inf (j > i); i is one-based            (eq. 2; App. A.1.1)
+  * flow and transport F_i = Softmax(R_i), Y_i = sum_{j<=i} F_ij I~_j (eq. 3)
+The derived quantities (Self mass, aggregate Exchange mass g, Exchange
+log-normaliser L^E, count-corrected aggregate A, allocation pi) follow
+eqs. (5)-(7) / App. A.1.2-A.1.4. The backward pass is computed by two
+independent routes from App. A.1.7: through the softmax Jacobian of F, and
+through the Self-Exchange factorisation (g, pi, c).
+
+The oracle consumes exactly the values given to the GPU (bf16 inputs are
+rounded by the caller and passed here as fp64). Library primitives used as
+steps: numpy matmul, scipy.special.expit / softmax / logsumexp.
+
+Conventions where the paper leaves a choice (each is listed with its reason in
+the design notes): the log is natural; row 1 has an empty history, so its
+L^E and A are -inf, g_1 = 0 and pi_1 = 0; the saved statistic for the
+backward pass is M_i = ln Z_i + lambda ln i.
+
+Rows are processed in blocks of ``row_block`` rows purely to bound memory at
+long T. Rows of F are independent (each is its own softmax), so the blocking
+changes no arithmetic of a row; only the order of the column sums that form
+dK and dV changes, at fp64 rounding level.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+from scipy.special import expit, logsumexp, softmax
+
+__all__ = ["forward", "backward", "TAU_S"]
+
+TAU_S = 2.0  # Self temperature used in all of the paper's experiments (Sec. 3.1)
+
+
+def _scale(D: int, scale: float | None) -> float:
+    # 1/sqrt(d_h) sits inside U (eq. 1)
+    return 1.0 / math.sqrt(D) if scale is None else float(scale)
+
+
+def _row_block_matrices(q, k, lam, tau_s, s, r0, r1):
+    """U, S, E, R for query rows r0..r1-1 (zero-based) of one head, all columns.
+
+    Returns U_blk [nb, T], S_blk [nb], E_blk [nb, T], R_blk [nb, T].
+    """
+    T = k.shape[0]
+    U = s * (q[r0:r1] @ k.T)                       # eq. (1)
+    rows = np.arange(r0, r1)
+    S = expit(U[np.arange(r1 - r0), rows] / tau_s)  # eq. (2), Self on the diagonal
+    E = U * expit(U)                                # eq. (2), SiLU(U) = U sigmoid(U)
+    ione = (rows + 1).astype(np.float64)            # one-based count index (App. A.1.1)
+    R = np.full_like(U, -np.inf)
+    cols = np.arange(T)
+    below = cols[None, :] < rows[:, None]           # j < i: historical Exchange entries
+    R[below] = (E - lam * np.log(ione)[:, None])[below]
+    R[np.arange(r1 - r0), rows] = S                 # j = i: Self
+    return U, S, E, R
+
+
+def forward(q, k, v, lam, *, tau_s: float = TAU_S, scale: float | None = None,
+            want_matrices: bool = True, row_block: int | None = None) -> dict:
+    """Full Relation forward for one head. q, k, v: [T, D] fp64 arrays.
+
+    Returns a dict with, per row i: Y [T, D], S, self_mass (F_ii), exch_mass (g),
+    LE (L^E, -inf for row 1), A, lnZ, M (= ln Z + lambda ln i); and, when
+    ``want_matrices``, the T x T matrices U, E, R, F and pi (pi_ij = F_ij / g_i
+    for j < i, zero elsewhere and on row 1).
+    """
+    q = np.asarray(q, np.float64)
+    k = np.asarray(k, np.float64)
+    v = np.asarray(v, np.float64)
+    T, D = q.shape
+    lam = float(lam)
+    s = _scale(D, scale)
+    rb = T if row_block is None else max(1, int(row_block))
+    ione = np.arange(1, T + 1, dtype=np.float64)
+
+    Y = np.empty((T, D))
+    S = np.empty(T)
+    self_mass = np.empty(T)
+    g = np.empty(T)
+    LE = np.empty(T)
+    lnZ = np.empty(T)
+    mats = {n: np.empty((T, T)) for n in ("U", "E", "R", "F", "pi")} if want_matrices else None
+
+    for r0 in range(0, T, rb):
+        r1 = min(T, r0 + rb)
+        nb = r1 - r0
+        rows = np.arange(r0, r1)
+        U, Sb, E, R = _row_block_matrices(q, k, lam, tau_s, s, r0, r1)
+        F = softmax(R, axis=1)                       # eq. (3): F_i = Softmax(R_i)
+        Y[r0:r1] = F @ v                             # eq. (3): Y_i = sum_j F_ij I~_j
+        S[r0:r1] = Sb
+        diagF = F[np.arange(nb), rows]
+        self_mass[r0:r1] = diagF
+        below = np.arange(T)[None, :] < rows[:, None]
+        g[r0:r1] = np.where(below, F, 0.0).sum(axis=1)       # g_i = sum_{j<i} F_ij (eq. 6)
+        LE[r0:r1] = logsumexp(np.where(below, E, -np.inf), axis=1)  # L^E_i (eq. 5)
+        lnZ[r0:r1] = logsumexp(R, axis=1)
+        if want_matrices:
+            mats["U"][r0:r1] = U
+            mats["E"][r0:r1] = E
+            mats["R"][r0:r1] = R
+            mats["F"][r0:r1] = F
+            with np.errstate(invalid="ignore", divide="ignore"):
+                pi = np.where(below, F / g[r0:r1, None], 0.0)  # pi_ij = F_ij / g_i (eq. 7)
+            mats["pi"][r0:r1] = pi
+
+    A = LE - lam * np.log(ione)                      # A_i = L^E_i - lambda log i (eq. 5)
+    out = {
+        "Y": Y, "S": S, "self_mass": self_mass, "exch_mass": g, "LE": LE, "A": A,
+        "lnZ": lnZ, "M": lnZ + lam * np.log(ione), "scale": s, "lam": lam, "tau_s": tau_s,
+    }
+    if want_matrices:
+        out.update(mats)
+    return out
+
+
+def _silu_grad(U):
+    # d SiLU(U) / dU = sigmoid(U) + U sigmoid(U) (1 - sigmoid(U))   (App. A.1.7)
+    sg = expit(U)
+    return sg + U * sg * (1.0 - sg)
+
+
+def backward(q, k, v, lam, dout, *, tau_s: float = TAU_S, scale: float | None = None,
+             route: str = "softmax", row_block: int | None = None) -> dict:
+    """Gradients of sum(dout * Y) for one head.
+
+    Returns dq, dk, dv [T, D], dlam (this head's contribution; lambda is shared
+    across heads, so the layer's gradient is the sum over heads) and dS [T]
+    (the gradient with respect to the Self logit R_ii = S_i).
+
+    route="softmax": through the softmax Jacobian of F (App. A.1.7, general
+        Relation transport): H_ij = G_i . I~_j, dR_ij = F_ij (H_ij - sum_k F_ik H_ik),
+        then the role-map derivatives and dlam = -sum_i log i sum_{j<i} dR_ij.
+    route="factorised": through g, pi and c_i = G_i . (Ibar_i - I~_i)
+        (App. A.1.7, Self-Exchange credit decomposition).
+    """
+    if route == "softmax":
+        return _backward_softmax(q, k, v, lam, dout, tau_s, scale, row_block)
+    if route == "factorised":
+        return _backward_factorised(q, k, v, lam, dout, tau_s, scale)
+    raise ValueError(f"unknown route {route!r}")
+
+
+def _backward_softmax(q, k, v, lam, dout, tau_s, scale, row_block):
+    q = np.asarray(q, np.float64)
+    k = np.asarray(k, np.float64)
+    v = np.asarray(v, np.float64)
+    G = np.asarray(dout, np.float64)
+    T, D = q.shape
+    lam = float(lam)
+    s = _scale(D, scale)
+    rb = T if row_block is None else max(1, int(row_block))
+    dq = np.empty((T, D))
+    dk = np.zeros((T, D))
+    dv = np.zeros((T, D))
+    dS = np.empty(T)
+    dlam = 0.0
+    for r0 in range(0, T, rb):
+        r1 = min(T, r0 + rb)
+        nb = r1 - r0
+        rows = np.arange(r0, r1)
+        U, Sb, E, R = _row_block_matrices(q, k, lam, tau_s, s, r0, r1)
+        F = softmax(R, axis=1)
+        Gb = G[r0:r1]
+        H = Gb @ v.T                                   # H_ij = G_i . I~_j
+        Drow = (F * H).sum(axis=1)                     # sum_{k<=i} F_ik H_ik
+        dR = F * (H - Drow[:, None])                   # softmax Jacobian (zero where F = 0)
+        below = np.arange(T)[None, :] < rows[:, None]
+        diag = (np.arange(nb), rows)
+        dU = np.where(below, dR * _silu_grad(U), 0.0)  # Exchange entries: dE/dU = SiLU'(U)
+        dU[diag] = dR[diag] * Sb * (1.0 - Sb) / tau_s  # Self entry: dS/dU_ii = S(1-S)/tau_S
+        dq[r0:r1] = s * (dU @ k)                       # grad P1 = grad_U P2 / sqrt(d_h)
+        dk += s * (dU.T @ q[r0:r1])                    # grad P2 = grad_U^T P1 / sqrt(d_h)
+        dv += F.T @ Gb                                 # dL/dI~_j = sum_i F_ij G_i
+        dS[r0:r1] = dR[diag]
+        ione = (rows + 1).astype(np.float64)
+        dlam += float(-(np.log(ione) * np.where(below, dR, 0.0).sum(axis=1)).sum())
+    return {"dq": dq, "dk": dk, "dv": dv, "dlam": dlam, "dS": dS}
+
+
+def _backward_factorised(q, k, v, lam, dout, tau_s, scale):
+    q = np.asarray(q, np.float64)
+    k = np.asarray(k, np.float64)
+    v = np.asarray(v, np.float64)
+    G = np.asarray(dout, np.float64)
+    T, D = q.shape
+    f = forward(q, k, v, lam, tau_s=tau_s, scale=scale, want_matrices=True)
+    s = f["scale"]
+    U, S, g, pi = f["U"], f["S"], f["exch_mass"], f["pi"]
+    # Exchange aggregate Ibar_i = sum_{j<i} pi_ij I~_j (eq. 8); row 1 has none and
+    # enters only through g_1 = 0, so it is left at zero.
+    Ibar = pi @ v
+    Delta = Ibar - v                                  # Delta_i = Ibar_i - I~_i
+    c = (G * Delta).sum(axis=1)                       # c_i = G_i . Delta_i
+    below = np.tril(np.ones((T, T), dtype=bool), k=-1)
+    # dL/dE_ij = g_i pi_ij [ (1-g_i) c_i + G_i . (I~_j - Ibar_i) ]
+    GI = G @ v.T                                      # G_i . I~_j
+    GIbar = (G * Ibar).sum(axis=1)                    # G_i . Ibar_i
+    dE = np.where(below, g[:, None] * pi * ((1.0 - g) * c)[:, None]
+                  + g[:, None] * pi * (GI - GIbar[:, None]), 0.0)
+    dS = -g * (1.0 - g) * c                           # dL/dS_i = -g_i (1 - g_i) c_i
+    dU = np.where(below, dE * _silu_grad(U), 0.0)
+    dU[np.diag_indices(T)] = dS * S * (1.0 - S) / tau_s
+    dq = s * (dU @ k)
+    dk = s * (dU.T @ q)
+    # dL/dI~_j = (1 - g_j) G_j + sum_{i>j} g_i pi_ij G_i
+    dv = (1.0 - g)[:, None] * G + (g[:, None] * pi).T @ G
+    ione = np.arange(1, T + 1, dtype=np.float64)
+    # dL/dlambda = -sum_{i>1} g_i (1 - g_i) c_i log i
+    dlam = float(-(g * (1.0 - g) * c * np.log(ione))[1:].sum())
+    return {"dq": dq, "dk": dk, "dv": dv, "dlam": dlam, "dS": dS}
+
+
+def forward_batched(q, k, v, lam, **kw) -> dict:
+    """Apply ``forward`` to every (b, h) head of [B, H, T, D] arrays (heads are
+    independent, Sec. 3.2 / App. A.2.1). Row quantities come back as [B, H, T]."""
+    B, H, T, D = q.shape
+    keys = ("Y", "S", "self_mass", "exch_mass", "LE", "A", "lnZ", "M")
+    out = {"Y": np.empty((B, H, T, D))}
+    for key in keys[1:]:
+        out[key] = np.empty((B, H, T))
+    kw = dict(kw)
+    kw.setdefault("want_matrices", False)
+    for b in range(B):
+        for h in range(H):
+            f = forward(q[b, h], k[b, h], v[b, h], lam, **kw)
+            for key in keys:
+                out[key][b, h] = f[key]
+    return out
+
+
+def backward_batched(q, k, v, lam, dout, **kw) -> dict:
+    """Apply ``backward`` to every head; dlam is summed over heads because
+    lambda is one scalar per layer shared by all heads (App. A.1.1)."""
+    B, H, T, D = q.shape
+    out = {n: np.empty((B, H, T, D)) for n in ("dq", "dk", "dv")}
+    out["dS"] = np.empty((B, H, T))
+    dlam = 0.0
+    for b in range(B):
+        for h in range(H):
+            r = backward(q[b, h], k[b, h], v[b, h], lam, dout[b, h], **kw)
+            for n in ("dq", "dk", "dv", "dS"):
+                out[n][b, h] = r[n]
+            dlam += r["dlam"]
+    out["dlam"] = dlam
+    return out
