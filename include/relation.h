@@ -1,0 +1,139 @@
+/*
+ * relation.h - C ABI of the FlashRelation library: the exact causal Full
+ * Relation operator (Self-Exchange Relation, one head per (b, h)) on gfx950.
+ *
+ * Operator (per head, rows i = 1..T one-based, from the paper's Sec. 3.1,
+ * eqs. (1)-(3), restated in App. A.1.1):
+ *   U_ij = scale * q_i . k_j                       scale = 1/sqrt(D) by default
+ *   S_i  = sigmoid(U_ii / tau_s)                   Self, on the diagonal
+ *   E_ij = SiLU(U_ij) = U_ij * sigmoid(U_ij)       Exchange, for j < i
+ *   R_ij = S_i (j = i); E_ij - lambda * ln(i) (j < i); -inf (j > i)
+ *   F_i  = softmax(R_i),   y_i = sum_{j <= i} F_ij v_j
+ * q and k are the two relation projections after RoPE, v is the information
+ * state after Givens head mixing; lambda is the layer's count-calibration
+ * scalar, shared by all heads (App. A.1.1), tau_s the fixed Self temperature
+ * (2 in the paper). The flash entry points never form U, R or F in memory:
+ * they run the tiled online Exchange scan of Sec. 5.1 (eqs. 11-13, App. A.3)
+ * and apply Self and lambda after the scan.
+ *
+ * Conventions shared by every entry point
+ *  - Tensors q, k, v, o, dout, dq, dk, dv are [B, H, T, D] with element
+ *    strides (stride_b, stride_h, stride_t) taken from rel_problem and a
+ *    contiguous last dimension. They all have the element type `dtype`.
+ *  - Row vectors (row_stat, self_mass, exch_mass, exch_lse, dself) are fp32,
+ *    dense [B, H, T]. T x T outputs (R, F, pi) are fp32, dense [B, H, T, T].
+ *  - lambda and dlambda point to one fp32 scalar in device memory.
+ *  - All pointers are device pointers owned by the caller. The library keeps
+ *    no allocation between calls; scratch memory comes from the caller's
+ *    workspace, sized by the *_workspace_bytes queries.
+ *  - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL means
+ *    the default stream). No entry point synchronises the host.
+ *  - Outputs are overwritten, never accumulated into.
+ *  - Arguments are validated on the host before any HIP call; on failure
+ *    nothing is launched and a rel_status < 0 is returned. The message of the
+ *    last failure on the calling thread is returned by relation_last_error().
+ *  - B * H * T == 0 returns REL_OK without launching anything.
+ */
+#ifndef RELATION_H
+#define RELATION_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RELATION_ABI_VERSION 1
+
+typedef enum rel_status {
+  REL_OK = 0,
+  REL_ERR_INVALID_ARG = -1, /* null/overlapping/misaligned pointer, bad size or stride, bad tau_s */
+  REL_ERR_UNSUPPORTED = -2, /* dtype, head dimension or causal flag this build has no kernel for */
+  REL_ERR_WORKSPACE = -3,   /* workspace pointer null or smaller than the query result */
+  REL_ERR_HIP = -4          /* a HIP/rocBLAS call failed; see relation_last_error() */
+} rel_status;
+
+typedef enum rel_dtype {
+  REL_F32 = 0,  /* fp32 storage, fp32 MFMA (parity path) */
+  REL_BF16 = 1  /* bf16 storage, bf16 MFMA with fp32 accumulation and statistics */
+} rel_dtype;
+
+typedef struct rel_problem {
+  int64_t B, H, T, D;   /* batch, heads, sequence length, head width. D in {32, 64, 128} */
+  int32_t dtype;        /* rel_dtype of q, k, v, o, dout, dq, dk, dv */
+  int32_t causal;       /* must be 1: the paper defines only the causal R (eq. 2) */
+  float tau_s;          /* Self temperature, finite and > 0 (paper: 2.0) */
+  float scale;          /* multiplier inside U; <= 0 selects 1/sqrt(D) (eq. 1) */
+  int64_t stride_b;     /* element strides shared by all [B,H,T,D] tensors; */
+  int64_t stride_h;     /* the last dimension is contiguous. stride_t must be a */
+  int64_t stride_t;     /* multiple of 16 bytes / element size and >= D */
+} rel_problem;
+
+/* Forward pass (FlashRelation, Sec. 5.1).
+ *   q, k, v   in  [B,H,T,D] dtype
+ *   lambda    in  device fp32 scalar
+ *   o         out [B,H,T,D] dtype: y_i = (1 - g_i) v_i + g_i * Ibar_i (eq. 13)
+ *   row_stat  out [B,H,T] fp32: M_i = ln Z_i + lambda ln i, the one statistic the
+ *             backward pass needs (then F_ij = exp(E_ij - M_i) for j < i). May be
+ *             NULL when no backward pass follows.
+ *   self_mass out [B,H,T] fp32, optional: F_ii = sigmoid(S_i - A_i) (eq. 6)
+ *   exch_mass out [B,H,T] fp32, optional: g_i = sigmoid(A_i - S_i) (eq. 6)
+ *   exch_lse  out [B,H,T] fp32, optional: L^E_i = LSE_{j<i} E_ij (eq. 5); -inf on
+ *             row 1. With it, the within-history allocation is
+ *             pi_ij = exp(E_ij - L^E_i) (eq. 7).
+ *   All optional outputs may be NULL. Row 1 has no history: g = 0, y = v (App. A.1.8). */
+rel_status relation_fwd(const rel_problem* p, const void* q, const void* k, const void* v,
+                        const float* lambda, void* o, float* row_stat, float* self_mass,
+                        float* exch_mass, float* exch_lse, void* stream);
+
+/* Within-history Exchange allocation pi (eq. 7), written densely:
+ *   pi    out [B,H,T,T] fp32: pi_ij = exp(E_ij - L^E_i) for j < i, 0 elsewhere
+ *         (all of row 1 is 0). This is O(T^2) output by nature; it is a
+ *         diagnostic, not part of the fused path.
+ *   exch_lse in [B,H,T] fp32, as written by relation_fwd. */
+rel_status relation_exchange_allocation(const rel_problem* p, const void* q, const void* k,
+                                        const float* exch_lse, float* pi, void* stream);
+
+/* Backward pass: gradients of sum(dout * o) (App. A.1.7), recomputed tile by
+ * tile from q, k, v, o and row_stat.
+ *   dq, dk, dv out [B,H,T,D] dtype
+ *   dlambda    out device fp32 scalar: sum over b, h, i of ln(i) * dR_ii, which
+ *              equals -sum g_i (1-g_i) c_i ln i of App. A.1.7. Reduced in a fixed
+ *              order.
+ *   dself      out [B,H,T] fp32, optional: dL/dS_i, the gradient reaching the
+ *              Self logit R_ii = S_i (-g_i (1 - g_i) c_i in App. A.1.7).
+ *   workspace  at least relation_bwd_workspace_bytes(p) bytes of device memory,
+ *              16-byte aligned; contents on entry are ignored.
+ *   dq accumulates in fp32 with device atomics, so its low-order bits can vary
+ *   from run to run; dk, dv, dlambda and dself are run-to-run identical. */
+size_t relation_bwd_workspace_bytes(const rel_problem* p);
+rel_status relation_bwd(const rel_problem* p, const void* q, const void* k, const void* v,
+                        const void* o, const void* dout, const float* lambda,
+                        const float* row_stat, void* dq, void* dk, void* dv, float* dlambda,
+                        float* dself, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Materialised Full Relation: U = scale q k^T is written to HBM in full
+ * (rocBLAS batched GEMM), a row kernel builds R and F = softmax(R) (eqs. 2-3),
+ * and a second GEMM forms o = F v. The baseline the fused path is measured
+ * against (Table 5(a)).
+ *   R, F, pi   out [B,H,T,T] fp32, optional: R with -inf above the diagonal,
+ *              F and pi (eq. 7) with 0 there.
+ *   self_mass, exch_mass  out [B,H,T] fp32, optional.
+ *   workspace  at least relation_fwd_materialized_workspace_bytes(p) bytes:
+ *              U in fp32 plus F in dtype, i.e. B*H*T*T*(4 + sizeof(dtype)). */
+size_t relation_fwd_materialized_workspace_bytes(const rel_problem* p);
+rel_status relation_fwd_materialized(const rel_problem* p, const void* q, const void* k,
+                                     const void* v, const float* lambda, void* o, float* R,
+                                     float* F, float* pi, float* self_mass, float* exch_mass,
+                                     void* workspace, size_t workspace_bytes, void* stream);
+
+const char* relation_status_string(rel_status s);
+const char* relation_last_error(void);
+int relation_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RELATION_H */

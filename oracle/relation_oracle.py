@@ -49,33 +49,36 @@ def _scale(D: int, scale: float | None) -> float:
     return 1.0 / math.sqrt(D) if scale is None else float(scale)
 
 
-def _row_block_matrices(q, k, lam, tau_s, s, r0, r1):
-    """U, S, E, R for query rows r0..r1-1 (zero-based) of one head, all columns.
-
-    Returns U_blk [nb, T], S_blk [nb], E_blk [nb, T], R_blk [nb, T].
+def _row_block_matrices(q, k, lam, tau_s, s, rows):
+    """U, S, E, R for the query rows ``rows`` (zero-based indices) of one head,
+    all columns. Returns U_blk [nb, T], S_blk [nb], E_blk [nb, T], R_blk [nb, T].
     """
     T = k.shape[0]
-    U = s * (q[r0:r1] @ k.T)                       # eq. (1)
-    rows = np.arange(r0, r1)
-    S = expit(U[np.arange(r1 - r0), rows] / tau_s)  # eq. (2), Self on the diagonal
+    nb = len(rows)
+    U = s * (q[rows] @ k.T)                         # eq. (1)
+    S = expit(U[np.arange(nb), rows] / tau_s)       # eq. (2), Self on the diagonal
     E = U * expit(U)                                # eq. (2), SiLU(U) = U sigmoid(U)
     ione = (rows + 1).astype(np.float64)            # one-based count index (App. A.1.1)
     R = np.full_like(U, -np.inf)
     cols = np.arange(T)
     below = cols[None, :] < rows[:, None]           # j < i: historical Exchange entries
     R[below] = (E - lam * np.log(ione)[:, None])[below]
-    R[np.arange(r1 - r0), rows] = S                 # j = i: Self
+    R[np.arange(nb), rows] = S                      # j = i: Self
     return U, S, E, R
 
 
 def forward(q, k, v, lam, *, tau_s: float = TAU_S, scale: float | None = None,
-            want_matrices: bool = True, row_block: int | None = None) -> dict:
+            want_matrices: bool = True, row_block: int | None = None, rows=None) -> dict:
     """Full Relation forward for one head. q, k, v: [T, D] fp64 arrays.
 
-    Returns a dict with, per row i: Y [T, D], S, self_mass (F_ii), exch_mass (g),
-    LE (L^E, -inf for row 1), A, lnZ, M (= ln Z + lambda ln i); and, when
-    ``want_matrices``, the T x T matrices U, E, R, F and pi (pi_ij = F_ij / g_i
-    for j < i, zero elsewhere and on row 1).
+    ``rows`` (optional, increasing zero-based indices) restricts the output to
+    those query rows; each row of F is its own softmax, so a row's result does
+    not depend on which other rows are evaluated.
+
+    Returns a dict with, per evaluated row i: Y [n, D], S, self_mass (F_ii),
+    exch_mass (g), LE (L^E, -inf for row 1), A, lnZ, M (= ln Z + lambda ln i);
+    and, when ``want_matrices``, the [n, T] rows of U, E, R, F and pi
+    (pi_ij = F_ij / g_i for j < i, zero elsewhere and on row 1).
     """
     q = np.asarray(q, np.float64)
     k = np.asarray(k, np.float64)
@@ -83,44 +86,46 @@ def forward(q, k, v, lam, *, tau_s: float = TAU_S, scale: float | None = None,
     T, D = q.shape
     lam = float(lam)
     s = _scale(D, scale)
-    rb = T if row_block is None else max(1, int(row_block))
-    ione = np.arange(1, T + 1, dtype=np.float64)
+    rows = np.arange(T) if rows is None else np.asarray(rows, dtype=np.int64)
+    n = len(rows)
+    rb = max(n, 1) if row_block is None else max(1, int(row_block))
 
-    Y = np.empty((T, D))
-    S = np.empty(T)
-    self_mass = np.empty(T)
-    g = np.empty(T)
-    LE = np.empty(T)
-    lnZ = np.empty(T)
-    mats = {n: np.empty((T, T)) for n in ("U", "E", "R", "F", "pi")} if want_matrices else None
+    Y = np.empty((n, D))
+    S = np.empty(n)
+    self_mass = np.empty(n)
+    g = np.empty(n)
+    LE = np.empty(n)
+    lnZ = np.empty(n)
+    mats = {m: np.empty((n, T)) for m in ("U", "E", "R", "F", "pi")} if want_matrices else None
 
-    for r0 in range(0, T, rb):
-        r1 = min(T, r0 + rb)
-        nb = r1 - r0
-        rows = np.arange(r0, r1)
-        U, Sb, E, R = _row_block_matrices(q, k, lam, tau_s, s, r0, r1)
+    for b0 in range(0, n, rb):
+        b1 = min(n, b0 + rb)
+        rr = rows[b0:b1]
+        U, Sb, E, R = _row_block_matrices(q, k, lam, tau_s, s, rr)
         F = softmax(R, axis=1)                       # eq. (3): F_i = Softmax(R_i)
-        Y[r0:r1] = F @ v                             # eq. (3): Y_i = sum_j F_ij I~_j
-        S[r0:r1] = Sb
-        diagF = F[np.arange(nb), rows]
-        self_mass[r0:r1] = diagF
-        below = np.arange(T)[None, :] < rows[:, None]
-        g[r0:r1] = np.where(below, F, 0.0).sum(axis=1)       # g_i = sum_{j<i} F_ij (eq. 6)
-        LE[r0:r1] = logsumexp(np.where(below, E, -np.inf), axis=1)  # L^E_i (eq. 5)
-        lnZ[r0:r1] = logsumexp(R, axis=1)
+        Y[b0:b1] = F @ v                             # eq. (3): Y_i = sum_j F_ij I~_j
+        S[b0:b1] = Sb
+        diagF = F[np.arange(b1 - b0), rr]
+        self_mass[b0:b1] = diagF
+        below = np.arange(T)[None, :] < rr[:, None]
+        g[b0:b1] = np.where(below, F, 0.0).sum(axis=1)       # g_i = sum_{j<i} F_ij (eq. 6)
+        LE[b0:b1] = logsumexp(np.where(below, E, -np.inf), axis=1)  # L^E_i (eq. 5)
+        lnZ[b0:b1] = logsumexp(R, axis=1)
         if want_matrices:
-            mats["U"][r0:r1] = U
-            mats["E"][r0:r1] = E
-            mats["R"][r0:r1] = R
-            mats["F"][r0:r1] = F
+            mats["U"][b0:b1] = U
+            mats["E"][b0:b1] = E
+            mats["R"][b0:b1] = R
+            mats["F"][b0:b1] = F
             with np.errstate(invalid="ignore", divide="ignore"):
-                pi = np.where(below, F / g[r0:r1, None], 0.0)  # pi_ij = F_ij / g_i (eq. 7)
-            mats["pi"][r0:r1] = pi
+                pi = np.where(below, F / g[b0:b1, None], 0.0)  # pi_ij = F_ij / g_i (eq. 7)
+            mats["pi"][b0:b1] = pi
 
+    ione = (rows + 1).astype(np.float64)
     A = LE - lam * np.log(ione)                      # A_i = L^E_i - lambda log i (eq. 5)
     out = {
         "Y": Y, "S": S, "self_mass": self_mass, "exch_mass": g, "LE": LE, "A": A,
         "lnZ": lnZ, "M": lnZ + lam * np.log(ione), "scale": s, "lam": lam, "tau_s": tau_s,
+        "rows": rows,
     }
     if want_matrices:
         out.update(mats)
@@ -134,7 +139,7 @@ def _silu_grad(U):
 
 
 def backward(q, k, v, lam, dout, *, tau_s: float = TAU_S, scale: float | None = None,
-             route: str = "softmax", row_block: int | None = None) -> dict:
+             route: str = "softmax", row_block: int | None = None, rows=None) -> dict:
     """Gradients of sum(dout * Y) for one head.
 
     Returns dq, dk, dv [T, D], dlam (this head's contribution; lambda is shared
@@ -146,15 +151,22 @@ def backward(q, k, v, lam, dout, *, tau_s: float = TAU_S, scale: float | None = 
         then the role-map derivatives and dlam = -sum_i log i sum_{j<i} dR_ij.
     route="factorised": through g, pi and c_i = G_i . (Ibar_i - I~_i)
         (App. A.1.7, Self-Exchange credit decomposition).
+
+    ``rows`` (softmax route only; increasing zero-based indices) evaluates only
+    the contributions of those query rows: dq, dS and dlam for those rows, and
+    dk, dv summed over those rows. With rows = {j0, ..., T-1}, dk_j and dv_j are
+    complete for every j >= j0, since only rows i >= j reach key j.
     """
     if route == "softmax":
-        return _backward_softmax(q, k, v, lam, dout, tau_s, scale, row_block)
+        return _backward_softmax(q, k, v, lam, dout, tau_s, scale, row_block, rows)
+    if rows is not None:
+        raise ValueError("row subsets are evaluated by the softmax route")
     if route == "factorised":
         return _backward_factorised(q, k, v, lam, dout, tau_s, scale)
     raise ValueError(f"unknown route {route!r}")
 
 
-def _backward_softmax(q, k, v, lam, dout, tau_s, scale, row_block):
+def _backward_softmax(q, k, v, lam, dout, tau_s, scale, row_block, rows):
     q = np.asarray(q, np.float64)
     k = np.asarray(k, np.float64)
     v = np.asarray(v, np.float64)
@@ -162,33 +174,35 @@ def _backward_softmax(q, k, v, lam, dout, tau_s, scale, row_block):
     T, D = q.shape
     lam = float(lam)
     s = _scale(D, scale)
-    rb = T if row_block is None else max(1, int(row_block))
-    dq = np.empty((T, D))
+    rows = np.arange(T) if rows is None else np.asarray(rows, dtype=np.int64)
+    n = len(rows)
+    rb = max(n, 1) if row_block is None else max(1, int(row_block))
+    dq = np.empty((n, D))
     dk = np.zeros((T, D))
     dv = np.zeros((T, D))
-    dS = np.empty(T)
+    dS = np.empty(n)
     dlam = 0.0
-    for r0 in range(0, T, rb):
-        r1 = min(T, r0 + rb)
-        nb = r1 - r0
-        rows = np.arange(r0, r1)
-        U, Sb, E, R = _row_block_matrices(q, k, lam, tau_s, s, r0, r1)
+    for b0 in range(0, n, rb):
+        b1 = min(n, b0 + rb)
+        rr = rows[b0:b1]
+        nb = b1 - b0
+        U, Sb, E, R = _row_block_matrices(q, k, lam, tau_s, s, rr)
         F = softmax(R, axis=1)
-        Gb = G[r0:r1]
+        Gb = G[rr]
         H = Gb @ v.T                                   # H_ij = G_i . I~_j
         Drow = (F * H).sum(axis=1)                     # sum_{k<=i} F_ik H_ik
         dR = F * (H - Drow[:, None])                   # softmax Jacobian (zero where F = 0)
-        below = np.arange(T)[None, :] < rows[:, None]
-        diag = (np.arange(nb), rows)
+        below = np.arange(T)[None, :] < rr[:, None]
+        diag = (np.arange(nb), rr)
         dU = np.where(below, dR * _silu_grad(U), 0.0)  # Exchange entries: dE/dU = SiLU'(U)
         dU[diag] = dR[diag] * Sb * (1.0 - Sb) / tau_s  # Self entry: dS/dU_ii = S(1-S)/tau_S
-        dq[r0:r1] = s * (dU @ k)                       # grad P1 = grad_U P2 / sqrt(d_h)
-        dk += s * (dU.T @ q[r0:r1])                    # grad P2 = grad_U^T P1 / sqrt(d_h)
+        dq[b0:b1] = s * (dU @ k)                       # grad P1 = grad_U P2 / sqrt(d_h)
+        dk += s * (dU.T @ q[rr])                       # grad P2 = grad_U^T P1 / sqrt(d_h)
         dv += F.T @ Gb                                 # dL/dI~_j = sum_i F_ij G_i
-        dS[r0:r1] = dR[diag]
-        ione = (rows + 1).astype(np.float64)
+        dS[b0:b1] = dR[diag]
+        ione = (rr + 1).astype(np.float64)
         dlam += float(-(np.log(ione) * np.where(below, dR, 0.0).sum(axis=1)).sum())
-    return {"dq": dq, "dk": dk, "dv": dv, "dlam": dlam, "dS": dS}
+    return {"dq": dq, "dk": dk, "dv": dv, "dlam": dlam, "dS": dS, "rows": rows}
 
 
 def _backward_factorised(q, k, v, lam, dout, tau_s, scale):

@@ -1,0 +1,258 @@
+"""Python binding of librelation.so (ctypes). Argument marshalling only: every
+step of the operator runs in the library's HIP kernels; torch provides device
+memory and the current stream.
+
+Functions carry the C-ABI names (relation_fwd, relation_bwd,
+relation_fwd_materialized, relation_exchange_allocation, ...). ``relation`` is
+the differentiable wrapper (torch.autograd.Function) over relation_fwd /
+relation_bwd.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "librelation.so")
+
+REL_OK, REL_ERR_INVALID_ARG, REL_ERR_UNSUPPORTED, REL_ERR_WORKSPACE, REL_ERR_HIP = 0, -1, -2, -3, -4
+REL_F32, REL_BF16 = 0, 1
+TAU_S = 2.0
+
+
+class RelProblem(ctypes.Structure):
+    _fields_ = [
+        ("B", ctypes.c_int64), ("H", ctypes.c_int64), ("T", ctypes.c_int64), ("D", ctypes.c_int64),
+        ("dtype", ctypes.c_int32), ("causal", ctypes.c_int32),
+        ("tau_s", ctypes.c_float), ("scale", ctypes.c_float),
+        ("stride_b", ctypes.c_int64), ("stride_h", ctypes.c_int64), ("stride_t", ctypes.c_int64),
+    ]
+
+
+_P = ctypes.c_void_p
+_SIGS = {
+    "relation_fwd": (ctypes.c_int, [ctypes.POINTER(RelProblem), _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "relation_exchange_allocation": (ctypes.c_int, [ctypes.POINTER(RelProblem), _P, _P, _P, _P, _P]),
+    "relation_bwd_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(RelProblem)]),
+    "relation_bwd": (ctypes.c_int, [ctypes.POINTER(RelProblem), _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                    _P, _P, _P, ctypes.c_size_t, _P]),
+    "relation_fwd_materialized_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(RelProblem)]),
+    "relation_fwd_materialized": (ctypes.c_int, [ctypes.POINTER(RelProblem), _P, _P, _P, _P, _P, _P, _P,
+                                                 _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "relation_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "relation_last_error": (ctypes.c_char_p, []),
+    "relation_abi_version": (ctypes.c_int, []),
+}
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load librelation.so once. Raises if it has not been built: there is no
+    fallback implementation."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"librelation.so not found at {path}; build it with "
+                           "`python -m paper_2608_20172_amd.build`")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in _SIGS.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(status: int, what: str) -> None:
+    if status != REL_OK:
+        lib = load_library()
+        msg = lib.relation_status_string(status).decode()
+        detail = lib.relation_last_error().decode()
+        raise RuntimeError(f"{what} failed: {msg} ({status}): {detail}")
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _dtype_code(dt: torch.dtype) -> int:
+    if dt == torch.bfloat16:
+        return REL_BF16
+    if dt == torch.float32:
+        return REL_F32
+    raise TypeError(f"unsupported dtype {dt}; use torch.bfloat16 or torch.float32")
+
+
+def make_problem(q: torch.Tensor, tau_s: float = TAU_S, scale: Optional[float] = None) -> RelProblem:
+    if q.dim() != 4:
+        raise ValueError("tensors must be [B, H, T, D]")
+    B, H, T, D = q.shape
+    sb, sh, st, sd = q.stride()
+    if sd != 1:
+        raise ValueError("the last dimension must be contiguous")
+    return RelProblem(B, H, T, D, _dtype_code(q.dtype), 1, float(tau_s),
+                      0.0 if scale is None else float(scale), sb, sh, st)
+
+
+def _same_layout(ref: torch.Tensor, *ts: torch.Tensor) -> list:
+    out = []
+    for t in ts:
+        if t.shape != ref.shape or t.dtype != ref.dtype or t.device != ref.device:
+            raise ValueError("q, k, v (and o, dout) must share shape, dtype and device")
+        if t.stride() != ref.stride():
+            t = torch.empty_strided(ref.shape, ref.stride(), dtype=ref.dtype, device=ref.device).copy_(t)
+        out.append(t)
+    return out
+
+
+def _lam_tensor(lam, device) -> torch.Tensor:
+    if isinstance(lam, torch.Tensor):
+        if lam.numel() != 1:
+            raise ValueError("lambda must be a single scalar")
+        return lam.detach().to(device=device, dtype=torch.float32).reshape(1).contiguous()
+    return torch.tensor([float(lam)], dtype=torch.float32, device=device)
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _layout_like(q: torch.Tensor) -> torch.Tensor:
+    # A dense [B, H, T, D] tensor keeps q's stride order; q's own strides are
+    # reused so that every tensor shares (stride_b, stride_h, stride_t).
+    return torch.empty_strided(q.shape, q.stride(), dtype=q.dtype, device=q.device)
+
+
+def relation_fwd(q, k, v, lam, *, tau_s: float = TAU_S, scale: Optional[float] = None,
+                 want_row_stat: bool = True, want_masses: bool = False, want_lse: bool = False):
+    """Fused forward. Returns dict(o, row_stat, self_mass, exch_mass, exch_lse);
+    outputs that were not requested are None."""
+    lib = load_library()
+    k, v = _same_layout(q, k, v)
+    p = make_problem(q, tau_s, scale)
+    B, H, T, D = q.shape
+    dev = q.device
+    lam_t = _lam_tensor(lam, dev)
+    o = _layout_like(q)
+    rows = lambda: torch.empty((B, H, T), dtype=torch.float32, device=dev)
+    row_stat = rows() if want_row_stat else None
+    self_mass = rows() if want_masses else None
+    exch_mass = rows() if want_masses else None
+    exch_lse = rows() if want_lse else None
+    st = lib.relation_fwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(lam_t), _ptr(o),
+                          _ptr(row_stat), _ptr(self_mass), _ptr(exch_mass), _ptr(exch_lse), _stream())
+    _check(st, "relation_fwd")
+    return {"o": o, "row_stat": row_stat, "self_mass": self_mass, "exch_mass": exch_mass,
+            "exch_lse": exch_lse}
+
+
+def relation_exchange_allocation(q, k, exch_lse, *, tau_s: float = TAU_S, scale: Optional[float] = None):
+    """pi_ij = exp(E_ij - L^E_i) for j < i (dense [B, H, T, T] fp32)."""
+    lib = load_library()
+    (k,) = _same_layout(q, k)
+    p = make_problem(q, tau_s, scale)
+    B, H, T, D = q.shape
+    pi = torch.empty((B, H, T, T), dtype=torch.float32, device=q.device)
+    lse = exch_lse.contiguous().to(torch.float32)
+    st = lib.relation_exchange_allocation(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(lse), _ptr(pi), _stream())
+    _check(st, "relation_exchange_allocation")
+    return pi
+
+
+def relation_bwd_workspace_bytes(q, *, tau_s: float = TAU_S, scale: Optional[float] = None) -> int:
+    lib = load_library()
+    p = make_problem(q, tau_s, scale)
+    return int(lib.relation_bwd_workspace_bytes(ctypes.byref(p)))
+
+
+def relation_bwd(q, k, v, o, dout, lam, row_stat, *, tau_s: float = TAU_S,
+                 scale: Optional[float] = None, want_dself: bool = False, workspace=None):
+    """Fused backward. Returns dict(dq, dk, dv, dlambda (1-element fp32 tensor), dself)."""
+    lib = load_library()
+    k, v, o, dout = _same_layout(q, k, v, o, dout)
+    p = make_problem(q, tau_s, scale)
+    B, H, T, D = q.shape
+    dev = q.device
+    lam_t = _lam_tensor(lam, dev)
+    dq, dk, dv = _layout_like(q), _layout_like(q), _layout_like(q)
+    dlam = torch.empty((1,), dtype=torch.float32, device=dev)
+    dself = torch.empty((B, H, T), dtype=torch.float32, device=dev) if want_dself else None
+    nbytes = int(lib.relation_bwd_workspace_bytes(ctypes.byref(p)))
+    if workspace is None or workspace.numel() * workspace.element_size() < nbytes:
+        workspace = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=dev)
+    rs = row_stat.contiguous()
+    st = lib.relation_bwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(dout), _ptr(lam_t),
+                          _ptr(rs), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dlam), _ptr(dself),
+                          _ptr(workspace), workspace.numel() * workspace.element_size(), _stream())
+    _check(st, "relation_bwd")
+    return {"dq": dq, "dk": dk, "dv": dv, "dlambda": dlam, "dself": dself}
+
+
+def relation_fwd_materialized_workspace_bytes(q, *, tau_s: float = TAU_S,
+                                              scale: Optional[float] = None) -> int:
+    lib = load_library()
+    p = make_problem(q, tau_s, scale)
+    return int(lib.relation_fwd_materialized_workspace_bytes(ctypes.byref(p)))
+
+
+def relation_fwd_materialized(q, k, v, lam, *, tau_s: float = TAU_S, scale: Optional[float] = None,
+                              want_R: bool = False, want_F: bool = False, want_pi: bool = False,
+                              want_masses: bool = False, workspace=None):
+    """Materialised baseline. Returns dict(o, R, F, pi, self_mass, exch_mass)."""
+    lib = load_library()
+    k, v = _same_layout(q, k, v)
+    p = make_problem(q, tau_s, scale)
+    B, H, T, D = q.shape
+    dev = q.device
+    lam_t = _lam_tensor(lam, dev)
+    o = _layout_like(q)
+    mat = lambda: torch.empty((B, H, T, T), dtype=torch.float32, device=dev)
+    rows = lambda: torch.empty((B, H, T), dtype=torch.float32, device=dev)
+    R = mat() if want_R else None
+    F = mat() if want_F else None
+    pi = mat() if want_pi else None
+    sm = rows() if want_masses else None
+    em = rows() if want_masses else None
+    nbytes = int(lib.relation_fwd_materialized_workspace_bytes(ctypes.byref(p)))
+    if workspace is None or workspace.numel() * workspace.element_size() < nbytes:
+        workspace = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=dev)
+    st = lib.relation_fwd_materialized(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(lam_t), _ptr(o),
+                                       _ptr(R), _ptr(F), _ptr(pi), _ptr(sm), _ptr(em), _ptr(workspace),
+                                       workspace.numel() * workspace.element_size(), _stream())
+    _check(st, "relation_fwd_materialized")
+    return {"o": o, "R": R, "F": F, "pi": pi, "self_mass": sm, "exch_mass": em}
+
+
+class _RelationFn(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, q, k, v, lam, tau_s, scale):
+        out = relation_fwd(q, k, v, lam, tau_s=tau_s, scale=scale)
+        ctx.save_for_backward(q, k, v, out["o"], lam, out["row_stat"])
+        ctx.tau_s, ctx.scale = tau_s, scale
+        return out["o"]
+
+    @staticmethod
+    def backward(ctx, dout):
+        q, k, v, o, lam, row_stat = ctx.saved_tensors
+        g = relation_bwd(q, k, v, o, dout.contiguous() if dout.stride() != q.stride() else dout, lam,
+                         row_stat, tau_s=ctx.tau_s, scale=ctx.scale)
+        dlam = g["dlambda"].reshape(lam.shape).to(lam.dtype)
+        return g["dq"], g["dk"], g["dv"], dlam, None, None
+
+
+def relation(q, k, v, lam, tau_s: float = TAU_S, scale: Optional[float] = None) -> torch.Tensor:
+    """Differentiable causal Full Relation over [B, H, T, D] tensors (fused
+    FlashRelation kernels). ``lam`` is a scalar tensor (the layer's lambda)."""
+    if not isinstance(lam, torch.Tensor):
+        lam = torch.tensor(float(lam), dtype=torch.float32, device=q.device)
+    return _RelationFn.apply(q, k, v, lam, tau_s, scale)
+
+
+def default_scale(D: int) -> float:
+    return 1.0 / math.sqrt(D)

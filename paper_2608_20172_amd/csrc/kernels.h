@@ -1,0 +1,77 @@
+// Internal launch interface between the C-ABI layer and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace rel {
+
+// Arguments of the fused forward pass (FlashRelation, Sec. 5.1).
+struct FwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const float* lambda;
+  void* o;
+  float* row_stat;   // M_i = ln Z_i + lambda ln i, or null
+  float* self_mass;  // optional
+  float* exch_mass;  // optional
+  float* exch_lse;   // optional
+  int64_t sb, sh, st;
+  int H, T;
+  float scale;    // multiplier inside U
+  float inv_tau;  // 1 / tau_S
+  TileMap map;
+};
+
+// Arguments of the fused backward pass.
+struct BwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* o;
+  const void* dout;
+  const float* lambda;
+  const float* row_stat;
+  void* dk;
+  void* dv;
+  float* dq_acc;     // fp32 [N, T, D] dense, zeroed before the main kernel
+  float* dlam_part;  // one partial per main-kernel workgroup slot
+  float* dself;      // optional [N, T]
+  int64_t sb, sh, st;
+  int H, T;
+  float scale;
+  float inv_tau;
+  TileMap map;
+};
+
+// Arguments of the allocation (pi) diagnostic and the materialised row kernel.
+struct RowArgs {
+  const float* U;      // [N, T, T] scale * q k^T (materialised path) or null
+  const void* q;       // allocation kernel: recomputes U from q, k
+  const void* k;
+  const float* exch_lse;
+  const float* lambda;
+  void* Fw;            // materialised: F in the storage dtype (GEMM operand)
+  float* R;
+  float* F;
+  float* pi;
+  float* self_mass;
+  float* exch_mass;
+  int64_t sb, sh, st;
+  int H, T, D;
+  float scale;
+  float inv_tau;
+};
+
+hipError_t launch_fwd(const FwdArgs& a, int dtype, int D, hipStream_t stream);
+hipError_t launch_bwd(const BwdArgs& a, int dtype, int D, void* dq_out, hipStream_t stream);
+int bwd_partials(int N, int T, int D, int dtype);
+hipError_t launch_dlambda(const float* part, int np, float* out, hipStream_t stream);
+hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t stream);
+hipError_t launch_allocation(const RowArgs& a, int dtype, int N, hipStream_t stream);
+hipError_t launch_materialized_rows(const RowArgs& a, int dtype, int N, hipStream_t stream);
+
+}  // namespace rel

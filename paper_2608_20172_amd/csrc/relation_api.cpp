@@ -1,0 +1,460 @@
+// C-ABI layer: argument validation on the host, workspace sizing, dispatch to
+// the HIP kernels, and the rocBLAS handle used by the materialised baseline.
+#include "../../include/relation.h"
+
+#include <rocblas/rocblas.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+rel_status fail(rel_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+rel_status hip_fail(hipError_t e, const char* where) {
+  return fail(REL_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+size_t elem_size(int32_t dtype) { return dtype == REL_BF16 ? 2 : 4; }
+
+// A [B, H, T, D] tensor with the problem's strides, as a set of element offsets
+// base + b*sb + h*sh + t*st + d.
+struct Lattice {
+  int64_t stride[4];
+  int64_t count[4];
+};
+
+Lattice lattice_of(const rel_problem* p) {
+  // ordered by decreasing stride so that the nested decomposition below works
+  int64_t s[4] = {p->stride_b, p->stride_h, p->stride_t, 1};
+  int64_t c[4] = {p->B, p->H, p->T, p->D};
+  int idx[4] = {0, 1, 2, 3};
+  std::sort(idx, idx + 3, [&](int a, int b) { return s[a] > s[b]; });
+  Lattice L;
+  for (int i = 0; i < 4; ++i) {
+    L.stride[i] = s[idx[i]];
+    L.count[i] = c[idx[i]];
+  }
+  return L;
+}
+
+// Strides are nested if each dimension's stride exceeds the span of all
+// dimensions with smaller strides; then distinct indices never share memory.
+bool nested(const Lattice& L) {
+  int64_t span = 0;
+  for (int i = 3; i >= 0; --i) {
+    if (L.count[i] > 1 && L.stride[i] <= span) return false;
+    span += (L.count[i] - 1) * L.stride[i];
+  }
+  return true;
+}
+
+// Is delta = sum_i c_i * stride_i with |c_i| < count_i ? (nested strides)
+bool representable(const Lattice& L, int dim, int64_t delta) {
+  if (dim == 3) return delta > -L.count[3] && delta < L.count[3];
+  const int64_t s = L.stride[dim];
+  if (L.count[dim] <= 1 || s == 0) return representable(L, dim + 1, delta);
+  int64_t lo = delta / s;  // truncation; try the two neighbours of delta / s
+  for (int64_t c : {lo - 1, lo, lo + 1}) {
+    if (c <= -L.count[dim] || c >= L.count[dim]) continue;
+    if (representable(L, dim + 1, delta - c * s)) return true;
+  }
+  return false;
+}
+
+int64_t extent_elems(const rel_problem* p) {
+  return (p->B - 1) * p->stride_b + (p->H - 1) * p->stride_h + (p->T - 1) * p->stride_t + p->D;
+}
+
+struct Buf {
+  const void* ptr;
+  size_t bytes;       // byte range starting at ptr
+  bool tensor;        // [B,H,T,D] lattice with the problem's strides
+  bool output;
+  const char* name;
+};
+
+bool ranges_overlap(const Buf& a, const Buf& b) {
+  const uintptr_t a0 = (uintptr_t)a.ptr, b0 = (uintptr_t)b.ptr;
+  return a0 < b0 + b.bytes && b0 < a0 + a.bytes;
+}
+
+bool aliases(const rel_problem* p, const Lattice& L, const Buf& a, const Buf& b) {
+  if (!ranges_overlap(a, b)) return false;
+  if (a.tensor && b.tensor) {
+    const size_t es = elem_size(p->dtype);
+    const int64_t delta = (int64_t)((intptr_t)b.ptr - (intptr_t)a.ptr);
+    if (delta % (int64_t)es != 0) return true;
+    return representable(L, 0, delta / (int64_t)es);
+  }
+  return true;
+}
+
+rel_status check_buffers(const rel_problem* p, const std::vector<Buf>& bufs) {
+  const Lattice L = lattice_of(p);
+  for (size_t i = 0; i < bufs.size(); ++i) {
+    if (!bufs[i].ptr || !bufs[i].output) continue;
+    for (size_t j = 0; j < bufs.size(); ++j) {
+      if (i == j || !bufs[j].ptr) continue;
+      if (bufs[j].output && j < i) continue;  // output pairs once
+      if (aliases(p, L, bufs[i], bufs[j]))
+        return fail(REL_ERR_INVALID_ARG, "output %s overlaps %s", bufs[i].name, bufs[j].name);
+    }
+  }
+  return REL_OK;
+}
+
+// Problem-level validation shared by every entry point. Sets *empty when there
+// is nothing to compute.
+rel_status check_problem(const rel_problem* p, bool* empty) {
+  if (!p) return fail(REL_ERR_INVALID_ARG, "problem is null");
+  if (p->B < 0 || p->H < 0 || p->T < 0 || p->D < 0)
+    return fail(REL_ERR_INVALID_ARG, "negative size B=%lld H=%lld T=%lld D=%lld", (long long)p->B,
+                (long long)p->H, (long long)p->T, (long long)p->D);
+  if (p->dtype != REL_F32 && p->dtype != REL_BF16)
+    return fail(REL_ERR_UNSUPPORTED, "unknown dtype %d", (int)p->dtype);
+  if (p->causal != 1)
+    return fail(REL_ERR_UNSUPPORTED, "only the causal operator is defined (causal=%d)", (int)p->causal);
+  if (!(std::isfinite(p->tau_s) && p->tau_s > 0.0f))
+    return fail(REL_ERR_INVALID_ARG, "tau_s must be finite and > 0 (got %g)", (double)p->tau_s);
+  if (!std::isfinite(p->scale)) return fail(REL_ERR_INVALID_ARG, "scale must be finite");
+  if (p->D != 32 && p->D != 64 && p->D != 128)
+    return fail(REL_ERR_UNSUPPORTED, "head dimension %lld not in {32, 64, 128}", (long long)p->D);
+  *empty = (p->B == 0 || p->H == 0 || p->T == 0);
+  if (*empty) return REL_OK;
+  if (p->T > (1 << 24)) return fail(REL_ERR_UNSUPPORTED, "T = %lld exceeds 2^24", (long long)p->T);
+  if (p->B * p->H > (1LL << 30)) return fail(REL_ERR_UNSUPPORTED, "B*H exceeds 2^30");
+  const int64_t es = (int64_t)elem_size(p->dtype);
+  const int64_t vec = 16 / es;  // elements per 16 bytes
+  if (p->stride_t < p->D) return fail(REL_ERR_INVALID_ARG, "stride_t (%lld) < D", (long long)p->stride_t);
+  if (p->stride_b < 0 || p->stride_h < 0) return fail(REL_ERR_INVALID_ARG, "negative stride");
+  if (p->stride_t % vec || p->stride_h % vec || p->stride_b % vec)
+    return fail(REL_ERR_INVALID_ARG, "strides must be multiples of 16 bytes");
+  if (!nested(lattice_of(p)))
+    return fail(REL_ERR_INVALID_ARG, "strides make distinct (b, h, t) rows overlap");
+  return REL_OK;
+}
+
+rel_status check_aligned(const void* ptr, size_t align, const char* name, bool required) {
+  if (!ptr) {
+    if (required) return fail(REL_ERR_INVALID_ARG, "%s is null", name);
+    return REL_OK;
+  }
+  if ((uintptr_t)ptr % align) return fail(REL_ERR_INVALID_ARG, "%s is not %zu-byte aligned", name, align);
+  return REL_OK;
+}
+
+float eff_scale(const rel_problem* p) {
+  return p->scale > 0.0f ? p->scale : 1.0f / std::sqrt((float)p->D);
+}
+
+bool test_fail_launch() {
+  const char* e = std::getenv("RELATION_TEST_FAIL_LAUNCH");
+  return e && e[0] == '1';
+}
+
+// rocBLAS handle shared by the materialised path, guarded by a mutex.
+std::mutex g_blas_mu;
+rocblas_handle g_blas = nullptr;
+int g_blas_dev = -1;
+
+}  // namespace
+
+#define REL_TRY(x)                  \
+  do {                              \
+    rel_status _s = (x);            \
+    if (_s != REL_OK) return _s;    \
+  } while (0)
+
+extern "C" {
+
+int relation_abi_version(void) { return RELATION_ABI_VERSION; }
+
+const char* relation_status_string(rel_status s) {
+  switch (s) {
+    case REL_OK: return "ok";
+    case REL_ERR_INVALID_ARG: return "invalid argument";
+    case REL_ERR_UNSUPPORTED: return "unsupported problem";
+    case REL_ERR_WORKSPACE: return "workspace too small";
+    case REL_ERR_HIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+const char* relation_last_error(void) { return g_last_error.c_str(); }
+
+rel_status relation_fwd(const rel_problem* p, const void* q, const void* k, const void* v,
+                        const float* lambda, void* o, float* row_stat, float* self_mass,
+                        float* exch_mass, float* exch_lse, void* stream) {
+  bool empty = false;
+  REL_TRY(check_problem(p, &empty));
+  if (empty) return REL_OK;
+  REL_TRY(check_aligned(q, 16, "q", true));
+  REL_TRY(check_aligned(k, 16, "k", true));
+  REL_TRY(check_aligned(v, 16, "v", true));
+  REL_TRY(check_aligned(o, 16, "o", true));
+  REL_TRY(check_aligned(lambda, 4, "lambda", true));
+  REL_TRY(check_aligned(row_stat, 4, "row_stat", false));
+  REL_TRY(check_aligned(self_mass, 4, "self_mass", false));
+  REL_TRY(check_aligned(exch_mass, 4, "exch_mass", false));
+  REL_TRY(check_aligned(exch_lse, 4, "exch_lse", false));
+  const size_t es = elem_size(p->dtype);
+  const size_t tb = (size_t)extent_elems(p) * es, rb = (size_t)(p->B * p->H * p->T) * 4;
+  REL_TRY(check_buffers(p, {{q, tb, true, false, "q"},
+                            {k, tb, true, false, "k"},
+                            {v, tb, true, false, "v"},
+                            {lambda, 4, false, false, "lambda"},
+                            {o, tb, true, true, "o"},
+                            {row_stat, rb, false, true, "row_stat"},
+                            {self_mass, rb, false, true, "self_mass"},
+                            {exch_mass, rb, false, true, "exch_mass"},
+                            {exch_lse, rb, false, true, "exch_lse"}}));
+  if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected by RELATION_TEST_FAIL_LAUNCH");
+  rel::FwdArgs a{};
+  a.q = q; a.k = k; a.v = v; a.lambda = lambda; a.o = o;
+  a.row_stat = row_stat; a.self_mass = self_mass; a.exch_mass = exch_mass; a.exch_lse = exch_lse;
+  a.sb = p->stride_b; a.sh = p->stride_h; a.st = p->stride_t;
+  a.H = (int)p->H; a.T = (int)p->T;
+  a.scale = eff_scale(p);
+  a.inv_tau = 1.0f / p->tau_s;
+  a.map = rel::make_tilemap((int)(p->B * p->H), 1);
+  hipError_t e = rel::launch_fwd(a, p->dtype, (int)p->D, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "relation_fwd launch");
+  return REL_OK;
+}
+
+rel_status relation_exchange_allocation(const rel_problem* p, const void* q, const void* k,
+                                        const float* exch_lse, float* pi, void* stream) {
+  bool empty = false;
+  REL_TRY(check_problem(p, &empty));
+  if (empty) return REL_OK;
+  REL_TRY(check_aligned(q, 16, "q", true));
+  REL_TRY(check_aligned(k, 16, "k", true));
+  REL_TRY(check_aligned(exch_lse, 4, "exch_lse", true));
+  REL_TRY(check_aligned(pi, 4, "pi", true));
+  const size_t es = elem_size(p->dtype);
+  const size_t tb = (size_t)extent_elems(p) * es, rb = (size_t)(p->B * p->H * p->T) * 4;
+  const size_t mb = (size_t)(p->B * p->H) * (size_t)p->T * (size_t)p->T * 4;
+  REL_TRY(check_buffers(p, {{q, tb, true, false, "q"},
+                            {k, tb, true, false, "k"},
+                            {exch_lse, rb, false, false, "exch_lse"},
+                            {pi, mb, false, true, "pi"}}));
+  if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected by RELATION_TEST_FAIL_LAUNCH");
+  rel::RowArgs a{};
+  a.q = q; a.k = k; a.exch_lse = exch_lse; a.pi = pi;
+  a.sb = p->stride_b; a.sh = p->stride_h; a.st = p->stride_t;
+  a.H = (int)p->H; a.T = (int)p->T; a.D = (int)p->D;
+  a.scale = eff_scale(p);
+  a.inv_tau = 1.0f / p->tau_s;
+  hipError_t e = rel::launch_allocation(a, p->dtype, (int)(p->B * p->H), (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "relation_exchange_allocation launch");
+  return REL_OK;
+}
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+size_t relation_bwd_workspace_bytes(const rel_problem* p) {
+  bool empty = false;
+  if (check_problem(p, &empty) != REL_OK) return 0;
+  if (empty) return 0;
+  const size_t N = (size_t)(p->B * p->H);
+  return align256(N * (size_t)p->T * (size_t)p->D * 4) +
+         align256((size_t)rel::bwd_partials((int)N, (int)p->T, (int)p->D, p->dtype) * 4);
+}
+
+rel_status relation_bwd(const rel_problem* p, const void* q, const void* k, const void* v,
+                        const void* o, const void* dout, const float* lambda,
+                        const float* row_stat, void* dq, void* dk, void* dv, float* dlambda,
+                        float* dself, void* workspace, size_t workspace_bytes, void* stream) {
+  bool empty = false;
+  REL_TRY(check_problem(p, &empty));
+  if (empty) {
+    if (dlambda) {
+      // nothing to differentiate: dlambda is still an output and must be zero
+      if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected");
+      hipError_t e = rel::launch_fill_zero(dlambda, 1, (hipStream_t)stream);
+      if (e != hipSuccess) return hip_fail(e, "relation_bwd dlambda clear");
+    }
+    return REL_OK;
+  }
+  if (p->dtype == REL_F32 && p->D > 64)
+    return fail(REL_ERR_UNSUPPORTED, "fp32 backward supports D <= 64 (got %lld)", (long long)p->D);
+  REL_TRY(check_aligned(q, 16, "q", true));
+  REL_TRY(check_aligned(k, 16, "k", true));
+  REL_TRY(check_aligned(v, 16, "v", true));
+  REL_TRY(check_aligned(o, 16, "o", true));
+  REL_TRY(check_aligned(dout, 16, "dout", true));
+  REL_TRY(check_aligned(dq, 16, "dq", true));
+  REL_TRY(check_aligned(dk, 16, "dk", true));
+  REL_TRY(check_aligned(dv, 16, "dv", true));
+  REL_TRY(check_aligned(lambda, 4, "lambda", true));
+  REL_TRY(check_aligned(row_stat, 4, "row_stat", true));
+  REL_TRY(check_aligned(dlambda, 4, "dlambda", true));
+  REL_TRY(check_aligned(dself, 4, "dself", false));
+  const size_t need = relation_bwd_workspace_bytes(p);
+  if (!workspace || workspace_bytes < need)
+    return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                workspace ? workspace_bytes : (size_t)0);
+  if ((uintptr_t)workspace % 16) return fail(REL_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
+  const size_t es = elem_size(p->dtype);
+  const size_t tb = (size_t)extent_elems(p) * es, rb = (size_t)(p->B * p->H * p->T) * 4;
+  REL_TRY(check_buffers(p, {{q, tb, true, false, "q"},
+                            {k, tb, true, false, "k"},
+                            {v, tb, true, false, "v"},
+                            {o, tb, true, false, "o"},
+                            {dout, tb, true, false, "dout"},
+                            {lambda, 4, false, false, "lambda"},
+                            {row_stat, rb, false, false, "row_stat"},
+                            {dq, tb, true, true, "dq"},
+                            {dk, tb, true, true, "dk"},
+                            {dv, tb, true, true, "dv"},
+                            {dlambda, 4, false, true, "dlambda"},
+                            {dself, rb, false, true, "dself"},
+                            {workspace, need, false, true, "workspace"}}));
+  if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected by RELATION_TEST_FAIL_LAUNCH");
+  const size_t N = (size_t)(p->B * p->H);
+  rel::BwdArgs a{};
+  a.q = q; a.k = k; a.v = v; a.o = o; a.dout = dout; a.lambda = lambda; a.row_stat = row_stat;
+  a.dk = dk; a.dv = dv; a.dself = dself;
+  a.dq_acc = (float*)workspace;
+  a.dlam_part = (float*)((char*)workspace + align256(N * (size_t)p->T * (size_t)p->D * 4));
+  a.sb = p->stride_b; a.sh = p->stride_h; a.st = p->stride_t;
+  a.H = (int)p->H; a.T = (int)p->T;
+  a.scale = eff_scale(p);
+  a.inv_tau = 1.0f / p->tau_s;
+  a.map = rel::make_tilemap((int)N, 1);
+  hipError_t e = rel::launch_bwd(a, p->dtype, (int)p->D, dq, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "relation_bwd launch");
+  e = rel::launch_dlambda(a.dlam_part, rel::bwd_partials((int)N, (int)p->T, (int)p->D, p->dtype),
+                          dlambda, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "relation_bwd dlambda reduction");
+  return REL_OK;
+}
+
+size_t relation_fwd_materialized_workspace_bytes(const rel_problem* p) {
+  bool empty = false;
+  if (check_problem(p, &empty) != REL_OK) return 0;
+  if (empty) return 0;
+  const size_t NTT = (size_t)(p->B * p->H) * (size_t)p->T * (size_t)p->T;
+  return align256(NTT * 4) + align256(NTT * elem_size(p->dtype));
+}
+
+rel_status relation_fwd_materialized(const rel_problem* p, const void* q, const void* k,
+                                     const void* v, const float* lambda, void* o, float* R,
+                                     float* F, float* pi, float* self_mass, float* exch_mass,
+                                     void* workspace, size_t workspace_bytes, void* stream) {
+  bool empty = false;
+  REL_TRY(check_problem(p, &empty));
+  if (empty) return REL_OK;
+  REL_TRY(check_aligned(q, 16, "q", true));
+  REL_TRY(check_aligned(k, 16, "k", true));
+  REL_TRY(check_aligned(v, 16, "v", true));
+  REL_TRY(check_aligned(o, 16, "o", true));
+  REL_TRY(check_aligned(lambda, 4, "lambda", true));
+  REL_TRY(check_aligned(R, 4, "R", false));
+  REL_TRY(check_aligned(F, 4, "F", false));
+  REL_TRY(check_aligned(pi, 4, "pi", false));
+  REL_TRY(check_aligned(self_mass, 4, "self_mass", false));
+  REL_TRY(check_aligned(exch_mass, 4, "exch_mass", false));
+  if (p->T > 65536 || (p->T * (int64_t)p->T) > (1LL << 31))
+    return fail(REL_ERR_UNSUPPORTED, "materialised path limited to T*T < 2^31 per head");
+  const size_t need = relation_fwd_materialized_workspace_bytes(p);
+  if (!workspace || workspace_bytes < need)
+    return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                workspace ? workspace_bytes : (size_t)0);
+  if ((uintptr_t)workspace % 16) return fail(REL_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
+  const size_t es = elem_size(p->dtype);
+  const size_t tb = (size_t)extent_elems(p) * es, rb = (size_t)(p->B * p->H * p->T) * 4;
+  const size_t N = (size_t)(p->B * p->H);
+  const size_t mb = N * (size_t)p->T * (size_t)p->T * 4;
+  REL_TRY(check_buffers(p, {{q, tb, true, false, "q"},
+                            {k, tb, true, false, "k"},
+                            {v, tb, true, false, "v"},
+                            {lambda, 4, false, false, "lambda"},
+                            {o, tb, true, true, "o"},
+                            {R, mb, false, true, "R"},
+                            {F, mb, false, true, "F"},
+                            {pi, mb, false, true, "pi"},
+                            {self_mass, rb, false, true, "self_mass"},
+                            {exch_mass, rb, false, true, "exch_mass"},
+                            {workspace, need, false, true, "workspace"}}));
+  if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected by RELATION_TEST_FAIL_LAUNCH");
+
+  const int T = (int)p->T, D = (int)p->D;
+  const float scale = eff_scale(p);
+  float* U = (float*)workspace;
+  void* Fw = (char*)workspace + align256(N * (size_t)T * (size_t)T * 4);
+  const rocblas_datatype io = p->dtype == REL_BF16 ? rocblas_datatype_bf16_r : rocblas_datatype_f32_r;
+
+  std::lock_guard<std::mutex> lock(g_blas_mu);
+  int dev = 0;
+  hipError_t he = hipGetDevice(&dev);
+  if (he != hipSuccess) return hip_fail(he, "hipGetDevice");
+  if (!g_blas || g_blas_dev != dev) {
+    if (g_blas) rocblas_destroy_handle(g_blas);
+    g_blas = nullptr;
+    if (rocblas_create_handle(&g_blas) != rocblas_status_success)
+      return fail(REL_ERR_HIP, "rocblas_create_handle failed");
+    g_blas_dev = dev;
+  }
+  if (rocblas_set_stream(g_blas, (hipStream_t)stream) != rocblas_status_success)
+    return fail(REL_ERR_HIP, "rocblas_set_stream failed");
+
+  const float one = 1.0f, zero = 0.0f;
+  // Heads of one batch index are equally spaced by stride_h, so each GEMM call
+  // batches over H; the calls loop over B.
+  for (int64_t b = 0; b < p->B; ++b) {
+    const char* qb = (const char*)q + (size_t)(b * p->stride_b) * es;
+    const char* kb = (const char*)k + (size_t)(b * p->stride_b) * es;
+    float* Ub = U + (size_t)b * p->H * T * (size_t)T;
+    // column-major view: U^T (T x T) = K Q^T  ->  row-major U = scale * Q K^T (eq. 1)
+    rocblas_status st = rocblas_gemm_strided_batched_ex(
+        g_blas, rocblas_operation_transpose, rocblas_operation_none, T, T, D, &scale, kb, io,
+        (rocblas_int)p->stride_t, p->stride_h, qb, io, (rocblas_int)p->stride_t, p->stride_h, &zero,
+        Ub, rocblas_datatype_f32_r, T, (rocblas_stride)T * T, Ub, rocblas_datatype_f32_r, T,
+        (rocblas_stride)T * T, (rocblas_int)p->H, rocblas_datatype_f32_r, rocblas_gemm_algo_standard,
+        0, 0);
+    if (st != rocblas_status_success) return fail(REL_ERR_HIP, "rocBLAS U GEMM failed (%d)", (int)st);
+  }
+  rel::RowArgs a{};
+  a.U = U; a.lambda = lambda; a.Fw = Fw; a.R = R; a.F = F; a.pi = pi;
+  a.self_mass = self_mass; a.exch_mass = exch_mass;
+  a.H = (int)p->H; a.T = T; a.D = D;
+  a.scale = scale;
+  a.inv_tau = 1.0f / p->tau_s;
+  he = rel::launch_materialized_rows(a, p->dtype, (int)N, (hipStream_t)stream);
+  if (he != hipSuccess) return hip_fail(he, "materialised row kernel launch");
+  for (int64_t b = 0; b < p->B; ++b) {
+    const char* vb = (const char*)v + (size_t)(b * p->stride_b) * es;
+    char* ob = (char*)o + (size_t)(b * p->stride_b) * es;
+    const char* Fb = (const char*)Fw + (size_t)b * p->H * T * (size_t)T * es;
+    // column-major view: Y^T (D x T) = V^T F^T  ->  row-major Y = F V (eq. 3)
+    rocblas_status st = rocblas_gemm_strided_batched_ex(
+        g_blas, rocblas_operation_none, rocblas_operation_none, D, T, T, &one, vb, io,
+        (rocblas_int)p->stride_t, p->stride_h, Fb, io, T, (rocblas_stride)T * T, &zero, ob, io,
+        (rocblas_int)p->stride_t, p->stride_h, ob, io, (rocblas_int)p->stride_t, p->stride_h,
+        (rocblas_int)p->H, rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
+    if (st != rocblas_status_success) return fail(REL_ERR_HIP, "rocBLAS F.V GEMM failed (%d)", (int)st);
+  }
+  return REL_OK;
+}
+
+}  // extern "C"

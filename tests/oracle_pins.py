@@ -283,6 +283,17 @@ def check_row_blocking(orc):
     for n in ("dq", "dk", "dv", "dS"):
         assert np.allclose(ra[n], rb[n], atol=1e-13), f"blocked {n}"
     assert abs(ra["dlam"] - rb["dlam"]) < 1e-12
+    # a subset of rows gives the same rows; rows {j0..T-1} give complete dk, dv for keys >= j0
+    sub = np.array([0, 3, 17, 30, 44])
+    c = orc.forward(q, k, v, 0.5, want_matrices=False, rows=sub, row_block=2)
+    for n in ("Y", "exch_mass", "M"):
+        assert np.allclose(c[n], a[n][sub], atol=1e-14, equal_nan=True), f"row subset {n}"
+    j0 = 30
+    rc = orc.backward(q, k, v, 0.5, dO, rows=np.arange(j0, T), row_block=4)
+    assert np.allclose(rc["dq"], ra["dq"][j0:], atol=1e-13), "row subset dq"
+    assert np.allclose(rc["dk"][j0:], ra["dk"][j0:], atol=1e-13), "row subset dk"
+    assert np.allclose(rc["dv"][j0:], ra["dv"][j0:], atol=1e-13), "row subset dv"
+    assert np.allclose(rc["dS"], ra["dS"][j0:], atol=1e-13), "row subset dS"
 
 
 ALL_CHECKS = [

@@ -1,0 +1,297 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle on the
+same seeded inputs. fp32: max-abs <= 1e-4; bf16: relative l2 <= 2e-2, for
+outputs and gradients."""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_20172_amd import inputs as I
+from paper_2608_20172_amd import binding as R
+from tests.gpu_helpers import (assert_close, assert_scalar_close, lam_value, log, oracle_heads,
+                               sample_heads, to_device)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    R.load_library()
+
+
+def _prep(inp, dtype):
+    q, qr = to_device(inp["q"], dtype)
+    k, kr = to_device(inp["k"], dtype)
+    v, vr = to_device(inp["v"], dtype)
+    out = {"q": q, "k": k, "v": v, "qr": qr, "kr": kr, "vr": vr, "lam": lam_value(inp["lam"])}
+    if inp.get("dout") is not None:
+        out["do"], out["dor"] = to_device(inp["dout"], dtype)
+    return out
+
+
+def _np(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def check_forward(x, dtype, heads=None, rows=None, row_block=256, with_aux=True):
+    """Fused forward vs oracle on the given heads (default: all)."""
+    B, H, T, D = x["q"].shape
+    log(f"[fwd] B={B} H={H} T={T} D={D} {dtype} lam={x['lam']:.4f}")
+    out = R.relation_fwd(x["q"], x["k"], x["v"], x["lam"], want_masses=with_aux, want_lse=with_aux)
+    torch.cuda.synchronize()
+    heads = heads or [(b, h) for b in range(B) for h in range(H)]
+    o = _np(out["o"])
+    for (b, h) in heads:
+        f = oracle.forward(x["qr"][b, h], x["kr"][b, h], x["vr"][b, h], x["lam"],
+                           want_matrices=False, row_block=row_block, rows=rows)
+        rr = f["rows"]
+        assert_close(f"o[{b},{h}]", o[b, h][rr], f["Y"], dtype)
+        # row statistics are fp32 in both dtypes; hold them to the same bar as the outputs
+        assert_close(f"M[{b},{h}]", _np(out["row_stat"])[b, h][rr], f["M"], dtype)
+        if with_aux:
+            assert_close(f"self_mass[{b},{h}]", _np(out["self_mass"])[b, h][rr], f["self_mass"], dtype)
+            assert_close(f"exch_mass[{b},{h}]", _np(out["exch_mass"])[b, h][rr], f["exch_mass"], dtype)
+            assert_close(f"exch_lse[{b},{h}]", _np(out["exch_lse"])[b, h][rr], f["LE"], dtype)
+    return out
+
+
+def check_backward(x, dtype, fwd, heads=None, rows=None, row_block=256, key_from=0):
+    B, H, T, D = x["q"].shape
+    log(f"[bwd] B={B} H={H} T={T} D={D} {dtype}")
+    g = R.relation_bwd(x["q"], x["k"], x["v"], fwd["o"], x["do"], x["lam"], fwd["row_stat"],
+                       want_dself=True)
+    torch.cuda.synchronize()
+    all_heads = heads is None
+    heads = heads or [(b, h) for b in range(B) for h in range(H)]
+    dq, dk, dv, dself = _np(g["dq"]), _np(g["dk"]), _np(g["dv"]), _np(g["dself"])
+    dlam_gpu = float(g["dlambda"].item())
+    dlam_ref, terms = 0.0, 0.0
+    for (b, h) in heads:
+        r = oracle.backward(x["qr"][b, h], x["kr"][b, h], x["vr"][b, h], x["lam"], x["dor"][b, h],
+                            row_block=row_block, rows=rows)
+        rr = r["rows"]
+        assert_close(f"dq[{b},{h}]", dq[b, h][rr], r["dq"], dtype)
+        assert_close(f"dk[{b},{h}]", dk[b, h][key_from:], r["dk"][key_from:], dtype)
+        assert_close(f"dv[{b},{h}]", dv[b, h][key_from:], r["dv"][key_from:], dtype)
+        assert_close(f"dself[{b},{h}]", dself[b, h][rr], r["dS"], dtype)
+        dlam_ref += r["dlam"]
+        terms += float(np.sum(np.abs(np.log(rr + 1.0) * r["dS"])))
+    if all_heads and rows is None:
+        assert_scalar_close("dlambda", dlam_gpu, dlam_ref, terms, dtype)
+    # dlambda is the ln(i)-weighted sum of the Self credits over every head and row
+    i1 = np.arange(1, T + 1, dtype=np.float64)
+    via_dself = float(np.sum(np.log(i1)[None, None, :] * dself))
+    tot_terms = float(np.sum(np.abs(np.log(i1)[None, None, :] * dself)))
+    assert abs(via_dself - dlam_gpu) <= 1e-4 * max(tot_terms, 1e-30) + 1e-6, \
+        f"dlambda {dlam_gpu} vs sum ln(i) dself {via_dself}"
+    return g
+
+
+# ----------------------------------------------------------------------------
+# the small fp32 workload: 1 x 2 heads, T=128, D=32, forward with R, F, masses
+# ----------------------------------------------------------------------------
+def test_tiny_fp32_forward_and_materialized():
+    w = I.WORKLOADS["tiny_fp32"]
+    x = _prep(I.make_workload_inputs(w), "f32")
+    out = check_forward(x, "f32")
+    B, H, T, D = x["q"].shape
+    m = R.relation_fwd_materialized(x["q"], x["k"], x["v"], x["lam"], want_R=True, want_F=True,
+                                    want_pi=True, want_masses=True)
+    torch.cuda.synchronize()
+    for b in range(B):
+        for h in range(H):
+            f = oracle.forward(x["qr"][b, h], x["kr"][b, h], x["vr"][b, h], x["lam"])
+            assert_close(f"mat.o[{b},{h}]", _np(m["o"])[b, h], f["Y"], "f32")
+            assert_close(f"mat.R[{b},{h}]", _np(m["R"])[b, h], f["R"], "f32")
+            assert_close(f"mat.F[{b},{h}]", _np(m["F"])[b, h], f["F"], "f32")
+            assert_close(f"mat.pi[{b},{h}]", _np(m["pi"])[b, h], f["pi"], "f32")
+            assert_close(f"mat.self_mass[{b},{h}]", _np(m["self_mass"])[b, h], f["self_mass"], "f32")
+            assert_close(f"mat.exch_mass[{b},{h}]", _np(m["exch_mass"])[b, h], f["exch_mass"], "f32")
+    pi = R.relation_exchange_allocation(x["q"], x["k"], out["exch_lse"])
+    torch.cuda.synchronize()
+    for b in range(B):
+        for h in range(H):
+            f = oracle.forward(x["qr"][b, h], x["kr"][b, h], x["vr"][b, h], x["lam"])
+            assert_close(f"flash.pi[{b},{h}]", _np(pi)[b, h], f["pi"], "f32")
+    # invariants on the device outputs: masses sum to one, row 1 is pure Self
+    sm, em = _np(out["self_mass"]), _np(out["exch_mass"])
+    assert np.max(np.abs(sm + em - 1.0)) < 1e-6
+    assert np.all(sm[:, :, 0] == 1.0) and np.all(em[:, :, 0] == 0.0)
+    assert np.array_equal(_np(out["o"])[:, :, 0], x["vr"][:, :, 0])
+
+
+@pytest.mark.parametrize("D", [32, 64, 128])
+def test_forward_bf16_ragged(D):
+    x = _prep(I.make_inputs(2, 3, 333, D, seed=7, qkv_std=1 / math.sqrt(D), with_dout=False, lam=0.5), "bf16")
+    check_forward(x, "bf16")
+
+
+@pytest.mark.parametrize("D", [32, 64, 128])
+def test_forward_fp32_ragged(D):
+    x = _prep(I.make_inputs(1, 2, 200, D, seed=8, qkv_std=1.0, with_dout=False, lam=0.3), "f32")
+    check_forward(x, "f32")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_forward_sharp(dtype):
+    """Evidence of tens of units: the running reference of the scan must move."""
+    x = _prep(I.make_sharp_inputs(2, 2, 300, 64, seed=9, with_dout=False, lam=0.5), dtype)
+    check_forward(x, dtype)
+
+
+@pytest.mark.parametrize("T", [1, 2, 3, 31, 32, 33, 63, 64, 65, 127, 128, 129, 1000])
+def test_forward_edge_lengths(T):
+    x = _prep(I.make_inputs(1, 2, T, 64, seed=T, qkv_std=0.5, with_dout=False, lam=0.5), "bf16")
+    out = check_forward(x, "bf16")
+    o = _np(out["o"])
+    assert np.array_equal(o[:, :, 0], x["vr"][:, :, 0]), "row 1 must be pure Self: y_1 = v_1"
+
+
+@pytest.mark.parametrize("lam", [0.5, 0.0, -1.0, 2.0, 8.0, -8.0])
+def test_forward_lambda_values(lam):
+    x = _prep(I.make_inputs(1, 2, 257, 64, seed=3, qkv_std=0.7, with_dout=False, lam=lam), "bf16")
+    check_forward(x, "bf16")
+
+
+@pytest.mark.parametrize("D", [32, 64, 128])
+def test_backward_bf16_ragged(D):
+    x = _prep(I.make_inputs(2, 2, 300, D, seed=11, qkv_std=1 / math.sqrt(D), lam=0.5), "bf16")
+    f = check_forward(x, "bf16", with_aux=False)
+    check_backward(x, "bf16", f)
+
+
+@pytest.mark.parametrize("D", [32, 64])
+def test_backward_fp32(D):
+    x = _prep(I.make_inputs(1, 2, 190, D, seed=12, qkv_std=1.0, lam=0.4), "f32")
+    f = check_forward(x, "f32", with_aux=False)
+    check_backward(x, "f32", f)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_backward_sharp(dtype):
+    x = _prep(I.make_sharp_inputs(1, 2, 260, 64, seed=13, lam=0.5), dtype)
+    f = check_forward(x, dtype, with_aux=False)
+    check_backward(x, dtype, f)
+
+
+@pytest.mark.parametrize("T", [1, 2, 65, 127, 128, 129])
+def test_backward_edge_lengths(T):
+    x = _prep(I.make_inputs(1, 2, T, 64, seed=100 + T, qkv_std=0.5, lam=-0.5), "bf16")
+    f = check_forward(x, "bf16", with_aux=False)
+    g = check_backward(x, "bf16", f)
+    if T == 1:
+        assert not _np(g["dq"]).any() and not _np(g["dk"]).any()
+        assert np.allclose(_np(g["dv"]), x["dor"], atol=0)
+
+
+def test_strided_layout_matches_contiguous():
+    """[B, T, H, D] storage (head stride D) gives the same results as [B, H, T, D]."""
+    inp = I.make_inputs(2, 3, 150, 64, seed=21, qkv_std=0.125, lam=0.5)
+    x = _prep(inp, "bf16")
+    f1 = R.relation_fwd(x["q"], x["k"], x["v"], x["lam"])
+    g1 = R.relation_bwd(x["q"], x["k"], x["v"], f1["o"], x["do"], x["lam"], f1["row_stat"])
+    t = lambda a: a.transpose(1, 2).contiguous().transpose(1, 2)  # same values, [B,T,H,D] storage
+    qs, ks, vs, ds = t(x["q"]), t(x["k"]), t(x["v"]), t(x["do"])
+    assert qs.stride() != x["q"].stride()
+    f2 = R.relation_fwd(qs, ks, vs, x["lam"])
+    g2 = R.relation_bwd(qs, ks, vs, f2["o"], ds, x["lam"], f2["row_stat"])
+    torch.cuda.synchronize()
+    assert torch.equal(f1["o"], f2["o"].contiguous())
+    assert torch.equal(f1["row_stat"], f2["row_stat"])
+    for n in ("dk", "dv"):
+        assert torch.equal(g1[n], g2[n].contiguous()), n
+    assert (g1["dq"].float() - g2["dq"].float()).abs().max().item() < 1e-2
+
+
+def test_autograd_wrapper():
+    x = _prep(I.make_inputs(1, 2, 130, 64, seed=22, qkv_std=0.125, lam=0.5), "bf16")
+    q = x["q"].clone().requires_grad_(True)
+    k = x["k"].clone().requires_grad_(True)
+    v = x["v"].clone().requires_grad_(True)
+    lam = torch.tensor(x["lam"], dtype=torch.float32, device="cuda", requires_grad=True)
+    y = R.relation(q, k, v, lam)
+    y.backward(x["do"])
+    f = R.relation_fwd(x["q"], x["k"], x["v"], x["lam"])
+    g = R.relation_bwd(x["q"], x["k"], x["v"], f["o"], x["do"], x["lam"], f["row_stat"])
+    torch.cuda.synchronize()
+    assert torch.equal(y.detach(), f["o"])
+    assert torch.equal(k.grad, g["dk"]) and torch.equal(v.grad, g["dv"])
+    assert abs(lam.grad.item() - g["dlambda"].item()) <= 1e-6 * max(1.0, abs(g["dlambda"].item()))
+
+
+def test_backward_repeatability():
+    """dk, dv, dlambda and dself are reduced in a fixed order: bitwise repeatable."""
+    x = _prep(I.make_inputs(2, 2, 400, 64, seed=23, qkv_std=0.125, lam=0.5), "bf16")
+    f = R.relation_fwd(x["q"], x["k"], x["v"], x["lam"])
+    runs = [R.relation_bwd(x["q"], x["k"], x["v"], f["o"], x["do"], x["lam"], f["row_stat"],
+                           want_dself=True) for _ in range(3)]
+    torch.cuda.synchronize()
+    for r in runs[1:]:
+        for n in ("dk", "dv", "dlambda", "dself"):
+            assert torch.equal(r[n], runs[0][n]), n
+
+
+# ----------------------------------------------------------------------------
+# decoder-scale workloads at full size, in the benchmark's launch configuration
+# ----------------------------------------------------------------------------
+def test_workload_dec10m_forward_vs_materialized():
+    w = I.WORKLOADS["dec10m_T512"]
+    x = _prep(I.make_workload_inputs(w), "bf16")
+    out = check_forward(x, "bf16", heads=sample_heads(w.B, w.H, 4))
+    m = R.relation_fwd_materialized(x["q"], x["k"], x["v"], x["lam"], want_masses=True)
+    torch.cuda.synchronize()
+    for b, h in sample_heads(w.B, w.H, 2):
+        f = oracle.forward(x["qr"][b, h], x["kr"][b, h], x["vr"][b, h], x["lam"], want_matrices=False,
+                           row_block=256)
+        assert_close(f"mat.o[{b},{h}]", _np(m["o"])[b, h], f["Y"], "bf16")
+        assert_close(f"mat.exch_mass[{b},{h}]", _np(m["exch_mass"])[b, h], f["exch_mass"], "bf16")
+    # every head: the fused and the materialised outputs agree
+    assert_close("flash vs materialised o", _np(out["o"]), _np(m["o"]), "bf16")
+
+
+def test_workload_dec30m_forward_backward():
+    w = I.WORKLOADS["dec30m_T1024"]
+    x = _prep(I.make_workload_inputs(w), "bf16")
+    heads = sample_heads(w.B, w.H, 3)
+    f = check_forward(x, "bf16", heads=heads)
+    check_backward(x, "bf16", f, heads=heads)
+
+
+def test_workload_dec100m_forward_backward():
+    w = I.WORKLOADS["dec100m_T2048"]
+    x = _prep(I.make_workload_inputs(w), "bf16")
+    # include a head that holds boosted rows
+    mask = I.make_workload_inputs(w)["boost_mask"]
+    heads = sample_heads(w.B, w.H, 2)
+    bh = np.argwhere(mask.any(axis=2))[0]
+    heads.append((int(bh[0]), int(bh[1])))
+    f = check_forward(x, "bf16", heads=heads)
+    check_backward(x, "bf16", f, heads=heads)
+
+
+def test_workload_long_context_sampled():
+    """T = 16384, D = 128: forward on sampled rows of two heads; backward on the
+    last 256 rows of one head, which completes dk, dv for the last 256 keys;
+    properties that hold at any size for everything else."""
+    w = I.WORKLOADS["long_T16384"]
+    x = _prep(I.make_workload_inputs(w), "bf16")
+    T = w.T
+    rows = np.unique(np.concatenate([np.arange(0, 8), np.linspace(8, T - 1, 56).astype(np.int64),
+                                     np.arange(T - 8, T)]))
+    f = check_forward(x, "bf16", heads=[(0, 0), (0, w.H - 1)], rows=rows)
+    tail = np.arange(T - 256, T)
+    g = check_backward(x, "bf16", f, heads=[(0, 3)], rows=tail, key_from=T - 256)
+    # sum_j dV_j = sum_i dO_i, because every row of F sums to one
+    dv = _np(g["dv"]).sum(axis=2)
+    do = x["dor"].sum(axis=2)
+    err = np.abs(dv - do).max() / np.abs(do).max()
+    log(f"  sum dV vs sum dO: rel err {err:.3e}")
+    assert err < 2e-2
+    sm = f["self_mass"]
+    assert sm is not None

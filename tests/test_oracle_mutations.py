@@ -15,20 +15,20 @@ SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
 # (name, exact text in the oracle, replacement)
 MUTATIONS = [
     ("silu_drops_U_factor", "E = U * expit(U)", "E = expit(U)"),
-    ("self_temperature_inverted", "expit(U[np.arange(r1 - r0), rows] / tau_s)",
-     "expit(U[np.arange(r1 - r0), rows] * tau_s)"),
+    ("self_temperature_inverted", "expit(U[np.arange(nb), rows] / tau_s)",
+     "expit(U[np.arange(nb), rows] * tau_s)"),
     ("count_correction_sign", "(E - lam * np.log(ione)[:, None])[below]",
      "(E + lam * np.log(ione)[:, None])[below]"),
-    ("count_index_zero_based_shift", "ione = (rows + 1).astype(np.float64)            # one-based",
+    ("count_index_zero_based_shift", "ione = (rows + 1).astype(np.float64)            # one-based count",
      "ione = (rows + 2).astype(np.float64)            # one-based"),
-    ("U_transposed_operands", "U = s * (q[r0:r1] @ k.T)", "U = s * (k[r0:r1] @ q.T)"),
-    ("missing_scale", "U = s * (q[r0:r1] @ k.T)", "U = (q[r0:r1] @ k.T)"),
-    ("transport_uses_keys", "Y[r0:r1] = F @ v ", "Y[r0:r1] = F @ k "),
-    ("exchange_mass_includes_self", "        below = np.arange(T)[None, :] < rows[:, None]\n        g[r0:r1]",
-     "        below = np.arange(T)[None, :] <= rows[:, None]\n        g[r0:r1]"),
+    ("U_transposed_operands", "U = s * (q[rows] @ k.T)", "U = s * (k[rows] @ q.T)"),
+    ("missing_scale", "U = s * (q[rows] @ k.T)", "U = (q[rows] @ k.T)"),
+    ("transport_uses_keys", "Y[b0:b1] = F @ v ", "Y[b0:b1] = F @ k "),
+    ("exchange_mass_includes_self", "        below = np.arange(T)[None, :] < rr[:, None]\n        g[b0:b1]",
+     "        below = np.arange(T)[None, :] <= rr[:, None]\n        g[b0:b1]"),
     ("self_grad_drops_tau", "dU[diag] = dR[diag] * Sb * (1.0 - Sb) / tau_s",
      "dU[diag] = dR[diag] * Sb * (1.0 - Sb)"),
-    ("dk_transposed", "dk += s * (dU.T @ q[r0:r1])", "dk += s * (dU @ q[r0:r1])"),
+    ("dk_transposed", "dk += s * (dU.T @ q[rr])", "dk += s * (dU @ q[rr])"),
     ("silu_grad_drops_term", "return sg + U * sg * (1.0 - sg)", "return sg"),
     ("dlam_sign", "dlam += float(-(np.log(ione)", "dlam += float((np.log(ione)"),
     ("factorised_dS_sign", "dS = -g * (1.0 - g) * c ", "dS = g * (1.0 - g) * c "),
