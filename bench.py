@@ -1,0 +1,348 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused causal Full Relation operator (FlashRelation) on one
+MI355X: forward + backward tokens/s on the 100M-decoder-scale layer
+(B=8, H=12, T=2048, D=64, bf16, 5% of query rows boosted x8).
+
+One step = relation_fwd + relation_bwd over the whole batch, inputs resident
+in HBM. Prints one JSON line. Extra legs: the materialised baseline's forward
+(for the speedup), per-kernel durations from HIP events recorded around the
+fused kernels inside the timed region, and the fp64 oracle on a bounded sample
+of heads on the host cores.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+  python bench.py --copy-bytes N   # plain device copy of N bytes (counter calibration)
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from paper_2608_20172_amd.inputs import WORKLOADS, make_workload_inputs  # noqa: E402
+
+METRIC = "FlashRelation fwd+bwd tokens/s and % bf16 MFMA peak; speedup vs materialised"
+PEAK_BF16 = 2.5e15      # MI355X dense bf16 MFMA, FLOP/s
+PEAK_HBM = 8.0e12       # MI355X HBM3E, B/s
+MATERIALIZED_BUDGET = 8 << 30  # bytes of T x T workspace the baseline may use
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "bwd_kernel_traffic.json")
+KERNEL_SOURCES = ["paper_2608_20172_amd/csrc/bwd.hip", "paper_2608_20172_amd/csrc/common.h"]
+
+
+def pairs(T: int) -> int:
+    return T * (T - 1) // 2
+
+
+def flops(w, which: str) -> float:
+    """Algorithmic MFMA flops: forward 4 D per strictly causal pair (QK^T and
+    F V), backward 10 D (QK^T recomputed, dO V^T, F^T dO, dU^T Q, dU K)."""
+    per = {"fwd": 4, "bwd": 10}[which]
+    return float(per * w.D * w.N * pairs(w.T))
+
+
+def sources_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline: the fp64 oracle on a bounded sample of heads
+# ---------------------------------------------------------------------------
+def _warm_worker(_):
+    import oracle  # noqa: F401
+    import scipy.special  # noqa: F401
+    from threadpoolctl import threadpool_limits  # noqa: F401
+    return os.getpid()
+
+
+def _oracle_head(args):
+    q, k, v, do, lam = args
+    from threadpoolctl import threadpool_limits
+    import oracle
+    with threadpool_limits(1):
+        t0 = time.perf_counter()
+        oracle.forward(q, k, v, lam, want_matrices=False, row_block=256)
+        oracle.backward(q, k, v, lam, do, row_block=256)
+        return time.perf_counter() - t0
+
+
+def cpu_baseline(w, rounded, lam, budget_s: float) -> dict:
+    import multiprocessing as mp
+    import numpy as np
+    workers = max(1, min(16, os.cpu_count() or 1))
+    heads = [(b, h) for b in range(w.B) for h in range(w.H)]
+    # one head to size the sample, then enough heads for ~budget_s of CPU work
+    probe = _oracle_head((rounded["q"][0, 0], rounded["k"][0, 0], rounded["v"][0, 0],
+                          rounded["dout"][0, 0], lam))
+    n = int(max(workers, min(len(heads), round(budget_s / max(probe, 1e-3)))))
+    n = max(1, min(len(heads), (n // workers) * workers or workers))
+    sample = heads[:n]
+    jobs = [(rounded["q"][b, h], rounded["k"][b, h], rounded["v"][b, h], rounded["dout"][b, h], lam)
+            for (b, h) in sample]
+    ctx = mp.get_context("spawn")
+    with ctx.Pool(workers) as pool:
+        pool.map(_warm_worker, range(4 * workers))  # start-up and imports are not timed
+        t0 = time.perf_counter()
+        per_head = pool.map(_oracle_head, jobs, chunksize=1)
+        wall = time.perf_counter() - t0
+    full_wall = wall * len(heads) / len(sample)
+    return {
+        "value": w.tokens / full_wall,
+        "unit": "tokens/s",
+        "cores": workers,
+        "kind": "oracle",
+        "sample": (f"fp64 oracle forward+backward on {len(sample)} of {len(heads)} heads "
+                   f"(T={w.T}, D={w.D}), {workers} worker processes x 1 BLAS thread, "
+                   f"{wall:.1f} s wall / {sum(per_head):.1f} s CPU; scaled to all heads"),
+    }
+
+
+def round_inputs(inp, dtype: str) -> dict:
+    """The exact values the device receives, as fp64 (bf16 rounding by torch on the CPU)."""
+    import torch
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    out = {}
+    for n in ("q", "k", "v", "dout"):
+        if inp.get(n) is not None:
+            out[n] = torch.from_numpy(inp[n]).to(tdt).to(torch.float64).numpy()
+    return out
+
+
+# ---------------------------------------------------------------------------
+# HIP events through the runtime library (recorded by librelation itself)
+# ---------------------------------------------------------------------------
+class Hip:
+    def __init__(self):
+        self.lib = ctypes.CDLL("libamdhip64.so")
+        self.lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def events(self, n):
+        evs = []
+        for _ in range(n):
+            e = ctypes.c_void_p()
+            if self.lib.hipEventCreate(ctypes.byref(e)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            evs.append(e.value)
+        return evs
+
+    def elapsed_ms(self, a, b) -> float:
+        ms = ctypes.c_float()
+        if self.lib.hipEventElapsedTime(ctypes.byref(ms), a, b) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(ms.value)
+
+    def destroy(self, evs):
+        for e in evs:
+            self.lib.hipEventDestroy(e)
+
+
+def arm(lib, kernel: str, evs):
+    arr = (ctypes.c_void_p * len(evs))(*evs)
+    st = lib.relation_profile_arm(kernel.encode(), arr, len(evs) // 2)
+    if st != 0:
+        raise RuntimeError("relation_profile_arm failed")
+    return arr
+
+
+def traffic_for(kernel_hash: str):
+    """HBM bytes per launch of the backward kernel, from the committed counter
+    summary, if it was taken on the current kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("sources_hash") != kernel_hash:
+        return None
+    return t.get("bytes_per_launch")
+
+
+# ---------------------------------------------------------------------------
+def copy_mode(nbytes: int, reps: int) -> None:
+    import torch
+    x = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").uniform_()
+    y = torch.empty_like(x)
+    for _ in range(reps):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": nbytes, "reps": reps}), flush=True)
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="dec100m_T2048", choices=sorted(WORKLOADS))
+    ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-materialized", action="store_true")
+    ap.add_argument("--copy-bytes", type=int, default=0)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: the fused operator is measured on one "
+              "MI355X; multi-GPU runs are not part of this build.", file=sys.stderr)
+        return 2
+    if args.copy_bytes:
+        copy_mode(args.copy_bytes, max(1, args.steps))
+        return 0
+
+    w = WORKLOADS[args.workload]
+    inp = make_workload_inputs(w)
+    lam = float(inp["lam"])
+
+    # CPU baseline first, before anything initialises the GPU
+    cpu = None
+    if not args.no_cpu_baseline and w.backward:
+        rounded = round_inputs(inp, w.dtype)
+        lam32 = float(__import__("numpy").float32(lam))
+        cpu = cpu_baseline(w, rounded, lam32, args.cpu_seconds)
+
+    import torch
+    from paper_2608_20172_amd import binding as R
+
+    lib = R.load_library()
+    hip = Hip()
+    dev = torch.device("cuda:0")
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    q, k, v = (torch.from_numpy(inp[n]).to(tdt).to(dev) for n in ("q", "k", "v"))
+    do = torch.from_numpy(inp["dout"]).to(tdt).to(dev) if w.backward else None
+    lam_t = torch.tensor([lam], dtype=torch.float32, device=dev)
+    ws = torch.empty(max(1, R.relation_bwd_workspace_bytes(q)), dtype=torch.uint8, device=dev)
+
+    def step():
+        f = R.relation_fwd(q, k, v, lam_t)
+        if w.backward:
+            R.relation_bwd(q, k, v, f["o"], do, lam_t, f["row_stat"], workspace=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    main_kernel = "bwd" if w.backward else "fwd"
+    kev = hip.events(2 * K)
+    keep = arm(lib, main_kernel, kev)
+    split = [torch.cuda.Event(enable_timing=True) for _ in range(3 * K)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for s in range(K):
+        split[3 * s].record()
+        f = R.relation_fwd(q, k, v, lam_t)
+        split[3 * s + 1].record()
+        if w.backward:
+            R.relation_bwd(q, k, v, f["o"], do, lam_t, f["row_stat"], workspace=ws)
+        split[3 * s + 2].record()
+    t1.record()
+    torch.cuda.synchronize()
+    recorded = lib.relation_profile_disarm()
+    del keep
+    total_ms = t0.elapsed_time(t1)
+    ms_step = total_ms / K
+    fwd_ms = sum(split[3 * s].elapsed_time(split[3 * s + 1]) for s in range(K)) / K
+    bwd_ms = sum(split[3 * s + 1].elapsed_time(split[3 * s + 2]) for s in range(K)) / K
+    kern_ms = sum(hip.elapsed_ms(kev[2 * s], kev[2 * s + 1]) for s in range(recorded)) / max(recorded, 1)
+    hip.destroy(kev)
+
+    # the fused forward kernel alone (second pass, same launches)
+    fev = hip.events(2 * K)
+    keep = arm(lib, "fwd", fev)
+    for _ in range(K):
+        R.relation_fwd(q, k, v, lam_t)
+    torch.cuda.synchronize()
+    nf = lib.relation_profile_disarm()
+    del keep
+    fwd_kern_ms = sum(hip.elapsed_ms(fev[2 * s], fev[2 * s + 1]) for s in range(nf)) / max(nf, 1)
+    hip.destroy(fev)
+
+    # materialised baseline forward
+    mat = {"status": "skipped"}
+    if not args.no_materialized:
+        need = R.relation_fwd_materialized_workspace_bytes(q)
+        if need > MATERIALIZED_BUDGET:
+            mat = {"status": f"skipped: T x T workspace {need / 2**30:.1f} GiB exceeds the "
+                              f"{MATERIALIZED_BUDGET / 2**30:.0f} GiB budget"}
+        else:
+            mws = torch.empty(need, dtype=torch.uint8, device=dev)
+            for _ in range(max(2, args.warmup)):
+                R.relation_fwd_materialized(q, k, v, lam_t, workspace=mws)
+            torch.cuda.synchronize()
+            m0 = torch.cuda.Event(enable_timing=True)
+            m1 = torch.cuda.Event(enable_timing=True)
+            mk = max(5, K // 2)
+            m0.record()
+            for _ in range(mk):
+                R.relation_fwd_materialized(q, k, v, lam_t, workspace=mws)
+            m1.record()
+            torch.cuda.synchronize()
+            mat_ms = m0.elapsed_time(m1) / mk
+            NTT = w.N * w.T * w.T
+            tt_bytes = NTT * (4 + 4 + 2 + 2)  # U written + read (fp32), F written + read (bf16)
+            mat = {"status": "ok", "fwd_ms": mat_ms, "speedup_fwd": mat_ms / fwd_ms,
+                   "txt_hbm_GBps": tt_bytes / (mat_ms * 1e-3) / 1e9}
+            del mws
+
+    fl_f, fl_b = flops(w, "fwd"), flops(w, "bwd") if w.backward else 0.0
+    kern_flops = fl_b if w.backward else fl_f
+    achieved = kern_flops / (kern_ms * 1e-3)
+    khash = sources_hash()
+    traffic = traffic_for(khash) if w.backward else None
+    out = {
+        "metric": METRIC,
+        "value": w.tokens / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "T": w.T, "D": w.D,
+                   "passes": "fwd+bwd" if w.backward else "fwd", "boost_frac": w.boost_frac,
+                   "parallelism": "single GPU"},
+        "step_tflops": (fl_f + fl_b) / (ms_step * 1e-3) / 1e12,
+        "mfma_peak_frac": (fl_f + fl_b) / (ms_step * 1e-3) / PEAK_BF16,
+        "fwd_ms": fwd_ms,
+        "bwd_ms": bwd_ms,
+        "fwd_kernel_ms": fwd_kern_ms,
+        "fwd_kernel_tflops": fl_f / (fwd_kern_ms * 1e-3) / 1e12,
+        "materialized": mat,
+        "roofline": {
+            "kernel": "bwd_bf16_kernel" if w.backward else "fwd_bf16_kernel",
+            "bound": "mfma",
+            "achieved": achieved / 1e12,
+            "peak": PEAK_BF16 / 1e12,
+            "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16,
+            "traffic": traffic,
+            "launches_timed": int(recorded),
+            "kernel_ms": kern_ms,
+            "sources_hash": khash,
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -128,6 +128,17 @@ rel_status relation_fwd_materialized(const rel_problem* p, const void* q, const 
                                      float* F, float* pi, float* self_mass, float* exch_mass,
                                      void* workspace, size_t workspace_bytes, void* stream);
 
+/* Measurement aid. While armed, every launch of the named kernel ("fwd": the
+ * fused forward kernel; "bwd": the fused backward main kernel) is bracketed by
+ * hipEventRecord on its launch stream, using the caller's events in pairs
+ * (events[2i] before launch i, events[2i+1] after it) until n_pairs launches
+ * have been recorded. The events are owned by the caller (hipEvent_t, created
+ * without the disable-timing flag). Arming replaces any previous arming.
+ * relation_profile_disarm() returns the number of pairs recorded. The state
+ * is process-wide and guarded by a mutex. */
+rel_status relation_profile_arm(const char* kernel, void** events, int n_pairs);
+int relation_profile_disarm(void);
+
 const char* relation_status_string(rel_status s);
 const char* relation_last_error(void);
 int relation_abi_version(void);

@@ -43,6 +43,8 @@ _SIGS = {
     "relation_fwd_materialized_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(RelProblem)]),
     "relation_fwd_materialized": (ctypes.c_int, [ctypes.POINTER(RelProblem), _P, _P, _P, _P, _P, _P, _P,
                                                  _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "relation_profile_arm": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]),
+    "relation_profile_disarm": (ctypes.c_int, []),
     "relation_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "relation_last_error": (ctypes.c_char_p, []),
     "relation_abi_version": (ctypes.c_int, []),
@@ -227,6 +229,19 @@ def relation_fwd_materialized(q, k, v, lam, *, tau_s: float = TAU_S, scale: Opti
                                        workspace.numel() * workspace.element_size(), _stream())
     _check(st, "relation_fwd_materialized")
     return {"o": o, "R": R, "F": F, "pi": pi, "self_mass": sm, "exch_mass": em}
+
+
+def relation_profile_arm(kernel: str, events: list) -> None:
+    """Record each listed torch.cuda.Event pair around successive launches of
+    ``kernel`` ("fwd" or "bwd"); events = [start0, stop0, start1, stop1, ...]."""
+    lib = load_library()
+    arr = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
+    _check(lib.relation_profile_arm(kernel.encode(), arr, len(events) // 2), "relation_profile_arm")
+    relation_profile_arm._keep = arr
+
+
+def relation_profile_disarm() -> int:
+    return int(load_library().relation_profile_disarm())
 
 
 class _RelationFn(torch.autograd.Function):

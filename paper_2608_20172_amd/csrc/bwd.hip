@@ -589,6 +589,9 @@ hipError_t launch_bwd(const BwdArgs& a0, int dtype, int D, void* dq_out, hipStre
                        stream, a.dq_acc, nacc);
   }
   const dim3 grid((unsigned)grid_size(a.map)), block(kNT);
+  hipEvent_t ev0, ev1;
+  const bool prof = profile_slot("bwd", &ev0, &ev1);
+  if (prof) (void)hipEventRecord(ev0, stream);
   if (dtype == 1) {
     if (D == 32) hipLaunchKernelGGL(bwd_bf16_kernel<32>, grid, block, 0, stream, a);
     else if (D == 64) hipLaunchKernelGGL(bwd_bf16_kernel<64>, grid, block, 0, stream, a);
@@ -599,6 +602,7 @@ hipError_t launch_bwd(const BwdArgs& a0, int dtype, int D, void* dq_out, hipStre
     else if (D == 64) hipLaunchKernelGGL(bwd_f32_kernel<64>, grid, block, 0, stream, a);
     else return hipErrorInvalidValue;
   }
+  if (prof) (void)hipEventRecord(ev1, stream);
   const int64_t rows = (int64_t)N * a.T;
   const unsigned fb = (unsigned)std::min<int64_t>((rows * D / 4 + 255) / 256, 8192);
   if (dtype == 1) {

@@ -408,6 +408,9 @@ hipError_t launch_fwd(const FwdArgs& a0, int dtype, int D, hipStream_t stream) {
   const int N = a.map.N;
   a.map = make_tilemap(N, (a.T + kBQ - 1) / kBQ);
   const dim3 grid((unsigned)grid_size(a.map)), block(kNT);
+  hipEvent_t ev0, ev1;
+  const bool prof = profile_slot("fwd", &ev0, &ev1);
+  if (prof) (void)hipEventRecord(ev0, stream);
   if (dtype == 1) {
     if (D == 32) hipLaunchKernelGGL(fwd_bf16_kernel<32>, grid, block, 0, stream, a);
     else if (D == 64) hipLaunchKernelGGL(fwd_bf16_kernel<64>, grid, block, 0, stream, a);
@@ -417,7 +420,9 @@ hipError_t launch_fwd(const FwdArgs& a0, int dtype, int D, hipStream_t stream) {
     else if (D == 64) hipLaunchKernelGGL(fwd_f32_kernel<64>, grid, block, 0, stream, a);
     else hipLaunchKernelGGL(fwd_f32_kernel<128>, grid, block, 0, stream, a);
   }
-  return hipGetLastError();
+  hipError_t e = hipGetLastError();
+  if (prof) (void)hipEventRecord(ev1, stream);
+  return e;
 }
 
 }  // namespace rel

@@ -66,6 +66,10 @@ struct RowArgs {
   float inv_tau;
 };
 
+// Measurement aid: if armed for kernel `name`, returns the event pair to record
+// around the next launch of that kernel (see relation_profile_arm).
+bool profile_slot(const char* name, hipEvent_t* start, hipEvent_t* stop);
+
 hipError_t launch_fwd(const FwdArgs& a, int dtype, int D, hipStream_t stream);
 hipError_t launch_bwd(const BwdArgs& a, int dtype, int D, void* dq_out, hipStream_t stream);
 int bwd_partials(int N, int T, int D, int dtype);

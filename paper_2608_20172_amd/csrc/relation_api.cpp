@@ -176,7 +176,23 @@ std::mutex g_blas_mu;
 rocblas_handle g_blas = nullptr;
 int g_blas_dev = -1;
 
+// Measurement aid state (relation_profile_arm).
+std::mutex g_prof_mu;
+std::string g_prof_name;
+std::vector<hipEvent_t> g_prof_events;
+int g_prof_next = 0;
+
 }  // namespace
+
+bool rel::profile_slot(const char* name, hipEvent_t* start, hipEvent_t* stop) {
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  if (g_prof_name.empty() || g_prof_name != name) return false;
+  if (2 * (size_t)g_prof_next + 1 >= g_prof_events.size()) return false;
+  *start = g_prof_events[2 * g_prof_next];
+  *stop = g_prof_events[2 * g_prof_next + 1];
+  ++g_prof_next;
+  return true;
+}
 
 #define REL_TRY(x)                  \
   do {                              \
@@ -200,6 +216,27 @@ const char* relation_status_string(rel_status s) {
 }
 
 const char* relation_last_error(void) { return g_last_error.c_str(); }
+
+rel_status relation_profile_arm(const char* kernel, void** events, int n_pairs) {
+  if (!kernel || (std::string(kernel) != "fwd" && std::string(kernel) != "bwd"))
+    return fail(REL_ERR_INVALID_ARG, "profile kernel must be \"fwd\" or \"bwd\"");
+  if (n_pairs < 0 || (n_pairs > 0 && !events)) return fail(REL_ERR_INVALID_ARG, "bad event array");
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  g_prof_name = kernel;
+  g_prof_events.clear();
+  for (int i = 0; i < 2 * n_pairs; ++i) g_prof_events.push_back((hipEvent_t)events[i]);
+  g_prof_next = 0;
+  return REL_OK;
+}
+
+int relation_profile_disarm(void) {
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  const int n = g_prof_next;
+  g_prof_name.clear();
+  g_prof_events.clear();
+  g_prof_next = 0;
+  return n;
+}
 
 rel_status relation_fwd(const rel_problem* p, const void* q, const void* k, const void* v,
                         const float* lambda, void* o, float* row_stat, float* self_mass,
