@@ -260,16 +260,26 @@ def main() -> int:
     kern_ms = sum(hip.elapsed_ms(kev[2 * s], kev[2 * s + 1]) for s in range(recorded)) / max(recorded, 1)
     hip.destroy(kev)
 
-    # the fused forward kernel alone (second pass, same launches)
-    fev = hip.events(2 * K)
-    keep = arm(lib, "fwd", fev)
-    for _ in range(K):
-        R.relation_fwd(q, k, v, lam_t)
-    torch.cuda.synchronize()
-    nf = lib.relation_profile_disarm()
-    del keep
-    fwd_kern_ms = sum(hip.elapsed_ms(fev[2 * s], fev[2 * s + 1]) for s in range(nf)) / max(nf, 1)
-    hip.destroy(fev)
+    # each fused kernel alone (further passes with the same launches)
+    def kernel_ms(name, call):
+        ev = hip.events(2 * K)
+        kp = arm(lib, name, ev)
+        for _ in range(K):
+            call()
+        torch.cuda.synchronize()
+        nrec = lib.relation_profile_disarm()
+        del kp
+        ms = sum(hip.elapsed_ms(ev[2 * s], ev[2 * s + 1]) for s in range(nrec)) / max(nrec, 1)
+        hip.destroy(ev)
+        return ms
+
+    fwd_kern_ms = kernel_ms("fwd", lambda: R.relation_fwd(q, k, v, lam_t))
+    per_kernel = {"fwd_kernel_ms": fwd_kern_ms}
+    if w.backward:
+        f_saved = R.relation_fwd(q, k, v, lam_t)
+        bcall = lambda: R.relation_bwd(q, k, v, f_saved["o"], do, lam_t, f_saved["row_stat"], workspace=ws)
+        per_kernel["bwd_dkdv_kernel_ms"] = kernel_ms("bwd_dkdv", bcall)
+        per_kernel["bwd_dq_kernel_ms"] = kernel_ms("bwd_dq", bcall)
 
     # materialised baseline forward
     mat = {"status": "skipped"}
@@ -323,11 +333,11 @@ def main() -> int:
         "mfma_peak_frac": (fl_f + fl_b) / (ms_step * 1e-3) / PEAK_BF16,
         "fwd_ms": fwd_ms,
         "bwd_ms": bwd_ms,
-        "fwd_kernel_ms": fwd_kern_ms,
+        **per_kernel,
         "fwd_kernel_tflops": fl_f / (fwd_kern_ms * 1e-3) / 1e12,
         "materialized": mat,
         "roofline": {
-            "kernel": "bwd_bf16_kernel" if w.backward else "fwd_bf16_kernel",
+            "kernel": "bwd_dkdv_kernel+bwd_dq_kernel" if w.backward else "fwd_kernel",
             "bound": "mfma",
             "achieved": achieved / 1e12,
             "peak": PEAK_BF16 / 1e12,

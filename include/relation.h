@@ -104,9 +104,10 @@ rel_status relation_exchange_allocation(const rel_problem* p, const void* q, con
  *   dself      out [B,H,T] fp32, optional: dL/dS_i, the gradient reaching the
  *              Self logit R_ii = S_i (-g_i (1 - g_i) c_i in App. A.1.7).
  *   workspace  at least relation_bwd_workspace_bytes(p) bytes of device memory,
- *              16-byte aligned; contents on entry are ignored.
- *   dq accumulates in fp32 with device atomics, so its low-order bits can vary
- *   from run to run; dk, dv, dlambda and dself are run-to-run identical. */
+ *              16-byte aligned, for the fixed-order dlambda reduction; contents
+ *              on entry are ignored.
+ *   Every output is written exactly once (no atomics): results are run-to-run
+ *   identical. */
 size_t relation_bwd_workspace_bytes(const rel_problem* p);
 rel_status relation_bwd(const rel_problem* p, const void* q, const void* k, const void* v,
                         const void* o, const void* dout, const float* lambda,
@@ -129,7 +130,8 @@ rel_status relation_fwd_materialized(const rel_problem* p, const void* q, const 
                                      void* workspace, size_t workspace_bytes, void* stream);
 
 /* Measurement aid. While armed, every launch of the named kernel ("fwd": the
- * fused forward kernel; "bwd": the fused backward main kernel) is bracketed by
+ * fused forward kernel; "bwd_dkdv", "bwd_dq": the two backward kernels; "bwd":
+ * both backward kernels, back to back) is bracketed by
  * hipEventRecord on its launch stream, using the caller's events in pairs
  * (events[2i] before launch i, events[2i+1] after it) until n_pairs launches
  * have been recorded. The events are owned by the caller (hipEvent_t, created

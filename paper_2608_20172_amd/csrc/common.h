@@ -91,6 +91,174 @@ template <> struct Elem<bf16> {
 };
 
 // ---------------------------------------------------------------------------
+// Operand policies. A kernel is written once against a policy that says how
+// one 16-wide slice of an MFMA contraction is fetched and multiplied.
+// For lane group g (= lane / 32) and element t in 0..7, both policies address
+// the same contraction index whenever the operand comes from a tile row
+// ("col" operands and register operands): index 16 ks + 8 (t / 4) + 4 g + t % 4,
+// which is also the row of accumulator register 8 h + t (h = ks % 2) of a
+// 32x32 block. So a 32x32 result block, re-packed from its registers, is
+// directly the operand of the next product along its rows.
+//   bf16: one 32x32x16 MFMA per slice; tiles are row-major in LDS with
+//         16-byte chunks XOR-swizzled by row; "col" operands by transpose reads.
+//   f32:  eight 32x32x2 MFMAs per slice; rows padded by one element.
+// ---------------------------------------------------------------------------
+typedef float floatx8 __attribute__((ext_vector_type(8)));
+
+struct Lane {
+  int n, g;            // lane % 32, lane / 32
+  int t_row, t_col;    // transpose-read source row / column offsets (bf16)
+  __device__ explicit Lane(int lane) {
+    n = lane & 31;
+    g = lane >> 5;
+    const int G = lane >> 4, i = lane & 15;
+    t_row = 4 * (G >> 1) + (i >> 2);
+    t_col = 16 * (G & 1) + 4 * (i & 3);
+  }
+};
+
+template <int D>
+struct PolBF16 {
+  using T = bf16;
+  using Op = bf16x8;
+  using Chunk = uintx4;                        // 16 bytes = 8 elements
+  static constexpr int CE = 8;                 // elements per chunk
+  static constexpr int NCH = D / 8;            // chunks per row
+  static constexpr int ROWB = 2 * D;           // bytes per LDS row
+  static constexpr int SWZ = (NCH < 8 ? NCH : 8) - 1;
+  static constexpr int tile_bytes(int rows) { return rows * ROWB; }
+  static __device__ __forceinline__ int off(int row, int col) {
+    return row * ROWB + (((col >> 3) ^ (row & SWZ)) << 4) + ((col & 7) << 1);
+  }
+  static __device__ __forceinline__ void stage(unsigned char* lds, int row, int ch, const Chunk& v) {
+    *(Chunk*)(lds + row * ROWB + ((ch ^ (row & SWZ)) << 4)) = v;
+  }
+  // contraction over the row's elements: element t = row[16 ks + 8 g + t]
+  static __device__ __forceinline__ Op row_op(const unsigned char* lds, int row, int ks, const Lane& L) {
+    return *(const Op*)(lds + row * ROWB + (((2 * ks + L.g) ^ (row & SWZ)) << 4));
+  }
+  static __device__ __forceinline__ Op row_op_g(const T* rowp, int ks, const Lane& L) {
+    return *(const Op*)(rowp + 16 * ks + 8 * L.g);
+  }
+  // contraction over tile rows: element t = M[16 ks + 8 (t/4) + 4 g + t%4][col0 + n]
+  static __device__ __forceinline__ Op col_op(const unsigned char* lds, int ks, int col0, const Lane& L) {
+    const int r0 = 16 * ks + L.t_row, c = col0 + L.t_col;
+    return tr_operand(lds + off(r0, c), lds + off(r0 + 8, c));
+  }
+  static __device__ __forceinline__ Op pack(const float* x) {
+    Op o;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) o[t] = (bf16)x[t];
+    return o;
+  }
+  static __device__ __forceinline__ floatx16 mma(const Op& a, const Op& b, const floatx16& c) {
+    return mfma32(a, b, c);
+  }
+  // dot product of two chunks (8 products)
+  static __device__ __forceinline__ float chunk_dot(const Chunk& a, const Chunk& b) {
+    float s = 0.0f;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      s = __builtin_fmaf(bf16_lo(a[t]), bf16_lo(b[t]), s);
+      s = __builtin_fmaf(bf16_hi(a[t]), bf16_hi(b[t]), s);
+    }
+    return s;
+  }
+  // dot product of two operands (8 products)
+  static __device__ __forceinline__ float op_dot(const Op& a, const Op& b) {
+    return chunk_dot(__builtin_bit_cast(uintx4, a), __builtin_bit_cast(uintx4, b));
+  }
+  // 4 consecutive elements
+  static __device__ __forceinline__ floatx4 load4(const T* p) {
+    const uintx2 u = *(const uintx2*)p;
+    return floatx4{bf16_lo(u[0]), bf16_hi(u[0]), bf16_lo(u[1]), bf16_hi(u[1])};
+  }
+  static __device__ __forceinline__ void store4(T* p, const floatx4& x) {
+    bf16x4 v;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = (bf16)x[e];
+    *(bf16x4*)p = v;
+  }
+};
+
+template <int D>
+struct PolF32 {
+  using T = float;
+  using Op = floatx8;
+  using Chunk = floatx4;                       // 16 bytes = 4 elements
+  static constexpr int CE = 4;
+  static constexpr int NCH = D / 4;
+  static constexpr int ROWF = D + 1;           // padded row, floats
+  static constexpr int tile_bytes(int rows) { return rows * ROWF * 4; }
+  static __device__ __forceinline__ const float* fp(const unsigned char* lds) { return (const float*)lds; }
+  static __device__ __forceinline__ void stage(unsigned char* lds, int row, int ch, const Chunk& v) {
+    float* f = (float*)lds + row * ROWF + 4 * ch;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) f[e] = v[e];
+  }
+  // element t = row[16 ks + 2 t + g]  (MFMA step t covers 16 ks + 2 t .. +1)
+  static __device__ __forceinline__ Op row_op(const unsigned char* lds, int row, int ks, const Lane& L) {
+    const float* f = fp(lds) + row * ROWF + 16 * ks + L.g;
+    Op o;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) o[t] = f[2 * t];
+    return o;
+  }
+  static __device__ __forceinline__ Op row_op_g(const T* rowp, int ks, const Lane& L) {
+    Op o;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) o[t] = rowp[16 * ks + 2 * t + L.g];
+    return o;
+  }
+  static __device__ __forceinline__ Op col_op(const unsigned char* lds, int ks, int col0, const Lane& L) {
+    const float* f = fp(lds) + col0 + L.n;
+    Op o;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) o[t] = f[(16 * ks + 8 * (t >> 2) + 4 * L.g + (t & 3)) * ROWF];
+    return o;
+  }
+  static __device__ __forceinline__ Op pack(const float* x) {
+    Op o;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) o[t] = x[t];
+    return o;
+  }
+  static __device__ __forceinline__ floatx16 mma(const Op& a, const Op& b, floatx16 c) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) c = mfma32f(a[t], b[t], c);
+    return c;
+  }
+  static __device__ __forceinline__ float chunk_dot(const Chunk& a, const Chunk& b) {
+    return __builtin_fmaf(a[0], b[0], __builtin_fmaf(a[1], b[1], __builtin_fmaf(a[2], b[2], a[3] * b[3])));
+  }
+  static __device__ __forceinline__ float op_dot(const Op& a, const Op& b) {
+    float s = 0.0f;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) s = __builtin_fmaf(a[t], b[t], s);
+    return s;
+  }
+  static __device__ __forceinline__ floatx4 load4(const T* p) { return *(const floatx4*)p; }
+  static __device__ __forceinline__ void store4(T* p, const floatx4& x) { *(floatx4*)p = x; }
+};
+
+// Register r* of a 32x32 block that holds row n for lane group g, if any:
+// acc_row(r, g) == n  <=>  g == (n >> 2) & 1  and  r == 4 (n >> 3) + (n & 3).
+__device__ __forceinline__ bool holds_row(int n, int g) { return ((n >> 2) & 1) == g; }
+__device__ __forceinline__ int row_reg(int n) { return 4 * (n >> 3) + (n & 3); }
+__device__ __forceinline__ float pick(const floatx16& x, int r) {
+  float v = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) v = (i == r) ? x[i] : v;
+  return v;
+}
+__device__ __forceinline__ float pick(const float* x, int r) {
+  float v = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) v = (i == r) ? x[i] : v;
+  return v;
+}
+
+// ---------------------------------------------------------------------------
 // Wave-level helpers
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32, 64); }

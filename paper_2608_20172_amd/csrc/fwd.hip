@@ -7,7 +7,8 @@
 // online scan stay inside the lane, plus one exchange with the partner lane
 // 32 away. The Exchange scan keeps (m, l, z) per row exactly as in eqs. (11)-(12)
 // of Sec. 5.1 / App. A.3, with Self excluded; Self and the count correction
-// join only in the epilogue (eq. 13).
+// join only in the epilogue (eq. 13). The Self logit U_ii is read off the
+// diagonal entry of the evidence tile that holds row i.
 //
 // Running reference m. SiLU(U) >= -0.2785, so exp(E - m) with m = 0 can never
 // underflow to an all-zero row; the reference is raised only when a tile's
@@ -26,21 +27,15 @@ constexpr int kNT = 256;  // threads per workgroup
 constexpr float kRescale = 8.0f;
 
 // Exchange logits of one 32x32 block, in place: s[r] (raw q.k) becomes
-// E*log2(e) - m, or -inf where j >= i. Tracks the diagonal entry (Self).
-__device__ __forceinline__ void exchange_logits(floatx16& s, bool diag_block, int n, int g, float c,
-                                                float m, float& mx, float& uii, bool& hasd) {
+// E log2(e) - m; in the diagonal block (DIAG) entries with key >= query get -inf.
+template <bool DIAG>
+__device__ __forceinline__ void exchange_logits(floatx16& s, const Lane& L, float c, float m, float& mx) {
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
-    const int kr = acc_row(r, g);
-    const float x = s[r];
-    if (diag_block && kr == n) {
-      uii = x;
-      hasd = true;
-    }
-    const float up = x * c;                                // U * log2(e)
+    const float up = s[r] * c;                             // U log2(e)
     const float sg = fast_rcp(1.0f + fast_exp2(-up));      // sigmoid(U)
-    float e = __builtin_fmaf(up, sg, -m);                  // SiLU(U) * log2(e) - m
-    if (diag_block && kr >= n) e = kNegInf;                // strictly historical: j < i
+    float e = __builtin_fmaf(up, sg, -m);                  // SiLU(U) log2(e) - m
+    if (DIAG && acc_row(r, L.g) >= L.n) e = kNegInf;       // strictly historical: j < i
     s[r] = e;
     mx = fmaxf(mx, e);
   }
@@ -50,7 +45,7 @@ struct RowEpilogue {
   float g, omg, inv_l, LE, lnZ, S;
 };
 
-// Completes row i (one-based index i1) from the terminal scan state (eqs. 12-13):
+// Completes row i from the terminal scan state (eqs. 12-13):
 // L^E = m + ln l, A = L^E - lambda ln i, g = sigmoid(A - S), 1-g = sigmoid(S - A).
 __device__ __forceinline__ RowEpilogue row_epilogue(float m_log2, float l, float uii, float scale,
                                                     float inv_tau, float lam, float ln_i) {
@@ -74,89 +69,70 @@ __device__ __forceinline__ RowEpilogue row_epilogue(float m_log2, float l, float
   return e;
 }
 
-__device__ __forceinline__ void store_row_stats(const FwdArgs& a, int64_t ridx, const RowEpilogue& e,
-                                                float lam, float ln_i) {
-  if (a.row_stat) a.row_stat[ridx] = e.lnZ + lam * ln_i;
-  if (a.self_mass) a.self_mass[ridx] = e.omg;
-  if (a.exch_mass) a.exch_mass[ridx] = e.g;
-  if (a.exch_lse) a.exch_lse[ridx] = e.LE;
-}
-
-// ---------------------------------------------------------------------------
-// bf16 kernel
-// ---------------------------------------------------------------------------
-template <int D>
-__global__ __launch_bounds__(kNT, 2) void fwd_bf16_kernel(FwdArgs a) {
-  constexpr int KS = D / 16;                      // MFMA k-steps over d
+template <class P, int D>
+__global__ __launch_bounds__(kNT, 2) void fwd_kernel(FwdArgs a) {
+  using E = typename P::T;
+  using Op = typename P::Op;
+  using Chunk = typename P::Chunk;
+  constexpr int KS = D / 16;                      // 16-wide slices of d
   constexpr int DB = D / 32;                      // 32-row blocks of O^T
-  constexpr int NCH = D / 8;                      // 16-byte chunks per tile row
   constexpr int SB = kBK / 32;                    // 32-key blocks per tile
-  constexpr int ROWB = D * 2;                     // bytes per tile row
-  constexpr int SWZ = (NCH < 8 ? NCH : 8) - 1;    // chunk swizzle mask
-  constexpr int NLD = kBK * NCH / kNT;            // chunks per thread per tensor
+  constexpr int NLD = kBK * P::NCH / kNT;         // chunks per thread per tensor
   static_assert(NLD >= 1, "tile too small for the workgroup");
-  __shared__ __attribute__((aligned(16))) unsigned char lds[2 * kBK * ROWB];
+  constexpr int TB = P::tile_bytes(kBK);
+  __shared__ __attribute__((aligned(16))) unsigned char lds[2 * TB];
   unsigned char* Ks = lds;
-  unsigned char* Vs = lds + kBK * ROWB;
+  unsigned char* Vs = lds + TB;
 
   int head, qt;
   if (!map_tile(a.map, blockIdx.x, head, qt, true)) return;
   const int T = a.T;
   const int64_t st = a.st;
   const int64_t hoff = (int64_t)(head / a.H) * a.sb + (int64_t)(head % a.H) * a.sh;
-  const bf16* q = (const bf16*)a.q + hoff;
-  const bf16* k = (const bf16*)a.k + hoff;
-  const bf16* v = (const bf16*)a.v + hoff;
-  bf16* o = (bf16*)a.o + hoff;
+  const E* q = (const E*)a.q + hoff;
+  const E* k = (const E*)a.k + hoff;
+  const E* v = (const E*)a.v + hoff;
+  E* o = (E*)a.o + hoff;
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int n = lane & 31, g = lane >> 5;
+  const int tid = threadIdx.x, w = tid >> 6;
+  const Lane L(tid & 63);
+  const int n = L.n, g = L.g;
   const int i0 = qt * kBQ, qr0 = i0 + 32 * w, qi = qr0 + n;
   const bool wave_live = qr0 < T;
   const float c = a.scale * kLog2e;
 
-  // B operand of U^T = K Q^T: lane (n, g) holds Q[qi][16 ks + 8 g .. +7]
-  bf16x8 qop[KS];
+  // B operand of U^T = K Q^T: this lane's query row
+  Op qop[KS];
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    if (qi < T) qop[ks] = *(const bf16x8*)(q + qi * st + 16 * ks + 8 * g);
-    else qop[ks] = bf16x8{};
-  }
+  for (int ks = 0; ks < KS; ++ks) qop[ks] = qi < T ? P::row_op_g(q + qi * st, ks, L) : Op{};
 
-  uintx4 kreg[NLD], vreg[NLD];
+  Chunk kreg[NLD], vreg[NLD];
   auto prefetch = [&](int j0) {
 #pragma unroll
     for (int j = 0; j < NLD; ++j) {
-      const int ci = tid + kNT * j, row = ci / NCH, ch = ci % NCH, key = j0 + row;
+      const int ci = tid + kNT * j, row = ci / P::NCH, ch = ci % P::NCH, key = j0 + row;
       if (key < T) {
-        kreg[j] = *(const uintx4*)(k + key * st + 8 * ch);
-        vreg[j] = *(const uintx4*)(v + key * st + 8 * ch);
+        kreg[j] = *(const Chunk*)(k + key * st + P::CE * ch);
+        vreg[j] = *(const Chunk*)(v + key * st + P::CE * ch);
       } else {
-        kreg[j] = uintx4{};
-        vreg[j] = uintx4{};
+        kreg[j] = Chunk{};
+        vreg[j] = Chunk{};
       }
     }
   };
   auto stage = [&]() {
 #pragma unroll
     for (int j = 0; j < NLD; ++j) {
-      const int ci = tid + kNT * j, row = ci / NCH, ch = ci % NCH;
-      const int off = row * ROWB + ((ch ^ (row & SWZ)) << 4);
-      *(uintx4*)(Ks + off) = kreg[j];
-      *(uintx4*)(Vs + off) = vreg[j];
+      const int ci = tid + kNT * j, row = ci / P::NCH, ch = ci % P::NCH;
+      P::stage(Ks, row, ch, kreg[j]);
+      P::stage(Vs, row, ch, vreg[j]);
     }
   };
 
   float m = 0.0f, l = 0.0f, uii = 0.0f;
-  bool hasd = false;
   floatx16 oacc[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) oacc[db] = floatx16{};
-
-  // lane constants of the transpose read of V: 16-lane group G, index i in group
-  const int tG = lane >> 4, ti = lane & 15;
-  const int t_row = 4 * (tG >> 1) + (ti >> 2);               // + 16 ks + 8 h
-  const int t_col = 16 * (tG & 1) + 4 * (ti & 3);            // + 32 db (elements)
 
   const int kmax = min(i0 + kBQ, T) - 1;  // the diagonal of the last row is included
   const int nkt = kmax / kBK + 1;
@@ -170,26 +146,22 @@ __global__ __launch_bounds__(kNT, 2) void fwd_bf16_kernel(FwdArgs a) {
     const int j0 = kt * kBK;
 
     floatx16 sacc[SB];
-    bool act[SB];
-#pragma unroll
-    for (int sb = 0; sb < SB; ++sb) {
-      act[sb] = (j0 + 32 * sb) <= qr0;  // some key of the block is <= some row of the wave
-      sacc[sb] = floatx16{};
-      if (act[sb]) {
-        const int row = 32 * sb + n;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8 kop =
-              *(const bf16x8*)(Ks + row * ROWB + (((2 * ks + g) ^ (row & SWZ)) << 4));
-          sacc[sb] = mfma32(kop, qop[ks], sacc[sb]);
-        }
-      }
-    }
-
     float mx = kNegInf;
 #pragma unroll
-    for (int sb = 0; sb < SB; ++sb)
-      if (act[sb]) exchange_logits(sacc[sb], j0 + 32 * sb == qr0, n, g, c, m, mx, uii, hasd);
+    for (int sb = 0; sb < SB; ++sb) {
+      const int kb0 = j0 + 32 * sb;
+      if (kb0 > qr0) continue;  // no key of the block precedes or meets a row of the wave
+      const int row = 32 * sb + n;
+      sacc[sb] = P::mma(P::row_op(Ks, row, 0, L), qop[0], floatx16{});
+#pragma unroll
+      for (int ks = 1; ks < KS; ++ks) sacc[sb] = P::mma(P::row_op(Ks, row, ks, L), qop[ks], sacc[sb]);
+      if (kb0 == qr0) {
+        if (holds_row(n, g)) uii = pick(sacc[sb], row_reg(n));  // the Self evidence U_ii
+        exchange_logits<true>(sacc[sb], L, c, m, mx);
+      } else {
+        exchange_logits<false>(sacc[sb], L, c, m, mx);
+      }
+    }
     mx = fmaxf(mx, xor32(mx));
     if (wave_any(mx > kRescale)) {
       const float d = fmaxf(mx, 0.0f);
@@ -208,26 +180,19 @@ __global__ __launch_bounds__(kNT, 2) void fwd_bf16_kernel(FwdArgs a) {
 
 #pragma unroll
     for (int sb = 0; sb < SB; ++sb) {
-      if (!act[sb]) continue;
+      if (j0 + 32 * sb > qr0) continue;
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
-        bf16x8 pop;
+        float p[8];
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
-          const float p = fast_exp2(sacc[sb][8 * hh + t]);
-          l += p;
-          pop[t] = f2bf(p);
+          p[t] = fast_exp2(sacc[sb][8 * hh + t]);
+          l += p[t];
         }
-        const int ks = 2 * sb + hh;
+        const Op pop = P::pack(p);
 #pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const int col = 32 * db + t_col;
-          const int row0 = 16 * ks + t_row, row1 = row0 + 8;
-          const bf16x8 vop = tr_operand(
-              Vs + row0 * ROWB + (((col >> 3) ^ (row0 & SWZ)) << 4) + ((col & 7) << 1),
-              Vs + row1 * ROWB + (((col >> 3) ^ (row1 & SWZ)) << 4) + ((col & 7) << 1));
-          oacc[db] = mfma32(vop, pop, oacc[db]);
-        }
+        for (int db = 0; db < DB; ++db)
+          oacc[db] = P::mma(P::col_op(Vs, 2 * sb + hh, 32 * db, L), pop, oacc[db]);
       }
     }
   }
@@ -235,8 +200,8 @@ __global__ __launch_bounds__(kNT, 2) void fwd_bf16_kernel(FwdArgs a) {
 
   // ---- epilogue: combine the two lane halves of each row, then eq. (13)
   const float lt = l + xor32(l);
-  const float u_other = xor32(hasd ? uii : 0.0f);
-  const float un = hasd ? uii : u_other;
+  const float u_other = xor32(uii);
+  const float un = holds_row(n, g) ? uii : u_other;
   if (qi >= T) return;
   const float lam = *a.lambda;
   const float ln_i = logf((float)(qi + 1));
@@ -246,179 +211,43 @@ __global__ __launch_bounds__(kNT, 2) void fwd_bf16_kernel(FwdArgs a) {
 #pragma unroll
     for (int rq = 0; rq < 4; ++rq) {
       const int d0 = 32 * db + 8 * rq + 4 * g;
-      const bf16x4 vi = *(const bf16x4*)(v + qi * st + d0);
-      bf16x4 out;
+      const floatx4 vi = P::load4(v + qi * st + d0);
+      floatx4 out;
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
-        out[t] = f2bf(__builtin_fmaf(e.omg, bf2f(vi[t]), e.inv_l * oacc[db][4 * rq + t]));
-      *(bf16x4*)(o + qi * st + d0) = out;
+      for (int t = 0; t < 4; ++t) out[t] = __builtin_fmaf(e.omg, vi[t], e.inv_l * oacc[db][4 * rq + t]);
+      P::store4(o + qi * st + d0, out);
     }
   }
-  if (g == 0) store_row_stats(a, (int64_t)head * T + qi, e, lam, ln_i);
+  if (g == 0) {
+    const int64_t ridx = (int64_t)head * T + qi;
+    if (a.row_stat) a.row_stat[ridx] = e.lnZ + lam * ln_i;
+    if (a.self_mass) a.self_mass[ridx] = e.omg;
+    if (a.exch_mass) a.exch_mass[ridx] = e.g;
+    if (a.exch_lse) a.exch_lse[ridx] = e.LE;
+  }
 }
 
-// ---------------------------------------------------------------------------
-// fp32 kernel (parity path): same scan, 32x32x2 f32 MFMAs, padded LDS rows.
-// ---------------------------------------------------------------------------
-template <int D>
-__global__ __launch_bounds__(kNT, 1) void fwd_f32_kernel(FwdArgs a) {
-  constexpr int DB = D / 32;
-  constexpr int KS = D / 2;
-  constexpr int NCH = D / 4;          // 16-byte chunks per row
-  constexpr int SB = kBK / 32;
-  constexpr int LDR = D + 1;          // padded LDS row (floats)
-  constexpr int NLD = kBK * NCH / kNT;
-  static_assert(NLD >= 1, "tile too small for the workgroup");
-  __shared__ float Ks[kBK * LDR];
-  __shared__ float Vs[kBK * LDR];
-
-  int head, qt;
-  if (!map_tile(a.map, blockIdx.x, head, qt, true)) return;
-  const int T = a.T;
-  const int64_t st = a.st;
-  const int64_t hoff = (int64_t)(head / a.H) * a.sb + (int64_t)(head % a.H) * a.sh;
-  const float* q = (const float*)a.q + hoff;
-  const float* k = (const float*)a.k + hoff;
-  const float* v = (const float*)a.v + hoff;
-  float* o = (float*)a.o + hoff;
-
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int n = lane & 31, g = lane >> 5;
-  const int i0 = qt * kBQ, qr0 = i0 + 32 * w, qi = qr0 + n;
-  const bool wave_live = qr0 < T;
-  const float c = a.scale * kLog2e;
-
-  float qop[KS];
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) qop[ks] = (qi < T) ? q[qi * st + 2 * ks + g] : 0.0f;
-
-  floatx4 kreg[NLD], vreg[NLD];
-  auto prefetch = [&](int j0) {
-#pragma unroll
-    for (int j = 0; j < NLD; ++j) {
-      const int ci = tid + kNT * j, row = ci / NCH, ch = ci % NCH, key = j0 + row;
-      if (key < T) {
-        kreg[j] = *(const floatx4*)(k + key * st + 4 * ch);
-        vreg[j] = *(const floatx4*)(v + key * st + 4 * ch);
-      } else {
-        kreg[j] = floatx4{};
-        vreg[j] = floatx4{};
-      }
-    }
-  };
-  auto stage = [&]() {
-#pragma unroll
-    for (int j = 0; j < NLD; ++j) {
-      const int ci = tid + kNT * j, row = ci / NCH, ch = ci % NCH;
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        Ks[row * LDR + 4 * ch + t] = kreg[j][t];
-        Vs[row * LDR + 4 * ch + t] = vreg[j][t];
-      }
-    }
-  };
-
-  float m = 0.0f, l = 0.0f, uii = 0.0f;
-  bool hasd = false;
-  floatx16 oacc[DB];
-#pragma unroll
-  for (int db = 0; db < DB; ++db) oacc[db] = floatx16{};
-
-  const int kmax = min(i0 + kBQ, T) - 1;
-  const int nkt = kmax / kBK + 1;
-  prefetch(0);
-  for (int kt = 0; kt < nkt; ++kt) {
-    __syncthreads();
-    stage();
-    __syncthreads();
-    if (kt + 1 < nkt) prefetch((kt + 1) * kBK);
-    if (!wave_live) continue;
-    const int j0 = kt * kBK;
-
-    floatx16 sacc[SB];
-    bool act[SB];
-#pragma unroll
-    for (int sb = 0; sb < SB; ++sb) {
-      act[sb] = (j0 + 32 * sb) <= qr0;
-      sacc[sb] = floatx16{};
-      if (act[sb]) {
-        const int row = 32 * sb + n;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) sacc[sb] = mfma32f(Ks[row * LDR + 2 * ks + g], qop[ks], sacc[sb]);
-      }
-    }
-
-    float mx = kNegInf;
-#pragma unroll
-    for (int sb = 0; sb < SB; ++sb)
-      if (act[sb]) exchange_logits(sacc[sb], j0 + 32 * sb == qr0, n, g, c, m, mx, uii, hasd);
-    mx = fmaxf(mx, xor32(mx));
-    if (wave_any(mx > kRescale)) {
-      const float d = fmaxf(mx, 0.0f);
-      m += d;
-      const float al = fast_exp2(-d);
-      l *= al;
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[db][r] *= al;
-#pragma unroll
-      for (int sb = 0; sb < SB; ++sb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[sb][r] -= d;
-    }
-
-#pragma unroll
-    for (int sb = 0; sb < SB; ++sb) {
-      if (!act[sb]) continue;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = fast_exp2(sacc[sb][r]);
-        l += p;
-        const int key = 32 * sb + acc_row(r, g);  // row of the LDS tile
-#pragma unroll
-        for (int db = 0; db < DB; ++db) oacc[db] = mfma32f(Vs[key * LDR + 32 * db + n], p, oacc[db]);
-      }
-    }
-  }
-  if (!wave_live) return;
-
-  const float lt = l + xor32(l);
-  const float u_other = xor32(hasd ? uii : 0.0f);
-  const float un = hasd ? uii : u_other;
-  if (qi >= T) return;
-  const float lam = *a.lambda;
-  const float ln_i = logf((float)(qi + 1));
-  const RowEpilogue e = row_epilogue(m, lt, un, a.scale, a.inv_tau, lam, ln_i);
-#pragma unroll
-  for (int db = 0; db < DB; ++db) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int d = 32 * db + acc_row(r, g);
-      o[qi * st + d] = __builtin_fmaf(e.omg, v[qi * st + d], e.inv_l * oacc[db][r]);
-    }
-  }
-  if (g == 0) store_row_stats(a, (int64_t)head * T + qi, e, lam, ln_i);
+template <class P, int D>
+void launch_one(const FwdArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL((fwd_kernel<P, D>), dim3((unsigned)grid_size(a.map)), dim3(kNT), 0, stream, a);
 }
 
 }  // namespace
 
 hipError_t launch_fwd(const FwdArgs& a0, int dtype, int D, hipStream_t stream) {
   FwdArgs a = a0;
-  const int N = a.map.N;
-  a.map = make_tilemap(N, (a.T + kBQ - 1) / kBQ);
-  const dim3 grid((unsigned)grid_size(a.map)), block(kNT);
+  a.map = make_tilemap(a.map.N, (a.T + kBQ - 1) / kBQ);
   hipEvent_t ev0, ev1;
   const bool prof = profile_slot("fwd", &ev0, &ev1);
   if (prof) (void)hipEventRecord(ev0, stream);
   if (dtype == 1) {
-    if (D == 32) hipLaunchKernelGGL(fwd_bf16_kernel<32>, grid, block, 0, stream, a);
-    else if (D == 64) hipLaunchKernelGGL(fwd_bf16_kernel<64>, grid, block, 0, stream, a);
-    else hipLaunchKernelGGL(fwd_bf16_kernel<128>, grid, block, 0, stream, a);
+    if (D == 32) launch_one<PolBF16<32>, 32>(a, stream);
+    else if (D == 64) launch_one<PolBF16<64>, 64>(a, stream);
+    else launch_one<PolBF16<128>, 128>(a, stream);
   } else {
-    if (D == 32) hipLaunchKernelGGL(fwd_f32_kernel<32>, grid, block, 0, stream, a);
-    else if (D == 64) hipLaunchKernelGGL(fwd_f32_kernel<64>, grid, block, 0, stream, a);
-    else hipLaunchKernelGGL(fwd_f32_kernel<128>, grid, block, 0, stream, a);
+    if (D == 32) launch_one<PolF32<32>, 32>(a, stream);
+    else if (D == 64) launch_one<PolF32<64>, 64>(a, stream);
+    else launch_one<PolF32<128>, 128>(a, stream);
   }
   hipError_t e = hipGetLastError();
   if (prof) (void)hipEventRecord(ev1, stream);

@@ -35,10 +35,10 @@ struct BwdArgs {
   const void* dout;
   const float* lambda;
   const float* row_stat;
+  void* dq;
   void* dk;
   void* dv;
-  float* dq_acc;     // fp32 [N, T, D] dense, zeroed before the main kernel
-  float* dlam_part;  // one partial per main-kernel workgroup slot
+  float* dlam_part;  // one partial per dQ-kernel workgroup slot
   float* dself;      // optional [N, T]
   int64_t sb, sh, st;
   int H, T;
@@ -71,7 +71,7 @@ struct RowArgs {
 bool profile_slot(const char* name, hipEvent_t* start, hipEvent_t* stop);
 
 hipError_t launch_fwd(const FwdArgs& a, int dtype, int D, hipStream_t stream);
-hipError_t launch_bwd(const BwdArgs& a, int dtype, int D, void* dq_out, hipStream_t stream);
+hipError_t launch_bwd(const BwdArgs& a, int dtype, int D, hipStream_t stream);
 int bwd_partials(int N, int T, int D, int dtype);
 hipError_t launch_dlambda(const float* part, int np, float* out, hipStream_t stream);
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t stream);

@@ -218,8 +218,10 @@ const char* relation_status_string(rel_status s) {
 const char* relation_last_error(void) { return g_last_error.c_str(); }
 
 rel_status relation_profile_arm(const char* kernel, void** events, int n_pairs) {
-  if (!kernel || (std::string(kernel) != "fwd" && std::string(kernel) != "bwd"))
-    return fail(REL_ERR_INVALID_ARG, "profile kernel must be \"fwd\" or \"bwd\"");
+  static const char* kNames[] = {"fwd", "bwd", "bwd_dkdv", "bwd_dq"};
+  bool known = false;
+  for (const char* nm : kNames) known = known || (kernel && std::string(kernel) == nm);
+  if (!known) return fail(REL_ERR_INVALID_ARG, "unknown kernel name for profiling");
   if (n_pairs < 0 || (n_pairs > 0 && !events)) return fail(REL_ERR_INVALID_ARG, "bad event array");
   std::lock_guard<std::mutex> lock(g_prof_mu);
   g_prof_name = kernel;
@@ -313,8 +315,7 @@ size_t relation_bwd_workspace_bytes(const rel_problem* p) {
   if (check_problem(p, &empty) != REL_OK) return 0;
   if (empty) return 0;
   const size_t N = (size_t)(p->B * p->H);
-  return align256(N * (size_t)p->T * (size_t)p->D * 4) +
-         align256((size_t)rel::bwd_partials((int)N, (int)p->T, (int)p->D, p->dtype) * 4);
+  return align256((size_t)rel::bwd_partials((int)N, (int)p->T, (int)p->D, p->dtype) * 4);
 }
 
 rel_status relation_bwd(const rel_problem* p, const void* q, const void* k, const void* v,
@@ -332,8 +333,6 @@ rel_status relation_bwd(const rel_problem* p, const void* q, const void* k, cons
     }
     return REL_OK;
   }
-  if (p->dtype == REL_F32 && p->D > 64)
-    return fail(REL_ERR_UNSUPPORTED, "fp32 backward supports D <= 64 (got %lld)", (long long)p->D);
   REL_TRY(check_aligned(q, 16, "q", true));
   REL_TRY(check_aligned(k, 16, "k", true));
   REL_TRY(check_aligned(v, 16, "v", true));
@@ -370,15 +369,14 @@ rel_status relation_bwd(const rel_problem* p, const void* q, const void* k, cons
   const size_t N = (size_t)(p->B * p->H);
   rel::BwdArgs a{};
   a.q = q; a.k = k; a.v = v; a.o = o; a.dout = dout; a.lambda = lambda; a.row_stat = row_stat;
-  a.dk = dk; a.dv = dv; a.dself = dself;
-  a.dq_acc = (float*)workspace;
-  a.dlam_part = (float*)((char*)workspace + align256(N * (size_t)p->T * (size_t)p->D * 4));
+  a.dq = dq; a.dk = dk; a.dv = dv; a.dself = dself;
+  a.dlam_part = (float*)workspace;
   a.sb = p->stride_b; a.sh = p->stride_h; a.st = p->stride_t;
   a.H = (int)p->H; a.T = (int)p->T;
   a.scale = eff_scale(p);
   a.inv_tau = 1.0f / p->tau_s;
   a.map = rel::make_tilemap((int)N, 1);
-  hipError_t e = rel::launch_bwd(a, p->dtype, (int)p->D, dq, (hipStream_t)stream);
+  hipError_t e = rel::launch_bwd(a, p->dtype, (int)p->D, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "relation_bwd launch");
   e = rel::launch_dlambda(a.dlam_part, rel::bwd_partials((int)N, (int)p->T, (int)p->D, p->dtype),
                           dlambda, (hipStream_t)stream);

@@ -118,16 +118,16 @@ def test_output_aliasing(lib):
 def test_bwd_workspace_and_dtype_limits(lib):
     p = prob(T=300)
     need = lib.relation_bwd_workspace_bytes(ctypes.byref(p))
-    assert need >= 1 * 2 * 300 * 64 * 4
+    assert 0 < need < 1 << 20  # per-workgroup dlambda partials only
     a = ptrs(16)
     args = [ctypes.byref(p), a[0], a[1], a[2], a[3], a[4], a[5], a[6], a[7], a[8], a[9], a[10], None]
     assert lib.relation_bwd(*args, a[11], need - 1, None) == R.REL_ERR_WORKSPACE
     assert lib.relation_bwd(*args, None, need, None) == R.REL_ERR_WORKSPACE
     assert lib.relation_bwd(*args, a[11], need, None) == R.REL_ERR_HIP
-    p32 = prob(T=300, D=128, dtype=R.REL_F32)
+    p32 = prob(T=300, D=128, dtype=R.REL_F32, st=128)
     n32 = lib.relation_bwd_workspace_bytes(ctypes.byref(p32))
     args32 = [ctypes.byref(p32)] + args[1:]
-    assert lib.relation_bwd(*args32, a[11], n32, None) == R.REL_ERR_UNSUPPORTED
+    assert lib.relation_bwd(*args32, a[11], n32, None) == R.REL_ERR_HIP  # supported, reaches launch
     assert lib.relation_bwd_workspace_bytes(None) == 0
 
 

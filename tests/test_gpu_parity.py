@@ -166,7 +166,7 @@ def test_backward_bf16_ragged(D):
     check_backward(x, "bf16", f)
 
 
-@pytest.mark.parametrize("D", [32, 64])
+@pytest.mark.parametrize("D", [32, 64, 128])
 def test_backward_fp32(D):
     x = _prep(I.make_inputs(1, 2, 190, D, seed=12, qkv_std=1.0, lam=0.4), "f32")
     f = check_forward(x, "f32", with_aux=False)
@@ -204,9 +204,8 @@ def test_strided_layout_matches_contiguous():
     torch.cuda.synchronize()
     assert torch.equal(f1["o"], f2["o"].contiguous())
     assert torch.equal(f1["row_stat"], f2["row_stat"])
-    for n in ("dk", "dv"):
+    for n in ("dq", "dk", "dv"):
         assert torch.equal(g1[n], g2[n].contiguous()), n
-    assert (g1["dq"].float() - g2["dq"].float()).abs().max().item() < 1e-2
 
 
 def test_autograd_wrapper():
@@ -221,19 +220,19 @@ def test_autograd_wrapper():
     g = R.relation_bwd(x["q"], x["k"], x["v"], f["o"], x["do"], x["lam"], f["row_stat"])
     torch.cuda.synchronize()
     assert torch.equal(y.detach(), f["o"])
-    assert torch.equal(k.grad, g["dk"]) and torch.equal(v.grad, g["dv"])
+    assert torch.equal(q.grad, g["dq"]) and torch.equal(k.grad, g["dk"]) and torch.equal(v.grad, g["dv"])
     assert abs(lam.grad.item() - g["dlambda"].item()) <= 1e-6 * max(1.0, abs(g["dlambda"].item()))
 
 
 def test_backward_repeatability():
-    """dk, dv, dlambda and dself are reduced in a fixed order: bitwise repeatable."""
+    """Every gradient is written once, with fixed-order reductions: bitwise repeatable."""
     x = _prep(I.make_inputs(2, 2, 400, 64, seed=23, qkv_std=0.125, lam=0.5), "bf16")
     f = R.relation_fwd(x["q"], x["k"], x["v"], x["lam"])
     runs = [R.relation_bwd(x["q"], x["k"], x["v"], f["o"], x["do"], x["lam"], f["row_stat"],
                            want_dself=True) for _ in range(3)]
     torch.cuda.synchronize()
     for r in runs[1:]:
-        for n in ("dk", "dv", "dlambda", "dself"):
+        for n in ("dq", "dk", "dv", "dlambda", "dself"):
             assert torch.equal(r[n], runs[0][n]), n
 
 
