@@ -18,7 +18,8 @@
 //    queries straight from registers; Q^T and dO^T come from the row-major LDS
 //    tiles by transpose reads.
 //  * dQ, query-major, shaped like the forward pass: lanes hold query rows and
-//    dQ^T += K^T dU^T contracts over keys straight from registers.
+//    dQ^T += K^T dU^T contracts over keys straight from registers. It runs
+//    first and also stores D_i for the dK/dV kernel.
 // Every gradient is written exactly once: no atomics, run-to-run identical.
 #include "kernels.h"
 
@@ -77,7 +78,7 @@ __device__ __forceinline__ SelfGrad self_grad(float u, float dp, float Mi2, floa
 // dK / dV
 // ---------------------------------------------------------------------------
 template <class P, int D>
-__global__ __launch_bounds__(kNT) void bwd_dkdv_kernel(BwdArgs a) {
+__global__ __launch_bounds__(kNT, (D <= 64 ? 2 : 1)) void bwd_dkdv_kernel(BwdArgs a) {
   using E = typename P::T;
   using Op = typename P::Op;
   using Chunk = typename P::Chunk;
@@ -103,9 +104,9 @@ __global__ __launch_bounds__(kNT) void bwd_dkdv_kernel(BwdArgs a) {
   const E* q = (const E*)a.q + hoff;
   const E* k = (const E*)a.k + hoff;
   const E* v = (const E*)a.v + hoff;
-  const E* o = (const E*)a.o + hoff;
   const E* dO = (const E*)a.dout + hoff;
   const float* Mst = a.row_stat + (int64_t)head * T;
+  const float* Dst = a.dvec + (int64_t)head * T;
   const float c = a.scale * kLog2e;
   const float lam = *a.lambda;
 
@@ -129,7 +130,7 @@ __global__ __launch_bounds__(kNT) void bwd_dkdv_kernel(BwdArgs a) {
     dVt[db] = floatx16{};
   }
 
-  Chunk qreg[NLQ], dreg[NLQ], oreg[NLQ];
+  Chunk qreg[NLQ], dreg[NLQ];
   auto prefetch = [&](int i0) {
 #pragma unroll
     for (int jj = 0; jj < NLQ; ++jj) {
@@ -137,11 +138,9 @@ __global__ __launch_bounds__(kNT) void bwd_dkdv_kernel(BwdArgs a) {
       if (qi < T) {
         qreg[jj] = *(const Chunk*)(q + qi * st + P::CE * ch);
         dreg[jj] = *(const Chunk*)(dO + qi * st + P::CE * ch);
-        oreg[jj] = *(const Chunk*)(o + qi * st + P::CE * ch);
       } else {
         qreg[jj] = Chunk{};
         dreg[jj] = Chunk{};
-        oreg[jj] = Chunk{};
       }
     }
   };
@@ -157,15 +156,11 @@ __global__ __launch_bounds__(kNT) void bwd_dkdv_kernel(BwdArgs a) {
       const int ci = tid + kNT * jj, row = ci / NCH, ch = ci % NCH;
       P::stage(Qs, row, ch, qreg[jj]);
       P::stage(dOs, row, ch, dreg[jj]);
-      // D_i = dO_i . O_i, reduced over the NCH consecutive lanes holding the row
-      float part = P::chunk_dot(dreg[jj], oreg[jj]);
-#pragma unroll
-      for (int s = 1; s < NCH; s <<= 1) part += __shfl_xor(part, s, 64);
-      if (ch == 0) Drow[row] = part;
     }
     if (tid < kBQI) {
       const int qi = i0 + tid;
       Mrow[tid] = qi < T ? Mst[qi] * kLog2e : 0.0f;
+      Drow[tid] = qi < T ? Dst[qi] : 0.0f;
     }
     __syncthreads();
     if (qt + 1 < nqt) prefetch(i0 + kBQI);
@@ -303,6 +298,7 @@ __global__ __launch_bounds__(kNT, 2) void bwd_dq_kernel(BwdArgs a) {
   }
   const float Di = part + xor32(part);
   const float Mi2 = row_ok ? a.row_stat[(int64_t)head * T + qi] * kLog2e : 0.0f;
+  if (row_ok && g == 0) a.dvec[(int64_t)head * T + qi] = Di;
 
   Chunk kreg[NLD], vreg[NLD];
   auto prefetch = [&](int j0) {
@@ -416,20 +412,21 @@ __global__ void finalize_dlam_kernel(const float* __restrict__ part, int np, flo
 template <class P, int D>
 void launch_pair(const BwdArgs& a, const TileMap& mkv, const TileMap& mq, hipStream_t stream,
                  hipEvent_t* prof) {
+  // dQ first: it also writes D_i, which the dK/dV kernel reads
   BwdArgs b = a;
-  b.map = mkv;
   hipEvent_t e0, e1;
   const bool p_all = prof != nullptr;
-  const bool p_kv = !p_all && profile_slot("bwd_dkdv", &e0, &e1);
   if (p_all) (void)hipEventRecord(prof[0], stream);
-  if (p_kv) (void)hipEventRecord(e0, stream);
-  hipLaunchKernelGGL((bwd_dkdv_kernel<P, D>), dim3((unsigned)grid_size(mkv)), dim3(kNT), 0, stream, b);
-  if (p_kv) (void)hipEventRecord(e1, stream);
   b.map = mq;
   const bool p_q = !p_all && profile_slot("bwd_dq", &e0, &e1);
   if (p_q) (void)hipEventRecord(e0, stream);
   hipLaunchKernelGGL((bwd_dq_kernel<P, D>), dim3((unsigned)grid_size(mq)), dim3(kNT), 0, stream, b);
   if (p_q) (void)hipEventRecord(e1, stream);
+  b.map = mkv;
+  const bool p_kv = !p_all && profile_slot("bwd_dkdv", &e0, &e1);
+  if (p_kv) (void)hipEventRecord(e0, stream);
+  hipLaunchKernelGGL((bwd_dkdv_kernel<P, D>), dim3((unsigned)grid_size(mkv)), dim3(kNT), 0, stream, b);
+  if (p_kv) (void)hipEventRecord(e1, stream);
   if (p_all) (void)hipEventRecord(prof[1], stream);
 }
 
