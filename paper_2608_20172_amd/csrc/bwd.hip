@@ -21,6 +21,8 @@
 //    dQ^T += K^T dU^T contracts over keys straight from registers. It runs
 //    first and also stores D_i for the dK/dV kernel.
 // Every gradient is written exactly once: no atomics, run-to-run identical.
+// The dP chains start from an accumulator holding -D_i, so the matrix cores
+// deliver dP_ij - D_i directly.
 #include "kernels.h"
 
 #include <algorithm>
@@ -34,6 +36,12 @@ constexpr int kBQI = 64;   // query rows per dK/dV iteration
 constexpr int kBQ = 128;   // query rows per dQ workgroup
 constexpr int kBK = 64;    // keys per dQ tile
 constexpr int kNT = 256;
+#ifndef REL_DQ_WAVES_PER_SIMD
+#define REL_DQ_WAVES_PER_SIMD 2   // occupancy the register allocation is held to
+#endif
+#ifndef REL_DKDV_WAVES_PER_SIMD
+#define REL_DKDV_WAVES_PER_SIMD 2
+#endif
 
 __global__ void fill_zero_kernel(float* p, int64_t n) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -44,8 +52,9 @@ struct Grad {
   float F, dU;
 };
 
-// One Exchange entry (j < i). u = q_i . k_j (raw), dp = dO_i . v_j, Mi2 = M_i log2(e).
-__device__ __forceinline__ Grad exchange_grad(float u, float dp, float Mi2, float Di, float c) {
+// One Exchange entry (j < i). u = q_i . k_j (raw), dpd = dO_i . v_j - D_i,
+// Mi2 = M_i log2(e).
+__device__ __forceinline__ Grad exchange_grad(float u, float dpd, float Mi2, float c) {
   const float up = u * c;                              // U log2(e)
   const float sg = fast_rcp(1.0f + fast_exp2(-up));    // sigmoid(U)
   const float wl = up * sg;                            // E log2(e)
@@ -54,7 +63,7 @@ __device__ __forceinline__ Grad exchange_grad(float u, float dp, float Mi2, floa
   const float dsilu = __builtin_fmaf(t1, kLn2, sg);    // sigmoid + E (1 - sigmoid)
   Grad r;
   r.F = F;
-  r.dU = F * (dp - Di) * dsilu;
+  r.dU = F * dpd * dsilu;
   return r;
 }
 
@@ -64,12 +73,12 @@ struct SelfGrad {
 
 // The Self entry (j = i): U_ii = scale u, S_i = sigmoid(U_ii / tau_S). Row 1
 // has no history, so F_11 = 1 and dR_11 = 0 exactly (App. A.1.8).
-__device__ __forceinline__ SelfGrad self_grad(float u, float dp, float Mi2, float Di, float scale,
+__device__ __forceinline__ SelfGrad self_grad(float u, float dpd, float Mi2, float scale,
                                               float inv_tau, float lam, float ln_i, bool first_row) {
   const float S = fast_rcp(1.0f + fast_exp2(-u * scale * inv_tau * kLog2e));
   SelfGrad r;
   r.F = first_row ? 1.0f : fast_exp2((S + lam * ln_i) * kLog2e - Mi2);
-  r.dR = first_row ? 0.0f : r.F * (dp - Di);
+  r.dR = first_row ? 0.0f : r.F * dpd;
   r.dU = r.dR * S * (1.0f - S) * inv_tau;
   return r;
 }
@@ -78,7 +87,7 @@ __device__ __forceinline__ SelfGrad self_grad(float u, float dp, float Mi2, floa
 // dK / dV
 // ---------------------------------------------------------------------------
 template <class P, int D>
-__global__ __launch_bounds__(kNT, (D <= 64 ? 2 : 1)) void bwd_dkdv_kernel(BwdArgs a) {
+__global__ __launch_bounds__(kNT, (D <= 64 ? REL_DKDV_WAVES_PER_SIMD : 1)) void bwd_dkdv_kernel(BwdArgs a) {
   using E = typename P::T;
   using Op = typename P::Op;
   using Chunk = typename P::Chunk;
@@ -160,7 +169,7 @@ __global__ __launch_bounds__(kNT, (D <= 64 ? 2 : 1)) void bwd_dkdv_kernel(BwdArg
     if (tid < kBQI) {
       const int qi = i0 + tid;
       Mrow[tid] = qi < T ? Mst[qi] * kLog2e : 0.0f;
-      Drow[tid] = qi < T ? Dst[qi] : 0.0f;
+      Drow[tid] = qi < T ? -Dst[qi] : 0.0f;  // the dP chains start from -D_i
     }
     __syncthreads();
     if (qt + 1 < nqt) prefetch(i0 + kBQI);
@@ -170,8 +179,20 @@ __global__ __launch_bounds__(kNT, (D <= 64 ? 2 : 1)) void bwd_dkdv_kernel(BwdArg
       const int qb0 = i0 + 32 * qb;
       if (!wave_keys || qb0 < kw0 || qb0 >= T) continue;  // no row of the block reaches a key
       const int row = 32 * qb + n;
+      floatx16 negD, Mb;  // per register: -D and M log2(e) of its query row
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        const int r0 = 32 * qb + 8 * rq + 4 * g;  // tile row of register 4 rq
+        const floatx4 D4 = *(const floatx4*)(Drow + r0);
+        const floatx4 M4 = *(const floatx4*)(Mrow + r0);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          negD[4 * rq + t] = D4[t];
+          Mb[4 * rq + t] = M4[t];
+        }
+      }
       floatx16 s = P::mma(P::row_op(Qs, row, 0, L), kop[0], floatx16{});
-      floatx16 dp = P::mma(P::row_op(dOs, row, 0, L), vop[0], floatx16{});
+      floatx16 dp = P::mma(P::row_op(dOs, row, 0, L), vop[0], negD);  // dP - D
 #pragma unroll
       for (int ks = 1; ks < KS; ++ks) {
         s = P::mma(P::row_op(Qs, row, ks, L), kop[ks], s);
@@ -179,16 +200,10 @@ __global__ __launch_bounds__(kNT, (D <= 64 ? 2 : 1)) void bwd_dkdv_kernel(BwdArg
       }
       float F[16], dU[16];
 #pragma unroll
-      for (int rq = 0; rq < 4; ++rq) {
-        const int r0 = 32 * qb + 8 * rq + 4 * g;  // tile row of register 4 rq
-        const floatx4 M4 = *(const floatx4*)(Mrow + r0);
-        const floatx4 D4 = *(const floatx4*)(Drow + r0);
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const Grad gr = exchange_grad(s[4 * rq + t], dp[4 * rq + t], M4[t], D4[t], c);
-          F[4 * rq + t] = gr.F;
-          dU[4 * rq + t] = gr.dU;
-        }
+      for (int r = 0; r < 16; ++r) {
+        const Grad gr = exchange_grad(s[r], dp[r], Mb[r], c);
+        F[r] = gr.F;
+        dU[r] = gr.dU;
       }
       if (qb0 == kw0) {  // diagonal block: row offset acc_row(r, g) against key offset n
 #pragma unroll
@@ -200,8 +215,8 @@ __global__ __launch_bounds__(kNT, (D <= 64 ? 2 : 1)) void bwd_dkdv_kernel(BwdArg
         }
         if (holds_row(n, g)) {
           const int rs = row_reg(n);
-          const SelfGrad sg = self_grad(pick(s, rs), pick(dp, rs), Mrow[row], Drow[row], a.scale,
-                                        a.inv_tau, lam, logf((float)(kj + 1)), kj == 0);
+          const SelfGrad sg = self_grad(pick(s, rs), pick(dp, rs), Mrow[row], a.scale, a.inv_tau,
+                                        lam, logf((float)(kj + 1)), kj == 0);
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             F[r] = r == rs ? sg.F : F[r];
@@ -247,7 +262,7 @@ __global__ __launch_bounds__(kNT, (D <= 64 ? 2 : 1)) void bwd_dkdv_kernel(BwdArg
 // dQ (plus dself and the per-workgroup dlambda partials)
 // ---------------------------------------------------------------------------
 template <class P, int D>
-__global__ __launch_bounds__(kNT, 2) void bwd_dq_kernel(BwdArgs a) {
+__global__ __launch_bounds__(kNT, REL_DQ_WAVES_PER_SIMD) void bwd_dq_kernel(BwdArgs a) {
   using E = typename P::T;
   using Op = typename P::Op;
   using Chunk = typename P::Chunk;
@@ -299,6 +314,9 @@ __global__ __launch_bounds__(kNT, 2) void bwd_dq_kernel(BwdArgs a) {
   const float Di = part + xor32(part);
   const float Mi2 = row_ok ? a.row_stat[(int64_t)head * T + qi] * kLog2e : 0.0f;
   if (row_ok && g == 0) a.dvec[(int64_t)head * T + qi] = Di;
+  floatx16 negD;  // the dP chains start from -D_i
+#pragma unroll
+  for (int r = 0; r < 16; ++r) negD[r] = -Di;
 
   Chunk kreg[NLD], vreg[NLD];
   auto prefetch = [&](int j0) {
@@ -341,7 +359,7 @@ __global__ __launch_bounds__(kNT, 2) void bwd_dq_kernel(BwdArgs a) {
       if (kb0 > qr0) continue;
       const int row = 32 * sb + n;
       floatx16 s = P::mma(P::row_op(Ks, row, 0, L), qop[0], floatx16{});
-      floatx16 dp = P::mma(P::row_op(Vs, row, 0, L), doop[0], floatx16{});
+      floatx16 dp = P::mma(P::row_op(Vs, row, 0, L), doop[0], negD);  // dP - D
 #pragma unroll
       for (int ks = 1; ks < KS; ++ks) {
         s = P::mma(P::row_op(Ks, row, ks, L), qop[ks], s);
@@ -349,7 +367,7 @@ __global__ __launch_bounds__(kNT, 2) void bwd_dq_kernel(BwdArgs a) {
       }
       float dU[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) dU[r] = exchange_grad(s[r], dp[r], Mi2, Di, c).dU;
+      for (int r = 0; r < 16; ++r) dU[r] = exchange_grad(s[r], dp[r], Mi2, c).dU;
       if (kb0 == qr0) {  // diagonal block: key offset acc_row(r, g) against row offset n
 #pragma unroll
         for (int r = 0; r < 16; ++r)
@@ -357,7 +375,7 @@ __global__ __launch_bounds__(kNT, 2) void bwd_dq_kernel(BwdArgs a) {
         if (holds_row(n, g) && row_ok) {
           const int rs = row_reg(n);
           const float ln_i = logf((float)(qi + 1));
-          const SelfGrad sg = self_grad(pick(s, rs), pick(dp, rs), Mi2, Di, a.scale, a.inv_tau, lam, ln_i, qi == 0);
+          const SelfGrad sg = self_grad(pick(s, rs), pick(dp, rs), Mi2, a.scale, a.inv_tau, lam, ln_i, qi == 0);
 #pragma unroll
           for (int r = 0; r < 16; ++r) dU[r] = r == rs ? sg.dU : dU[r];
           dlam = __builtin_fmaf(ln_i, sg.dR, dlam);

@@ -154,6 +154,10 @@ struct PolBF16 {
   static __device__ __forceinline__ floatx16 mma(const Op& a, const Op& b, const floatx16& c) {
     return mfma32(a, b, c);
   }
+  static __device__ __forceinline__ Op ones() {
+    const uintx4 u = {0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u};  // bf16 1.0 x 8
+    return __builtin_bit_cast(Op, u);
+  }
   // dot product of two chunks (8 products)
   static __device__ __forceinline__ float chunk_dot(const Chunk& a, const Chunk& b) {
     float s = 0.0f;
@@ -227,6 +231,12 @@ struct PolF32 {
 #pragma unroll
     for (int t = 0; t < 8; ++t) c = mfma32f(a[t], b[t], c);
     return c;
+  }
+  static __device__ __forceinline__ Op ones() {
+    Op o;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) o[t] = 1.0f;
+    return o;
   }
   static __device__ __forceinline__ float chunk_dot(const Chunk& a, const Chunk& b) {
     return __builtin_fmaf(a[0], b[0], __builtin_fmaf(a[1], b[1], __builtin_fmaf(a[2], b[2], a[3] * b[3])));

@@ -25,6 +25,9 @@ constexpr int kBQ = 128;  // query rows per workgroup
 constexpr int kBK = 64;   // keys per tile
 constexpr int kNT = 256;  // threads per workgroup
 constexpr float kRescale = 8.0f;
+#ifndef REL_FWD_WAVES_PER_SIMD
+#define REL_FWD_WAVES_PER_SIMD 2  // occupancy the register allocation is held to
+#endif
 
 // Exchange logits of one 32x32 block, in place: s[r] (raw q.k) becomes
 // E log2(e) - m; in the diagonal block (DIAG) entries with key >= query get -inf.
@@ -70,7 +73,7 @@ __device__ __forceinline__ RowEpilogue row_epilogue(float m_log2, float l, float
 }
 
 template <class P, int D>
-__global__ __launch_bounds__(kNT, 2) void fwd_kernel(FwdArgs a) {
+__global__ __launch_bounds__(kNT, REL_FWD_WAVES_PER_SIMD) void fwd_kernel(FwdArgs a) {
   using E = typename P::T;
   using Op = typename P::Op;
   using Chunk = typename P::Chunk;
@@ -129,6 +132,8 @@ __global__ __launch_bounds__(kNT, 2) void fwd_kernel(FwdArgs a) {
     }
   };
 
+  // l sums the fp32 p (not the bf16-rounded MFMA operand), so that L^E and the
+  // saved statistic M carry no operand rounding
   float m = 0.0f, l = 0.0f, uii = 0.0f;
   floatx16 oacc[DB];
 #pragma unroll
