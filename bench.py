@@ -11,6 +11,8 @@ of heads on the host cores.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
   python bench.py --copy-bytes N   # plain device copy of N bytes (counter calibration)
+  python bench.py --summarize-counters F.csv W.csv CF.csv CW.csv --copy-bytes N
+                                   # backward HBM traffic from rocprofv3 --pmc runs
 """
 from __future__ import annotations
 
@@ -170,6 +172,47 @@ def traffic_for(kernel_hash: str):
     return t.get("bytes_per_launch")
 
 
+def _counter_rows(path: str) -> dict:
+    """Mean counter value per kernel over the dispatches of a rocprofv3
+    --pmc CSV (one row per dispatch and counter; repeated rows of one
+    dispatch are collapsed)."""
+    import csv
+    seen, acc = set(), {}
+    with open(path, newline="") as f:
+        for r in csv.DictReader(f):
+            key = (r["Dispatch_Id"], r["Counter_Name"])
+            if key in seen:
+                continue
+            seen.add(key)
+            acc.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+    return {k: sum(v) / len(v) for k, v in acc.items()}
+
+
+def summarize_counters(paths, copy_bytes: int) -> dict:
+    """HBM bytes per launch of each fused kernel from FETCH_SIZE and WRITE_SIZE
+    (KiB per dispatch), each scaled by what the same counter reads for a plain
+    device copy of ``copy_bytes`` bytes (read once, written once)."""
+    fetch, write, cfetch, cwrite = (_counter_rows(p) for p in paths)
+    copy_name = max(cfetch, key=cfetch.get)
+    f_scale = copy_bytes / (cfetch[copy_name] * 1024.0)
+    w_scale = copy_bytes / (cwrite[max(cwrite, key=cwrite.get)] * 1024.0)
+    per = {}
+    for short in ("fwd_kernel", "bwd_dq_kernel", "bwd_dkdv_kernel"):
+        names = [n for n in fetch if short + "<" in n and "PolBF16<64>" in n]
+        if not names:
+            continue
+        n = names[0]
+        fb = fetch[n] * 1024.0 * f_scale
+        wb = write.get(n, 0.0) * 1024.0 * w_scale
+        per[short] = {"fetch_kib_raw": fetch[n], "write_kib_raw": write.get(n, 0.0),
+                      "read_bytes": fb, "write_bytes": wb, "bytes": fb + wb}
+    bwd = per["bwd_dq_kernel"]["bytes"] + per["bwd_dkdv_kernel"]["bytes"]
+    return {"sources_hash": sources_hash(), "workload": "dec100m_T2048",
+            "bytes_per_launch": bwd, "per_kernel": per,
+            "calibration": {"copy_bytes": copy_bytes, "copy_kernel": copy_name,
+                            "fetch_factor": f_scale, "write_factor": w_scale}}
+
+
 # ---------------------------------------------------------------------------
 def copy_mode(nbytes: int, reps: int) -> None:
     import torch
@@ -191,7 +234,17 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-materialized", action="store_true")
     ap.add_argument("--copy-bytes", type=int, default=0)
+    ap.add_argument("--summarize-counters", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
+                    help="write the backward traffic file from four rocprofv3 --pmc CSVs "
+                         "(needs --copy-bytes of the calibration copy)")
     args = ap.parse_args()
+
+    if args.summarize_counters:
+        t = summarize_counters(args.summarize_counters, args.copy_bytes)
+        with open(TRAFFIC_FILE, "w") as f:
+            json.dump(t, f, indent=1)
+        print(json.dumps(t))
+        return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the fused operator is measured on one "

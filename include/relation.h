@@ -20,6 +20,7 @@
  *  - Tensors q, k, v, o, dout, dq, dk, dv are [B, H, T, D] with element
  *    strides (stride_b, stride_h, stride_t) taken from rel_problem and a
  *    contiguous last dimension. They all have the element type `dtype`.
+ *    The rows of one head must span less than 2 GiB (T * stride_t elements).
  *  - Row vectors (row_stat, self_mass, exch_mass, exch_lse, dself) are fp32,
  *    dense [B, H, T]. T x T outputs (R, F, pi) are fp32, dense [B, H, T, T].
  *  - lambda and dlambda point to one fp32 scalar in device memory.
@@ -49,7 +50,8 @@ extern "C" {
 typedef enum rel_status {
   REL_OK = 0,
   REL_ERR_INVALID_ARG = -1, /* null/overlapping/misaligned pointer, bad size or stride, bad tau_s */
-  REL_ERR_UNSUPPORTED = -2, /* dtype, head dimension or causal flag this build has no kernel for */
+  REL_ERR_UNSUPPORTED = -2, /* dtype, head dimension or causal flag this build has no kernel for,
+                               T > 2^24, B*H > 2^30, or T * stride_t * element size >= 2^31 bytes */
   REL_ERR_WORKSPACE = -3,   /* workspace pointer null or smaller than the query result */
   REL_ERR_HIP = -4          /* a HIP/rocBLAS call failed; see relation_last_error() */
 } rel_status;

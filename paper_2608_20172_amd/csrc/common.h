@@ -140,6 +140,27 @@ struct PolBF16 {
   static __device__ __forceinline__ Op row_op_g(const T* rowp, int ks, const Lane& L) {
     return *(const Op*)(rowp + 16 * ks + 8 * L.g);
   }
+  // row_op_g of the row times c, split as hi + lo with hi = bf16(x c) and
+  // lo = bf16(x c - hi): a product against hi and then lo carries the factor c
+  // to about 2^-16 relative, with no per-entry multiply afterwards.
+  static __device__ __forceinline__ void row_op_scaled(const T* rowp, int ks, const Lane& L, float c,
+                                                       Op& hi, Op& lo) {
+    const uintx4 u = *(const uintx4*)(rowp + 16 * ks + 8 * L.g);
+    float x[8], r[8];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      x[2 * t] = bf16_lo(u[t]) * c;
+      x[2 * t + 1] = bf16_hi(u[t]) * c;
+    }
+    hi = pack(x);
+    const uintx4 h = __builtin_bit_cast(uintx4, hi);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      r[2 * t] = x[2 * t] - bf16_lo(h[t]);
+      r[2 * t + 1] = x[2 * t + 1] - bf16_hi(h[t]);
+    }
+    lo = pack(r);
+  }
   // contraction over tile rows: element t = M[16 ks + 8 (t/4) + 4 g + t%4][col0 + n]
   static __device__ __forceinline__ Op col_op(const unsigned char* lds, int ks, int col0, const Lane& L) {
     const int r0 = 16 * ks + L.t_row, c = col0 + L.t_col;
@@ -213,6 +234,13 @@ struct PolF32 {
 #pragma unroll
     for (int t = 0; t < 8; ++t) o[t] = rowp[16 * ks + 2 * t + L.g];
     return o;
+  }
+  // fp32 rows take the factor c in one rounding; lo stays unused
+  static __device__ __forceinline__ void row_op_scaled(const T* rowp, int ks, const Lane& L, float c,
+                                                       Op& hi, Op& lo) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) hi[t] = rowp[16 * ks + 2 * t + L.g] * c;
+    lo = Op{};
   }
   static __device__ __forceinline__ Op col_op(const unsigned char* lds, int ks, int col0, const Lane& L) {
     const float* f = fp(lds) + col0 + L.n;

@@ -150,6 +150,10 @@ rel_status check_problem(const rel_problem* p, bool* empty) {
     return fail(REL_ERR_INVALID_ARG, "strides must be multiples of 16 bytes");
   if (!nested(lattice_of(p)))
     return fail(REL_ERR_INVALID_ARG, "strides make distinct (b, h, t) rows overlap");
+  // the kernels address the rows of one head with 32-bit byte offsets
+  if (p->T * p->stride_t * es >= (1LL << 31))
+    return fail(REL_ERR_UNSUPPORTED, "one head spans T * stride_t = %lld elements, over 2 GiB",
+                (long long)(p->T * p->stride_t));
   return REL_OK;
 }
 

@@ -80,6 +80,7 @@ def test_valid_call_reaches_launch(lib):
     (dict(st=68), R.REL_ERR_INVALID_ARG),          # not a multiple of 16 bytes
     (dict(sh=64), R.REL_ERR_INVALID_ARG),          # heads overlap rows
     (dict(T=(1 << 24) + 8), R.REL_ERR_UNSUPPORTED),
+    (dict(T=1 << 22, st=256), R.REL_ERR_UNSUPPORTED),  # one head spans 2 GiB of bf16
 ])
 def test_problem_validation(lib, mut, code):
     assert fwd(lib, prob(**mut)) == code
