@@ -106,8 +106,10 @@ rel_status relation_exchange_allocation(const rel_problem* p, const void* q, con
  *   dself      out [B,H,T] fp32, optional: dL/dS_i, the gradient reaching the
  *              Self logit R_ii = S_i (-g_i (1 - g_i) c_i in App. A.1.7).
  *   workspace  at least relation_bwd_workspace_bytes(p) bytes of device memory,
- *              16-byte aligned, for the fixed-order dlambda reduction; contents
- *              on entry are ignored.
+ *              16-byte aligned: two fp32 values per row (-D_i = -dout_i . o_i and
+ *              M_i log2(e), passed from the dQ pass to the dK/dV pass) and one
+ *              partial per dQ workgroup for the fixed-order dlambda reduction;
+ *              contents on entry are ignored.
  *   Every output is written exactly once (no atomics): results are run-to-run
  *   identical. */
 size_t relation_bwd_workspace_bytes(const rel_problem* p);

@@ -12,59 +12,85 @@
 // M_i = ln Z_i + lambda ln i is the one statistic saved by the forward pass.
 //
 // Two kernels, both recomputing the evidence tiles from q, k, v, dO:
+//  * dQ, query-major, shaped like the forward pass: lanes hold query rows and
+//    dQ^T += K^T dU^T contracts over keys straight from registers. It runs
+//    first and stores -D_i and M_i log2(e) per row for the dK/dV kernel.
 //  * dK/dV, key-major: a workgroup owns 128 keys (32 per wave) and walks the
 //    64-row query tiles at or below its diagonal. U = Q K^T and dP = dO V^T are
 //    formed with keys on lanes, so dV += F^T dO and dK += dU^T Q contract over
 //    queries straight from registers; Q^T and dO^T come from the row-major LDS
 //    tiles by transpose reads.
-//  * dQ, query-major, shaped like the forward pass: lanes hold query rows and
-//    dQ^T += K^T dU^T contracts over keys straight from registers. It runs
-//    first and also stores D_i for the dK/dV kernel.
-// Every gradient is written exactly once: no atomics, run-to-run identical.
-// The dP chains start from an accumulator holding -D_i, so the matrix cores
-// deliver dP_ij - D_i directly.
+// Tiles go HBM -> LDS by buffer loads that write LDS directly (two buffers,
+// one barrier per tile; rows past T read as zeros). Every gradient is written
+// exactly once: no atomics, run-to-run identical. The dP chains start from an
+// accumulator holding -D_i, so the matrix cores deliver dP_ij - D_i directly.
 #include "kernels.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace rel {
 
 namespace {
 
 constexpr int kBKW = 128;  // keys per dK/dV workgroup
-constexpr int kBQI = 64;   // query rows per dK/dV iteration
+constexpr int kBQI = 64;   // query rows per dK/dV tile
 constexpr int kBQ = 128;   // query rows per dQ workgroup
 constexpr int kBK = 64;    // keys per dQ tile
 constexpr int kNT = 256;
 #ifndef REL_DQ_WAVES_PER_SIMD
-#define REL_DQ_WAVES_PER_SIMD 2   // occupancy the register allocation is held to
+#define REL_DQ_WAVES_PER_SIMD 3   // bf16, d <= 64
+#endif
+#ifndef REL_DQ_NEGD_SEED
+#define REL_DQ_NEGD_SEED 0  // dQ: 1 = the dP chains start from -D_i (16 registers); 0 = subtract D_i per entry
+#endif
+#ifndef REL_DQ_OPERAND_BATCH
+#define REL_DQ_OPERAND_BATCH 1
 #endif
 #ifndef REL_DKDV_WAVES_PER_SIMD
-#define REL_DKDV_WAVES_PER_SIMD 2
+#define REL_DKDV_WAVES_PER_SIMD 2 // bf16, d <= 64
 #endif
+
+template <class P, int D>
+constexpr int dq_occupancy() {
+  return sizeof(typename P::T) == 2 ? (D <= 64 ? REL_DQ_WAVES_PER_SIMD : 1) : (D <= 32 ? 2 : 1);
+}
+template <class P, int D>
+constexpr int dkdv_occupancy() {
+  return sizeof(typename P::T) == 2 ? (D <= 64 ? REL_DKDV_WAVES_PER_SIMD : 1) : 1;
+}
 
 __global__ void fill_zero_kernel(float* p, int64_t n) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = 0.0f;
 }
 
-struct Grad {
-  float F, dU;
-};
-
-// One Exchange entry (j < i). u = q_i . k_j (raw), dpd = dO_i . v_j - D_i,
-// Mi2 = M_i log2(e).
-__device__ __forceinline__ Grad exchange_grad(float u, float dpd, float Mi2, float c) {
-  const float up = u * c;                              // U log2(e)
-  const float sg = fast_rcp(1.0f + fast_exp2(-up));    // sigmoid(U)
-  const float wl = up * sg;                            // E log2(e)
-  const float F = fast_exp2(wl - Mi2);                 // F_ij = exp(E_ij - M_i)
-  const float t1 = __builtin_fmaf(-wl, sg, wl);        // E log2(e) (1 - sigmoid)
-  const float dsilu = __builtin_fmaf(t1, kLn2, sg);    // sigmoid + E (1 - sigmoid)
-  Grad r;
-  r.F = F;
-  r.dU = F * dpd * dsilu;
-  return r;
+// Exchange entries (j < i) of one 32x32 block, in place: s holds raw q . k and
+// becomes F_ij = exp(E_ij - M_i); dp holds dP_ij - D_i and becomes dU_ij.
+// M2(r) = M log2(e) of the query row of register r. Passes over groups of 4
+// independent entries keep instructions off transcendental results.
+template <class MF>
+__device__ __forceinline__ void exchange_grads(floatx16& s, floatx16& dp, MF M2, float c, float dsub = 0.0f) {
+#pragma unroll
+  for (int r0 = 0; r0 < 16; r0 += 4) {
+    float up[4], sg[4], wl[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) up[r] = s[r0 + r] * c;                  // U log2(e)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sg[r] = fast_exp2(-up[r]);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sg[r] = fast_rcp(1.0f + sg[r]);         // sigmoid(U)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) wl[r] = up[r] * sg[r];                  // E log2(e)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float F = fast_exp2(wl[r] - M2(r0 + r));                    // F_ij = exp(E_ij - M_i)
+      const float t1 = __builtin_fmaf(-wl[r], sg[r], wl[r]);            // E log2(e) (1 - sigmoid)
+      const float dsilu = __builtin_fmaf(t1, kLn2, sg[r]);              // sigmoid + E (1 - sigmoid)
+      s[r0 + r] = F;
+      dp[r0 + r] = F * (dp[r0 + r] - dsub) * dsilu;
+    }
+  }
 }
 
 struct SelfGrad {
@@ -84,201 +110,24 @@ __device__ __forceinline__ SelfGrad self_grad(float u, float dpd, float Mi2, flo
 }
 
 // ---------------------------------------------------------------------------
-// dK / dV
+// dQ (plus dself, -D, M log2(e) and the per-workgroup dlambda partials)
 // ---------------------------------------------------------------------------
 template <class P, int D>
-__global__ __launch_bounds__(kNT, (D <= 64 ? REL_DKDV_WAVES_PER_SIMD : 1)) void bwd_dkdv_kernel(BwdArgs a) {
+__global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(BwdArgs a) {
   using E = typename P::T;
   using Op = typename P::Op;
-  using Chunk = typename P::Chunk;
   constexpr int KS = D / 16;
   constexpr int DB = D / 32;
-  constexpr int NCH = P::NCH;
-  constexpr int NLQ = kBQI * NCH / kNT;   // chunks per thread for a query tile
-  static_assert(NLQ >= 1, "query tile too small");
-  constexpr int TB = P::tile_bytes(kBQI);
-  __shared__ __attribute__((aligned(16))) unsigned char Qs[TB];
-  __shared__ __attribute__((aligned(16))) unsigned char dOs[TB];
-  __shared__ __attribute__((aligned(16))) float Mrow[kBQI];
-  __shared__ __attribute__((aligned(16))) float Drow[kBQI];
-
-  const int tid = threadIdx.x, w = tid >> 6;
-  const Lane L(tid & 63);
-  const int n = L.n, g = L.g;
-  int head, kt;
-  if (!map_tile(a.map, blockIdx.x, head, kt, false)) return;
-  const int T = a.T;
-  const int64_t st = a.st;
-  const int64_t hoff = (int64_t)(head / a.H) * a.sb + (int64_t)(head % a.H) * a.sh;
-  const E* q = (const E*)a.q + hoff;
-  const E* k = (const E*)a.k + hoff;
-  const E* v = (const E*)a.v + hoff;
-  const E* dO = (const E*)a.dout + hoff;
-  const float* Mst = a.row_stat + (int64_t)head * T;
-  const float* Dst = a.dvec + (int64_t)head * T;
-  const float c = a.scale * kLog2e;
-  const float lam = *a.lambda;
-
-  const int j0 = kt * kBKW;
-  const int kw0 = j0 + 32 * w;        // first key of this wave
-  const int kj = kw0 + n;             // this lane's key
-  const bool wave_keys = kw0 < T;
-
-  // B operands of U = Q K^T and dP = dO V^T: this lane's key row
-  Op kop[KS], vop[KS];
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    kop[ks] = kj < T ? P::row_op_g(k + kj * st, ks, L) : Op{};
-    vop[ks] = kj < T ? P::row_op_g(v + kj * st, ks, L) : Op{};
-  }
-
-  floatx16 dKt[DB], dVt[DB];
-#pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    dKt[db] = floatx16{};
-    dVt[db] = floatx16{};
-  }
-
-  Chunk qreg[NLQ], dreg[NLQ];
-  auto prefetch = [&](int i0) {
-#pragma unroll
-    for (int jj = 0; jj < NLQ; ++jj) {
-      const int ci = tid + kNT * jj, row = ci / NCH, ch = ci % NCH, qi = i0 + row;
-      if (qi < T) {
-        qreg[jj] = *(const Chunk*)(q + qi * st + P::CE * ch);
-        dreg[jj] = *(const Chunk*)(dO + qi * st + P::CE * ch);
-      } else {
-        qreg[jj] = Chunk{};
-        dreg[jj] = Chunk{};
-      }
-    }
-  };
-
-  const int nqt = (T + kBQI - 1) / kBQI;
-  const int qt0 = j0 / kBQI;
-  prefetch(qt0 * kBQI);
-  for (int qt = qt0; qt < nqt; ++qt) {
-    const int i0 = qt * kBQI;
-    __syncthreads();  // the previous tile is no longer read
-#pragma unroll
-    for (int jj = 0; jj < NLQ; ++jj) {
-      const int ci = tid + kNT * jj, row = ci / NCH, ch = ci % NCH;
-      P::stage(Qs, row, ch, qreg[jj]);
-      P::stage(dOs, row, ch, dreg[jj]);
-    }
-    if (tid < kBQI) {
-      const int qi = i0 + tid;
-      Mrow[tid] = qi < T ? Mst[qi] * kLog2e : 0.0f;
-      Drow[tid] = qi < T ? -Dst[qi] : 0.0f;  // the dP chains start from -D_i
-    }
-    __syncthreads();
-    if (qt + 1 < nqt) prefetch(i0 + kBQI);
-
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      const int qb0 = i0 + 32 * qb;
-      if (!wave_keys || qb0 < kw0 || qb0 >= T) continue;  // no row of the block reaches a key
-      const int row = 32 * qb + n;
-      floatx16 negD, Mb;  // per register: -D and M log2(e) of its query row
-#pragma unroll
-      for (int rq = 0; rq < 4; ++rq) {
-        const int r0 = 32 * qb + 8 * rq + 4 * g;  // tile row of register 4 rq
-        const floatx4 D4 = *(const floatx4*)(Drow + r0);
-        const floatx4 M4 = *(const floatx4*)(Mrow + r0);
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          negD[4 * rq + t] = D4[t];
-          Mb[4 * rq + t] = M4[t];
-        }
-      }
-      floatx16 s = P::mma(P::row_op(Qs, row, 0, L), kop[0], floatx16{});
-      floatx16 dp = P::mma(P::row_op(dOs, row, 0, L), vop[0], negD);  // dP - D
-#pragma unroll
-      for (int ks = 1; ks < KS; ++ks) {
-        s = P::mma(P::row_op(Qs, row, ks, L), kop[ks], s);
-        dp = P::mma(P::row_op(dOs, row, ks, L), vop[ks], dp);
-      }
-      float F[16], dU[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const Grad gr = exchange_grad(s[r], dp[r], Mb[r], c);
-        F[r] = gr.F;
-        dU[r] = gr.dU;
-      }
-      if (qb0 == kw0) {  // diagonal block: row offset acc_row(r, g) against key offset n
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          if (acc_row(r, g) < n) {
-            F[r] = 0.0f;
-            dU[r] = 0.0f;
-          }
-        }
-        if (holds_row(n, g)) {
-          const int rs = row_reg(n);
-          const SelfGrad sg = self_grad(pick(s, rs), pick(dp, rs), Mrow[row], a.scale, a.inv_tau,
-                                        lam, logf((float)(kj + 1)), kj == 0);
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            F[r] = r == rs ? sg.F : F[r];
-            dU[r] = r == rs ? sg.dU : dU[r];
-          }
-        }
-      }
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const Op fop = P::pack(F + 8 * hh);
-        const Op uop = P::pack(dU + 8 * hh);
-        const int ks = 2 * qb + hh;
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          dVt[db] = P::mma(P::col_op(dOs, ks, 32 * db, L), fop, dVt[db]);
-          dKt[db] = P::mma(P::col_op(Qs, ks, 32 * db, L), uop, dKt[db]);
-        }
-      }
-    }
-  }
-
-  if (kj < T) {
-    E* dk = (E*)a.dk + hoff;
-    E* dv = (E*)a.dv + hoff;
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int rq = 0; rq < 4; ++rq) {
-        const int d0 = 32 * db + 8 * rq + 4 * g;
-        floatx4 kk, vv;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          kk[t] = a.scale * dKt[db][4 * rq + t];
-          vv[t] = dVt[db][4 * rq + t];
-        }
-        P::store4(dk + kj * st + d0, kk);
-        P::store4(dv + kj * st + d0, vv);
-      }
-  }
-}
-
-// ---------------------------------------------------------------------------
-// dQ (plus dself and the per-workgroup dlambda partials)
-// ---------------------------------------------------------------------------
-template <class P, int D>
-__global__ __launch_bounds__(kNT, REL_DQ_WAVES_PER_SIMD) void bwd_dq_kernel(BwdArgs a) {
-  using E = typename P::T;
-  using Op = typename P::Op;
-  using Chunk = typename P::Chunk;
-  constexpr int KS = D / 16;
-  constexpr int DB = D / 32;
-  constexpr int SB = kBK / 32;
-  constexpr int NLD = kBK * P::NCH / kNT;
-  static_assert(NLD >= 1, "tile too small for the workgroup");
-  constexpr int TB = P::tile_bytes(kBK);
-  __shared__ __attribute__((aligned(16))) unsigned char lds[2 * TB];
+  constexpr int TB = kBK * P::ROWB;
+  constexpr int NSEG = TB / 1024;
+  constexpr int SEGW = 2 * NSEG / 4;
+  static_assert(SEGW >= 1 && 2 * NSEG % 4 == 0, "tile does not split over the waves");
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[2][2 * TB];
   __shared__ float red[kNT / 64];
-  unsigned char* Ks = lds;
-  unsigned char* Vs = lds + TB;
 
-  const int tid = threadIdx.x, w = tid >> 6;
-  const Lane L(tid & 63);
+  const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int lane = tid & 63;
+  const Lane L(lane);
   const int n = L.n, g = L.g;
   int head, qt;
   if (!map_tile(a.map, blockIdx.x, head, qt, true)) {
@@ -300,6 +149,18 @@ __global__ __launch_bounds__(kNT, REL_DQ_WAVES_PER_SIMD) void bwd_dq_kernel(BwdA
   const bool wave_live = qr0 < T;
   const bool row_ok = qi < T;
 
+  const int row_bytes = (int)(st * (int64_t)sizeof(E));
+  const __amdgpu_buffer_rsrc_t krs = make_rsrc(k, T * row_bytes);
+  const __amdgpu_buffer_rsrc_t vrs = make_rsrc(v, T * row_bytes);
+  auto load_tile = [&](int j0, int buf) {
+#pragma unroll
+    for (int s = 0; s < SEGW; ++s) {
+      const int seg = w * SEGW + s, tens = seg / NSEG;
+      dma_segment<P>(tens ? vrs : krs, lds[buf] + tens * TB, seg % NSEG, row_bytes, j0, lane);
+    }
+  };
+  load_tile(0, 0);
+
   // B operands: this lane's query row of Q and dO; D_i = dO_i . O_i from the
   // same slices, completed across the two lane halves
   Op qop[KS], doop[KS];
@@ -313,82 +174,94 @@ __global__ __launch_bounds__(kNT, REL_DQ_WAVES_PER_SIMD) void bwd_dq_kernel(BwdA
   }
   const float Di = part + xor32(part);
   const float Mi2 = row_ok ? a.row_stat[(int64_t)head * T + qi] * kLog2e : 0.0f;
-  if (row_ok && g == 0) a.dvec[(int64_t)head * T + qi] = Di;
+  if (row_ok && g == 0) {
+    a.negd[(int64_t)head * T + qi] = -Di;
+    a.m2[(int64_t)head * T + qi] = Mi2;
+  }
   floatx16 negD;  // the dP chains start from -D_i
 #pragma unroll
-  for (int r = 0; r < 16; ++r) negD[r] = -Di;
-
-  Chunk kreg[NLD], vreg[NLD];
-  auto prefetch = [&](int j0) {
-#pragma unroll
-    for (int j = 0; j < NLD; ++j) {
-      const int ci = tid + kNT * j, row = ci / P::NCH, ch = ci % P::NCH, key = j0 + row;
-      if (key < T) {
-        kreg[j] = *(const Chunk*)(k + key * st + P::CE * ch);
-        vreg[j] = *(const Chunk*)(v + key * st + P::CE * ch);
-      } else {
-        kreg[j] = Chunk{};
-        vreg[j] = Chunk{};
-      }
-    }
-  };
+  for (int r = 0; r < 16; ++r) negD[r] = REL_DQ_NEGD_SEED ? -Di : 0.0f;
+  const float dsub = REL_DQ_NEGD_SEED ? 0.0f : Di;
 
   floatx16 dQt[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) dQt[db] = floatx16{};
   float dlam = 0.0f;
 
+  // one 32-key block (krow0 .. krow0+31 of the tile); DIAG: the wave's own
+  // diagonal block (key offset acc_row(r, g) against row offset n)
+  auto block = [&](const unsigned char* Ks, const unsigned char* Vs, int krow0, auto diag_c) {
+    constexpr bool DIAG = decltype(diag_c)::value;
+    const int row = krow0 + n;
+    floatx16 s = {}, dp = negD;
+    constexpr int NB = REL_DQ_OPERAND_BATCH;  // K/V operand slices read per batch
+#pragma unroll
+    for (int k0 = 0; k0 < KS; k0 += NB) {
+      Op ka[NB], va[NB];
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        ka[j] = P::row_op(Ks, row, k0 + j, L);
+        va[j] = P::row_op(Vs, row, k0 + j, L);
+      }
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        s = P::mma(ka[j], qop[k0 + j], s);
+        dp = P::mma(va[j], doop[k0 + j], dp);  // dP - D
+      }
+    }
+    float uself = 0.0f, dself = 0.0f;
+    const int rs = row_reg(n);
+    if (DIAG) {
+      uself = pick(s, rs);
+      dself = pick(dp, rs);
+    }
+    if (!REL_DQ_NEGD_SEED && DIAG) dself -= Di;
+    exchange_grads(s, dp, [&](int) { return Mi2; }, c, dsub);
+    if (DIAG) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (acc_row(r, g) >= n) dp[r] = 0.0f;  // strictly historical: j < i
+      if (holds_row(n, g) && row_ok) {
+        const float ln_i = logf((float)(qi + 1));
+        const SelfGrad sg = self_grad(uself, dself, Mi2, a.scale, a.inv_tau, lam, ln_i, qi == 0);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) dp[r] = r == rs ? sg.dU : dp[r];
+        dlam = __builtin_fmaf(ln_i, sg.dR, dlam);
+        if (a.dself) a.dself[(int64_t)head * T + qi] = sg.dR;
+      }
+    }
+    const int ks0 = krow0 / 16;
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      float u8[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) u8[t] = dp[8 * hh + t];
+      const Op uop = P::pack(u8);
+#pragma unroll
+      for (int db = 0; db < DB; ++db) dQt[db] = P::mma(P::col_op(Ks, ks0 + hh, 32 * db, L), uop, dQt[db]);
+    }
+  };
+
   const int kmax = min(i0 + kBQ, T) - 1;
   const int nkt = kmax / kBK + 1;
-  prefetch(0);
   for (int kt = 0; kt < nkt; ++kt) {
+    wait_loads();
     __syncthreads();
-#pragma unroll
-    for (int j = 0; j < NLD; ++j) {
-      const int ci = tid + kNT * j, row = ci / P::NCH, ch = ci % P::NCH;
-      P::stage(Ks, row, ch, kreg[j]);
-      P::stage(Vs, row, ch, vreg[j]);
-    }
-    __syncthreads();
-    if (kt + 1 < nkt) prefetch((kt + 1) * kBK);
+    if (kt + 1 < nkt) load_tile((kt + 1) * kBK, (kt + 1) & 1);
     if (!wave_live) continue;
+    const unsigned char* Ks = lds[kt & 1];
+    const unsigned char* Vs = Ks + TB;
     const int j0 = kt * kBK;
-#pragma unroll
-    for (int sb = 0; sb < SB; ++sb) {
-      const int kb0 = j0 + 32 * sb;
-      if (kb0 > qr0) continue;
-      const int row = 32 * sb + n;
-      floatx16 s = P::mma(P::row_op(Ks, row, 0, L), qop[0], floatx16{});
-      floatx16 dp = P::mma(P::row_op(Vs, row, 0, L), doop[0], negD);  // dP - D
-#pragma unroll
-      for (int ks = 1; ks < KS; ++ks) {
-        s = P::mma(P::row_op(Ks, row, ks, L), qop[ks], s);
-        dp = P::mma(P::row_op(Vs, row, ks, L), doop[ks], dp);
-      }
-      float dU[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) dU[r] = exchange_grad(s[r], dp[r], Mi2, c).dU;
-      if (kb0 == qr0) {  // diagonal block: key offset acc_row(r, g) against row offset n
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (acc_row(r, g) >= n) dU[r] = 0.0f;
-        if (holds_row(n, g) && row_ok) {
-          const int rs = row_reg(n);
-          const float ln_i = logf((float)(qi + 1));
-          const SelfGrad sg = self_grad(pick(s, rs), pick(dp, rs), Mi2, a.scale, a.inv_tau, lam, ln_i, qi == 0);
-#pragma unroll
-          for (int r = 0; r < 16; ++r) dU[r] = r == rs ? sg.dU : dU[r];
-          dlam = __builtin_fmaf(ln_i, sg.dR, dlam);
-          if (a.dself) a.dself[(int64_t)head * T + qi] = sg.dR;
-        }
-      }
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const Op uop = P::pack(dU + 8 * hh);
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-          dQt[db] = P::mma(P::col_op(Ks, 2 * sb + hh, 32 * db, L), uop, dQt[db]);
-      }
+    using F0 = std::false_type;
+    using T1 = std::true_type;
+    if (j0 + 64 <= qr0) {
+      block(Ks, Vs, 0, F0{});
+      block(Ks, Vs, 32, F0{});
+    } else if (j0 + 32 == qr0) {
+      block(Ks, Vs, 0, F0{});
+      block(Ks, Vs, 32, T1{});
+    } else if (j0 == qr0) {
+      block(Ks, Vs, 0, T1{});
     }
   }
 
@@ -408,9 +281,198 @@ __global__ __launch_bounds__(kNT, REL_DQ_WAVES_PER_SIMD) void bwd_dq_kernel(BwdA
   // this workgroup's dlambda partial, summed in a fixed order
 #pragma unroll
   for (int s = 32; s >= 1; s >>= 1) dlam += __shfl_xor(dlam, s, 64);
-  if ((tid & 63) == 0) red[w] = dlam;
+  if (lane == 0) red[w] = dlam;
   __syncthreads();
   if (tid == 0) a.dlam_part[blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// ---------------------------------------------------------------------------
+// dK / dV
+// ---------------------------------------------------------------------------
+template <class P, int D>
+__global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel(BwdArgs a) {
+  using E = typename P::T;
+  using Op = typename P::Op;
+  constexpr int KS = D / 16;
+  constexpr int DB = D / 32;
+  constexpr int TB = kBQI * P::ROWB;            // one tensor tile (Q or dO)
+  constexpr int NSEG = TB / 1024;
+  constexpr int SEGW = 2 * NSEG / 4;
+  static_assert(SEGW >= 1 && 2 * NSEG % 4 == 0, "tile does not split over the waves");
+  constexpr int BUF = 2 * TB + 2 * kBQI * 4;    // Q, dO, M log2(e), -D
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[2][BUF];
+
+  const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int lane = tid & 63;
+  const Lane L(lane);
+  const int n = L.n, g = L.g;
+  int head, kt;
+  if (!map_tile(a.map, blockIdx.x, head, kt, false)) return;
+  const int T = a.T;
+  const int64_t st = a.st;
+  const int64_t hoff = (int64_t)(head / a.H) * a.sb + (int64_t)(head % a.H) * a.sh;
+  const E* q = (const E*)a.q + hoff;
+  const E* k = (const E*)a.k + hoff;
+  const E* v = (const E*)a.v + hoff;
+  const E* dO = (const E*)a.dout + hoff;
+  const float c = a.scale * kLog2e;
+  const float lam = *a.lambda;
+
+  const int j0 = kt * kBKW;
+  const int kw0 = j0 + 32 * w;        // first key of this wave
+  const int kj = kw0 + n;             // this lane's key
+  const bool wave_keys = kw0 < T;
+
+  // query tiles of Q and dO, and the per-row -D and M log2(e); rows past T
+  // read as zeros, so they add nothing to dK and dV
+  const int row_bytes = (int)(st * (int64_t)sizeof(E));
+  const __amdgpu_buffer_rsrc_t qrs = make_rsrc(q, T * row_bytes);
+  const __amdgpu_buffer_rsrc_t drs = make_rsrc(dO, T * row_bytes);
+  const __amdgpu_buffer_rsrc_t mrs = make_rsrc(a.m2 + (int64_t)head * T, T * 4);
+  const __amdgpu_buffer_rsrc_t nrs = make_rsrc(a.negd + (int64_t)head * T, T * 4);
+  auto load_tile = [&](int i0, int buf) {
+#pragma unroll
+    for (int s = 0; s < SEGW; ++s) {
+      const int seg = w * SEGW + s, tens = seg / NSEG;
+      dma_segment<P>(tens ? drs : qrs, lds[buf] + tens * TB, seg % NSEG, row_bytes, i0, lane);
+    }
+    if (w < 2) dma_row64(w ? nrs : mrs, (float*)(lds[buf] + 2 * TB) + w * kBQI, i0, lane);
+  };
+
+  const int nqt = (T + kBQI - 1) / kBQI;
+  const int qt0 = j0 / kBQI;
+  load_tile(qt0 * kBQI, 0);
+
+  // B operands of U = Q K^T and dP = dO V^T: this lane's key row
+  Op kop[KS], vop[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    kop[ks] = kj < T ? P::row_op_g(k + kj * st, ks, L) : Op{};
+    vop[ks] = kj < T ? P::row_op_g(v + kj * st, ks, L) : Op{};
+  }
+
+  floatx16 dKt[DB], dVt[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    dKt[db] = floatx16{};
+    dVt[db] = floatx16{};
+  }
+
+  // one 32-row query block qb of the tile; DIAG: the block whose rows start at
+  // this wave's first key (row offset acc_row(r, g) against key offset n)
+  auto block = [&](const unsigned char* buf, int qb, auto diag_c) {
+    constexpr bool DIAG = decltype(diag_c)::value;
+    const unsigned char* Qs = buf;
+    const unsigned char* dOs = buf + TB;
+    const float* Mrow = (const float*)(buf + 2 * TB);
+    const float* Nrow = Mrow + kBQI;
+    const int row = 32 * qb + n;
+    floatx16 Mb, dp;  // per register: M log2(e) and -D of its query row
+#pragma unroll
+    for (int rq = 0; rq < 4; ++rq) {
+      const int r0 = 32 * qb + 8 * rq + 4 * g;  // tile row of register 4 rq
+      const floatx4 M4 = *(const floatx4*)(Mrow + r0);
+      const floatx4 D4 = *(const floatx4*)(Nrow + r0);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        Mb[4 * rq + t] = M4[t];
+        dp[4 * rq + t] = D4[t];
+      }
+    }
+    floatx16 s = {};
+#pragma unroll
+    for (int k0 = 0; k0 < KS; k0 += 2) {
+      Op qa[2], da[2];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        qa[j] = P::row_op(Qs, row, k0 + j, L);
+        da[j] = P::row_op(dOs, row, k0 + j, L);
+      }
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        s = P::mma(qa[j], kop[k0 + j], s);
+        dp = P::mma(da[j], vop[k0 + j], dp);  // dP - D
+      }
+    }
+    float uself = 0.0f, dself = 0.0f;
+    const int rs = row_reg(n);
+    if (DIAG) {
+      uself = pick(s, rs);
+      dself = pick(dp, rs);
+    }
+    exchange_grads(s, dp, [&](int r) { return Mb[r]; }, c);
+    if (DIAG) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        if (acc_row(r, g) < n) {  // query before the key: no flow
+          s[r] = 0.0f;
+          dp[r] = 0.0f;
+        }
+      }
+      if (holds_row(n, g)) {
+        const SelfGrad sg = self_grad(uself, dself, Mb[rs], a.scale, a.inv_tau, lam, logf((float)(kj + 1)), kj == 0);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          s[r] = r == rs ? sg.F : s[r];
+          dp[r] = r == rs ? sg.dU : dp[r];
+        }
+      }
+    }
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      float f8[8], u8[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        f8[t] = s[8 * hh + t];
+        u8[t] = dp[8 * hh + t];
+      }
+      const Op fop = P::pack(f8);
+      const Op uop = P::pack(u8);
+      const int ks = 2 * qb + hh;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        dVt[db] = P::mma(P::col_op(dOs, ks, 32 * db, L), fop, dVt[db]);
+        dKt[db] = P::mma(P::col_op(Qs, ks, 32 * db, L), uop, dKt[db]);
+      }
+    }
+  };
+
+  for (int qt = qt0; qt < nqt; ++qt) {
+    const int i0 = qt * kBQI;
+    wait_loads();
+    __syncthreads();
+    if (qt + 1 < nqt) load_tile(i0 + kBQI, (qt + 1 - qt0) & 1);
+    if (!wave_keys) continue;
+    const unsigned char* buf = lds[(qt - qt0) & 1];
+    using F0 = std::false_type;
+    using T1 = std::true_type;
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const int qb0 = i0 + 32 * qb;
+      if (qb0 < kw0 || qb0 >= T) continue;  // no row of the block reaches a key of the wave
+      if (qb0 == kw0) block(buf, qb, T1{});
+      else block(buf, qb, F0{});
+    }
+  }
+
+  if (kj < T) {
+    E* dk = (E*)a.dk + hoff;
+    E* dv = (E*)a.dv + hoff;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        const int d0 = 32 * db + 8 * rq + 4 * g;
+        floatx4 kk, vv;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          kk[t] = a.scale * dKt[db][4 * rq + t];
+          vv[t] = dVt[db][4 * rq + t];
+        }
+        P::store4(dk + kj * st + d0, kk);
+        P::store4(dv + kj * st + d0, vv);
+      }
+  }
 }
 
 // dlambda = sum of the per-workgroup partials, in a fixed order.

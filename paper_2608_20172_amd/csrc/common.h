@@ -100,8 +100,9 @@ template <> struct Elem<bf16> {
 // 32x32 block. So a 32x32 result block, re-packed from its registers, is
 // directly the operand of the next product along its rows.
 //   bf16: one 32x32x16 MFMA per slice; tiles are row-major in LDS with
-//         16-byte chunks XOR-swizzled by row; "col" operands by transpose reads.
-//   f32:  eight 32x32x2 MFMAs per slice; rows padded by one element.
+//         16-byte chunks XOR-swizzled by row (swz); "col" operands by
+//         transpose reads.
+//   f32:  eight 32x32x2 MFMAs per slice; plain row-major tiles.
 // ---------------------------------------------------------------------------
 typedef float floatx8 __attribute__((ext_vector_type(8)));
 
@@ -124,21 +125,47 @@ struct PolBF16 {
   using Chunk = uintx4;                        // 16 bytes = 8 elements
   static constexpr int CE = 8;                 // elements per chunk
   static constexpr int NCH = D / 8;            // chunks per row
-  static constexpr int ROWB = 2 * D;           // bytes per LDS row
-  static constexpr int SWZ = (NCH < 8 ? NCH : 8) - 1;
+  static constexpr int ROWB = 2 * D;           // bytes of one tile row
+  static constexpr int TR = 64;                // rows of every tile
+  static constexpr int SUB = TR * 64;          // bytes of a 32-column sub-tile
   static constexpr int tile_bytes(int rows) { return rows * ROWB; }
-  static __device__ __forceinline__ int off(int row, int col) {
-    return row * ROWB + (((col >> 3) ^ (row & SWZ)) << 4) + ((col & 7) << 1);
+  // A 64-row tile is stored as D/32 sub-tiles of 32 columns (64-byte rows),
+  // so a 32-column block is an immediate offset. Within a sub-tile, 16-byte
+  // chunk c of row r sits at chunk c ^ swz(r): swz mixes row bits 1-3 so that
+  // both access patterns below are free of bank conflicts with 32 or 64 LDS
+  // banks (16-byte reads of consecutive rows, and transpose reads of 4 rows x
+  // 32 bytes per 16 lanes).
+  static __device__ __forceinline__ constexpr int swz(int r) {
+    return ((r >> 2) & 1) | ((((r >> 1) ^ (r >> 3)) & 1) << 1);
   }
-  static __device__ __forceinline__ void stage(unsigned char* lds, int row, int ch, const Chunk& v) {
-    *(Chunk*)(lds + row * ROWB + ((ch ^ (row & SWZ)) << 4)) = v;
+  static __device__ __forceinline__ int off(int row, int col) {
+    return (col >> 5) * SUB + row * 64 + ((((col >> 3) & 3) ^ swz(row)) << 4) + ((col & 7) << 1);
   }
   // contraction over the row's elements: element t = row[16 ks + 8 g + t]
   static __device__ __forceinline__ Op row_op(const unsigned char* lds, int row, int ks, const Lane& L) {
-    return *(const Op*)(lds + row * ROWB + (((2 * ks + L.g) ^ (row & SWZ)) << 4));
+    const int ch = 2 * ks + L.g;  // 16-byte chunk of the row
+    return *(const Op*)(lds + (ch >> 2) * SUB + row * 64 + (((ch & 3) ^ swz(row)) << 4));
   }
   static __device__ __forceinline__ Op row_op_g(const T* rowp, int ks, const Lane& L) {
     return *(const Op*)(rowp + 16 * ks + 8 * L.g);
+  }
+  // contraction over tile rows: element t = M[16 ks + 8 (t/4) + 4 g + t%4][col0 + n]
+  static __device__ __forceinline__ Op col_op(const unsigned char* lds, int ks, int col0, const Lane& L) {
+    // rows 16 ks + t_row and 16 ks + t_row + 8; the swizzle sees only t_row
+    const int c = L.t_col;  // column within the 32-column block col0
+    const int base = (col0 >> 5) * SUB + (16 * ks + L.t_row) * 64 + ((c & 7) << 1);
+    return tr_operand(lds + base + (((c >> 3) ^ swz(L.t_row)) << 4),
+                      lds + base + 8 * 64 + (((c >> 3) ^ swz(L.t_row + 8)) << 4));
+  }
+  // Direct-load slot of lane `lane` in 1 KB segment `seg` of a tile: the tile
+  // row, the byte offset of its 16 bytes within the tensor row, and the LDS
+  // byte offset of the segment (16 rows of one sub-tile).
+  static __device__ __forceinline__ void seg_map(int seg, int lane, int& row, int& gbyte, int& lds_off) {
+    constexpr int SPS = TR / 16;  // segments per sub-tile
+    const int db = seg / SPS, r0 = (seg % SPS) * 16;
+    row = r0 + (lane >> 2);
+    gbyte = 64 * db + 16 * ((lane & 3) ^ swz(row));
+    lds_off = db * SUB + r0 * 64;
   }
   // row_op_g of the row times c, split as hi + lo with hi = bf16(x c) and
   // lo = bf16(x c - hi): a product against hi and then lo carries the factor c
@@ -160,11 +187,6 @@ struct PolBF16 {
       r[2 * t + 1] = x[2 * t + 1] - bf16_hi(h[t]);
     }
     lo = pack(r);
-  }
-  // contraction over tile rows: element t = M[16 ks + 8 (t/4) + 4 g + t%4][col0 + n]
-  static __device__ __forceinline__ Op col_op(const unsigned char* lds, int ks, int col0, const Lane& L) {
-    const int r0 = 16 * ks + L.t_row, c = col0 + L.t_col;
-    return tr_operand(lds + off(r0, c), lds + off(r0 + 8, c));
   }
   static __device__ __forceinline__ Op pack(const float* x) {
     Op o;
@@ -213,14 +235,20 @@ struct PolF32 {
   using Chunk = floatx4;                       // 16 bytes = 4 elements
   static constexpr int CE = 4;
   static constexpr int NCH = D / 4;
-  static constexpr int ROWF = D + 1;           // padded row, floats
+  static constexpr int ROWF = D;               // row, floats (no padding: tiles are filled by DMA)
+  static constexpr int ROWB = 4 * D;           // bytes per LDS row
+  static constexpr int TR = 64;                // rows of every tile
+  // Direct-load slot (see PolBF16::seg_map): plain row-major rows.
+  static __device__ __forceinline__ void seg_map(int seg, int lane, int& row, int& gbyte, int& lds_off) {
+    constexpr int CH = ROWB / 16, SEG_ROWS = 1024 / ROWB;
+    static_assert(SEG_ROWS * ROWB == 1024, "a row must divide 1 KB");
+    const int r0 = seg * SEG_ROWS;
+    row = r0 + lane / CH;
+    gbyte = 16 * (lane % CH);
+    lds_off = r0 * ROWB;
+  }
   static constexpr int tile_bytes(int rows) { return rows * ROWF * 4; }
   static __device__ __forceinline__ const float* fp(const unsigned char* lds) { return (const float*)lds; }
-  static __device__ __forceinline__ void stage(unsigned char* lds, int row, int ch, const Chunk& v) {
-    float* f = (float*)lds + row * ROWF + 4 * ch;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) f[e] = v[e];
-  }
   // element t = row[16 ks + 2 t + g]  (MFMA step t covers 16 ks + 2 t .. +1)
   static __device__ __forceinline__ Op row_op(const unsigned char* lds, int row, int ks, const Lane& L) {
     const float* f = fp(lds) + row * ROWF + 16 * ks + L.g;
@@ -278,6 +306,35 @@ struct PolF32 {
   static __device__ __forceinline__ floatx4 load4(const T* p) { return *(const floatx4*)p; }
   static __device__ __forceinline__ void store4(T* p, const floatx4& x) { *(floatx4*)p = x; }
 };
+
+// ---------------------------------------------------------------------------
+// Tiles HBM -> LDS without registers: buffer loads that write LDS directly.
+// One 64-lane load moves 1 KB: lane l's 16 bytes land at segment + 16 l, so
+// each lane fetches whichever 16 bytes of the tensor the policy's layout puts
+// in that slot (seg_map). Rows past the end of the buffer resource read as
+// zeros (the hardware range check), which is how tiles running past T are
+// padded.
+// ---------------------------------------------------------------------------
+typedef __attribute__((address_space(3))) void lds_void;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
+}
+// 1 KB segment `seg` of a 64-row tile whose row 0 is tensor row j0 (row
+// stride row_bytes); `tile` is the LDS tile, wave-uniform.
+template <class P>
+__device__ __forceinline__ void dma_segment(__amdgpu_buffer_rsrc_t rs, unsigned char* tile, int seg, int row_bytes,
+                                            int j0, int lane) {
+  int row, gbyte, lds_off;
+  P::seg_map(seg, lane, row, gbyte, lds_off);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(tile + lds_off), 16, row * row_bytes + gbyte,
+                                           j0 * row_bytes, 0, 0);
+}
+// 64 consecutive fp32 values from element j0 of a row vector into dst[0..63].
+__device__ __forceinline__ void dma_row64(__amdgpu_buffer_rsrc_t rs, float* dst, int j0, int lane) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)dst, 4, 4 * lane, 4 * j0, 0, 0);
+}
+// Waits until this wave's loads have landed (vmcnt 0; other counters untouched).
+__device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x0f70); }
 
 // Register r* of a 32x32 block that holds row n for lane group g, if any:
 // acc_row(r, g) == n  <=>  g == (n >> 2) & 1  and  r == 4 (n >> 3) + (n & 3).

@@ -16,19 +16,11 @@
 // the same ratios z/l and L^E = m + ln l, so the result is exact. The test is
 // lane-local; only a raise combines the two halves of a row.
 //
-// Two kernels:
-//  * bf16 (fwdb_kernel): K/V tiles go HBM -> LDS directly (buffer loads to
-//    LDS, 16 bytes per lane), two buffers, one barrier per tile, so no staging
-//    registers are held. With 4 waves a wave scans every 64-key tile for its 32
-//    rows; with 8 waves, waves 0-3 scan the first 64 keys of every 128-key tile
-//    and waves 4-7 the last 64 for the same rows, and the two partial scan
-//    states of a row are merged at the end (the (m, l, z) state is
-//    associative: m = max, l and z rescaled and added).
-//  * fp32 (fwd_kernel): 4 waves per workgroup, 64-key tiles staged through
-//    registers into padded LDS rows.
+// K/V tiles of 64 keys go HBM -> LDS by buffer loads that write LDS directly
+// (no staging registers), into two buffers with one barrier per tile; four
+// waves per workgroup, three per SIMD for bf16 with d <= 64.
 #include "kernels.h"
 
-#include <type_traits>
 
 namespace rel {
 
@@ -37,7 +29,7 @@ namespace {
 constexpr int kBQ = 128;  // query rows per workgroup
 constexpr float kRescale = 8.0f;
 #ifndef REL_FWD_WAVES_PER_SIMD
-#define REL_FWD_WAVES_PER_SIMD 2  // occupancy of the fp32 kernel
+#define REL_FWD_WAVES_PER_SIMD 2  // occupancy of the fp32 kernel for d <= 64
 #endif
 
 // How the query operand carries c = scale log2(e):
@@ -241,32 +233,24 @@ __device__ __forceinline__ void load_query(const typename P::T* q, int64_t st, i
   }
 }
 
-// ---------------------------------------------------------------------------
-// bf16: NW = 4 or 8 waves. With 8, waves 0-3 and 4-7 take the two 64-key
-// halves of every 128-key tile for the same 128 rows and merge at the end.
-// ---------------------------------------------------------------------------
-#ifndef REL_FWD_BF16_WAVES
-#define REL_FWD_BF16_WAVES 4
-#endif
-template <int NW, int D>
-constexpr int fwd_bf16_occupancy() {
-  return D > 64 ? 2 : (NW == 8 ? 4 : 3);
+constexpr int kBK = 64;   // keys per tile
+constexpr int kNT = 256;  // threads per workgroup
+
+template <class P, int D>
+constexpr int fwd_occupancy() {
+  return sizeof(typename P::T) == 2 ? (D <= 64 ? 3 : 2) : (D <= 64 ? REL_FWD_WAVES_PER_SIMD : 1);
 }
 
-template <int D, int NW>
-__global__ __launch_bounds__(NW * 64, (fwd_bf16_occupancy<NW, D>())) void fwdb_kernel(FwdArgs a) {
-  using P = PolBF16<D>;
-  using E = bf16;
+template <class P, int D>
+__global__ __launch_bounds__(kNT, (fwd_occupancy<P, D>())) void fwd_kernel(FwdArgs a) {
+  using E = typename P::T;
   using Op = typename P::Op;
   constexpr int QM = qmode<P, D>();
   constexpr int KS = D / 16, DB = D / 32;
-  constexpr int KH = NW / 4;                   // key halves
-  constexpr int BK = 64 * KH;                  // keys per tile
-  constexpr int TB = BK * P::ROWB;             // bytes of one tensor tile
-  constexpr int SEG_ROWS = 1024 / P::ROWB;     // tile rows filled by one 64-lane load
-  constexpr int NSEG = BK / SEG_ROWS;          // such loads per tensor tile
-  constexpr int SEGW = 2 * NSEG / NW;          // per wave, K and V together
-  static_assert(2 * NSEG % NW == 0 && 64 % P::NCH == 0, "tile does not split over the waves");
+  constexpr int TB = kBK * P::ROWB;            // bytes of one tensor tile
+  constexpr int NSEG = TB / 1024;              // 1 KB loads per tensor tile
+  constexpr int SEGW = 2 * NSEG / 4;           // per wave, K and V together
+  static_assert(SEGW >= 1 && 2 * NSEG % 4 == 0, "tile does not split over the waves");
   __shared__ __attribute__((aligned(1024))) unsigned char lds[2][2 * TB];
 
   int head, qt;
@@ -282,148 +266,25 @@ __global__ __launch_bounds__(NW * 64, (fwd_bf16_occupancy<NW, D>())) void fwdb_k
   const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int lane = tid & 63;
   const Lane L(lane);
-  const int rw = w & 3, kh = w >> 2;  // row group, key half
-  const int i0 = qt * kBQ, qr0 = i0 + 32 * rw, qi = qr0 + L.n;
-  const bool wave_live = qr0 < T;
-  const float c = a.scale * kLog2e;
-
-  // One 1 KB segment per load: lane l fills physical chunk l % NCH of tile row
-  // r0 + l / NCH, which holds logical chunk (l % NCH) ^ (row & SWZ) (the XOR
-  // swizzle of the tile layout). Rows past T repeat row T-1: such keys only
-  // meet masked (zero) weights. Buffer loads take a scalar base per tensor and
-  // head and a 32-bit byte offset per lane (the host keeps a head within 2 GiB).
-  const int row_bytes = (int)(st * 2);
-  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc((void*)k, (short)0, T * row_bytes, 0x00020000);
-  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc((void*)v, (short)0, T * row_bytes, 0x00020000);
-  auto load_tile = [&](int j0, int buf) {
-    const int last = T - 1 - j0;  // last valid row of this tile
-#pragma unroll
-    for (int s = 0; s < SEGW; ++s) {
-      const int seg = w * SEGW + s;
-      const int tens = seg / NSEG, r0 = (seg % NSEG) * SEG_ROWS;
-      const int row = r0 + lane / P::NCH, ch = (lane % P::NCH) ^ (row & P::SWZ);
-      const int voff = min(row, last) * row_bytes + 16 * ch;
-      unsigned char* dst = lds[buf] + tens * TB + r0 * P::ROWB;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(tens ? vrs : krs, (__attribute__((address_space(3))) void*)dst, 16,
-                                               voff, j0 * row_bytes, 0, 0);
-    }
-  };
-
-  Op qhi[KS], qlo[KS];
-  load_query<P, KS, QM>(q, st, qi, T, L, c, qhi, qlo);
-
-  float m = 0.0f, l = 0.0f, uii = 0.0f;
-  floatx16 oacc[DB];
-#pragma unroll
-  for (int db = 0; db < DB; ++db) oacc[db] = floatx16{};
-
-  const int kmax = min(i0 + kBQ, T) - 1;  // the diagonal of the last row is included
-  const int nkt = kmax / BK + 1;
-  load_tile(0, 0);
-  for (int kt = 0; kt < nkt; ++kt) {
-    __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this wave's part of tile kt is in LDS
-    __syncthreads();                     // ... and every wave's; tile kt-1 is no longer read
-    if (kt + 1 < nkt) load_tile((kt + 1) * BK, (kt + 1) & 1);
-    if (wave_live) {
-      const unsigned char* Ks = lds[kt & 1];
-      scan_keys64<P, D, QM>(Ks, Ks + TB, 64 * kh, kt * BK + 64 * kh, qr0, qhi, qlo, oacc, m, l, uii, L, c);
-    }
-  }
-
-  if (KH == 2) {
-    // ---- merge the two key halves of every row (waves w and w + 4)
-    constexpr int NV = DB * 16 + 3;  // values per lane: z, then m, l, U_ii
-    static_assert(KH == 1 || 4 * NV * 64 * 4 <= 2 * 2 * TB, "merge buffer exceeds the tile buffers");
-    float* red = (float*)&lds[0][0];
-    __syncthreads();
-    if (kh == 1 && wave_live) {
-      float* r = red + rw * NV * 64 + lane;
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int t = 0; t < 16; ++t) r[(16 * db + t) * 64] = oacc[db][t];
-      r[(DB * 16) * 64] = m;
-      r[(DB * 16 + 1) * 64] = l;
-      r[(DB * 16 + 2) * 64] = uii;
-    }
-    __syncthreads();
-    if (kh == 1 || !wave_live) return;
-    const float* r = red + rw * NV * 64 + lane;
-    const float m1 = r[(DB * 16) * 64], l1 = r[(DB * 16 + 1) * 64], u1 = r[(DB * 16 + 2) * 64];
-    const float mt = fmaxf(m, m1);
-    const float a0 = fast_exp2(m - mt), a1 = fast_exp2(m1 - mt);
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int t = 0; t < 16; ++t) oacc[db][t] = __builtin_fmaf(oacc[db][t], a0, r[(16 * db + t) * 64] * a1);
-    l = __builtin_fmaf(l, a0, l1 * a1);
-    m = mt;
-    uii += u1;  // only the half that met the diagonal block set it
-  }
-  if (!wave_live) return;
-  finish_row<P, D, QM>(a, o, v, st, head, qi, m, l, uii, oacc, L, c);
-}
-
-// ---------------------------------------------------------------------------
-// fp32: 4 waves, 64-key tiles through registers into padded LDS rows
-// ---------------------------------------------------------------------------
-constexpr int kBK = 64;   // keys per tile
-constexpr int kNT = 256;  // threads per workgroup
-
-template <class P, int D>
-__global__ __launch_bounds__(kNT, REL_FWD_WAVES_PER_SIMD) void fwd_kernel(FwdArgs a) {
-  using E = typename P::T;
-  using Op = typename P::Op;
-  using Chunk = typename P::Chunk;
-  constexpr int QM = qmode<P, D>();
-  constexpr int KS = D / 16;                      // 16-wide slices of d
-  constexpr int DB = D / 32;                      // 32-row blocks of O^T
-  constexpr int NLD = kBK * P::NCH / kNT;         // chunks per thread per tensor
-  static_assert(NLD >= 1, "tile too small for the workgroup");
-  constexpr int TB = P::tile_bytes(kBK);
-  __shared__ __attribute__((aligned(16))) unsigned char lds[2][2 * TB];
-
-  int head, qt;
-  if (!map_tile(a.map, blockIdx.x, head, qt, true)) return;
-  const int T = a.T;
-  const int64_t st = a.st;
-  const int64_t hoff = (int64_t)(head / a.H) * a.sb + (int64_t)(head % a.H) * a.sh;
-  const E* q = (const E*)a.q + hoff;
-  const E* k = (const E*)a.k + hoff;
-  const E* v = (const E*)a.v + hoff;
-  E* o = (E*)a.o + hoff;
-
-  const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
-  const Lane L(tid & 63);
   const int i0 = qt * kBQ, qr0 = i0 + 32 * w, qi = qr0 + L.n;
   const bool wave_live = qr0 < T;
   const float c = a.scale * kLog2e;
 
+  // the head's K and V rows; keys past T read as zeros (they only meet masked
+  // weights). The host keeps one head within 2 GiB.
+  const int row_bytes = (int)(st * (int64_t)sizeof(E));
+  const __amdgpu_buffer_rsrc_t krs = make_rsrc(k, T * row_bytes);
+  const __amdgpu_buffer_rsrc_t vrs = make_rsrc(v, T * row_bytes);
+  auto load_tile = [&](int j0, int buf) {
+#pragma unroll
+    for (int s = 0; s < SEGW; ++s) {
+      const int seg = w * SEGW + s, tens = seg / NSEG;
+      dma_segment<P>(tens ? vrs : krs, lds[buf] + tens * TB, seg % NSEG, row_bytes, j0, lane);
+    }
+  };
+
   Op qhi[KS], qlo[KS];
   load_query<P, KS, QM>(q, st, qi, T, L, c, qhi, qlo);
-
-  Chunk kreg[NLD], vreg[NLD];
-  auto prefetch = [&](int j0) {
-#pragma unroll
-    for (int j = 0; j < NLD; ++j) {
-      const int ci = tid + kNT * j, row = ci / P::NCH, ch = ci % P::NCH, key = j0 + row;
-      if (key < T) {
-        kreg[j] = *(const Chunk*)(k + key * st + P::CE * ch);
-        vreg[j] = *(const Chunk*)(v + key * st + P::CE * ch);
-      } else {
-        kreg[j] = Chunk{};
-        vreg[j] = Chunk{};
-      }
-    }
-  };
-  auto stage = [&](int buf) {
-#pragma unroll
-    for (int j = 0; j < NLD; ++j) {
-      const int ci = tid + kNT * j, row = ci / P::NCH, ch = ci % P::NCH;
-      P::stage(lds[buf], row, ch, kreg[j]);
-      P::stage(lds[buf] + TB, row, ch, vreg[j]);
-    }
-  };
 
   float m = 0.0f, l = 0.0f, uii = 0.0f;
   floatx16 oacc[DB];
@@ -432,33 +293,23 @@ __global__ __launch_bounds__(kNT, REL_FWD_WAVES_PER_SIMD) void fwd_kernel(FwdArg
 
   const int kmax = min(i0 + kBQ, T) - 1;  // the diagonal of the last row is included
   const int nkt = kmax / kBK + 1;
-  prefetch(0);
-  stage(0);
-  if (nkt > 1) prefetch(kBK);
-  __syncthreads();
+  load_tile(0, 0);
   for (int kt = 0; kt < nkt; ++kt) {
+    wait_loads();      // this wave's part of tile kt is in LDS
+    __syncthreads();   // ... and every wave's; tile kt-1 is no longer read
+    if (kt + 1 < nkt) load_tile((kt + 1) * kBK, (kt + 1) & 1);
     if (wave_live) {
       const unsigned char* Ks = lds[kt & 1];
       scan_keys64<P, D, QM>(Ks, Ks + TB, 0, kt * kBK, qr0, qhi, qlo, oacc, m, l, uii, L, c);
-    }
-    if (kt + 1 < nkt) {
-      stage((kt + 1) & 1);
-      __syncthreads();
-      if (kt + 2 < nkt) prefetch((kt + 2) * kBK);
     }
   }
   if (!wave_live) return;
   finish_row<P, D, QM>(a, o, v, st, head, qi, m, l, uii, oacc, L, c);
 }
 
-template <int D>
-void launch_bf16(const FwdArgs& a, hipStream_t stream) {
-  constexpr int NW = REL_FWD_BF16_WAVES;
-  hipLaunchKernelGGL((fwdb_kernel<D, NW>), dim3((unsigned)grid_size(a.map)), dim3(NW * 64), 0, stream, a);
-}
-template <int D>
-void launch_f32(const FwdArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL((fwd_kernel<PolF32<D>, D>), dim3((unsigned)grid_size(a.map)), dim3(kNT), 0, stream, a);
+template <class P, int D>
+void launch_one(const FwdArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL((fwd_kernel<P, D>), dim3((unsigned)grid_size(a.map)), dim3(kNT), 0, stream, a);
 }
 
 }  // namespace
@@ -470,13 +321,13 @@ hipError_t launch_fwd(const FwdArgs& a0, int dtype, int D, hipStream_t stream) {
   const bool prof = profile_slot("fwd", &ev0, &ev1);
   if (prof) (void)hipEventRecord(ev0, stream);
   if (dtype == 1) {
-    if (D == 32) launch_bf16<32>(a, stream);
-    else if (D == 64) launch_bf16<64>(a, stream);
-    else launch_bf16<128>(a, stream);
+    if (D == 32) launch_one<PolBF16<32>, 32>(a, stream);
+    else if (D == 64) launch_one<PolBF16<64>, 64>(a, stream);
+    else launch_one<PolBF16<128>, 128>(a, stream);
   } else {
-    if (D == 32) launch_f32<32>(a, stream);
-    else if (D == 64) launch_f32<64>(a, stream);
-    else launch_f32<128>(a, stream);
+    if (D == 32) launch_one<PolF32<32>, 32>(a, stream);
+    else if (D == 64) launch_one<PolF32<64>, 64>(a, stream);
+    else launch_one<PolF32<128>, 128>(a, stream);
   }
   hipError_t e = hipGetLastError();
   if (prof) (void)hipEventRecord(ev1, stream);

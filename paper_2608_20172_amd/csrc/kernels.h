@@ -39,7 +39,8 @@ struct BwdArgs {
   void* dk;
   void* dv;
   float* dlam_part;  // one partial per dQ-kernel workgroup slot
-  float* dvec;       // D_i = dO_i . o_i, [N, T], written by the dQ kernel
+  float* negd;       // -D_i = -dO_i . o_i, [N, T], written by the dQ kernel
+  float* m2;         // M_i log2(e), [N, T], written by the dQ kernel
   float* dself;      // optional [N, T]
   int64_t sb, sh, st;
   int H, T;

@@ -319,7 +319,7 @@ size_t relation_bwd_workspace_bytes(const rel_problem* p) {
   if (check_problem(p, &empty) != REL_OK) return 0;
   if (empty) return 0;
   const size_t N = (size_t)(p->B * p->H);
-  return align256(N * (size_t)p->T * 4) +
+  return 2 * align256(N * (size_t)p->T * 4) +
          align256((size_t)rel::bwd_partials((int)N, (int)p->T, (int)p->D, p->dtype) * 4);
 }
 
@@ -375,8 +375,10 @@ rel_status relation_bwd(const rel_problem* p, const void* q, const void* k, cons
   rel::BwdArgs a{};
   a.q = q; a.k = k; a.v = v; a.o = o; a.dout = dout; a.lambda = lambda; a.row_stat = row_stat;
   a.dq = dq; a.dk = dk; a.dv = dv; a.dself = dself;
-  a.dvec = (float*)workspace;
-  a.dlam_part = (float*)((char*)workspace + align256(N * (size_t)p->T * 4));
+  const size_t rowv = align256(N * (size_t)p->T * 4);
+  a.negd = (float*)workspace;
+  a.m2 = (float*)((char*)workspace + rowv);
+  a.dlam_part = (float*)((char*)workspace + 2 * rowv);
   a.sb = p->stride_b; a.sh = p->stride_h; a.st = p->stride_t;
   a.H = (int)p->H; a.T = (int)p->T;
   a.scale = eff_scale(p);
