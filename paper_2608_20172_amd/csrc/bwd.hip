@@ -188,9 +188,10 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
   for (int db = 0; db < DB; ++db) dQt[db] = floatx16{};
   float dlam = 0.0f;
 
-  // one 32-key block (krow0 .. krow0+31 of the tile); DIAG: the wave's own
-  // diagonal block (key offset acc_row(r, g) against row offset n)
-  auto block = [&](const unsigned char* Ks, const unsigned char* Vs, int krow0, auto diag_c) {
+  // dU of one 32-key block (krow0 .. krow0+31 of the tile), packed as the
+  // operands of its two 16-key halves; DIAG: the wave's own diagonal block
+  // (key offset acc_row(r, g) against row offset n)
+  auto block = [&](const unsigned char* Ks, const unsigned char* Vs, int krow0, Op (&uop)[2], auto diag_c) {
     constexpr bool DIAG = decltype(diag_c)::value;
     const int row = krow0 + n;
     floatx16 s = {}, dp = negD;
@@ -230,38 +231,37 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
         if (a.dself) a.dself[(int64_t)head * T + qi] = sg.dR;
       }
     }
-    const int ks0 = krow0 / 16;
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
       float u8[8];
 #pragma unroll
       for (int t = 0; t < 8; ++t) u8[t] = dp[8 * hh + t];
-      const Op uop = P::pack(u8);
-#pragma unroll
-      for (int db = 0; db < DB; ++db) dQt[db] = P::mma(P::col_op(Ks, ks0 + hh, 32 * db, L), uop, dQt[db]);
+      uop[hh] = P::pack(u8);
     }
   };
 
   const int kmax = min(i0 + kBQ, T) - 1;
   const int nkt = kmax / kBK + 1;
+  const int qlast = wave_live ? qr0 : -1;  // rows of a wave past T meet no key
   for (int kt = 0; kt < nkt; ++kt) {
     wait_loads();
     __syncthreads();
     if (kt + 1 < nkt) load_tile((kt + 1) * kBK, (kt + 1) & 1);
-    if (!wave_live) continue;
     const unsigned char* Ks = lds[kt & 1];
     const unsigned char* Vs = Ks + TB;
     const int j0 = kt * kBK;
-    using F0 = std::false_type;
-    using T1 = std::true_type;
-    if (j0 + 64 <= qr0) {
-      block(Ks, Vs, 0, F0{});
-      block(Ks, Vs, 32, F0{});
-    } else if (j0 + 32 == qr0) {
-      block(Ks, Vs, 0, F0{});
-      block(Ks, Vs, 32, T1{});
-    } else if (j0 == qr0) {
-      block(Ks, Vs, 0, T1{});
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      // a block at or above the wave's rows contributes zero dU, so the dQ
+      // products (and the accumulators) run on every path
+      const int kb0 = j0 + 32 * b;
+      Op uop[2] = {Op{}, Op{}};
+      if (kb0 < qlast) block(Ks, Vs, 32 * b, uop, std::false_type{});
+      else if (kb0 == qlast) block(Ks, Vs, 32 * b, uop, std::true_type{});
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+        for (int db = 0; db < DB; ++db) dQt[db] = P::mma(P::col_op(Ks, 2 * b + hh, 32 * db, L), uop[hh], dQt[db]);
     }
   }
 
@@ -358,9 +358,10 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
     dVt[db] = floatx16{};
   }
 
-  // one 32-row query block qb of the tile; DIAG: the block whose rows start at
-  // this wave's first key (row offset acc_row(r, g) against key offset n)
-  auto block = [&](const unsigned char* buf, int qb, auto diag_c) {
+  // F and dU of one 32-row query block qb of the tile, packed as the operands
+  // of its two 16-row halves; DIAG: the block whose rows start at this wave's
+  // first key (row offset acc_row(r, g) against key offset n)
+  auto block = [&](const unsigned char* buf, int qb, Op (&fop)[2], Op (&uop)[2], auto diag_c) {
     constexpr bool DIAG = decltype(diag_c)::value;
     const unsigned char* Qs = buf;
     const unsigned char* dOs = buf + TB;
@@ -426,32 +427,35 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
         f8[t] = s[8 * hh + t];
         u8[t] = dp[8 * hh + t];
       }
-      const Op fop = P::pack(f8);
-      const Op uop = P::pack(u8);
-      const int ks = 2 * qb + hh;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        dVt[db] = P::mma(P::col_op(dOs, ks, 32 * db, L), fop, dVt[db]);
-        dKt[db] = P::mma(P::col_op(Qs, ks, 32 * db, L), uop, dKt[db]);
-      }
+      fop[hh] = P::pack(f8);
+      uop[hh] = P::pack(u8);
     }
   };
 
+  const int kfirst = wave_keys ? kw0 : (1 << 30);  // a wave past T meets no query
   for (int qt = qt0; qt < nqt; ++qt) {
     const int i0 = qt * kBQI;
     wait_loads();
     __syncthreads();
     if (qt + 1 < nqt) load_tile(i0 + kBQI, (qt + 1 - qt0) & 1);
-    if (!wave_keys) continue;
     const unsigned char* buf = lds[(qt - qt0) & 1];
-    using F0 = std::false_type;
-    using T1 = std::true_type;
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
+      // a block before the wave's keys or past T contributes zero F and dU,
+      // so the dV / dK products (and the accumulators) run on every path
       const int qb0 = i0 + 32 * qb;
-      if (qb0 < kw0 || qb0 >= T) continue;  // no row of the block reaches a key of the wave
-      if (qb0 == kw0) block(buf, qb, T1{});
-      else block(buf, qb, F0{});
+      Op fop[2] = {Op{}, Op{}}, uop[2] = {Op{}, Op{}};
+      if (qb0 > kfirst && qb0 < T) block(buf, qb, fop, uop, std::false_type{});
+      else if (qb0 == kfirst) block(buf, qb, fop, uop, std::true_type{});
+      const unsigned char* Qs = buf;
+      const unsigned char* dOs = buf + TB;
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          dVt[db] = P::mma(P::col_op(dOs, 2 * qb + hh, 32 * db, L), fop[hh], dVt[db]);
+          dKt[db] = P::mma(P::col_op(Qs, 2 * qb + hh, 32 * db, L), uop[hh], dKt[db]);
+        }
     }
   }
 

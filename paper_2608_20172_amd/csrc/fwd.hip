@@ -129,26 +129,77 @@ __device__ __forceinline__ floatx16 evidence(const unsigned char* Ks, int krow0,
   return s;
 }
 
-// The 64 keys krow0 .. krow0+63 of a tile (two 32-key blocks) for a wave whose
-// rows start at qr0 and whose keys start at kglob (global index of krow0).
+// Common-case block: the logits of the block, then, if none exceeds the
+// running reference by more than kRescale, the packed weights P of its two
+// 16-key halves and their sum into l. Returns false (and changes neither l nor
+// pop) when the reference has to be raised first.
+template <class P, int D, int QM, bool DIAG>
+__device__ __forceinline__ bool fast_block(floatx16 s, float m, float& l, float& uii, typename P::Op (&pop)[2],
+                                           const Lane& L, float c) {
+  if (DIAG && holds_row(L.n, L.g)) uii = pick(s, row_reg(L.n));  // the Self evidence
+  float mx = kNegInf;
+  exchange_logits<DIAG, QM>(s, L, c, m, mx);
+  if (wave_any(mx > kRescale)) return false;
+  // l sums the fp32 p (not the bf16-rounded MFMA operand), so that L^E and the
+  // saved statistic M carry no operand rounding
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    float p[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      p[t] = fast_exp2(s[8 * hh + t]);
+      l += p[t];
+    }
+    pop[hh] = P::pack(p);
+  }
+  return true;
+}
+
+// The 64 keys krow0 .. krow0+63 of a tile (two 32-key blocks, the first at
+// global key kglob) for a wave whose rows start at qr0, without moving the
+// running reference. A block above the wave's rows contributes zero weights,
+// so the P V products (and the accumulators) run on every path. Returns -1,
+// or the first block that needs the reference raised (not accumulated).
 template <class P, int D, int QM>
-__device__ __forceinline__ void scan_keys64(const unsigned char* Ks, const unsigned char* Vs, int krow0, int kglob,
-                                            int qr0, const typename P::Op (&qhi)[D / 16],
+__device__ __forceinline__ int fast_keys64(const unsigned char* Ks, const unsigned char* Vs, int krow0, int kglob,
+                                           int qr0, const typename P::Op (&qhi)[D / 16],
+                                           const typename P::Op (&qlo)[D / 16], floatx16 (&oacc)[D / 32], float m,
+                                           float& l, float& uii, const Lane& L, float c) {
+  constexpr int KS = D / 16, DB = D / 32;
+  using Op = typename P::Op;
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    const int kb0 = kglob + 32 * b;
+    Op pop[2] = {Op{}, Op{}};
+    if (kb0 <= qr0) {
+      const floatx16 s = evidence<P, KS, QM>(Ks, krow0 + 32 * b, qhi, qlo, L);
+      const bool ok = kb0 == qr0 ? fast_block<P, D, QM, true>(s, m, l, uii, pop, L, c)
+                                 : fast_block<P, D, QM, false>(s, m, l, uii, pop, L, c);
+      if (!ok) return b;
+    }
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+        oacc[db] = P::mma(P::col_op(Vs, krow0 / 16 + 2 * b + hh, 32 * db, L), pop[hh], oacc[db]);
+  }
+  return -1;
+}
+
+// The same 64 keys from block b0 on, raising the running reference as needed
+// (taken once a block has exceeded it; rare).
+template <class P, int D, int QM>
+__device__ __forceinline__ void slow_keys64(const unsigned char* Ks, const unsigned char* Vs, int krow0, int kglob,
+                                            int qr0, int b0, const typename P::Op (&qhi)[D / 16],
                                             const typename P::Op (&qlo)[D / 16], floatx16 (&oacc)[D / 32], float& m,
                                             float& l, float& uii, const Lane& L, float c) {
   constexpr int KS = D / 16;
-  const int vs0 = krow0 / 16;
-  // one block at a time: the evidence of block 1 is formed only after block 0
-  // is mapped, which keeps the register footprint small enough for four
-  // waves per SIMD (the other waves fill the matrix-core latency)
-  if (kglob + 64 <= qr0) {  // both blocks before every row: the common case
-    scan_block<P, D, QM, false>(evidence<P, KS, QM>(Ks, krow0, qhi, qlo, L), oacc, m, l, uii, Vs, vs0, L, c);
-    scan_block<P, D, QM, false>(evidence<P, KS, QM>(Ks, krow0 + 32, qhi, qlo, L), oacc, m, l, uii, Vs, vs0 + 2, L, c);
-  } else if (kglob + 32 == qr0) {  // block 1 is the diagonal block
-    scan_block<P, D, QM, false>(evidence<P, KS, QM>(Ks, krow0, qhi, qlo, L), oacc, m, l, uii, Vs, vs0, L, c);
-    scan_block<P, D, QM, true>(evidence<P, KS, QM>(Ks, krow0 + 32, qhi, qlo, L), oacc, m, l, uii, Vs, vs0 + 2, L, c);
-  } else if (kglob == qr0) {  // block 0 is the diagonal block, block 1 lies above it
-    scan_block<P, D, QM, true>(evidence<P, KS, QM>(Ks, krow0, qhi, qlo, L), oacc, m, l, uii, Vs, vs0, L, c);
+  for (int b = b0; b < 2; ++b) {
+    const int kb0 = kglob + 32 * b;
+    if (kb0 > qr0) break;
+    const floatx16 s = evidence<P, KS, QM>(Ks, krow0 + 32 * b, qhi, qlo, L);
+    if (kb0 == qr0) scan_block<P, D, QM, true>(s, oacc, m, l, uii, Vs, krow0 / 16 + 2 * b, L, c);
+    else scan_block<P, D, QM, false>(s, oacc, m, l, uii, Vs, krow0 / 16 + 2 * b, L, c);
   }
 }
 
@@ -294,13 +345,28 @@ __global__ __launch_bounds__(kNT, (fwd_occupancy<P, D>())) void fwd_kernel(FwdAr
   const int kmax = min(i0 + kBQ, T) - 1;  // the diagonal of the last row is included
   const int nkt = kmax / kBK + 1;
   load_tile(0, 0);
-  for (int kt = 0; kt < nkt; ++kt) {
+  int kt = 0, resume = -1;
+  for (; kt < nkt; ++kt) {
     wait_loads();      // this wave's part of tile kt is in LDS
     __syncthreads();   // ... and every wave's; tile kt-1 is no longer read
     if (kt + 1 < nkt) load_tile((kt + 1) * kBK, (kt + 1) & 1);
     if (wave_live) {
       const unsigned char* Ks = lds[kt & 1];
-      scan_keys64<P, D, QM>(Ks, Ks + TB, 0, kt * kBK, qr0, qhi, qlo, oacc, m, l, uii, L, c);
+      resume = fast_keys64<P, D, QM>(Ks, Ks + TB, 0, kt * kBK, qr0, qhi, qlo, oacc, m, l, uii, L, c);
+      if (resume >= 0) break;
+    }
+  }
+  if (resume >= 0) {
+    // a block exceeded the running reference: finish the scan with rescaling,
+    // passing the same barriers as the rest of the workgroup
+    const unsigned char* Ks = lds[kt & 1];
+    slow_keys64<P, D, QM>(Ks, Ks + TB, 0, kt * kBK, qr0, resume, qhi, qlo, oacc, m, l, uii, L, c);
+    for (++kt; kt < nkt; ++kt) {
+      wait_loads();
+      __syncthreads();
+      if (kt + 1 < nkt) load_tile((kt + 1) * kBK, (kt + 1) & 1);
+      const unsigned char* Kt = lds[kt & 1];
+      slow_keys64<P, D, QM>(Kt, Kt + TB, 0, kt * kBK, qr0, 0, qhi, qlo, oacc, m, l, uii, L, c);
     }
   }
   if (!wave_live) return;
