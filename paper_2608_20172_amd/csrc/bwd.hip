@@ -122,7 +122,10 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
   constexpr int NSEG = TB / 1024;
   constexpr int SEGW = 2 * NSEG / 4;
   static_assert(SEGW >= 1 && 2 * NSEG % 4 == 0, "tile does not split over the waves");
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[2][2 * TB];
+  // two tile buffers as distinct objects: the compiler can then see that
+  // reads of one do not wait for the loads in flight into the other
+  __shared__ __attribute__((aligned(1024))) unsigned char bufA[2 * TB];
+  __shared__ __attribute__((aligned(1024))) unsigned char bufB[2 * TB];
   __shared__ float red[kNT / 64];
 
   const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
@@ -152,14 +155,14 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
   const int row_bytes = (int)(st * (int64_t)sizeof(E));
   const __amdgpu_buffer_rsrc_t krs = make_rsrc(k, T * row_bytes);
   const __amdgpu_buffer_rsrc_t vrs = make_rsrc(v, T * row_bytes);
-  auto load_tile = [&](int j0, int buf) {
+  auto load_tile = [&](int j0, unsigned char* buf) {
 #pragma unroll
     for (int s = 0; s < SEGW; ++s) {
       const int seg = w * SEGW + s, tens = seg / NSEG;
-      dma_segment<P>(tens ? vrs : krs, lds[buf] + tens * TB, seg % NSEG, row_bytes, j0, lane);
+      dma_segment<P>(tens ? vrs : krs, buf + tens * TB, seg % NSEG, row_bytes, j0, lane);
     }
   };
-  load_tile(0, 0);
+  load_tile(0, bufA);
 
   // B operands: this lane's query row of Q and dO; D_i = dO_i . O_i from the
   // same slices, completed across the two lane halves
@@ -243,11 +246,10 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
   const int kmax = min(i0 + kBQ, T) - 1;
   const int nkt = kmax / kBK + 1;
   const int qlast = wave_live ? qr0 : -1;  // rows of a wave past T meet no key
-  for (int kt = 0; kt < nkt; ++kt) {
+  auto step = [&](int kt, const unsigned char* Ks, unsigned char* nxt) {
     wait_loads();
     __syncthreads();
-    if (kt + 1 < nkt) load_tile((kt + 1) * kBK, (kt + 1) & 1);
-    const unsigned char* Ks = lds[kt & 1];
+    if (kt + 1 < nkt) load_tile((kt + 1) * kBK, nxt);
     const unsigned char* Vs = Ks + TB;
     const int j0 = kt * kBK;
 #pragma unroll
@@ -263,6 +265,10 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
 #pragma unroll
         for (int db = 0; db < DB; ++db) dQt[db] = P::mma(P::col_op(Ks, 2 * b + hh, 32 * db, L), uop[hh], dQt[db]);
     }
+  };
+  for (int kt = 0; kt < nkt; kt += 2) {  // even tiles in bufA, odd ones in bufB
+    step(kt, bufA, bufB);
+    if (kt + 1 < nkt) step(kt + 1, bufB, bufA);
   }
 
   if (wave_live && row_ok) {
@@ -300,7 +306,10 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
   constexpr int SEGW = 2 * NSEG / 4;
   static_assert(SEGW >= 1 && 2 * NSEG % 4 == 0, "tile does not split over the waves");
   constexpr int BUF = 2 * TB + 2 * kBQI * 4;    // Q, dO, M log2(e), -D
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[2][BUF];
+  // two tile buffers as distinct objects: the compiler can then see that
+  // reads of one do not wait for the loads in flight into the other
+  __shared__ __attribute__((aligned(1024))) unsigned char bufA[BUF];
+  __shared__ __attribute__((aligned(1024))) unsigned char bufB[BUF];
 
   const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int lane = tid & 63;
@@ -330,18 +339,18 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
   const __amdgpu_buffer_rsrc_t drs = make_rsrc(dO, T * row_bytes);
   const __amdgpu_buffer_rsrc_t mrs = make_rsrc(a.m2 + (int64_t)head * T, T * 4);
   const __amdgpu_buffer_rsrc_t nrs = make_rsrc(a.negd + (int64_t)head * T, T * 4);
-  auto load_tile = [&](int i0, int buf) {
+  auto load_tile = [&](int i0, unsigned char* buf) {
 #pragma unroll
     for (int s = 0; s < SEGW; ++s) {
       const int seg = w * SEGW + s, tens = seg / NSEG;
-      dma_segment<P>(tens ? drs : qrs, lds[buf] + tens * TB, seg % NSEG, row_bytes, i0, lane);
+      dma_segment<P>(tens ? drs : qrs, buf + tens * TB, seg % NSEG, row_bytes, i0, lane);
     }
-    if (w < 2) dma_row64(w ? nrs : mrs, (float*)(lds[buf] + 2 * TB) + w * kBQI, i0, lane);
+    if (w < 2) dma_row64(w ? nrs : mrs, (float*)(buf + 2 * TB) + w * kBQI, i0, lane);
   };
 
   const int nqt = (T + kBQI - 1) / kBQI;
   const int qt0 = j0 / kBQI;
-  load_tile(qt0 * kBQI, 0);
+  load_tile(qt0 * kBQI, bufA);
 
   // B operands of U = Q K^T and dP = dO V^T: this lane's key row
   Op kop[KS], vop[KS];
@@ -433,12 +442,11 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
   };
 
   const int kfirst = wave_keys ? kw0 : (1 << 30);  // a wave past T meets no query
-  for (int qt = qt0; qt < nqt; ++qt) {
+  auto step = [&](int qt, const unsigned char* buf, unsigned char* nxt) {
     const int i0 = qt * kBQI;
     wait_loads();
     __syncthreads();
-    if (qt + 1 < nqt) load_tile(i0 + kBQI, (qt + 1 - qt0) & 1);
-    const unsigned char* buf = lds[(qt - qt0) & 1];
+    if (qt + 1 < nqt) load_tile(i0 + kBQI, nxt);
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       // a block before the wave's keys or past T contributes zero F and dU,
@@ -457,6 +465,10 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
           dKt[db] = P::mma(P::col_op(Qs, 2 * qb + hh, 32 * db, L), uop[hh], dKt[db]);
         }
     }
+  };
+  for (int qt = qt0; qt < nqt; qt += 2) {  // tiles alternate: bufA, bufB
+    step(qt, bufA, bufB);
+    if (qt + 1 < nqt) step(qt + 1, bufB, bufA);
   }
 
   if (kj < T) {

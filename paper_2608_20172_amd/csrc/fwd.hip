@@ -300,9 +300,14 @@ __global__ __launch_bounds__(kNT, (fwd_occupancy<P, D>())) void fwd_kernel(FwdAr
   constexpr int KS = D / 16, DB = D / 32;
   constexpr int TB = kBK * P::ROWB;            // bytes of one tensor tile
   constexpr int NSEG = TB / 1024;              // 1 KB loads per tensor tile
-  constexpr int SEGW = 2 * NSEG / 4;           // per wave, K and V together
-  static_assert(SEGW >= 1 && 2 * NSEG % 4 == 0, "tile does not split over the waves");
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[2][2 * TB];
+  constexpr int SEGW = NSEG / 4;               // per wave and tensor
+  static_assert(SEGW >= 1 && NSEG % 4 == 0, "tile does not split over the waves");
+  // K and V tiles, two of each, as distinct objects: the compiler can then see
+  // that reads of one do not wait for the loads in flight into another
+  __shared__ __attribute__((aligned(1024))) unsigned char KA[TB];
+  __shared__ __attribute__((aligned(1024))) unsigned char VA[TB];
+  __shared__ __attribute__((aligned(1024))) unsigned char KB[TB];
+  __shared__ __attribute__((aligned(1024))) unsigned char VB[TB];
 
   int head, qt;
   if (!map_tile(a.map, blockIdx.x, head, qt, true)) return;
@@ -326,11 +331,11 @@ __global__ __launch_bounds__(kNT, (fwd_occupancy<P, D>())) void fwd_kernel(FwdAr
   const int row_bytes = (int)(st * (int64_t)sizeof(E));
   const __amdgpu_buffer_rsrc_t krs = make_rsrc(k, T * row_bytes);
   const __amdgpu_buffer_rsrc_t vrs = make_rsrc(v, T * row_bytes);
-  auto load_tile = [&](int j0, int buf) {
+  auto load_tile = [&](int j0, unsigned char* Kd, unsigned char* Vd) {
 #pragma unroll
     for (int s = 0; s < SEGW; ++s) {
-      const int seg = w * SEGW + s, tens = seg / NSEG;
-      dma_segment<P>(tens ? vrs : krs, lds[buf] + tens * TB, seg % NSEG, row_bytes, j0, lane);
+      dma_segment<P>(krs, Kd, w * SEGW + s, row_bytes, j0, lane);
+      dma_segment<P>(vrs, Vd, w * SEGW + s, row_bytes, j0, lane);
     }
   };
 
@@ -344,29 +349,41 @@ __global__ __launch_bounds__(kNT, (fwd_occupancy<P, D>())) void fwd_kernel(FwdAr
 
   const int kmax = min(i0 + kBQ, T) - 1;  // the diagonal of the last row is included
   const int nkt = kmax / kBK + 1;
-  load_tile(0, 0);
-  int kt = 0, resume = -1;
-  for (; kt < nkt; ++kt) {
+  // Tiles alternate between the buffers: even ones in KA/VA, odd ones in
+  // KB/VB. A fast step returns the block that needs the running reference
+  // raised, or -1.
+  const int qlast = wave_live ? qr0 : -1;  // rows of a wave past T meet no key
+  auto fast_step = [&](int kt, const unsigned char* Ks, const unsigned char* Vs, unsigned char* Kn,
+                       unsigned char* Vn) {
     wait_loads();      // this wave's part of tile kt is in LDS
     __syncthreads();   // ... and every wave's; tile kt-1 is no longer read
-    if (kt + 1 < nkt) load_tile((kt + 1) * kBK, (kt + 1) & 1);
-    if (wave_live) {
-      const unsigned char* Ks = lds[kt & 1];
-      resume = fast_keys64<P, D, QM>(Ks, Ks + TB, 0, kt * kBK, qr0, qhi, qlo, oacc, m, l, uii, L, c);
-      if (resume >= 0) break;
+    if (kt + 1 < nkt) load_tile((kt + 1) * kBK, Kn, Vn);
+    return fast_keys64<P, D, QM>(Ks, Vs, 0, kt * kBK, qlast, qhi, qlo, oacc, m, l, uii, L, c);
+  };
+  load_tile(0, KA, VA);
+  int kt = 0, resume = -1;
+  for (; kt < nkt; kt += 2) {
+    resume = fast_step(kt, KA, VA, KB, VB);
+    if (resume >= 0) break;
+    if (kt + 1 < nkt) {
+      resume = fast_step(kt + 1, KB, VB, KA, VA);
+      if (resume >= 0) {
+        ++kt;
+        break;
+      }
     }
   }
   if (resume >= 0) {
     // a block exceeded the running reference: finish the scan with rescaling,
     // passing the same barriers as the rest of the workgroup
-    const unsigned char* Ks = lds[kt & 1];
-    slow_keys64<P, D, QM>(Ks, Ks + TB, 0, kt * kBK, qr0, resume, qhi, qlo, oacc, m, l, uii, L, c);
+    slow_keys64<P, D, QM>((kt & 1) ? KB : KA, (kt & 1) ? VB : VA, 0, kt * kBK, qlast, resume, qhi, qlo, oacc, m,
+                          l, uii, L, c);
     for (++kt; kt < nkt; ++kt) {
+      const bool odd = kt & 1;
       wait_loads();
       __syncthreads();
-      if (kt + 1 < nkt) load_tile((kt + 1) * kBK, (kt + 1) & 1);
-      const unsigned char* Kt = lds[kt & 1];
-      slow_keys64<P, D, QM>(Kt, Kt + TB, 0, kt * kBK, qr0, 0, qhi, qlo, oacc, m, l, uii, L, c);
+      if (kt + 1 < nkt) load_tile((kt + 1) * kBK, odd ? KA : KB, odd ? VA : VB);
+      slow_keys64<P, D, QM>(odd ? KB : KA, odd ? VB : VA, 0, kt * kBK, qlast, 0, qhi, qlo, oacc, m, l, uii, L, c);
     }
   }
   if (!wave_live) return;
