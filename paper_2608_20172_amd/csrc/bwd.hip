@@ -44,6 +44,9 @@ constexpr int kNT = 256;
 #ifndef REL_DQ_NEGD_SEED
 #define REL_DQ_NEGD_SEED 0  // dQ: 1 = the dP chains start from -D_i (16 registers); 0 = subtract D_i per entry
 #endif
+#ifndef REL_DQ_PIPELINE
+#define REL_DQ_PIPELINE 0  // dQ: 1 = evidence of block 1 before the products of block 0 (needs 2 waves per SIMD)
+#endif
 #ifndef REL_DQ_OPERAND_BATCH
 #define REL_DQ_OPERAND_BATCH 1
 #endif
@@ -191,13 +194,12 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
   for (int db = 0; db < DB; ++db) dQt[db] = floatx16{};
   float dlam = 0.0f;
 
-  // dU of one 32-key block (krow0 .. krow0+31 of the tile), packed as the
-  // operands of its two 16-key halves; DIAG: the wave's own diagonal block
-  // (key offset acc_row(r, g) against row offset n)
-  auto block = [&](const unsigned char* Ks, const unsigned char* Vs, int krow0, Op (&uop)[2], auto diag_c) {
-    constexpr bool DIAG = decltype(diag_c)::value;
+  // Key block (keys krow0 .. krow0+31 of the tile): the evidence and dP - D
+  // chains on the matrix cores ...
+  auto evid = [&](const unsigned char* Ks, const unsigned char* Vs, int krow0, floatx16& s, floatx16& dp) {
     const int row = krow0 + n;
-    floatx16 s = {}, dp = negD;
+    s = floatx16{};
+    dp = negD;
     constexpr int NB = REL_DQ_OPERAND_BATCH;  // K/V operand slices read per batch
 #pragma unroll
     for (int k0 = 0; k0 < KS; k0 += NB) {
@@ -213,6 +215,12 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
         dp = P::mma(va[j], doop[k0 + j], dp);  // dP - D
       }
     }
+  };
+  // ... then dU on the vector units, packed as the operands of the two 16-key
+  // halves; DIAG: the wave's own diagonal block (key offset acc_row(r, g)
+  // against row offset n)
+  auto grads = [&](floatx16& s, floatx16& dp, Op (&uop)[2], auto diag_c) {
+    constexpr bool DIAG = decltype(diag_c)::value;
     float uself = 0.0f, dself = 0.0f;
     const int rs = row_reg(n);
     if (DIAG) {
@@ -242,29 +250,60 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
       uop[hh] = P::pack(u8);
     }
   };
+  // dQ^T += K^T dU^T for key block b of the tile
+  auto accum = [&](const unsigned char* Ks, int b, const Op (&uop)[2]) {
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+      for (int db = 0; db < DB; ++db) dQt[db] = P::mma(P::col_op(Ks, 2 * b + hh, 32 * db, L), uop[hh], dQt[db]);
+  };
 
   const int kmax = min(i0 + kBQ, T) - 1;
   const int nkt = kmax / kBK + 1;
   const int qlast = wave_live ? qr0 : -1;  // rows of a wave past T meet no key
+  // One key tile. A block at or above the wave's rows contributes zero dU, so
+  // the dQ products (and the accumulators) run on every path. Order: evidence
+  // of block 0, its vector work, evidence of block 1, then the products of
+  // block 0 (which run under the vector work of block 1).
   auto step = [&](int kt, const unsigned char* Ks, unsigned char* nxt) {
     wait_loads();
     __syncthreads();
     if (kt + 1 < nkt) load_tile((kt + 1) * kBK, nxt);
     const unsigned char* Vs = Ks + TB;
-    const int j0 = kt * kBK;
+    const int k0 = kt * kBK, k1 = k0 + 32;
+    if (!REL_DQ_PIPELINE) {
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      // a block at or above the wave's rows contributes zero dU, so the dQ
-      // products (and the accumulators) run on every path
-      const int kb0 = j0 + 32 * b;
-      Op uop[2] = {Op{}, Op{}};
-      if (kb0 < qlast) block(Ks, Vs, 32 * b, uop, std::false_type{});
-      else if (kb0 == qlast) block(Ks, Vs, 32 * b, uop, std::true_type{});
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-        for (int db = 0; db < DB; ++db) dQt[db] = P::mma(P::col_op(Ks, 2 * b + hh, 32 * db, L), uop[hh], dQt[db]);
+      for (int b = 0; b < 2; ++b) {
+        const int kb = k0 + 32 * b;
+        Op u[2] = {Op{}, Op{}};
+        floatx16 s, dp;
+        if (kb < qlast) {
+          evid(Ks, Vs, 32 * b, s, dp);
+          grads(s, dp, u, std::false_type{});
+        } else if (kb == qlast) {
+          evid(Ks, Vs, 32 * b, s, dp);
+          grads(s, dp, u, std::true_type{});
+        }
+        accum(Ks, b, u);
+      }
+      return;
     }
+    floatx16 s0, dp0, s1, dp1;
+    Op u0[2] = {Op{}, Op{}}, u1[2] = {Op{}, Op{}};
+    if (k0 <= qlast) {
+      evid(Ks, Vs, 0, s0, dp0);
+      if (k0 == qlast) grads(s0, dp0, u0, std::true_type{});
+      else grads(s0, dp0, u0, std::false_type{});
+    }
+    if (k1 <= qlast) evid(Ks, Vs, 32, s1, dp1);
+    __builtin_amdgcn_sched_barrier(0);
+    accum(Ks, 0, u0);
+    __builtin_amdgcn_sched_barrier(0);
+    if (k1 <= qlast) {
+      if (k1 == qlast) grads(s1, dp1, u1, std::true_type{});
+      else grads(s1, dp1, u1, std::false_type{});
+    }
+    accum(Ks, 1, u1);
   };
   for (int kt = 0; kt < nkt; kt += 2) {  // even tiles in bufA, odd ones in bufB
     step(kt, bufA, bufB);
@@ -367,29 +406,20 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
     dVt[db] = floatx16{};
   }
 
-  // F and dU of one 32-row query block qb of the tile, packed as the operands
-  // of its two 16-row halves; DIAG: the block whose rows start at this wave's
-  // first key (row offset acc_row(r, g) against key offset n)
-  auto block = [&](const unsigned char* buf, int qb, Op (&fop)[2], Op (&uop)[2], auto diag_c) {
-    constexpr bool DIAG = decltype(diag_c)::value;
+  // Query block qb (rows 32 qb .. 32 qb + 31 of the tile): the evidence and
+  // dP - D chains on the matrix cores ...
+  auto evid = [&](const unsigned char* buf, int qb, floatx16& s, floatx16& dp) {
     const unsigned char* Qs = buf;
     const unsigned char* dOs = buf + TB;
-    const float* Mrow = (const float*)(buf + 2 * TB);
-    const float* Nrow = Mrow + kBQI;
+    const float* Nrow = (const float*)(buf + 2 * TB) + kBQI;
     const int row = 32 * qb + n;
-    floatx16 Mb, dp;  // per register: M log2(e) and -D of its query row
 #pragma unroll
-    for (int rq = 0; rq < 4; ++rq) {
-      const int r0 = 32 * qb + 8 * rq + 4 * g;  // tile row of register 4 rq
-      const floatx4 M4 = *(const floatx4*)(Mrow + r0);
-      const floatx4 D4 = *(const floatx4*)(Nrow + r0);
+    for (int rq = 0; rq < 4; ++rq) {  // -D of the query row of every register
+      const floatx4 D4 = *(const floatx4*)(Nrow + 32 * qb + 8 * rq + 4 * g);
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        Mb[4 * rq + t] = M4[t];
-        dp[4 * rq + t] = D4[t];
-      }
+      for (int t = 0; t < 4; ++t) dp[4 * rq + t] = D4[t];
     }
-    floatx16 s = {};
+    s = floatx16{};
 #pragma unroll
     for (int k0 = 0; k0 < KS; k0 += 2) {
       Op qa[2], da[2];
@@ -403,6 +433,21 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
         s = P::mma(qa[j], kop[k0 + j], s);
         dp = P::mma(da[j], vop[k0 + j], dp);  // dP - D
       }
+    }
+  };
+  // ... then F and dU on the vector units, packed as the operands of the two
+  // 16-row halves; DIAG: the block whose rows start at this wave's first key
+  // (row offset acc_row(r, g) against key offset n)
+  auto grads = [&](const unsigned char* buf, int qb, floatx16& s, floatx16& dp, Op (&fop)[2], Op (&uop)[2],
+                   auto diag_c) {
+    constexpr bool DIAG = decltype(diag_c)::value;
+    const float* Mrow = (const float*)(buf + 2 * TB);
+    floatx16 Mb;  // per register: M log2(e) of its query row
+#pragma unroll
+    for (int rq = 0; rq < 4; ++rq) {
+      const floatx4 M4 = *(const floatx4*)(Mrow + 32 * qb + 8 * rq + 4 * g);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) Mb[4 * rq + t] = M4[t];
     }
     float uself = 0.0f, dself = 0.0f;
     const int rs = row_reg(n);
@@ -440,31 +485,47 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
       uop[hh] = P::pack(u8);
     }
   };
+  // dV += F^T dO and dK += dU^T Q for query block qb
+  auto accum = [&](const unsigned char* buf, int qb, const Op (&fop)[2], const Op (&uop)[2]) {
+    const unsigned char* Qs = buf;
+    const unsigned char* dOs = buf + TB;
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        dVt[db] = P::mma(P::col_op(dOs, 2 * qb + hh, 32 * db, L), fop[hh], dVt[db]);
+        dKt[db] = P::mma(P::col_op(Qs, 2 * qb + hh, 32 * db, L), uop[hh], dKt[db]);
+      }
+  };
 
   const int kfirst = wave_keys ? kw0 : (1 << 30);  // a wave past T meets no query
+  // One query tile. A block before the wave's keys or past T contributes zero
+  // F and dU, so the dV / dK products (and the accumulators) run on every
+  // path. Order: evidence of block 0, its vector work, evidence of block 1,
+  // then the products of block 0 (which run under the vector work of block 1).
   auto step = [&](int qt, const unsigned char* buf, unsigned char* nxt) {
     const int i0 = qt * kBQI;
     wait_loads();
     __syncthreads();
     if (qt + 1 < nqt) load_tile(i0 + kBQI, nxt);
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      // a block before the wave's keys or past T contributes zero F and dU,
-      // so the dV / dK products (and the accumulators) run on every path
-      const int qb0 = i0 + 32 * qb;
-      Op fop[2] = {Op{}, Op{}}, uop[2] = {Op{}, Op{}};
-      if (qb0 > kfirst && qb0 < T) block(buf, qb, fop, uop, std::false_type{});
-      else if (qb0 == kfirst) block(buf, qb, fop, uop, std::true_type{});
-      const unsigned char* Qs = buf;
-      const unsigned char* dOs = buf + TB;
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          dVt[db] = P::mma(P::col_op(dOs, 2 * qb + hh, 32 * db, L), fop[hh], dVt[db]);
-          dKt[db] = P::mma(P::col_op(Qs, 2 * qb + hh, 32 * db, L), uop[hh], dKt[db]);
-        }
+    const int q0 = i0, q1 = i0 + 32;
+    const bool live0 = q0 >= kfirst && q0 < T, live1 = q1 >= kfirst && q1 < T;
+    floatx16 s0, dp0, s1, dp1;
+    Op f0[2] = {Op{}, Op{}}, u0[2] = {Op{}, Op{}}, f1[2] = {Op{}, Op{}}, u1[2] = {Op{}, Op{}};
+    if (live0) {
+      evid(buf, 0, s0, dp0);
+      if (q0 == kfirst) grads(buf, 0, s0, dp0, f0, u0, std::true_type{});
+      else grads(buf, 0, s0, dp0, f0, u0, std::false_type{});
     }
+    if (live1) evid(buf, 1, s1, dp1);
+    __builtin_amdgcn_sched_barrier(0);
+    accum(buf, 0, f0, u0);
+    __builtin_amdgcn_sched_barrier(0);
+    if (live1) {
+      if (q1 == kfirst) grads(buf, 1, s1, dp1, f1, u1, std::true_type{});
+      else grads(buf, 1, s1, dp1, f1, u1, std::false_type{});
+    }
+    accum(buf, 1, f1, u1);
   };
   for (int qt = qt0; qt < nqt; qt += 2) {  // tiles alternate: bufA, bufB
     step(qt, bufA, bufB);

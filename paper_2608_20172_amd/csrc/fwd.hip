@@ -167,22 +167,34 @@ __device__ __forceinline__ int fast_keys64(const unsigned char* Ks, const unsign
                                            float& l, float& uii, const Lane& L, float c) {
   constexpr int KS = D / 16, DB = D / 32;
   using Op = typename P::Op;
-#pragma unroll
-  for (int b = 0; b < 2; ++b) {
-    const int kb0 = kglob + 32 * b;
-    Op pop[2] = {Op{}, Op{}};
-    if (kb0 <= qr0) {
-      const floatx16 s = evidence<P, KS, QM>(Ks, krow0 + 32 * b, qhi, qlo, L);
-      const bool ok = kb0 == qr0 ? fast_block<P, D, QM, true>(s, m, l, uii, pop, L, c)
-                                 : fast_block<P, D, QM, false>(s, m, l, uii, pop, L, c);
-      if (!ok) return b;
-    }
+  auto pv = [&](int b, const Op (&pop)[2]) {
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
       for (int db = 0; db < DB; ++db)
         oacc[db] = P::mma(P::col_op(Vs, krow0 / 16 + 2 * b + hh, 32 * db, L), pop[hh], oacc[db]);
+  };
+  // order: evidence of block 0, its vector work, evidence of block 1, then the
+  // P V products of block 0 (which run under the vector work of block 1)
+  const int k0 = kglob, k1 = kglob + 32;
+  Op p0[2] = {Op{}, Op{}}, p1[2] = {Op{}, Op{}};
+  floatx16 s1;
+  if (k0 <= qr0) {
+    const floatx16 s0 = evidence<P, KS, QM>(Ks, krow0, qhi, qlo, L);
+    const bool ok = k0 == qr0 ? fast_block<P, D, QM, true>(s0, m, l, uii, p0, L, c)
+                              : fast_block<P, D, QM, false>(s0, m, l, uii, p0, L, c);
+    if (!ok) return 0;
   }
+  if (k1 <= qr0) s1 = evidence<P, KS, QM>(Ks, krow0 + 32, qhi, qlo, L);
+  __builtin_amdgcn_sched_barrier(0);
+  pv(0, p0);
+  __builtin_amdgcn_sched_barrier(0);
+  if (k1 <= qr0) {
+    const bool ok = k1 == qr0 ? fast_block<P, D, QM, true>(s1, m, l, uii, p1, L, c)
+                              : fast_block<P, D, QM, false>(s1, m, l, uii, p1, L, c);
+    if (!ok) return 1;
+  }
+  pv(1, p1);
   return -1;
 }
 
