@@ -354,6 +354,21 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
   const int lane = tid & 63;
   const Lane L(lane);
   const int n = L.n, g = L.g;
+  if (blockIdx.x == 0 && a.dlambda) {
+    // dlambda: the dQ kernel (which ran before this one) left one partial per
+    // workgroup; summed here in a fixed order, so the result is run-to-run
+    // identical
+    __shared__ float red[kNT];
+    float acc = 0.0f;
+    for (int i = tid; i < a.nparts; i += kNT) acc += a.dlam_part[i];
+    red[tid] = acc;
+    __syncthreads();
+    for (int h = kNT / 2; h >= 1; h >>= 1) {
+      if (tid < h) red[tid] += red[tid + h];
+      __syncthreads();
+    }
+    if (tid == 0) *a.dlambda = red[0];
+  }
   int head, kt;
   if (!map_tile(a.map, blockIdx.x, head, kt, false)) return;
   const int T = a.T;
@@ -552,20 +567,6 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
   }
 }
 
-// dlambda = sum of the per-workgroup partials, in a fixed order.
-__global__ void finalize_dlam_kernel(const float* __restrict__ part, int np, float* __restrict__ out) {
-  __shared__ float s[256];
-  float acc = 0.0f;
-  for (int i = threadIdx.x; i < np; i += 256) acc += part[i];
-  s[threadIdx.x] = acc;
-  __syncthreads();
-  for (int h = 128; h >= 1; h >>= 1) {
-    if ((int)threadIdx.x < h) s[threadIdx.x] += s[threadIdx.x + h];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) *out = s[0];
-}
-
 template <class P, int D>
 void launch_pair(const BwdArgs& a, const TileMap& mkv, const TileMap& mq, hipStream_t stream,
                  hipEvent_t* prof) {
@@ -620,9 +621,5 @@ hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t stream) {
   return hipGetLastError();
 }
 
-hipError_t launch_dlambda(const float* part, int np, float* out, hipStream_t stream) {
-  hipLaunchKernelGGL(finalize_dlam_kernel, dim3(1), dim3(256), 0, stream, part, np, out);
-  return hipGetLastError();
-}
 
 }  // namespace rel

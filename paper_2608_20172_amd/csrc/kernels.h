@@ -39,6 +39,8 @@ struct BwdArgs {
   void* dk;
   void* dv;
   float* dlam_part;  // one partial per dQ-kernel workgroup slot
+  int nparts;        // number of those partials
+  float* dlambda;    // out: their sum in a fixed order
   float* negd;       // -D_i = -dO_i . o_i, [N, T], written by the dQ kernel
   float* m2;         // M_i log2(e), [N, T], written by the dQ kernel
   float* dself;      // optional [N, T]
@@ -75,7 +77,6 @@ bool profile_slot(const char* name, hipEvent_t* start, hipEvent_t* stop);
 hipError_t launch_fwd(const FwdArgs& a, int dtype, int D, hipStream_t stream);
 hipError_t launch_bwd(const BwdArgs& a, int dtype, int D, hipStream_t stream);
 int bwd_partials(int N, int T, int D, int dtype);
-hipError_t launch_dlambda(const float* part, int np, float* out, hipStream_t stream);
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t stream);
 hipError_t launch_allocation(const RowArgs& a, int dtype, int N, hipStream_t stream);
 hipError_t launch_materialized_rows(const RowArgs& a, int dtype, int N, hipStream_t stream);

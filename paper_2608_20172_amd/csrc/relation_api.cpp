@@ -384,11 +384,10 @@ rel_status relation_bwd(const rel_problem* p, const void* q, const void* k, cons
   a.scale = eff_scale(p);
   a.inv_tau = 1.0f / p->tau_s;
   a.map = rel::make_tilemap((int)N, 1);
+  a.nparts = rel::bwd_partials((int)N, (int)p->T, (int)p->D, p->dtype);
+  a.dlambda = dlambda;
   hipError_t e = rel::launch_bwd(a, p->dtype, (int)p->D, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "relation_bwd launch");
-  e = rel::launch_dlambda(a.dlam_part, rel::bwd_partials((int)N, (int)p->T, (int)p->D, p->dtype),
-                          dlambda, (hipStream_t)stream);
-  if (e != hipSuccess) return hip_fail(e, "relation_bwd dlambda reduction");
   return REL_OK;
 }
 

@@ -294,3 +294,4 @@ def test_workload_long_context_sampled():
     assert err < 2e-2
     sm = f["self_mass"]
     assert sm is not None
+
