@@ -54,6 +54,29 @@ constexpr int kNT = 256;
 #define REL_DKDV_WAVES_PER_SIMD 2 // bf16, d <= 64
 #endif
 
+#ifndef REL_DQ_FULL_PATH
+#define REL_DQ_FULL_PATH 1
+#endif
+#ifndef REL_DKDV_INTERLEAVE
+#define REL_DKDV_INTERLEAVE 1
+#endif
+#ifndef REL_DKDV_IL_VALU
+#define REL_DKDV_IL_VALU 12  // vector instructions scheduled after each matrix instruction
+#endif
+
+// Scheduling pattern for one basic block holding NM matrix instructions and
+// independent vector work: the LDS reads first, then each matrix instruction
+// followed by NV vector instructions.
+template <int NM, int NV, int ID>
+__device__ __forceinline__ void interleave() {
+  __builtin_amdgcn_sched_group_barrier(0x100, 64, ID);  // LDS reads
+#pragma unroll
+  for (int i = 0; i < NM; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, ID);   // matrix
+    __builtin_amdgcn_sched_group_barrier(0x002, NV, ID);  // vector
+  }
+}
+
 template <class P, int D>
 constexpr int dq_occupancy() {
   return sizeof(typename P::T) == 2 ? (D <= 64 ? REL_DQ_WAVES_PER_SIMD : 1) : (D <= 32 ? 2 : 1);
@@ -265,7 +288,7 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
   // the dQ products (and the accumulators) run on every path. Order: evidence
   // of block 0, its vector work, evidence of block 1, then the products of
   // block 0 (which run under the vector work of block 1).
-  auto step = [&](int kt, const unsigned char* Ks, unsigned char* nxt) {
+  auto step = [&](int kt, const unsigned char* Ks, unsigned char* nxt) __attribute__((always_inline)) {
     wait_loads();
     __syncthreads();
     if (kt + 1 < nkt) load_tile((kt + 1) * kBK, nxt);
@@ -305,10 +328,36 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
     }
     accum(Ks, 1, u1);
   };
-  for (int kt = 0; kt < nkt; kt += 2) {  // even tiles in bufA, odd ones in bufB
-    step(kt, bufA, bufB);
-    if (kt + 1 < nkt) step(kt + 1, bufB, bufA);
-  }
+  // A full tile (both blocks below every wave's rows) runs without branches.
+  auto full = [&](int kt, const unsigned char* Ks, unsigned char* nxt) __attribute__((always_inline)) {
+    wait_loads();
+    __syncthreads();
+    if (kt + 1 < nkt) load_tile((kt + 1) * kBK, nxt);
+    const unsigned char* Vs = Ks + TB;
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      Op u[2];
+      floatx16 s, dp;
+      evid(Ks, Vs, 32 * b, s, dp);
+      grads(s, dp, u, std::false_type{});
+      accum(Ks, b, u);
+    }
+  };
+  // even tiles in bufA, odd ones in bufB
+  auto run = [&](int ka, int kb, auto st) __attribute__((always_inline)) {
+    int kt = ka;
+    if (kt < kb && (kt & 1)) {
+      st(kt, bufB, bufA);
+      ++kt;
+    }
+    for (; kt < kb; kt += 2) {
+      st(kt, bufA, bufB);
+      if (kt + 1 < kb) st(kt + 1, bufB, bufA);
+    }
+  };
+  const int kf = REL_DQ_FULL_PATH ? min(i0 / kBK, nkt) : 0;  // tiles below the workgroup's diagonal
+  run(0, kf, full);
+  run(kf, nkt, step);
 
   if (wave_live && row_ok) {
     E* dq = (E*)a.dq + hoff;
@@ -518,7 +567,7 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
   // F and dU, so the dV / dK products (and the accumulators) run on every
   // path. Order: evidence of block 0, its vector work, evidence of block 1,
   // then the products of block 0 (which run under the vector work of block 1).
-  auto step = [&](int qt, const unsigned char* buf, unsigned char* nxt) {
+  auto step = [&](int qt, const unsigned char* buf, unsigned char* nxt) __attribute__((always_inline)) {
     const int i0 = qt * kBQI;
     wait_loads();
     __syncthreads();
@@ -542,10 +591,46 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
     }
     accum(buf, 1, f1, u1);
   };
-  for (int qt = qt0; qt < nqt; qt += 2) {  // tiles alternate: bufA, bufB
-    step(qt, bufA, bufB);
-    if (qt + 1 < nqt) step(qt + 1, bufB, bufA);
-  }
+  // A full tile (both blocks live and past every wave's diagonal) is one
+  // basic block: the evidence of block 1 and then the products of block 0 are
+  // interleaved with the vector work of blocks 0 and 1, so that one wave keeps
+  // the matrix and the vector units busy together.
+  auto full = [&](int qt, const unsigned char* buf, unsigned char* nxt) __attribute__((always_inline)) {
+    const int i0 = qt * kBQI;
+    wait_loads();
+    __syncthreads();
+    if (qt + 1 < nqt) load_tile(i0 + kBQI, nxt);
+    floatx16 s0, dp0, s1, dp1;
+    Op f0[2], u0[2], f1[2], u1[2];
+    evid(buf, 0, s0, dp0);
+    __builtin_amdgcn_sched_barrier(0);
+    evid(buf, 1, s1, dp1);
+    grads(buf, 0, s0, dp0, f0, u0, std::false_type{});
+    if (REL_DKDV_INTERLEAVE) interleave<2 * KS, REL_DKDV_IL_VALU, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+    accum(buf, 0, f0, u0);
+    grads(buf, 1, s1, dp1, f1, u1, std::false_type{});
+    if (REL_DKDV_INTERLEAVE) interleave<4 * DB, REL_DKDV_IL_VALU, 1>();
+    __builtin_amdgcn_sched_barrier(0);
+    accum(buf, 1, f1, u1);
+  };
+  // tiles alternate between bufA and bufB, starting with bufA at qt0
+  auto run = [&](int qa, int qb, auto st) __attribute__((always_inline)) {
+    int qt = qa;
+    if (qt < qb && ((qt - qt0) & 1)) {
+      st(qt, bufB, bufA);
+      ++qt;
+    }
+    for (; qt < qb; qt += 2) {
+      st(qt, bufA, bufB);
+      if (qt + 1 < qb) st(qt + 1, bufB, bufA);
+    }
+  };
+  const int qf0 = min(qt0 + kBKW / kBQI, nqt);  // tiles with the workgroup's diagonals
+  const int qf1 = max(qf0, T / kBQI);             // full tiles end here
+  run(qt0, qf0, step);
+  run(qf0, qf1, full);
+  run(qf1, nqt, step);
 
   if (kj < T) {
     E* dk = (E*)a.dk + hoff;

@@ -21,6 +21,8 @@
 // waves per workgroup, three per SIMD for bf16 with d <= 64.
 #include "kernels.h"
 
+#include <type_traits>
+
 
 namespace rel {
 
@@ -28,6 +30,9 @@ namespace {
 
 constexpr int kBQ = 128;  // query rows per workgroup
 constexpr float kRescale = 8.0f;
+#ifndef REL_FWD_BF16_WAVES_PER_SIMD
+#define REL_FWD_BF16_WAVES_PER_SIMD 3  // occupancy of the bf16 kernel for d <= 64
+#endif
 #ifndef REL_FWD_WAVES_PER_SIMD
 #define REL_FWD_WAVES_PER_SIMD 2  // occupancy of the fp32 kernel for d <= 64
 #endif
@@ -36,6 +41,9 @@ constexpr float kRescale = 8.0f;
 //   0: raw q; each evidence entry is multiplied by c
 //   1: q c in the operand (fp32)
 //   2: q c as bf16 hi + lo, two MFMAs per slice
+#ifndef REL_FWD_FULL_PATH
+#define REL_FWD_FULL_PATH 1  // branch-free fast steps for tiles below the workgroup's rows
+#endif
 #ifndef REL_FWD_BF16_QMODE
 #define REL_FWD_BF16_QMODE 0
 #endif
@@ -160,7 +168,7 @@ __device__ __forceinline__ bool fast_block(floatx16 s, float m, float& l, float&
 // running reference. A block above the wave's rows contributes zero weights,
 // so the P V products (and the accumulators) run on every path. Returns -1,
 // or the first block that needs the reference raised (not accumulated).
-template <class P, int D, int QM>
+template <class P, int D, int QM, bool FULL>
 __device__ __forceinline__ int fast_keys64(const unsigned char* Ks, const unsigned char* Vs, int krow0, int kglob,
                                            int qr0, const typename P::Op (&qhi)[D / 16],
                                            const typename P::Op (&qlo)[D / 16], floatx16 (&oacc)[D / 32], float m,
@@ -179,6 +187,17 @@ __device__ __forceinline__ int fast_keys64(const unsigned char* Ks, const unsign
   const int k0 = kglob, k1 = kglob + 32;
   Op p0[2] = {Op{}, Op{}}, p1[2] = {Op{}, Op{}};
   floatx16 s1;
+  if (FULL) {  // both blocks below the wave's rows
+    const floatx16 s0 = evidence<P, KS, QM>(Ks, krow0, qhi, qlo, L);
+    if (!fast_block<P, D, QM, false>(s0, m, l, uii, p0, L, c)) return 0;
+    s1 = evidence<P, KS, QM>(Ks, krow0 + 32, qhi, qlo, L);
+    __builtin_amdgcn_sched_barrier(0);
+    pv(0, p0);
+    __builtin_amdgcn_sched_barrier(0);
+    if (!fast_block<P, D, QM, false>(s1, m, l, uii, p1, L, c)) return 1;
+    pv(1, p1);
+    return -1;
+  }
   if (k0 <= qr0) {
     const floatx16 s0 = evidence<P, KS, QM>(Ks, krow0, qhi, qlo, L);
     const bool ok = k0 == qr0 ? fast_block<P, D, QM, true>(s0, m, l, uii, p0, L, c)
@@ -301,7 +320,8 @@ constexpr int kNT = 256;  // threads per workgroup
 
 template <class P, int D>
 constexpr int fwd_occupancy() {
-  return sizeof(typename P::T) == 2 ? (D <= 64 ? 3 : 2) : (D <= 64 ? REL_FWD_WAVES_PER_SIMD : 1);
+  return sizeof(typename P::T) == 2 ? (D <= 64 ? REL_FWD_BF16_WAVES_PER_SIMD : 2)
+                                    : (D <= 64 ? REL_FWD_WAVES_PER_SIMD : 1);
 }
 
 template <class P, int D>
@@ -365,26 +385,42 @@ __global__ __launch_bounds__(kNT, (fwd_occupancy<P, D>())) void fwd_kernel(FwdAr
   // KB/VB. A fast step returns the block that needs the running reference
   // raised, or -1.
   const int qlast = wave_live ? qr0 : -1;  // rows of a wave past T meet no key
-  auto fast_step = [&](int kt, const unsigned char* Ks, const unsigned char* Vs, unsigned char* Kn,
-                       unsigned char* Vn) {
+  auto fast_step = [&](auto full, int kt, const unsigned char* Ks, const unsigned char* Vs, unsigned char* Kn,
+                       unsigned char* Vn) __attribute__((always_inline)) {
     wait_loads();      // this wave's part of tile kt is in LDS
     __syncthreads();   // ... and every wave's; tile kt-1 is no longer read
     if (kt + 1 < nkt) load_tile((kt + 1) * kBK, Kn, Vn);
-    return fast_keys64<P, D, QM>(Ks, Vs, 0, kt * kBK, qlast, qhi, qlo, oacc, m, l, uii, L, c);
+    return fast_keys64<P, D, QM, decltype(full)::value>(Ks, Vs, 0, kt * kBK, qlast, qhi, qlo, oacc, m, l, uii, L,
+                                                          c);
   };
-  load_tile(0, KA, VA);
-  int kt = 0, resume = -1;
-  for (; kt < nkt; kt += 2) {
-    resume = fast_step(kt, KA, VA, KB, VB);
-    if (resume >= 0) break;
-    if (kt + 1 < nkt) {
-      resume = fast_step(kt + 1, KB, VB, KA, VA);
-      if (resume >= 0) {
-        ++kt;
-        break;
+  // fast steps over tiles ka .. kb-1; returns the block that needs the
+  // reference raised (kt then names its tile), or -1
+  int kt = 0;
+  auto run_fast = [&](int ka, int kb, auto full) __attribute__((always_inline)) {
+    kt = ka;
+    if (kt < kb && (kt & 1)) {
+      const int r = fast_step(full, kt, KB, VB, KA, VA);
+      if (r >= 0) return r;
+      ++kt;
+    }
+    for (; kt < kb; kt += 2) {
+      int r = fast_step(full, kt, KA, VA, KB, VB);
+      if (r >= 0) return r;
+      if (kt + 1 < kb) {
+        r = fast_step(full, kt + 1, KB, VB, KA, VA);
+        if (r >= 0) {
+          ++kt;
+          return r;
+        }
       }
     }
-  }
+    return -1;
+  };
+  load_tile(0, KA, VA);
+  // tiles below the workgroup's first row have both blocks below every wave's rows
+  const int kf = REL_FWD_FULL_PATH ? min(i0 / kBK, nkt) : 0;
+  int resume = run_fast(0, kf, std::true_type{});
+  if (resume < 0) resume = run_fast(kf, nkt, std::false_type{});
   if (resume >= 0) {
     // a block exceeded the running reference: finish the scan with rescaling,
     // passing the same barriers as the rest of the workgroup
