@@ -57,6 +57,12 @@ constexpr int kNT = 256;
 #ifndef REL_DQ_FULL_PATH
 #define REL_DQ_FULL_PATH 1
 #endif
+#ifndef REL_DQ_INTERLEAVE
+#define REL_DQ_INTERLEAVE 1
+#endif
+#ifndef REL_DQ_IL_VALU
+#define REL_DQ_IL_VALU 28
+#endif
 #ifndef REL_DKDV_INTERLEAVE
 #define REL_DKDV_INTERLEAVE 1
 #endif
@@ -334,6 +340,22 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
     __syncthreads();
     if (kt + 1 < nkt) load_tile((kt + 1) * kBK, nxt);
     const unsigned char* Vs = Ks + TB;
+    if (REL_DQ_INTERLEAVE) {
+      // the products of block 0 between the vector work of block 1
+      Op u0[2], u1[2];
+      floatx16 s, dp;
+      evid(Ks, Vs, 0, s, dp);
+      grads(s, dp, u0, std::false_type{});
+      __builtin_amdgcn_sched_barrier(0);
+      evid(Ks, Vs, 32, s, dp);
+      __builtin_amdgcn_sched_barrier(0);
+      accum(Ks, 0, u0);
+      grads(s, dp, u1, std::false_type{});
+      interleave<2 * DB, REL_DQ_IL_VALU, 0>();
+      __builtin_amdgcn_sched_barrier(0);
+      accum(Ks, 1, u1);
+      return;
+    }
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       Op u[2];

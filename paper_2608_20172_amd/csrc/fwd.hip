@@ -44,6 +44,12 @@ constexpr float kRescale = 8.0f;
 #ifndef REL_FWD_FULL_PATH
 #define REL_FWD_FULL_PATH 1  // branch-free fast steps for tiles below the workgroup's rows
 #endif
+#ifndef REL_FWD_INTERLEAVE
+#define REL_FWD_INTERLEAVE 1
+#endif
+#ifndef REL_FWD_IL_VALU
+#define REL_FWD_IL_VALU 28
+#endif
 #ifndef REL_FWD_BF16_QMODE
 #define REL_FWD_BF16_QMODE 0
 #endif
@@ -193,8 +199,17 @@ __device__ __forceinline__ int fast_keys64(const unsigned char* Ks, const unsign
     s1 = evidence<P, KS, QM>(Ks, krow0 + 32, qhi, qlo, L);
     __builtin_amdgcn_sched_barrier(0);
     pv(0, p0);
-    __builtin_amdgcn_sched_barrier(0);
-    if (!fast_block<P, D, QM, false>(s1, m, l, uii, p1, L, c)) return 1;
+    if (!REL_FWD_INTERLEAVE) __builtin_amdgcn_sched_barrier(0);
+    const bool ok = fast_block<P, D, QM, false>(s1, m, l, uii, p1, L, c);
+    if (REL_FWD_INTERLEAVE) {  // the P V products of block 0 between the vector work of block 1
+      __builtin_amdgcn_sched_group_barrier(0x100, 64, 0);
+#pragma unroll
+      for (int i = 0; i < 2 * DB; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, REL_FWD_IL_VALU, 0);
+      }
+    }
+    if (!ok) return 1;
     pv(1, p1);
     return -1;
   }
