@@ -180,7 +180,7 @@ def test_backward_sharp(dtype):
     check_backward(x, dtype, f)
 
 
-@pytest.mark.parametrize("T", [1, 2, 65, 127, 128, 129])
+@pytest.mark.parametrize("T", [1, 2, 65, 127, 128, 129, 319, 640, 1000])
 def test_backward_edge_lengths(T):
     x = _prep(I.make_inputs(1, 2, T, 64, seed=100 + T, qkv_std=0.5, lam=-0.5), "bf16")
     f = check_forward(x, "bf16", with_aux=False)
