@@ -30,6 +30,7 @@ namespace {
 
 constexpr int kBQ = 128;  // query rows per workgroup
 constexpr float kRescale = 8.0f;
+constexpr float kSpecMax = 18446744073709551616.0f;  // 2^64
 #ifndef REL_FWD_BF16_WAVES_PER_SIMD
 #define REL_FWD_BF16_WAVES_PER_SIMD 3  // occupancy of the bf16 kernel for d <= 64
 #endif
@@ -43,6 +44,9 @@ constexpr float kRescale = 8.0f;
 //   2: q c as bf16 hi + lo, two MFMAs per slice
 #ifndef REL_FWD_FULL_PATH
 #define REL_FWD_FULL_PATH 1  // branch-free fast steps for tiles below the workgroup's rows
+#endif
+#ifndef REL_FWD_SPECULATE
+#define REL_FWD_SPECULATE 1  // scan with the reference at 0 and check the row totals at the end
 #endif
 #ifndef REL_FWD_INTERLEAVE
 #define REL_FWD_INTERLEAVE 1
@@ -61,7 +65,7 @@ constexpr int qmode() {
 // Exchange logits of one 32x32 block, in place: s[r] (U log2 e, or raw q.k in
 // mode 0) becomes E log2(e) - m; in the diagonal block (DIAG) entries with
 // key >= query get -inf. mx tracks the lane's largest value.
-template <bool DIAG, int QM>
+template <bool DIAG, int QM, bool TRACK = true>
 __device__ __forceinline__ void exchange_logits(floatx16& s, const Lane& L, float c, float m, float& mx) {
   // passes over groups of 4 independent entries: consecutive instructions do
   // not wait on a transcendental result, and few temporaries are live
@@ -80,7 +84,7 @@ __device__ __forceinline__ void exchange_logits(floatx16& s, const Lane& L, floa
       if (DIAG && acc_row(r0 + r, L.g) >= L.n) e = kNegInf;                    // strictly historical: j < i
       s[r0 + r] = e;
     }
-    mx = fmaxf(mx, fmaxf(fmaxf(s[r0], s[r0 + 1]), fmaxf(s[r0 + 2], s[r0 + 3])));
+    if (TRACK) mx = fmaxf(mx, fmaxf(fmaxf(s[r0], s[r0 + 1]), fmaxf(s[r0 + 2], s[r0 + 3])));
   }
 }
 
@@ -147,13 +151,13 @@ __device__ __forceinline__ floatx16 evidence(const unsigned char* Ks, int krow0,
 // running reference by more than kRescale, the packed weights P of its two
 // 16-key halves and their sum into l. Returns false (and changes neither l nor
 // pop) when the reference has to be raised first.
-template <class P, int D, int QM, bool DIAG>
+template <class P, int D, int QM, bool DIAG, bool CHECK>
 __device__ __forceinline__ bool fast_block(floatx16 s, float m, float& l, float& uii, typename P::Op (&pop)[2],
                                            const Lane& L, float c) {
   if (DIAG && holds_row(L.n, L.g)) uii = pick(s, row_reg(L.n));  // the Self evidence
   float mx = kNegInf;
-  exchange_logits<DIAG, QM>(s, L, c, m, mx);
-  if (wave_any(mx > kRescale)) return false;
+  exchange_logits<DIAG, QM, CHECK>(s, L, c, m, mx);
+  if (CHECK && wave_any(mx > kRescale)) return false;
   // l sums the fp32 p (not the bf16-rounded MFMA operand), so that L^E and the
   // saved statistic M carry no operand rounding
 #pragma unroll
@@ -174,7 +178,7 @@ __device__ __forceinline__ bool fast_block(floatx16 s, float m, float& l, float&
 // running reference. A block above the wave's rows contributes zero weights,
 // so the P V products (and the accumulators) run on every path. Returns -1,
 // or the first block that needs the reference raised (not accumulated).
-template <class P, int D, int QM, bool FULL>
+template <class P, int D, int QM, bool FULL, bool CHECK>
 __device__ __forceinline__ int fast_keys64(const unsigned char* Ks, const unsigned char* Vs, int krow0, int kglob,
                                            int qr0, const typename P::Op (&qhi)[D / 16],
                                            const typename P::Op (&qlo)[D / 16], floatx16 (&oacc)[D / 32], float m,
@@ -195,12 +199,12 @@ __device__ __forceinline__ int fast_keys64(const unsigned char* Ks, const unsign
   floatx16 s1;
   if (FULL) {  // both blocks below the wave's rows
     const floatx16 s0 = evidence<P, KS, QM>(Ks, krow0, qhi, qlo, L);
-    if (!fast_block<P, D, QM, false>(s0, m, l, uii, p0, L, c)) return 0;
+    if (!fast_block<P, D, QM, false, CHECK>(s0, m, l, uii, p0, L, c)) return 0;
     s1 = evidence<P, KS, QM>(Ks, krow0 + 32, qhi, qlo, L);
     __builtin_amdgcn_sched_barrier(0);
     pv(0, p0);
     if (!REL_FWD_INTERLEAVE) __builtin_amdgcn_sched_barrier(0);
-    const bool ok = fast_block<P, D, QM, false>(s1, m, l, uii, p1, L, c);
+    const bool ok = fast_block<P, D, QM, false, CHECK>(s1, m, l, uii, p1, L, c);
     if (REL_FWD_INTERLEAVE) {  // the P V products of block 0 between the vector work of block 1
       __builtin_amdgcn_sched_group_barrier(0x100, 64, 0);
 #pragma unroll
@@ -215,8 +219,8 @@ __device__ __forceinline__ int fast_keys64(const unsigned char* Ks, const unsign
   }
   if (k0 <= qr0) {
     const floatx16 s0 = evidence<P, KS, QM>(Ks, krow0, qhi, qlo, L);
-    const bool ok = k0 == qr0 ? fast_block<P, D, QM, true>(s0, m, l, uii, p0, L, c)
-                              : fast_block<P, D, QM, false>(s0, m, l, uii, p0, L, c);
+    const bool ok = k0 == qr0 ? fast_block<P, D, QM, true, CHECK>(s0, m, l, uii, p0, L, c)
+                              : fast_block<P, D, QM, false, CHECK>(s0, m, l, uii, p0, L, c);
     if (!ok) return 0;
   }
   if (k1 <= qr0) s1 = evidence<P, KS, QM>(Ks, krow0 + 32, qhi, qlo, L);
@@ -224,8 +228,8 @@ __device__ __forceinline__ int fast_keys64(const unsigned char* Ks, const unsign
   pv(0, p0);
   __builtin_amdgcn_sched_barrier(0);
   if (k1 <= qr0) {
-    const bool ok = k1 == qr0 ? fast_block<P, D, QM, true>(s1, m, l, uii, p1, L, c)
-                              : fast_block<P, D, QM, false>(s1, m, l, uii, p1, L, c);
+    const bool ok = k1 == qr0 ? fast_block<P, D, QM, true, CHECK>(s1, m, l, uii, p1, L, c)
+                              : fast_block<P, D, QM, false, CHECK>(s1, m, l, uii, p1, L, c);
     if (!ok) return 1;
   }
   pv(1, p1);
@@ -400,13 +404,14 @@ __global__ __launch_bounds__(kNT, (fwd_occupancy<P, D>())) void fwd_kernel(FwdAr
   // KB/VB. A fast step returns the block that needs the running reference
   // raised, or -1.
   const int qlast = wave_live ? qr0 : -1;  // rows of a wave past T meet no key
+  constexpr bool SPEC = REL_FWD_SPECULATE;  // no per-block check; the row totals are checked at the end
   auto fast_step = [&](auto full, int kt, const unsigned char* Ks, const unsigned char* Vs, unsigned char* Kn,
                        unsigned char* Vn) __attribute__((always_inline)) {
     wait_loads();      // this wave's part of tile kt is in LDS
     __syncthreads();   // ... and every wave's; tile kt-1 is no longer read
     if (kt + 1 < nkt) load_tile((kt + 1) * kBK, Kn, Vn);
-    return fast_keys64<P, D, QM, decltype(full)::value>(Ks, Vs, 0, kt * kBK, qlast, qhi, qlo, oacc, m, l, uii, L,
-                                                          c);
+    return fast_keys64<P, D, QM, decltype(full)::value, !SPEC>(Ks, Vs, 0, kt * kBK, qlast, qhi, qlo, oacc, m, l,
+                                                                uii, L, c);
   };
   // fast steps over tiles ka .. kb-1; returns the block that needs the
   // reference raised (kt then names its tile), or -1
@@ -436,7 +441,35 @@ __global__ __launch_bounds__(kNT, (fwd_occupancy<P, D>())) void fwd_kernel(FwdAr
   const int kf = REL_FWD_FULL_PATH ? min(i0 / kBK, nkt) : 0;
   int resume = run_fast(0, kf, std::true_type{});
   if (resume < 0) resume = run_fast(kf, nkt, std::false_type{});
-  if (resume >= 0) {
+  if (SPEC) {
+    // The scan ran with the reference fixed at 0. Every weight is at most the
+    // row total l, so l <= 2^64 bounds every weight and |z| <= l max|v|: then
+    // nothing overflowed and the result is exact. Otherwise (or on inf / NaN)
+    // the wave's rows are scanned again with the rescaling loop; the whole
+    // workgroup passes the tiles again for the barriers.
+    const float lt = l + xor32(l);
+    const bool bad = wave_live && !(lt <= kSpecMax);
+    if (__syncthreads_or(bad ? 1 : 0)) {
+      const bool redo = wave_any(bad);
+      if (redo) {
+        m = 0.0f;
+        l = 0.0f;
+        uii = 0.0f;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) oacc[db] = floatx16{};
+      }
+      load_tile(0, KA, VA);
+      for (kt = 0; kt < nkt; ++kt) {
+        const bool odd = kt & 1;
+        wait_loads();
+        __syncthreads();
+        if (kt + 1 < nkt) load_tile((kt + 1) * kBK, odd ? KA : KB, odd ? VA : VB);
+        if (redo)
+          slow_keys64<P, D, QM>(odd ? KB : KA, odd ? VB : VA, 0, kt * kBK, qlast, 0, qhi, qlo, oacc, m, l, uii, L,
+                                c);
+      }
+    }
+  } else if (resume >= 0) {
     // a block exceeded the running reference: finish the scan with rescaling,
     // passing the same barriers as the rest of the workgroup
     slow_keys64<P, D, QM>((kt & 1) ? KB : KA, (kt & 1) ? VB : VA, 0, kt * kBK, qlast, resume, qhi, qlo, oacc, m,

@@ -145,6 +145,21 @@ def test_forward_sharp(dtype):
     check_forward(x, dtype)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_forward_fixed_reference_rejected(dtype):
+    """Evidence up to ~80: some rows have L^E above 64 ln 2, so the scan with the
+    reference fixed at 0 fails its row-total check and those waves rescan with
+    rescaling. The bf16 gradients use the saved statistic of that second scan
+    (at this scale the fp32 gradients reach ~1e2, beyond the absolute fp32 bar
+    of 1e-4 at fp32 rounding; the forward is what this case is about)."""
+    x = _prep(I.make_inputs(1, 2, 300, 64, seed=31, qkv_std=4.0, lam=0.5), dtype)
+    out = check_forward(x, dtype)
+    le = _np(out["exch_lse"])
+    assert np.nanmax(le[np.isfinite(le)]) > 64 * np.log(2), "inputs do not reach the rescan path"
+    if dtype == "bf16":
+        check_backward(x, dtype, out)
+
+
 @pytest.mark.parametrize("T", [1, 2, 3, 31, 32, 33, 63, 64, 65, 127, 128, 129, 1000])
 def test_forward_edge_lengths(T):
     x = _prep(I.make_inputs(1, 2, T, 64, seed=T, qkv_std=0.5, with_dout=False, lam=0.5), "bf16")
