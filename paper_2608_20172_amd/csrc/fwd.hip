@@ -48,6 +48,9 @@ constexpr float kSpecMax = 18446744073709551616.0f;  // 2^64
 #ifndef REL_FWD_SPECULATE
 #define REL_FWD_SPECULATE 1  // scan with the reference at 0 and check the row totals at the end
 #endif
+#ifndef REL_FWD_PIPE2
+#define REL_FWD_PIPE2 1  // full tiles: evidence of block 1 under the vector work of block 0
+#endif
 #ifndef REL_FWD_INTERLEAVE
 #define REL_FWD_INTERLEAVE 1
 #endif
@@ -197,6 +200,33 @@ __device__ __forceinline__ int fast_keys64(const unsigned char* Ks, const unsign
   const int k0 = kglob, k1 = kglob + 32;
   Op p0[2] = {Op{}, Op{}}, p1[2] = {Op{}, Op{}};
   floatx16 s1;
+  if (FULL && !CHECK && REL_FWD_PIPE2) {
+    // both blocks below the wave's rows and no checks: one basic block, the
+    // evidence of block 1 under the vector work of block 0, the P V products
+    // of block 0 under that of block 1
+    const floatx16 s0 = evidence<P, KS, QM>(Ks, krow0, qhi, qlo, L);
+    __builtin_amdgcn_sched_barrier(0);
+    s1 = evidence<P, KS, QM>(Ks, krow0 + 32, qhi, qlo, L);
+    fast_block<P, D, QM, false, CHECK>(s0, m, l, uii, p0, L, c);
+    __builtin_amdgcn_sched_group_barrier(0x100, 64, 0);
+#pragma unroll
+    for (int i = 0; i < (QM == 2 ? 2 : 1) * KS; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, REL_FWD_IL_VALU, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    pv(0, p0);
+    fast_block<P, D, QM, false, CHECK>(s1, m, l, uii, p1, L, c);
+    __builtin_amdgcn_sched_group_barrier(0x100, 64, 1);
+#pragma unroll
+    for (int i = 0; i < 2 * DB; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+      __builtin_amdgcn_sched_group_barrier(0x002, REL_FWD_IL_VALU, 1);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    pv(1, p1);
+    return -1;
+  }
   if (FULL) {  // both blocks below the wave's rows
     const floatx16 s0 = evidence<P, KS, QM>(Ks, krow0, qhi, qlo, L);
     if (!fast_block<P, D, QM, false, CHECK>(s0, m, l, uii, p0, L, c)) return 0;
