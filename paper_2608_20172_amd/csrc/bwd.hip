@@ -42,7 +42,8 @@ constexpr int kNT = 256;
 #define REL_DQ_WAVES_PER_SIMD 3   // bf16, d <= 64
 #endif
 #ifndef REL_DQ_NEGD_SEED
-#define REL_DQ_NEGD_SEED 0  // dQ: 1 = the dP chains start from -D_i (16 registers); 0 = subtract D_i per entry
+#define REL_DQ_NEGD_SEED 2  // dQ: 1 = the dP chains start from -D_i (16 registers); 0 = subtract D_i per entry;
+                            // 2 = one more MFMA per block adds -D_i (bf16; 0 on the fp32 path)
 #endif
 #ifndef REL_DQ_PIPELINE
 #define REL_DQ_PIPELINE 0  // dQ: 1 = evidence of block 1 before the products of block 0 (needs 2 waves per SIMD)
@@ -213,10 +214,25 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
     a.negd[(int64_t)head * T + qi] = -Di;
     a.m2[(int64_t)head * T + qi] = Mi2;
   }
-  floatx16 negD;  // the dP chains start from -D_i
+  // -D_i enters the dP chains: as their starting accumulator (mode 1), as one
+  // more product of a 0/1 column against -D_i split into two bf16 terms
+  // (mode 2: every key row of this lane's query gets -D_hi - D_lo), or by a
+  // subtraction per entry (mode 0)
+  constexpr int NDM = (REL_DQ_NEGD_SEED == 2 && sizeof(E) != 2) ? 0 : REL_DQ_NEGD_SEED;
+  floatx16 negD;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) negD[r] = REL_DQ_NEGD_SEED ? -Di : 0.0f;
-  const float dsub = REL_DQ_NEGD_SEED ? 0.0f : Di;
+  for (int r = 0; r < 16; ++r) negD[r] = NDM == 1 ? -Di : 0.0f;
+  const float dsub = NDM == 0 ? Di : 0.0f;
+  Op dcol{}, dval{};
+  if constexpr (NDM == 2) {
+    const bf16 hi = f2bf(-Di);
+    const bf16 lo = f2bf(-Di - bf2f(hi));
+    const unsigned w = (unsigned)__builtin_bit_cast(unsigned short, hi) |
+                       ((unsigned)__builtin_bit_cast(unsigned short, lo) << 16);
+    const bool g0 = g == 0;  // contraction indices 0 and 1 live in elements 0, 1 of lane group 0
+    dcol = __builtin_bit_cast(Op, uintx4{g0 ? 0x3f803f80u : 0u, 0u, 0u, 0u});
+    dval = __builtin_bit_cast(Op, uintx4{g0 ? w : 0u, 0u, 0u, 0u});
+  }
 
   floatx16 dQt[DB];
 #pragma unroll
@@ -244,6 +260,7 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
         dp = P::mma(va[j], doop[k0 + j], dp);  // dP - D
       }
     }
+    if constexpr (NDM == 2) dp = P::mma(dcol, dval, dp);
   };
   // ... then dU on the vector units, packed as the operands of the two 16-key
   // halves; DIAG: the wave's own diagonal block (key offset acc_row(r, g)
@@ -256,7 +273,7 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
       uself = pick(s, rs);
       dself = pick(dp, rs);
     }
-    if (!REL_DQ_NEGD_SEED && DIAG) dself -= Di;
+    if (NDM == 0 && DIAG) dself -= Di;
     exchange_grads(s, dp, [&](int) { return Mi2; }, c, dsub);
     if (DIAG) {
 #pragma unroll
