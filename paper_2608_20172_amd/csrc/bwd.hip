@@ -41,6 +41,9 @@ constexpr int kNT = 256;
 #ifndef REL_DQ_WAVES_PER_SIMD
 #define REL_DQ_WAVES_PER_SIMD 3   // bf16, d <= 64
 #endif
+#ifndef REL_DQ_WAVES_PER_SIMD_D128
+#define REL_DQ_WAVES_PER_SIMD_D128 2  // bf16, d = 128
+#endif
 #ifndef REL_DQ_NEGD_SEED
 #define REL_DQ_NEGD_SEED 2  // dQ: 1 = the dP chains start from -D_i (16 registers); 0 = subtract D_i per entry;
                             // 2 = one more MFMA per block adds -D_i (bf16; 0 on the fp32 path)
@@ -86,7 +89,8 @@ __device__ __forceinline__ void interleave() {
 
 template <class P, int D>
 constexpr int dq_occupancy() {
-  return sizeof(typename P::T) == 2 ? (D <= 64 ? REL_DQ_WAVES_PER_SIMD : 1) : (D <= 32 ? 2 : 1);
+  return sizeof(typename P::T) == 2 ? (D <= 64 ? REL_DQ_WAVES_PER_SIMD : REL_DQ_WAVES_PER_SIMD_D128)
+                                    : (D <= 32 ? 2 : 1);
 }
 template <class P, int D>
 constexpr int dkdv_occupancy() {
