@@ -22,8 +22,9 @@
 //    tiles by transpose reads.
 // Tiles go HBM -> LDS by buffer loads that write LDS directly (two buffers,
 // one barrier per tile; rows past T read as zeros). Every gradient is written
-// exactly once: no atomics, run-to-run identical. The dP chains start from an
-// accumulator holding -D_i, so the matrix cores deliver dP_ij - D_i directly.
+// exactly once: no atomics, run-to-run identical. The matrix cores deliver
+// dP_ij - D_i directly: in dK/dV the dP chains start from an accumulator
+// holding -D of each query row, in dQ one more product adds -D_i.
 #include "kernels.h"
 
 #include <algorithm>

@@ -10,11 +10,13 @@
 // read off the diagonal entry of the evidence block that holds row i.
 //
 // Running reference m. SiLU(U) >= -0.2785, so exp(E - m) with m = 0 can never
-// underflow to an all-zero row; the reference is raised only when a block's
-// largest E exceeds it by more than 8 (in log2 units), which keeps every
-// exp2 argument <= 8 and the sums far from fp32 overflow. Any reference gives
-// the same ratios z/l and L^E = m + ln l, so the result is exact. The test is
-// lane-local; only a raise combines the two halves of a row.
+// underflow to an all-zero row. Any reference gives the same ratios z/l and
+// L^E = m + ln l, so the result is exact as long as nothing overflows. The
+// scan therefore runs with m fixed at 0 and checks the row total at the end:
+// every weight is at most l, so l <= 2^64 bounds every weight and |z|. A wave
+// with a row above that rescans with a lazy reference, raised only when a
+// block's largest E exceeds it by more than 8 (in log2 units), which keeps
+// every exp2 argument <= 8.
 //
 // K/V tiles of 64 keys go HBM -> LDS by buffer loads that write LDS directly
 // (no staging registers), into two buffers with one barrier per tile; four
@@ -22,7 +24,6 @@
 #include "kernels.h"
 
 #include <type_traits>
-
 
 namespace rel {
 
