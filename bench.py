@@ -231,6 +231,33 @@ def copy_mode(nbytes: int, reps: int, kind: str) -> None:
     print(json.dumps({"copy_bytes": nbytes, "reps": reps, "kind": kind}), flush=True)
 
 
+def materialized_backward(w, q, k, v, do, lam_t, fwd_ms, bwd_ms, mat_fwd_ms, K, args):
+    """Time the materialised backward (U and H = dO V^T in HBM, dU and F written
+    for the three gradient GEMMs) and compare whole steps."""
+    import torch
+    from paper_2608_20172_amd import binding as R
+    need = R.relation_bwd_materialized_workspace_bytes(q)
+    if need > MATERIALIZED_BUDGET:
+        return {"bwd_status": f"skipped: T x T workspace {need / 2**30:.1f} GiB exceeds the "
+                              f"{MATERIALIZED_BUDGET / 2**30:.0f} GiB budget"}
+    mws = torch.empty(need, dtype=torch.uint8, device=q.device)
+    for _ in range(max(2, args.warmup)):
+        R.relation_bwd_materialized(q, k, v, do, lam_t, workspace=mws)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    mk = max(5, K // 2)
+    e0.record()
+    for _ in range(mk):
+        R.relation_bwd_materialized(q, k, v, do, lam_t, workspace=mws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / mk
+    del mws
+    return {"bwd_status": "ok", "bwd_ms": ms, "speedup_bwd": ms / bwd_ms,
+            "step_ms": mat_fwd_ms + ms, "speedup_step": (mat_fwd_ms + ms) / (fwd_ms + bwd_ms)}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -375,6 +402,8 @@ def main() -> int:
             mat = {"status": "ok", "fwd_ms": mat_ms, "speedup_fwd": mat_ms / fwd_ms,
                    "txt_hbm_GBps": tt_bytes / (mat_ms * 1e-3) / 1e9}
             del mws
+            if w.backward:
+                mat.update(materialized_backward(w, q, k, v, do, lam_t, fwd_ms, bwd_ms, mat_ms, K, args))
 
     fl_f, fl_b = flops(w, "fwd"), flops(w, "bwd") if w.backward else 0.0
     kern_flops = fl_b if w.backward else fl_f

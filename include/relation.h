@@ -133,6 +133,29 @@ rel_status relation_fwd_materialized(const rel_problem* p, const void* q, const 
                                      float* F, float* pi, float* self_mass, float* exch_mass,
                                      void* workspace, size_t workspace_bytes, void* stream);
 
+/* Materialised backward pass (App. A.1.7 with every T x T tensor in HBM): the
+ * baseline of the fused backward. U = scale q k^T and H = dout v^T are
+ * written by rocBLAS batched GEMMs; a row kernel forms F_i = softmax(R_i) again
+ * from U_i, D_i = sum_j F_ij H_ij, dR_ij = F_ij (H_ij - D_i) and
+ * dU_ij = dR_ij SiLU'(U_ij) (j < i), dU_ii = dR_ii S_i (1 - S_i) / tau_S, and
+ * the row's term -ln(i) sum_{j<i} dR_ij of dlambda; three GEMMs form
+ * dq = scale dU k, dk = scale dU^T q, dv = F^T dout.
+ *   q, k, v, dout  in [B,H,T,D] dtype; lambda in device fp32 scalar
+ *   dq, dk, dv     out [B,H,T,D] dtype (overwritten)
+ *   dlambda        out device fp32 scalar, the row terms summed in a fixed order
+ *   workspace      at least relation_bwd_materialized_workspace_bytes(p) bytes,
+ *                  16-byte aligned: U and H in fp32, dU and F in dtype, one
+ *                  fp32 per row; i.e. B*H*T*T*(8 + 2 sizeof(dtype)) + 4 B*H*T
+ *                  bytes (with 256-byte alignment of each part). Contents on
+ *                  entry are ignored.
+ *   T*T < 2^31 and 8 T <= 159 KiB (two rows of fp32 in LDS), else
+ *   REL_ERR_UNSUPPORTED. */
+size_t relation_bwd_materialized_workspace_bytes(const rel_problem* p);
+rel_status relation_bwd_materialized(const rel_problem* p, const void* q, const void* k,
+                                     const void* v, const void* dout, const float* lambda, void* dq,
+                                     void* dk, void* dv, float* dlambda, void* workspace,
+                                     size_t workspace_bytes, void* stream);
+
 /* Measurement aid. While armed, every launch of the named kernel ("fwd": the
  * fused forward kernel; "bwd_dkdv", "bwd_dq": the two backward kernels; "bwd":
  * both backward kernels, back to back) is bracketed by

@@ -3,9 +3,9 @@ step of the operator runs in the library's HIP kernels; torch provides device
 memory and the current stream.
 
 Functions carry the C-ABI names (relation_fwd, relation_bwd,
-relation_fwd_materialized, relation_exchange_allocation, ...). ``relation`` is
-the differentiable wrapper (torch.autograd.Function) over relation_fwd /
-relation_bwd.
+relation_fwd_materialized, relation_bwd_materialized,
+relation_exchange_allocation, ...). ``relation`` is the differentiable wrapper
+(torch.autograd.Function) over relation_fwd / relation_bwd.
 """
 from __future__ import annotations
 
@@ -43,6 +43,9 @@ _SIGS = {
     "relation_fwd_materialized_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(RelProblem)]),
     "relation_fwd_materialized": (ctypes.c_int, [ctypes.POINTER(RelProblem), _P, _P, _P, _P, _P, _P, _P,
                                                  _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "relation_bwd_materialized_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(RelProblem)]),
+    "relation_bwd_materialized": (ctypes.c_int, [ctypes.POINTER(RelProblem), _P, _P, _P, _P, _P, _P, _P, _P,
+                                                 _P, _P, ctypes.c_size_t, _P]),
     "relation_profile_arm": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]),
     "relation_profile_disarm": (ctypes.c_int, []),
     "relation_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -229,6 +232,34 @@ def relation_fwd_materialized(q, k, v, lam, *, tau_s: float = TAU_S, scale: Opti
                                        workspace.numel() * workspace.element_size(), _stream())
     _check(st, "relation_fwd_materialized")
     return {"o": o, "R": R, "F": F, "pi": pi, "self_mass": sm, "exch_mass": em}
+
+
+def relation_bwd_materialized_workspace_bytes(q, *, tau_s: float = TAU_S,
+                                              scale: Optional[float] = None) -> int:
+    lib = load_library()
+    p = make_problem(q, tau_s, scale)
+    return int(lib.relation_bwd_materialized_workspace_bytes(ctypes.byref(p)))
+
+
+def relation_bwd_materialized(q, k, v, dout, lam, *, tau_s: float = TAU_S, scale: Optional[float] = None,
+                              workspace=None):
+    """Materialised backward baseline (every T x T tensor in HBM). Returns
+    dict(dq, dk, dv, dlambda (1-element fp32 tensor))."""
+    lib = load_library()
+    k, v, dout = _same_layout(q, k, v, dout)
+    p = make_problem(q, tau_s, scale)
+    dev = q.device
+    lam_t = _lam_tensor(lam, dev)
+    dq, dk, dv = _layout_like(q), _layout_like(q), _layout_like(q)
+    dlam = torch.empty((1,), dtype=torch.float32, device=dev)
+    nbytes = int(lib.relation_bwd_materialized_workspace_bytes(ctypes.byref(p)))
+    if workspace is None or workspace.numel() * workspace.element_size() < nbytes:
+        workspace = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=dev)
+    st = lib.relation_bwd_materialized(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(dout), _ptr(lam_t),
+                                       _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dlam), _ptr(workspace),
+                                       workspace.numel() * workspace.element_size(), _stream())
+    _check(st, "relation_bwd_materialized")
+    return {"dq": dq, "dk": dk, "dv": dv, "dlambda": dlam}
 
 
 def relation_profile_arm(kernel: str, events: list) -> None:

@@ -70,6 +70,18 @@ struct RowArgs {
   float inv_tau;
 };
 
+// Arguments of the materialised backward row kernel (one workgroup per row).
+struct RowBwdArgs {
+  const float* U;      // [N, T, T] scale * q k^T
+  const float* Hm;     // [N, T, T] dO v^T
+  const float* lambda;
+  void* dUw;           // out: dU in the storage dtype (GEMM operand), zeros above the diagonal
+  void* Fw;            // out: F in the storage dtype (GEMM operand), zeros above the diagonal
+  float* dlam_row;     // out: [N, T] per-row terms of dlambda
+  int T;
+  float inv_tau;
+};
+
 // Measurement aid: if armed for kernel `name`, returns the event pair to record
 // around the next launch of that kernel (see relation_profile_arm).
 bool profile_slot(const char* name, hipEvent_t* start, hipEvent_t* stop);
@@ -80,5 +92,7 @@ int bwd_partials(int N, int T, int D, int dtype);
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t stream);
 hipError_t launch_allocation(const RowArgs& a, int dtype, int N, hipStream_t stream);
 hipError_t launch_materialized_rows(const RowArgs& a, int dtype, int N, hipStream_t stream);
+hipError_t launch_materialized_bwd_rows(const RowBwdArgs& a, int dtype, int N, hipStream_t stream);
+hipError_t launch_sum_fixed_order(const float* x, int64_t n, float* out, hipStream_t stream);
 
 }  // namespace rel

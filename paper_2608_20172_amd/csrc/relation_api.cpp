@@ -180,6 +180,24 @@ std::mutex g_blas_mu;
 rocblas_handle g_blas = nullptr;
 int g_blas_dev = -1;
 
+// The rocBLAS handle of the current device, bound to `stream`. Call with
+// g_blas_mu held.
+rel_status blas_on_stream(void* stream) {
+  int dev = 0;
+  hipError_t he = hipGetDevice(&dev);
+  if (he != hipSuccess) return hip_fail(he, "hipGetDevice");
+  if (!g_blas || g_blas_dev != dev) {
+    if (g_blas) rocblas_destroy_handle(g_blas);
+    g_blas = nullptr;
+    if (rocblas_create_handle(&g_blas) != rocblas_status_success)
+      return fail(REL_ERR_HIP, "rocblas_create_handle failed");
+    g_blas_dev = dev;
+  }
+  if (rocblas_set_stream(g_blas, (hipStream_t)stream) != rocblas_status_success)
+    return fail(REL_ERR_HIP, "rocblas_set_stream failed");
+  return REL_OK;
+}
+
 // Measurement aid state (relation_profile_arm).
 std::mutex g_prof_mu;
 std::string g_prof_name;
@@ -447,18 +465,8 @@ rel_status relation_fwd_materialized(const rel_problem* p, const void* q, const 
   const rocblas_datatype io = p->dtype == REL_BF16 ? rocblas_datatype_bf16_r : rocblas_datatype_f32_r;
 
   std::lock_guard<std::mutex> lock(g_blas_mu);
-  int dev = 0;
-  hipError_t he = hipGetDevice(&dev);
-  if (he != hipSuccess) return hip_fail(he, "hipGetDevice");
-  if (!g_blas || g_blas_dev != dev) {
-    if (g_blas) rocblas_destroy_handle(g_blas);
-    g_blas = nullptr;
-    if (rocblas_create_handle(&g_blas) != rocblas_status_success)
-      return fail(REL_ERR_HIP, "rocblas_create_handle failed");
-    g_blas_dev = dev;
-  }
-  if (rocblas_set_stream(g_blas, (hipStream_t)stream) != rocblas_status_success)
-    return fail(REL_ERR_HIP, "rocblas_set_stream failed");
+  REL_TRY(blas_on_stream(stream));
+  hipError_t he = hipSuccess;
 
   const float one = 1.0f, zero = 0.0f;
   // Heads of one batch index are equally spaced by stride_h, so each GEMM call
@@ -496,6 +504,135 @@ rel_status relation_fwd_materialized(const rel_problem* p, const void* q, const 
         (rocblas_int)p->H, rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
     if (st != rocblas_status_success) return fail(REL_ERR_HIP, "rocBLAS F.V GEMM failed (%d)", (int)st);
   }
+  return REL_OK;
+}
+
+size_t relation_bwd_materialized_workspace_bytes(const rel_problem* p) {
+  bool empty = false;
+  if (check_problem(p, &empty) != REL_OK) return 0;
+  if (empty) return 0;
+  const size_t N = (size_t)(p->B * p->H);
+  const size_t NTT = N * (size_t)p->T * (size_t)p->T;
+  const size_t es = elem_size(p->dtype);
+  return 2 * align256(NTT * 4) + 2 * align256(NTT * es) + align256(N * (size_t)p->T * 4);
+}
+
+rel_status relation_bwd_materialized(const rel_problem* p, const void* q, const void* k,
+                                     const void* v, const void* dout, const float* lambda, void* dq,
+                                     void* dk, void* dv, float* dlambda, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
+  bool empty = false;
+  REL_TRY(check_problem(p, &empty));
+  if (empty) {
+    if (dlambda) {
+      if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected");
+      hipError_t e = rel::launch_fill_zero(dlambda, 1, (hipStream_t)stream);
+      if (e != hipSuccess) return hip_fail(e, "relation_bwd_materialized dlambda clear");
+    }
+    return REL_OK;
+  }
+  REL_TRY(check_aligned(q, 16, "q", true));
+  REL_TRY(check_aligned(k, 16, "k", true));
+  REL_TRY(check_aligned(v, 16, "v", true));
+  REL_TRY(check_aligned(dout, 16, "dout", true));
+  REL_TRY(check_aligned(dq, 16, "dq", true));
+  REL_TRY(check_aligned(dk, 16, "dk", true));
+  REL_TRY(check_aligned(dv, 16, "dv", true));
+  REL_TRY(check_aligned(lambda, 4, "lambda", true));
+  REL_TRY(check_aligned(dlambda, 4, "dlambda", true));
+  if (p->T > 65536 || (p->T * (int64_t)p->T) > (1LL << 31))
+    return fail(REL_ERR_UNSUPPORTED, "materialised path limited to T*T < 2^31 per head");
+  if (2 * p->T * 4 > 159 * 1024)
+    return fail(REL_ERR_UNSUPPORTED, "materialised backward keeps two fp32 rows in LDS: T <= %d",
+                (int)(159 * 1024 / 8));
+  const size_t need = relation_bwd_materialized_workspace_bytes(p);
+  if (!workspace || workspace_bytes < need)
+    return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                workspace ? workspace_bytes : (size_t)0);
+  if ((uintptr_t)workspace % 16) return fail(REL_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
+  const size_t es = elem_size(p->dtype);
+  const size_t tb = (size_t)extent_elems(p) * es;
+  REL_TRY(check_buffers(p, {{q, tb, true, false, "q"},
+                            {k, tb, true, false, "k"},
+                            {v, tb, true, false, "v"},
+                            {dout, tb, true, false, "dout"},
+                            {lambda, 4, false, false, "lambda"},
+                            {dq, tb, true, true, "dq"},
+                            {dk, tb, true, true, "dk"},
+                            {dv, tb, true, true, "dv"},
+                            {dlambda, 4, false, true, "dlambda"},
+                            {workspace, need, false, true, "workspace"}}));
+  if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected by RELATION_TEST_FAIL_LAUNCH");
+
+  const int T = (int)p->T, D = (int)p->D;
+  const size_t N = (size_t)(p->B * p->H);
+  const size_t NTT = N * (size_t)T * (size_t)T;
+  const float scale = eff_scale(p);
+  char* ws = (char*)workspace;
+  float* U = (float*)ws;
+  float* Hm = (float*)(ws + align256(NTT * 4));
+  void* dUw = ws + 2 * align256(NTT * 4);
+  void* Fw = ws + 2 * align256(NTT * 4) + align256(NTT * es);
+  float* dlam_row = (float*)(ws + 2 * align256(NTT * 4) + 2 * align256(NTT * es));
+  const rocblas_datatype io = p->dtype == REL_BF16 ? rocblas_datatype_bf16_r : rocblas_datatype_f32_r;
+  const rocblas_stride sTT = (rocblas_stride)T * T;
+  const rocblas_int ld = (rocblas_int)p->stride_t, nh = (rocblas_int)p->H;
+
+  std::lock_guard<std::mutex> lock(g_blas_mu);
+  REL_TRY(blas_on_stream(stream));
+  const float one = 1.0f, zero = 0.0f;
+  // Row-major T x T results are column-major transposes: X^T = B^T A^T.
+  for (int64_t b = 0; b < p->B; ++b) {
+    const size_t off = (size_t)(b * p->stride_b) * es;
+    const char *qb = (const char*)q + off, *kb = (const char*)k + off, *vb = (const char*)v + off;
+    const char* gb = (const char*)dout + off;
+    float* Ub = U + (size_t)b * p->H * T * (size_t)T;
+    float* Hb = Hm + (size_t)b * p->H * T * (size_t)T;
+    // U = scale q k^T (eq. 1) and H = dout v^T
+    rocblas_status st = rocblas_gemm_strided_batched_ex(
+        g_blas, rocblas_operation_transpose, rocblas_operation_none, T, T, D, &scale, kb, io, ld, p->stride_h,
+        qb, io, ld, p->stride_h, &zero, Ub, rocblas_datatype_f32_r, T, sTT, Ub, rocblas_datatype_f32_r, T, sTT, nh,
+        rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
+    if (st != rocblas_status_success) return fail(REL_ERR_HIP, "rocBLAS U GEMM failed (%d)", (int)st);
+    st = rocblas_gemm_strided_batched_ex(
+        g_blas, rocblas_operation_transpose, rocblas_operation_none, T, T, D, &one, vb, io, ld, p->stride_h, gb,
+        io, ld, p->stride_h, &zero, Hb, rocblas_datatype_f32_r, T, sTT, Hb, rocblas_datatype_f32_r, T, sTT, nh,
+        rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
+    if (st != rocblas_status_success) return fail(REL_ERR_HIP, "rocBLAS H GEMM failed (%d)", (int)st);
+  }
+  rel::RowBwdArgs a{};
+  a.U = U; a.Hm = Hm; a.lambda = lambda; a.dUw = dUw; a.Fw = Fw; a.dlam_row = dlam_row;
+  a.T = T;
+  a.inv_tau = 1.0f / p->tau_s;
+  hipError_t he = rel::launch_materialized_bwd_rows(a, p->dtype, (int)N, (hipStream_t)stream);
+  if (he != hipSuccess) return hip_fail(he, "materialised backward row kernel launch");
+  for (int64_t b = 0; b < p->B; ++b) {
+    const size_t off = (size_t)(b * p->stride_b) * es;
+    const char *qb = (const char*)q + off, *kb = (const char*)k + off, *gb = (const char*)dout + off;
+    char *dqb = (char*)dq + off, *dkb = (char*)dk + off, *dvb = (char*)dv + off;
+    const char* dUb = (const char*)dUw + (size_t)b * p->H * T * (size_t)T * es;
+    const char* Fb = (const char*)Fw + (size_t)b * p->H * T * (size_t)T * es;
+    // dq^T (D x T) = k^T dU^T: row-major dq = scale dU k
+    rocblas_status st = rocblas_gemm_strided_batched_ex(
+        g_blas, rocblas_operation_none, rocblas_operation_none, D, T, T, &scale, kb, io, ld, p->stride_h, dUb,
+        io, T, sTT, &zero, dqb, io, ld, p->stride_h, dqb, io, ld, p->stride_h, nh, rocblas_datatype_f32_r,
+        rocblas_gemm_algo_standard, 0, 0);
+    if (st != rocblas_status_success) return fail(REL_ERR_HIP, "rocBLAS dq GEMM failed (%d)", (int)st);
+    // dk^T (D x T) = q^T dU: row-major dk = scale dU^T q
+    st = rocblas_gemm_strided_batched_ex(
+        g_blas, rocblas_operation_none, rocblas_operation_transpose, D, T, T, &scale, qb, io, ld, p->stride_h,
+        dUb, io, T, sTT, &zero, dkb, io, ld, p->stride_h, dkb, io, ld, p->stride_h, nh, rocblas_datatype_f32_r,
+        rocblas_gemm_algo_standard, 0, 0);
+    if (st != rocblas_status_success) return fail(REL_ERR_HIP, "rocBLAS dk GEMM failed (%d)", (int)st);
+    // dv^T (D x T) = dout^T F: row-major dv = F^T dout
+    st = rocblas_gemm_strided_batched_ex(
+        g_blas, rocblas_operation_none, rocblas_operation_transpose, D, T, T, &one, gb, io, ld, p->stride_h, Fb,
+        io, T, sTT, &zero, dvb, io, ld, p->stride_h, dvb, io, ld, p->stride_h, nh, rocblas_datatype_f32_r,
+        rocblas_gemm_algo_standard, 0, 0);
+    if (st != rocblas_status_success) return fail(REL_ERR_HIP, "rocBLAS dv GEMM failed (%d)", (int)st);
+  }
+  he = rel::launch_sum_fixed_order(dlam_row, (int64_t)N * T, dlambda, (hipStream_t)stream);
+  if (he != hipSuccess) return hip_fail(he, "dlambda reduction launch");
   return REL_OK;
 }
 

@@ -93,6 +93,29 @@ def check_backward(x, dtype, fwd, heads=None, rows=None, row_block=256, key_from
     return g
 
 
+def check_materialized_backward(x, dtype, heads=None):
+    """Materialised backward (rocBLAS GEMMs + the row kernel) vs the oracle."""
+    B, H, T, D = x["q"].shape
+    log(f"[mat bwd] B={B} H={H} T={T} D={D} {dtype}")
+    g = R.relation_bwd_materialized(x["q"], x["k"], x["v"], x["do"], x["lam"])
+    torch.cuda.synchronize()
+    all_heads = heads is None
+    heads = heads or [(b, h) for b in range(B) for h in range(H)]
+    dq, dk, dv = _np(g["dq"]), _np(g["dk"]), _np(g["dv"])
+    dlam_ref, terms = 0.0, 0.0
+    for (b, h) in heads:
+        r = oracle.backward(x["qr"][b, h], x["kr"][b, h], x["vr"][b, h], x["lam"], x["dor"][b, h],
+                            row_block=256)
+        assert_close(f"mat.dq[{b},{h}]", dq[b, h], r["dq"], dtype)
+        assert_close(f"mat.dk[{b},{h}]", dk[b, h], r["dk"], dtype)
+        assert_close(f"mat.dv[{b},{h}]", dv[b, h], r["dv"], dtype)
+        dlam_ref += r["dlam"]
+        terms += float(np.sum(np.abs(np.log(r["rows"] + 1.0) * r["dS"])))
+    if all_heads:
+        assert_scalar_close("mat.dlambda", float(g["dlambda"].item()), dlam_ref, terms, dtype)
+    return g
+
+
 # ----------------------------------------------------------------------------
 # the small fp32 workload: 1 x 2 heads, T=128, D=32, forward with R, F, masses
 # ----------------------------------------------------------------------------
@@ -205,6 +228,21 @@ def test_backward_edge_lengths(T):
         assert np.allclose(_np(g["dv"]), x["dor"], atol=0)
 
 
+@pytest.mark.parametrize("dtype,T", [("f32", 190), ("bf16", 300), ("bf16", 1), ("bf16", 2), ("bf16", 129)])
+def test_materialized_backward(dtype, T):
+    std = 1.0 if dtype == "f32" else 0.125
+    x = _prep(I.make_inputs(2 if dtype == "bf16" else 1, 2, T, 64, seed=40 + T, qkv_std=std, lam=0.4), dtype)
+    g = check_materialized_backward(x, dtype)
+    if T == 1:
+        assert not _np(g["dq"]).any() and not _np(g["dk"]).any()
+        assert np.allclose(_np(g["dv"]), x["dor"], atol=0)
+
+
+def test_materialized_backward_sharp():
+    x = _prep(I.make_sharp_inputs(1, 2, 260, 64, seed=43, lam=0.5), "f32")
+    check_materialized_backward(x, "f32")
+
+
 def test_strided_layout_matches_contiguous():
     """[B, T, H, D] storage (head stride D) gives the same results as [B, H, T, D]."""
     inp = I.make_inputs(2, 3, 150, 64, seed=21, qkv_std=0.125, lam=0.5)
@@ -286,7 +324,17 @@ def test_workload_dec100m_forward_backward():
     bh = np.argwhere(mask.any(axis=2))[0]
     heads.append((int(bh[0]), int(bh[1])))
     f = check_forward(x, "bf16", heads=heads)
-    check_backward(x, "bf16", f, heads=heads)
+    g = check_backward(x, "bf16", f, heads=heads)
+    # the materialised backward on the same layer: oracle on two heads, and the
+    # fused gradients on every head
+    m = check_materialized_backward(x, "bf16", heads=heads[:2])
+    for n in ("dq", "dk", "dv"):
+        assert_close(f"flash vs materialised {n}", _np(g[n]), _np(m[n]), "bf16")
+    dl_f, dl_m = float(g["dlambda"].item()), float(m["dlambda"].item())
+    log(f"  dlambda flash {dl_f:.6e} materialised {dl_m:.6e}")
+    lnw = np.log(np.arange(1, w.T + 1, dtype=np.float64))
+    terms = float(np.abs(lnw[None, None, :] * _np(g["dself"])).sum())
+    assert abs(dl_f - dl_m) <= 2e-2 * max(abs(dl_f), 1e-3 * terms)
 
 
 def test_workload_long_context_sampled():
