@@ -145,11 +145,11 @@ rel_status relation_fwd_materialized(const rel_problem* p, const void* q, const 
  *   dlambda        out device fp32 scalar, the row terms summed in a fixed order
  *   workspace      at least relation_bwd_materialized_workspace_bytes(p) bytes,
  *                  16-byte aligned: U and H in fp32, dU and F in dtype, one
- *                  fp32 per row; i.e. B*H*T*T*(8 + 2 sizeof(dtype)) + 4 B*H*T
- *                  bytes (with 256-byte alignment of each part). Contents on
- *                  entry are ignored.
- *   T*T < 2^31 and 8 T <= 159 KiB (two rows of fp32 in LDS), else
- *   REL_ERR_UNSUPPORTED. */
+ *                  fp32 per row and 256 fp32 partial sums; i.e.
+ *                  B*H*T*T*(8 + 2 sizeof(dtype)) + 4 B*H*T + 1024 bytes (with
+ *                  256-byte alignment of each part). Contents on entry are
+ *                  ignored.
+ *   T <= 65536 and T*T <= 2^31, else REL_ERR_UNSUPPORTED. */
 size_t relation_bwd_materialized_workspace_bytes(const rel_problem* p);
 rel_status relation_bwd_materialized(const rel_problem* p, const void* q, const void* k,
                                      const void* v, const void* dout, const float* lambda, void* dq,

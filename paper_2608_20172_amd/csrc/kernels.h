@@ -70,7 +70,7 @@ struct RowArgs {
   float inv_tau;
 };
 
-// Arguments of the materialised backward row kernel (one workgroup per row).
+// Arguments of the materialised backward row kernel (one wave per row).
 struct RowBwdArgs {
   const float* U;      // [N, T, T] scale * q k^T
   const float* Hm;     // [N, T, T] dO v^T
@@ -93,6 +93,8 @@ hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t stream);
 hipError_t launch_allocation(const RowArgs& a, int dtype, int N, hipStream_t stream);
 hipError_t launch_materialized_rows(const RowArgs& a, int dtype, int N, hipStream_t stream);
 hipError_t launch_materialized_bwd_rows(const RowBwdArgs& a, int dtype, int N, hipStream_t stream);
-hipError_t launch_sum_fixed_order(const float* x, int64_t n, float* out, hipStream_t stream);
+// Fixed-order sum of n floats; `partial` holds sum_fixed_order_parts() floats.
+int sum_fixed_order_parts();
+hipError_t launch_sum_fixed_order(const float* x, int64_t n, float* partial, float* out, hipStream_t stream);
 
 }  // namespace rel

@@ -435,7 +435,7 @@ rel_status relation_fwd_materialized(const rel_problem* p, const void* q, const 
   REL_TRY(check_aligned(self_mass, 4, "self_mass", false));
   REL_TRY(check_aligned(exch_mass, 4, "exch_mass", false));
   if (p->T > 65536 || (p->T * (int64_t)p->T) > (1LL << 31))
-    return fail(REL_ERR_UNSUPPORTED, "materialised path limited to T*T < 2^31 per head");
+    return fail(REL_ERR_UNSUPPORTED, "materialised path limited to T <= 65536 and T*T <= 2^31 per head");
   const size_t need = relation_fwd_materialized_workspace_bytes(p);
   if (!workspace || workspace_bytes < need)
     return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
@@ -514,7 +514,8 @@ size_t relation_bwd_materialized_workspace_bytes(const rel_problem* p) {
   const size_t N = (size_t)(p->B * p->H);
   const size_t NTT = N * (size_t)p->T * (size_t)p->T;
   const size_t es = elem_size(p->dtype);
-  return 2 * align256(NTT * 4) + 2 * align256(NTT * es) + align256(N * (size_t)p->T * 4);
+  return 2 * align256(NTT * 4) + 2 * align256(NTT * es) + align256(N * (size_t)p->T * 4) +
+         align256((size_t)rel::sum_fixed_order_parts() * 4);
 }
 
 rel_status relation_bwd_materialized(const rel_problem* p, const void* q, const void* k,
@@ -541,10 +542,7 @@ rel_status relation_bwd_materialized(const rel_problem* p, const void* q, const 
   REL_TRY(check_aligned(lambda, 4, "lambda", true));
   REL_TRY(check_aligned(dlambda, 4, "dlambda", true));
   if (p->T > 65536 || (p->T * (int64_t)p->T) > (1LL << 31))
-    return fail(REL_ERR_UNSUPPORTED, "materialised path limited to T*T < 2^31 per head");
-  if (2 * p->T * 4 > 159 * 1024)
-    return fail(REL_ERR_UNSUPPORTED, "materialised backward keeps two fp32 rows in LDS: T <= %d",
-                (int)(159 * 1024 / 8));
+    return fail(REL_ERR_UNSUPPORTED, "materialised path limited to T <= 65536 and T*T <= 2^31 per head");
   const size_t need = relation_bwd_materialized_workspace_bytes(p);
   if (!workspace || workspace_bytes < need)
     return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
@@ -574,6 +572,7 @@ rel_status relation_bwd_materialized(const rel_problem* p, const void* q, const 
   void* dUw = ws + 2 * align256(NTT * 4);
   void* Fw = ws + 2 * align256(NTT * 4) + align256(NTT * es);
   float* dlam_row = (float*)(ws + 2 * align256(NTT * 4) + 2 * align256(NTT * es));
+  float* dlam_part = (float*)((char*)dlam_row + align256(N * (size_t)T * 4));
   const rocblas_datatype io = p->dtype == REL_BF16 ? rocblas_datatype_bf16_r : rocblas_datatype_f32_r;
   const rocblas_stride sTT = (rocblas_stride)T * T;
   const rocblas_int ld = (rocblas_int)p->stride_t, nh = (rocblas_int)p->H;
@@ -631,7 +630,7 @@ rel_status relation_bwd_materialized(const rel_problem* p, const void* q, const 
         rocblas_gemm_algo_standard, 0, 0);
     if (st != rocblas_status_success) return fail(REL_ERR_HIP, "rocBLAS dv GEMM failed (%d)", (int)st);
   }
-  he = rel::launch_sum_fixed_order(dlam_row, (int64_t)N * T, dlambda, (hipStream_t)stream);
+  he = rel::launch_sum_fixed_order(dlam_row, (int64_t)N * T, dlam_part, dlambda, (hipStream_t)stream);
   if (he != hipSuccess) return hip_fail(he, "dlambda reduction launch");
   return REL_OK;
 }

@@ -147,16 +147,16 @@ def test_materialized_backward_workspace(lib):
     p = prob(T=256)
     need = lib.relation_bwd_materialized_workspace_bytes(ctypes.byref(p))
     # U and H in fp32, dU and F in bf16, one fp32 dlambda term per row
-    assert need >= 2 * 256 * 256 * (2 * 4 + 2 * 2) + 2 * 256 * 4
+    assert need >= 2 * 256 * 256 * (2 * 4 + 2 * 2) + 2 * 256 * 4 + 256 * 4
     a = ptrs(12)
     call = lambda pp, ws, n: lib.relation_bwd_materialized(ctypes.byref(pp), a[0], a[1], a[2], a[3], a[4],
                                                            a[5], a[6], a[7], a[8], ws, n, None)
     assert call(p, a[9], need - 1) == R.REL_ERR_WORKSPACE
     assert call(p, None, need) == R.REL_ERR_WORKSPACE
     assert call(p, a[9], need) == R.REL_ERR_HIP  # valid request; fails only at the device
-    # two fp32 rows of T in LDS per workgroup bound T
-    big = prob(B=1, H=1, T=20480)
-    assert call(big, a[9], 1 << 40) == R.REL_ERR_UNSUPPORTED
+    # T x T per head must stay within 2^31 elements
+    big = prob(B=1, H=1, T=46341)
+    assert call(big, a[9], 1 << 45) == R.REL_ERR_UNSUPPORTED
     assert lib.relation_bwd_materialized_workspace_bytes(ctypes.byref(prob(T=0))) == 0
     assert lib.relation_bwd_materialized_workspace_bytes(None) == 0
 

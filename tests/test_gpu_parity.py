@@ -228,6 +228,25 @@ def test_backward_edge_lengths(T):
         assert np.allclose(_np(g["dv"]), x["dor"], atol=0)
 
 
+@pytest.mark.parametrize("dtype,T", [("f32", 131), ("bf16", 1), ("bf16", 2), ("bf16", 300)])
+def test_materialized_forward(dtype, T):
+    """Materialised forward at lengths off the 4-element row vectors (T % 4 != 0)
+    and on them, against the oracle: o, R, F, pi and the masses."""
+    std = 1.0 if dtype == "f32" else 0.125
+    x = _prep(I.make_inputs(1, 2, T, 64, seed=60 + T, qkv_std=std, lam=0.4), dtype)
+    m = R.relation_fwd_materialized(x["q"], x["k"], x["v"], x["lam"], want_R=True, want_F=True,
+                                    want_pi=True, want_masses=True)
+    torch.cuda.synchronize()
+    for h in range(2):
+        f = oracle.forward(x["qr"][0, h], x["kr"][0, h], x["vr"][0, h], x["lam"])
+        assert_close(f"mat.o[0,{h}]", _np(m["o"])[0, h], f["Y"], dtype)
+        # the T x T outputs are fp32 in both dtypes, from logits of the rounded inputs
+        for n, ref in (("R", f["R"]), ("F", f["F"]), ("pi", f["pi"])):
+            assert_close(f"mat.{n}[0,{h}]", _np(m[n])[0, h], ref, dtype)
+        assert_close(f"mat.self_mass[0,{h}]", _np(m["self_mass"])[0, h], f["self_mass"], dtype)
+        assert_close(f"mat.exch_mass[0,{h}]", _np(m["exch_mass"])[0, h], f["exch_mass"], dtype)
+
+
 @pytest.mark.parametrize("dtype,T", [("f32", 190), ("bf16", 300), ("bf16", 1), ("bf16", 2), ("bf16", 129)])
 def test_materialized_backward(dtype, T):
     std = 1.0 if dtype == "f32" else 0.125
