@@ -1,6 +1,8 @@
-"""fp64 CPU oracle for the causal Full Relation operator.
+"""fp64 CPU oracle for the causal Full Relation operator and the steps around
+it in a layer (RoPE on the relation projections, Givens head-pair mixing).
 
 TEST INFRASTRUCTURE: only tests, the smoke check and the benchmark's CPU
 baseline import this package; the product path never does.
 """
 from .relation_oracle import forward, backward, forward_batched, backward_batched, TAU_S  # noqa: F401
+from . import layer_oracle  # noqa: F401
