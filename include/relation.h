@@ -62,14 +62,16 @@ typedef enum rel_dtype {
 } rel_dtype;
 
 typedef struct rel_problem {
-  int64_t B, H, T, D;   /* batch, heads, sequence length, head width. D in {32, 64, 128} */
+  int64_t B, H, T, D;   /* batch, heads, sequence length, head width. D in {32, 64, 128}
+                           (the layer entry points take any D <= 128) */
   int32_t dtype;        /* rel_dtype of q, k, v, o, dout, dq, dk, dv */
   int32_t causal;       /* must be 1: the paper defines only the causal R (eq. 2) */
   float tau_s;          /* Self temperature, finite and > 0 (paper: 2.0) */
   float scale;          /* multiplier inside U; <= 0 selects 1/sqrt(D) (eq. 1) */
   int64_t stride_b;     /* element strides shared by all [B,H,T,D] tensors; */
   int64_t stride_h;     /* the last dimension is contiguous. stride_t must be a */
-  int64_t stride_t;     /* multiple of 16 bytes / element size and >= D */
+  int64_t stride_t;     /* multiple of 16 bytes / element size and >= D (any
+                           multiple of the element size for the layer entry points) */
 } rel_problem;
 
 /* Forward pass (FlashRelation, Sec. 5.1).
@@ -155,6 +157,62 @@ rel_status relation_bwd_materialized(const rel_problem* p, const void* q, const 
                                      const void* v, const void* dout, const float* lambda, void* dq,
                                      void* dk, void* dv, float* dlambda, void* workspace,
                                      size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Layer entry points: the operator together with the steps that surround it in
+ * a Relation layer (Sec. 3.1 and eq. 4; App. A.2.2-A.2.3; App. B):
+ *   q, k  -> RoPE over the full head width, channel d turned with channel
+ *            d + D/2 by t * rope_base^(-2d/D), t the zero-based position;
+ *   v     -> Givens mixing of head pairs: for pair p = (a, b),
+ *            v~_a = cos(theta_p) v_a - sin(theta_p) v_b,
+ *            v~_b = sin(theta_p) v_a + cos(theta_p) v_b,
+ *            pairing A = (1,2), (3,4), ..., (H-1,H), pairing B = (2,3), (4,5),
+ *            ..., (H,1) (one-based heads; the pairing alternates over depth);
+ *   y     =  the causal Full Relation of (RoPE(q), RoPE(k), v~).
+ * Here p->D is the true head width d_h: any D <= 128 (even when RoPE is on).
+ * Widths the fused kernels do not tile (e.g. the paper's 48, 60, 80) are run
+ * with zero channels appended up to 32, 64 or 128; scale <= 0 still means
+ * 1/sqrt(d_h) of the true width. Strides need only be multiples of the
+ * element size here.
+ *   opts        rope_base > 0 turns RoPE on (the paper uses 1e4), 0 off;
+ *               givens = REL_GIVENS_NONE / _A / _B (H even for A and B).
+ *   theta       device fp32 [H/2] angles (read when givens != NONE).
+ *   out         [B,H,T,D] dtype: y.   row_stat  [B,H,T] fp32: M_i for the
+ *               backward pass (as relation_fwd).
+ *   workspace   relation_layer_*_workspace_bytes(p, opts) bytes, 16-byte
+ *               aligned, contents ignored on entry: the prepared (rotated,
+ *               mixed, padded) operands [B,H,T,DP], a [T, D/2] table of
+ *               cos/sin, and, for the backward pass, padded copies of out and
+ *               dout, the gradients in the padded layout, relation_bwd's own
+ *               workspace and one fp32 dtheta term per (pair, b, t).
+ * The backward pass recomputes the prepared operands from q, k, v and returns
+ * dq, dk, dv with respect to the unrotated, unmixed inputs, dlambda as
+ * relation_bwd, and dtheta [H/2] fp32 (required when givens != NONE, each
+ * angle's gradient summed over batch, positions and channels in a fixed
+ * order). Results are run-to-run identical. */
+typedef enum rel_givens {
+  REL_GIVENS_NONE = 0,
+  REL_GIVENS_A = 1,
+  REL_GIVENS_B = 2
+} rel_givens;
+
+typedef struct rel_layer_opts {
+  double rope_base;  /* > 0: RoPE with this base; 0: no RoPE */
+  int32_t givens;    /* rel_givens */
+  int32_t reserved;  /* must be 0 */
+} rel_layer_opts;
+
+size_t relation_layer_fwd_workspace_bytes(const rel_problem* p, const rel_layer_opts* opts);
+rel_status relation_layer_fwd(const rel_problem* p, const rel_layer_opts* opts, const void* q,
+                              const void* k, const void* v, const float* lambda, const float* theta,
+                              void* out, float* row_stat, void* workspace, size_t workspace_bytes,
+                              void* stream);
+size_t relation_layer_bwd_workspace_bytes(const rel_problem* p, const rel_layer_opts* opts);
+rel_status relation_layer_bwd(const rel_problem* p, const rel_layer_opts* opts, const void* q,
+                              const void* k, const void* v, const void* out, const void* dout,
+                              const float* lambda, const float* theta, const float* row_stat,
+                              void* dq, void* dk, void* dv, float* dlambda, float* dtheta,
+                              void* workspace, size_t workspace_bytes, void* stream);
 
 /* Measurement aid. While armed, every launch of the named kernel ("fwd": the
  * fused forward kernel; "bwd_dkdv", "bwd_dq": the two backward kernels; "bwd":

@@ -132,5 +132,5 @@ def layer_backward(q, k, v, lam, dout, theta=None, pairing=None, rope_base: floa
         dv, dth = givens_backward(r["dv"], v, theta, pairing)
     else:
         dv, dth = r["dv"], None
-    return {"dq": dq, "dk": dk, "dv": dv, "dlam": r["dlam"], "dtheta": dth,
+    return {"dq": dq, "dk": dk, "dv": dv, "dlam": r["dlam"], "dtheta": dth, "dS": r["dS"],
             "dq_rot": r["dq"], "dk_rot": r["dk"], "dvt": r["dv"]}

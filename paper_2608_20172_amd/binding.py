@@ -4,7 +4,7 @@ memory and the current stream.
 
 Functions carry the C-ABI names (relation_fwd, relation_bwd,
 relation_fwd_materialized, relation_bwd_materialized,
-relation_exchange_allocation, ...). ``relation`` is the differentiable wrapper
+relation_exchange_allocation, relation_layer_fwd, relation_layer_bwd, ...). ``relation`` is the differentiable wrapper
 (torch.autograd.Function) over relation_fwd / relation_bwd.
 """
 from __future__ import annotations
@@ -33,7 +33,16 @@ class RelProblem(ctypes.Structure):
     ]
 
 
+class RelLayerOpts(ctypes.Structure):
+    _fields_ = [("rope_base", ctypes.c_double), ("givens", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+REL_GIVENS = {None: 0, "A": 1, "B": 2}
+ROPE_BASE = 1.0e4
+
 _P = ctypes.c_void_p
+_PP = ctypes.POINTER(RelProblem)
+_PO = ctypes.POINTER(RelLayerOpts)
 _SIGS = {
     "relation_fwd": (ctypes.c_int, [ctypes.POINTER(RelProblem), _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
     "relation_exchange_allocation": (ctypes.c_int, [ctypes.POINTER(RelProblem), _P, _P, _P, _P, _P]),
@@ -46,6 +55,11 @@ _SIGS = {
     "relation_bwd_materialized_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(RelProblem)]),
     "relation_bwd_materialized": (ctypes.c_int, [ctypes.POINTER(RelProblem), _P, _P, _P, _P, _P, _P, _P, _P,
                                                  _P, _P, ctypes.c_size_t, _P]),
+    "relation_layer_fwd_workspace_bytes": (ctypes.c_size_t, [_PP, _PO]),
+    "relation_layer_fwd": (ctypes.c_int, [_PP, _PO, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "relation_layer_bwd_workspace_bytes": (ctypes.c_size_t, [_PP, _PO]),
+    "relation_layer_bwd": (ctypes.c_int, [_PP, _PO, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                          ctypes.c_size_t, _P]),
     "relation_profile_arm": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]),
     "relation_profile_disarm": (ctypes.c_int, []),
     "relation_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -260,6 +274,79 @@ def relation_bwd_materialized(q, k, v, dout, lam, *, tau_s: float = TAU_S, scale
                                        workspace.numel() * workspace.element_size(), _stream())
     _check(st, "relation_bwd_materialized")
     return {"dq": dq, "dk": dk, "dv": dv, "dlambda": dlam}
+
+
+def make_layer_opts(pairing: Optional[str] = None, rope_base: float = ROPE_BASE) -> RelLayerOpts:
+    if pairing not in REL_GIVENS:
+        raise ValueError("pairing must be None, 'A' or 'B'")
+    return RelLayerOpts(float(rope_base or 0.0), REL_GIVENS[pairing], 0)
+
+
+def _theta_tensor(theta, H: int, device):
+    if theta is None:
+        return None
+    t = torch.as_tensor(theta, dtype=torch.float32, device=device).reshape(-1).contiguous()
+    if t.numel() != H // 2:
+        raise ValueError("theta must hold H/2 angles")
+    return t
+
+
+def _workspace(nbytes: int, ws, device):
+    if nbytes == 0:
+        return None
+    if ws is None or ws.numel() * ws.element_size() < nbytes:
+        ws = torch.empty((nbytes,), dtype=torch.uint8, device=device)
+    return ws
+
+
+def relation_layer_fwd(q, k, v, lam, theta=None, *, pairing: Optional[str] = None,
+                       rope_base: float = ROPE_BASE, tau_s: float = TAU_S, scale: Optional[float] = None,
+                       workspace=None):
+    """Layer forward: RoPE on q, k (rope_base 0: off), Givens mixing of v over
+    head pairs ("A", "B" or None) with angles ``theta`` [H/2], then the fused
+    operator. Any head width up to 128. Returns dict(o, row_stat)."""
+    lib = load_library()
+    k, v = _same_layout(q, k, v)
+    p = make_problem(q, tau_s, scale)
+    opts = make_layer_opts(pairing, rope_base)
+    dev = q.device
+    lam_t = _lam_tensor(lam, dev)
+    th = _theta_tensor(theta, q.shape[1], dev) if pairing else None
+    o = _layout_like(q)
+    rs = torch.empty(q.shape[:3], dtype=torch.float32, device=dev)
+    nbytes = int(lib.relation_layer_fwd_workspace_bytes(ctypes.byref(p), ctypes.byref(opts)))
+    ws = _workspace(nbytes, workspace, dev)
+    st = lib.relation_layer_fwd(ctypes.byref(p), ctypes.byref(opts), _ptr(q), _ptr(k), _ptr(v), _ptr(lam_t),
+                                _ptr(th), _ptr(o), _ptr(rs), _ptr(ws),
+                                0 if ws is None else ws.numel() * ws.element_size(), _stream())
+    _check(st, "relation_layer_fwd")
+    return {"o": o, "row_stat": rs}
+
+
+def relation_layer_bwd(q, k, v, o, dout, lam, row_stat, theta=None, *, pairing: Optional[str] = None,
+                       rope_base: float = ROPE_BASE, tau_s: float = TAU_S, scale: Optional[float] = None,
+                       workspace=None):
+    """Layer backward. Returns dict(dq, dk, dv, dlambda [1], dtheta [H/2] or None)."""
+    lib = load_library()
+    k, v, o, dout = _same_layout(q, k, v, o, dout)
+    p = make_problem(q, tau_s, scale)
+    opts = make_layer_opts(pairing, rope_base)
+    dev = q.device
+    lam_t = _lam_tensor(lam, dev)
+    H = q.shape[1]
+    th = _theta_tensor(theta, H, dev) if pairing else None
+    rs = row_stat.contiguous()
+    dq, dk, dv = _layout_like(q), _layout_like(q), _layout_like(q)
+    dlam = torch.empty((1,), dtype=torch.float32, device=dev)
+    dth = torch.empty((H // 2,), dtype=torch.float32, device=dev) if pairing else None
+    nbytes = int(lib.relation_layer_bwd_workspace_bytes(ctypes.byref(p), ctypes.byref(opts)))
+    ws = _workspace(max(nbytes, 1), workspace, dev)
+    st = lib.relation_layer_bwd(ctypes.byref(p), ctypes.byref(opts), _ptr(q), _ptr(k), _ptr(v), _ptr(o),
+                                _ptr(dout), _ptr(lam_t), _ptr(th), _ptr(rs), _ptr(dq),
+                                _ptr(dk), _ptr(dv), _ptr(dlam), _ptr(dth), _ptr(ws),
+                                ws.numel() * ws.element_size(), _stream())
+    _check(st, "relation_layer_bwd")
+    return {"dq": dq, "dk": dk, "dv": dv, "dlambda": dlam, "dtheta": dth}
 
 
 def relation_profile_arm(kernel: str, events: list) -> None:

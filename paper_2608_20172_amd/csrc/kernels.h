@@ -82,6 +82,30 @@ struct RowBwdArgs {
   float inv_tau;
 };
 
+// Arguments of the layer prologue / epilogue kernels (RoPE, Givens mixing,
+// padding). Caller tensors use (sb, sh, st); prepared tensors are contiguous
+// [B, H, T, DP].
+struct LayerArgs {
+  const void* q;        // caller projections / information state (true width D)
+  const void* k;
+  const void* v;
+  int64_t sb, sh, st;
+  void* qr;             // out: rotated, padded q and k, or null (not written)
+  void* kr;
+  void* vt;             // out: mixed, padded v, or null
+  const float2* rope;   // [T, D/2] (cos, sin), or null: no RoPE
+  const float* theta;   // [H/2] Givens angles (givens != 0)
+  int givens;           // 0 none, 1 pairing A, 2 pairing B
+  int B, H, T, D, DP;
+  const void* gq;       // epilogue in: gradients in the padded layout, or null
+  const void* gk;
+  const void* gv;
+  void* dq;             // epilogue out: caller layout
+  void* dk;
+  void* dv;
+  float* dth_rows;      // epilogue out: [H/2, B, T] per-row terms of dL/dtheta
+};
+
 // Measurement aid: if armed for kernel `name`, returns the event pair to record
 // around the next launch of that kernel (see relation_profile_arm).
 bool profile_slot(const char* name, hipEvent_t* start, hipEvent_t* stop);
@@ -91,6 +115,12 @@ hipError_t launch_bwd(const BwdArgs& a, int dtype, int D, hipStream_t stream);
 int bwd_partials(int N, int T, int D, int dtype);
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t stream);
 hipError_t launch_allocation(const RowArgs& a, int dtype, int N, hipStream_t stream);
+hipError_t launch_rope_table(float2* tab, int T, int D, double base, hipStream_t stream);
+hipError_t launch_layer_prologue(const LayerArgs& a, int dtype, hipStream_t stream);
+hipError_t launch_layer_repad(const void* src, void* dst, const LayerArgs& a, bool to_padded, int dtype,
+                              hipStream_t stream);
+hipError_t launch_layer_epilogue(const LayerArgs& a, int dtype, hipStream_t stream);
+hipError_t launch_segment_sum(const float* x, int nseg, int64_t seg_len, float* out, hipStream_t stream);
 hipError_t launch_materialized_rows(const RowArgs& a, int dtype, int N, hipStream_t stream);
 hipError_t launch_materialized_bwd_rows(const RowBwdArgs& a, int dtype, int N, hipStream_t stream);
 // Fixed-order sum of n floats; `partial` holds sum_fixed_order_parts() floats.

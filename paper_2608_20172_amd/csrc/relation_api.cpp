@@ -157,6 +157,101 @@ rel_status check_problem(const rel_problem* p, bool* empty) {
   return REL_OK;
 }
 
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Validation of the layer entry points: as check_problem, but any head width
+// up to 128 (even with RoPE), element-aligned strides, and the option checks.
+rel_status check_layer_problem(const rel_problem* p, const rel_layer_opts* o, bool* empty) {
+  if (!p) return fail(REL_ERR_INVALID_ARG, "problem is null");
+  if (!o) return fail(REL_ERR_INVALID_ARG, "layer options are null");
+  if (p->B < 0 || p->H < 0 || p->T < 0 || p->D < 0)
+    return fail(REL_ERR_INVALID_ARG, "negative size B=%lld H=%lld T=%lld D=%lld", (long long)p->B,
+                (long long)p->H, (long long)p->T, (long long)p->D);
+  if (p->dtype != REL_F32 && p->dtype != REL_BF16)
+    return fail(REL_ERR_UNSUPPORTED, "unknown dtype %d", (int)p->dtype);
+  if (p->causal != 1)
+    return fail(REL_ERR_UNSUPPORTED, "only the causal operator is defined (causal=%d)", (int)p->causal);
+  if (!(std::isfinite(p->tau_s) && p->tau_s > 0.0f))
+    return fail(REL_ERR_INVALID_ARG, "tau_s must be finite and > 0 (got %g)", (double)p->tau_s);
+  if (!std::isfinite(p->scale)) return fail(REL_ERR_INVALID_ARG, "scale must be finite");
+  if (!(std::isfinite(o->rope_base) && o->rope_base >= 0.0))
+    return fail(REL_ERR_INVALID_ARG, "rope_base must be finite and >= 0");
+  if (o->rope_base > 0.0 && o->rope_base <= 1.0)
+    return fail(REL_ERR_INVALID_ARG, "rope_base must exceed 1");
+  if (o->givens < REL_GIVENS_NONE || o->givens > REL_GIVENS_B)
+    return fail(REL_ERR_INVALID_ARG, "unknown Givens pairing %d", (int)o->givens);
+  if (o->reserved != 0) return fail(REL_ERR_INVALID_ARG, "reserved layer option must be 0");
+  if (p->D < 1 || p->D > 128)
+    return fail(REL_ERR_UNSUPPORTED, "head width %lld not in 1..128", (long long)p->D);
+  if (o->rope_base > 0.0 && p->D % 2)
+    return fail(REL_ERR_INVALID_ARG, "RoPE needs an even head width (D = %lld)", (long long)p->D);
+  if (o->givens != REL_GIVENS_NONE && p->H % 2)
+    return fail(REL_ERR_INVALID_ARG, "Givens mixing pairs heads: H = %lld is odd", (long long)p->H);
+  *empty = (p->B == 0 || p->H == 0 || p->T == 0);
+  if (*empty) return REL_OK;
+  if (p->T > (1 << 24)) return fail(REL_ERR_UNSUPPORTED, "T = %lld exceeds 2^24", (long long)p->T);
+  if (p->B * p->H > (1LL << 30)) return fail(REL_ERR_UNSUPPORTED, "B*H exceeds 2^30");
+  if (p->stride_t < p->D) return fail(REL_ERR_INVALID_ARG, "stride_t (%lld) < D", (long long)p->stride_t);
+  if (p->stride_b < 0 || p->stride_h < 0) return fail(REL_ERR_INVALID_ARG, "negative stride");
+  if (!nested(lattice_of(p)))
+    return fail(REL_ERR_INVALID_ARG, "strides make distinct (b, h, t) rows overlap");
+  const int64_t es = (int64_t)elem_size(p->dtype);
+  if (p->T * std::max<int64_t>(p->stride_t, 128) * es >= (1LL << 31))
+    return fail(REL_ERR_UNSUPPORTED, "one head spans over 2 GiB");
+  return REL_OK;
+}
+
+// Workspace layout of the layer entry points. The prepared operands and the
+// padded gradients are contiguous [B, H, T, DP].
+struct LayerPlan {
+  rel_problem pp;       // the problem the fused kernels see
+  int64_t DP;
+  bool direct;          // caller tensors already have the prepared layout
+  bool prep_qk, prep_v; // which prepared operands are written
+  size_t tab, qr, kr, vt, yp, dop, gq, gk, gv, bws, dth, total;
+};
+
+// `aligned` says whether every caller tensor pointer is 16-byte aligned; the
+// workspace queries pass false, which sizes for the largest plan.
+LayerPlan plan_layer(const rel_problem* p, const rel_layer_opts* o, bool backward, bool aligned) {
+  LayerPlan L{};
+  L.DP = p->D <= 32 ? 32 : p->D <= 64 ? 64 : 128;
+  const int64_t contig_t = p->D, contig_h = p->T * p->D, contig_b = p->H * p->T * p->D;
+  L.direct = aligned && L.DP == p->D && p->stride_t == contig_t && (p->H == 1 || p->stride_h == contig_h) &&
+             (p->B == 1 || p->stride_b == contig_b);
+  const bool rope = o->rope_base > 0.0, giv = o->givens != REL_GIVENS_NONE;
+  L.prep_qk = rope || !L.direct;
+  L.prep_v = giv || !L.direct;
+  L.pp = *p;
+  L.pp.D = L.DP;
+  L.pp.stride_t = L.DP;
+  L.pp.stride_h = p->T * L.DP;
+  L.pp.stride_b = p->H * p->T * L.DP;
+  L.pp.scale = p->scale > 0.0f ? p->scale : 1.0f / std::sqrt((float)p->D);
+  const size_t es = elem_size(p->dtype);
+  const size_t tensor = align256((size_t)(p->B * p->H * p->T * L.DP) * es);
+  size_t off = 0;
+  auto take = [&](bool need, size_t bytes) {
+    if (!need) return (size_t)-1;
+    const size_t at = off;
+    off += bytes;
+    return at;
+  };
+  L.tab = take(rope, align256((size_t)p->T * (size_t)(p->D / 2) * 8));
+  L.qr = take(L.prep_qk, tensor);
+  L.kr = take(L.prep_qk, tensor);
+  L.vt = take(L.prep_v, tensor);
+  L.yp = take(!L.direct, tensor);
+  L.dop = take(backward && !L.direct, tensor);
+  L.gq = take(backward && (rope || !L.direct), tensor);
+  L.gk = take(backward && (rope || !L.direct), tensor);
+  L.gv = take(backward && (giv || !L.direct), tensor);
+  L.bws = take(backward, align256(relation_bwd_workspace_bytes(&L.pp)));
+  L.dth = take(backward && giv, align256((size_t)(p->H / 2) * (size_t)p->B * (size_t)p->T * 4));
+  L.total = off;
+  return L;
+}
+
 rel_status check_aligned(const void* ptr, size_t align, const char* name, bool required) {
   if (!ptr) {
     if (required) return fail(REL_ERR_INVALID_ARG, "%s is null", name);
@@ -330,7 +425,6 @@ rel_status relation_exchange_allocation(const rel_problem* p, const void* q, con
   return REL_OK;
 }
 
-static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 size_t relation_bwd_workspace_bytes(const rel_problem* p) {
   bool empty = false;
@@ -632,6 +726,173 @@ rel_status relation_bwd_materialized(const rel_problem* p, const void* q, const 
   }
   he = rel::launch_sum_fixed_order(dlam_row, (int64_t)N * T, dlam_part, dlambda, (hipStream_t)stream);
   if (he != hipSuccess) return hip_fail(he, "dlambda reduction launch");
+  return REL_OK;
+}
+
+constexpr size_t kNone = (size_t)-1;
+
+bool al16(std::initializer_list<const void*> ps) {
+  for (const void* x : ps)
+    if ((uintptr_t)x % 16) return false;
+  return true;
+}
+
+rel::LayerArgs layer_args(const rel_problem* p, const rel_layer_opts* o, const LayerPlan& L, char* ws,
+                          const void* q, const void* k, const void* v, const float* theta) {
+  rel::LayerArgs a{};
+  a.q = q; a.k = k; a.v = v;
+  a.sb = p->stride_b; a.sh = p->stride_h; a.st = p->stride_t;
+  a.qr = L.prep_qk ? ws + L.qr : nullptr;
+  a.kr = L.prep_qk ? ws + L.kr : nullptr;
+  a.vt = L.prep_v ? ws + L.vt : nullptr;
+  a.rope = L.tab != kNone ? (const float2*)(ws + L.tab) : nullptr;
+  a.theta = theta;
+  a.givens = o->givens;
+  a.B = (int)p->B; a.H = (int)p->H; a.T = (int)p->T; a.D = (int)p->D; a.DP = (int)L.DP;
+  return a;
+}
+
+size_t relation_layer_fwd_workspace_bytes(const rel_problem* p, const rel_layer_opts* opts) {
+  bool empty = false;
+  if (check_layer_problem(p, opts, &empty) != REL_OK || empty) return 0;
+  return plan_layer(p, opts, false, false).total;
+}
+
+size_t relation_layer_bwd_workspace_bytes(const rel_problem* p, const rel_layer_opts* opts) {
+  bool empty = false;
+  if (check_layer_problem(p, opts, &empty) != REL_OK || empty) return 0;
+  return plan_layer(p, opts, true, false).total;
+}
+
+rel_status relation_layer_fwd(const rel_problem* p, const rel_layer_opts* opts, const void* q,
+                              const void* k, const void* v, const float* lambda, const float* theta,
+                              void* out, float* row_stat, void* workspace, size_t workspace_bytes,
+                              void* stream) {
+  bool empty = false;
+  REL_TRY(check_layer_problem(p, opts, &empty));
+  if (empty) return REL_OK;
+  const size_t es = elem_size(p->dtype);
+  const bool giv = opts->givens != REL_GIVENS_NONE;
+  REL_TRY(check_aligned(q, es, "q", true));
+  REL_TRY(check_aligned(k, es, "k", true));
+  REL_TRY(check_aligned(v, es, "v", true));
+  REL_TRY(check_aligned(out, es, "out", true));
+  REL_TRY(check_aligned(lambda, 4, "lambda", true));
+  REL_TRY(check_aligned(theta, 4, "theta", giv));
+  REL_TRY(check_aligned(row_stat, 4, "row_stat", false));
+  const LayerPlan L = plan_layer(p, opts, false, al16({q, k, v, out}));
+  if (L.total > 0 && (!workspace || workspace_bytes < L.total))
+    return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
+                workspace ? workspace_bytes : (size_t)0);
+  if ((uintptr_t)workspace % 16) return fail(REL_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
+  const size_t tb = (size_t)extent_elems(p) * es, rb = (size_t)(p->B * p->H * p->T) * 4;
+  REL_TRY(check_buffers(p, {{q, tb, true, false, "q"},
+                            {k, tb, true, false, "k"},
+                            {v, tb, true, false, "v"},
+                            {lambda, 4, false, false, "lambda"},
+                            {giv ? theta : nullptr, (size_t)(p->H / 2) * 4, false, false, "theta"},
+                            {out, tb, true, true, "out"},
+                            {row_stat, rb, false, true, "row_stat"},
+                            {L.total ? workspace : nullptr, L.total, false, true, "workspace"}}));
+  if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected by RELATION_TEST_FAIL_LAUNCH");
+  char* ws = (char*)workspace;
+  const hipStream_t s = (hipStream_t)stream;
+  const rel::LayerArgs a = layer_args(p, opts, L, ws, q, k, v, theta);
+  hipError_t he = hipSuccess;
+  if (a.rope && (he = rel::launch_rope_table((float2*)a.rope, (int)p->T, (int)p->D, opts->rope_base, s)))
+    return hip_fail(he, "RoPE table launch");
+  if ((L.prep_qk || L.prep_v) && (he = rel::launch_layer_prologue(a, p->dtype, s)))
+    return hip_fail(he, "layer prologue launch");
+  void* y = L.direct ? out : ws + L.yp;
+  REL_TRY(relation_fwd(&L.pp, L.prep_qk ? a.qr : q, L.prep_qk ? a.kr : k, L.prep_v ? a.vt : v, lambda, y,
+                       row_stat, nullptr, nullptr, nullptr, stream));
+  if (!L.direct && (he = rel::launch_layer_repad(y, out, a, false, p->dtype, s)))
+    return hip_fail(he, "layer output copy launch");
+  return REL_OK;
+}
+
+rel_status relation_layer_bwd(const rel_problem* p, const rel_layer_opts* opts, const void* q,
+                              const void* k, const void* v, const void* out, const void* dout,
+                              const float* lambda, const float* theta, const float* row_stat,
+                              void* dq, void* dk, void* dv, float* dlambda, float* dtheta,
+                              void* workspace, size_t workspace_bytes, void* stream) {
+  bool empty = false;
+  REL_TRY(check_layer_problem(p, opts, &empty));
+  const bool giv = opts->givens != REL_GIVENS_NONE;
+  const hipStream_t s = (hipStream_t)stream;
+  if (empty) {
+    // nothing to differentiate: dlambda and dtheta are still outputs and must be zero
+    if (test_fail_launch() && (dlambda || (giv && dtheta))) return fail(REL_ERR_HIP, "launch failure injected");
+    hipError_t e = hipSuccess;
+    if (dlambda && (e = rel::launch_fill_zero(dlambda, 1, s))) return hip_fail(e, "dlambda clear");
+    if (giv && dtheta && p->H > 0 && (e = rel::launch_fill_zero(dtheta, p->H / 2, s)))
+      return hip_fail(e, "dtheta clear");
+    return REL_OK;
+  }
+  const size_t es = elem_size(p->dtype);
+  REL_TRY(check_aligned(q, es, "q", true));
+  REL_TRY(check_aligned(k, es, "k", true));
+  REL_TRY(check_aligned(v, es, "v", true));
+  REL_TRY(check_aligned(out, es, "out", true));
+  REL_TRY(check_aligned(dout, es, "dout", true));
+  REL_TRY(check_aligned(dq, es, "dq", true));
+  REL_TRY(check_aligned(dk, es, "dk", true));
+  REL_TRY(check_aligned(dv, es, "dv", true));
+  REL_TRY(check_aligned(lambda, 4, "lambda", true));
+  REL_TRY(check_aligned(row_stat, 4, "row_stat", true));
+  REL_TRY(check_aligned(dlambda, 4, "dlambda", true));
+  REL_TRY(check_aligned(theta, 4, "theta", giv));
+  REL_TRY(check_aligned(dtheta, 4, "dtheta", giv));
+  const LayerPlan L = plan_layer(p, opts, true, al16({q, k, v, out, dout, dq, dk, dv}));
+  if (!workspace || workspace_bytes < L.total)
+    return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
+                workspace ? workspace_bytes : (size_t)0);
+  if ((uintptr_t)workspace % 16) return fail(REL_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
+  const size_t tb = (size_t)extent_elems(p) * es, rb = (size_t)(p->B * p->H * p->T) * 4;
+  const size_t thb = (size_t)(p->H / 2) * 4;
+  REL_TRY(check_buffers(p, {{q, tb, true, false, "q"},
+                            {k, tb, true, false, "k"},
+                            {v, tb, true, false, "v"},
+                            {out, tb, true, false, "out"},
+                            {dout, tb, true, false, "dout"},
+                            {lambda, 4, false, false, "lambda"},
+                            {giv ? theta : nullptr, thb, false, false, "theta"},
+                            {row_stat, rb, false, false, "row_stat"},
+                            {dq, tb, true, true, "dq"},
+                            {dk, tb, true, true, "dk"},
+                            {dv, tb, true, true, "dv"},
+                            {dlambda, 4, false, true, "dlambda"},
+                            {giv ? dtheta : nullptr, thb, false, true, "dtheta"},
+                            {workspace, L.total, false, true, "workspace"}}));
+  if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected by RELATION_TEST_FAIL_LAUNCH");
+  char* ws = (char*)workspace;
+  rel::LayerArgs a = layer_args(p, opts, L, ws, q, k, v, theta);
+  hipError_t he = hipSuccess;
+  if (a.rope && (he = rel::launch_rope_table((float2*)a.rope, (int)p->T, (int)p->D, opts->rope_base, s)))
+    return hip_fail(he, "RoPE table launch");
+  if ((L.prep_qk || L.prep_v) && (he = rel::launch_layer_prologue(a, p->dtype, s)))
+    return hip_fail(he, "layer prologue launch");
+  const void* y = out;
+  const void* g = dout;
+  if (!L.direct) {
+    if ((he = rel::launch_layer_repad(out, ws + L.yp, a, true, p->dtype, s)) ||
+        (he = rel::launch_layer_repad(dout, ws + L.dop, a, true, p->dtype, s)))
+      return hip_fail(he, "layer padding launch");
+    y = ws + L.yp;
+    g = ws + L.dop;
+  }
+  a.gq = L.gq != kNone ? ws + L.gq : nullptr;
+  a.gk = L.gk != kNone ? ws + L.gk : nullptr;
+  a.gv = L.gv != kNone ? ws + L.gv : nullptr;
+  a.dq = dq; a.dk = dk; a.dv = dv;
+  a.dth_rows = giv ? (float*)(ws + L.dth) : nullptr;
+  REL_TRY(relation_bwd(&L.pp, L.prep_qk ? a.qr : q, L.prep_qk ? a.kr : k, L.prep_v ? a.vt : v, y, g, lambda,
+                       row_stat, a.gq ? (void*)a.gq : dq, a.gk ? (void*)a.gk : dk, a.gv ? (void*)a.gv : dv,
+                       dlambda, nullptr, ws + L.bws, relation_bwd_workspace_bytes(&L.pp), stream));
+  if ((a.gq || a.gv) && (he = rel::launch_layer_epilogue(a, p->dtype, s)))
+    return hip_fail(he, "layer epilogue launch");
+  if (giv && (he = rel::launch_segment_sum(a.dth_rows, (int)(p->H / 2), p->B * p->T, dtheta, s)))
+    return hip_fail(he, "dtheta reduction launch");
   return REL_OK;
 }
 

@@ -65,6 +65,16 @@ WORKLOADS = {
     "long_T16384": Workload("long_T16384", 1, 16, 16384, 128, "bf16", _std(128), True),
 }
 
+# Layers at the paper's own model geometries (8 heads of width 48, 64, 80 and
+# 60; context 1024, 2048, 4096 and 2048; the micro-batch of each scale), run
+# through the layer entry points with RoPE and Givens mixing.
+LAYER_WORKLOADS = {
+    "paper10m_layer": Workload("paper10m_layer", 32, 8, 1024, 48, "bf16", _std(48), True),
+    "paper30m_layer": Workload("paper30m_layer", 16, 8, 2048, 64, "bf16", _std(64), True),
+    "paper100m_layer": Workload("paper100m_layer", 4, 8, 4096, 80, "bf16", _std(80), True),
+    "hybrid30m_layer": Workload("hybrid30m_layer", 16, 8, 2048, 60, "bf16", _std(60), True),
+}
+
 
 def make_inputs(B: int, H: int, T: int, D: int, *, seed: int = 42, qkv_std: float = 1.0,
                 with_dout: bool = True, lam_std: float = 0.02, lam: float | None = None,
@@ -91,6 +101,13 @@ def make_inputs(B: int, H: int, T: int, D: int, *, seed: int = 42, qkv_std: floa
         "lam": lam_drawn if lam is None else float(lam),
         "boost_mask": mask,
     }
+
+
+def make_givens_angles(H: int, seed: int = 42, spread: float = math.pi) -> np.ndarray:
+    """H/2 head-pair angles ~ U(-spread, spread), fp64, from a stream of their
+    own (the paper initialises them to zero; tests need general angles)."""
+    rng = np.random.default_rng(seed + 7919)
+    return rng.uniform(-spread, spread, H // 2)
 
 
 def make_workload_inputs(w: Workload, seed: int = 42, lam: float | None = None) -> dict:

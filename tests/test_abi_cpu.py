@@ -173,3 +173,80 @@ def test_injected_launch_failure_raises(lib, monkeypatch):
     assert b"injected" in lib.relation_last_error()
     with pytest.raises(RuntimeError, match="relation_fwd failed"):
         R._check(R.REL_ERR_HIP, "relation_fwd")
+
+
+# ---------------------------------------------------------------------------
+# layer entry points (RoPE, Givens mixing, padded head widths)
+# ---------------------------------------------------------------------------
+def lopts(rope=1.0e4, givens=1, reserved=0):
+    return R.RelLayerOpts(rope, givens, reserved)
+
+
+def layer_fwd(lib, p, o, theta=True, ws_bytes=None):
+    a = ptrs(8)
+    need = lib.relation_layer_fwd_workspace_bytes(ctypes.byref(p), ctypes.byref(o))
+    n = need if ws_bytes is None else ws_bytes
+    return lib.relation_layer_fwd(ctypes.byref(p), ctypes.byref(o), a[0], a[1], a[2], a[3],
+                                  a[4] if theta else None, a[5], a[6], a[7], n, None)
+
+
+def test_layer_workspace_sizes(lib):
+    p = prob(B=2, H=4, T=100, D=60, st=60)
+    es, DP = 2, 64
+    tensor = 2 * 4 * 100 * DP * es
+    fw = lib.relation_layer_fwd_workspace_bytes(ctypes.byref(p), ctypes.byref(lopts()))
+    bw = lib.relation_layer_bwd_workspace_bytes(ctypes.byref(p), ctypes.byref(lopts()))
+    # forward: rotated q, k, mixed v and the padded output; the [T, D/2] cos/sin table
+    assert fw >= 4 * tensor + 100 * 30 * 8
+    # backward adds padded out and dout, three padded gradients, one dtheta term per (pair, b, t)
+    assert bw >= fw + 4 * tensor + 2 * 2 * 100 * 4
+    # no RoPE, no mixing, a tiled width, contiguous: nothing is prepared in the largest plan
+    # except the copies made when the caller's pointers are not 16-byte aligned
+    p64 = prob(B=2, H=4, T=100, D=64)
+    plain = lib.relation_layer_fwd_workspace_bytes(ctypes.byref(p64), ctypes.byref(lopts(0.0, 0)))
+    assert plain >= 4 * 2 * 4 * 100 * 64 * 2
+    assert lib.relation_layer_fwd_workspace_bytes(ctypes.byref(prob(T=0)), ctypes.byref(lopts())) == 0
+    assert lib.relation_layer_fwd_workspace_bytes(None, ctypes.byref(lopts())) == 0
+    assert lib.relation_layer_fwd_workspace_bytes(ctypes.byref(p), None) == 0
+
+
+@pytest.mark.parametrize("pmut,omut,code", [
+    (dict(D=60, st=60), {}, R.REL_ERR_HIP),             # paper width 60, rows 120 bytes apart: accepted
+    (dict(D=48, st=48), {}, R.REL_ERR_HIP),
+    (dict(D=80, st=80), {}, R.REL_ERR_HIP),
+    (dict(D=130, st=130), {}, R.REL_ERR_UNSUPPORTED),
+    (dict(D=61, st=61), {}, R.REL_ERR_INVALID_ARG),    # RoPE needs an even width
+    (dict(D=61, st=61), dict(rope=0.0), R.REL_ERR_HIP),
+    (dict(H=3), {}, R.REL_ERR_INVALID_ARG),            # Givens needs paired heads
+    (dict(H=3), dict(givens=0), R.REL_ERR_HIP),
+    ({}, dict(givens=3), R.REL_ERR_INVALID_ARG),
+    ({}, dict(reserved=1), R.REL_ERR_INVALID_ARG),
+    ({}, dict(rope=0.5), R.REL_ERR_INVALID_ARG),
+    ({}, dict(rope=float("nan")), R.REL_ERR_INVALID_ARG),
+    (dict(causal=0), {}, R.REL_ERR_UNSUPPORTED),
+])
+def test_layer_validation(lib, pmut, omut, code):
+    assert layer_fwd(lib, prob(**pmut), lopts(**omut)) == code
+
+
+def test_layer_arguments(lib):
+    p = prob(D=60, st=60)
+    assert layer_fwd(lib, p, lopts(), theta=False) == R.REL_ERR_INVALID_ARG      # angles required
+    assert layer_fwd(lib, p, lopts(givens=0), theta=False) == R.REL_ERR_HIP
+    assert layer_fwd(lib, p, lopts(), ws_bytes=16) == R.REL_ERR_WORKSPACE
+    a = ptrs(8)
+    o = lopts()
+    assert lib.relation_layer_fwd(ctypes.byref(p), ctypes.byref(o), a[0], a[1], a[2], a[3], a[4], a[0],
+                                  a[6], a[7], 1 << 30, None) == R.REL_ERR_INVALID_ARG  # out == q
+    # backward: a valid request reaches the device; a short workspace does not
+    need = lib.relation_layer_bwd_workspace_bytes(ctypes.byref(p), ctypes.byref(o))
+    b = ptrs(16)
+    args = [ctypes.byref(p), ctypes.byref(o)] + b[:14]
+    assert lib.relation_layer_bwd(*args, need - 1, None) == R.REL_ERR_WORKSPACE
+    assert lib.relation_layer_bwd(*args, need, None) == R.REL_ERR_HIP
+    args_nodth = [ctypes.byref(p), ctypes.byref(o)] + b[:12] + [None, b[13]]
+    assert lib.relation_layer_bwd(*args_nodth, need, None) == R.REL_ERR_INVALID_ARG  # dtheta required
+    # empty problem with no scalar outputs: nothing to launch
+    pe = prob(B=0)
+    assert lib.relation_layer_bwd(ctypes.byref(pe), ctypes.byref(o), *([None] * 11), None, None, None, 0,
+                                  None) == R.REL_OK
