@@ -258,6 +258,71 @@ def materialized_backward(w, q, k, v, do, lam_t, fwd_ms, bwd_ms, mat_fwd_ms, K, 
             "step_ms": mat_fwd_ms + ms, "speedup_step": (mat_fwd_ms + ms) / (fwd_ms + bwd_ms)}
 
 
+def layer_leg(hip, lib, K: int, warmup: int) -> dict:
+    """The layer entry points at the paper's 100M geometry (4 x 8 heads of width
+    80, T = 4096, RoPE base 1e4, Givens pairing A): whole-step time, the fused
+    kernels' share (HIP events on their launch stream), and the rest, the
+    layer's own linear passes, against the HBM peak."""
+    import numpy as np
+    import torch
+    from paper_2608_20172_amd import binding as R
+    from paper_2608_20172_amd.inputs import LAYER_WORKLOADS, make_givens_angles
+
+    w = LAYER_WORKLOADS["paper100m_layer"]
+    inp = make_workload_inputs(w)
+    dev = torch.device("cuda:0")
+    q, k, v, do = (torch.from_numpy(inp[n]).to(torch.bfloat16).to(dev) for n in ("q", "k", "v", "dout"))
+    lam_t = torch.tensor([float(inp["lam"])], dtype=torch.float32, device=dev)
+    th = torch.from_numpy(np.asarray(make_givens_angles(w.H), dtype=np.float32)).to(dev)
+    kw = dict(pairing="A", rope_base=1.0e4)
+    bws = torch.empty(max(1, R.relation_layer_bwd_workspace_bytes(q, **kw)), dtype=torch.uint8, device=dev)
+
+    def step():
+        f = R.relation_layer_fwd(q, k, v, lam_t, th, **kw)  # keeps the prepared operands for the backward
+        g = R.relation_layer_bwd(q, k, v, f["o"], do, lam_t, f["row_stat"], th, saved=f["saved"], workspace=bws,
+                                 **kw)
+        return f, g
+
+    for _ in range(max(2, warmup)):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(K):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / K
+
+    def kernel_ms(name):
+        ev = hip.events(2 * K)
+        keep = arm(lib, name, ev)
+        for _ in range(K):
+            step()
+        torch.cuda.synchronize()
+        n = lib.relation_profile_disarm()
+        del keep
+        t = sum(hip.elapsed_ms(ev[2 * i], ev[2 * i + 1]) for i in range(n)) / max(n, 1)
+        hip.destroy(ev)
+        return t
+
+    fused = kernel_ms("fwd") + kernel_ms("bwd")
+    N, T, D, DP, es = w.N, w.T, w.D, 128, 2
+    row, prow = N * T * D * es, N * T * DP * es
+    # algorithmic bytes of the layer's own passes in one step (the backward
+    # reads the forward's prepared operands, so it prepares nothing again)
+    fwd_bytes = 3 * row + 3 * prow + prow + row   # q, k, v in; rotated q, k, mixed v out; padded y to the caller
+    bwd_bytes = (row + prow                       # dO padded
+                 + 3 * prow + row + 3 * row)      # epilogue: padded gradients and v in, dq, dk, dv out
+    passes_ms = ms - fused
+    nbytes = fwd_bytes + bwd_bytes
+    return {"workload": w.name, "B": w.B, "H": w.H, "T": w.T, "D": w.D, "padded_D": DP,
+            "rope_base": 1.0e4, "givens": "A", "ms_per_step": ms, "tokens_per_s": w.tokens / (ms * 1e-3),
+            "fused_kernels_ms": fused, "layer_passes_ms": passes_ms, "layer_passes_bytes": nbytes,
+            "layer_passes_GBps": nbytes / (passes_ms * 1e-3) / 1e9 if passes_ms > 0 else None,
+            "layer_passes_hbm_frac": nbytes / (passes_ms * 1e-3) / PEAK_HBM if passes_ms > 0 else None}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -267,6 +332,7 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-materialized", action="store_true")
+    ap.add_argument("--no-layer", action="store_true", help="skip the layer entry points leg")
     ap.add_argument("--copy-bytes", type=int, default=0)
     ap.add_argument("--copy-kind", choices=("memcpy", "elementwise"), default="elementwise")
     ap.add_argument("--summarize-counters", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
@@ -405,6 +471,10 @@ def main() -> int:
             if w.backward:
                 mat.update(materialized_backward(w, q, k, v, do, lam_t, fwd_ms, bwd_ms, mat_ms, K, args))
 
+    layer = {"status": "skipped"}
+    if not args.no_layer:
+        layer = layer_leg(hip, lib, K, args.warmup)
+
     fl_f, fl_b = flops(w, "fwd"), flops(w, "bwd") if w.backward else 0.0
     kern_flops = fl_b if w.backward else fl_f
     achieved = kern_flops / (kern_ms * 1e-3)
@@ -433,6 +503,7 @@ def main() -> int:
         **per_kernel,
         "fwd_kernel_tflops": fl_f / (fwd_kern_ms * 1e-3) / 1e12,
         "materialized": mat,
+        "layer": layer,
         "roofline": {
             "kernel": "bwd_dkdv_kernel+bwd_dq_kernel" if w.backward else "fwd_kernel",
             "bound": "mfma",

@@ -179,17 +179,31 @@ rel_status relation_bwd_materialized(const rel_problem* p, const void* q, const 
  *   theta       device fp32 [H/2] angles (read when givens != NONE).
  *   out         [B,H,T,D] dtype: y.   row_stat  [B,H,T] fp32: M_i for the
  *               backward pass (as relation_fwd).
- *   workspace   relation_layer_*_workspace_bytes(p, opts) bytes, 16-byte
- *               aligned, contents ignored on entry: the prepared (rotated,
- *               mixed, padded) operands [B,H,T,DP], a [T, D/2] table of
- *               cos/sin, and, for the backward pass, padded copies of out and
- *               dout, the gradients in the padded layout, relation_bwd's own
- *               workspace and one fp32 dtheta term per (pair, b, t).
- * The backward pass recomputes the prepared operands from q, k, v and returns
- * dq, dk, dv with respect to the unrotated, unmixed inputs, dlambda as
- * relation_bwd, and dtheta [H/2] fp32 (required when givens != NONE, each
- * angle's gradient summed over batch, positions and channels in a fixed
- * order). Results are run-to-run identical. */
+ *   saved       relation_layer_saved_bytes(p, opts) bytes of device memory,
+ *               16-byte aligned, owned by the caller from the forward call to
+ *               the backward call: the prepared operands (rotated q and k,
+ *               mixed v, the forward's output, each [B,H,T,DP] with DP = 32,
+ *               64 or 128 the tiled width) and a [T, D/2] cos/sin table. The
+ *               forward pass writes it; the backward pass reads it instead of
+ *               preparing the operands again. NULL: the forward pass prepares
+ *               them in its workspace and the backward pass recomputes them.
+ *               A layer with no RoPE, no mixing, a tiled width and contiguous
+ *               tensors needs none of this (0 bytes) and runs relation_fwd /
+ *               relation_bwd on the caller's tensors, which must then meet
+ *               their alignment rules.
+ *   workspace   forward: relation_layer_fwd_workspace_bytes(p, opts) bytes
+ *               when saved is NULL (none otherwise). Backward:
+ *               relation_layer_bwd_workspace_bytes(p, opts) bytes (which
+ *               include room to recompute the prepared operands; with saved,
+ *               the saved size may be subtracted): padded dout, the gradients
+ *               in the padded layout, relation_bwd's own workspace, one fp32
+ *               dtheta term per (pair, b, t) and their partial sums.
+ *               16-byte aligned, contents ignored on entry.
+ *   out (backward) must be the tensor the forward call wrote.
+ * The backward pass returns dq, dk, dv with respect to the unrotated, unmixed
+ * inputs, dlambda as relation_bwd, and dtheta [H/2] fp32 (required when
+ * givens != NONE, each angle's gradient summed over batch, positions and
+ * channels in a fixed order). Results are run-to-run identical. */
 typedef enum rel_givens {
   REL_GIVENS_NONE = 0,
   REL_GIVENS_A = 1,
@@ -202,17 +216,19 @@ typedef struct rel_layer_opts {
   int32_t reserved;  /* must be 0 */
 } rel_layer_opts;
 
+size_t relation_layer_saved_bytes(const rel_problem* p, const rel_layer_opts* opts);
 size_t relation_layer_fwd_workspace_bytes(const rel_problem* p, const rel_layer_opts* opts);
 rel_status relation_layer_fwd(const rel_problem* p, const rel_layer_opts* opts, const void* q,
                               const void* k, const void* v, const float* lambda, const float* theta,
-                              void* out, float* row_stat, void* workspace, size_t workspace_bytes,
-                              void* stream);
+                              void* out, float* row_stat, void* saved, size_t saved_bytes,
+                              void* workspace, size_t workspace_bytes, void* stream);
 size_t relation_layer_bwd_workspace_bytes(const rel_problem* p, const rel_layer_opts* opts);
 rel_status relation_layer_bwd(const rel_problem* p, const rel_layer_opts* opts, const void* q,
                               const void* k, const void* v, const void* out, const void* dout,
                               const float* lambda, const float* theta, const float* row_stat,
-                              void* dq, void* dk, void* dv, float* dlambda, float* dtheta,
-                              void* workspace, size_t workspace_bytes, void* stream);
+                              const void* saved, size_t saved_bytes, void* dq, void* dk, void* dv,
+                              float* dlambda, float* dtheta, void* workspace, size_t workspace_bytes,
+                              void* stream);
 
 /* Measurement aid. While armed, every launch of the named kernel ("fwd": the
  * fused forward kernel; "bwd_dkdv", "bwd_dq": the two backward kernels; "bwd":

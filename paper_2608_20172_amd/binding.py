@@ -55,11 +55,13 @@ _SIGS = {
     "relation_bwd_materialized_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(RelProblem)]),
     "relation_bwd_materialized": (ctypes.c_int, [ctypes.POINTER(RelProblem), _P, _P, _P, _P, _P, _P, _P, _P,
                                                  _P, _P, ctypes.c_size_t, _P]),
+    "relation_layer_saved_bytes": (ctypes.c_size_t, [_PP, _PO]),
     "relation_layer_fwd_workspace_bytes": (ctypes.c_size_t, [_PP, _PO]),
-    "relation_layer_fwd": (ctypes.c_int, [_PP, _PO, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
-    "relation_layer_bwd_workspace_bytes": (ctypes.c_size_t, [_PP, _PO]),
-    "relation_layer_bwd": (ctypes.c_int, [_PP, _PO, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+    "relation_layer_fwd": (ctypes.c_int, [_PP, _PO, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P,
                                           ctypes.c_size_t, _P]),
+    "relation_layer_bwd_workspace_bytes": (ctypes.c_size_t, [_PP, _PO]),
+    "relation_layer_bwd": (ctypes.c_int, [_PP, _PO, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t,
+                                          _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "relation_profile_arm": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]),
     "relation_profile_disarm": (ctypes.c_int, []),
     "relation_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -299,12 +301,39 @@ def _workspace(nbytes: int, ws, device):
     return ws
 
 
+def _layer_size(fn: str, q, pairing, rope_base, tau_s, scale) -> int:
+    p, o = make_problem(q, tau_s, scale), make_layer_opts(pairing, rope_base)
+    return int(getattr(load_library(), fn)(ctypes.byref(p), ctypes.byref(o)))
+
+
+def relation_layer_saved_bytes(q, *, pairing: Optional[str] = None, rope_base: float = ROPE_BASE,
+                               tau_s: float = TAU_S, scale: Optional[float] = None) -> int:
+    return _layer_size("relation_layer_saved_bytes", q, pairing, rope_base, tau_s, scale)
+
+
+def relation_layer_fwd_workspace_bytes(q, *, pairing: Optional[str] = None, rope_base: float = ROPE_BASE,
+                                       tau_s: float = TAU_S, scale: Optional[float] = None) -> int:
+    return _layer_size("relation_layer_fwd_workspace_bytes", q, pairing, rope_base, tau_s, scale)
+
+
+def relation_layer_bwd_workspace_bytes(q, *, pairing: Optional[str] = None, rope_base: float = ROPE_BASE,
+                                       tau_s: float = TAU_S, scale: Optional[float] = None) -> int:
+    return _layer_size("relation_layer_bwd_workspace_bytes", q, pairing, rope_base, tau_s, scale)
+
+
+def _nbytes(t) -> int:
+    return 0 if t is None else t.numel() * t.element_size()
+
+
 def relation_layer_fwd(q, k, v, lam, theta=None, *, pairing: Optional[str] = None,
                        rope_base: float = ROPE_BASE, tau_s: float = TAU_S, scale: Optional[float] = None,
-                       workspace=None):
+                       keep_saved: bool = True, workspace=None):
     """Layer forward: RoPE on q, k (rope_base 0: off), Givens mixing of v over
     head pairs ("A", "B" or None) with angles ``theta`` [H/2], then the fused
-    operator. Any head width up to 128. Returns dict(o, row_stat)."""
+    operator. Any head width up to 128. Returns dict(o, row_stat, saved):
+    ``saved`` (a uint8 device tensor, or None) holds the prepared operands for
+    relation_layer_bwd; with keep_saved=False it is None and the backward pass
+    prepares them again."""
     lib = load_library()
     k, v = _same_layout(q, k, v)
     p = make_problem(q, tau_s, scale)
@@ -314,19 +343,22 @@ def relation_layer_fwd(q, k, v, lam, theta=None, *, pairing: Optional[str] = Non
     th = _theta_tensor(theta, q.shape[1], dev) if pairing else None
     o = _layout_like(q)
     rs = torch.empty(q.shape[:3], dtype=torch.float32, device=dev)
-    nbytes = int(lib.relation_layer_fwd_workspace_bytes(ctypes.byref(p), ctypes.byref(opts)))
-    ws = _workspace(nbytes, workspace, dev)
+    nsaved = int(lib.relation_layer_saved_bytes(ctypes.byref(p), ctypes.byref(opts)))
+    saved = torch.empty((nsaved,), dtype=torch.uint8, device=dev) if keep_saved and nsaved else None
+    ws = None if saved is not None else _workspace(
+        int(lib.relation_layer_fwd_workspace_bytes(ctypes.byref(p), ctypes.byref(opts))), workspace, dev)
     st = lib.relation_layer_fwd(ctypes.byref(p), ctypes.byref(opts), _ptr(q), _ptr(k), _ptr(v), _ptr(lam_t),
-                                _ptr(th), _ptr(o), _ptr(rs), _ptr(ws),
-                                0 if ws is None else ws.numel() * ws.element_size(), _stream())
+                                _ptr(th), _ptr(o), _ptr(rs), _ptr(saved), _nbytes(saved), _ptr(ws), _nbytes(ws),
+                                _stream())
     _check(st, "relation_layer_fwd")
-    return {"o": o, "row_stat": rs}
+    return {"o": o, "row_stat": rs, "saved": saved}
 
 
-def relation_layer_bwd(q, k, v, o, dout, lam, row_stat, theta=None, *, pairing: Optional[str] = None,
+def relation_layer_bwd(q, k, v, o, dout, lam, row_stat, theta=None, *, saved=None, pairing: Optional[str] = None,
                        rope_base: float = ROPE_BASE, tau_s: float = TAU_S, scale: Optional[float] = None,
                        workspace=None):
-    """Layer backward. Returns dict(dq, dk, dv, dlambda [1], dtheta [H/2] or None)."""
+    """Layer backward; ``saved`` is the forward call's (None: recompute).
+    Returns dict(dq, dk, dv, dlambda [1], dtheta [H/2] or None)."""
     lib = load_library()
     k, v, o, dout = _same_layout(q, k, v, o, dout)
     p = make_problem(q, tau_s, scale)
@@ -342,9 +374,9 @@ def relation_layer_bwd(q, k, v, o, dout, lam, row_stat, theta=None, *, pairing: 
     nbytes = int(lib.relation_layer_bwd_workspace_bytes(ctypes.byref(p), ctypes.byref(opts)))
     ws = _workspace(max(nbytes, 1), workspace, dev)
     st = lib.relation_layer_bwd(ctypes.byref(p), ctypes.byref(opts), _ptr(q), _ptr(k), _ptr(v), _ptr(o),
-                                _ptr(dout), _ptr(lam_t), _ptr(th), _ptr(rs), _ptr(dq),
-                                _ptr(dk), _ptr(dv), _ptr(dlam), _ptr(dth), _ptr(ws),
-                                ws.numel() * ws.element_size(), _stream())
+                                _ptr(dout), _ptr(lam_t), _ptr(th), _ptr(rs), _ptr(saved), _nbytes(saved),
+                                _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dlam), _ptr(dth), _ptr(ws), _nbytes(ws),
+                                _stream())
     _check(st, "relation_layer_bwd")
     return {"dq": dq, "dk": dk, "dv": dv, "dlambda": dlam, "dtheta": dth}
 

@@ -115,12 +115,18 @@ hipError_t launch_bwd(const BwdArgs& a, int dtype, int D, hipStream_t stream);
 int bwd_partials(int N, int T, int D, int dtype);
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t stream);
 hipError_t launch_allocation(const RowArgs& a, int dtype, int N, hipStream_t stream);
+// Layer passes. `vec` (8, 2 or 1 for bf16; 4, 2 or 1 for fp32) is the number
+// of contiguous channels one thread moves; the caller's tensors must allow it
+// (D, D/2 with RoPE, and the strides multiples of vec; pointers aligned to it).
 hipError_t launch_rope_table(float2* tab, int T, int D, double base, hipStream_t stream);
-hipError_t launch_layer_prologue(const LayerArgs& a, int dtype, hipStream_t stream);
+hipError_t launch_layer_prologue(const LayerArgs& a, int dtype, int vec, hipStream_t stream);
 hipError_t launch_layer_repad(const void* src, void* dst, const LayerArgs& a, bool to_padded, int dtype,
+                              int vec, hipStream_t stream);
+hipError_t launch_layer_epilogue(const LayerArgs& a, int dtype, int vec, hipStream_t stream);
+// Fixed-order sums of nseg segments; `part` holds nseg * layer_sum_parts() floats.
+int layer_sum_parts();
+hipError_t launch_segment_sum(const float* x, int nseg, int64_t seg_len, float* part, float* out,
                               hipStream_t stream);
-hipError_t launch_layer_epilogue(const LayerArgs& a, int dtype, hipStream_t stream);
-hipError_t launch_segment_sum(const float* x, int nseg, int64_t seg_len, float* out, hipStream_t stream);
 hipError_t launch_materialized_rows(const RowArgs& a, int dtype, int N, hipStream_t stream);
 hipError_t launch_materialized_bwd_rows(const RowBwdArgs& a, int dtype, int N, hipStream_t stream);
 // Fixed-order sum of n floats; `partial` holds sum_fixed_order_parts() floats.

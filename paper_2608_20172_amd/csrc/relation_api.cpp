@@ -201,27 +201,31 @@ rel_status check_layer_problem(const rel_problem* p, const rel_layer_opts* o, bo
   return REL_OK;
 }
 
-// Workspace layout of the layer entry points. The prepared operands and the
-// padded gradients are contiguous [B, H, T, DP].
+// Memory plan of the layer entry points. The prepared operands (rotated q and
+// k, mixed v, the forward's output, all contiguous [B, H, T, DP]) and the cos /
+// sin table form the "prepared" region: the caller's saved buffer, or the
+// start of the workspace. The backward pass's own scratch follows in the
+// workspace. A pass-through layer (no RoPE, no mixing, a tiled width,
+// contiguous tensors) has no prepared region and calls the operator directly.
+constexpr size_t kNone = (size_t)-1;
+
 struct LayerPlan {
   rel_problem pp;       // the problem the fused kernels see
   int64_t DP;
-  bool direct;          // caller tensors already have the prepared layout
-  bool prep_qk, prep_v; // which prepared operands are written
-  size_t tab, qr, kr, vt, yp, dop, gq, gk, gv, bws, dth, total;
+  bool pass;            // pass-through
+  bool contiguous_tiled;  // the caller's layout equals the padded layout
+  size_t tab, qr, kr, vt, yp, prep;                 // prepared region
+  size_t dop, gq, gk, gv, bws, dth, dpart, scratch;  // backward scratch
 };
 
-// `aligned` says whether every caller tensor pointer is 16-byte aligned; the
-// workspace queries pass false, which sizes for the largest plan.
-LayerPlan plan_layer(const rel_problem* p, const rel_layer_opts* o, bool backward, bool aligned) {
+LayerPlan plan_layer(const rel_problem* p, const rel_layer_opts* o) {
   LayerPlan L{};
   L.DP = p->D <= 32 ? 32 : p->D <= 64 ? 64 : 128;
-  const int64_t contig_t = p->D, contig_h = p->T * p->D, contig_b = p->H * p->T * p->D;
-  L.direct = aligned && L.DP == p->D && p->stride_t == contig_t && (p->H == 1 || p->stride_h == contig_h) &&
-             (p->B == 1 || p->stride_b == contig_b);
+  const bool contiguous = p->stride_t == p->D && (p->H == 1 || p->stride_h == p->T * p->D) &&
+                          (p->B == 1 || p->stride_b == p->H * p->T * p->D);
   const bool rope = o->rope_base > 0.0, giv = o->givens != REL_GIVENS_NONE;
-  L.prep_qk = rope || !L.direct;
-  L.prep_v = giv || !L.direct;
+  L.contiguous_tiled = contiguous && L.DP == p->D;
+  L.pass = L.contiguous_tiled && !rope && !giv;
   L.pp = *p;
   L.pp.D = L.DP;
   L.pp.stride_t = L.DP;
@@ -232,24 +236,42 @@ LayerPlan plan_layer(const rel_problem* p, const rel_layer_opts* o, bool backwar
   const size_t tensor = align256((size_t)(p->B * p->H * p->T * L.DP) * es);
   size_t off = 0;
   auto take = [&](bool need, size_t bytes) {
-    if (!need) return (size_t)-1;
+    if (!need) return kNone;
     const size_t at = off;
     off += bytes;
     return at;
   };
-  L.tab = take(rope, align256((size_t)p->T * (size_t)(p->D / 2) * 8));
-  L.qr = take(L.prep_qk, tensor);
-  L.kr = take(L.prep_qk, tensor);
-  L.vt = take(L.prep_v, tensor);
-  L.yp = take(!L.direct, tensor);
-  L.dop = take(backward && !L.direct, tensor);
-  L.gq = take(backward && (rope || !L.direct), tensor);
-  L.gk = take(backward && (rope || !L.direct), tensor);
-  L.gv = take(backward && (giv || !L.direct), tensor);
-  L.bws = take(backward, align256(relation_bwd_workspace_bytes(&L.pp)));
-  L.dth = take(backward && giv, align256((size_t)(p->H / 2) * (size_t)p->B * (size_t)p->T * 4));
-  L.total = off;
+  const bool prep = !L.pass;
+  L.tab = take(prep && rope, align256((size_t)p->T * (size_t)(p->D / 2) * 8));
+  L.qr = take(prep, tensor);
+  L.kr = take(prep, tensor);
+  L.vt = take(prep, tensor);
+  L.yp = take(prep, tensor);
+  L.prep = off;
+  off = 0;
+  L.dop = take(prep, tensor);
+  L.gq = take(prep, tensor);
+  L.gk = take(prep, tensor);
+  L.gv = take(prep, tensor);
+  L.bws = take(true, align256(relation_bwd_workspace_bytes(&L.pp)));
+  L.dth = take(prep && giv, align256((size_t)(p->H / 2) * (size_t)p->B * (size_t)p->T * 4));
+  L.dpart = take(prep && giv, align256((size_t)(p->H / 2) * (size_t)rel::layer_sum_parts() * 4));
+  L.scratch = off;
   return L;
+}
+
+// The widest chunk (channels per thread) the caller's tensors allow: D, D/2
+// (with RoPE) and the strides must be multiples of it, the pointers aligned to it.
+int layer_vec(const rel_problem* p, const rel_layer_opts* o, std::initializer_list<const void*> ptrs) {
+  const size_t es = elem_size(p->dtype);
+  const int vmax = (int)(16 / es);
+  for (int v : {vmax, 2, 1}) {
+    bool ok = p->D % v == 0 && p->stride_t % v == 0 && p->stride_h % v == 0 && p->stride_b % v == 0;
+    if (o->rope_base > 0.0) ok = ok && (p->D / 2) % v == 0;
+    for (const void* x : ptrs) ok = ok && (uintptr_t)x % (v * es) == 0;
+    if (ok) return v;
+  }
+  return 1;
 }
 
 rel_status check_aligned(const void* ptr, size_t align, const char* name, bool required) {
@@ -729,45 +751,48 @@ rel_status relation_bwd_materialized(const rel_problem* p, const void* q, const 
   return REL_OK;
 }
 
-constexpr size_t kNone = (size_t)-1;
-
 bool al16(std::initializer_list<const void*> ps) {
   for (const void* x : ps)
     if ((uintptr_t)x % 16) return false;
   return true;
 }
 
-rel::LayerArgs layer_args(const rel_problem* p, const rel_layer_opts* o, const LayerPlan& L, char* ws,
+rel::LayerArgs layer_args(const rel_problem* p, const rel_layer_opts* o, const LayerPlan& L, char* prep,
                           const void* q, const void* k, const void* v, const float* theta) {
   rel::LayerArgs a{};
   a.q = q; a.k = k; a.v = v;
   a.sb = p->stride_b; a.sh = p->stride_h; a.st = p->stride_t;
-  a.qr = L.prep_qk ? ws + L.qr : nullptr;
-  a.kr = L.prep_qk ? ws + L.kr : nullptr;
-  a.vt = L.prep_v ? ws + L.vt : nullptr;
-  a.rope = L.tab != kNone ? (const float2*)(ws + L.tab) : nullptr;
+  a.qr = prep + L.qr;
+  a.kr = prep + L.kr;
+  a.vt = prep + L.vt;
+  a.rope = L.tab != kNone ? (const float2*)(prep + L.tab) : nullptr;
   a.theta = theta;
   a.givens = o->givens;
   a.B = (int)p->B; a.H = (int)p->H; a.T = (int)p->T; a.D = (int)p->D; a.DP = (int)L.DP;
   return a;
 }
 
-size_t relation_layer_fwd_workspace_bytes(const rel_problem* p, const rel_layer_opts* opts) {
+size_t relation_layer_saved_bytes(const rel_problem* p, const rel_layer_opts* opts) {
   bool empty = false;
   if (check_layer_problem(p, opts, &empty) != REL_OK || empty) return 0;
-  return plan_layer(p, opts, false, false).total;
+  return plan_layer(p, opts).prep;
+}
+
+size_t relation_layer_fwd_workspace_bytes(const rel_problem* p, const rel_layer_opts* opts) {
+  return relation_layer_saved_bytes(p, opts);
 }
 
 size_t relation_layer_bwd_workspace_bytes(const rel_problem* p, const rel_layer_opts* opts) {
   bool empty = false;
   if (check_layer_problem(p, opts, &empty) != REL_OK || empty) return 0;
-  return plan_layer(p, opts, true, false).total;
+  const LayerPlan L = plan_layer(p, opts);
+  return L.prep + L.scratch;
 }
 
 rel_status relation_layer_fwd(const rel_problem* p, const rel_layer_opts* opts, const void* q,
                               const void* k, const void* v, const float* lambda, const float* theta,
-                              void* out, float* row_stat, void* workspace, size_t workspace_bytes,
-                              void* stream) {
+                              void* out, float* row_stat, void* saved, size_t saved_bytes,
+                              void* workspace, size_t workspace_bytes, void* stream) {
   bool empty = false;
   REL_TRY(check_layer_problem(p, opts, &empty));
   if (empty) return REL_OK;
@@ -780,11 +805,19 @@ rel_status relation_layer_fwd(const rel_problem* p, const rel_layer_opts* opts, 
   REL_TRY(check_aligned(lambda, 4, "lambda", true));
   REL_TRY(check_aligned(theta, 4, "theta", giv));
   REL_TRY(check_aligned(row_stat, 4, "row_stat", false));
-  const LayerPlan L = plan_layer(p, opts, false, al16({q, k, v, out}));
-  if (L.total > 0 && (!workspace || workspace_bytes < L.total))
-    return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
-                workspace ? workspace_bytes : (size_t)0);
-  if ((uintptr_t)workspace % 16) return fail(REL_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
+  REL_TRY(check_aligned(saved, 16, "saved", false));
+  const LayerPlan L = plan_layer(p, opts);
+  if (L.pass) return relation_fwd(&L.pp, q, k, v, lambda, out, row_stat, nullptr, nullptr, nullptr, stream);
+  if (saved && saved_bytes < L.prep)
+    return fail(REL_ERR_WORKSPACE, "saved buffer of %zu bytes needed, %zu given", L.prep, saved_bytes);
+  char* prep = (char*)saved;
+  if (!prep) {
+    if (!workspace || workspace_bytes < L.prep)
+      return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", L.prep,
+                  workspace ? workspace_bytes : (size_t)0);
+    REL_TRY(check_aligned(workspace, 16, "workspace", true));
+    prep = (char*)workspace;
+  }
   const size_t tb = (size_t)extent_elems(p) * es, rb = (size_t)(p->B * p->H * p->T) * 4;
   REL_TRY(check_buffers(p, {{q, tb, true, false, "q"},
                             {k, tb, true, false, "k"},
@@ -793,20 +826,20 @@ rel_status relation_layer_fwd(const rel_problem* p, const rel_layer_opts* opts, 
                             {giv ? theta : nullptr, (size_t)(p->H / 2) * 4, false, false, "theta"},
                             {out, tb, true, true, "out"},
                             {row_stat, rb, false, true, "row_stat"},
-                            {L.total ? workspace : nullptr, L.total, false, true, "workspace"}}));
+                            {prep, L.prep, false, true, "saved / workspace"}}));
   if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected by RELATION_TEST_FAIL_LAUNCH");
-  char* ws = (char*)workspace;
   const hipStream_t s = (hipStream_t)stream;
-  const rel::LayerArgs a = layer_args(p, opts, L, ws, q, k, v, theta);
+  const rel::LayerArgs a = layer_args(p, opts, L, prep, q, k, v, theta);
+  const int vec = layer_vec(p, opts, {q, k, v, out});
   hipError_t he = hipSuccess;
   if (a.rope && (he = rel::launch_rope_table((float2*)a.rope, (int)p->T, (int)p->D, opts->rope_base, s)))
     return hip_fail(he, "RoPE table launch");
-  if ((L.prep_qk || L.prep_v) && (he = rel::launch_layer_prologue(a, p->dtype, s)))
-    return hip_fail(he, "layer prologue launch");
-  void* y = L.direct ? out : ws + L.yp;
-  REL_TRY(relation_fwd(&L.pp, L.prep_qk ? a.qr : q, L.prep_qk ? a.kr : k, L.prep_v ? a.vt : v, lambda, y,
-                       row_stat, nullptr, nullptr, nullptr, stream));
-  if (!L.direct && (he = rel::launch_layer_repad(y, out, a, false, p->dtype, s)))
+  if ((he = rel::launch_layer_prologue(a, p->dtype, vec, s))) return hip_fail(he, "layer prologue launch");
+  // the output goes straight to the caller when its layout is the padded one
+  const bool y_direct = L.contiguous_tiled && al16({out});
+  void* y = y_direct ? out : prep + L.yp;
+  REL_TRY(relation_fwd(&L.pp, a.qr, a.kr, a.vt, lambda, y, row_stat, nullptr, nullptr, nullptr, stream));
+  if (!y_direct && (he = rel::launch_layer_repad(y, out, a, false, p->dtype, vec, s)))
     return hip_fail(he, "layer output copy launch");
   return REL_OK;
 }
@@ -814,8 +847,9 @@ rel_status relation_layer_fwd(const rel_problem* p, const rel_layer_opts* opts, 
 rel_status relation_layer_bwd(const rel_problem* p, const rel_layer_opts* opts, const void* q,
                               const void* k, const void* v, const void* out, const void* dout,
                               const float* lambda, const float* theta, const float* row_stat,
-                              void* dq, void* dk, void* dv, float* dlambda, float* dtheta,
-                              void* workspace, size_t workspace_bytes, void* stream) {
+                              const void* saved, size_t saved_bytes, void* dq, void* dk, void* dv,
+                              float* dlambda, float* dtheta, void* workspace, size_t workspace_bytes,
+                              void* stream) {
   bool empty = false;
   REL_TRY(check_layer_problem(p, opts, &empty));
   const bool giv = opts->givens != REL_GIVENS_NONE;
@@ -843,11 +877,21 @@ rel_status relation_layer_bwd(const rel_problem* p, const rel_layer_opts* opts, 
   REL_TRY(check_aligned(dlambda, 4, "dlambda", true));
   REL_TRY(check_aligned(theta, 4, "theta", giv));
   REL_TRY(check_aligned(dtheta, 4, "dtheta", giv));
-  const LayerPlan L = plan_layer(p, opts, true, al16({q, k, v, out, dout, dq, dk, dv}));
-  if (!workspace || workspace_bytes < L.total)
-    return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
+  REL_TRY(check_aligned(saved, 16, "saved", false));
+  const LayerPlan L = plan_layer(p, opts);
+  if (saved && !L.pass && saved_bytes < L.prep)
+    return fail(REL_ERR_WORKSPACE, "saved buffer of %zu bytes needed, %zu given", L.prep, saved_bytes);
+  const size_t need = (saved || L.pass ? 0 : L.prep) + L.scratch;
+  if (!workspace || workspace_bytes < need)
+    return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
                 workspace ? workspace_bytes : (size_t)0);
-  if ((uintptr_t)workspace % 16) return fail(REL_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
+  REL_TRY(check_aligned(workspace, 16, "workspace", true));
+  char* ws = (char*)workspace;
+  if (L.pass)
+    return relation_bwd(&L.pp, q, k, v, out, dout, lambda, row_stat, dq, dk, dv, dlambda, nullptr, ws + L.bws,
+                        relation_bwd_workspace_bytes(&L.pp), stream);
+  char* prep = saved ? (char*)saved : ws;
+  char* scr = saved ? ws : ws + L.prep;
   const size_t tb = (size_t)extent_elems(p) * es, rb = (size_t)(p->B * p->H * p->T) * 4;
   const size_t thb = (size_t)(p->H / 2) * 4;
   REL_TRY(check_buffers(p, {{q, tb, true, false, "q"},
@@ -858,40 +902,40 @@ rel_status relation_layer_bwd(const rel_problem* p, const rel_layer_opts* opts, 
                             {lambda, 4, false, false, "lambda"},
                             {giv ? theta : nullptr, thb, false, false, "theta"},
                             {row_stat, rb, false, false, "row_stat"},
+                            {saved, L.prep, false, false, "saved"},
                             {dq, tb, true, true, "dq"},
                             {dk, tb, true, true, "dk"},
                             {dv, tb, true, true, "dv"},
                             {dlambda, 4, false, true, "dlambda"},
                             {giv ? dtheta : nullptr, thb, false, true, "dtheta"},
-                            {workspace, L.total, false, true, "workspace"}}));
+                            {workspace, need, false, true, "workspace"}}));
   if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected by RELATION_TEST_FAIL_LAUNCH");
-  char* ws = (char*)workspace;
-  rel::LayerArgs a = layer_args(p, opts, L, ws, q, k, v, theta);
+  rel::LayerArgs a = layer_args(p, opts, L, prep, q, k, v, theta);
+  const int vec = layer_vec(p, opts, {q, k, v, out, dout, dq, dk, dv});
   hipError_t he = hipSuccess;
-  if (a.rope && (he = rel::launch_rope_table((float2*)a.rope, (int)p->T, (int)p->D, opts->rope_base, s)))
-    return hip_fail(he, "RoPE table launch");
-  if ((L.prep_qk || L.prep_v) && (he = rel::launch_layer_prologue(a, p->dtype, s)))
-    return hip_fail(he, "layer prologue launch");
-  const void* y = out;
-  const void* g = dout;
-  if (!L.direct) {
-    if ((he = rel::launch_layer_repad(out, ws + L.yp, a, true, p->dtype, s)) ||
-        (he = rel::launch_layer_repad(dout, ws + L.dop, a, true, p->dtype, s)))
+  const bool y_direct = L.contiguous_tiled && al16({out});
+  if (!saved) {
+    // recompute what the forward pass prepared
+    if (a.rope && (he = rel::launch_rope_table((float2*)a.rope, (int)p->T, (int)p->D, opts->rope_base, s)))
+      return hip_fail(he, "RoPE table launch");
+    if ((he = rel::launch_layer_prologue(a, p->dtype, vec, s))) return hip_fail(he, "layer prologue launch");
+    if (!y_direct && (he = rel::launch_layer_repad(out, prep + L.yp, a, true, p->dtype, vec, s)))
       return hip_fail(he, "layer padding launch");
-    y = ws + L.yp;
-    g = ws + L.dop;
   }
-  a.gq = L.gq != kNone ? ws + L.gq : nullptr;
-  a.gk = L.gk != kNone ? ws + L.gk : nullptr;
-  a.gv = L.gv != kNone ? ws + L.gv : nullptr;
+  const bool do_direct = L.contiguous_tiled && al16({dout});
+  if (!do_direct && (he = rel::launch_layer_repad(dout, scr + L.dop, a, true, p->dtype, vec, s)))
+    return hip_fail(he, "layer padding launch");
+  a.gq = scr + L.gq;
+  a.gk = scr + L.gk;
+  a.gv = scr + L.gv;
   a.dq = dq; a.dk = dk; a.dv = dv;
-  a.dth_rows = giv ? (float*)(ws + L.dth) : nullptr;
-  REL_TRY(relation_bwd(&L.pp, L.prep_qk ? a.qr : q, L.prep_qk ? a.kr : k, L.prep_v ? a.vt : v, y, g, lambda,
-                       row_stat, a.gq ? (void*)a.gq : dq, a.gk ? (void*)a.gk : dk, a.gv ? (void*)a.gv : dv,
-                       dlambda, nullptr, ws + L.bws, relation_bwd_workspace_bytes(&L.pp), stream));
-  if ((a.gq || a.gv) && (he = rel::launch_layer_epilogue(a, p->dtype, s)))
-    return hip_fail(he, "layer epilogue launch");
-  if (giv && (he = rel::launch_segment_sum(a.dth_rows, (int)(p->H / 2), p->B * p->T, dtheta, s)))
+  a.dth_rows = giv ? (float*)(scr + L.dth) : nullptr;
+  REL_TRY(relation_bwd(&L.pp, a.qr, a.kr, a.vt, y_direct ? out : prep + L.yp, do_direct ? dout : scr + L.dop,
+                       lambda, row_stat, (void*)a.gq, (void*)a.gk, (void*)a.gv, dlambda, nullptr, scr + L.bws,
+                       relation_bwd_workspace_bytes(&L.pp), stream));
+  if ((he = rel::launch_layer_epilogue(a, p->dtype, vec, s))) return hip_fail(he, "layer epilogue launch");
+  if (giv && (he = rel::launch_segment_sum(a.dth_rows, (int)(p->H / 2), p->B * p->T, (float*)(scr + L.dpart),
+                                           dtheta, s)))
     return hip_fail(he, "dtheta reduction launch");
   return REL_OK;
 }

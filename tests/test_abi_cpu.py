@@ -182,29 +182,29 @@ def lopts(rope=1.0e4, givens=1, reserved=0):
     return R.RelLayerOpts(rope, givens, reserved)
 
 
-def layer_fwd(lib, p, o, theta=True, ws_bytes=None):
+def layer_fwd(lib, p, o, theta=True, ws_bytes=None, saved=None, saved_bytes=0):
     a = ptrs(8)
     need = lib.relation_layer_fwd_workspace_bytes(ctypes.byref(p), ctypes.byref(o))
     n = need if ws_bytes is None else ws_bytes
     return lib.relation_layer_fwd(ctypes.byref(p), ctypes.byref(o), a[0], a[1], a[2], a[3],
-                                  a[4] if theta else None, a[5], a[6], a[7], n, None)
+                                  a[4] if theta else None, a[5], a[6], saved, saved_bytes, a[7], n, None)
 
 
 def test_layer_workspace_sizes(lib):
     p = prob(B=2, H=4, T=100, D=60, st=60)
     es, DP = 2, 64
     tensor = 2 * 4 * 100 * DP * es
+    sv = lib.relation_layer_saved_bytes(ctypes.byref(p), ctypes.byref(lopts()))
     fw = lib.relation_layer_fwd_workspace_bytes(ctypes.byref(p), ctypes.byref(lopts()))
     bw = lib.relation_layer_bwd_workspace_bytes(ctypes.byref(p), ctypes.byref(lopts()))
-    # forward: rotated q, k, mixed v and the padded output; the [T, D/2] cos/sin table
-    assert fw >= 4 * tensor + 100 * 30 * 8
-    # backward adds padded out and dout, three padded gradients, one dtheta term per (pair, b, t)
-    assert bw >= fw + 4 * tensor + 2 * 2 * 100 * 4
-    # no RoPE, no mixing, a tiled width, contiguous: nothing is prepared in the largest plan
-    # except the copies made when the caller's pointers are not 16-byte aligned
+    # saved: rotated q, k, mixed v and the padded output; the [T, D/2] cos/sin table
+    assert sv >= 4 * tensor + 100 * 30 * 8 and fw == sv
+    # backward adds padded dout, three padded gradients, one dtheta term per (pair, b, t)
+    assert bw >= sv + 4 * tensor + 2 * 2 * 100 * 4
+    # a pass-through layer (no RoPE, no mixing, tiled width, contiguous) prepares nothing
     p64 = prob(B=2, H=4, T=100, D=64)
-    plain = lib.relation_layer_fwd_workspace_bytes(ctypes.byref(p64), ctypes.byref(lopts(0.0, 0)))
-    assert plain >= 4 * 2 * 4 * 100 * 64 * 2
+    assert lib.relation_layer_saved_bytes(ctypes.byref(p64), ctypes.byref(lopts(0.0, 0))) == 0
+    assert lib.relation_layer_saved_bytes(ctypes.byref(p64), ctypes.byref(lopts(1.0e4, 0))) > 0
     assert lib.relation_layer_fwd_workspace_bytes(ctypes.byref(prob(T=0)), ctypes.byref(lopts())) == 0
     assert lib.relation_layer_fwd_workspace_bytes(None, ctypes.byref(lopts())) == 0
     assert lib.relation_layer_fwd_workspace_bytes(ctypes.byref(p), None) == 0
@@ -231,22 +231,34 @@ def test_layer_validation(lib, pmut, omut, code):
 
 def test_layer_arguments(lib):
     p = prob(D=60, st=60)
-    assert layer_fwd(lib, p, lopts(), theta=False) == R.REL_ERR_INVALID_ARG      # angles required
-    assert layer_fwd(lib, p, lopts(givens=0), theta=False) == R.REL_ERR_HIP
-    assert layer_fwd(lib, p, lopts(), ws_bytes=16) == R.REL_ERR_WORKSPACE
-    a = ptrs(8)
     o = lopts()
+    assert layer_fwd(lib, p, o, theta=False) == R.REL_ERR_INVALID_ARG      # angles required
+    assert layer_fwd(lib, p, lopts(givens=0), theta=False) == R.REL_ERR_HIP
+    assert layer_fwd(lib, p, o, ws_bytes=16) == R.REL_ERR_WORKSPACE
+    sv = lib.relation_layer_saved_bytes(ctypes.byref(p), ctypes.byref(o))
+    saved = BASE + 12 * MB
+    assert layer_fwd(lib, p, o, ws_bytes=0, saved=saved, saved_bytes=sv - 1) == R.REL_ERR_WORKSPACE
+    assert layer_fwd(lib, p, o, ws_bytes=0, saved=saved, saved_bytes=sv) == R.REL_ERR_HIP  # no workspace needed
+    assert layer_fwd(lib, p, o, saved=saved + 8, saved_bytes=sv) == R.REL_ERR_INVALID_ARG  # misaligned
+    a = ptrs(8)
     assert lib.relation_layer_fwd(ctypes.byref(p), ctypes.byref(o), a[0], a[1], a[2], a[3], a[4], a[0],
-                                  a[6], a[7], 1 << 30, None) == R.REL_ERR_INVALID_ARG  # out == q
+                                  a[6], None, 0, a[7], 1 << 30, None) == R.REL_ERR_INVALID_ARG  # out == q
     # backward: a valid request reaches the device; a short workspace does not
     need = lib.relation_layer_bwd_workspace_bytes(ctypes.byref(p), ctypes.byref(o))
     b = ptrs(16)
-    args = [ctypes.byref(p), ctypes.byref(o)] + b[:14]
-    assert lib.relation_layer_bwd(*args, need - 1, None) == R.REL_ERR_WORKSPACE
-    assert lib.relation_layer_bwd(*args, need, None) == R.REL_ERR_HIP
-    args_nodth = [ctypes.byref(p), ctypes.byref(o)] + b[:12] + [None, b[13]]
-    assert lib.relation_layer_bwd(*args_nodth, need, None) == R.REL_ERR_INVALID_ARG  # dtheta required
+
+    def bwd(saved_ptr, saved_n, ws_n, dtheta=True):
+        args = b[:8] + [saved_ptr, saved_n] + b[8:11] + [b[11], b[12] if dtheta else None, b[13], ws_n]
+        return lib.relation_layer_bwd(ctypes.byref(p), ctypes.byref(o), *args, None)
+
+    assert bwd(None, 0, need - 1) == R.REL_ERR_WORKSPACE
+    assert bwd(None, 0, need) == R.REL_ERR_HIP
+    assert bwd(None, 0, need, dtheta=False) == R.REL_ERR_INVALID_ARG     # dtheta required
+    # with the forward's saved buffer the backward needs less workspace
+    assert bwd(b[14], sv, need - sv) == R.REL_ERR_HIP
+    assert bwd(b[14], sv, need - sv - 1) == R.REL_ERR_WORKSPACE
+    assert bwd(b[14], sv - 1, need) == R.REL_ERR_WORKSPACE
     # empty problem with no scalar outputs: nothing to launch
     pe = prob(B=0)
-    assert lib.relation_layer_bwd(ctypes.byref(pe), ctypes.byref(o), *([None] * 11), None, None, None, 0,
-                                  None) == R.REL_OK
+    assert lib.relation_layer_bwd(ctypes.byref(pe), ctypes.byref(o), *([None] * 8), None, 0, *([None] * 5), None,
+                                  0, None) == R.REL_OK

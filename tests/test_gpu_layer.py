@@ -54,8 +54,17 @@ def check_layer(x, dtype, pairing, rope_base):
     th = x["theta"] if pairing else None
     f = R.relation_layer_fwd(x["q"], x["k"], x["v"], x["lam"], th, pairing=pairing, rope_base=rope_base)
     g = R.relation_layer_bwd(x["q"], x["k"], x["v"], f["o"], x["dout"], x["lam"], f["row_stat"], th,
-                             pairing=pairing, rope_base=rope_base)
+                             saved=f["saved"], pairing=pairing, rope_base=rope_base)
+    # without the saved operands: the forward prepares them in its workspace and
+    # the backward recomputes them, with the same kernels, so bit for bit the same
+    f2 = R.relation_layer_fwd(x["q"], x["k"], x["v"], x["lam"], th, pairing=pairing, rope_base=rope_base,
+                              keep_saved=False)
+    g2 = R.relation_layer_bwd(x["q"], x["k"], x["v"], f2["o"], x["dout"], x["lam"], f2["row_stat"], th,
+                              pairing=pairing, rope_base=rope_base)
     torch.cuda.synchronize()
+    assert torch.equal(f["o"], f2["o"]) and torch.equal(f["row_stat"], f2["row_stat"])
+    for n in ("dq", "dk", "dv", "dlambda") + (("dtheta",) if pairing else ()):
+        assert torch.equal(g[n], g2[n]), f"{n}: saved and recomputed operands differ"
     thr = x["thr"] if pairing else None
     of = LO.layer_forward(x["qr"], x["kr"], x["vr"], x["lam"], thr, pairing, rope_base)
     ob = LO.layer_backward(x["qr"], x["kr"], x["vr"], x["lam"], x["doutr"], thr, pairing, rope_base)
@@ -110,6 +119,7 @@ def test_layer_plain_matches_operator():
     points run the operator on the caller's tensors, bit for bit."""
     x = _prep(2, 4, 257, 64, "bf16", seed=601)
     f1 = R.relation_layer_fwd(x["q"], x["k"], x["v"], x["lam"], rope_base=0.0)
+    assert f1["saved"] is None  # nothing to prepare
     f2 = R.relation_fwd(x["q"], x["k"], x["v"], x["lam"])
     g1 = R.relation_layer_bwd(x["q"], x["k"], x["v"], f1["o"], x["dout"], x["lam"], f1["row_stat"], rope_base=0.0)
     g2 = R.relation_bwd(x["q"], x["k"], x["v"], f2["o"], x["dout"], x["lam"], f2["row_stat"])
@@ -127,7 +137,8 @@ def test_layer_strided_matches_contiguous():
     outs = []
     for q, k, v, do in ((x["q"], x["k"], x["v"], x["dout"]), (t(x["q"]), t(x["k"]), t(x["v"]), t(x["dout"]))):
         f = R.relation_layer_fwd(q, k, v, x["lam"], x["theta"], pairing="A")
-        g = R.relation_layer_bwd(q, k, v, f["o"], do, x["lam"], f["row_stat"], x["theta"], pairing="A")
+        g = R.relation_layer_bwd(q, k, v, f["o"], do, x["lam"], f["row_stat"], x["theta"], saved=f["saved"],
+                                 pairing="A")
         outs.append((f, g))
     torch.cuda.synchronize()
     (f1, g1), (f2, g2) = outs
@@ -141,7 +152,7 @@ def test_layer_repeatability():
     x = _prep(2, 4, 333, 80, "bf16", seed=603)
     f = R.relation_layer_fwd(x["q"], x["k"], x["v"], x["lam"], x["theta"], pairing="B")
     runs = [R.relation_layer_bwd(x["q"], x["k"], x["v"], f["o"], x["dout"], x["lam"], f["row_stat"], x["theta"],
-                                 pairing="B") for _ in range(3)]
+                                 saved=f["saved"], pairing="B") for _ in range(3)]
     torch.cuda.synchronize()
     for r in runs[1:]:
         for n in ("dq", "dk", "dv", "dlambda", "dtheta"):
@@ -159,7 +170,8 @@ def test_layer_paper_geometries(name):
     log(f"[{name}] running B={B} of {w.B}")
     th = x["theta"]
     f = R.relation_layer_fwd(x["q"], x["k"], x["v"], x["lam"], th, pairing="A")
-    g = R.relation_layer_bwd(x["q"], x["k"], x["v"], f["o"], x["dout"], x["lam"], f["row_stat"], th, pairing="A")
+    g = R.relation_layer_bwd(x["q"], x["k"], x["v"], f["o"], x["dout"], x["lam"], f["row_stat"], th,
+                             saved=f["saved"], pairing="A")
     torch.cuda.synchronize()
     # oracle on one batch entry (all heads, since Givens couples head pairs)
     sl = lambda a: a[:1]
