@@ -307,7 +307,8 @@ def layer_leg(hip, lib, K: int, warmup: int) -> dict:
         return t
 
     fused = kernel_ms("fwd") + kernel_ms("bwd")
-    N, T, D, DP, es = w.N, w.T, w.D, 128, 2
+    N, T, D, es = w.N, w.T, w.D, 2
+    DP = 32 if D <= 32 else 64 if D <= 64 else 96 if D <= 96 else 128  # tiled width (bf16)
     row, prow = N * T * D * es, N * T * DP * es
     # algorithmic bytes of the layer's own passes in one step (the backward
     # reads the forward's prepared operands, so it prepares nothing again)

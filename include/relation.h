@@ -62,8 +62,8 @@ typedef enum rel_dtype {
 } rel_dtype;
 
 typedef struct rel_problem {
-  int64_t B, H, T, D;   /* batch, heads, sequence length, head width. D in {32, 64, 128}
-                           (the layer entry points take any D <= 128) */
+  int64_t B, H, T, D;   /* batch, heads, sequence length, head width. D in {32, 64, 128},
+                           or 96 with bf16 (the layer entry points take any D <= 128) */
   int32_t dtype;        /* rel_dtype of q, k, v, o, dout, dq, dk, dv */
   int32_t causal;       /* must be 1: the paper defines only the causal R (eq. 2) */
   float tau_s;          /* Self temperature, finite and > 0 (paper: 2.0) */
@@ -171,7 +171,7 @@ rel_status relation_bwd_materialized(const rel_problem* p, const void* q, const 
  *   y     =  the causal Full Relation of (RoPE(q), RoPE(k), v~).
  * Here p->D is the true head width d_h: any D <= 128 (even when RoPE is on).
  * Widths the fused kernels do not tile (e.g. the paper's 48, 60, 80) are run
- * with zero channels appended up to 32, 64 or 128; scale <= 0 still means
+ * with zero channels appended up to 32, 64, 96 (bf16) or 128; scale <= 0 still means
  * 1/sqrt(d_h) of the true width. Strides need only be multiples of the
  * element size here.
  *   opts        rope_base > 0 turns RoPE on (the paper uses 1e4), 0 off;
@@ -183,7 +183,7 @@ rel_status relation_bwd_materialized(const rel_problem* p, const void* q, const 
  *               16-byte aligned, owned by the caller from the forward call to
  *               the backward call: the prepared operands (rotated q and k,
  *               mixed v, the forward's output, each [B,H,T,DP] with DP = 32,
- *               64 or 128 the tiled width) and a [T, D/2] cos/sin table. The
+ *               64, 96 or 128 the tiled width) and a [T, D/2] cos/sin table. The
  *               forward pass writes it; the backward pass reads it instead of
  *               preparing the operands again. NULL: the forward pass prepares
  *               them in its workspace and the backward pass recomputes them.

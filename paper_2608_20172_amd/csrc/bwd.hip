@@ -735,6 +735,7 @@ hipError_t launch_bwd(const BwdArgs& a, int dtype, int D, hipStream_t stream) {
   if (dtype == 1) {
     if (D == 32) launch_pair<PolBF16<32>, 32>(a, mkv, mq, stream, pe);
     else if (D == 64) launch_pair<PolBF16<64>, 64>(a, mkv, mq, stream, pe);
+    else if (D == 96) launch_pair<PolBF16<96>, 96>(a, mkv, mq, stream, pe);
     else launch_pair<PolBF16<128>, 128>(a, mkv, mq, stream, pe);
   } else {
     if (D == 32) launch_pair<PolF32<32>, 32>(a, mkv, mq, stream, pe);

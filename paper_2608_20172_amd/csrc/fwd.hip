@@ -533,6 +533,7 @@ hipError_t launch_fwd(const FwdArgs& a0, int dtype, int D, hipStream_t stream) {
   if (dtype == 1) {
     if (D == 32) launch_one<PolBF16<32>, 32>(a, stream);
     else if (D == 64) launch_one<PolBF16<64>, 64>(a, stream);
+    else if (D == 96) launch_one<PolBF16<96>, 96>(a, stream);
     else launch_one<PolBF16<128>, 128>(a, stream);
   } else {
     if (D == 32) launch_one<PolF32<32>, 32>(a, stream);

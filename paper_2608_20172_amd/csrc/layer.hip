@@ -7,8 +7,8 @@
 // against the T^2 work of the fused kernels, so the rotation, the mixing and the
 // padding run once per row here instead of once per key tile inside the fused
 // kernels. They are bound by HBM: every thread moves VEC contiguous channels
-// (16 bytes when the caller's layout allows it), TPR = min(64, DP / VEC)
-// threads cover one row, and rows are contiguous in the padded layout.
+// (16 bytes when the caller's layout allows it), TPR threads (a power of two,
+// at most 64) cover one row, and rows are contiguous in the padded layout.
 //
 // RoPE rotates channel d with channel d + D/2 by t * base^(-2d/D) (t zero-based),
 // with cos and sin from a per-call [T, D/2] table evaluated in fp64.
@@ -330,10 +330,13 @@ dim3 row_grid(const LayerArgs& a, int tpr) {
   return dim3((unsigned)((rows + per - 1) / per));
 }
 
-// Instantiates kernel K for (TI, VEC) with TPR = min(64, DP / VEC).
+// Instantiates kernel K for (TI, VEC) with TPR = the power of two at or above
+// DP / VEC, at most 64 (with DP = 96 some threads of a row stay idle, which
+// keeps a row's loads in one pass and the row groups aligned within a wave).
 #define REL_LAYER_DISPATCH(K, TI, VEC, ...)                                                           \
   do {                                                                                                \
-    const int tpr_ = a.DP / (VEC) >= 64 ? 64 : a.DP / (VEC);                                          \
+    int tpr_ = 4;                                                                                     \
+    while (tpr_ < 64 && tpr_ * (VEC) < a.DP) tpr_ *= 2;                                               \
     if (tpr_ == 64)                                                                                   \
       hipLaunchKernelGGL((K<TI, VEC, 64>), row_grid(a, 64), dim3(kLThreads), 0, stream, __VA_ARGS__); \
     else if (tpr_ == 32)                                                                              \

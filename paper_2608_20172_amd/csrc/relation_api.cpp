@@ -136,8 +136,9 @@ rel_status check_problem(const rel_problem* p, bool* empty) {
   if (!(std::isfinite(p->tau_s) && p->tau_s > 0.0f))
     return fail(REL_ERR_INVALID_ARG, "tau_s must be finite and > 0 (got %g)", (double)p->tau_s);
   if (!std::isfinite(p->scale)) return fail(REL_ERR_INVALID_ARG, "scale must be finite");
-  if (p->D != 32 && p->D != 64 && p->D != 128)
-    return fail(REL_ERR_UNSUPPORTED, "head dimension %lld not in {32, 64, 128}", (long long)p->D);
+  if (p->D != 32 && p->D != 64 && p->D != 128 && !(p->D == 96 && p->dtype == REL_BF16))
+    return fail(REL_ERR_UNSUPPORTED, "head dimension %lld not in {32, 64, 128} (or 96 for bf16)",
+                (long long)p->D);
   *empty = (p->B == 0 || p->H == 0 || p->T == 0);
   if (*empty) return REL_OK;
   if (p->T > (1 << 24)) return fail(REL_ERR_UNSUPPORTED, "T = %lld exceeds 2^24", (long long)p->T);
@@ -220,7 +221,7 @@ struct LayerPlan {
 
 LayerPlan plan_layer(const rel_problem* p, const rel_layer_opts* o) {
   LayerPlan L{};
-  L.DP = p->D <= 32 ? 32 : p->D <= 64 ? 64 : 128;
+  L.DP = p->D <= 32 ? 32 : p->D <= 64 ? 64 : (p->D <= 96 && p->dtype == REL_BF16) ? 96 : 128;
   const bool contiguous = p->stride_t == p->D && (p->H == 1 || p->stride_h == p->T * p->D) &&
                           (p->B == 1 || p->stride_b == p->H * p->T * p->D);
   const bool rope = o->rope_base > 0.0, giv = o->givens != REL_GIVENS_NONE;

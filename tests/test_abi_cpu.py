@@ -63,11 +63,13 @@ def fwd(lib, p, q=None, k=None, v=None, lam=None, o=None, rs=None, sm=None, em=N
 
 def test_valid_call_reaches_launch(lib):
     assert fwd(lib, prob()) == R.REL_ERR_HIP
+    assert fwd(lib, prob(D=96)) == R.REL_ERR_HIP  # bf16 width 96
     assert b"device" in lib.relation_last_error() or b"HIP" in lib.relation_last_error()
 
 
 @pytest.mark.parametrize("mut,code", [
     (dict(D=48), R.REL_ERR_UNSUPPORTED),
+    (dict(D=96, dtype=R.REL_F32), R.REL_ERR_UNSUPPORTED),   # 96 is tiled for bf16 only
     (dict(D=256), R.REL_ERR_UNSUPPORTED),
     (dict(causal=0), R.REL_ERR_UNSUPPORTED),
     (dict(dtype=7), R.REL_ERR_UNSUPPORTED),

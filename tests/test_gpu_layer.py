@@ -93,6 +93,7 @@ def check_layer(x, dtype, pairing, rope_base):
 @pytest.mark.parametrize("D,pairing,rope", [
     (48, "A", 1.0e4), (60, "B", 1.0e4), (80, "A", 1.0e4), (64, "B", 1.0e4),
     (64, None, 1.0e4), (64, "A", 0.0), (60, None, 0.0), (128, "B", 1.0e4), (20, "A", 100.0),
+    (96, "A", 1.0e4), (100, "B", 1.0e4),
 ])
 def test_layer_bf16(D, pairing, rope):
     x = _prep(2, 4, 300, D, "bf16", seed=300 + D)

@@ -149,7 +149,7 @@ def test_tiny_fp32_forward_and_materialized():
     assert np.array_equal(_np(out["o"])[:, :, 0], x["vr"][:, :, 0])
 
 
-@pytest.mark.parametrize("D", [32, 64, 128])
+@pytest.mark.parametrize("D", [32, 64, 96, 128])
 def test_forward_bf16_ragged(D):
     x = _prep(I.make_inputs(2, 3, 333, D, seed=7, qkv_std=1 / math.sqrt(D), with_dout=False, lam=0.5), "bf16")
     check_forward(x, "bf16")
@@ -197,7 +197,7 @@ def test_forward_lambda_values(lam):
     check_forward(x, "bf16")
 
 
-@pytest.mark.parametrize("D", [32, 64, 128])
+@pytest.mark.parametrize("D", [32, 64, 96, 128])
 def test_backward_bf16_ragged(D):
     x = _prep(I.make_inputs(2, 2, 300, D, seed=11, qkv_std=1 / math.sqrt(D), lam=0.5), "bf16")
     f = check_forward(x, "bf16", with_aux=False)
