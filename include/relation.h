@@ -230,6 +230,45 @@ rel_status relation_layer_bwd(const rel_problem* p, const rel_layer_opts* opts, 
                               float* dlambda, float* dtheta, void* workspace, size_t workspace_bytes,
                               void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Decode step: the one new row of every (b, h) against a KV cache (eq. 2 at
+ * the token's absolute position). The new token's own key and value must
+ * already be in the cache at entry lengths[b] (one-based), which is its
+ * position i, so the count correction is -lambda ln(lengths[b]); entries
+ * 1 .. lengths[b] - 1 are its history. The result equals row i of
+ * relation_fwd over the sequence (and its row_stat).
+ *   p          B, H, D, dtype, tau_s, scale as for relation_fwd; T is the cache
+ *              capacity Tmax >= 1, and the strides are those of the caches.
+ *   q          [B,H,D] dtype, dense: the new token's relation query.
+ *   k_cache, v_cache  [B,H,Tmax,D] dtype with the problem's strides.
+ *   lengths    device int32 [B]: entries of the cache in use, new token
+ *              included; values outside 1..Tmax are clamped into it.
+ *   out        [B,H,D] dtype, dense: y_i.   row_stat  [B,H] fp32, optional:
+ *              M_i = ln Z_i + lambda ln i.
+ *   workspace  relation_decode_workspace_bytes(p) bytes, 16-byte aligned: the
+ *              Exchange scan states of the history's slices of 256 keys.
+ * relation_decode_states and relation_decode_merge are its two halves, for a
+ * cache split over devices (context parallelism): each device writes the
+ * states of its keys [key_begin, key_end) of its own cache (only keys before
+ * the row's own entry count) as nstates slices, in
+ *   states     fp32 [nstates][B*H][D + 2]: per slice and row m = max E_ij,
+ *              l = sum exp(E_ij - m), z = sum exp(E_ij - m) v_j (eq. 11;
+ *              an empty slice has m = -inf, l = 0, z = 0);
+ * the device that holds the new token's entry merges any number of such
+ * states (concatenated along the first axis) with the Self entry read at
+ * lengths[b] of its k_cache / v_cache. The merge rescales the states to their
+ * common maximum and adds them, then applies eqs. 12-13. */
+size_t relation_decode_workspace_bytes(const rel_problem* p);
+rel_status relation_decode(const rel_problem* p, const void* q, const void* k_cache, const void* v_cache,
+                           const int32_t* lengths, const float* lambda, void* out, float* row_stat,
+                           void* workspace, size_t workspace_bytes, void* stream);
+rel_status relation_decode_states(const rel_problem* p, const void* q, const void* k_cache,
+                                  const void* v_cache, const int32_t* lengths, int32_t key_begin,
+                                  int32_t key_end, int32_t nstates, float* states, void* stream);
+rel_status relation_decode_merge(const rel_problem* p, int32_t nstates, const float* states, const void* q,
+                                 const void* k_cache, const void* v_cache, const int32_t* lengths,
+                                 const float* lambda, void* out, float* row_stat, void* stream);
+
 /* Measurement aid. While armed, every launch of the named kernel ("fwd": the
  * fused forward kernel; "bwd_dkdv", "bwd_dq": the two backward kernels; "bwd":
  * both backward kernels, back to back) is bracketed by

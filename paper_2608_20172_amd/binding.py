@@ -4,7 +4,8 @@ memory and the current stream.
 
 Functions carry the C-ABI names (relation_fwd, relation_bwd,
 relation_fwd_materialized, relation_bwd_materialized,
-relation_exchange_allocation, relation_layer_fwd, relation_layer_bwd, ...). ``relation`` is the differentiable wrapper
+relation_exchange_allocation, relation_layer_fwd, relation_layer_bwd,
+relation_decode, relation_decode_states, relation_decode_merge, ...). ``relation`` is the differentiable wrapper
 (torch.autograd.Function) over relation_fwd / relation_bwd.
 """
 from __future__ import annotations
@@ -62,6 +63,11 @@ _SIGS = {
     "relation_layer_bwd_workspace_bytes": (ctypes.c_size_t, [_PP, _PO]),
     "relation_layer_bwd": (ctypes.c_int, [_PP, _PO, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t,
                                           _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "relation_decode_workspace_bytes": (ctypes.c_size_t, [_PP]),
+    "relation_decode": (ctypes.c_int, [_PP, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "relation_decode_states": (ctypes.c_int, [_PP, _P, _P, _P, _P, ctypes.c_int32, ctypes.c_int32,
+                                              ctypes.c_int32, _P, _P]),
+    "relation_decode_merge": (ctypes.c_int, [_PP, ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
     "relation_profile_arm": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]),
     "relation_profile_disarm": (ctypes.c_int, []),
     "relation_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -379,6 +385,64 @@ def relation_layer_bwd(q, k, v, o, dout, lam, row_stat, theta=None, *, saved=Non
                                 _stream())
     _check(st, "relation_layer_bwd")
     return {"dq": dq, "dk": dk, "dv": dv, "dlambda": dlam, "dtheta": dth}
+
+
+def _decode_io(q, k_cache, v_cache, lengths, tau_s, scale):
+    v_cache = _same_layout(k_cache, v_cache)[0]
+    B, H, T, D = k_cache.shape
+    if q.shape != (B, H, D) or q.dtype != k_cache.dtype:
+        raise ValueError("q must be [B, H, D] with the caches' dtype")
+    q = q.contiguous()
+    lengths = torch.as_tensor(lengths, dtype=torch.int32, device=q.device).reshape(B).contiguous()
+    return q, k_cache, v_cache, lengths, make_problem(k_cache, tau_s, scale)
+
+
+def relation_decode(q, k_cache, v_cache, lengths, lam, *, tau_s: float = TAU_S, scale: Optional[float] = None,
+                    workspace=None):
+    """One decode step: q [B, H, D] of the new tokens, caches [B, H, Tmax, D]
+    holding lengths[b] entries each (the new token's own entry last).
+    Returns dict(o [B, H, D], row_stat [B, H])."""
+    lib = load_library()
+    q, k_cache, v_cache, lengths, p = _decode_io(q, k_cache, v_cache, lengths, tau_s, scale)
+    dev = q.device
+    lam_t = _lam_tensor(lam, dev)
+    o = torch.empty_like(q)
+    rs = torch.empty(q.shape[:2], dtype=torch.float32, device=dev)
+    ws = _workspace(max(1, int(lib.relation_decode_workspace_bytes(ctypes.byref(p)))), workspace, dev)
+    st = lib.relation_decode(ctypes.byref(p), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(lengths), _ptr(lam_t),
+                             _ptr(o), _ptr(rs), _ptr(ws), _nbytes(ws), _stream())
+    _check(st, "relation_decode")
+    return {"o": o, "row_stat": rs}
+
+
+def relation_decode_states(q, k_cache, v_cache, lengths, key_begin: int, key_end: int, nstates: int = 1, *,
+                           tau_s: float = TAU_S, scale: Optional[float] = None):
+    """Exchange scan states [nstates, B*H, D + 2] (m, l, z) of cache keys
+    [key_begin, key_end) for the new tokens' rows."""
+    lib = load_library()
+    q, k_cache, v_cache, lengths, p = _decode_io(q, k_cache, v_cache, lengths, tau_s, scale)
+    B, H, _, D = k_cache.shape
+    states = torch.empty((nstates, B * H, D + 2), dtype=torch.float32, device=q.device)
+    st = lib.relation_decode_states(ctypes.byref(p), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(lengths),
+                                    int(key_begin), int(key_end), int(nstates), _ptr(states), _stream())
+    _check(st, "relation_decode_states")
+    return states
+
+
+def relation_decode_merge(states, q, k_cache, v_cache, lengths, lam, *, tau_s: float = TAU_S,
+                          scale: Optional[float] = None):
+    """Merge states [n, B*H, D + 2] with the Self entry; dict(o, row_stat)."""
+    lib = load_library()
+    q, k_cache, v_cache, lengths, p = _decode_io(q, k_cache, v_cache, lengths, tau_s, scale)
+    dev = q.device
+    states = states.to(dtype=torch.float32).contiguous()
+    lam_t = _lam_tensor(lam, dev)
+    o = torch.empty_like(q)
+    rs = torch.empty(q.shape[:2], dtype=torch.float32, device=dev)
+    st = lib.relation_decode_merge(ctypes.byref(p), int(states.shape[0]), _ptr(states), _ptr(q), _ptr(k_cache),
+                                   _ptr(v_cache), _ptr(lengths), _ptr(lam_t), _ptr(o), _ptr(rs), _stream())
+    _check(st, "relation_decode_merge")
+    return {"o": o, "row_stat": rs}
 
 
 def relation_profile_arm(kernel: str, events: list) -> None:

@@ -106,6 +106,24 @@ struct LayerArgs {
   float* dth_rows;      // epilogue out: [H/2, B, T] per-row terms of dL/dtheta
 };
 
+// Arguments of the decode kernels (one new row per (b, h) against a KV cache).
+struct DecodeArgs {
+  const void* q;            // [B, H, D] dense: the new token's relation query
+  const void* k;            // caches [B, H, Tmax, D] with (sb, sh, st)
+  const void* v;
+  const int32_t* lengths;   // [B] valid entries per batch entry (the new token's own included)
+  int64_t sb, sh, st;
+  int B, H, Tmax, D;
+  float scale, inv_tau;
+  const float* lambda;
+  int key0, key1;           // states kernel: keys scanned (zero-based, half-open)
+  int nsplit;               // states kernel: slices of [key0, key1)
+  float* states;            // [nsplit or nstates][B H][D + 2]: m, l, z
+  int nstates;              // merge kernel: states per row
+  void* out;                // merge kernel: [B, H, D] dense
+  float* row_stat;          // merge kernel: [B, H] or null
+};
+
 // Measurement aid: if armed for kernel `name`, returns the event pair to record
 // around the next launch of that kernel (see relation_profile_arm).
 bool profile_slot(const char* name, hipEvent_t* start, hipEvent_t* stop);
@@ -118,6 +136,9 @@ hipError_t launch_allocation(const RowArgs& a, int dtype, int N, hipStream_t str
 // Layer passes. `vec` (8, 2 or 1 for bf16; 4, 2 or 1 for fp32) is the number
 // of contiguous channels one thread moves; the caller's tensors must allow it
 // (D, D/2 with RoPE, and the strides multiples of vec; pointers aligned to it).
+int decode_slice_keys();
+hipError_t launch_decode_states(const DecodeArgs& a, int dtype, hipStream_t stream);
+hipError_t launch_decode_merge(const DecodeArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_rope_table(float2* tab, int T, int D, double base, hipStream_t stream);
 hipError_t launch_layer_prologue(const LayerArgs& a, int dtype, int vec, hipStream_t stream);
 hipError_t launch_layer_repad(const void* src, void* dst, const LayerArgs& a, bool to_padded, int dtype,

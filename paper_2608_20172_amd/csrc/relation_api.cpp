@@ -941,4 +941,121 @@ rel_status relation_layer_bwd(const rel_problem* p, const rel_layer_opts* opts, 
   return REL_OK;
 }
 
+// ---------------------------------------------------------------------------
+// decode step
+// ---------------------------------------------------------------------------
+static rel_status check_decode(const rel_problem* p, bool* empty) {
+  REL_TRY(check_problem(p, empty));
+  if (p && p->B * p->H > 0 && p->T < 1)
+    return fail(REL_ERR_INVALID_ARG, "the cache holds at least the new token's own entry (T >= 1)");
+  if (p && p->T > (1 << 30)) return fail(REL_ERR_UNSUPPORTED, "cache capacity exceeds 2^30");
+  return REL_OK;
+}
+
+static rel::DecodeArgs decode_args(const rel_problem* p, const void* q, const void* k, const void* v,
+                                   const int32_t* lengths, const float* lambda) {
+  rel::DecodeArgs a{};
+  a.q = q; a.k = k; a.v = v; a.lengths = lengths; a.lambda = lambda;
+  a.sb = p->stride_b; a.sh = p->stride_h; a.st = p->stride_t;
+  a.B = (int)p->B; a.H = (int)p->H; a.Tmax = (int)p->T; a.D = (int)p->D;
+  a.scale = eff_scale(p);
+  a.inv_tau = 1.0f / p->tau_s;
+  return a;
+}
+
+static int decode_slices(const rel_problem* p) {
+  const int64_t hist = std::max<int64_t>(p->T - 1, 1);
+  return (int)((hist + rel::decode_slice_keys() - 1) / rel::decode_slice_keys());
+}
+
+static rel_status check_decode_io(const rel_problem* p, const void* q, const void* k, const void* v,
+                                  const int32_t* lengths, const void* out, const float* row_stat,
+                                  const float* states, size_t states_bytes, bool states_out) {
+  REL_TRY(check_aligned(q, 16, "q", true));
+  REL_TRY(check_aligned(k, 16, "k_cache", true));
+  REL_TRY(check_aligned(v, 16, "v_cache", true));
+  REL_TRY(check_aligned(lengths, 4, "lengths", true));
+  REL_TRY(check_aligned(out, 16, "out", !states_out));
+  REL_TRY(check_aligned(row_stat, 4, "row_stat", false));
+  REL_TRY(check_aligned(states, 4, "states", states_bytes > 0));
+  const size_t es = elem_size(p->dtype);
+  const size_t cb = (size_t)extent_elems(p) * es, rowb = (size_t)(p->B * p->H * p->D) * es;
+  const size_t nb = (size_t)(p->B * p->H) * 4;
+  return check_buffers(p, {{q, rowb, false, false, "q"},
+                           {k, cb, true, false, "k_cache"},
+                           {v, cb, true, false, "v_cache"},
+                           {lengths, (size_t)p->B * 4, false, false, "lengths"},
+                           {states, states_bytes, false, states_out, "states"},
+                           {states_out ? nullptr : out, rowb, false, true, "out"},
+                           {states_out ? nullptr : row_stat, nb, false, true, "row_stat"}});
+}
+
+size_t relation_decode_workspace_bytes(const rel_problem* p) {
+  bool empty = false;
+  if (check_decode(p, &empty) != REL_OK || empty) return 0;
+  return align256((size_t)decode_slices(p) * (size_t)(p->B * p->H) * (size_t)(p->D + 2) * 4);
+}
+
+rel_status relation_decode_states(const rel_problem* p, const void* q, const void* k_cache,
+                                  const void* v_cache, const int32_t* lengths, int32_t key_begin,
+                                  int32_t key_end, int32_t nstates, float* states, void* stream) {
+  bool empty = false;
+  REL_TRY(check_decode(p, &empty));
+  if (empty) return REL_OK;
+  if (key_begin < 0 || key_end < key_begin || key_end > p->T)
+    return fail(REL_ERR_INVALID_ARG, "key range [%d, %d) outside the cache of %lld entries", key_begin,
+                key_end, (long long)p->T);
+  if (nstates < 1 || nstates > 65535) return fail(REL_ERR_INVALID_ARG, "nstates must be in 1..65535");
+  const size_t sb = (size_t)nstates * (size_t)(p->B * p->H) * (size_t)(p->D + 2) * 4;
+  REL_TRY(check_decode_io(p, q, k_cache, v_cache, lengths, nullptr, nullptr, states, sb, true));
+  if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected by RELATION_TEST_FAIL_LAUNCH");
+  rel::DecodeArgs a = decode_args(p, q, k_cache, v_cache, lengths, nullptr);
+  a.key0 = key_begin; a.key1 = key_end; a.nsplit = nstates; a.states = states;
+  const hipError_t e = rel::launch_decode_states(a, p->dtype, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "decode states launch");
+  return REL_OK;
+}
+
+rel_status relation_decode_merge(const rel_problem* p, int32_t nstates, const float* states, const void* q,
+                                 const void* k_cache, const void* v_cache, const int32_t* lengths,
+                                 const float* lambda, void* out, float* row_stat, void* stream) {
+  bool empty = false;
+  REL_TRY(check_decode(p, &empty));
+  if (empty) return REL_OK;
+  if (nstates < 0 || nstates > 65535) return fail(REL_ERR_INVALID_ARG, "nstates must be in 0..65535");
+  REL_TRY(check_aligned(lambda, 4, "lambda", true));
+  const size_t sb = (size_t)nstates * (size_t)(p->B * p->H) * (size_t)(p->D + 2) * 4;
+  REL_TRY(check_decode_io(p, q, k_cache, v_cache, lengths, out, row_stat, nstates ? states : nullptr, sb, false));
+  if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected by RELATION_TEST_FAIL_LAUNCH");
+  rel::DecodeArgs a = decode_args(p, q, k_cache, v_cache, lengths, lambda);
+  a.nstates = nstates; a.states = (float*)states; a.out = out; a.row_stat = row_stat;
+  const hipError_t e = rel::launch_decode_merge(a, p->dtype, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "decode merge launch");
+  return REL_OK;
+}
+
+rel_status relation_decode(const rel_problem* p, const void* q, const void* k_cache, const void* v_cache,
+                           const int32_t* lengths, const float* lambda, void* out, float* row_stat,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  bool empty = false;
+  REL_TRY(check_decode(p, &empty));
+  if (empty) return REL_OK;
+  const size_t need = relation_decode_workspace_bytes(p);
+  if (!workspace || workspace_bytes < need)
+    return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                workspace ? workspace_bytes : (size_t)0);
+  REL_TRY(check_aligned(workspace, 16, "workspace", true));
+  REL_TRY(check_aligned(lambda, 4, "lambda", true));
+  REL_TRY(check_decode_io(p, q, k_cache, v_cache, lengths, out, row_stat, (const float*)workspace, need, false));
+  if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected by RELATION_TEST_FAIL_LAUNCH");
+  rel::DecodeArgs a = decode_args(p, q, k_cache, v_cache, lengths, lambda);
+  a.key0 = 0; a.key1 = (int)p->T; a.nsplit = decode_slices(p); a.states = (float*)workspace;
+  a.nstates = a.nsplit; a.out = out; a.row_stat = row_stat;
+  hipError_t e = rel::launch_decode_states(a, p->dtype, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "decode states launch");
+  e = rel::launch_decode_merge(a, p->dtype, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "decode merge launch");
+  return REL_OK;
+}
+
 }  // extern "C"

@@ -264,3 +264,36 @@ def test_layer_arguments(lib):
     pe = prob(B=0)
     assert lib.relation_layer_bwd(ctypes.byref(pe), ctypes.byref(o), *([None] * 8), None, 0, *([None] * 5), None,
                                   0, None) == R.REL_OK
+
+
+# ---------------------------------------------------------------------------
+# decode step
+# ---------------------------------------------------------------------------
+def test_decode_validation(lib):
+    p = prob(B=2, H=3, T=1000, D=64)
+    need = lib.relation_decode_workspace_bytes(ctypes.byref(p))
+    # one state (2 + D floats) per 256-key slice of the history and (b, h) row
+    assert need >= 4 * 2 * 3 * 66 * 4
+    a = ptrs(10)
+    call = lambda pp, ws_n, **kw: lib.relation_decode(ctypes.byref(pp), kw.get("q", a[0]), a[1], a[2], a[3], a[4],
+                                                       kw.get("out", a[5]), None, a[6], ws_n, None)
+    assert call(p, need) == R.REL_ERR_HIP                 # valid: reaches the device
+    assert call(p, need - 1) == R.REL_ERR_WORKSPACE
+    assert call(p, need, q=a[0] + 8) == R.REL_ERR_INVALID_ARG   # q not 16-byte aligned
+    assert call(p, need, out=a[0]) == R.REL_ERR_INVALID_ARG     # out overlaps q
+    assert call(prob(B=2, H=3, T=0, D=64), 1 << 20) == R.REL_ERR_INVALID_ARG  # no room for the new entry
+    assert call(prob(B=0, H=3, T=8, D=64), 0) == R.REL_OK
+    assert call(prob(D=48), 1 << 20) == R.REL_ERR_UNSUPPORTED
+    # states: the key range must lie in the cache, nstates >= 1
+    st = lambda k0, k1, n: lib.relation_decode_states(ctypes.byref(p), a[0], a[1], a[2], a[3], k0, k1, n, a[7], None)
+    assert st(0, 1000, 4) == R.REL_ERR_HIP
+    assert st(-1, 10, 1) == R.REL_ERR_INVALID_ARG
+    assert st(10, 1001, 1) == R.REL_ERR_INVALID_ARG
+    assert st(20, 10, 1) == R.REL_ERR_INVALID_ARG
+    assert st(0, 10, 0) == R.REL_ERR_INVALID_ARG
+    mg = lambda n, states: lib.relation_decode_merge(ctypes.byref(p), n, states, a[0], a[1], a[2], a[3], a[4],
+                                                     a[5], None, None)
+    assert mg(3, a[7]) == R.REL_ERR_HIP
+    assert mg(0, None) == R.REL_ERR_HIP                   # no states: a pure Self row
+    assert mg(-1, a[7]) == R.REL_ERR_INVALID_ARG
+    assert mg(2, a[5]) == R.REL_ERR_INVALID_ARG           # states inside out
