@@ -324,6 +324,52 @@ def layer_leg(hip, lib, K: int, warmup: int) -> dict:
             "layer_passes_hbm_frac": nbytes / (passes_ms * 1e-3) / PEAK_HBM if passes_ms > 0 else None}
 
 
+DECODE_SHAPES = [  # (name, B, H, cache length, D): one new token per sequence
+    ("dec100m_T2048", 8, 12, 2048, 64),
+    ("batch64_T4096", 64, 12, 4096, 64),
+    ("long_T16384", 1, 16, 16384, 128),
+]
+
+
+def decode_leg(K: int) -> list:
+    """relation_decode with full caches of bf16 Gaussians at three shapes:
+    time per step and the algorithmic bytes (history K and V read once, the
+    new token's q, k, v read, y written) against the HBM peak."""
+    import numpy as np
+    import torch
+    from paper_2608_20172_amd import binding as R
+
+    out = []
+    rng = np.random.default_rng(11)
+    for name, B, H, L, D in DECODE_SHAPES:
+        dev = torch.device("cuda:0")
+        std = 1.0 / math.sqrt(D)
+        kc = (torch.randn(B, H, L, D, device=dev) * std).to(torch.bfloat16)
+        vc = torch.randn(B, H, L, D, device=dev).to(torch.bfloat16)
+        q = (torch.randn(B, H, D, device=dev) * std).to(torch.bfloat16)
+        lens = torch.full((B,), L, dtype=torch.int32, device=dev)
+        lam = torch.tensor([float(rng.normal(0, 0.02))], dtype=torch.float32, device=dev)
+        ws = torch.empty(max(1, int(R.load_library().relation_decode_workspace_bytes(
+            ctypes.byref(R.make_problem(kc))))), dtype=torch.uint8, device=dev)
+        for _ in range(3):
+            R.relation_decode(q, kc, vc, lens, lam, workspace=ws)
+        torch.cuda.synchronize()
+        n = max(10, K)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            R.relation_decode(q, kc, vc, lens, lam, workspace=ws)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / n
+        nbytes = B * H * ((L - 1) * 2 * D * 2 + 4 * D * 2)
+        out.append({"shape": name, "B": B, "H": H, "T": L, "D": D, "us_per_step": ms * 1e3,
+                    "bytes": nbytes, "GBps": nbytes / (ms * 1e-3) / 1e9,
+                    "hbm_frac": nbytes / (ms * 1e-3) / PEAK_HBM})
+        del kc, vc, q, ws
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -334,6 +380,7 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-materialized", action="store_true")
     ap.add_argument("--no-layer", action="store_true", help="skip the layer entry points leg")
+    ap.add_argument("--no-decode", action="store_true", help="skip the decode leg")
     ap.add_argument("--copy-bytes", type=int, default=0)
     ap.add_argument("--copy-kind", choices=("memcpy", "elementwise"), default="elementwise")
     ap.add_argument("--summarize-counters", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
@@ -475,6 +522,9 @@ def main() -> int:
     layer = {"status": "skipped"}
     if not args.no_layer:
         layer = layer_leg(hip, lib, K, args.warmup)
+    decode = {"status": "skipped"}
+    if not args.no_decode:
+        decode = decode_leg(K)
 
     fl_f, fl_b = flops(w, "fwd"), flops(w, "bwd") if w.backward else 0.0
     kern_flops = fl_b if w.backward else fl_f
@@ -505,6 +555,7 @@ def main() -> int:
         "fwd_kernel_tflops": fl_f / (fwd_kern_ms * 1e-3) / 1e12,
         "materialized": mat,
         "layer": layer,
+        "decode": decode,
         "roofline": {
             "kernel": "bwd_dkdv_kernel+bwd_dq_kernel" if w.backward else "fwd_kernel",
             "bound": "mfma",

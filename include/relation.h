@@ -251,7 +251,7 @@ rel_status relation_layer_bwd(const rel_problem* p, const rel_layer_opts* opts, 
  * cache split over devices (context parallelism): each device writes the
  * states of its keys [key_begin, key_end) of its own cache (only keys before
  * the row's own entry count) as nstates slices, in
- *   states     fp32 [nstates][B*H][D + 2]: per slice and row m = max E_ij,
+ *   states     fp32 [nstates][B*H][D + 2], 8-byte aligned: per slice and row m = max E_ij,
  *              l = sum exp(E_ij - m), z = sum exp(E_ij - m) v_j (eq. 11;
  *              an empty slice has m = -inf, l = 0, z = 0);
  * the device that holds the new token's entry merges any number of such

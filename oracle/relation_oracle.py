@@ -68,8 +68,13 @@ def _row_block_matrices(q, k, lam, tau_s, s, rows):
 
 
 def forward(q, k, v, lam, *, tau_s: float = TAU_S, scale: float | None = None,
-            want_matrices: bool = True, row_block: int | None = None, rows=None) -> dict:
+            want_matrices: bool = True, row_block: int | None = None, rows=None,
+            transport: str = "full") -> dict:
     """Full Relation forward for one head. q, k, v: [T, D] fp64 arrays.
+
+    ``transport="exchange"`` is the exchange-only ablation (App. C, ablation
+    definitions): the same F, but Y_i = sum_{j<i} F_ij I~_j, without the Self
+    term and without renormalising the historical weights.
 
     ``rows`` (optional, increasing zero-based indices) restricts the output to
     those query rows; each row of F is its own softmax, so a row's result does
@@ -89,6 +94,7 @@ def forward(q, k, v, lam, *, tau_s: float = TAU_S, scale: float | None = None,
     rows = np.arange(T) if rows is None else np.asarray(rows, dtype=np.int64)
     n = len(rows)
     rb = max(n, 1) if row_block is None else max(1, int(row_block))
+    exch_only = _transport(transport)
 
     Y = np.empty((n, D))
     S = np.empty(n)
@@ -103,7 +109,11 @@ def forward(q, k, v, lam, *, tau_s: float = TAU_S, scale: float | None = None,
         rr = rows[b0:b1]
         U, Sb, E, R = _row_block_matrices(q, k, lam, tau_s, s, rr)
         F = softmax(R, axis=1)                       # eq. (3): F_i = Softmax(R_i)
-        Y[b0:b1] = F @ v                             # eq. (3): Y_i = sum_j F_ij I~_j
+        Ft = F
+        if exch_only:                                # transport of historical entries only
+            Ft = F.copy()
+            Ft[np.arange(b1 - b0), rr] = 0.0
+        Y[b0:b1] = Ft @ v                            # eq. (3): Y_i = sum_j F_ij I~_j
         S[b0:b1] = Sb
         diagF = F[np.arange(b1 - b0), rr]
         self_mass[b0:b1] = diagF
@@ -132,6 +142,12 @@ def forward(q, k, v, lam, *, tau_s: float = TAU_S, scale: float | None = None,
     return out
 
 
+def _transport(transport: str) -> bool:
+    if transport not in ("full", "exchange"):
+        raise ValueError(f"unknown transport {transport!r}")
+    return transport == "exchange"
+
+
 def _silu_grad(U):
     # d SiLU(U) / dU = sigmoid(U) + U sigmoid(U) (1 - sigmoid(U))   (App. A.1.7)
     sg = expit(U)
@@ -139,7 +155,8 @@ def _silu_grad(U):
 
 
 def backward(q, k, v, lam, dout, *, tau_s: float = TAU_S, scale: float | None = None,
-             route: str = "softmax", row_block: int | None = None, rows=None) -> dict:
+             route: str = "softmax", row_block: int | None = None, rows=None,
+             transport: str = "full") -> dict:
     """Gradients of sum(dout * Y) for one head.
 
     Returns dq, dk, dv [T, D], dlam (this head's contribution; lambda is shared
@@ -156,17 +173,21 @@ def backward(q, k, v, lam, dout, *, tau_s: float = TAU_S, scale: float | None = 
     the contributions of those query rows: dq, dS and dlam for those rows, and
     dk, dv summed over those rows. With rows = {j0, ..., T-1}, dk_j and dv_j are
     complete for every j >= j0, since only rows i >= j reach key j.
+
+    ``transport="exchange"`` (softmax route only): gradients of the
+    exchange-only output, where Y_i does not depend on F_ii, so dL/dF_ii = 0
+    and I~_i receives nothing from its own row.
     """
     if route == "softmax":
-        return _backward_softmax(q, k, v, lam, dout, tau_s, scale, row_block, rows)
-    if rows is not None:
-        raise ValueError("row subsets are evaluated by the softmax route")
+        return _backward_softmax(q, k, v, lam, dout, tau_s, scale, row_block, rows, _transport(transport))
+    if rows is not None or _transport(transport):
+        raise ValueError("row subsets and exchange-only transport are evaluated by the softmax route")
     if route == "factorised":
         return _backward_factorised(q, k, v, lam, dout, tau_s, scale)
     raise ValueError(f"unknown route {route!r}")
 
 
-def _backward_softmax(q, k, v, lam, dout, tau_s, scale, row_block, rows):
+def _backward_softmax(q, k, v, lam, dout, tau_s, scale, row_block, rows, exch_only=False):
     q = np.asarray(q, np.float64)
     k = np.asarray(k, np.float64)
     v = np.asarray(v, np.float64)
@@ -189,7 +210,12 @@ def _backward_softmax(q, k, v, lam, dout, tau_s, scale, row_block, rows):
         U, Sb, E, R = _row_block_matrices(q, k, lam, tau_s, s, rr)
         F = softmax(R, axis=1)
         Gb = G[rr]
-        H = Gb @ v.T                                   # H_ij = G_i . I~_j
+        H = Gb @ v.T                                   # H_ij = G_i . I~_j = dL/dF_ij
+        Ft = F
+        if exch_only:                                  # F_ii is not transported
+            H[np.arange(nb), rr] = 0.0
+            Ft = F.copy()
+            Ft[np.arange(nb), rr] = 0.0
         Drow = (F * H).sum(axis=1)                     # sum_{k<=i} F_ik H_ik
         dR = F * (H - Drow[:, None])                   # softmax Jacobian (zero where F = 0)
         below = np.arange(T)[None, :] < rr[:, None]
@@ -198,7 +224,7 @@ def _backward_softmax(q, k, v, lam, dout, tau_s, scale, row_block, rows):
         dU[diag] = dR[diag] * Sb * (1.0 - Sb) / tau_s  # Self entry: dS/dU_ii = S(1-S)/tau_S
         dq[b0:b1] = s * (dU @ k)                       # grad P1 = grad_U P2 / sqrt(d_h)
         dk += s * (dU.T @ q[rr])                       # grad P2 = grad_U^T P1 / sqrt(d_h)
-        dv += F.T @ Gb                                 # dL/dI~_j = sum_i F_ij G_i
+        dv += Ft.T @ Gb                                # dL/dI~_j = sum_i F_ij G_i (transported entries)
         dS[b0:b1] = dR[diag]
         ione = (rr + 1).astype(np.float64)
         dlam += float(-(np.log(ione) * np.where(below, dR, 0.0).sum(axis=1)).sum())

@@ -24,6 +24,7 @@ namespace {
 
 constexpr int kDT = 256;      // threads of the states kernel
 constexpr int kSlice = 256;   // keys per workgroup in relation_decode
+constexpr int kUnroll = 2;    // keys per lane group whose loads are in flight together
 
 template <typename TI, int VEC>
 struct Row;
@@ -101,13 +102,13 @@ __global__ __launch_bounds__(kDT) void decode_states_kernel(DecodeArgs a) {
   float m = kNegInf, l = 0.0f, z[VEC];
 #pragma unroll
   for (int e = 0; e < VEC; ++e) z[e] = 0.0f;
-  // two keys per lane group in flight: j = s0 + (2 it NW + 2 w + u) KPW + kg.
+  // kUnroll keys per lane group in flight: j = s0 + (kUnroll (it NW + w) + u) KPW + kg.
   // The loop runs on a wave-uniform base, so every lane reaches the shuffles.
-  for (int base = s0 + 2 * w * KPW; base < s1; base += 2 * NW * KPW) {
-    float kx[2][VEC], vx[2][VEC];
-    bool ok[2];
+  for (int base = s0 + kUnroll * w * KPW; base < s1; base += kUnroll * NW * KPW) {
+    float kx[kUnroll][VEC], vx[kUnroll][VEC];
+    bool ok[kUnroll];
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < kUnroll; ++u) {
       const int j = base + u * KPW + kg;
       ok[u] = j < s1;
 #pragma unroll
@@ -118,7 +119,7 @@ __global__ __launch_bounds__(kDT) void decode_states_kernel(DecodeArgs a) {
       }
     }
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < kUnroll; ++u) {
       float d = 0.0f;
 #pragma unroll
       for (int e = 0; e < VEC; ++e) d = __builtin_fmaf(q[e], kx[u][e], d);
@@ -177,35 +178,72 @@ __global__ __launch_bounds__(kDT) void decode_states_kernel(DecodeArgs a) {
   }
 }
 
-// One wave per (b, h) row: merge the row's a.nstates states, then Self and the
-// count correction (eqs. 12-13) at i = the row's cache length.
+// One workgroup per (b, h) row: merge the row's a.nstates states, then Self
+// and the count correction (eqs. 12-13) at i = the row's cache length. Lanes
+// run over states and wave w over channels 32 w .. 32 w + 31, so the loads of
+// all states are in flight at once; the lane sums then meet by shuffles.
 template <typename TI>
 __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
-  const int64_t n = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (n >= (int64_t)a.B * a.H) return;  // whole wave
-  const int b = (int)(n / a.H), h = (int)(n % a.H);
+  __shared__ float zsh[128];
+  __shared__ float lsh;
+  const int n = blockIdx.x;  // b * H + h
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int b = n / a.H, h = n % a.H;
   const int len = clamp_len(a.lengths, b, a.Tmax);
-  const int64_t NS = (int64_t)a.B * a.H;
+  const int64_t stride_s = (int64_t)a.B * a.H * (a.D + 2);
+  const float* st0 = a.states + (int64_t)n * (a.D + 2);
+  // the Self entry's reads first (the first wave), so that they overlap the states' reads
   const int64_t selfrow = (int64_t)b * a.sb + (int64_t)h * a.sh + (int64_t)(len - 1) * a.st;
-  const TI* q = (const TI*)a.q + n * a.D;
-  // merged Exchange state; lanes hold channels lane and lane + 64
-  float m = kNegInf;
-  for (int s = 0; s < a.nstates; ++s) m = fmaxf(m, a.states[(s * NS + n) * (a.D + 2)]);
-  float l = 0.0f, z0 = 0.0f, z1 = 0.0f;
-  for (int s = 0; s < a.nstates; ++s) {
-    const float* st = a.states + (s * NS + n) * (a.D + 2);
-    const float ms = st[0];
-    if (ms == kNegInf) continue;
-    const float f = fast_exp2((ms - m) * kLog2e);
-    l += st[1] * f;
-    if (lane < a.D) z0 += st[2 + lane] * f;
-    if (lane + 64 < a.D) z1 += st[2 + lane + 64] * f;
+  const TI* q = (const TI*)a.q + (int64_t)n * a.D;
+  float d = 0.0f, vi0 = 0.0f, vi1 = 0.0f;
+  if (w == 0) {
+    if (lane < a.D) {
+      d = Elem<TI>::load(q + lane) * Elem<TI>::load((const TI*)a.k + selfrow + lane);
+      vi0 = Elem<TI>::load((const TI*)a.v + selfrow + lane);
+    }
+    if (lane + 64 < a.D) {
+      d += Elem<TI>::load(q + lane + 64) * Elem<TI>::load((const TI*)a.k + selfrow + lane + 64);
+      vi1 = Elem<TI>::load((const TI*)a.v + selfrow + lane + 64);
+    }
   }
+  float m = kNegInf;
+  for (int s = lane; s < a.nstates; s += 64) m = fmaxf(m, st0[s * stride_s]);
+  for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+  const int cb = 32 * w;
+  if (cb < a.D) {  // wave-uniform
+    float acc[32];
+#pragma unroll
+    for (int e = 0; e < 32; ++e) acc[e] = 0.0f;
+    float l = 0.0f;
+    for (int s = lane; s < a.nstates; s += 64) {
+      const float* st = st0 + s * stride_s;
+      const float ms = st[0];
+      const float f = ms == kNegInf ? 0.0f : fast_exp2((ms - m) * kLog2e);
+      l = __builtin_fmaf(st[1], f, l);
+      const float2* zp = reinterpret_cast<const float2*>(st + 2 + cb);  // 8-byte aligned: D + 2 and cb even
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const float2 zz = zp[e];
+        acc[2 * e] = __builtin_fmaf(zz.x, f, acc[2 * e]);
+        acc[2 * e + 1] = __builtin_fmaf(zz.y, f, acc[2 * e + 1]);
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 32; ++e)
+      for (int o = 32; o >= 1; o >>= 1) acc[e] += __shfl_xor(acc[e], o, 64);
+    for (int o = 32; o >= 1; o >>= 1) l += __shfl_xor(l, o, 64);
+    if (lane == 0) {
+#pragma unroll
+      for (int e = 0; e < 32; ++e) zsh[cb + e] = acc[e];
+      if (w == 0) lsh = l;
+    }
+  }
+  __syncthreads();
+  if (w != 0) return;  // the first wave finishes the row
+  const float l = lsh;
+  const float z0 = lane < a.D ? zsh[lane] : 0.0f;
+  const float z1 = lane + 64 < a.D ? zsh[lane + 64] : 0.0f;
   // Self: U_ii = scale q . k_i, S = sigmoid(U_ii / tau_S)
-  float d = 0.0f;
-  if (lane < a.D) d = Elem<TI>::load(q + lane) * Elem<TI>::load((const TI*)a.k + selfrow + lane);
-  if (lane + 64 < a.D) d += Elem<TI>::load(q + lane + 64) * Elem<TI>::load((const TI*)a.k + selfrow + lane + 64);
   for (int o = 32; o >= 1; o >>= 1) d += __shfl_xor(d, o, 64);
   const float S = 1.0f / (1.0f + expf(-d * a.scale * a.inv_tau));
   const float ln_i = logf((float)len);
@@ -220,15 +258,9 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
     zr1 = z1 * il;
     lnZ = fmaxf(S, A) + log1pf(expf(-fabsf(S - A)));
   }
-  TI* o = (TI*)a.out + n * a.D;
-  if (lane < a.D) {
-    const float vi = Elem<TI>::load((const TI*)a.v + selfrow + lane);
-    Elem<TI>::store(o + lane, omg * vi + g * zr0);
-  }
-  if (lane + 64 < a.D) {
-    const float vi = Elem<TI>::load((const TI*)a.v + selfrow + lane + 64);
-    Elem<TI>::store(o + lane + 64, omg * vi + g * zr1);
-  }
+  TI* o = (TI*)a.out + (int64_t)n * a.D;
+  if (lane < a.D) Elem<TI>::store(o + lane, omg * vi0 + g * zr0);
+  if (lane + 64 < a.D) Elem<TI>::store(o + lane + 64, omg * vi1 + g * zr1);
   if (lane == 0 && a.row_stat) a.row_stat[n] = lnZ + lam * ln_i;
 }
 
@@ -256,7 +288,7 @@ hipError_t launch_decode_states(const DecodeArgs& a, int dtype, hipStream_t stre
 }
 
 hipError_t launch_decode_merge(const DecodeArgs& a, int dtype, hipStream_t stream) {
-  const dim3 grid((unsigned)((a.B * a.H + 3) / 4));
+  const dim3 grid((unsigned)(a.B * a.H));
   if (dtype == 1)
     hipLaunchKernelGGL(decode_merge_kernel<bf16>, grid, dim3(256), 0, stream, a);
   else

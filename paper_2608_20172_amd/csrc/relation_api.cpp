@@ -977,7 +977,7 @@ static rel_status check_decode_io(const rel_problem* p, const void* q, const voi
   REL_TRY(check_aligned(lengths, 4, "lengths", true));
   REL_TRY(check_aligned(out, 16, "out", !states_out));
   REL_TRY(check_aligned(row_stat, 4, "row_stat", false));
-  REL_TRY(check_aligned(states, 4, "states", states_bytes > 0));
+  REL_TRY(check_aligned(states, 8, "states", states_bytes > 0));
   const size_t es = elem_size(p->dtype);
   const size_t cb = (size_t)extent_elems(p) * es, rowb = (size_t)(p->B * p->H * p->D) * es;
   const size_t nb = (size_t)(p->B * p->H) * 4;

@@ -296,8 +296,46 @@ def check_row_blocking(orc):
     assert np.allclose(rc["dS"], ra["dS"][j0:], atol=1e-13), "row subset dS"
 
 
+# ---------------------------------------------------------------------------
+# 7. Exchange-only transport (App. C, ablation definitions): the same flow F,
+#    Y_i = sum_{j<i} F_ij I~_j, historical weights not renormalised
+# ---------------------------------------------------------------------------
+def check_exchange_only(orc):
+    for seed, (T, D, lam) in enumerate([(6, 3, 0.5), (8, 2, -0.9)]):
+        q, k, v, dO = _rand(T, D, 300 + seed, std=1.4)
+        # brute force: F from the pure-Python definition, the historical part transported
+        _, Fb = brute_force_forward(q.tolist(), k.tolist(), v.tolist(), lam)
+        Yb = [[sum(Fb[i][j] * v[j][d] for j in range(i)) for d in range(D)] for i in range(T)]
+        f = orc.forward(q, k, v, lam, transport="exchange")
+        assert np.allclose(f["Y"], np.array(Yb), rtol=0, atol=1e-13), "exchange-only Y vs brute force"
+        assert not f["Y"][0].any(), "row 1 transports nothing"
+        # the flow itself is the full operator's
+        g = orc.forward(q, k, v, lam)
+        assert np.allclose(f["F"], g["F"], atol=0) and np.allclose(f["exch_mass"], g["exch_mass"], atol=0)
+        # central differences of sum(dO * Y) for every input entry and lambda
+        r = orc.backward(q, k, v, lam, dO, transport="exchange")
+        loss = lambda q_, k_, v_, l_: float(np.sum(dO * orc.forward(q_, k_, v_, l_, want_matrices=False,
+                                                                     transport="exchange")["Y"]))
+        h = 1e-6
+        for name, X in (("dq", q), ("dk", k), ("dv", v)):
+            num = np.empty_like(X)
+            for idx in np.ndindex(X.shape):
+                old = X[idx]
+                X[idx] = old + h
+                lp = loss(q, k, v, lam)
+                X[idx] = old - h
+                lm = loss(q, k, v, lam)
+                X[idx] = old
+                num[idx] = (lp - lm) / (2 * h)
+            assert np.allclose(r[name], num, atol=2e-8), f"exchange-only {name} vs FD"
+        num_l = (loss(q, k, v, lam + h) - loss(q, k, v, lam - h)) / (2 * h)
+        assert abs(r["dlam"] - num_l) < 2e-8, "exchange-only dlam vs FD"
+        # the columns of dV add up to the rows of dO weighted by the Exchange mass g_i
+        assert np.allclose(r["dv"].sum(0), (g["exch_mass"][:, None] * dO).sum(0), atol=1e-12)
+
+
 ALL_CHECKS = [
     check_brute_force, check_invariants, check_flash_scan, check_closed_forms,
     check_lambda_limits, check_gradients_fd, check_routes_agree,
-    check_gradient_special_cases, check_row_blocking,
+    check_gradient_special_cases, check_row_blocking, check_exchange_only,
 ]

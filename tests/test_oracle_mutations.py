@@ -23,7 +23,11 @@ MUTATIONS = [
      "ione = (rows + 2).astype(np.float64)            # one-based"),
     ("U_transposed_operands", "U = s * (q[rows] @ k.T)", "U = s * (k[rows] @ q.T)"),
     ("missing_scale", "U = s * (q[rows] @ k.T)", "U = (q[rows] @ k.T)"),
-    ("transport_uses_keys", "Y[b0:b1] = F @ v ", "Y[b0:b1] = F @ k "),
+    ("transport_uses_keys", "Y[b0:b1] = Ft @ v ", "Y[b0:b1] = Ft @ k "),
+    ("exchange_only_keeps_self", "            Ft[np.arange(b1 - b0), rr] = 0.0\n",
+     "            Ft[np.arange(b1 - b0), rr] = Ft[np.arange(b1 - b0), rr]\n"),
+    ("exchange_only_grad_keeps_self_flow", "            H[np.arange(nb), rr] = 0.0\n", "            pass\n"),
+    ("exchange_only_dv_keeps_self", "            Ft[np.arange(nb), rr] = 0.0\n", "            pass\n"),
     ("exchange_mass_includes_self", "        below = np.arange(T)[None, :] < rr[:, None]\n        g[b0:b1]",
      "        below = np.arange(T)[None, :] <= rr[:, None]\n        g[b0:b1]"),
     ("self_grad_drops_tau", "dU[diag] = dR[diag] * Sb * (1.0 - Sb) / tau_s",
