@@ -175,7 +175,11 @@ rel_status relation_bwd_materialized(const rel_problem* p, const void* q, const 
  * 1/sqrt(d_h) of the true width. Strides need only be multiples of the
  * element size here.
  *   opts        rope_base > 0 turns RoPE on (the paper uses 1e4), 0 off;
- *               givens = REL_GIVENS_NONE / _A / _B (H even for A and B).
+ *               givens = REL_GIVENS_NONE / _A / _B (H even for A and B);
+ *               transport = REL_TRANSPORT_FULL, or _EXCHANGE for the
+ *               exchange-only ablation (forward and backward). The other
+ *               structural ablations need no flag: lambda = 0 is "no count
+ *               calibration", givens = NONE is "no Givens mixing".
  *   theta       device fp32 [H/2] angles (read when givens != NONE).
  *   out         [B,H,T,D] dtype: y.   row_stat  [B,H,T] fp32: M_i for the
  *               backward pass (as relation_fwd).
@@ -210,10 +214,16 @@ typedef enum rel_givens {
   REL_GIVENS_B = 2
 } rel_givens;
 
+typedef enum rel_transport {
+  REL_TRANSPORT_FULL = 0,     /* y_i = sum_{j <= i} F_ij v~_j (eq. 3) */
+  REL_TRANSPORT_EXCHANGE = 1  /* exchange-only ablation (App. C): y_i = sum_{j < i} F_ij v~_j,
+                                 the same F, historical weights not renormalised */
+} rel_transport;
+
 typedef struct rel_layer_opts {
-  double rope_base;  /* > 0: RoPE with this base; 0: no RoPE */
-  int32_t givens;    /* rel_givens */
-  int32_t reserved;  /* must be 0 */
+  double rope_base;   /* > 0: RoPE with this base; 0: no RoPE */
+  int32_t givens;     /* rel_givens */
+  int32_t transport;  /* rel_transport */
 } rel_layer_opts;
 
 size_t relation_layer_saved_bytes(const rel_problem* p, const rel_layer_opts* opts);

@@ -35,10 +35,11 @@ class RelProblem(ctypes.Structure):
 
 
 class RelLayerOpts(ctypes.Structure):
-    _fields_ = [("rope_base", ctypes.c_double), ("givens", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+    _fields_ = [("rope_base", ctypes.c_double), ("givens", ctypes.c_int32), ("transport", ctypes.c_int32)]
 
 
 REL_GIVENS = {None: 0, "A": 1, "B": 2}
+REL_TRANSPORT = {"full": 0, "exchange": 1}
 ROPE_BASE = 1.0e4
 
 _P = ctypes.c_void_p
@@ -284,10 +285,13 @@ def relation_bwd_materialized(q, k, v, dout, lam, *, tau_s: float = TAU_S, scale
     return {"dq": dq, "dk": dk, "dv": dv, "dlambda": dlam}
 
 
-def make_layer_opts(pairing: Optional[str] = None, rope_base: float = ROPE_BASE) -> RelLayerOpts:
+def make_layer_opts(pairing: Optional[str] = None, rope_base: float = ROPE_BASE,
+                    transport: str = "full") -> RelLayerOpts:
     if pairing not in REL_GIVENS:
         raise ValueError("pairing must be None, 'A' or 'B'")
-    return RelLayerOpts(float(rope_base or 0.0), REL_GIVENS[pairing], 0)
+    if transport not in REL_TRANSPORT:
+        raise ValueError("transport must be 'full' or 'exchange'")
+    return RelLayerOpts(float(rope_base or 0.0), REL_GIVENS[pairing], REL_TRANSPORT[transport])
 
 
 def _theta_tensor(theta, H: int, device):
@@ -332,8 +336,8 @@ def _nbytes(t) -> int:
 
 
 def relation_layer_fwd(q, k, v, lam, theta=None, *, pairing: Optional[str] = None,
-                       rope_base: float = ROPE_BASE, tau_s: float = TAU_S, scale: Optional[float] = None,
-                       keep_saved: bool = True, workspace=None):
+                       rope_base: float = ROPE_BASE, transport: str = "full", tau_s: float = TAU_S,
+                       scale: Optional[float] = None, keep_saved: bool = True, workspace=None):
     """Layer forward: RoPE on q, k (rope_base 0: off), Givens mixing of v over
     head pairs ("A", "B" or None) with angles ``theta`` [H/2], then the fused
     operator. Any head width up to 128. Returns dict(o, row_stat, saved):
@@ -343,7 +347,7 @@ def relation_layer_fwd(q, k, v, lam, theta=None, *, pairing: Optional[str] = Non
     lib = load_library()
     k, v = _same_layout(q, k, v)
     p = make_problem(q, tau_s, scale)
-    opts = make_layer_opts(pairing, rope_base)
+    opts = make_layer_opts(pairing, rope_base, transport)
     dev = q.device
     lam_t = _lam_tensor(lam, dev)
     th = _theta_tensor(theta, q.shape[1], dev) if pairing else None
@@ -361,14 +365,14 @@ def relation_layer_fwd(q, k, v, lam, theta=None, *, pairing: Optional[str] = Non
 
 
 def relation_layer_bwd(q, k, v, o, dout, lam, row_stat, theta=None, *, saved=None, pairing: Optional[str] = None,
-                       rope_base: float = ROPE_BASE, tau_s: float = TAU_S, scale: Optional[float] = None,
-                       workspace=None):
+                       rope_base: float = ROPE_BASE, transport: str = "full", tau_s: float = TAU_S,
+                       scale: Optional[float] = None, workspace=None):
     """Layer backward; ``saved`` is the forward call's (None: recompute).
     Returns dict(dq, dk, dv, dlambda [1], dtheta [H/2] or None)."""
     lib = load_library()
     k, v, o, dout = _same_layout(q, k, v, o, dout)
     p = make_problem(q, tau_s, scale)
-    opts = make_layer_opts(pairing, rope_base)
+    opts = make_layer_opts(pairing, rope_base, transport)
     dev = q.device
     lam_t = _lam_tensor(lam, dev)
     H = q.shape[1]

@@ -279,6 +279,7 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
       dself = pick(dp, rs);
     }
     if (NDM == 0 && DIAG) dself -= Di;
+    if (DIAG && a.exch_only) dself = -Di;  // exchange-only: dL/dF_ii = 0, so dR_ii = -F_ii D_i
     exchange_grads(s, dp, [&](int) { return Mi2; }, c, dsub);
     if (DIAG) {
 #pragma unroll
@@ -562,6 +563,8 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
     if (DIAG) {
       uself = pick(s, rs);
       dself = pick(dp, rs);
+      // exchange-only: dL/dF_ii = 0, so dR_ii = -F_ii D_i with -D_i of the query row equal to the key
+      if (a.exch_only) dself = ((const float*)(buf + 2 * TB) + kBQI)[32 * qb + n];
     }
     exchange_grads(s, dp, [&](int r) { return Mb[r]; }, c);
     if (DIAG) {
@@ -574,9 +577,10 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
       }
       if (holds_row(n, g)) {
         const SelfGrad sg = self_grad(uself, dself, Mb[rs], a.scale, a.inv_tau, lam, logf((float)(kj + 1)), kj == 0);
+        const float fself = a.exch_only ? 0.0f : sg.F;  // F_ii carries dO_i to v_i unless exchange-only
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          s[r] = r == rs ? sg.F : s[r];
+          s[r] = r == rs ? fself : s[r];
           dp[r] = r == rs ? sg.dU : dp[r];
         }
       }

@@ -329,6 +329,7 @@ __device__ __forceinline__ void finish_row(const FwdArgs& a, typename P::T* o, c
   const float lam = *a.lambda;
   const float ln_i = logf((float)(qi + 1));
   const RowEpilogue e = row_epilogue(m, lt, un, a.inv_tau, lam, ln_i);
+  const float wself = a.exch_only ? 0.0f : e.omg;  // the exchange-only ablation drops the Self term
 #pragma unroll
   for (int db = 0; db < DB; ++db) {
 #pragma unroll
@@ -337,7 +338,7 @@ __device__ __forceinline__ void finish_row(const FwdArgs& a, typename P::T* o, c
       const floatx4 vi = P::load4(v + qi * st + d0);
       floatx4 out;
 #pragma unroll
-      for (int t = 0; t < 4; ++t) out[t] = __builtin_fmaf(e.omg, vi[t], e.inv_l * oacc[db][4 * rq + t]);
+      for (int t = 0; t < 4; ++t) out[t] = __builtin_fmaf(wself, vi[t], e.inv_l * oacc[db][4 * rq + t]);
       P::store4(o + qi * st + d0, out);
     }
   }

@@ -23,6 +23,7 @@ struct FwdArgs {
   int H, T;
   float scale;    // multiplier inside U
   float inv_tau;  // 1 / tau_S
+  int exch_only;  // 1: exchange-only transport, y_i = sum_{j<i} F_ij v_j
   TileMap map;
 };
 
@@ -48,6 +49,7 @@ struct BwdArgs {
   int H, T;
   float scale;
   float inv_tau;
+  int exch_only;     // 1: gradients of the exchange-only output
   TileMap map;
 };
 

@@ -181,7 +181,8 @@ rel_status check_layer_problem(const rel_problem* p, const rel_layer_opts* o, bo
     return fail(REL_ERR_INVALID_ARG, "rope_base must exceed 1");
   if (o->givens < REL_GIVENS_NONE || o->givens > REL_GIVENS_B)
     return fail(REL_ERR_INVALID_ARG, "unknown Givens pairing %d", (int)o->givens);
-  if (o->reserved != 0) return fail(REL_ERR_INVALID_ARG, "reserved layer option must be 0");
+  if (o->transport != REL_TRANSPORT_FULL && o->transport != REL_TRANSPORT_EXCHANGE)
+    return fail(REL_ERR_INVALID_ARG, "unknown transport %d", (int)o->transport);
   if (p->D < 1 || p->D > 128)
     return fail(REL_ERR_UNSUPPORTED, "head width %lld not in 1..128", (long long)p->D);
   if (o->rope_base > 0.0 && p->D % 2)
@@ -380,9 +381,9 @@ int relation_profile_disarm(void) {
   return n;
 }
 
-rel_status relation_fwd(const rel_problem* p, const void* q, const void* k, const void* v,
-                        const float* lambda, void* o, float* row_stat, float* self_mass,
-                        float* exch_mass, float* exch_lse, void* stream) {
+static rel_status fwd_impl(const rel_problem* p, const void* q, const void* k, const void* v,
+                           const float* lambda, void* o, float* row_stat, float* self_mass,
+                           float* exch_mass, float* exch_lse, void* stream, int exch_only) {
   bool empty = false;
   REL_TRY(check_problem(p, &empty));
   if (empty) return REL_OK;
@@ -413,11 +414,18 @@ rel_status relation_fwd(const rel_problem* p, const void* q, const void* k, cons
   a.sb = p->stride_b; a.sh = p->stride_h; a.st = p->stride_t;
   a.H = (int)p->H; a.T = (int)p->T;
   a.scale = eff_scale(p);
+  a.exch_only = exch_only;
   a.inv_tau = 1.0f / p->tau_s;
   a.map = rel::make_tilemap((int)(p->B * p->H), 1);
   hipError_t e = rel::launch_fwd(a, p->dtype, (int)p->D, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "relation_fwd launch");
   return REL_OK;
+}
+
+rel_status relation_fwd(const rel_problem* p, const void* q, const void* k, const void* v,
+                        const float* lambda, void* o, float* row_stat, float* self_mass,
+                        float* exch_mass, float* exch_lse, void* stream) {
+  return fwd_impl(p, q, k, v, lambda, o, row_stat, self_mass, exch_mass, exch_lse, stream, 0);
 }
 
 rel_status relation_exchange_allocation(const rel_problem* p, const void* q, const void* k,
@@ -458,10 +466,11 @@ size_t relation_bwd_workspace_bytes(const rel_problem* p) {
          align256((size_t)rel::bwd_partials((int)N, (int)p->T, (int)p->D, p->dtype) * 4);
 }
 
-rel_status relation_bwd(const rel_problem* p, const void* q, const void* k, const void* v,
-                        const void* o, const void* dout, const float* lambda,
-                        const float* row_stat, void* dq, void* dk, void* dv, float* dlambda,
-                        float* dself, void* workspace, size_t workspace_bytes, void* stream) {
+static rel_status bwd_impl(const rel_problem* p, const void* q, const void* k, const void* v,
+                           const void* o, const void* dout, const float* lambda,
+                           const float* row_stat, void* dq, void* dk, void* dv, float* dlambda,
+                           float* dself, void* workspace, size_t workspace_bytes, void* stream,
+                           int exch_only) {
   bool empty = false;
   REL_TRY(check_problem(p, &empty));
   if (empty) {
@@ -517,6 +526,7 @@ rel_status relation_bwd(const rel_problem* p, const void* q, const void* k, cons
   a.sb = p->stride_b; a.sh = p->stride_h; a.st = p->stride_t;
   a.H = (int)p->H; a.T = (int)p->T;
   a.scale = eff_scale(p);
+  a.exch_only = exch_only;
   a.inv_tau = 1.0f / p->tau_s;
   a.map = rel::make_tilemap((int)N, 1);
   a.nparts = rel::bwd_partials((int)N, (int)p->T, (int)p->D, p->dtype);
@@ -524,6 +534,14 @@ rel_status relation_bwd(const rel_problem* p, const void* q, const void* k, cons
   hipError_t e = rel::launch_bwd(a, p->dtype, (int)p->D, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "relation_bwd launch");
   return REL_OK;
+}
+
+rel_status relation_bwd(const rel_problem* p, const void* q, const void* k, const void* v,
+                        const void* o, const void* dout, const float* lambda,
+                        const float* row_stat, void* dq, void* dk, void* dv, float* dlambda,
+                        float* dself, void* workspace, size_t workspace_bytes, void* stream) {
+  return bwd_impl(p, q, k, v, o, dout, lambda, row_stat, dq, dk, dv, dlambda, dself, workspace,
+                  workspace_bytes, stream, 0);
 }
 
 size_t relation_fwd_materialized_workspace_bytes(const rel_problem* p) {
@@ -808,7 +826,8 @@ rel_status relation_layer_fwd(const rel_problem* p, const rel_layer_opts* opts, 
   REL_TRY(check_aligned(row_stat, 4, "row_stat", false));
   REL_TRY(check_aligned(saved, 16, "saved", false));
   const LayerPlan L = plan_layer(p, opts);
-  if (L.pass) return relation_fwd(&L.pp, q, k, v, lambda, out, row_stat, nullptr, nullptr, nullptr, stream);
+  if (L.pass)
+    return fwd_impl(&L.pp, q, k, v, lambda, out, row_stat, nullptr, nullptr, nullptr, stream, opts->transport);
   if (saved && saved_bytes < L.prep)
     return fail(REL_ERR_WORKSPACE, "saved buffer of %zu bytes needed, %zu given", L.prep, saved_bytes);
   char* prep = (char*)saved;
@@ -839,7 +858,8 @@ rel_status relation_layer_fwd(const rel_problem* p, const rel_layer_opts* opts, 
   // the output goes straight to the caller when its layout is the padded one
   const bool y_direct = L.contiguous_tiled && al16({out});
   void* y = y_direct ? out : prep + L.yp;
-  REL_TRY(relation_fwd(&L.pp, a.qr, a.kr, a.vt, lambda, y, row_stat, nullptr, nullptr, nullptr, stream));
+  REL_TRY(fwd_impl(&L.pp, a.qr, a.kr, a.vt, lambda, y, row_stat, nullptr, nullptr, nullptr, stream,
+                   opts->transport));
   if (!y_direct && (he = rel::launch_layer_repad(y, out, a, false, p->dtype, vec, s)))
     return hip_fail(he, "layer output copy launch");
   return REL_OK;
@@ -889,8 +909,8 @@ rel_status relation_layer_bwd(const rel_problem* p, const rel_layer_opts* opts, 
   REL_TRY(check_aligned(workspace, 16, "workspace", true));
   char* ws = (char*)workspace;
   if (L.pass)
-    return relation_bwd(&L.pp, q, k, v, out, dout, lambda, row_stat, dq, dk, dv, dlambda, nullptr, ws + L.bws,
-                        relation_bwd_workspace_bytes(&L.pp), stream);
+    return bwd_impl(&L.pp, q, k, v, out, dout, lambda, row_stat, dq, dk, dv, dlambda, nullptr, ws + L.bws,
+                    relation_bwd_workspace_bytes(&L.pp), stream, opts->transport);
   char* prep = saved ? (char*)saved : ws;
   char* scr = saved ? ws : ws + L.prep;
   const size_t tb = (size_t)extent_elems(p) * es, rb = (size_t)(p->B * p->H * p->T) * 4;
@@ -931,9 +951,9 @@ rel_status relation_layer_bwd(const rel_problem* p, const rel_layer_opts* opts, 
   a.gv = scr + L.gv;
   a.dq = dq; a.dk = dk; a.dv = dv;
   a.dth_rows = giv ? (float*)(scr + L.dth) : nullptr;
-  REL_TRY(relation_bwd(&L.pp, a.qr, a.kr, a.vt, y_direct ? out : prep + L.yp, do_direct ? dout : scr + L.dop,
-                       lambda, row_stat, (void*)a.gq, (void*)a.gk, (void*)a.gv, dlambda, nullptr, scr + L.bws,
-                       relation_bwd_workspace_bytes(&L.pp), stream));
+  REL_TRY(bwd_impl(&L.pp, a.qr, a.kr, a.vt, y_direct ? out : prep + L.yp, do_direct ? dout : scr + L.dop,
+                   lambda, row_stat, (void*)a.gq, (void*)a.gk, (void*)a.gv, dlambda, nullptr, scr + L.bws,
+                   relation_bwd_workspace_bytes(&L.pp), stream, opts->transport));
   if ((he = rel::launch_layer_epilogue(a, p->dtype, vec, s))) return hip_fail(he, "layer epilogue launch");
   if (giv && (he = rel::launch_segment_sum(a.dth_rows, (int)(p->H / 2), p->B * p->T, (float*)(scr + L.dpart),
                                            dtheta, s)))

@@ -180,8 +180,8 @@ def test_injected_launch_failure_raises(lib, monkeypatch):
 # ---------------------------------------------------------------------------
 # layer entry points (RoPE, Givens mixing, padded head widths)
 # ---------------------------------------------------------------------------
-def lopts(rope=1.0e4, givens=1, reserved=0):
-    return R.RelLayerOpts(rope, givens, reserved)
+def lopts(rope=1.0e4, givens=1, transport=0):
+    return R.RelLayerOpts(rope, givens, transport)
 
 
 def layer_fwd(lib, p, o, theta=True, ws_bytes=None, saved=None, saved_bytes=0):
@@ -222,7 +222,8 @@ def test_layer_workspace_sizes(lib):
     (dict(H=3), {}, R.REL_ERR_INVALID_ARG),            # Givens needs paired heads
     (dict(H=3), dict(givens=0), R.REL_ERR_HIP),
     ({}, dict(givens=3), R.REL_ERR_INVALID_ARG),
-    ({}, dict(reserved=1), R.REL_ERR_INVALID_ARG),
+    ({}, dict(transport=2), R.REL_ERR_INVALID_ARG),
+    ({}, dict(transport=1), R.REL_ERR_HIP),           # exchange-only ablation
     ({}, dict(rope=0.5), R.REL_ERR_INVALID_ARG),
     ({}, dict(rope=float("nan")), R.REL_ERR_INVALID_ARG),
     (dict(causal=0), {}, R.REL_ERR_UNSUPPORTED),

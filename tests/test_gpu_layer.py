@@ -48,26 +48,26 @@ def _assert_vec(name, x, ref, terms, dtype):
         assert_scalar_close(f"{name}[{p}]", float(a), float(b), t, dtype)
 
 
-def check_layer(x, dtype, pairing, rope_base):
+def check_layer(x, dtype, pairing, rope_base, transport="full"):
     B, H, T, D = x["q"].shape
-    log(f"[layer] B={B} H={H} T={T} D={D} {dtype} pairing={pairing} rope={rope_base}")
+    log(f"[layer] B={B} H={H} T={T} D={D} {dtype} pairing={pairing} rope={rope_base} transport={transport}")
     th = x["theta"] if pairing else None
-    f = R.relation_layer_fwd(x["q"], x["k"], x["v"], x["lam"], th, pairing=pairing, rope_base=rope_base)
+    kw = dict(pairing=pairing, rope_base=rope_base, transport=transport)
+    f = R.relation_layer_fwd(x["q"], x["k"], x["v"], x["lam"], th, **kw)
     g = R.relation_layer_bwd(x["q"], x["k"], x["v"], f["o"], x["dout"], x["lam"], f["row_stat"], th,
-                             saved=f["saved"], pairing=pairing, rope_base=rope_base)
+                             saved=f["saved"], **kw)
     # without the saved operands: the forward prepares them in its workspace and
     # the backward recomputes them, with the same kernels, so bit for bit the same
-    f2 = R.relation_layer_fwd(x["q"], x["k"], x["v"], x["lam"], th, pairing=pairing, rope_base=rope_base,
-                              keep_saved=False)
-    g2 = R.relation_layer_bwd(x["q"], x["k"], x["v"], f2["o"], x["dout"], x["lam"], f2["row_stat"], th,
-                              pairing=pairing, rope_base=rope_base)
+    f2 = R.relation_layer_fwd(x["q"], x["k"], x["v"], x["lam"], th, keep_saved=False, **kw)
+    g2 = R.relation_layer_bwd(x["q"], x["k"], x["v"], f2["o"], x["dout"], x["lam"], f2["row_stat"], th, **kw)
     torch.cuda.synchronize()
     assert torch.equal(f["o"], f2["o"]) and torch.equal(f["row_stat"], f2["row_stat"])
     for n in ("dq", "dk", "dv", "dlambda") + (("dtheta",) if pairing else ()):
         assert torch.equal(g[n], g2[n]), f"{n}: saved and recomputed operands differ"
     thr = x["thr"] if pairing else None
-    of = LO.layer_forward(x["qr"], x["kr"], x["vr"], x["lam"], thr, pairing, rope_base)
-    ob = LO.layer_backward(x["qr"], x["kr"], x["vr"], x["lam"], x["doutr"], thr, pairing, rope_base)
+    of = LO.layer_forward(x["qr"], x["kr"], x["vr"], x["lam"], thr, pairing, rope_base, transport=transport)
+    ob = LO.layer_backward(x["qr"], x["kr"], x["vr"], x["lam"], x["doutr"], thr, pairing, rope_base,
+                           transport=transport)
     for name, gpu, ref in (("o", f["o"], of["Y"]), ("dq", g["dq"], ob["dq"]), ("dk", g["dk"], ob["dk"]),
                            ("dv", g["dv"], ob["dv"])):
         assert_close(name, _np(gpu), ref, dtype)
@@ -104,6 +104,29 @@ def test_layer_bf16(D, pairing, rope):
 def test_layer_fp32(D, pairing, rope):
     x = _prep(1, 4, 190, D, "f32", seed=400 + D, std=1.0)
     check_layer(x, "f32", pairing, rope)
+
+
+@pytest.mark.parametrize("D,pairing,rope,dtype,T", [
+    (64, None, 0.0, "bf16", 300), (80, "A", 1.0e4, "bf16", 300), (64, "B", 1.0e4, "f32", 190),
+    (60, None, 0.0, "bf16", 1), (64, None, 0.0, "bf16", 2), (128, None, 0.0, "bf16", 129),
+])
+def test_layer_exchange_only(D, pairing, rope, dtype, T):
+    """The exchange-only ablation (App. C): y_i = sum_{j<i} F_ij v~_j, forward and backward."""
+    std = 1.0 if dtype == "f32" else None
+    x = _prep(1 if dtype == "f32" else 2, 4, T, D, dtype, seed=900 + D + T, std=std)
+    f, g = check_layer(x, dtype, pairing, rope, transport="exchange")
+    assert not _np(f["o"])[:, :, 0].any()  # row 1 transports nothing
+
+
+def test_exchange_only_sharp():
+    """Sharp evidence (the running maximum moves), operator-level layer call."""
+    inp = I.make_sharp_inputs(1, 2, 260, 64, seed=950, lam=0.5)
+    x = {}
+    for n in ("q", "k", "v", "dout"):
+        x[n], x[n + "r"] = to_device(inp[n], "f32")
+    x["lam"] = lam_value(inp["lam"])
+    x["theta"], x["thr"] = None, None
+    check_layer(x, "f32", None, 0.0, transport="exchange")
 
 
 @pytest.mark.parametrize("T", [1, 2, 129])
