@@ -262,6 +262,15 @@ def test_materialized_backward_sharp():
     check_materialized_backward(x, "f32")
 
 
+def test_backward_no_count_calibration():
+    """The "no count calibration" ablation is lambda = 0: the same kernels, and
+    dlambda is still the gradient a learnable lambda would get at zero."""
+    x = _prep(I.make_inputs(2, 2, 300, 64, seed=17, qkv_std=0.125, lam=0.0), "bf16")
+    assert x["lam"] == 0.0
+    f = check_forward(x, "bf16", with_aux=False)
+    check_backward(x, "bf16", f)
+
+
 def test_strided_layout_matches_contiguous():
     """[B, T, H, D] storage (head stride D) gives the same results as [B, H, T, D]."""
     inp = I.make_inputs(2, 3, 150, 64, seed=21, qkv_std=0.125, lam=0.5)
