@@ -279,6 +279,30 @@ rel_status relation_decode_merge(const rel_problem* p, int32_t nstates, const fl
                                  const void* k_cache, const void* v_cache, const int32_t* lengths,
                                  const float* lambda, void* out, float* row_stat, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Linear Relation (Sec. 5.2, App. A.4): Self explicit, Exchange read from a
+ * recurrent D x D state per head with channel-wise retention alpha = exp(g):
+ *   S_t = sigmoid(scale p1_t . p2_t / tau_s), ^p = p / |p|,
+ *   C_t^- = Diag(alpha_t) C_{t-1} (C_0 = 0),  y_t = v_t + S_t (C_t^-)^T ^p1_t,
+ *   C_t = C_t^- + S_t ^p2_t v_t^T.
+ *   p          B, H, T, D (32, 64 or 128), dtype, tau_s, scale, strides of
+ *              p1, p2, v, out, as for relation_fwd.
+ *   p1, p2     [B,H,T,D] dtype: the two relation coordinates after RoPE.
+ *   v          [B,H,T,D] dtype: the information state I~.
+ *   g          [B,H,T,D] fp32, dense: log-retention g_t = log alpha_t <= 0 (the
+ *              gate of eq. 9 is the caller's elementwise map; positive values
+ *              are not checked and grow the state).
+ *   out        [B,H,T,D] dtype: y.
+ *   state_out  [B,H,D,D] fp32, optional: C_T, the decode state after the last
+ *              token (rows: relation channel, columns: information channel).
+ *   workspace  relation_linear_fwd_workspace_bytes(p) bytes, 16-byte aligned:
+ *              per chunk of 64 tokens its state contribution and retention
+ *              product, and the state entering it (fp32). */
+size_t relation_linear_fwd_workspace_bytes(const rel_problem* p);
+rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
+                               const float* g, void* out, float* state_out, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
 /* Measurement aid. While armed, every launch of the named kernel ("fwd": the
  * fused forward kernel; "bwd_dkdv", "bwd_dq": the two backward kernels; "bwd":
  * both backward kernels, back to back) is bracketed by

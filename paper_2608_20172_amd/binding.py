@@ -69,6 +69,8 @@ _SIGS = {
     "relation_decode_states": (ctypes.c_int, [_PP, _P, _P, _P, _P, ctypes.c_int32, ctypes.c_int32,
                                               ctypes.c_int32, _P, _P]),
     "relation_decode_merge": (ctypes.c_int, [_PP, ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "relation_linear_fwd_workspace_bytes": (ctypes.c_size_t, [_PP]),
+    "relation_linear_fwd": (ctypes.c_int, [_PP, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "relation_profile_arm": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]),
     "relation_profile_disarm": (ctypes.c_int, []),
     "relation_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -447,6 +449,28 @@ def relation_decode_merge(states, q, k_cache, v_cache, lengths, lam, *, tau_s: f
                                    _ptr(v_cache), _ptr(lengths), _ptr(lam_t), _ptr(o), _ptr(rs), _stream())
     _check(st, "relation_decode_merge")
     return {"o": o, "row_stat": rs}
+
+
+def relation_linear_fwd(p1, p2, v, g, *, tau_s: float = TAU_S, scale: Optional[float] = None,
+                        want_state: bool = False, workspace=None):
+    """Linear Relation forward over [B, H, T, D] tensors; g is the fp32
+    log-retention. Returns dict(o, state (the [B, H, D, D] state after the last
+    token, or None))."""
+    lib = load_library()
+    p2, v = _same_layout(p1, p2, v)
+    p = make_problem(p1, tau_s, scale)
+    dev = p1.device
+    g = g.to(device=dev, dtype=torch.float32).contiguous()
+    if g.shape != p1.shape:
+        raise ValueError("g must have the shape of p1")
+    o = _layout_like(p1)
+    B, H, T, D = p1.shape
+    state = torch.empty((B, H, D, D), dtype=torch.float32, device=dev) if want_state else None
+    ws = _workspace(max(1, int(lib.relation_linear_fwd_workspace_bytes(ctypes.byref(p)))), workspace, dev)
+    st = lib.relation_linear_fwd(ctypes.byref(p), _ptr(p1), _ptr(p2), _ptr(v), _ptr(g), _ptr(o), _ptr(state),
+                                 _ptr(ws), _nbytes(ws), _stream())
+    _check(st, "relation_linear_fwd")
+    return {"o": o, "state": state}
 
 
 def relation_profile_arm(kernel: str, events: list) -> None:

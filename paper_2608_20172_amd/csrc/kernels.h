@@ -126,6 +126,23 @@ struct DecodeArgs {
   float* row_stat;          // merge kernel: [B, H] or null
 };
 
+// Arguments of the Linear Relation kernels (chunks of linear_chunk() tokens).
+struct LinearArgs {
+  const void* p1;        // [B, H, T, D] dtype with (sb, sh, st): relation coordinates after RoPE
+  const void* p2;
+  const void* v;         // information state I~
+  const float* g;        // [B, H, T, D] fp32, dense: log-retention (<= 0)
+  int64_t sb, sh, st;
+  int B, H, T, D;
+  float scale, inv_tau;
+  int nchunks;
+  float* dstate;         // [N, nchunks, D, D]: each chunk's state contribution
+  float* gamma;          // [N, nchunks, D]: each chunk's retention product
+  float* cprev;          // [N, nchunks, D, D]: the state entering each chunk
+  float* state_out;      // [N, D, D] or null: the state after the last token
+  void* out;             // [B, H, T, D] dtype: Y
+};
+
 // Measurement aid: if armed for kernel `name`, returns the event pair to record
 // around the next launch of that kernel (see relation_profile_arm).
 bool profile_slot(const char* name, hipEvent_t* start, hipEvent_t* stop);
@@ -138,6 +155,8 @@ hipError_t launch_allocation(const RowArgs& a, int dtype, int N, hipStream_t str
 // Layer passes. `vec` (8, 2 or 1 for bf16; 4, 2 or 1 for fp32) is the number
 // of contiguous channels one thread moves; the caller's tensors must allow it
 // (D, D/2 with RoPE, and the strides multiples of vec; pointers aligned to it).
+int linear_chunk();
+hipError_t launch_linear_fwd(const LinearArgs& a, int dtype, hipStream_t stream);
 int decode_slice_keys();
 hipError_t launch_decode_states(const DecodeArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_decode_merge(const DecodeArgs& a, int dtype, hipStream_t stream);

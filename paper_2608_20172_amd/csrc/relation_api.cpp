@@ -1078,4 +1078,83 @@ rel_status relation_decode(const rel_problem* p, const void* q, const void* k_ca
   return REL_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Linear Relation
+// ---------------------------------------------------------------------------
+static rel_status check_linear(const rel_problem* p, bool* empty) {
+  if (!p) return fail(REL_ERR_INVALID_ARG, "problem is null");
+  if (p->D != 32 && p->D != 64 && p->D != 128)
+    return fail(REL_ERR_UNSUPPORTED, "Linear Relation head width %lld not in {32, 64, 128}", (long long)p->D);
+  return check_problem(p, empty);
+}
+
+static int linear_chunks(const rel_problem* p) {
+  return (int)((p->T + rel::linear_chunk() - 1) / rel::linear_chunk());
+}
+
+struct LinearPlan {
+  size_t dstate, gamma, cprev, total;
+};
+
+static LinearPlan plan_linear(const rel_problem* p) {
+  LinearPlan L{};
+  const size_t N = (size_t)(p->B * p->H), nc = (size_t)linear_chunks(p), D = (size_t)p->D;
+  L.dstate = 0;
+  L.gamma = align256(N * nc * D * D * 4);
+  L.cprev = L.gamma + align256(N * nc * D * 4);
+  L.total = L.cprev + align256(N * nc * D * D * 4);
+  return L;
+}
+
+size_t relation_linear_fwd_workspace_bytes(const rel_problem* p) {
+  bool empty = false;
+  if (check_linear(p, &empty) != REL_OK || empty) return 0;
+  return plan_linear(p).total;
+}
+
+rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
+                               const float* g, void* out, float* state_out, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+  bool empty = false;
+  REL_TRY(check_linear(p, &empty));
+  if (empty) return REL_OK;
+  const size_t es = elem_size(p->dtype);
+  REL_TRY(check_aligned(p1, es, "p1", true));
+  REL_TRY(check_aligned(p2, es, "p2", true));
+  REL_TRY(check_aligned(v, es, "v", true));
+  REL_TRY(check_aligned(g, 4, "g", true));
+  REL_TRY(check_aligned(out, es, "out", true));
+  REL_TRY(check_aligned(state_out, 4, "state_out", false));
+  const LinearPlan L = plan_linear(p);
+  if (!workspace || workspace_bytes < L.total)
+    return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
+                workspace ? workspace_bytes : (size_t)0);
+  REL_TRY(check_aligned(workspace, 16, "workspace", true));
+  const size_t tb = (size_t)extent_elems(p) * es;
+  const size_t N = (size_t)(p->B * p->H);
+  const size_t gb = N * (size_t)p->T * (size_t)p->D * 4;
+  REL_TRY(check_buffers(p, {{p1, tb, true, false, "p1"},
+                            {p2, tb, true, false, "p2"},
+                            {v, tb, true, false, "v"},
+                            {g, gb, false, false, "g"},
+                            {out, tb, true, true, "out"},
+                            {state_out, N * (size_t)(p->D * p->D) * 4, false, true, "state_out"},
+                            {workspace, L.total, false, true, "workspace"}}));
+  if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected by RELATION_TEST_FAIL_LAUNCH");
+  rel::LinearArgs a{};
+  a.p1 = p1; a.p2 = p2; a.v = v; a.g = g; a.out = out; a.state_out = state_out;
+  a.sb = p->stride_b; a.sh = p->stride_h; a.st = p->stride_t;
+  a.B = (int)p->B; a.H = (int)p->H; a.T = (int)p->T; a.D = (int)p->D;
+  a.scale = eff_scale(p);
+  a.inv_tau = 1.0f / p->tau_s;
+  a.nchunks = linear_chunks(p);
+  char* ws = (char*)workspace;
+  a.dstate = (float*)(ws + L.dstate);
+  a.gamma = (float*)(ws + L.gamma);
+  a.cprev = (float*)(ws + L.cprev);
+  const hipError_t e = rel::launch_linear_fwd(a, p->dtype, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "Linear Relation launch");
+  return REL_OK;
+}
+
 }  // extern "C"

@@ -110,6 +110,13 @@ def make_givens_angles(H: int, seed: int = 42, spread: float = math.pi) -> np.nd
     return rng.uniform(-spread, spread, H // 2)
 
 
+def make_log_retention(B: int, H: int, T: int, D: int, seed: int = 42, gmax: float = 0.5) -> np.ndarray:
+    """Per-channel log-retention values ~ -U(0, gmax), [B, H, T, D] fp64, from
+    a stream of their own (retention alpha = exp(g) in (exp(-gmax), 1])."""
+    rng = np.random.default_rng(seed + 104729)
+    return -rng.uniform(0.0, gmax, (B, H, T, D))
+
+
 def make_workload_inputs(w: Workload, seed: int = 42, lam: float | None = None) -> dict:
     return make_inputs(w.B, w.H, w.T, w.D, seed=seed, qkv_std=w.qkv_std,
                        with_dout=w.backward, lam_std=w.lam_std, lam=lam,
