@@ -303,6 +303,19 @@ rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void*
                                const float* g, void* out, float* state_out, void* workspace,
                                size_t workspace_bytes, void* stream);
 
+/* Linear Relation backward: gradients of sum(dout * y) with respect to p1,
+ * p2, v (dtype, the problem's strides) and g (fp32, dense [B,H,T,D]). The
+ * chunk states are recomputed from the inputs. D in {32, 64} (a chunk of 64
+ * tokens and its gradients stay in LDS), else REL_ERR_UNSUPPORTED.
+ *   workspace  relation_linear_bwd_workspace_bytes(p) bytes, 16-byte aligned:
+ *              the forward workspace plus, per chunk, the D x D products that
+ *              the reverse scan over chunks reads and the state gradients it
+ *              writes. */
+size_t relation_linear_bwd_workspace_bytes(const rel_problem* p);
+rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
+                               const float* g, const void* dout, void* dp1, void* dp2, void* dv, float* dg,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
 /* Measurement aid. While armed, every launch of the named kernel ("fwd": the
  * fused forward kernel; "bwd_dkdv", "bwd_dq": the two backward kernels; "bwd":
  * both backward kernels, back to back) is bracketed by

@@ -71,6 +71,8 @@ _SIGS = {
     "relation_decode_merge": (ctypes.c_int, [_PP, ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
     "relation_linear_fwd_workspace_bytes": (ctypes.c_size_t, [_PP]),
     "relation_linear_fwd": (ctypes.c_int, [_PP, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "relation_linear_bwd_workspace_bytes": (ctypes.c_size_t, [_PP]),
+    "relation_linear_bwd": (ctypes.c_int, [_PP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "relation_profile_arm": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]),
     "relation_profile_disarm": (ctypes.c_int, []),
     "relation_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -471,6 +473,23 @@ def relation_linear_fwd(p1, p2, v, g, *, tau_s: float = TAU_S, scale: Optional[f
                                  _ptr(ws), _nbytes(ws), _stream())
     _check(st, "relation_linear_fwd")
     return {"o": o, "state": state}
+
+
+def relation_linear_bwd(p1, p2, v, g, dout, *, tau_s: float = TAU_S, scale: Optional[float] = None,
+                        workspace=None):
+    """Linear Relation backward. Returns dict(dp1, dp2, dv, dg (fp32))."""
+    lib = load_library()
+    p2, v, dout = _same_layout(p1, p2, v, dout)
+    p = make_problem(p1, tau_s, scale)
+    dev = p1.device
+    g = g.to(device=dev, dtype=torch.float32).contiguous()
+    dp1, dp2, dv = _layout_like(p1), _layout_like(p1), _layout_like(p1)
+    dg = torch.empty(p1.shape, dtype=torch.float32, device=dev)
+    ws = _workspace(max(1, int(lib.relation_linear_bwd_workspace_bytes(ctypes.byref(p)))), workspace, dev)
+    st = lib.relation_linear_bwd(ctypes.byref(p), _ptr(p1), _ptr(p2), _ptr(v), _ptr(g), _ptr(dout), _ptr(dp1),
+                                 _ptr(dp2), _ptr(dv), _ptr(dg), _ptr(ws), _nbytes(ws), _stream())
+    _check(st, "relation_linear_bwd")
+    return {"dp1": dp1, "dp2": dp2, "dv": dv, "dg": dg}
 
 
 def relation_profile_arm(kernel: str, events: list) -> None:

@@ -141,6 +141,14 @@ struct LinearArgs {
   float* cprev;          // [N, nchunks, D, D]: the state entering each chunk
   float* state_out;      // [N, D, D] or null: the state after the last token
   void* out;             // [B, H, T, D] dtype: Y
+  // backward
+  const void* dy;        // [B, H, T, D] dtype: dL/dY
+  float* pstate;         // [N, nchunks, D, D]: Qe^T dY of each chunk
+  float* gout;           // [N, nchunks, D, D]: dL/d(state leaving each chunk)
+  void* dp1;             // [B, H, T, D] dtype
+  void* dp2;
+  void* dv;
+  float* dg;             // [B, H, T, D] fp32, dense
 };
 
 // Measurement aid: if armed for kernel `name`, returns the event pair to record
@@ -157,6 +165,7 @@ hipError_t launch_allocation(const RowArgs& a, int dtype, int N, hipStream_t str
 // (D, D/2 with RoPE, and the strides multiples of vec; pointers aligned to it).
 int linear_chunk();
 hipError_t launch_linear_fwd(const LinearArgs& a, int dtype, hipStream_t stream);
+hipError_t launch_linear_bwd(const LinearArgs& a, int dtype, hipStream_t stream);
 int decode_slice_keys();
 hipError_t launch_decode_states(const DecodeArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_decode_merge(const DecodeArgs& a, int dtype, hipStream_t stream);

@@ -219,6 +219,299 @@ __global__ __launch_bounds__(kLT) void linear_out_kernel(LinearArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Backward. With Qe = qt e^{b}, Kd = kt e^{b_last - b} and the chunk's state
+// C0 (entering) and G (gradient of the state leaving the chunk):
+//   inter read   E = Qe C0:            dQe = dY C0^T,  P = Qe^T dY (to the scan)
+//   state write  C1 = gamma C0 + Kd^T v: dKd = v G^T, dv += Kd G, dgamma_a = sum_e G C0
+//   intra        A_tj = sum_a qt_ta kt_ja e^{b_ta - b_ja} (j < t):
+//                dA_tj = dY_t . v_j, dv_j += sum_t A_tj dY_t,
+//                dqt_t += sum_j dA_tj kt_j e^{..}, dkt_j += sum_t dA_tj qt_t e^{..}
+//   b (running sum of g): db_t = qt dqt_intra - kt dkt_intra + dQe Qe - dKd Kd,
+//                db_last += sum_j dKd Kd + dgamma gamma; dg = reverse running sum of db
+//   then qt = S ^p1, kt = S ^p2 through S and the normalisation.
+// The scan runs forward for C0 and backward for G, both per state entry.
+// ---------------------------------------------------------------------------
+
+// Per chunk: the state contribution (as in the forward pass) and P = Qe^T dY.
+template <typename TI, int D>
+__global__ __launch_bounds__(kLT) void linear_bstate_kernel(LinearArgs a) {
+  __shared__ float qt[kL][D], kt[kL][D], vv[kL][D], bb[kL][D], dy[kL][D];
+  __shared__ float Srow[kL];
+  const ChunkPos p = chunk_pos(a);
+  load_chunk<TI, D>(a, p, qt, kt, vv, bb, Srow);
+  const int tid = threadIdx.x;
+  {
+    const int b = p.n / a.H, h = p.n % a.H;
+    const TI* DY = (const TI*)a.dy + (int64_t)b * a.sb + (int64_t)h * a.sh;
+    for (int i = tid; i < kL * D; i += kLT) {
+      const int r = i / D, d = i % D;
+      dy[r][d] = r < p.len ? Elem<TI>::load(DY + (int64_t)(p.t0 + r) * a.st + d) : 0.0f;
+      kt[r][d] *= fast_exp2((bb[kL - 1][d] - bb[r][d]) * kLog2e);
+      qt[r][d] *= fast_exp2(bb[r][d] * kLog2e);
+    }
+  }
+  __syncthreads();
+  const int64_t base = ((int64_t)p.n * a.nchunks + p.c);
+  if (tid < D) a.gamma[base * D + tid] = fast_exp2(bb[kL - 1][tid] * kLog2e);
+  constexpr int TE = 4;
+  constexpr int TA = D * D / (kLT * TE);
+  constexpr int NE = D / TE;
+  const int a0 = (tid / NE) * TA, e0 = (tid % NE) * TE;
+  float c1[TA][TE], c2[TA][TE];
+#pragma unroll
+  for (int i = 0; i < TA; ++i)
+#pragma unroll
+    for (int j = 0; j < TE; ++j) c1[i][j] = c2[i][j] = 0.0f;
+  for (int r = 0; r < kL; ++r) {
+    float kr[TA], qr[TA], vr[TE], gr[TE];
+#pragma unroll
+    for (int i = 0; i < TA; ++i) {
+      kr[i] = kt[r][a0 + i];
+      qr[i] = qt[r][a0 + i];
+    }
+#pragma unroll
+    for (int j = 0; j < TE; ++j) {
+      vr[j] = vv[r][e0 + j];
+      gr[j] = dy[r][e0 + j];
+    }
+#pragma unroll
+    for (int i = 0; i < TA; ++i)
+#pragma unroll
+      for (int j = 0; j < TE; ++j) {
+        c1[i][j] = __builtin_fmaf(kr[i], vr[j], c1[i][j]);
+        c2[i][j] = __builtin_fmaf(qr[i], gr[j], c2[i][j]);
+      }
+  }
+  float* dC = a.dstate + base * D * D;
+  float* P = a.pstate + base * D * D;
+#pragma unroll
+  for (int i = 0; i < TA; ++i)
+#pragma unroll
+    for (int j = 0; j < TE; ++j) {
+      dC[(a0 + i) * D + e0 + j] = c1[i][j];
+      P[(a0 + i) * D + e0 + j] = c2[i][j];
+    }
+}
+
+// Per head and state entry: C entering every chunk (forward), and the gradient
+// of the state leaving every chunk (backward): G_last = 0, G_{c-1} = gamma_c G_c + P_c.
+__global__ __launch_bounds__(256) void linear_bscan_kernel(LinearArgs a) {
+  const int D = a.D;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)D * D) return;
+  const int n = blockIdx.y;
+  const int ar = (int)(idx / D);
+  float C = 0.0f;
+  for (int c = 0; c < a.nchunks; ++c) {
+    const int64_t base = (int64_t)n * a.nchunks + c;
+    a.cprev[base * D * D + idx] = C;
+    C = a.gamma[base * D + ar] * C + a.dstate[base * D * D + idx];
+  }
+  float G = 0.0f;
+  for (int c = a.nchunks - 1; c >= 0; --c) {
+    const int64_t base = (int64_t)n * a.nchunks + c;
+    a.gout[base * D * D + idx] = G;
+    G = a.gamma[base * D + ar] * G + a.pstate[base * D * D + idx];
+  }
+}
+
+// Per chunk: every input gradient. Thread (row r = tid / 4, quarter Q of the
+// channels) keeps its row's gradients for the channels of Q in registers.
+template <typename TI, int D>
+__global__ __launch_bounds__(kLT) void linear_grad_kernel(LinearArgs a) {
+  static_assert(D <= 64, "the backward kernel keeps the chunk of D <= 64 channels in LDS");
+  __shared__ float qt[kL][D], kt[kL][D], vv[kL][D], bb[kL][D], dy[kL][D], dbs[kL][D], tmp[kL][D];
+  __shared__ float M1[kL][kL + 1], M2[kL][kL + 1];  // A, dA; then C0 and G
+  __shared__ float Srow[kL];
+  constexpr int QW = D / 4;  // channels per thread
+  const ChunkPos p = chunk_pos(a);
+  load_chunk<TI, D>(a, p, qt, kt, vv, bb, Srow);
+  const int tid = threadIdx.x;
+  const int b = p.n / a.H, h = p.n % a.H;
+  const int64_t hoff = (int64_t)b * a.sb + (int64_t)h * a.sh;
+  for (int i = tid; i < kL * D; i += kLT) {
+    const int r = i / D, d = i % D;
+    dy[r][d] = r < p.len ? Elem<TI>::load((const TI*)a.dy + hoff + (int64_t)(p.t0 + r) * a.st + d) : 0.0f;
+  }
+  __syncthreads();
+  const int r = tid >> 2, q0 = (tid & 3) * QW;
+  float dq[QW], dk[QW], dv[QW], db[QW];
+#pragma unroll
+  for (int i = 0; i < QW; ++i) {
+    dq[i] = 0.0f;
+    dk[i] = 0.0f;
+    dv[i] = dy[r][q0 + i];  // Y = I~ + E
+    db[i] = 0.0f;
+  }
+  // Phase I (row r as t): A[r][j], dA[r][j] for j < r; dqt_intra
+#pragma unroll 2
+  for (int j = 0; j < kL; ++j) {
+    float pa = 0.0f, pd = 0.0f;
+    if (j < r) {
+#pragma unroll
+      for (int i = 0; i < QW; ++i) pd = __builtin_fmaf(dy[r][q0 + i], vv[j][q0 + i], pd);
+    }
+    pd += __shfl_xor(pd, 1, 64);
+    pd += __shfl_xor(pd, 2, 64);  // dA[r][j] over all channels
+    if (j < r) {
+#pragma unroll
+      for (int i = 0; i < QW; ++i) {
+        const int d = q0 + i;
+        const float w = kt[j][d] * fast_exp2((bb[r][d] - bb[j][d]) * kLog2e);
+        pa = __builtin_fmaf(qt[r][d], w, pa);
+        dq[i] = __builtin_fmaf(pd, w, dq[i]);
+      }
+    }
+    pa += __shfl_xor(pa, 1, 64);
+    pa += __shfl_xor(pa, 2, 64);
+    if ((tid & 3) == 0) {
+      M1[r][j] = j < r ? pa : 0.0f;
+      M2[r][j] = j < r ? pd : 0.0f;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < QW; ++i) db[i] = qt[r][q0 + i] * dq[i];
+  __syncthreads();
+  // Phase II (row r as j): dv_intra, dkt_intra
+#pragma unroll 2
+  for (int t = r + 1; t < kL; ++t) {
+    const float At = M1[t][r], dAt = M2[t][r];
+#pragma unroll
+    for (int i = 0; i < QW; ++i) {
+      const int d = q0 + i;
+      dv[i] = __builtin_fmaf(At, dy[t][d], dv[i]);
+      dk[i] = __builtin_fmaf(dAt * qt[t][d], fast_exp2((bb[t][d] - bb[r][d]) * kLog2e), dk[i]);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < QW; ++i) db[i] -= kt[r][q0 + i] * dk[i];
+  __syncthreads();
+  // Phase III: stage C0 and G over A, dA
+  const int64_t base = (int64_t)p.n * a.nchunks + p.c;
+  for (int i = tid; i < D * D; i += kLT) {
+    M1[i / D][i % D] = a.cprev[base * D * D + i];
+    M2[i / D][i % D] = a.gout[base * D * D + i];
+  }
+  __syncthreads();
+  // inter read: dQe[r][d] = sum_e dY[r][e] C0[d][e]; write: dKd[r][d] = sum_e v[r][e] G[d][e]
+  float dqe_[QW], dkd_[QW];
+#pragma unroll
+  for (int i = 0; i < QW; ++i) dqe_[i] = dkd_[i] = 0.0f;
+#pragma unroll 2
+  for (int e = 0; e < D; ++e) {
+    const float ye = dy[r][e], ve = vv[r][e];
+#pragma unroll
+    for (int i = 0; i < QW; ++i) {
+      dqe_[i] = __builtin_fmaf(ye, M1[q0 + i][e], dqe_[i]);
+      dkd_[i] = __builtin_fmaf(ve, M2[q0 + i][e], dkd_[i]);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < QW; ++i) {
+    const int d = q0 + i;
+    const float dqe = dqe_[i], dkd = dkd_[i];
+    const float eb = fast_exp2(bb[r][d] * kLog2e);
+    const float ek = fast_exp2((bb[kL - 1][d] - bb[r][d]) * kLog2e);
+    dq[i] = __builtin_fmaf(dqe, eb, dq[i]);
+    dk[i] = __builtin_fmaf(dkd, ek, dk[i]);
+    const float kd = kt[r][d] * ek;
+    db[i] += dqe * qt[r][d] * eb - dkd * kd;
+    tmp[r][d] = dkd * kd;  // its column sum goes to the chunk's last row
+  }
+  // dv += Kd G: dv[r][e] += sum_d Kd[r][d] G[d][e]
+#pragma unroll 2
+  for (int d = 0; d < D; ++d) {
+    const float kd = kt[r][d] * fast_exp2((bb[kL - 1][d] - bb[r][d]) * kLog2e);
+#pragma unroll
+    for (int i = 0; i < QW; ++i) dv[i] = __builtin_fmaf(kd, M2[d][q0 + i], dv[i]);
+  }
+#pragma unroll
+  for (int i = 0; i < QW; ++i) dbs[r][q0 + i] = db[i];
+  __syncthreads();
+  // dg: reverse running sum of db down the chunk, with the last row's extra terms
+  if (tid < D) {
+    const int d = tid;
+    float extra = 0.0f, dgam = 0.0f;
+    for (int j = 0; j < kL; ++j) extra += tmp[j][d];
+    for (int e = 0; e < D; ++e) dgam = __builtin_fmaf(M2[d][e], M1[d][e], dgam);
+    float acc = extra + dgam * fast_exp2(bb[kL - 1][d] * kLog2e);
+    float* dG = a.dg + (int64_t)p.n * a.T * D;
+    for (int j = kL - 1; j >= 0; --j) {
+      acc += dbs[j][d];
+      if (j < p.len) dG[(int64_t)(p.t0 + j) * D + d] = acc;
+    }
+  }
+  // through qt = S p1 / |p1|, kt = S p2 / |p2|, S = sigmoid(scale p1 . p2 / tau_S)
+  const TI* P1 = (const TI*)a.p1 + hoff + (int64_t)(p.t0 + r) * a.st;
+  const TI* P2 = (const TI*)a.p2 + hoff + (int64_t)(p.t0 + r) * a.st;
+  const bool ok = r < p.len;
+  float x1[QW], x2[QW];
+  float s11 = 0.0f, s22 = 0.0f, s12 = 0.0f;
+#pragma unroll
+  for (int i = 0; i < QW; ++i) {
+    x1[i] = ok ? Elem<TI>::load(P1 + q0 + i) : 0.0f;
+    x2[i] = ok ? Elem<TI>::load(P2 + q0 + i) : 0.0f;
+    s11 += x1[i] * x1[i];
+    s22 += x2[i] * x2[i];
+    s12 += x1[i] * x2[i];
+  }
+  s11 += __shfl_xor(s11, 1, 64); s11 += __shfl_xor(s11, 2, 64);
+  s22 += __shfl_xor(s22, 1, 64); s22 += __shfl_xor(s22, 2, 64);
+  s12 += __shfl_xor(s12, 1, 64); s12 += __shfl_xor(s12, 2, 64);
+  const float S = Srow[r];
+  const float in1 = s11 > 0.0f ? rsqrtf(s11) : 0.0f, in2 = s22 > 0.0f ? rsqrtf(s22) : 0.0f;
+  // dS = dqt . ^p1 + dkt . ^p2; ^p . d^p for the projections
+  float ds = 0.0f, h1d = 0.0f, h2d = 0.0f;
+#pragma unroll
+  for (int i = 0; i < QW; ++i) {
+    ds += dq[i] * x1[i] * in1 + dk[i] * x2[i] * in2;
+    h1d += x1[i] * in1 * dq[i];
+    h2d += x2[i] * in2 * dk[i];
+  }
+  ds += __shfl_xor(ds, 1, 64); ds += __shfl_xor(ds, 2, 64);
+  h1d += __shfl_xor(h1d, 1, 64); h1d += __shfl_xor(h1d, 2, 64);
+  h2d += __shfl_xor(h2d, 1, 64); h2d += __shfl_xor(h2d, 2, 64);
+  if (ok) {
+    const float dU = ds * S * (1.0f - S) * a.scale * a.inv_tau;
+    TI* DP1 = (TI*)a.dp1 + hoff + (int64_t)(p.t0 + r) * a.st;
+    TI* DP2 = (TI*)a.dp2 + hoff + (int64_t)(p.t0 + r) * a.st;
+    TI* DV = (TI*)a.dv + hoff + (int64_t)(p.t0 + r) * a.st;
+#pragma unroll
+    for (int i = 0; i < QW; ++i) {
+      // d^p1 = S dqt; dp1 = dU p2 + (d^p1 - ^p1 (^p1 . d^p1)) / |p1|
+      const float g1 = dU * x2[i] + S * (dq[i] - x1[i] * in1 * h1d) * in1;
+      const float g2 = dU * x1[i] + S * (dk[i] - x2[i] * in2 * h2d) * in2;
+      Elem<TI>::store(DP1 + q0 + i, g1);
+      Elem<TI>::store(DP2 + q0 + i, g2);
+      Elem<TI>::store(DV + q0 + i, dv[i]);
+    }
+  }
+}
+
+template <typename TI, int D>
+hipError_t launch_bwd_d(const LinearArgs& a, hipStream_t stream) {
+  const dim3 grid((unsigned)a.nchunks, (unsigned)(a.B * a.H));
+  hipLaunchKernelGGL((linear_bstate_kernel<TI, D>), grid, dim3(kLT), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const dim3 sgrid((unsigned)((D * D + 255) / 256), (unsigned)(a.B * a.H));
+  hipLaunchKernelGGL(linear_bscan_kernel, sgrid, dim3(256), 0, stream, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((linear_grad_kernel<TI, D>), grid, dim3(kLT), 0, stream, a);
+  return hipGetLastError();
+}
+
+template <typename TI>
+hipError_t launch_bwd_t(const LinearArgs& a, hipStream_t stream) {
+  switch (a.D) {
+    case 32: return launch_bwd_d<TI, 32>(a, stream);
+    case 64: return launch_bwd_d<TI, 64>(a, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 template <typename TI, int D>
 hipError_t launch_fwd_d(const LinearArgs& a, hipStream_t stream) {
   const dim3 grid((unsigned)a.nchunks, (unsigned)(a.B * a.H));
@@ -249,6 +542,10 @@ int linear_chunk() { return kL; }
 
 hipError_t launch_linear_fwd(const LinearArgs& a, int dtype, hipStream_t stream) {
   return dtype == 1 ? launch_fwd_t<bf16>(a, stream) : launch_fwd_t<float>(a, stream);
+}
+
+hipError_t launch_linear_bwd(const LinearArgs& a, int dtype, hipStream_t stream) {
+  return dtype == 1 ? launch_bwd_t<bf16>(a, stream) : launch_bwd_t<float>(a, stream);
 }
 
 }  // namespace rel

@@ -1157,4 +1157,70 @@ rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void*
   return REL_OK;
 }
 
+size_t relation_linear_bwd_workspace_bytes(const rel_problem* p) {
+  bool empty = false;
+  if (check_linear(p, &empty) != REL_OK || empty || p->D > 64) return 0;
+  const size_t N = (size_t)(p->B * p->H), nc = (size_t)linear_chunks(p), D = (size_t)p->D;
+  return plan_linear(p).total + 2 * align256(N * nc * D * D * 4);
+}
+
+rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
+                               const float* g, const void* dout, void* dp1, void* dp2, void* dv, float* dg,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  bool empty = false;
+  REL_TRY(check_linear(p, &empty));
+  if (empty) return REL_OK;
+  if (p->D > 64)
+    return fail(REL_ERR_UNSUPPORTED, "the Linear Relation backward keeps a chunk in LDS: D <= 64 (got %lld)",
+                (long long)p->D);
+  const size_t es = elem_size(p->dtype);
+  REL_TRY(check_aligned(p1, es, "p1", true));
+  REL_TRY(check_aligned(p2, es, "p2", true));
+  REL_TRY(check_aligned(v, es, "v", true));
+  REL_TRY(check_aligned(g, 4, "g", true));
+  REL_TRY(check_aligned(dout, es, "dout", true));
+  REL_TRY(check_aligned(dp1, es, "dp1", true));
+  REL_TRY(check_aligned(dp2, es, "dp2", true));
+  REL_TRY(check_aligned(dv, es, "dv", true));
+  REL_TRY(check_aligned(dg, 4, "dg", true));
+  const size_t need = relation_linear_bwd_workspace_bytes(p);
+  if (!workspace || workspace_bytes < need)
+    return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                workspace ? workspace_bytes : (size_t)0);
+  REL_TRY(check_aligned(workspace, 16, "workspace", true));
+  const size_t tb = (size_t)extent_elems(p) * es;
+  const size_t N = (size_t)(p->B * p->H);
+  const size_t gb = N * (size_t)p->T * (size_t)p->D * 4;
+  REL_TRY(check_buffers(p, {{p1, tb, true, false, "p1"},
+                            {p2, tb, true, false, "p2"},
+                            {v, tb, true, false, "v"},
+                            {g, gb, false, false, "g"},
+                            {dout, tb, true, false, "dout"},
+                            {dp1, tb, true, true, "dp1"},
+                            {dp2, tb, true, true, "dp2"},
+                            {dv, tb, true, true, "dv"},
+                            {dg, gb, false, true, "dg"},
+                            {workspace, need, false, true, "workspace"}}));
+  if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected by RELATION_TEST_FAIL_LAUNCH");
+  const LinearPlan L = plan_linear(p);
+  const size_t nc = (size_t)linear_chunks(p), D = (size_t)p->D;
+  rel::LinearArgs a{};
+  a.p1 = p1; a.p2 = p2; a.v = v; a.g = g; a.dy = dout;
+  a.dp1 = dp1; a.dp2 = dp2; a.dv = dv; a.dg = dg;
+  a.sb = p->stride_b; a.sh = p->stride_h; a.st = p->stride_t;
+  a.B = (int)p->B; a.H = (int)p->H; a.T = (int)p->T; a.D = (int)p->D;
+  a.scale = eff_scale(p);
+  a.inv_tau = 1.0f / p->tau_s;
+  a.nchunks = (int)nc;
+  char* ws = (char*)workspace;
+  a.dstate = (float*)(ws + L.dstate);
+  a.gamma = (float*)(ws + L.gamma);
+  a.cprev = (float*)(ws + L.cprev);
+  a.pstate = (float*)(ws + L.total);
+  a.gout = (float*)(ws + L.total + align256(N * nc * D * D * 4));
+  const hipError_t e = rel::launch_linear_bwd(a, p->dtype, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "Linear Relation backward launch");
+  return REL_OK;
+}
+
 }  // extern "C"

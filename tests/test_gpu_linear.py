@@ -85,3 +85,45 @@ def test_linear_forward_strided():
     b = R.relation_linear_fwd(t(x["p1"]), t(x["p2"]), t(x["v"]), x["g"])
     torch.cuda.synchronize()
     assert torch.equal(a["o"], b["o"].contiguous())
+
+
+def check_linear_bwd(x, dtype, heads=None):
+    B, H, T, D = x["p1"].shape
+    log(f"[linear bwd] B={B} H={H} T={T} D={D} {dtype}")
+    r = R.relation_linear_bwd(x["p1"], x["p2"], x["v"], x["g"], x["dy"])
+    torch.cuda.synchronize()
+    heads = heads or [(b, h) for b in range(B) for h in range(H)]
+    for b, h in heads:
+        o = LO.backward(x["p1r"][b, h], x["p2r"][b, h], x["vr"][b, h], x["gr"][b, h], x["dyr"][b, h])
+        for n in ("dp1", "dp2", "dv", "dg"):
+            assert_close(f"{n}[{b},{h}]", _np(r[n])[b, h], o[n], dtype)
+    return r
+
+
+@pytest.mark.parametrize("B,H,T,D,dtype", [
+    (2, 2, 300, 64, "bf16"), (1, 2, 190, 32, "f32"), (1, 3, 64, 64, "f32"), (1, 2, 1, 64, "bf16"),
+    (1, 2, 65, 32, "bf16"), (1, 2, 129, 64, "f32"),
+])
+def test_linear_backward(B, H, T, D, dtype):
+    x = _prep(B, H, T, D, dtype, seed=1400 + T + D)
+    check_linear_bwd(x, dtype)
+
+
+@pytest.mark.parametrize("gmax", [1e-3, 8.0])
+def test_linear_backward_retention_range(gmax):
+    x = _prep(1, 2, 200, 64, "f32", seed=1500, gmax=gmax)
+    check_linear_bwd(x, "f32")
+
+
+def test_linear_backward_long():
+    x = _prep(1, 2, 2048, 64, "bf16", seed=1600, gmax=0.05)
+    check_linear_bwd(x, "bf16", heads=[(0, 1)])
+
+
+def test_linear_backward_repeatable():
+    x = _prep(2, 2, 300, 64, "bf16", seed=1700)
+    a = R.relation_linear_bwd(x["p1"], x["p2"], x["v"], x["g"], x["dy"])
+    b = R.relation_linear_bwd(x["p1"], x["p2"], x["v"], x["g"], x["dy"])
+    torch.cuda.synchronize()
+    for n in ("dp1", "dp2", "dv", "dg"):
+        assert torch.equal(a[n], b[n]), n
