@@ -370,6 +370,56 @@ def decode_leg(K: int) -> list:
     return out
 
 
+LINEAR_SHAPES = [  # (B, H, T, D): one Linear Relation layer, 8 heads of width 64 (the paper's 60, padded)
+    (1, 8, 4096, 64),
+    (1, 8, 16384, 64),
+    (1, 8, 32768, 64),
+]
+
+
+def linear_leg(K: int) -> list:
+    """relation_linear_fwd + relation_linear_bwd on bf16 Gaussians and
+    log-retention -U(0, 0.05): time per step, tokens/s, and the forward alone."""
+    import torch
+    from paper_2608_20172_amd import binding as R
+
+    out = []
+    for B, H, T, D in LINEAR_SHAPES:
+        dev = torch.device("cuda:0")
+        gen = torch.Generator(device=dev).manual_seed(5)
+        p1, p2, v, dy = (torch.randn(B, H, T, D, device=dev, generator=gen).to(torch.bfloat16) for _ in range(4))
+        g = -torch.rand(B, H, T, D, device=dev, generator=gen) * 0.05
+        fws = torch.empty(max(1, int(R.load_library().relation_linear_fwd_workspace_bytes(
+            ctypes.byref(R.make_problem(p1))))), dtype=torch.uint8, device=dev)
+        bws = torch.empty(max(1, int(R.load_library().relation_linear_bwd_workspace_bytes(
+            ctypes.byref(R.make_problem(p1))))), dtype=torch.uint8, device=dev)
+
+        def fwd():
+            return R.relation_linear_fwd(p1, p2, v, g, workspace=fws)
+
+        def step():
+            fwd()
+            R.relation_linear_bwd(p1, p2, v, g, dy, workspace=bws)
+
+        for _ in range(3):
+            step()
+        torch.cuda.synchronize()
+        n = max(5, K // 3)
+        res = {}
+        for name, fn in (("fwd_bwd", step), ("fwd", fwd)):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(n):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            res[name] = e0.elapsed_time(e1) / n
+        out.append({"B": B, "H": H, "T": T, "D": D, "ms_fwd_bwd": res["fwd_bwd"], "ms_fwd": res["fwd"],
+                    "tokens_per_s": B * T / (res["fwd_bwd"] * 1e-3)})
+        del p1, p2, v, dy, g, fws, bws
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -381,6 +431,7 @@ def main() -> int:
     ap.add_argument("--no-materialized", action="store_true")
     ap.add_argument("--no-layer", action="store_true", help="skip the layer entry points leg")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode leg")
+    ap.add_argument("--no-linear", action="store_true", help="skip the Linear Relation leg")
     ap.add_argument("--copy-bytes", type=int, default=0)
     ap.add_argument("--copy-kind", choices=("memcpy", "elementwise"), default="elementwise")
     ap.add_argument("--summarize-counters", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
@@ -525,6 +576,9 @@ def main() -> int:
     decode = {"status": "skipped"}
     if not args.no_decode:
         decode = decode_leg(K)
+    linear = {"status": "skipped"}
+    if not args.no_linear:
+        linear = linear_leg(K)
 
     fl_f, fl_b = flops(w, "fwd"), flops(w, "bwd") if w.backward else 0.0
     kern_flops = fl_b if w.backward else fl_f
@@ -556,6 +610,7 @@ def main() -> int:
         "materialized": mat,
         "layer": layer,
         "decode": decode,
+        "linear": linear,
         "roofline": {
             "kernel": "bwd_dkdv_kernel+bwd_dq_kernel" if w.backward else "fwd_kernel",
             "bound": "mfma",

@@ -20,7 +20,9 @@ namespace rel {
 namespace {
 
 constexpr int kL = 64;      // tokens per chunk
-constexpr int kLT = 256;    // threads per workgroup
+constexpr int kLT = 256;    // threads per workgroup of the state kernels
+constexpr int kTPR = 8;     // threads per token row in the output and gradient kernels
+constexpr int kLT2 = kL * kTPR;
 
 struct ChunkPos {
   int n, c, t0, len;  // head, chunk, first token, valid tokens
@@ -38,7 +40,7 @@ __device__ __forceinline__ ChunkPos chunk_pos(const LinearArgs& a) {
 // Loads the chunk into LDS as fp32 and forms qt = S ^p1, kt = S ^p2 (rows past
 // the sequence are zero), v, and b = running sum of g (zero g past the end, so
 // b stays at its last value). One wave per row for the norms and S.
-template <typename TI, int D>
+template <typename TI, int D, int NT>
 __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& p, float (*qt)[D], float (*kt)[D],
                                            float (*vv)[D], float (*bb)[D], float* Srow) {
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
@@ -48,7 +50,7 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
   const TI* P2 = (const TI*)a.p2 + hoff;
   const TI* V = (const TI*)a.v + hoff;
   const float* G = a.g + (int64_t)p.n * a.T * D;
-  for (int r = w; r < kL; r += kLT / 64) {
+  for (int r = w; r < kL; r += NT / 64) {
     const bool ok = r < p.len;
     const int64_t row = (int64_t)(p.t0 + r);
     float x1[2] = {0.0f, 0.0f}, x2[2] = {0.0f, 0.0f};
@@ -87,7 +89,7 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
         kt[r][d] = x2[u] * i2;
       }
     }
-    if (lane == 0) Srow[r] = S;
+    if (lane == 0 && Srow) Srow[r] = S;
   }
   __syncthreads();
   if (tid < D) {  // running sum of g down the chunk, one channel per thread
@@ -104,9 +106,8 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
 template <typename TI, int D>
 __global__ __launch_bounds__(kLT) void linear_state_kernel(LinearArgs a) {
   __shared__ float qt[kL][D], kt[kL][D], vv[kL][D], bb[kL][D];
-  __shared__ float Srow[kL];
   const ChunkPos p = chunk_pos(a);
-  load_chunk<TI, D>(a, p, qt, kt, vv, bb, Srow);
+  load_chunk<TI, D, kLT>(a, p, qt, kt, vv, bb, nullptr);
   const int tid = threadIdx.x;
   // kt <- kt e^{b_last - b}
   for (int i = tid; i < kL * D; i += kLT) {
@@ -152,6 +153,7 @@ __global__ __launch_bounds__(256) void linear_scan_kernel(LinearArgs a) {
   const int n = blockIdx.y;
   const int ar = (int)(idx / D);
   float C = 0.0f;
+#pragma unroll 4
   for (int c = 0; c < a.nchunks; ++c) {
     const int64_t base = (int64_t)n * a.nchunks + c;
     a.cprev[base * D * D + idx] = C;
@@ -162,52 +164,61 @@ __global__ __launch_bounds__(256) void linear_scan_kernel(LinearArgs a) {
 
 // Per chunk: Y_t = v_t + intra + inter (see the top of the file).
 template <typename TI, int D>
-__global__ __launch_bounds__(kLT) void linear_out_kernel(LinearArgs a) {
-  __shared__ float qt[kL][D], kt[kL][D], vv[kL][D], bb[kL][D];
-  __shared__ float A[kL][kL + 1];
-  __shared__ float Srow[kL];
+__global__ __launch_bounds__(kLT2) void linear_out_kernel(LinearArgs a) {
+  static_assert(2 * kL * D >= D * D, "the state entering the chunk is staged over kt and bb");
+  __shared__ float qt[kL][D], vv[kL][D];
+  __shared__ float kb[2][kL][D];  // kt, bb; then the state entering the chunk
+  __shared__ float A[kL][kL];     // column j of row t stored at j ^ (t % 8): rows read together hit distinct banks
+  float (*kt)[D] = kb[0];
+  float (*bb)[D] = kb[1];
   const ChunkPos p = chunk_pos(a);
-  load_chunk<TI, D>(a, p, qt, kt, vv, bb, Srow);
+  load_chunk<TI, D, kLT2>(a, p, qt, kt, vv, bb, nullptr);
   const int tid = threadIdx.x;
-  // intra scores A[t][j], j < t: thread -> row t = tid / 4, columns j = tid % 4 + 4 m
+  // intra scores A[t][j], j < t: thread -> row t = tid / kTPR, columns j = tid % kTPR + kTPR m
   {
-    const int t = tid >> 2, j0 = tid & 3;
-    float acc[kL / 4];
+    const int t = tid / kTPR, j0 = tid % kTPR;
+    float acc[kL / kTPR];
 #pragma unroll
-    for (int m = 0; m < kL / 4; ++m) acc[m] = 0.0f;
+    for (int m = 0; m < kL / kTPR; ++m) acc[m] = 0.0f;
     for (int d = 0; d < D; ++d) {
       const float qd = qt[t][d], bd = bb[t][d];
 #pragma unroll
-      for (int m = 0; m < kL / 4; ++m) {
-        const int j = j0 + 4 * m;
+      for (int m = 0; m < kL / kTPR; ++m) {
+        const int j = j0 + kTPR * m;
         if (j < t) acc[m] = __builtin_fmaf(qd * kt[j][d], fast_exp2((bd - bb[j][d]) * kLog2e), acc[m]);
       }
     }
 #pragma unroll
-    for (int m = 0; m < kL / 4; ++m) A[t][j0 + 4 * m] = acc[m];
+    for (int m = 0; m < kL / kTPR; ++m) A[t][(j0 + kTPR * m) ^ (t & 7)] = acc[m];
   }
   __syncthreads();
   // qt <- qt e^{b} (the inter read's query)
-  for (int i = tid; i < kL * D; i += kLT) {
+  for (int i = tid; i < kL * D; i += kLT2) {
     const int r = i / D, d = i % D;
     qt[r][d] *= fast_exp2(bb[r][d] * kLog2e);
   }
   __syncthreads();
-  // outputs: thread -> row t = tid / 4, channels e0 .. e0 + D/4
-  constexpr int TE = D / 4;
-  const int t = tid >> 2, e0 = (tid & 3) * TE;
+  // the state entering the chunk, over kt and bb (no longer read)
+  float* C0s = &kb[0][0][0];
+  {
+    const float* C0 = a.cprev + ((int64_t)p.n * a.nchunks + p.c) * D * D;
+    for (int i = tid; i < D * D; i += kLT2) C0s[i] = C0[i];
+  }
+  __syncthreads();
+  // outputs: thread -> row t = tid / kTPR, channels e0 .. e0 + D / kTPR
+  constexpr int TE = D / kTPR;
+  const int t = tid / kTPR, e0 = (tid % kTPR) * TE;
   float acc[TE];
 #pragma unroll
   for (int j = 0; j < TE; ++j) acc[j] = vv[t][e0 + j];
   for (int j = 0; j < t; ++j) {
-    const float w = A[t][j];
+    const float w = A[t][j ^ (t & 7)];
 #pragma unroll
     for (int e = 0; e < TE; ++e) acc[e] = __builtin_fmaf(w, vv[j][e0 + e], acc[e]);
   }
-  const float* C0 = a.cprev + ((int64_t)p.n * a.nchunks + p.c) * D * D;
   for (int d = 0; d < D; ++d) {
     const float qd = qt[t][d];
-    const float* crow = C0 + d * D + e0;
+    const float* crow = C0s + d * D + e0;
 #pragma unroll
     for (int e = 0; e < TE; ++e) acc[e] = __builtin_fmaf(qd, crow[e], acc[e]);
   }
@@ -237,9 +248,8 @@ __global__ __launch_bounds__(kLT) void linear_out_kernel(LinearArgs a) {
 template <typename TI, int D>
 __global__ __launch_bounds__(kLT) void linear_bstate_kernel(LinearArgs a) {
   __shared__ float qt[kL][D], kt[kL][D], vv[kL][D], bb[kL][D], dy[kL][D];
-  __shared__ float Srow[kL];
   const ChunkPos p = chunk_pos(a);
-  load_chunk<TI, D>(a, p, qt, kt, vv, bb, Srow);
+  load_chunk<TI, D, kLT>(a, p, qt, kt, vv, bb, nullptr);
   const int tid = threadIdx.x;
   {
     const int b = p.n / a.H, h = p.n % a.H;
@@ -303,12 +313,14 @@ __global__ __launch_bounds__(256) void linear_bscan_kernel(LinearArgs a) {
   const int n = blockIdx.y;
   const int ar = (int)(idx / D);
   float C = 0.0f;
+#pragma unroll 4
   for (int c = 0; c < a.nchunks; ++c) {
     const int64_t base = (int64_t)n * a.nchunks + c;
     a.cprev[base * D * D + idx] = C;
     C = a.gamma[base * D + ar] * C + a.dstate[base * D * D + idx];
   }
   float G = 0.0f;
+#pragma unroll 4
   for (int c = a.nchunks - 1; c >= 0; --c) {
     const int64_t base = (int64_t)n * a.nchunks + c;
     a.gout[base * D * D + idx] = G;
@@ -316,26 +328,26 @@ __global__ __launch_bounds__(256) void linear_bscan_kernel(LinearArgs a) {
   }
 }
 
-// Per chunk: every input gradient. Thread (row r = tid / 4, quarter Q of the
+// Per chunk: every input gradient. Thread (row r = tid / kTPR, part Q of the
 // channels) keeps its row's gradients for the channels of Q in registers.
 template <typename TI, int D>
-__global__ __launch_bounds__(kLT) void linear_grad_kernel(LinearArgs a) {
+__global__ __launch_bounds__(kLT2) void linear_grad_kernel(LinearArgs a) {
   static_assert(D <= 64, "the backward kernel keeps the chunk of D <= 64 channels in LDS");
   __shared__ float qt[kL][D], kt[kL][D], vv[kL][D], bb[kL][D], dy[kL][D], dbs[kL][D], tmp[kL][D];
   __shared__ float M1[kL][kL + 1], M2[kL][kL + 1];  // A, dA; then C0 and G
   __shared__ float Srow[kL];
-  constexpr int QW = D / 4;  // channels per thread
+  constexpr int QW = D / kTPR;  // channels per thread
   const ChunkPos p = chunk_pos(a);
-  load_chunk<TI, D>(a, p, qt, kt, vv, bb, Srow);
+  load_chunk<TI, D, kLT2>(a, p, qt, kt, vv, bb, Srow);
   const int tid = threadIdx.x;
   const int b = p.n / a.H, h = p.n % a.H;
   const int64_t hoff = (int64_t)b * a.sb + (int64_t)h * a.sh;
-  for (int i = tid; i < kL * D; i += kLT) {
+  for (int i = tid; i < kL * D; i += kLT2) {
     const int r = i / D, d = i % D;
     dy[r][d] = r < p.len ? Elem<TI>::load((const TI*)a.dy + hoff + (int64_t)(p.t0 + r) * a.st + d) : 0.0f;
   }
   __syncthreads();
-  const int r = tid >> 2, q0 = (tid & 3) * QW;
+  const int r = tid / kTPR, q0 = (tid % kTPR) * QW;
   float dq[QW], dk[QW], dv[QW], db[QW];
 #pragma unroll
   for (int i = 0; i < QW; ++i) {
@@ -352,8 +364,7 @@ __global__ __launch_bounds__(kLT) void linear_grad_kernel(LinearArgs a) {
 #pragma unroll
       for (int i = 0; i < QW; ++i) pd = __builtin_fmaf(dy[r][q0 + i], vv[j][q0 + i], pd);
     }
-    pd += __shfl_xor(pd, 1, 64);
-    pd += __shfl_xor(pd, 2, 64);  // dA[r][j] over all channels
+    for (int o = 1; o < kTPR; o <<= 1) pd += __shfl_xor(pd, o, 64);  // dA[r][j] over all channels
     if (j < r) {
 #pragma unroll
       for (int i = 0; i < QW; ++i) {
@@ -363,9 +374,8 @@ __global__ __launch_bounds__(kLT) void linear_grad_kernel(LinearArgs a) {
         dq[i] = __builtin_fmaf(pd, w, dq[i]);
       }
     }
-    pa += __shfl_xor(pa, 1, 64);
-    pa += __shfl_xor(pa, 2, 64);
-    if ((tid & 3) == 0) {
+    for (int o = 1; o < kTPR; o <<= 1) pa += __shfl_xor(pa, o, 64);
+    if (tid % kTPR == 0) {
       M1[r][j] = j < r ? pa : 0.0f;
       M2[r][j] = j < r ? pd : 0.0f;
     }
@@ -389,7 +399,7 @@ __global__ __launch_bounds__(kLT) void linear_grad_kernel(LinearArgs a) {
   __syncthreads();
   // Phase III: stage C0 and G over A, dA
   const int64_t base = (int64_t)p.n * a.nchunks + p.c;
-  for (int i = tid; i < D * D; i += kLT) {
+  for (int i = tid; i < D * D; i += kLT2) {
     M1[i / D][i % D] = a.cprev[base * D * D + i];
     M2[i / D][i % D] = a.gout[base * D * D + i];
   }
@@ -456,9 +466,11 @@ __global__ __launch_bounds__(kLT) void linear_grad_kernel(LinearArgs a) {
     s22 += x2[i] * x2[i];
     s12 += x1[i] * x2[i];
   }
-  s11 += __shfl_xor(s11, 1, 64); s11 += __shfl_xor(s11, 2, 64);
-  s22 += __shfl_xor(s22, 1, 64); s22 += __shfl_xor(s22, 2, 64);
-  s12 += __shfl_xor(s12, 1, 64); s12 += __shfl_xor(s12, 2, 64);
+  for (int o = 1; o < kTPR; o <<= 1) {
+    s11 += __shfl_xor(s11, o, 64);
+    s22 += __shfl_xor(s22, o, 64);
+    s12 += __shfl_xor(s12, o, 64);
+  }
   const float S = Srow[r];
   const float in1 = s11 > 0.0f ? rsqrtf(s11) : 0.0f, in2 = s22 > 0.0f ? rsqrtf(s22) : 0.0f;
   // dS = dqt . ^p1 + dkt . ^p2; ^p . d^p for the projections
@@ -469,9 +481,11 @@ __global__ __launch_bounds__(kLT) void linear_grad_kernel(LinearArgs a) {
     h1d += x1[i] * in1 * dq[i];
     h2d += x2[i] * in2 * dk[i];
   }
-  ds += __shfl_xor(ds, 1, 64); ds += __shfl_xor(ds, 2, 64);
-  h1d += __shfl_xor(h1d, 1, 64); h1d += __shfl_xor(h1d, 2, 64);
-  h2d += __shfl_xor(h2d, 1, 64); h2d += __shfl_xor(h2d, 2, 64);
+  for (int o = 1; o < kTPR; o <<= 1) {
+    ds += __shfl_xor(ds, o, 64);
+    h1d += __shfl_xor(h1d, o, 64);
+    h2d += __shfl_xor(h2d, o, 64);
+  }
   if (ok) {
     const float dU = ds * S * (1.0f - S) * a.scale * a.inv_tau;
     TI* DP1 = (TI*)a.dp1 + hoff + (int64_t)(p.t0 + r) * a.st;
@@ -499,7 +513,7 @@ hipError_t launch_bwd_d(const LinearArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(linear_bscan_kernel, sgrid, dim3(256), 0, stream, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((linear_grad_kernel<TI, D>), grid, dim3(kLT), 0, stream, a);
+  hipLaunchKernelGGL((linear_grad_kernel<TI, D>), grid, dim3(kLT2), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -522,7 +536,7 @@ hipError_t launch_fwd_d(const LinearArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(linear_scan_kernel, sgrid, dim3(256), 0, stream, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((linear_out_kernel<TI, D>), grid, dim3(kLT), 0, stream, a);
+  hipLaunchKernelGGL((linear_out_kernel<TI, D>), grid, dim3(kLT2), 0, stream, a);
   return hipGetLastError();
 }
 
