@@ -180,7 +180,10 @@ __global__ __launch_bounds__(kLT2) void linear_out_kernel(LinearArgs a) {
     float acc[kL / kTPR];
 #pragma unroll
     for (int m = 0; m < kL / kTPR; ++m) acc[m] = 0.0f;
-    for (int d = 0; d < D; ++d) {
+    // channel order skewed per lane so that the lanes of a wave read distinct banks
+    const int skew = 8 * (t & 7) + j0;
+    for (int dd = 0; dd < D; ++dd) {
+      const int d = (dd + skew) & (D - 1);
       const float qd = qt[t][d], bd = bb[t][d];
 #pragma unroll
       for (int m = 0; m < kL / kTPR; ++m) {
@@ -357,20 +360,27 @@ __global__ __launch_bounds__(kLT2) void linear_grad_kernel(LinearArgs a) {
     db[i] = 0.0f;
   }
   // Phase I (row r as t): A[r][j], dA[r][j] for j < r; dqt_intra
+  float yself[QW], qself[QW], bsr[QW];
+#pragma unroll
+  for (int i = 0; i < QW; ++i) {
+    yself[i] = dy[r][q0 + i];
+    qself[i] = qt[r][q0 + i];
+    bsr[i] = bb[r][q0 + i];
+  }
 #pragma unroll 2
   for (int j = 0; j < kL; ++j) {
     float pa = 0.0f, pd = 0.0f;
     if (j < r) {
 #pragma unroll
-      for (int i = 0; i < QW; ++i) pd = __builtin_fmaf(dy[r][q0 + i], vv[j][q0 + i], pd);
+      for (int i = 0; i < QW; ++i) pd = __builtin_fmaf(yself[i], vv[j][q0 + i], pd);
     }
     for (int o = 1; o < kTPR; o <<= 1) pd += __shfl_xor(pd, o, 64);  // dA[r][j] over all channels
     if (j < r) {
 #pragma unroll
       for (int i = 0; i < QW; ++i) {
         const int d = q0 + i;
-        const float w = kt[j][d] * fast_exp2((bb[r][d] - bb[j][d]) * kLog2e);
-        pa = __builtin_fmaf(qt[r][d], w, pa);
+        const float w = kt[j][d] * fast_exp2((bsr[i] - bb[j][d]) * kLog2e);
+        pa = __builtin_fmaf(qself[i], w, pa);
         dq[i] = __builtin_fmaf(pd, w, dq[i]);
       }
     }
@@ -383,15 +393,22 @@ __global__ __launch_bounds__(kLT2) void linear_grad_kernel(LinearArgs a) {
 #pragma unroll
   for (int i = 0; i < QW; ++i) db[i] = qt[r][q0 + i] * dq[i];
   __syncthreads();
-  // Phase II (row r as j): dv_intra, dkt_intra
-#pragma unroll 2
-  for (int t = r + 1; t < kL; ++t) {
-    const float At = M1[t][r], dAt = M2[t][r];
+  // Phase II (row r as j): dv_intra, dkt_intra; every lane walks the same rows t
+  {
+    float bself[QW];
 #pragma unroll
-    for (int i = 0; i < QW; ++i) {
-      const int d = q0 + i;
-      dv[i] = __builtin_fmaf(At, dy[t][d], dv[i]);
-      dk[i] = __builtin_fmaf(dAt * qt[t][d], fast_exp2((bb[t][d] - bb[r][d]) * kLog2e), dk[i]);
+    for (int i = 0; i < QW; ++i) bself[i] = bb[r][q0 + i];
+#pragma unroll 2
+    for (int t = 1; t < kL; ++t) {
+      if (t > r) {
+        const float At = M1[t][r], dAt = M2[t][r];
+#pragma unroll
+        for (int i = 0; i < QW; ++i) {
+          const int d = q0 + i;
+          dv[i] = __builtin_fmaf(At, dy[t][d], dv[i]);
+          dk[i] = __builtin_fmaf(dAt * qt[t][d], fast_exp2((bb[t][d] - bself[i]) * kLog2e), dk[i]);
+        }
+      }
     }
   }
 #pragma unroll
@@ -409,7 +426,8 @@ __global__ __launch_bounds__(kLT2) void linear_grad_kernel(LinearArgs a) {
 #pragma unroll
   for (int i = 0; i < QW; ++i) dqe_[i] = dkd_[i] = 0.0f;
 #pragma unroll 2
-  for (int e = 0; e < D; ++e) {
+  for (int ee = 0; ee < D; ++ee) {
+    const int e = (ee + r) & (D - 1);  // skewed per row: the rows of a wave read distinct banks
     const float ye = dy[r][e], ve = vv[r][e];
 #pragma unroll
     for (int i = 0; i < QW; ++i) {
@@ -431,7 +449,8 @@ __global__ __launch_bounds__(kLT2) void linear_grad_kernel(LinearArgs a) {
   }
   // dv += Kd G: dv[r][e] += sum_d Kd[r][d] G[d][e]
 #pragma unroll 2
-  for (int d = 0; d < D; ++d) {
+  for (int dd = 0; dd < D; ++dd) {
+    const int d = (dd + r) & (D - 1);
     const float kd = kt[r][d] * fast_exp2((bb[kL - 1][d] - bb[r][d]) * kLog2e);
 #pragma unroll
     for (int i = 0; i < QW; ++i) dv[i] = __builtin_fmaf(kd, M2[d][q0 + i], dv[i]);
