@@ -297,7 +297,8 @@ rel_status relation_decode_merge(const rel_problem* p, int32_t nstates, const fl
  *              token (rows: relation channel, columns: information channel).
  *   workspace  relation_linear_fwd_workspace_bytes(p) bytes, 16-byte aligned:
  *              per chunk of 64 tokens its state contribution and retention
- *              product, and the state entering it (fp32). */
+ *              product, and the state entering it; per segment of 16 chunks
+ *              the scan's summary (fp32). */
 size_t relation_linear_fwd_workspace_bytes(const rel_problem* p);
 rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
                                const float* g, void* out, float* state_out, void* workspace,
@@ -310,7 +311,7 @@ rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void*
  *   workspace  relation_linear_bwd_workspace_bytes(p) bytes, 16-byte aligned:
  *              the forward workspace plus, per chunk, the D x D products that
  *              the reverse scan over chunks reads and the state gradients it
- *              writes. */
+ *              writes, and per segment of 16 chunks the reverse summary. */
 size_t relation_linear_bwd_workspace_bytes(const rel_problem* p);
 rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
                                const float* g, const void* dout, void* dp1, void* dp2, void* dv, float* dg,

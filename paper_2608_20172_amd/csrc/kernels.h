@@ -149,6 +149,11 @@ struct LinearArgs {
   void* dp2;
   void* dv;
   float* dg;             // [B, H, T, D] fp32, dense
+  // state scans over segments of linear_scan_segment() chunks
+  int nseg;
+  float* segc;           // [N, nseg, D, D]: each segment's forward result from a zero start
+  float* segg;           // [N, nseg, D]: each segment's retention product
+  float* segp;           // [N, nseg, D, D]: each segment's reverse (gradient) result from a zero start
 };
 
 // Measurement aid: if armed for kernel `name`, returns the event pair to record
@@ -164,6 +169,7 @@ hipError_t launch_allocation(const RowArgs& a, int dtype, int N, hipStream_t str
 // of contiguous channels one thread moves; the caller's tensors must allow it
 // (D, D/2 with RoPE, and the strides multiples of vec; pointers aligned to it).
 int linear_chunk();
+int linear_scan_segment();  // chunks per segment of the state scans
 hipError_t launch_linear_fwd(const LinearArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_linear_bwd(const LinearArgs& a, int dtype, hipStream_t stream);
 int decode_slice_keys();

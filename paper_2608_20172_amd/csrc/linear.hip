@@ -14,6 +14,7 @@
 // per head the scan over chunks (the state entering every chunk); per chunk the
 // output. All arithmetic is fp32 on the vector units.
 #include "kernels.h"
+#include "lanes.h"
 
 namespace rel {
 
@@ -23,6 +24,9 @@ constexpr int kL = 64;      // tokens per chunk
 constexpr int kLT = 256;    // threads per workgroup of the state kernels
 constexpr int kTPR = 8;     // threads per token row in the output and gradient kernels
 constexpr int kLT2 = kL * kTPR;
+constexpr int kTPRG = 16;   // threads per token row in the gradient kernel
+constexpr int kLTG = kL * kTPRG;
+constexpr int kRowsPerWave = 64 / kTPRG;
 
 struct ChunkPos {
   int n, c, t0, len;  // head, chunk, first token, valid tokens
@@ -145,21 +149,83 @@ __global__ __launch_bounds__(kLT) void linear_state_kernel(LinearArgs a) {
     for (int j = 0; j < TE; ++j) dC[(a0 + i) * D + e0 + j] = acc[i][j];
 }
 
-// Per head and state entry: C entering chunk c, C_0 = 0, C_{c+1} = gamma_c C_c + dC_c.
-__global__ __launch_bounds__(256) void linear_scan_kernel(LinearArgs a) {
+// The state scans. Per head and state element, over the chunks c:
+//   forward   C_c = gamma_c C_{c-1} + dstate_c   (cprev_c = C_{c-1}, C_{-1} = 0)
+//   reverse   G_c = gamma_c G_{c+1} + pstate_c   (gout_c = G_{c+1}, G_{nchunks} = 0)
+// with gamma_c per state row. The chunks are cut into segments of kSegChunks so
+// that the grid is wide enough to keep HBM busy: linear_seg_kernel reduces each
+// segment to its retention product and its result from a zero start;
+// linear_seg_apply_kernel folds the summaries of the segments before (forward)
+// or after (reverse) its own into the state entering it, then walks its chunks.
+constexpr int kSegChunks = 16;
+
+__device__ __forceinline__ int seg_begin(const LinearArgs& a, int s) { return s * kSegChunks; }
+__device__ __forceinline__ int seg_end(const LinearArgs& a, int s) { return min(a.nchunks, (s + 1) * kSegChunks); }
+
+__global__ __launch_bounds__(256) void linear_seg_kernel(LinearArgs a, int reverse) {
   const int D = a.D;
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (int64_t)D * D) return;
-  const int n = blockIdx.y;
+  const int s = blockIdx.y, n = blockIdx.z;
   const int ar = (int)(idx / D);
+  const int c0 = seg_begin(a, s), c1 = seg_end(a, s);
+  const int64_t hb = (int64_t)n * a.nchunks;
+  float C = 0.0f, prod = 1.0f;
+#pragma unroll 4
+  for (int c = c0; c < c1; ++c) {
+    const float gm = a.gamma[(hb + c) * D + ar];
+    C = gm * C + a.dstate[(hb + c) * D * D + idx];
+    prod *= gm;
+  }
+  const int64_t sb = (int64_t)n * a.nseg + s;
+  a.segc[sb * D * D + idx] = C;
+  if (idx % D == 0) a.segg[sb * D + ar] = prod;
+  if (reverse) {
+    float G = 0.0f;
+#pragma unroll 4
+    for (int c = c1 - 1; c >= c0; --c) G = a.gamma[(hb + c) * D + ar] * G + a.pstate[(hb + c) * D * D + idx];
+    a.segp[sb * D * D + idx] = G;
+  }
+}
+
+__global__ __launch_bounds__(256) void linear_seg_apply_kernel(LinearArgs a, int reverse) {
+  const int D = a.D;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)D * D) return;
+  const int s = blockIdx.y, n = blockIdx.z;
+  const int ar = (int)(idx / D);
+  const int c0 = seg_begin(a, s), c1 = seg_end(a, s);
+  const int64_t hb = (int64_t)n * a.nchunks, sh = (int64_t)n * a.nseg;
   float C = 0.0f;
 #pragma unroll 4
-  for (int c = 0; c < a.nchunks; ++c) {
-    const int64_t base = (int64_t)n * a.nchunks + c;
-    a.cprev[base * D * D + idx] = C;
-    C = a.gamma[base * D + ar] * C + a.dstate[base * D * D + idx];
+  for (int u = 0; u < s; ++u) C = a.segg[(sh + u) * D + ar] * C + a.segc[(sh + u) * D * D + idx];
+#pragma unroll 4
+  for (int c = c0; c < c1; ++c) {
+    a.cprev[(hb + c) * D * D + idx] = C;
+    C = a.gamma[(hb + c) * D + ar] * C + a.dstate[(hb + c) * D * D + idx];
   }
-  if (a.state_out) a.state_out[(int64_t)n * D * D + idx] = C;
+  if (a.state_out && s == a.nseg - 1) a.state_out[(int64_t)n * D * D + idx] = C;
+  if (reverse) {
+    float G = 0.0f;
+#pragma unroll 4
+    for (int u = a.nseg - 1; u > s; --u) G = a.segg[(sh + u) * D + ar] * G + a.segp[(sh + u) * D * D + idx];
+#pragma unroll 4
+    for (int c = c1 - 1; c >= c0; --c) {
+      a.gout[(hb + c) * D * D + idx] = G;
+      G = a.gamma[(hb + c) * D + ar] * G + a.pstate[(hb + c) * D * D + idx];
+    }
+  }
+}
+
+hipError_t launch_state_scan(const LinearArgs& a, int reverse, hipStream_t stream) {
+  const dim3 grid((unsigned)((a.D * a.D + 255) / 256), (unsigned)a.nseg, (unsigned)(a.B * a.H));
+  if (a.nseg > 1) {
+    hipLaunchKernelGGL(linear_seg_kernel, grid, dim3(256), 0, stream, a, reverse);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(linear_seg_apply_kernel, grid, dim3(256), 0, stream, a, reverse);
+  return hipGetLastError();
 }
 
 // Per chunk: Y_t = v_t + intra + inter (see the top of the file).
@@ -307,50 +373,30 @@ __global__ __launch_bounds__(kLT) void linear_bstate_kernel(LinearArgs a) {
     }
 }
 
-// Per head and state entry: C entering every chunk (forward), and the gradient
-// of the state leaving every chunk (backward): G_last = 0, G_{c-1} = gamma_c G_c + P_c.
-__global__ __launch_bounds__(256) void linear_bscan_kernel(LinearArgs a) {
-  const int D = a.D;
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (int64_t)D * D) return;
-  const int n = blockIdx.y;
-  const int ar = (int)(idx / D);
-  float C = 0.0f;
-#pragma unroll 4
-  for (int c = 0; c < a.nchunks; ++c) {
-    const int64_t base = (int64_t)n * a.nchunks + c;
-    a.cprev[base * D * D + idx] = C;
-    C = a.gamma[base * D + ar] * C + a.dstate[base * D * D + idx];
-  }
-  float G = 0.0f;
-#pragma unroll 4
-  for (int c = a.nchunks - 1; c >= 0; --c) {
-    const int64_t base = (int64_t)n * a.nchunks + c;
-    a.gout[base * D * D + idx] = G;
-    G = a.gamma[base * D + ar] * G + a.pstate[base * D * D + idx];
-  }
-}
-
-// Per chunk: every input gradient. Thread (row r = tid / kTPR, part Q of the
-// channels) keeps its row's gradients for the channels of Q in registers.
+// Per chunk: every input gradient. Thread (row r = tid / kTPRG, part Q of the
+// channels) keeps its row's gradients for the channels of Q in registers. A
+// wave holds kRowsPerWave consecutive rows, so the triangular loops below end
+// (phase I) or start (phase II) at a wave-uniform row, and a wave's two
+// phases together always walk about kL rows.
 template <typename TI, int D>
-__global__ __launch_bounds__(kLT2) void linear_grad_kernel(LinearArgs a) {
+__global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
   static_assert(D <= 64, "the backward kernel keeps the chunk of D <= 64 channels in LDS");
   __shared__ float qt[kL][D], kt[kL][D], vv[kL][D], bb[kL][D], dy[kL][D], dbs[kL][D], tmp[kL][D];
   __shared__ float M1[kL][kL + 1], M2[kL][kL + 1];  // A, dA; then C0 and G
   __shared__ float Srow[kL];
-  constexpr int QW = D / kTPR;  // channels per thread
+  constexpr int QW = D / kTPRG;  // channels per thread
   const ChunkPos p = chunk_pos(a);
-  load_chunk<TI, D, kLT2>(a, p, qt, kt, vv, bb, Srow);
+  load_chunk<TI, D, kLTG>(a, p, qt, kt, vv, bb, Srow);
   const int tid = threadIdx.x;
   const int b = p.n / a.H, h = p.n % a.H;
   const int64_t hoff = (int64_t)b * a.sb + (int64_t)h * a.sh;
-  for (int i = tid; i < kL * D; i += kLT2) {
+  for (int i = tid; i < kL * D; i += kLTG) {
     const int r = i / D, d = i % D;
     dy[r][d] = r < p.len ? Elem<TI>::load((const TI*)a.dy + hoff + (int64_t)(p.t0 + r) * a.st + d) : 0.0f;
   }
   __syncthreads();
-  const int r = tid / kTPR, q0 = (tid % kTPR) * QW;
+  const int r = tid / kTPRG, q0 = (tid % kTPRG) * QW;
+  const int wrow = (tid >> 6) * kRowsPerWave;  // first row of this wave
   float dq[QW], dk[QW], dv[QW], db[QW];
 #pragma unroll
   for (int i = 0; i < QW; ++i) {
@@ -367,27 +413,32 @@ __global__ __launch_bounds__(kLT2) void linear_grad_kernel(LinearArgs a) {
     qself[i] = qt[r][q0 + i];
     bsr[i] = bb[r][q0 + i];
   }
-#pragma unroll 2
-  for (int j = 0; j < kL; ++j) {
-    float pa = 0.0f, pd = 0.0f;
-    if (j < r) {
+  // j < r holds for some row of the wave iff j < wrow + kRowsPerWave - 1; the
+  // loop runs in pairs of j (the last one may be past every row: zeros)
+  for (int j0 = 0; j0 < wrow + kRowsPerWave; j0 += 2) {
 #pragma unroll
-      for (int i = 0; i < QW; ++i) pd = __builtin_fmaf(yself[i], vv[j][q0 + i], pd);
-    }
-    for (int o = 1; o < kTPR; o <<= 1) pd += __shfl_xor(pd, o, 64);  // dA[r][j] over all channels
-    if (j < r) {
+    for (int u = 0; u < 2; ++u) {
+      const int j = j0 + u;
+      float pa = 0.0f, pd = 0.0f;
+      if (j < r) {
 #pragma unroll
-      for (int i = 0; i < QW; ++i) {
-        const int d = q0 + i;
-        const float w = kt[j][d] * fast_exp2((bsr[i] - bb[j][d]) * kLog2e);
-        pa = __builtin_fmaf(qself[i], w, pa);
-        dq[i] = __builtin_fmaf(pd, w, dq[i]);
+        for (int i = 0; i < QW; ++i) pd = __builtin_fmaf(yself[i], vv[j][q0 + i], pd);
       }
-    }
-    for (int o = 1; o < kTPR; o <<= 1) pa += __shfl_xor(pa, o, 64);
-    if (tid % kTPR == 0) {
-      M1[r][j] = j < r ? pa : 0.0f;
-      M2[r][j] = j < r ? pd : 0.0f;
+      pd = group_sum<kTPRG>(pd);  // dA[r][j] over all channels
+      if (j < r) {
+#pragma unroll
+        for (int i = 0; i < QW; ++i) {
+          const int d = q0 + i;
+          const float w = kt[j][d] * fast_exp2((bsr[i] - bb[j][d]) * kLog2e);
+          pa = __builtin_fmaf(qself[i], w, pa);
+          dq[i] = __builtin_fmaf(pd, w, dq[i]);
+        }
+      }
+      pa = group_sum<kTPRG>(pa);
+      if (tid % kTPRG == 0) {
+        M1[r][j] = j < r ? pa : 0.0f;
+        M2[r][j] = j < r ? pd : 0.0f;
+      }
     }
   }
 #pragma unroll
@@ -399,7 +450,7 @@ __global__ __launch_bounds__(kLT2) void linear_grad_kernel(LinearArgs a) {
 #pragma unroll
     for (int i = 0; i < QW; ++i) bself[i] = bb[r][q0 + i];
 #pragma unroll 2
-    for (int t = 1; t < kL; ++t) {
+    for (int t = wrow + 1; t < kL; ++t) {
       if (t > r) {
         const float At = M1[t][r], dAt = M2[t][r];
 #pragma unroll
@@ -416,7 +467,7 @@ __global__ __launch_bounds__(kLT2) void linear_grad_kernel(LinearArgs a) {
   __syncthreads();
   // Phase III: stage C0 and G over A, dA
   const int64_t base = (int64_t)p.n * a.nchunks + p.c;
-  for (int i = tid; i < D * D; i += kLT2) {
+  for (int i = tid; i < D * D; i += kLTG) {
     M1[i / D][i % D] = a.cprev[base * D * D + i];
     M2[i / D][i % D] = a.gout[base * D * D + i];
   }
@@ -485,11 +536,9 @@ __global__ __launch_bounds__(kLT2) void linear_grad_kernel(LinearArgs a) {
     s22 += x2[i] * x2[i];
     s12 += x1[i] * x2[i];
   }
-  for (int o = 1; o < kTPR; o <<= 1) {
-    s11 += __shfl_xor(s11, o, 64);
-    s22 += __shfl_xor(s22, o, 64);
-    s12 += __shfl_xor(s12, o, 64);
-  }
+  s11 = group_sum<kTPRG>(s11);
+  s22 = group_sum<kTPRG>(s22);
+  s12 = group_sum<kTPRG>(s12);
   const float S = Srow[r];
   const float in1 = s11 > 0.0f ? rsqrtf(s11) : 0.0f, in2 = s22 > 0.0f ? rsqrtf(s22) : 0.0f;
   // dS = dqt . ^p1 + dkt . ^p2; ^p . d^p for the projections
@@ -500,11 +549,9 @@ __global__ __launch_bounds__(kLT2) void linear_grad_kernel(LinearArgs a) {
     h1d += x1[i] * in1 * dq[i];
     h2d += x2[i] * in2 * dk[i];
   }
-  for (int o = 1; o < kTPR; o <<= 1) {
-    ds += __shfl_xor(ds, o, 64);
-    h1d += __shfl_xor(h1d, o, 64);
-    h2d += __shfl_xor(h2d, o, 64);
-  }
+  ds = group_sum<kTPRG>(ds);
+  h1d = group_sum<kTPRG>(h1d);
+  h2d = group_sum<kTPRG>(h2d);
   if (ok) {
     const float dU = ds * S * (1.0f - S) * a.scale * a.inv_tau;
     TI* DP1 = (TI*)a.dp1 + hoff + (int64_t)(p.t0 + r) * a.st;
@@ -528,11 +575,9 @@ hipError_t launch_bwd_d(const LinearArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL((linear_bstate_kernel<TI, D>), grid, dim3(kLT), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const dim3 sgrid((unsigned)((D * D + 255) / 256), (unsigned)(a.B * a.H));
-  hipLaunchKernelGGL(linear_bscan_kernel, sgrid, dim3(256), 0, stream, a);
-  e = hipGetLastError();
+  e = launch_state_scan(a, 1, stream);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((linear_grad_kernel<TI, D>), grid, dim3(kLT2), 0, stream, a);
+  hipLaunchKernelGGL((linear_grad_kernel<TI, D>), grid, dim3(kLTG), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -551,9 +596,7 @@ hipError_t launch_fwd_d(const LinearArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL((linear_state_kernel<TI, D>), grid, dim3(kLT), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const dim3 sgrid((unsigned)((D * D + 255) / 256), (unsigned)(a.B * a.H));
-  hipLaunchKernelGGL(linear_scan_kernel, sgrid, dim3(256), 0, stream, a);
-  e = hipGetLastError();
+  e = launch_state_scan(a, 0, stream);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((linear_out_kernel<TI, D>), grid, dim3(kLT2), 0, stream, a);
   return hipGetLastError();
@@ -572,6 +615,7 @@ hipError_t launch_fwd_t(const LinearArgs& a, hipStream_t stream) {
 }  // namespace
 
 int linear_chunk() { return kL; }
+int linear_scan_segment() { return kSegChunks; }
 
 hipError_t launch_linear_fwd(const LinearArgs& a, int dtype, hipStream_t stream) {
   return dtype == 1 ? launch_fwd_t<bf16>(a, stream) : launch_fwd_t<float>(a, stream);

@@ -1092,18 +1092,47 @@ static int linear_chunks(const rel_problem* p) {
   return (int)((p->T + rel::linear_chunk() - 1) / rel::linear_chunk());
 }
 
+static int linear_segments(const rel_problem* p) {
+  return (linear_chunks(p) + rel::linear_scan_segment() - 1) / rel::linear_scan_segment();
+}
+
+// Forward workspace: per chunk its state contribution, retention product and
+// entering state; per segment of chunks the scan summaries. The backward adds
+// per chunk the gradient contribution and the gradient of the leaving state,
+// and per segment the reverse summaries.
 struct LinearPlan {
-  size_t dstate, gamma, cprev, total;
+  size_t dstate, gamma, cprev, segc, segg, total;  // forward
+  size_t pstate, gout, segp, total_bwd;            // backward
 };
 
 static LinearPlan plan_linear(const rel_problem* p) {
   LinearPlan L{};
   const size_t N = (size_t)(p->B * p->H), nc = (size_t)linear_chunks(p), D = (size_t)p->D;
+  const size_t ns = (size_t)linear_segments(p);
   L.dstate = 0;
   L.gamma = align256(N * nc * D * D * 4);
   L.cprev = L.gamma + align256(N * nc * D * 4);
-  L.total = L.cprev + align256(N * nc * D * D * 4);
+  L.segc = L.cprev + align256(N * nc * D * D * 4);
+  L.segg = L.segc + align256(N * ns * D * D * 4);
+  L.total = L.segg + align256(N * ns * D * 4);
+  L.pstate = L.total;
+  L.gout = L.pstate + align256(N * nc * D * D * 4);
+  L.segp = L.gout + align256(N * nc * D * D * 4);
+  L.total_bwd = L.segp + align256(N * ns * D * D * 4);
   return L;
+}
+
+static void set_linear_workspace(rel::LinearArgs& a, const LinearPlan& L, char* ws, bool backward) {
+  a.dstate = (float*)(ws + L.dstate);
+  a.gamma = (float*)(ws + L.gamma);
+  a.cprev = (float*)(ws + L.cprev);
+  a.segc = (float*)(ws + L.segc);
+  a.segg = (float*)(ws + L.segg);
+  if (backward) {
+    a.pstate = (float*)(ws + L.pstate);
+    a.gout = (float*)(ws + L.gout);
+    a.segp = (float*)(ws + L.segp);
+  }
 }
 
 size_t relation_linear_fwd_workspace_bytes(const rel_problem* p) {
@@ -1148,10 +1177,8 @@ rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void*
   a.scale = eff_scale(p);
   a.inv_tau = 1.0f / p->tau_s;
   a.nchunks = linear_chunks(p);
-  char* ws = (char*)workspace;
-  a.dstate = (float*)(ws + L.dstate);
-  a.gamma = (float*)(ws + L.gamma);
-  a.cprev = (float*)(ws + L.cprev);
+  a.nseg = linear_segments(p);
+  set_linear_workspace(a, L, (char*)workspace, false);
   const hipError_t e = rel::launch_linear_fwd(a, p->dtype, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "Linear Relation launch");
   return REL_OK;
@@ -1160,8 +1187,7 @@ rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void*
 size_t relation_linear_bwd_workspace_bytes(const rel_problem* p) {
   bool empty = false;
   if (check_linear(p, &empty) != REL_OK || empty || p->D > 64) return 0;
-  const size_t N = (size_t)(p->B * p->H), nc = (size_t)linear_chunks(p), D = (size_t)p->D;
-  return plan_linear(p).total + 2 * align256(N * nc * D * D * 4);
+  return plan_linear(p).total_bwd;
 }
 
 rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
@@ -1203,7 +1229,6 @@ rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void*
                             {workspace, need, false, true, "workspace"}}));
   if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected by RELATION_TEST_FAIL_LAUNCH");
   const LinearPlan L = plan_linear(p);
-  const size_t nc = (size_t)linear_chunks(p), D = (size_t)p->D;
   rel::LinearArgs a{};
   a.p1 = p1; a.p2 = p2; a.v = v; a.g = g; a.dy = dout;
   a.dp1 = dp1; a.dp2 = dp2; a.dv = dv; a.dg = dg;
@@ -1211,13 +1236,9 @@ rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void*
   a.B = (int)p->B; a.H = (int)p->H; a.T = (int)p->T; a.D = (int)p->D;
   a.scale = eff_scale(p);
   a.inv_tau = 1.0f / p->tau_s;
-  a.nchunks = (int)nc;
-  char* ws = (char*)workspace;
-  a.dstate = (float*)(ws + L.dstate);
-  a.gamma = (float*)(ws + L.gamma);
-  a.cprev = (float*)(ws + L.cprev);
-  a.pstate = (float*)(ws + L.total);
-  a.gout = (float*)(ws + L.total + align256(N * nc * D * D * 4));
+  a.nchunks = linear_chunks(p);
+  a.nseg = linear_segments(p);
+  set_linear_workspace(a, L, (char*)workspace, true);
   const hipError_t e = rel::launch_linear_bwd(a, p->dtype, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "Linear Relation backward launch");
   return REL_OK;

@@ -78,6 +78,15 @@ def test_linear_forward_long():
     check_linear_fwd(x, "bf16", heads=[(0, 0), (0, 3)])
 
 
+@pytest.mark.parametrize("T,gmax", [(1024, 0.02), (1025, 0.02), (3000, 0.005), (3000, 2.0)])
+def test_linear_forward_scan_segments(T, gmax):
+    """The state scan works over segments of 16 chunks (1024 tokens): one full
+    segment, one plus a one-token chunk, and three with a ragged last chunk,
+    with slow retention so that the state crosses segment boundaries."""
+    x = _prep(1, 2, T, 64, "f32", seed=1250 + T, gmax=gmax)
+    check_linear_fwd(x, "f32")
+
+
 def test_linear_forward_strided():
     x = _prep(2, 3, 150, 64, "bf16", seed=1300)
     a = R.relation_linear_fwd(x["p1"], x["p2"], x["v"], x["g"])
@@ -118,6 +127,13 @@ def test_linear_backward_retention_range(gmax):
 def test_linear_backward_long():
     x = _prep(1, 2, 2048, 64, "bf16", seed=1600, gmax=0.05)
     check_linear_bwd(x, "bf16", heads=[(0, 1)])
+
+
+@pytest.mark.parametrize("T,gmax", [(1025, 0.02), (3000, 0.005)])
+def test_linear_backward_scan_segments(T, gmax):
+    """Forward and reverse state scans across segments of 16 chunks."""
+    x = _prep(1, 1, T, 64, "f32", seed=1650 + T, gmax=gmax)
+    check_linear_bwd(x, "f32")
 
 
 def test_linear_backward_repeatable():
