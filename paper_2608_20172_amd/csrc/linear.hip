@@ -42,42 +42,67 @@ __device__ __forceinline__ ChunkPos chunk_pos(const LinearArgs& a) {
 }
 
 // Loads the chunk into LDS as fp32 and forms qt = S ^p1, kt = S ^p2 (rows past
-// the sequence are zero), v, and b = running sum of g (zero g past the end, so
-// b stays at its last value). One wave per row for the norms and S.
-template <typename TI, int D, int NT>
+// the sequence are zero), v, optionally dY, and b = running sum of g (zero g
+// past the end, so b stays at its last value). One wave per row for the norms
+// and S; a wave's rows are a fixed-count loop, so all of its loads are in
+// flight together.
+// Column of element (r, c) of a row-major [kL][D] array stored with its
+// 16-byte chunks XOR-swizzled by row: rows read together at one column (lanes
+// over rows) then hit different banks, and four consecutive columns from a
+// multiple of 4 stay one aligned 16-byte chunk.
+template <int D>
+__device__ __forceinline__ int swz(int r, int c) {
+  return (((c >> 2) ^ (r & (D / 4 - 1))) << 2) | (c & 3);
+}
+
+template <typename TI, int D, int NT, bool SWZ = false>
 __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& p, float (*qt)[D], float (*kt)[D],
-                                           float (*vv)[D], float (*bb)[D], float* Srow) {
+                                           float (*vv)[D], float (*bb)[D], float* Srow,
+                                           float (*dyl)[D] = nullptr) {
+  static_assert(NT % 64 == 0 && kL % (NT / 64) == 0 && NT % D == 0, "rows and channels split evenly");
+  constexpr int RPW = kL / (NT / 64);  // rows per wave
+  constexpr int U = (D + 63) / 64;     // channels per lane
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int b = p.n / a.H, h = p.n % a.H;
   const int64_t hoff = (int64_t)b * a.sb + (int64_t)h * a.sh;
   const TI* P1 = (const TI*)a.p1 + hoff;
   const TI* P2 = (const TI*)a.p2 + hoff;
   const TI* V = (const TI*)a.v + hoff;
+  const TI* DY = dyl ? (const TI*)a.dy + hoff : nullptr;
   const float* G = a.g + (int64_t)p.n * a.T * D;
-  for (int r = w; r < kL; r += NT / 64) {
+#pragma unroll
+  for (int k = 0; k < RPW; ++k) {
+    const int r = w + k * (NT / 64);
     const bool ok = r < p.len;
     const int64_t row = (int64_t)(p.t0 + r);
-    float x1[2] = {0.0f, 0.0f}, x2[2] = {0.0f, 0.0f};
+    float x1[U], x2[U];
     float s11 = 0.0f, s22 = 0.0f, s12 = 0.0f;
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < U; ++u) {
       const int d = lane + 64 * u;
+      x1[u] = x2[u] = 0.0f;
       if (d < D) {
-        float vx = 0.0f, gx = 0.0f;
+        float vx = 0.0f, gx = 0.0f, dx = 0.0f;
         if (ok) {
           x1[u] = Elem<TI>::load(P1 + row * a.st + d);
           x2[u] = Elem<TI>::load(P2 + row * a.st + d);
           vx = Elem<TI>::load(V + row * a.st + d);
           gx = G[row * D + d];
+          if (dyl) dx = Elem<TI>::load(DY + row * a.st + d);
         }
-        vv[r][d] = vx;
+        const int ds = SWZ ? swz<D>(r, d) : d;
+        vv[r][ds] = vx;
         bb[r][d] = gx;
+        if (dyl) dyl[r][ds] = dx;
         s11 += x1[u] * x1[u];
         s22 += x2[u] * x2[u];
         s12 += x1[u] * x2[u];
       }
     }
-    for (int o = 32; o >= 1; o >>= 1) {
+    s11 = group_sum<16>(s11);
+    s22 = group_sum<16>(s22);
+    s12 = group_sum<16>(s12);
+    for (int o = 16; o <= 32; o <<= 1) {
       s11 += __shfl_xor(s11, o, 64);
       s22 += __shfl_xor(s22, o, 64);
       s12 += __shfl_xor(s12, o, 64);
@@ -86,7 +111,7 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
     const float i1 = ok && s11 > 0.0f ? S * rsqrtf(s11) : 0.0f;
     const float i2 = ok && s22 > 0.0f ? S * rsqrtf(s22) : 0.0f;
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < U; ++u) {
       const int d = lane + 64 * u;
       if (d < D) {
         qt[r][d] = x1[u] * i1;
@@ -96,12 +121,25 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
     if (lane == 0 && Srow) Srow[r] = S;
   }
   __syncthreads();
-  if (tid < D) {  // running sum of g down the chunk, one channel per thread
-    float acc = 0.0f;
-    for (int r = 0; r < kL; ++r) {
-      acc += bb[r][tid];
-      bb[r][tid] = acc;
-    }
+  // running sum of g down the chunk: thread (channel, segment of SR rows) sums
+  // its segment in place, then adds the totals of the segments above it
+  constexpr int NSEG = NT / D, SR = kL / NSEG;
+  const int d = tid % D, sg = tid / D;
+  float x[SR];
+  float acc = 0.0f;
+#pragma unroll
+  for (int i = 0; i < SR; ++i) x[i] = bb[sg * SR + i][d];
+#pragma unroll
+  for (int i = 0; i < SR; ++i) x[i] = acc += x[i];
+#pragma unroll
+  for (int i = 0; i < SR; ++i) bb[sg * SR + i][d] = x[i];
+  __syncthreads();
+  float off = 0.0f;
+  for (int u = 0; u < sg; ++u) off += bb[u * SR + SR - 1][d];
+  __syncthreads();  // every segment total read
+  if (sg > 0) {
+#pragma unroll
+    for (int i = 0; i < SR; ++i) bb[sg * SR + i][d] = x[i] + off;
   }
   __syncthreads();
 }
@@ -159,7 +197,7 @@ __global__ __launch_bounds__(kLT) void linear_state_kernel(LinearArgs a) {
 // or after (reverse) its own into the state entering it, then walks its chunks.
 constexpr int kSegChunks = 16;
 
-__device__ __forceinline__ int seg_begin(const LinearArgs& a, int s) { return s * kSegChunks; }
+__device__ __forceinline__ int seg_begin(int s) { return s * kSegChunks; }
 __device__ __forceinline__ int seg_end(const LinearArgs& a, int s) { return min(a.nchunks, (s + 1) * kSegChunks); }
 
 __global__ __launch_bounds__(256) void linear_seg_kernel(LinearArgs a, int reverse) {
@@ -168,7 +206,7 @@ __global__ __launch_bounds__(256) void linear_seg_kernel(LinearArgs a, int rever
   if (idx >= (int64_t)D * D) return;
   const int s = blockIdx.y, n = blockIdx.z;
   const int ar = (int)(idx / D);
-  const int c0 = seg_begin(a, s), c1 = seg_end(a, s);
+  const int c0 = seg_begin(s), c1 = seg_end(a, s);
   const int64_t hb = (int64_t)n * a.nchunks;
   float C = 0.0f, prod = 1.0f;
 #pragma unroll 4
@@ -194,7 +232,7 @@ __global__ __launch_bounds__(256) void linear_seg_apply_kernel(LinearArgs a, int
   if (idx >= (int64_t)D * D) return;
   const int s = blockIdx.y, n = blockIdx.z;
   const int ar = (int)(idx / D);
-  const int c0 = seg_begin(a, s), c1 = seg_end(a, s);
+  const int c0 = seg_begin(s), c1 = seg_end(a, s);
   const int64_t hb = (int64_t)n * a.nchunks, sh = (int64_t)n * a.nseg;
   float C = 0.0f;
 #pragma unroll 4
@@ -318,17 +356,12 @@ template <typename TI, int D>
 __global__ __launch_bounds__(kLT) void linear_bstate_kernel(LinearArgs a) {
   __shared__ float qt[kL][D], kt[kL][D], vv[kL][D], bb[kL][D], dy[kL][D];
   const ChunkPos p = chunk_pos(a);
-  load_chunk<TI, D, kLT>(a, p, qt, kt, vv, bb, nullptr);
+  load_chunk<TI, D, kLT>(a, p, qt, kt, vv, bb, nullptr, dy);
   const int tid = threadIdx.x;
-  {
-    const int b = p.n / a.H, h = p.n % a.H;
-    const TI* DY = (const TI*)a.dy + (int64_t)b * a.sb + (int64_t)h * a.sh;
-    for (int i = tid; i < kL * D; i += kLT) {
-      const int r = i / D, d = i % D;
-      dy[r][d] = r < p.len ? Elem<TI>::load(DY + (int64_t)(p.t0 + r) * a.st + d) : 0.0f;
-      kt[r][d] *= fast_exp2((bb[kL - 1][d] - bb[r][d]) * kLog2e);
-      qt[r][d] *= fast_exp2(bb[r][d] * kLog2e);
-    }
+  for (int i = tid; i < kL * D; i += kLT) {
+    const int r = i / D, d = i % D;
+    kt[r][d] *= fast_exp2((bb[kL - 1][d] - bb[r][d]) * kLog2e);
+    qt[r][d] *= fast_exp2(bb[r][d] * kLog2e);
   }
   __syncthreads();
   const int64_t base = ((int64_t)p.n * a.nchunks + p.c);
@@ -373,56 +406,97 @@ __global__ __launch_bounds__(kLT) void linear_bstate_kernel(LinearArgs a) {
     }
 }
 
+// One 32 x 32 block (rows rb.., columns cb..) of a kL x D product whose
+// contraction runs over D, on the matrix cores (32x32x2 fp32 steps). The row
+// operand X is a swizzled [kL][D] array; the column operand is B(k, j) of
+// the product. Lane group g takes the contraction indices D/2 g .. D/2 g + D/2 - 1
+// in order, four per 16-byte read of its row.
+template <int D, typename ColOp>
+__device__ __forceinline__ floatx16 block_product(const float (*X)[D], int rb, int cb, ColOp B) {
+  constexpr int KH = D / 2;
+  const int lane = threadIdx.x & 63, ln = lane & 31, lg = lane >> 5;
+  const int xr = rb + ln;
+  floatx16 acc;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
+#pragma unroll 2
+  for (int s0 = 0; s0 < KH; s0 += 4) {
+    const int kk = KH * lg + s0;
+    const floatx4 xa = *reinterpret_cast<const floatx4*>(&X[xr][swz<D>(xr, kk)]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc = mfma32f(xa[u], B(kk + u, cb + ln), acc);
+  }
+  return acc;
+}
+
 // Per chunk: every input gradient. Thread (row r = tid / kTPRG, part Q of the
 // channels) keeps its row's gradients for the channels of Q in registers. A
-// wave holds kRowsPerWave consecutive rows, so the triangular loops below end
-// (phase I) or start (phase II) at a wave-uniform row, and a wave's two
-// phases together always walk about kL rows.
+// wave holds kRowsPerWave consecutive rows, so the triangular loops of the
+// intra-chunk phases end (phase I) or start (phase II) at a wave-uniform row,
+// and a wave's two phases together always walk about kL rows. The three
+// inter-chunk products are dense (kL x D by D x D) and run on the matrix
+// cores, one 32 x 32 block per wave.
 template <typename TI, int D>
 __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
-  static_assert(D <= 64, "the backward kernel keeps the chunk of D <= 64 channels in LDS");
+  static_assert(D == 32 || D == 64, "the backward kernel keeps the chunk of D <= 64 channels in LDS");
+  // vv, dy (and tmp while it holds Kd) are swizzled (swz): they are row
+  // operands of the matrix-core products
   __shared__ float qt[kL][D], kt[kL][D], vv[kL][D], bb[kL][D], dy[kL][D], dbs[kL][D], tmp[kL][D];
-  __shared__ float M1[kL][kL + 1], M2[kL][kL + 1];  // A, dA; then C0 and G
+  // AD: A[t][j] at [t][j] and dA[t][j] at [j][t] for j < t; then G. C0s: C0.
+  __shared__ float AD[kL][kL + 1], C0s[kL][kL + 1];
   __shared__ float Srow[kL];
   constexpr int QW = D / kTPRG;  // channels per thread
+  constexpr int NCG = D * D / kLTG;  // elements of C0 and of G per thread
+  static_assert(D * D % kLTG == 0, "C0 and G split evenly over the threads");
   const ChunkPos p = chunk_pos(a);
-  load_chunk<TI, D, kLTG>(a, p, qt, kt, vv, bb, Srow);
   const int tid = threadIdx.x;
+  // C0 and G are read from HBM now and reach LDS later, so that their latency
+  // hides behind the chunk's load and the intra-chunk phases
+  const int64_t base = (int64_t)p.n * a.nchunks + p.c;
+  float c0r[NCG], gr[NCG];
+#pragma unroll
+  for (int k = 0; k < NCG; ++k) {
+    c0r[k] = a.cprev[base * D * D + tid + k * kLTG];
+    gr[k] = a.gout[base * D * D + tid + k * kLTG];
+  }
+  load_chunk<TI, D, kLTG, true>(a, p, qt, kt, vv, bb, Srow, dy);
+#pragma unroll
+  for (int k = 0; k < NCG; ++k) {
+    const int i = tid + k * kLTG;
+    C0s[i / D][i % D] = c0r[k];  // read after the barrier that ends phase II
+  }
   const int b = p.n / a.H, h = p.n % a.H;
   const int64_t hoff = (int64_t)b * a.sb + (int64_t)h * a.sh;
-  for (int i = tid; i < kL * D; i += kLTG) {
-    const int r = i / D, d = i % D;
-    dy[r][d] = r < p.len ? Elem<TI>::load((const TI*)a.dy + hoff + (int64_t)(p.t0 + r) * a.st + d) : 0.0f;
-  }
-  __syncthreads();
   const int r = tid / kTPRG, q0 = (tid % kTPRG) * QW;
+  const int qs = swz<D>(r, q0);                // this thread's channels in a swizzled row r
   const int wrow = (tid >> 6) * kRowsPerWave;  // first row of this wave
   float dq[QW], dk[QW], dv[QW], db[QW];
 #pragma unroll
   for (int i = 0; i < QW; ++i) {
     dq[i] = 0.0f;
     dk[i] = 0.0f;
-    dv[i] = dy[r][q0 + i];  // Y = I~ + E
+    dv[i] = dy[r][qs + i];  // Y = I~ + E
     db[i] = 0.0f;
   }
   // Phase I (row r as t): A[r][j], dA[r][j] for j < r; dqt_intra
   float yself[QW], qself[QW], bsr[QW];
 #pragma unroll
   for (int i = 0; i < QW; ++i) {
-    yself[i] = dy[r][q0 + i];
+    yself[i] = dy[r][qs + i];
     qself[i] = qt[r][q0 + i];
     bsr[i] = bb[r][q0 + i];
   }
   // j < r holds for some row of the wave iff j < wrow + kRowsPerWave - 1; the
-  // loop runs in pairs of j (the last one may be past every row: zeros)
+  // loop runs in pairs of j (the last one may be past every row)
   for (int j0 = 0; j0 < wrow + kRowsPerWave; j0 += 2) {
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int j = j0 + u;
       float pa = 0.0f, pd = 0.0f;
       if (j < r) {
+        const int js = swz<D>(j, q0);
 #pragma unroll
-        for (int i = 0; i < QW; ++i) pd = __builtin_fmaf(yself[i], vv[j][q0 + i], pd);
+        for (int i = 0; i < QW; ++i) pd = __builtin_fmaf(yself[i], vv[j][js + i], pd);
       }
       pd = group_sum<kTPRG>(pd);  // dA[r][j] over all channels
       if (j < r) {
@@ -435,9 +509,9 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
         }
       }
       pa = group_sum<kTPRG>(pa);
-      if (tid % kTPRG == 0) {
-        M1[r][j] = j < r ? pa : 0.0f;
-        M2[r][j] = j < r ? pd : 0.0f;
+      if (tid % kTPRG == 0 && j < r) {
+        AD[r][j] = pa;
+        AD[j][r] = pd;
       }
     }
   }
@@ -452,59 +526,77 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
 #pragma unroll 2
     for (int t = wrow + 1; t < kL; ++t) {
       if (t > r) {
-        const float At = M1[t][r], dAt = M2[t][r];
+        const float At = AD[t][r], dAt = AD[r][t];
+        const int ts = swz<D>(t, q0);
 #pragma unroll
         for (int i = 0; i < QW; ++i) {
           const int d = q0 + i;
-          dv[i] = __builtin_fmaf(At, dy[t][d], dv[i]);
+          dv[i] = __builtin_fmaf(At, dy[t][ts + i], dv[i]);
           dk[i] = __builtin_fmaf(dAt * qt[t][d], fast_exp2((bb[t][d] - bself[i]) * kLog2e), dk[i]);
         }
       }
     }
   }
-#pragma unroll
-  for (int i = 0; i < QW; ++i) db[i] -= kt[r][q0 + i] * dk[i];
-  __syncthreads();
-  // Phase III: stage C0 and G over A, dA
-  const int64_t base = (int64_t)p.n * a.nchunks + p.c;
-  for (int i = tid; i < D * D; i += kLTG) {
-    M1[i / D][i % D] = a.cprev[base * D * D + i];
-    M2[i / D][i % D] = a.gout[base * D * D + i];
-  }
-  __syncthreads();
-  // inter read: dQe[r][d] = sum_e dY[r][e] C0[d][e]; write: dKd[r][d] = sum_e v[r][e] G[d][e]
-  float dqe_[QW], dkd_[QW];
-#pragma unroll
-  for (int i = 0; i < QW; ++i) dqe_[i] = dkd_[i] = 0.0f;
-#pragma unroll 2
-  for (int ee = 0; ee < D; ++ee) {
-    const int e = (ee + r) & (D - 1);  // skewed per row: the rows of a wave read distinct banks
-    const float ye = dy[r][e], ve = vv[r][e];
-#pragma unroll
-    for (int i = 0; i < QW; ++i) {
-      dqe_[i] = __builtin_fmaf(ye, M1[q0 + i][e], dqe_[i]);
-      dkd_[i] = __builtin_fmaf(ve, M2[q0 + i][e], dkd_[i]);
-    }
-  }
+  // Kd = kt e^{b_last - b}: the row operand of dV += Kd G, to tmp
+  float ek[QW], kd[QW];
 #pragma unroll
   for (int i = 0; i < QW; ++i) {
     const int d = q0 + i;
-    const float dqe = dqe_[i], dkd = dkd_[i];
-    const float eb = fast_exp2(bb[r][d] * kLog2e);
-    const float ek = fast_exp2((bb[kL - 1][d] - bb[r][d]) * kLog2e);
-    dq[i] = __builtin_fmaf(dqe, eb, dq[i]);
-    dk[i] = __builtin_fmaf(dkd, ek, dk[i]);
-    const float kd = kt[r][d] * ek;
-    db[i] += dqe * qt[r][d] * eb - dkd * kd;
-    tmp[r][d] = dkd * kd;  // its column sum goes to the chunk's last row
+    db[i] -= kt[r][d] * dk[i];
+    ek[i] = fast_exp2((bb[kL - 1][d] - bb[r][d]) * kLog2e);
+    kd[i] = kt[r][d] * ek[i];
+    tmp[r][qs + i] = kd[i];
   }
-  // dv += Kd G: dv[r][e] += sum_d Kd[r][d] G[d][e]
-#pragma unroll 2
-  for (int dd = 0; dd < D; ++dd) {
-    const int d = (dd + r) & (D - 1);
-    const float kd = kt[r][d] * fast_exp2((bb[kL - 1][d] - bb[r][d]) * kLog2e);
+  __syncthreads();
+  // G over A, dA
 #pragma unroll
-    for (int i = 0; i < QW; ++i) dv[i] = __builtin_fmaf(kd, M2[d][q0 + i], dv[i]);
+  for (int k = 0; k < NCG; ++k) {
+    const int i = tid + k * kLTG;
+    AD[i / D][i % D] = gr[k];
+  }
+  // p1 and p2 of this thread's row and channels, for the last step
+  const TI* P1 = (const TI*)a.p1 + hoff + (int64_t)(p.t0 + r) * a.st;
+  const TI* P2 = (const TI*)a.p2 + hoff + (int64_t)(p.t0 + r) * a.st;
+  const bool ok = r < p.len;
+  float x1[QW], x2[QW];
+#pragma unroll
+  for (int i = 0; i < QW; ++i) {
+    x1[i] = ok ? Elem<TI>::load(P1 + q0 + i) : 0.0f;
+    x2[i] = ok ? Elem<TI>::load(P2 + q0 + i) : 0.0f;
+  }
+  __syncthreads();
+  // Phase III, the inter-chunk terms: wave w < 3 NB takes block w % NB of
+  //   product 0: dQe = dY C0^T,  1: dKd = V G^T,  2: dVx = Kd G.
+  constexpr int NBC = D / 32, NB = (kL / 32) * NBC;
+  static_assert(3 * NB <= kLTG / 64, "one block per wave");
+  const int w = tid >> 6, prod = w / NB, blk = w % NB;
+  const int rb = 32 * (blk / NBC), cb = 32 * (blk % NBC);
+  floatx16 acc;
+  if (prod == 0) {
+    acc = block_product<D>(dy, rb, cb, [&](int k, int j) { return C0s[j][k]; });
+  } else if (prod == 1) {
+    acc = block_product<D>(vv, rb, cb, [&](int k, int j) { return AD[j][k]; });
+  } else if (prod == 2) {
+    acc = block_product<D>(tmp, rb, cb, [&](int k, int j) { return AD[k][j]; });
+  }
+  __syncthreads();  // every operand read: dy, vv, dbs take the three results
+  if (prod < 3) {
+    float (*O)[D] = prod == 0 ? dy : prod == 1 ? vv : dbs;
+    const int lane = tid & 63;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) O[rb + acc_row(v, lane >> 5)][cb + (lane & 31)] = acc[v];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < QW; ++i) {
+    const int d = q0 + i;
+    const float dqe = dy[r][d], dkd = vv[r][d];
+    const float eb = fast_exp2(bb[r][d] * kLog2e);
+    dq[i] = __builtin_fmaf(dqe, eb, dq[i]);
+    dk[i] = __builtin_fmaf(dkd, ek[i], dk[i]);
+    dv[i] += dbs[r][d];
+    db[i] += dqe * qt[r][d] * eb - dkd * kd[i];
+    tmp[r][d] = dkd * kd[i];  // its column sum goes to the chunk's last row
   }
 #pragma unroll
   for (int i = 0; i < QW; ++i) dbs[r][q0 + i] = db[i];
@@ -514,24 +606,18 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
     const int d = tid;
     float extra = 0.0f, dgam = 0.0f;
     for (int j = 0; j < kL; ++j) extra += tmp[j][d];
-    for (int e = 0; e < D; ++e) dgam = __builtin_fmaf(M2[d][e], M1[d][e], dgam);
-    float acc = extra + dgam * fast_exp2(bb[kL - 1][d] * kLog2e);
+    for (int e = 0; e < D; ++e) dgam = __builtin_fmaf(AD[d][e], C0s[d][e], dgam);
+    float accg = extra + dgam * fast_exp2(bb[kL - 1][d] * kLog2e);
     float* dG = a.dg + (int64_t)p.n * a.T * D;
     for (int j = kL - 1; j >= 0; --j) {
-      acc += dbs[j][d];
-      if (j < p.len) dG[(int64_t)(p.t0 + j) * D + d] = acc;
+      accg += dbs[j][d];
+      if (j < p.len) dG[(int64_t)(p.t0 + j) * D + d] = accg;
     }
   }
   // through qt = S p1 / |p1|, kt = S p2 / |p2|, S = sigmoid(scale p1 . p2 / tau_S)
-  const TI* P1 = (const TI*)a.p1 + hoff + (int64_t)(p.t0 + r) * a.st;
-  const TI* P2 = (const TI*)a.p2 + hoff + (int64_t)(p.t0 + r) * a.st;
-  const bool ok = r < p.len;
-  float x1[QW], x2[QW];
   float s11 = 0.0f, s22 = 0.0f, s12 = 0.0f;
 #pragma unroll
   for (int i = 0; i < QW; ++i) {
-    x1[i] = ok ? Elem<TI>::load(P1 + q0 + i) : 0.0f;
-    x2[i] = ok ? Elem<TI>::load(P2 + q0 + i) : 0.0f;
     s11 += x1[i] * x1[i];
     s22 += x2[i] * x2[i];
     s12 += x1[i] * x2[i];
