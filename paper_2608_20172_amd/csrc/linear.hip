@@ -41,11 +41,6 @@ __device__ __forceinline__ ChunkPos chunk_pos(const LinearArgs& a) {
   return p;
 }
 
-// Loads the chunk into LDS as fp32 and forms qt = S ^p1, kt = S ^p2 (rows past
-// the sequence are zero), v, optionally dY, and b = running sum of g (zero g
-// past the end, so b stays at its last value). One wave per row for the norms
-// and S; a wave's rows are a fixed-count loop, so all of its loads are in
-// flight together.
 // Column of element (r, c) of a row-major [kL][D] array stored with its
 // 16-byte chunks XOR-swizzled by row: rows read together at one column (lanes
 // over rows) then hit different banks, and four consecutive columns from a
@@ -55,7 +50,11 @@ __device__ __forceinline__ int swz(int r, int c) {
   return (((c >> 2) ^ (r & (D / 4 - 1))) << 2) | (c & 3);
 }
 
-template <typename TI, int D, int NT, bool SWZ = false>
+// Loads the chunk into LDS as fp32 and forms qt = S ^p1, kt = S ^p2 (rows past
+// the sequence are zero), v, optionally dY (v and dY swizzled if SWZ), and
+// b = running sum of g (zero g past the end, so b stays at its last value).
+// One wave per row for the norms and S.
+template <typename TI, int D, int NT, bool SWZ = false, bool WITH_DY = false>
 __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& p, float (*qt)[D], float (*kt)[D],
                                            float (*vv)[D], float (*bb)[D], float* Srow,
                                            float (*dyl)[D] = nullptr) {
@@ -68,57 +67,69 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
   const TI* P1 = (const TI*)a.p1 + hoff;
   const TI* P2 = (const TI*)a.p2 + hoff;
   const TI* V = (const TI*)a.v + hoff;
-  const TI* DY = dyl ? (const TI*)a.dy + hoff : nullptr;
+  const TI* DY = WITH_DY ? (const TI*)a.dy + hoff : nullptr;
   const float* G = a.g + (int64_t)p.n * a.T * D;
+  // rows in batches whose loads are issued together: the loads are
+  // unconditional (rows past the sequence read its last row, then count as
+  // zero) so that the compiler can hoist them over the reductions
+  constexpr int BATCH = RPW < 8 / U ? RPW : 8 / U;
+  static_assert(RPW % BATCH == 0, "whole batches");
+  for (int k0 = 0; k0 < RPW; k0 += BATCH) {
+    float x1[BATCH][U], x2[BATCH][U], vx[BATCH][U], gx[BATCH][U], dx[BATCH][U];
 #pragma unroll
-  for (int k = 0; k < RPW; ++k) {
-    const int r = w + k * (NT / 64);
-    const bool ok = r < p.len;
-    const int64_t row = (int64_t)(p.t0 + r);
-    float x1[U], x2[U];
-    float s11 = 0.0f, s22 = 0.0f, s12 = 0.0f;
+    for (int kb = 0; kb < BATCH; ++kb) {
+      const int r = w + (k0 + kb) * (NT / 64);
+      const int64_t row = (int64_t)min(p.t0 + r, a.T - 1);
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int d = lane + 64 * u;
-      x1[u] = x2[u] = 0.0f;
-      if (d < D) {
-        float vx = 0.0f, gx = 0.0f, dx = 0.0f;
-        if (ok) {
-          x1[u] = Elem<TI>::load(P1 + row * a.st + d);
-          x2[u] = Elem<TI>::load(P2 + row * a.st + d);
-          vx = Elem<TI>::load(V + row * a.st + d);
-          gx = G[row * D + d];
-          if (dyl) dx = Elem<TI>::load(DY + row * a.st + d);
+      for (int u = 0; u < U; ++u) {
+        const int d = min(lane + 64 * u, D - 1);
+        x1[kb][u] = Elem<TI>::load(P1 + row * a.st + d);
+        x2[kb][u] = Elem<TI>::load(P2 + row * a.st + d);
+        vx[kb][u] = Elem<TI>::load(V + row * a.st + d);
+        gx[kb][u] = G[row * D + d];
+        dx[kb][u] = WITH_DY ? Elem<TI>::load(DY + row * a.st + d) : 0.0f;
+      }
+    }
+#pragma unroll
+    for (int kb = 0; kb < BATCH; ++kb) {
+      const int r = w + (k0 + kb) * (NT / 64);
+      const bool ok = r < p.len;
+      float s11 = 0.0f, s22 = 0.0f, s12 = 0.0f;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int d = lane + 64 * u;
+        if (!ok || d >= D) x1[kb][u] = x2[kb][u] = vx[kb][u] = gx[kb][u] = dx[kb][u] = 0.0f;
+        if (d < D) {
+          const int ds = SWZ ? swz<D>(r, d) : d;
+          vv[r][ds] = vx[kb][u];
+          bb[r][d] = gx[kb][u];
+          if constexpr (WITH_DY) dyl[r][ds] = dx[kb][u];
         }
-        const int ds = SWZ ? swz<D>(r, d) : d;
-        vv[r][ds] = vx;
-        bb[r][d] = gx;
-        if (dyl) dyl[r][ds] = dx;
-        s11 += x1[u] * x1[u];
-        s22 += x2[u] * x2[u];
-        s12 += x1[u] * x2[u];
+        s11 += x1[kb][u] * x1[kb][u];
+        s22 += x2[kb][u] * x2[kb][u];
+        s12 += x1[kb][u] * x2[kb][u];
       }
-    }
-    s11 = group_sum<16>(s11);
-    s22 = group_sum<16>(s22);
-    s12 = group_sum<16>(s12);
-    for (int o = 16; o <= 32; o <<= 1) {
-      s11 += __shfl_xor(s11, o, 64);
-      s22 += __shfl_xor(s22, o, 64);
-      s12 += __shfl_xor(s12, o, 64);
-    }
-    const float S = ok ? 1.0f / (1.0f + expf(-s12 * a.scale * a.inv_tau)) : 0.0f;
-    const float i1 = ok && s11 > 0.0f ? S * rsqrtf(s11) : 0.0f;
-    const float i2 = ok && s22 > 0.0f ? S * rsqrtf(s22) : 0.0f;
+      s11 = group_sum<16>(s11);
+      s22 = group_sum<16>(s22);
+      s12 = group_sum<16>(s12);
+      for (int o = 16; o <= 32; o <<= 1) {
+        s11 += __shfl_xor(s11, o, 64);
+        s22 += __shfl_xor(s22, o, 64);
+        s12 += __shfl_xor(s12, o, 64);
+      }
+      const float S = ok ? 1.0f / (1.0f + expf(-s12 * a.scale * a.inv_tau)) : 0.0f;
+      const float i1 = ok && s11 > 0.0f ? S * rsqrtf(s11) : 0.0f;
+      const float i2 = ok && s22 > 0.0f ? S * rsqrtf(s22) : 0.0f;
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int d = lane + 64 * u;
-      if (d < D) {
-        qt[r][d] = x1[u] * i1;
-        kt[r][d] = x2[u] * i2;
+      for (int u = 0; u < U; ++u) {
+        const int d = lane + 64 * u;
+        if (d < D) {
+          qt[r][d] = x1[kb][u] * i1;
+          kt[r][d] = x2[kb][u] * i2;
+        }
       }
+      if (lane == 0 && Srow) Srow[r] = S;
     }
-    if (lane == 0 && Srow) Srow[r] = S;
   }
   __syncthreads();
   // running sum of g down the chunk: thread (channel, segment of SR rows) sums
@@ -266,74 +277,131 @@ hipError_t launch_state_scan(const LinearArgs& a, int reverse, hipStream_t strea
   return hipGetLastError();
 }
 
-// Per chunk: Y_t = v_t + intra + inter (see the top of the file).
+// acc += one 32 x 32 block (rows rb.., columns cb..) of a product X B whose
+// contraction runs over the K columns of X, on the matrix cores (32x32x2 fp32
+// steps). X is a swizzled (swz) row-major [kL][K] array; B(k, j) gives the
+// column operand. Lane group g takes the contraction indices K/2 g ..
+// K/2 g + K/2 - 1 in order, four per 16-byte read of its row of X.
+template <int K, typename ColOp>
+__device__ __forceinline__ floatx16 block_product(const float (*X)[K], int rb, int cb, floatx16 acc, ColOp B) {
+  constexpr int KH = K / 2;
+  const int lane = threadIdx.x & 63, ln = lane & 31, lg = lane >> 5;
+  const int xr = rb + ln;
+#pragma unroll 2
+  for (int s0 = 0; s0 < KH; s0 += 4) {
+    const int kk = KH * lg + s0;
+    const floatx4 xa = *reinterpret_cast<const floatx4*>(&X[xr][swz<K>(xr, kk)]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc = mfma32f(xa[u], B(kk + u, cb + ln), acc);
+  }
+  return acc;
+}
+
+__device__ __forceinline__ floatx16 zero16() {
+  floatx16 z;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) z[v] = 0.0f;
+  return z;
+}
+
+// Per chunk: Y_t = v_t + intra + inter (see the top of the file). The
+// decay-weighted scores A (j < t) are formed on the vector units; then
+// Y = v + A V + Qe C0 (Qe = qt e^{b}) is two dense products on the matrix
+// cores, 32 x 32 output blocks per wave.
 template <typename TI, int D>
 __global__ __launch_bounds__(kLT2) void linear_out_kernel(LinearArgs a) {
-  static_assert(2 * kL * D >= D * D, "the state entering the chunk is staged over kt and bb");
-  __shared__ float qt[kL][D], vv[kL][D];
-  __shared__ float kb[2][kL][D];  // kt, bb; then the state entering the chunk
-  __shared__ float A[kL][kL];     // column j of row t stored at j ^ (t % 8): rows read together hit distinct banks
-  float (*kt)[D] = kb[0];
-  float (*bb)[D] = kb[1];
+  static_assert(2 * kL * D >= D * D, "the state entering the chunk is staged over qt and bb");
+  __shared__ float qb[2][kL][D];  // qt, bb; then the state entering the chunk
+  __shared__ float kt[kL][D];     // kt; then Qe, swizzled
+  __shared__ float vv[kL][D];
+  __shared__ float A[kL][kL];     // scores, swizzled; then a partial output
+  float (*qt)[D] = qb[0];
+  float (*bb)[D] = qb[1];
   const ChunkPos p = chunk_pos(a);
-  load_chunk<TI, D, kLT2>(a, p, qt, kt, vv, bb, nullptr);
   const int tid = threadIdx.x;
+  const float* C0 = a.cprev + ((int64_t)p.n * a.nchunks + p.c) * D * D;
+  constexpr int NC0 = D * D / kLT2;  // elements of C0 per thread
+  constexpr bool PREFETCH = NC0 <= 8;
+  float c0r[PREFETCH ? NC0 : 1];
+  if constexpr (PREFETCH) {
+#pragma unroll
+    for (int k = 0; k < NC0; ++k) c0r[k] = C0[tid + k * kLT2];
+  }
+  load_chunk<TI, D, kLT2>(a, p, qt, kt, vv, bb, nullptr);
   // intra scores A[t][j], j < t: thread -> row t = tid / kTPR, columns j = tid % kTPR + kTPR m
   {
-    const int t = tid / kTPR, j0 = tid % kTPR;
+    static_assert(kTPR == 8, "a wave holds rows 8 tw .. 8 tw + 7 and columns j = 8 m + j0");
+    const int t = tid / kTPR, j0 = tid % kTPR, tw = __builtin_amdgcn_readfirstlane(tid >> 6);
     float acc[kL / kTPR];
 #pragma unroll
     for (int m = 0; m < kL / kTPR; ++m) acc[m] = 0.0f;
     // channel order skewed per lane so that the lanes of a wave read distinct banks
     const int skew = 8 * (t & 7) + j0;
+#pragma unroll 2
     for (int dd = 0; dd < D; ++dd) {
       const int d = (dd + skew) & (D - 1);
       const float qd = qt[t][d], bd = bb[t][d];
 #pragma unroll
       for (int m = 0; m < kL / kTPR; ++m) {
-        const int j = j0 + kTPR * m;
-        if (j < t) acc[m] = __builtin_fmaf(qd * kt[j][d], fast_exp2((bd - bb[j][d]) * kLog2e), acc[m]);
+        if (m <= tw) {  // column blocks at or below the wave's rows (wave-uniform)
+          const int j = j0 + kTPR * m;
+          const float x = __builtin_fmaf(qd * kt[j][d], fast_exp2((bd - bb[j][d]) * kLog2e), acc[m]);
+          acc[m] = (m < tw || j < t) ? x : acc[m];  // the diagonal block keeps j < t only
+        }
       }
     }
 #pragma unroll
-    for (int m = 0; m < kL / kTPR; ++m) A[t][(j0 + kTPR * m) ^ (t & 7)] = acc[m];
+    for (int m = 0; m < kL / kTPR; ++m) A[t][swz<kL>(t, j0 + kTPR * m)] = acc[m];
   }
   __syncthreads();
-  // qt <- qt e^{b} (the inter read's query)
+  // Qe = qt e^{b} (the inter read's query), over kt
   for (int i = tid; i < kL * D; i += kLT2) {
     const int r = i / D, d = i % D;
-    qt[r][d] *= fast_exp2(bb[r][d] * kLog2e);
+    kt[r][swz<D>(r, d)] = qt[r][d] * fast_exp2(bb[r][d] * kLog2e);
   }
   __syncthreads();
-  // the state entering the chunk, over kt and bb (no longer read)
-  float* C0s = &kb[0][0][0];
-  {
-    const float* C0 = a.cprev + ((int64_t)p.n * a.nchunks + p.c) * D * D;
+  // the state entering the chunk, over qt and bb
+  float* C0s = &qb[0][0][0];
+  if constexpr (PREFETCH) {
+#pragma unroll
+    for (int k = 0; k < NC0; ++k) C0s[tid + k * kLT2] = c0r[k];
+  } else {
     for (int i = tid; i < D * D; i += kLT2) C0s[i] = C0[i];
   }
   __syncthreads();
-  // outputs: thread -> row t = tid / kTPR, channels e0 .. e0 + D / kTPR
-  constexpr int TE = D / kTPR;
-  const int t = tid / kTPR, e0 = (tid % kTPR) * TE;
-  float acc[TE];
+  // wave -> output block; with few blocks, waves NB .. 2 NB - 1 take the
+  // inter product of block w - NB and hand it over through LDS
+  constexpr int NBC = D / 32, NB = (kL / 32) * NBC, NW = kLT2 / 64;
+  constexpr bool SPLIT = 2 * NB <= NW;
+  static_assert(NB <= NW, "one block per wave");
+  const int w = tid >> 6, lane = tid & 63;
+  const int blk = w % NB, part = SPLIT ? w / NB : 0;
+  const int rb = 32 * (blk / NBC), cb = 32 * (blk % NBC);
+  const bool busy = w < (SPLIT ? 2 * NB : NB);
+  floatx16 acc = zero16();
+  if (busy && part == 0) acc = block_product<kL>(A, rb, cb, acc, [&](int k, int j) { return vv[k][j]; });
+  if (busy && (!SPLIT || part == 1))
+    acc = block_product<D>(kt, rb, cb, acc, [&](int k, int j) { return C0s[k * D + j]; });
+  float* Ap = &A[0][0];
+  if constexpr (SPLIT) {
+    __syncthreads();  // every operand of A read
+    if (busy && part == 1) {
 #pragma unroll
-  for (int j = 0; j < TE; ++j) acc[j] = vv[t][e0 + j];
-  for (int j = 0; j < t; ++j) {
-    const float w = A[t][j ^ (t & 7)];
-#pragma unroll
-    for (int e = 0; e < TE; ++e) acc[e] = __builtin_fmaf(w, vv[j][e0 + e], acc[e]);
+      for (int v = 0; v < 16; ++v) Ap[(rb + acc_row(v, lane >> 5)) * D + cb + (lane & 31)] = acc[v];
+    }
+    __syncthreads();
   }
-  for (int d = 0; d < D; ++d) {
-    const float qd = qt[t][d];
-    const float* crow = C0s + d * D + e0;
-#pragma unroll
-    for (int e = 0; e < TE; ++e) acc[e] = __builtin_fmaf(qd, crow[e], acc[e]);
-  }
-  if (t < p.len) {
+  if (busy && part == 0) {
     const int b = p.n / a.H, h = p.n % a.H;
-    TI* Y = (TI*)a.out + (int64_t)b * a.sb + (int64_t)h * a.sh + (int64_t)(p.t0 + t) * a.st;
+    TI* Y = (TI*)a.out + (int64_t)b * a.sb + (int64_t)h * a.sh;
+    const int col = cb + (lane & 31);
 #pragma unroll
-    for (int e = 0; e < TE; ++e) Elem<TI>::store(Y + e0 + e, acc[e]);
+    for (int v = 0; v < 16; ++v) {
+      const int row = rb + acc_row(v, lane >> 5);
+      float y = acc[v] + vv[row][col];
+      if constexpr (SPLIT) y += Ap[row * D + col];
+      if (row < p.len) Elem<TI>::store(Y + (int64_t)(p.t0 + row) * a.st + col, y);
+    }
   }
 }
 
@@ -356,7 +424,7 @@ template <typename TI, int D>
 __global__ __launch_bounds__(kLT) void linear_bstate_kernel(LinearArgs a) {
   __shared__ float qt[kL][D], kt[kL][D], vv[kL][D], bb[kL][D], dy[kL][D];
   const ChunkPos p = chunk_pos(a);
-  load_chunk<TI, D, kLT>(a, p, qt, kt, vv, bb, nullptr, dy);
+  load_chunk<TI, D, kLT, false, true>(a, p, qt, kt, vv, bb, nullptr, dy);
   const int tid = threadIdx.x;
   for (int i = tid; i < kL * D; i += kLT) {
     const int r = i / D, d = i % D;
@@ -406,29 +474,6 @@ __global__ __launch_bounds__(kLT) void linear_bstate_kernel(LinearArgs a) {
     }
 }
 
-// One 32 x 32 block (rows rb.., columns cb..) of a kL x D product whose
-// contraction runs over D, on the matrix cores (32x32x2 fp32 steps). The row
-// operand X is a swizzled [kL][D] array; the column operand is B(k, j) of
-// the product. Lane group g takes the contraction indices D/2 g .. D/2 g + D/2 - 1
-// in order, four per 16-byte read of its row.
-template <int D, typename ColOp>
-__device__ __forceinline__ floatx16 block_product(const float (*X)[D], int rb, int cb, ColOp B) {
-  constexpr int KH = D / 2;
-  const int lane = threadIdx.x & 63, ln = lane & 31, lg = lane >> 5;
-  const int xr = rb + ln;
-  floatx16 acc;
-#pragma unroll
-  for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
-#pragma unroll 2
-  for (int s0 = 0; s0 < KH; s0 += 4) {
-    const int kk = KH * lg + s0;
-    const floatx4 xa = *reinterpret_cast<const floatx4*>(&X[xr][swz<D>(xr, kk)]);
-#pragma unroll
-    for (int u = 0; u < 4; ++u) acc = mfma32f(xa[u], B(kk + u, cb + ln), acc);
-  }
-  return acc;
-}
-
 // Per chunk: every input gradient. Thread (row r = tid / kTPRG, part Q of the
 // channels) keeps its row's gradients for the channels of Q in registers. A
 // wave holds kRowsPerWave consecutive rows, so the triangular loops of the
@@ -459,7 +504,7 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
     c0r[k] = a.cprev[base * D * D + tid + k * kLTG];
     gr[k] = a.gout[base * D * D + tid + k * kLTG];
   }
-  load_chunk<TI, D, kLTG, true>(a, p, qt, kt, vv, bb, Srow, dy);
+  load_chunk<TI, D, kLTG, true, true>(a, p, qt, kt, vv, bb, Srow, dy);
 #pragma unroll
   for (int k = 0; k < NCG; ++k) {
     const int i = tid + k * kLTG;
@@ -469,7 +514,7 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
   const int64_t hoff = (int64_t)b * a.sb + (int64_t)h * a.sh;
   const int r = tid / kTPRG, q0 = (tid % kTPRG) * QW;
   const int qs = swz<D>(r, q0);                // this thread's channels in a swizzled row r
-  const int wrow = (tid >> 6) * kRowsPerWave;  // first row of this wave
+  const int wrow = __builtin_amdgcn_readfirstlane(tid >> 6) * kRowsPerWave;  // first row of this wave
   float dq[QW], dk[QW], dv[QW], db[QW];
 #pragma unroll
   for (int i = 0; i < QW; ++i) {
@@ -487,10 +532,10 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
     bsr[i] = bb[r][q0 + i];
   }
   // j < r holds for some row of the wave iff j < wrow + kRowsPerWave - 1; the
-  // loop runs in pairs of j (the last one may be past every row)
-  for (int j0 = 0; j0 < wrow + kRowsPerWave; j0 += 2) {
+  // loop runs in groups of kRowsPerWave j (the last one is past every row)
+  for (int j0 = 0; j0 < wrow + kRowsPerWave; j0 += kRowsPerWave) {
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < kRowsPerWave; ++u) {
       const int j = j0 + u;
       float pa = 0.0f, pd = 0.0f;
       if (j < r) {
@@ -523,7 +568,7 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
     float bself[QW];
 #pragma unroll
     for (int i = 0; i < QW; ++i) bself[i] = bb[r][q0 + i];
-#pragma unroll 2
+#pragma unroll 4
     for (int t = wrow + 1; t < kL; ++t) {
       if (t > r) {
         const float At = AD[t][r], dAt = AD[r][t];
@@ -555,14 +600,20 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
     AD[i / D][i % D] = gr[k];
   }
   // p1 and p2 of this thread's row and channels, for the last step
-  const TI* P1 = (const TI*)a.p1 + hoff + (int64_t)(p.t0 + r) * a.st;
-  const TI* P2 = (const TI*)a.p2 + hoff + (int64_t)(p.t0 + r) * a.st;
+  const int64_t prow = (int64_t)min(p.t0 + r, a.T - 1);  // rows past the sequence: loaded, then zero
+  const TI* P1 = (const TI*)a.p1 + hoff + prow * a.st;
+  const TI* P2 = (const TI*)a.p2 + hoff + prow * a.st;
   const bool ok = r < p.len;
   float x1[QW], x2[QW];
 #pragma unroll
   for (int i = 0; i < QW; ++i) {
-    x1[i] = ok ? Elem<TI>::load(P1 + q0 + i) : 0.0f;
-    x2[i] = ok ? Elem<TI>::load(P2 + q0 + i) : 0.0f;
+    x1[i] = Elem<TI>::load(P1 + q0 + i);
+    x2[i] = Elem<TI>::load(P2 + q0 + i);
+  }
+#pragma unroll
+  for (int i = 0; i < QW; ++i) {
+    x1[i] = ok ? x1[i] : 0.0f;
+    x2[i] = ok ? x2[i] : 0.0f;
   }
   __syncthreads();
   // Phase III, the inter-chunk terms: wave w < 3 NB takes block w % NB of
@@ -573,11 +624,11 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
   const int rb = 32 * (blk / NBC), cb = 32 * (blk % NBC);
   floatx16 acc;
   if (prod == 0) {
-    acc = block_product<D>(dy, rb, cb, [&](int k, int j) { return C0s[j][k]; });
+    acc = block_product<D>(dy, rb, cb, zero16(), [&](int k, int j) { return C0s[j][k]; });
   } else if (prod == 1) {
-    acc = block_product<D>(vv, rb, cb, [&](int k, int j) { return AD[j][k]; });
+    acc = block_product<D>(vv, rb, cb, zero16(), [&](int k, int j) { return AD[j][k]; });
   } else if (prod == 2) {
-    acc = block_product<D>(tmp, rb, cb, [&](int k, int j) { return AD[k][j]; });
+    acc = block_product<D>(tmp, rb, cb, zero16(), [&](int k, int j) { return AD[k][j]; });
   }
   __syncthreads();  // every operand read: dy, vv, dbs take the three results
   if (prod < 3) {
