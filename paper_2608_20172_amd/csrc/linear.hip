@@ -51,10 +51,10 @@ __device__ __forceinline__ int swz(int r, int c) {
 }
 
 // Loads the chunk into LDS as fp32 and forms qt = S ^p1, kt = S ^p2 (rows past
-// the sequence are zero), v, optionally dY (v and dY swizzled if SWZ), and
-// b = running sum of g (zero g past the end, so b stays at its last value).
-// One wave per row for the norms and S.
-template <typename TI, int D, int NT, bool SWZ = false, bool WITH_DY = false>
+// the sequence are zero), v, optionally dY, and b = running sum of g (zero g
+// past the end, so b stays at its last value). SWZ_VD stores v and dY
+// swizzled (swz), SWZ_QKB qt, kt and b. One wave per row for the norms and S.
+template <typename TI, int D, int NT, bool SWZ_VD = false, bool WITH_DY = false, bool SWZ_QKB = false>
 __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& p, float (*qt)[D], float (*kt)[D],
                                            float (*vv)[D], float (*bb)[D], float* Srow,
                                            float (*dyl)[D] = nullptr) {
@@ -100,9 +100,9 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
         const int d = lane + 64 * u;
         if (!ok || d >= D) x1[kb][u] = x2[kb][u] = vx[kb][u] = gx[kb][u] = dx[kb][u] = 0.0f;
         if (d < D) {
-          const int ds = SWZ ? swz<D>(r, d) : d;
+          const int ds = SWZ_VD ? swz<D>(r, d) : d;
           vv[r][ds] = vx[kb][u];
-          bb[r][d] = gx[kb][u];
+          bb[r][SWZ_QKB ? swz<D>(r, d) : d] = gx[kb][u];
           if constexpr (WITH_DY) dyl[r][ds] = dx[kb][u];
         }
         s11 += x1[kb][u] * x1[kb][u];
@@ -124,8 +124,9 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
       for (int u = 0; u < U; ++u) {
         const int d = lane + 64 * u;
         if (d < D) {
-          qt[r][d] = x1[kb][u] * i1;
-          kt[r][d] = x2[kb][u] * i2;
+          const int dq = SWZ_QKB ? swz<D>(r, d) : d;
+          qt[r][dq] = x1[kb][u] * i1;
+          kt[r][dq] = x2[kb][u] * i2;
         }
       }
       if (lane == 0 && Srow) Srow[r] = S;
@@ -136,21 +137,22 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
   // its segment in place, then adds the totals of the segments above it
   constexpr int NSEG = NT / D, SR = kL / NSEG;
   const int d = tid % D, sg = tid / D;
+  auto col = [&](int row) { return SWZ_QKB ? swz<D>(row, d) : d; };
   float x[SR];
   float acc = 0.0f;
 #pragma unroll
-  for (int i = 0; i < SR; ++i) x[i] = bb[sg * SR + i][d];
+  for (int i = 0; i < SR; ++i) x[i] = bb[sg * SR + i][col(sg * SR + i)];
 #pragma unroll
   for (int i = 0; i < SR; ++i) x[i] = acc += x[i];
 #pragma unroll
-  for (int i = 0; i < SR; ++i) bb[sg * SR + i][d] = x[i];
+  for (int i = 0; i < SR; ++i) bb[sg * SR + i][col(sg * SR + i)] = x[i];
   __syncthreads();
   float off = 0.0f;
-  for (int u = 0; u < sg; ++u) off += bb[u * SR + SR - 1][d];
+  for (int u = 0; u < sg; ++u) off += bb[u * SR + SR - 1][col(u * SR + SR - 1)];
   __syncthreads();  // every segment total read
   if (sg > 0) {
 #pragma unroll
-    for (int i = 0; i < SR; ++i) bb[sg * SR + i][d] = x[i] + off;
+    for (int i = 0; i < SR; ++i) bb[sg * SR + i][col(sg * SR + i)] = x[i] + off;
   }
   __syncthreads();
 }
@@ -304,15 +306,99 @@ __device__ __forceinline__ floatx16 zero16() {
   return z;
 }
 
-// Per chunk: Y_t = v_t + intra + inter (see the top of the file). The
-// decay-weighted scores A (j < t) are formed on the vector units; then
-// Y = v + A V + Qe C0 (Qe = qt e^{b}) is two dense products on the matrix
-// cores, 32 x 32 output blocks per wave.
+__device__ __forceinline__ floatx4 mfma16f(float a, float b, const floatx4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// Chunk c (4 channels) of row r of a swizzled (swz) [kL][D] array.
+template <int D>
+__device__ __forceinline__ floatx4 ld4(const float (*X)[D], int r, int c) {
+  return *reinterpret_cast<const floatx4*>(&X[r][(c ^ (r & (D / 4 - 1))) << 2]);
+}
+
+// Intra-chunk scores A[t][j] = sum_a qt_{t,a} kt_{j,a} e^{b_{t,a} - b_{j,a}}
+// (j < t) into the swizzled A, in 16 x 16 sub-blocks. qt, kt and b are
+// swizzled. Below the diagonal, block (tb, jb) factors the decay at the last
+// row rf of key block jb: e^{b_t - b_j} = e^{b_t - b_rf} e^{b_rf - b_j}, both
+// factors <= 1 (b does not increase down the chunk), so the block is a plain
+// product of qt e^{b - b_rf} and kt e^{b_rf - b} on the matrix cores
+// (16x16x4 fp32 steps, the operands formed in registers). The four diagonal
+// blocks are summed term by term on the vector units. Waves 0-3: diagonal
+// block w; waves 4-7: blocks w - 4 and w (of the six below the diagonal).
+template <int D>
+__device__ __forceinline__ void chunk_scores(const float (*qt)[D], const float (*kt)[D], const float (*bb)[D],
+                                             float (*A)[kL]) {
+  constexpr int SB = 16, NSB = kL / SB, CH = D / 4;
+  static_assert(kLT2 == 512 && NSB == 4, "eight waves: four diagonal blocks, six below");
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (w < NSB) {
+    // lane -> row t = SB w + lane / 4 and columns j = SB w + lane % 4 + 4 m
+    const int t = SB * w + (lane >> 2), jq = lane & 3;
+    float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll 2
+    for (int c = 0; c < CH; ++c) {
+      const floatx4 q4 = ld4<D>(qt, t, c), bt4 = ld4<D>(bb, t, c);
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const int j = SB * w + jq + 4 * m;
+        const floatx4 k4 = ld4<D>(kt, j, c), bj4 = ld4<D>(bb, j, c);
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          acc[m] = __builtin_fmaf(q4[u] * k4[u], fast_exp2((bt4[u] - bj4[u]) * kLog2e), acc[m]);
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      const int j = SB * w + jq + 4 * m;
+      A[t][swz<kL>(t, j)] = j < t ? acc[m] : 0.0f;  // above the diagonal: zero
+    }
+    // the blocks above the diagonal block's row band are zero
+    for (int jb = w + 1; jb < NSB; ++jb) {
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const int j = SB * jb + jq + 4 * m;
+        A[t][swz<kL>(t, j)] = 0.0f;
+      }
+    }
+  } else {
+    const int i = lane & 15, g = lane >> 4;
+    for (int bi = w - NSB; bi < NSB * (NSB - 1) / 2; bi += NSB) {
+      // blocks below the diagonal, bi = 0..5: (1,0) (2,0) (3,0) (2,1) (3,1) (3,2)
+      const int jb = bi < 3 ? 0 : bi < 5 ? 1 : 2;
+      const int tb = jb + 1 + (bi < 3 ? bi : bi < 5 ? bi - 3 : 0);
+      const int rf = SB * jb + SB - 1, tr = SB * tb + i, jr = SB * jb + i;
+      floatx4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+      // lane group g takes the channel chunks CH/4 g .. CH/4 g + CH/4 - 1
+#pragma unroll 2
+      for (int c0 = 0; c0 < CH / 4; ++c0) {
+        const int c = (CH / 4) * g + c0;
+        const floatx4 q4 = ld4<D>(qt, tr, c), bt4 = ld4<D>(bb, tr, c), br4 = ld4<D>(bb, rf, c);
+        const floatx4 k4 = ld4<D>(kt, jr, c), bj4 = ld4<D>(bb, jr, c);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float qa = q4[u] * fast_exp2((bt4[u] - br4[u]) * kLog2e);
+          const float kb = k4[u] * fast_exp2((br4[u] - bj4[u]) * kLog2e);
+          acc = mfma16f(qa, kb, acc);
+        }
+      }
+      // register v of lane (i, g): row 4 g + v, column i of the block
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int r = SB * tb + 4 * g + v;
+        A[r][swz<kL>(r, SB * jb + i)] = acc[v];
+      }
+    }
+  }
+}
+
+// Per chunk: Y_t = v_t + intra + inter (see the top of the file). The scores
+// A (j < t) come from chunk_scores; then Y = v + A V + Qe C0 (Qe = qt e^{b})
+// is two dense products on the matrix cores, 32 x 32 output blocks per wave.
 template <typename TI, int D>
 __global__ __launch_bounds__(kLT2) void linear_out_kernel(LinearArgs a) {
   static_assert(2 * kL * D >= D * D, "the state entering the chunk is staged over qt and bb");
-  __shared__ float qb[2][kL][D];  // qt, bb; then the state entering the chunk
-  __shared__ float kt[kL][D];     // kt; then Qe, swizzled
+  __shared__ float qb[2][kL][D];  // qt, bb (swizzled); then the state entering the chunk
+  __shared__ float kt[kL][D];     // kt; then Qe (both swizzled)
   __shared__ float vv[kL][D];
   __shared__ float A[kL][kL];     // scores, swizzled; then a partial output
   float (*qt)[D] = qb[0];
@@ -327,37 +413,13 @@ __global__ __launch_bounds__(kLT2) void linear_out_kernel(LinearArgs a) {
 #pragma unroll
     for (int k = 0; k < NC0; ++k) c0r[k] = C0[tid + k * kLT2];
   }
-  load_chunk<TI, D, kLT2>(a, p, qt, kt, vv, bb, nullptr);
-  // intra scores A[t][j], j < t: thread -> row t = tid / kTPR, columns j = tid % kTPR + kTPR m
-  {
-    static_assert(kTPR == 8, "a wave holds rows 8 tw .. 8 tw + 7 and columns j = 8 m + j0");
-    const int t = tid / kTPR, j0 = tid % kTPR, tw = __builtin_amdgcn_readfirstlane(tid >> 6);
-    float acc[kL / kTPR];
-#pragma unroll
-    for (int m = 0; m < kL / kTPR; ++m) acc[m] = 0.0f;
-    // channel order skewed per lane so that the lanes of a wave read distinct banks
-    const int skew = 8 * (t & 7) + j0;
-#pragma unroll 2
-    for (int dd = 0; dd < D; ++dd) {
-      const int d = (dd + skew) & (D - 1);
-      const float qd = qt[t][d], bd = bb[t][d];
-#pragma unroll
-      for (int m = 0; m < kL / kTPR; ++m) {
-        if (m <= tw) {  // column blocks at or below the wave's rows (wave-uniform)
-          const int j = j0 + kTPR * m;
-          const float x = __builtin_fmaf(qd * kt[j][d], fast_exp2((bd - bb[j][d]) * kLog2e), acc[m]);
-          acc[m] = (m < tw || j < t) ? x : acc[m];  // the diagonal block keeps j < t only
-        }
-      }
-    }
-#pragma unroll
-    for (int m = 0; m < kL / kTPR; ++m) A[t][swz<kL>(t, j0 + kTPR * m)] = acc[m];
-  }
+  load_chunk<TI, D, kLT2, false, false, true>(a, p, qt, kt, vv, bb, nullptr);
+  chunk_scores<D>(qt, kt, bb, A);
   __syncthreads();
-  // Qe = qt e^{b} (the inter read's query), over kt
+  // Qe = qt e^{b} (the inter read's query), over kt; all three swizzled alike
   for (int i = tid; i < kL * D; i += kLT2) {
-    const int r = i / D, d = i % D;
-    kt[r][swz<D>(r, d)] = qt[r][d] * fast_exp2(bb[r][d] * kLog2e);
+    const int r = i / D, c = i % D;
+    kt[r][c] = qt[r][c] * fast_exp2(bb[r][c] * kLog2e);
   }
   __syncthreads();
   // the state entering the chunk, over qt and bb
