@@ -323,14 +323,19 @@ __device__ __forceinline__ floatx4 ld4(const float (*X)[D], int r, int c) {
 // factors <= 1 (b does not increase down the chunk), so the block is a plain
 // product of qt e^{b - b_rf} and kt e^{b_rf - b} on the matrix cores
 // (16x16x4 fp32 steps, the operands formed in registers). The four diagonal
-// blocks are summed term by term on the vector units. Waves 0-3: diagonal
-// block w; waves 4-7: blocks w - 4 and w (of the six below the diagonal).
-template <int D>
+// blocks are summed term by term on the vector units. Waves 0-3 of the
+// workgroup: diagonal block w; waves 4-7: blocks w - 4 and w (of the six below
+// the diagonal). With TRANS the scores go to A as A^T (A[j][t]).
+template <int D, bool TRANS = false>
 __device__ __forceinline__ void chunk_scores(const float (*qt)[D], const float (*kt)[D], const float (*bb)[D],
                                              float (*A)[kL]) {
   constexpr int SB = 16, NSB = kL / SB, CH = D / 4;
-  static_assert(kLT2 == 512 && NSB == 4, "eight waves: four diagonal blocks, six below");
+  static_assert(NSB == 4, "four diagonal blocks, six below");
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  auto put = [&](int t, int j, float x) {
+    if (TRANS) A[j][swz<kL>(j, t)] = x;
+    else A[t][swz<kL>(t, j)] = x;
+  };
   if (w < NSB) {
     // lane -> row t = SB w + lane / 4 and columns j = SB w + lane % 4 + 4 m
     const int t = SB * w + (lane >> 2), jq = lane & 3;
@@ -350,17 +355,16 @@ __device__ __forceinline__ void chunk_scores(const float (*qt)[D], const float (
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
       const int j = SB * w + jq + 4 * m;
-      A[t][swz<kL>(t, j)] = j < t ? acc[m] : 0.0f;  // above the diagonal: zero
+      put(t, j, j < t ? acc[m] : 0.0f);  // above the diagonal: zero
     }
     // the blocks above the diagonal block's row band are zero
     for (int jb = w + 1; jb < NSB; ++jb) {
 #pragma unroll
       for (int m = 0; m < 4; ++m) {
-        const int j = SB * jb + jq + 4 * m;
-        A[t][swz<kL>(t, j)] = 0.0f;
+        put(t, SB * jb + jq + 4 * m, 0.0f);
       }
     }
-  } else {
+  } else if (w < 2 * NSB) {
     const int i = lane & 15, g = lane >> 4;
     for (int bi = w - NSB; bi < NSB * (NSB - 1) / 2; bi += NSB) {
       // blocks below the diagonal, bi = 0..5: (1,0) (2,0) (3,0) (2,1) (3,1) (3,2)
@@ -384,8 +388,7 @@ __device__ __forceinline__ void chunk_scores(const float (*qt)[D], const float (
       // register v of lane (i, g): row 4 g + v, column i of the block
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int r = SB * tb + 4 * g + v;
-        A[r][swz<kL>(r, SB * jb + i)] = acc[v];
+        put(SB * tb + 4 * g + v, SB * jb + i, acc[v]);
       }
     }
   }
@@ -536,29 +539,53 @@ __global__ __launch_bounds__(kLT) void linear_bstate_kernel(LinearArgs a) {
     }
 }
 
+// One 16 x 16 tile of a product on the matrix cores (16x16x4 fp32 steps):
+// acc[v] of lane (i, g) = sum over k in [k0, k0 + K) of X[r0 + i][k] B(k, c0 + ...)
+// for output row r0 + 4 g + v and column c0 + i. X is a swizzled [kL][W]
+// array; B(k, j) gives the column operand. K is a multiple of 16 and k0 of 4;
+// lane group g takes the indices k0 + K/4 g .. k0 + K/4 g + K/4 - 1.
+template <int W, typename ColOp>
+__device__ __forceinline__ floatx4 tile_product(const float (*X)[W], int r0, int c0, int k0, int K, ColOp B) {
+  const int lane = threadIdx.x & 63, i = lane & 15, g = lane >> 4;
+  const int kq = K >> 2, xr = r0 + i;
+  floatx4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int s0 = 0; s0 < kq; s0 += 4) {
+    const int k = k0 + kq * g + s0;
+    const floatx4 xa = ld4<W>(X, xr, k >> 2);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc = mfma16f(xa[u], B(k + u, c0 + i), acc);
+  }
+  return acc;
+}
+
 // Per chunk: every input gradient. Thread (row r = tid / kTPRG, part Q of the
-// channels) keeps its row's gradients for the channels of Q in registers. A
-// wave holds kRowsPerWave consecutive rows, so the triangular loops of the
-// intra-chunk phases end (phase I) or start (phase II) at a wave-uniform row,
-// and a wave's two phases together always walk about kL rows. The three
-// inter-chunk products are dense (kL x D by D x D) and run on the matrix
-// cores, one 32 x 32 block per wave.
+// channels) keeps its row's gradients for the channels of Q in registers.
+// The intra-chunk terms use the 16-row sub-blocks of the forward scores:
+//   A (chunk_scores) and dA = dY V^T (j <= t blocks) on the matrix cores;
+//   dv_intra = A^T dY; dq_intra, dk_intra below the diagonal as products with
+//   the decay factored at a block boundary (q side: the row before the
+//   query block; k side: the last row of the key block), both factors <= 1;
+//   the diagonal blocks term by term on the vector units.
+// The three inter-chunk products are dense (kL x D by D x D), 32 x 32 blocks.
 template <typename TI, int D>
 __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
   static_assert(D == 32 || D == 64, "the backward kernel keeps the chunk of D <= 64 channels in LDS");
-  // vv, dy (and tmp while it holds Kd) are swizzled (swz): they are row
-  // operands of the matrix-core products
-  __shared__ float qt[kL][D], kt[kL][D], vv[kL][D], bb[kL][D], dy[kL][D], dbs[kL][D], tmp[kL][D];
-  // AD: A[t][j] at [t][j] and dA[t][j] at [j][t] for j < t; then G. C0s: C0.
-  __shared__ float AD[kL][kL + 1], C0s[kL][kL + 1];
+  constexpr int SB = 16, NSB = kL / SB, NE = D / 16;
+  // all swizzled (swz) unless noted
+  __shared__ float qt[kL][D], kt[kL][D], vv[kL][D], bb[kL][D], dy[kL][D];
+  // M0: A^T; then dv_intra (plain); then Kd; then dKd Kd (plain)
+  // M1: dA;  then dq_intra (plain); then G
+  // M2: dA^T; then dk_intra (plain); then dVx and db (plain)
+  __shared__ float M0[kL][kL], M1[kL][kL], M2[kL][kL];
+  __shared__ float C0s[kL][kL + 1];  // plain, padded
   __shared__ float Srow[kL];
-  constexpr int QW = D / kTPRG;  // channels per thread
+  constexpr int QW = D / kTPRG;      // channels per thread
   constexpr int NCG = D * D / kLTG;  // elements of C0 and of G per thread
   static_assert(D * D % kLTG == 0, "C0 and G split evenly over the threads");
   const ChunkPos p = chunk_pos(a);
-  const int tid = threadIdx.x;
-  // C0 and G are read from HBM now and reach LDS later, so that their latency
-  // hides behind the chunk's load and the intra-chunk phases
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // C0 and G are read from HBM now and reach LDS later
   const int64_t base = (int64_t)p.n * a.nchunks + p.c;
   float c0r[NCG], gr[NCG];
 #pragma unroll
@@ -566,100 +593,161 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
     c0r[k] = a.cprev[base * D * D + tid + k * kLTG];
     gr[k] = a.gout[base * D * D + tid + k * kLTG];
   }
-  load_chunk<TI, D, kLTG, true, true>(a, p, qt, kt, vv, bb, Srow, dy);
+  load_chunk<TI, D, kLTG, true, true, true>(a, p, qt, kt, vv, bb, Srow, dy);
 #pragma unroll
   for (int k = 0; k < NCG; ++k) {
-    const int i = tid + k * kLTG;
-    C0s[i / D][i % D] = c0r[k];  // read after the barrier that ends phase II
+    const int e = tid + k * kLTG;
+    C0s[e / D][e % D] = c0r[k];
   }
   const int b = p.n / a.H, h = p.n % a.H;
   const int64_t hoff = (int64_t)b * a.sb + (int64_t)h * a.sh;
   const int r = tid / kTPRG, q0 = (tid % kTPRG) * QW;
-  const int qs = swz<D>(r, q0);                // this thread's channels in a swizzled row r
-  const int wrow = __builtin_amdgcn_readfirstlane(tid >> 6) * kRowsPerWave;  // first row of this wave
+  const int qs = swz<D>(r, q0);  // this thread's channels in a swizzled row r (contiguous)
+  const int wrow = w * kRowsPerWave;
+  // ---- scores and dA: waves 0-7 the scores (to M0 as A^T), waves 8-15 dA
+  if (w < 8) {
+    chunk_scores<D, true>(qt, kt, bb, M0);
+  } else {
+    // the ten blocks (tb, jb) with jb <= tb; wave 8 + i takes blocks i and i + 8
+    const int i = lane & 15, g = lane >> 4;
+    for (int bi = w - 8; bi < NSB * (NSB + 1) / 2; bi += 8) {
+      int tb = 0, jb = bi;
+      while (jb > tb) {
+        jb -= tb + 1;
+        ++tb;
+      }
+      const floatx4 acc = tile_product<D>(dy, SB * tb, SB * jb, 0, D, [&](int k, int j) { return vv[j][swz<D>(j, k)]; });
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int t = SB * tb + 4 * g + v, j = SB * jb + i;
+        const float x = j < t ? acc[v] : 0.0f;
+        M1[t][swz<kL>(t, j)] = x;
+        M2[j][swz<kL>(j, t)] = x;
+      }
+    }
+  }
+  __syncthreads();
+  // ---- intra products below the diagonal: 16 x 16 tiles, wave w takes tiles w, w + 16, w + 32
+  //   type 0 (4 NE tiles): dv_intra[j][e] = sum_{t >= 16 jb} A^T[j][t] dY[t][e]
+  //   type 1 (3 NE): dq_intra[t][d] = e^{b_t - b_rf} sum_{j < 16 tb} dA[t][j] kt[j][d] e^{b_rf - b_j}, rf = 16 tb - 1
+  //   type 2 (3 NE): dk_intra[j][d] = e^{b_rf - b_j} sum_{t > rf} dA^T[j][t] qt[t][d] e^{b_t - b_rf}, rf = 16 jb + 15
+  constexpr int NT0 = NSB * NE, NT1 = (NSB - 1) * NE, NTT = NT0 + 2 * NT1;
+  constexpr int MAXT = (NTT + 15) / 16;
+  floatx4 res[MAXT];
+#pragma unroll
+  for (int m = 0; m < MAXT; ++m) {
+    const int tau = w + 16 * m;
+    res[m] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+    if (tau < NT0) {
+      const int jb = tau / NE, eb = tau % NE;
+      res[m] = tile_product<kL>(M0, SB * jb, SB * eb, SB * jb, kL - SB * jb,
+                                [&](int k, int e) { return dy[k][swz<D>(k, e)]; });
+    } else if (tau < NT0 + NT1) {
+      const int tb = 1 + (tau - NT0) / NE, db = (tau - NT0) % NE;
+      const int rf = SB * tb - 1, col = SB * db + (lane & 15);
+      const float brf = bb[rf][swz<D>(rf, col)];
+      floatx4 acc = tile_product<kL>(M1, SB * tb, SB * db, 0, SB * tb, [&](int k, int d) {
+        const int c = swz<D>(k, d);
+        return kt[k][c] * fast_exp2((brf - bb[k][c]) * kLog2e);
+      });
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int t = SB * tb + 4 * (lane >> 4) + v;
+        acc[v] *= fast_exp2((bb[t][swz<D>(t, col)] - brf) * kLog2e);
+      }
+      res[m] = acc;
+    } else if (tau < NTT) {
+      const int jb = (tau - NT0 - NT1) / NE, db = (tau - NT0 - NT1) % NE;
+      const int rf = SB * jb + SB - 1, col = SB * db + (lane & 15);
+      const float brf = bb[rf][swz<D>(rf, col)];
+      floatx4 acc = tile_product<kL>(M2, SB * jb, SB * db, rf + 1, kL - rf - 1, [&](int k, int d) {
+        const int c = swz<D>(k, d);
+        return qt[k][c] * fast_exp2((bb[k][c] - brf) * kLog2e);
+      });
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int j = SB * jb + 4 * (lane >> 4) + v;
+        acc[v] *= fast_exp2((brf - bb[j][swz<D>(j, col)]) * kLog2e);
+      }
+      res[m] = acc;
+    }
+  }
+  // ---- diagonal blocks on the vector units, in the thread's row and channels
   float dq[QW], dk[QW], dv[QW], db[QW];
+  float qself[QW], kself[QW], bself[QW];
 #pragma unroll
   for (int i = 0; i < QW; ++i) {
-    dq[i] = 0.0f;
-    dk[i] = 0.0f;
+    qself[i] = qt[r][qs + i];
+    kself[i] = kt[r][qs + i];
+    bself[i] = bb[r][qs + i];
+    dq[i] = dk[i] = 0.0f;
     dv[i] = dy[r][qs + i];  // Y = I~ + E
-    db[i] = 0.0f;
   }
-  // Phase I (row r as t): A[r][j], dA[r][j] for j < r; dqt_intra
-  float yself[QW], qself[QW], bsr[QW];
-#pragma unroll
-  for (int i = 0; i < QW; ++i) {
-    yself[i] = dy[r][qs + i];
-    qself[i] = qt[r][q0 + i];
-    bsr[i] = bb[r][q0 + i];
-  }
-  // j < r holds for some row of the wave iff j < wrow + kRowsPerWave - 1; the
-  // loop runs in groups of kRowsPerWave j (the last one is past every row)
-  for (int j0 = 0; j0 < wrow + kRowsPerWave; j0 += kRowsPerWave) {
-#pragma unroll
-    for (int u = 0; u < kRowsPerWave; ++u) {
-      const int j = j0 + u;
-      float pa = 0.0f, pd = 0.0f;
+  {
+    const int blo = (wrow / SB) * SB;  // the wave's rows share one 16-row block
+    // dq: j in [blo, r)
+    for (int j = blo; j < wrow + kRowsPerWave - 1; ++j) {
       if (j < r) {
+        const float dA = M1[r][swz<kL>(r, j)];
         const int js = swz<D>(j, q0);
 #pragma unroll
-        for (int i = 0; i < QW; ++i) pd = __builtin_fmaf(yself[i], vv[j][js + i], pd);
-      }
-      pd = group_sum<kTPRG>(pd);  // dA[r][j] over all channels
-      if (j < r) {
-#pragma unroll
-        for (int i = 0; i < QW; ++i) {
-          const int d = q0 + i;
-          const float w = kt[j][d] * fast_exp2((bsr[i] - bb[j][d]) * kLog2e);
-          pa = __builtin_fmaf(qself[i], w, pa);
-          dq[i] = __builtin_fmaf(pd, w, dq[i]);
-        }
-      }
-      pa = group_sum<kTPRG>(pa);
-      if (tid % kTPRG == 0 && j < r) {
-        AD[r][j] = pa;
-        AD[j][r] = pd;
+        for (int i = 0; i < QW; ++i)
+          dq[i] = __builtin_fmaf(dA * kt[j][js + i], fast_exp2((bself[i] - bb[j][js + i]) * kLog2e), dq[i]);
       }
     }
-  }
-#pragma unroll
-  for (int i = 0; i < QW; ++i) db[i] = qt[r][q0 + i] * dq[i];
-  __syncthreads();
-  // Phase II (row r as j): dv_intra, dkt_intra; every lane walks the same rows t
-  {
-    float bself[QW];
-#pragma unroll
-    for (int i = 0; i < QW; ++i) bself[i] = bb[r][q0 + i];
-#pragma unroll 4
-    for (int t = wrow + 1; t < kL; ++t) {
+    // dk: t in (r, blo + SB)
+    for (int t = wrow + 1; t < blo + SB; ++t) {
       if (t > r) {
-        const float At = AD[t][r], dAt = AD[r][t];
+        const float dA = M2[r][swz<kL>(r, t)];
         const int ts = swz<D>(t, q0);
 #pragma unroll
-        for (int i = 0; i < QW; ++i) {
-          const int d = q0 + i;
-          dv[i] = __builtin_fmaf(At, dy[t][ts + i], dv[i]);
-          dk[i] = __builtin_fmaf(dAt * qt[t][d], fast_exp2((bb[t][d] - bself[i]) * kLog2e), dk[i]);
-        }
+        for (int i = 0; i < QW; ++i)
+          dk[i] = __builtin_fmaf(dA * qt[t][ts + i], fast_exp2((bb[t][ts + i] - bself[i]) * kLog2e), dk[i]);
       }
     }
   }
-  // Kd = kt e^{b_last - b}: the row operand of dV += Kd G, to tmp
+  __syncthreads();  // every read of A^T, dA, dA^T done
+  {
+    float(*R0)[D] = reinterpret_cast<float(*)[D]>(&M0[0][0]);
+    float(*R1)[D] = reinterpret_cast<float(*)[D]>(&M1[0][0]);
+    float(*R2)[D] = reinterpret_cast<float(*)[D]>(&M2[0][0]);
+#pragma unroll
+    for (int m = 0; m < MAXT; ++m) {
+      const int tau = w + 16 * m;
+      if (tau < NTT) {
+        const int ty = tau < NT0 ? 0 : tau < NT0 + NT1 ? 1 : 2;
+        const int u = tau - (ty == 0 ? 0 : ty == 1 ? NT0 : NT0 + NT1);
+        const int rb = ty == 1 ? SB * (1 + u / NE) : SB * (u / NE), cb = SB * (u % NE);
+        float(*R)[D] = ty == 0 ? R0 : ty == 1 ? R1 : R2;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) R[rb + 4 * (lane >> 4) + v][cb + (lane & 15)] = res[m][v];
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < QW; ++i) {
+      dv[i] += R0[r][q0 + i];
+      if (r >= SB) dq[i] += R1[r][q0 + i];
+      if (r < kL - SB) dk[i] += R2[r][q0 + i];
+      db[i] = qself[i] * dq[i] - kself[i] * dk[i];
+    }
+  }
+  __syncthreads();  // M0, M1 free
+  // Kd = kt e^{b_last - b} (row operand of dV += Kd G) to M0, G to M1, both swizzled [kL][D]
+  float(*Kd)[D] = reinterpret_cast<float(*)[D]>(&M0[0][0]);
+  float(*Gs)[D] = reinterpret_cast<float(*)[D]>(&M1[0][0]);
   float ek[QW], kd[QW];
 #pragma unroll
   for (int i = 0; i < QW; ++i) {
     const int d = q0 + i;
-    db[i] -= kt[r][d] * dk[i];
-    ek[i] = fast_exp2((bb[kL - 1][d] - bb[r][d]) * kLog2e);
-    kd[i] = kt[r][d] * ek[i];
-    tmp[r][qs + i] = kd[i];
+    ek[i] = fast_exp2((bb[kL - 1][swz<D>(kL - 1, d)] - bself[i]) * kLog2e);
+    kd[i] = kself[i] * ek[i];
+    Kd[r][qs + i] = kd[i];
   }
-  __syncthreads();
-  // G over A, dA
 #pragma unroll
   for (int k = 0; k < NCG; ++k) {
-    const int i = tid + k * kLTG;
-    AD[i / D][i % D] = gr[k];
+    const int e = tid + k * kLTG, gd = e / D, ge = e % D;
+    Gs[gd][swz<D>(gd, ge)] = gr[k];
   }
   // p1 and p2 of this thread's row and channels, for the last step
   const int64_t prow = (int64_t)min(p.t0 + r, a.T - 1);  // rows past the sequence: loaded, then zero
@@ -678,52 +766,53 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
     x2[i] = ok ? x2[i] : 0.0f;
   }
   __syncthreads();
-  // Phase III, the inter-chunk terms: wave w < 3 NB takes block w % NB of
+  // ---- inter-chunk terms: wave w < 3 NB takes block w % NB of
   //   product 0: dQe = dY C0^T,  1: dKd = V G^T,  2: dVx = Kd G.
   constexpr int NBC = D / 32, NB = (kL / 32) * NBC;
   static_assert(3 * NB <= kLTG / 64, "one block per wave");
-  const int w = tid >> 6, prod = w / NB, blk = w % NB;
+  const int prod = w / NB, blk = w % NB;
   const int rb = 32 * (blk / NBC), cb = 32 * (blk % NBC);
   floatx16 acc;
   if (prod == 0) {
     acc = block_product<D>(dy, rb, cb, zero16(), [&](int k, int j) { return C0s[j][k]; });
   } else if (prod == 1) {
-    acc = block_product<D>(vv, rb, cb, zero16(), [&](int k, int j) { return AD[j][k]; });
+    acc = block_product<D>(vv, rb, cb, zero16(), [&](int k, int j) { return Gs[j][swz<D>(j, k)]; });
   } else if (prod == 2) {
-    acc = block_product<D>(tmp, rb, cb, zero16(), [&](int k, int j) { return AD[k][j]; });
+    acc = block_product<D>(Kd, rb, cb, zero16(), [&](int k, int j) { return Gs[k][swz<D>(k, j)]; });
   }
-  __syncthreads();  // every operand read: dy, vv, dbs take the three results
+  __syncthreads();  // every operand read: dy, vv, M2 take the three results (plain)
+  float(*Dx)[D] = reinterpret_cast<float(*)[D]>(&M2[0][0]);
   if (prod < 3) {
-    float (*O)[D] = prod == 0 ? dy : prod == 1 ? vv : dbs;
-    const int lane = tid & 63;
+    float(*O)[D] = prod == 0 ? dy : prod == 1 ? vv : Dx;
 #pragma unroll
     for (int v = 0; v < 16; ++v) O[rb + acc_row(v, lane >> 5)][cb + (lane & 31)] = acc[v];
   }
   __syncthreads();
+  float(*tmp)[D] = Kd;  // now plain: the column sums of dKd Kd go to the chunk's last row
 #pragma unroll
   for (int i = 0; i < QW; ++i) {
     const int d = q0 + i;
     const float dqe = dy[r][d], dkd = vv[r][d];
-    const float eb = fast_exp2(bb[r][d] * kLog2e);
+    const float eb = fast_exp2(bself[i] * kLog2e);
     dq[i] = __builtin_fmaf(dqe, eb, dq[i]);
     dk[i] = __builtin_fmaf(dkd, ek[i], dk[i]);
-    dv[i] += dbs[r][d];
-    db[i] += dqe * qt[r][d] * eb - dkd * kd[i];
-    tmp[r][d] = dkd * kd[i];  // its column sum goes to the chunk's last row
+    dv[i] += Dx[r][d];
+    db[i] += dqe * qself[i] * eb - dkd * kd[i];
+    tmp[r][d] = dkd * kd[i];
   }
 #pragma unroll
-  for (int i = 0; i < QW; ++i) dbs[r][q0 + i] = db[i];
+  for (int i = 0; i < QW; ++i) Dx[r][q0 + i] = db[i];
   __syncthreads();
   // dg: reverse running sum of db down the chunk, with the last row's extra terms
   if (tid < D) {
     const int d = tid;
     float extra = 0.0f, dgam = 0.0f;
     for (int j = 0; j < kL; ++j) extra += tmp[j][d];
-    for (int e = 0; e < D; ++e) dgam = __builtin_fmaf(AD[d][e], C0s[d][e], dgam);
-    float accg = extra + dgam * fast_exp2(bb[kL - 1][d] * kLog2e);
+    for (int e = 0; e < D; ++e) dgam = __builtin_fmaf(Gs[d][swz<D>(d, e)], C0s[d][e], dgam);
+    float accg = extra + dgam * fast_exp2(bb[kL - 1][swz<D>(kL - 1, d)] * kLog2e);
     float* dG = a.dg + (int64_t)p.n * a.T * D;
     for (int j = kL - 1; j >= 0; --j) {
-      accg += dbs[j][d];
+      accg += Dx[j][d];
       if (j < p.len) dG[(int64_t)(p.t0 + j) * D + d] = accg;
     }
   }
