@@ -157,6 +157,31 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
   __syncthreads();
 }
 
+// One 32 x 32 block (rows ab.., columns eb..) of X^T Y, the contraction over
+// the kL rows of the chunk (X, Y plain [kL][D] arrays), on the matrix cores
+// (32x32x2 fp32 steps; lane group g takes the rows of parity g).
+template <int D>
+__device__ __forceinline__ floatx16 gram_block(const float (*X)[D], const float (*Y)[D], int ab, int eb) {
+  const int lane = threadIdx.x & 63, ln = lane & 31, lg = lane >> 5;
+  floatx16 acc;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
+#pragma unroll 8
+  for (int s2 = 0; s2 < kL / 2; ++s2) {
+    const int r = 2 * s2 + lg;
+    acc = mfma32f(X[r][ab + ln], Y[r][eb + ln], acc);
+  }
+  return acc;
+}
+
+// Stores a 32 x 32 accumulator block at (ab, eb) of a dense D x D matrix.
+template <int D>
+__device__ __forceinline__ void store_block(float* out, const floatx16& acc, int ab, int eb) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) out[(ab + acc_row(v, lane >> 5)) * D + eb + (lane & 31)] = acc[v];
+}
+
 // Per chunk: dC[a][e] = sum_j kt_{j,a} e^{b_last,a - b_j,a} v_{j,e}, gamma_a = e^{b_last,a}.
 template <typename TI, int D>
 __global__ __launch_bounds__(kLT) void linear_state_kernel(LinearArgs a) {
@@ -172,32 +197,12 @@ __global__ __launch_bounds__(kLT) void linear_state_kernel(LinearArgs a) {
   __syncthreads();
   const int64_t base = ((int64_t)p.n * a.nchunks + p.c);
   if (tid < D) a.gamma[base * D + tid] = fast_exp2(bb[kL - 1][tid] * kLog2e);
-  // thread tile: TA rows a x TE columns e of dC
-  constexpr int TE = D <= 64 ? 4 : 8;
-  constexpr int TA = D * D / (kLT * TE);
-  constexpr int NE = D / TE;
-  const int a0 = (tid / NE) * TA, e0 = (tid % NE) * TE;
-  float acc[TA][TE];
-#pragma unroll
-  for (int i = 0; i < TA; ++i)
-#pragma unroll
-    for (int j = 0; j < TE; ++j) acc[i][j] = 0.0f;
-  for (int r = 0; r < kL; ++r) {
-    float kr[TA], vr[TE];
-#pragma unroll
-    for (int i = 0; i < TA; ++i) kr[i] = kt[r][a0 + i];
-#pragma unroll
-    for (int j = 0; j < TE; ++j) vr[j] = vv[r][e0 + j];
-#pragma unroll
-    for (int i = 0; i < TA; ++i)
-#pragma unroll
-      for (int j = 0; j < TE; ++j) acc[i][j] = __builtin_fmaf(kr[i], vr[j], acc[i][j]);
+  // dC on the matrix cores, 32 x 32 blocks, wave w takes blocks w, w + 4, ...
+  constexpr int NBE = D / 32;
+  for (int bk = __builtin_amdgcn_readfirstlane(tid >> 6); bk < NBE * NBE; bk += kLT / 64) {
+    const int ab = 32 * (bk / NBE), eb = 32 * (bk % NBE);
+    store_block<D>(a.dstate + base * D * D, gram_block<D>(kt, vv, ab, eb), ab, eb);
   }
-  float* dC = a.dstate + base * D * D;
-#pragma unroll
-  for (int i = 0; i < TA; ++i)
-#pragma unroll
-    for (int j = 0; j < TE; ++j) dC[(a0 + i) * D + e0 + j] = acc[i][j];
 }
 
 // The state scans. Per head and state element, over the chunks c:
@@ -499,44 +504,14 @@ __global__ __launch_bounds__(kLT) void linear_bstate_kernel(LinearArgs a) {
   __syncthreads();
   const int64_t base = ((int64_t)p.n * a.nchunks + p.c);
   if (tid < D) a.gamma[base * D + tid] = fast_exp2(bb[kL - 1][tid] * kLog2e);
-  constexpr int TE = 4;
-  constexpr int TA = D * D / (kLT * TE);
-  constexpr int NE = D / TE;
-  const int a0 = (tid / NE) * TA, e0 = (tid % NE) * TE;
-  float c1[TA][TE], c2[TA][TE];
-#pragma unroll
-  for (int i = 0; i < TA; ++i)
-#pragma unroll
-    for (int j = 0; j < TE; ++j) c1[i][j] = c2[i][j] = 0.0f;
-  for (int r = 0; r < kL; ++r) {
-    float kr[TA], qr[TA], vr[TE], gr[TE];
-#pragma unroll
-    for (int i = 0; i < TA; ++i) {
-      kr[i] = kt[r][a0 + i];
-      qr[i] = qt[r][a0 + i];
-    }
-#pragma unroll
-    for (int j = 0; j < TE; ++j) {
-      vr[j] = vv[r][e0 + j];
-      gr[j] = dy[r][e0 + j];
-    }
-#pragma unroll
-    for (int i = 0; i < TA; ++i)
-#pragma unroll
-      for (int j = 0; j < TE; ++j) {
-        c1[i][j] = __builtin_fmaf(kr[i], vr[j], c1[i][j]);
-        c2[i][j] = __builtin_fmaf(qr[i], gr[j], c2[i][j]);
-      }
+  // dC = Kd^T v and P = Qe^T dY on the matrix cores, 32 x 32 blocks; wave w
+  // takes blocks w, w + 4, ... of the two products
+  constexpr int NBE = D / 32, NBB = NBE * NBE;
+  for (int bk = __builtin_amdgcn_readfirstlane(tid >> 6); bk < 2 * NBB; bk += kLT / 64) {
+    const int ab = 32 * ((bk % NBB) / NBE), eb = 32 * (bk % NBE);
+    if (bk < NBB) store_block<D>(a.dstate + base * D * D, gram_block<D>(kt, vv, ab, eb), ab, eb);
+    else store_block<D>(a.pstate + base * D * D, gram_block<D>(qt, dy, ab, eb), ab, eb);
   }
-  float* dC = a.dstate + base * D * D;
-  float* P = a.pstate + base * D * D;
-#pragma unroll
-  for (int i = 0; i < TA; ++i)
-#pragma unroll
-    for (int j = 0; j < TE; ++j) {
-      dC[(a0 + i) * D + e0 + j] = c1[i][j];
-      P[(a0 + i) * D + e0 + j] = c2[i][j];
-    }
 }
 
 // One 16 x 16 tile of a product on the matrix cores (16x16x4 fp32 steps):
