@@ -17,6 +17,7 @@
 // Every lane group keeps its own running (m, l) and VEC channels of z, and the
 // groups of a workgroup are merged at the end.
 #include "kernels.h"
+#include "lanes.h"
 
 namespace rel {
 
@@ -123,8 +124,7 @@ __global__ __launch_bounds__(kDT) void decode_states_kernel(DecodeArgs a) {
       float d = 0.0f;
 #pragma unroll
       for (int e = 0; e < VEC; ++e) d = __builtin_fmaf(q[e], kx[u][e], d);
-#pragma unroll
-      for (int o = LPK / 2; o >= 1; o >>= 1) d += __shfl_xor(d, o, 64);
+      d = lane_group_sum<LPK>(d);
       if (ok[u]) {
         const float uu = d * a.scale;
         const float E = uu * sigm(uu);             // Exchange map, eq. (2)

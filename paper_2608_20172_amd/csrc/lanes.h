@@ -25,4 +25,20 @@ __device__ __forceinline__ float group_sum(float x) {
   return x;
 }
 
+// Sum over each aligned group of G lanes, G a power of two up to 64: DPP
+// within rows of 16 lanes, then lane exchanges across rows.
+template <int G>
+__device__ __forceinline__ float lane_group_sum(float x) {
+  if constexpr (G == 1) {
+    return x;
+  } else if constexpr (G <= 16) {
+    return group_sum<G>(x);
+  } else {
+    x = group_sum<16>(x);
+    x += __shfl_xor(x, 16, 64);
+    if constexpr (G == 64) x += __shfl_xor(x, 32, 64);
+    return x;
+  }
+}
+
 }  // namespace rel
