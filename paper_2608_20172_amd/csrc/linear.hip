@@ -21,7 +21,7 @@ namespace rel {
 namespace {
 
 constexpr int kL = 64;      // tokens per chunk
-constexpr int kLT = 256;    // threads per workgroup of the state kernels
+constexpr int kLT = 512;    // threads per workgroup of the state kernels
 constexpr int kTPR = 8;     // threads per token row in the output and gradient kernels
 constexpr int kLT2 = kL * kTPR;
 constexpr int kTPRG = 16;   // threads per token row in the gradient kernel
@@ -53,7 +53,8 @@ __device__ __forceinline__ int swz(int r, int c) {
 // Loads the chunk into LDS as fp32 and forms qt = S ^p1, kt = S ^p2 (rows past
 // the sequence are zero), v, optionally dY, and b = running sum of g (zero g
 // past the end, so b stays at its last value). SWZ_VD stores v and dY
-// swizzled (swz), SWZ_QKB qt, kt and b. One wave per row for the norms and S.
+// swizzled (swz), SWZ_QKB qt, kt and b; qt may be null (not stored). One wave
+// per row for the norms and S.
 template <typename TI, int D, int NT, bool SWZ_VD = false, bool WITH_DY = false, bool SWZ_QKB = false>
 __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& p, float (*qt)[D], float (*kt)[D],
                                            float (*vv)[D], float (*bb)[D], float* Srow,
@@ -125,7 +126,7 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
         const int d = lane + 64 * u;
         if (d < D) {
           const int dq = SWZ_QKB ? swz<D>(r, d) : d;
-          qt[r][dq] = x1[kb][u] * i1;
+          if (qt) qt[r][dq] = x1[kb][u] * i1;
           kt[r][dq] = x2[kb][u] * i2;
         }
       }
@@ -185,9 +186,9 @@ __device__ __forceinline__ void store_block(float* out, const floatx16& acc, int
 // Per chunk: dC[a][e] = sum_j kt_{j,a} e^{b_last,a - b_j,a} v_{j,e}, gamma_a = e^{b_last,a}.
 template <typename TI, int D>
 __global__ __launch_bounds__(kLT) void linear_state_kernel(LinearArgs a) {
-  __shared__ float qt[kL][D], kt[kL][D], vv[kL][D], bb[kL][D];
+  __shared__ float kt[kL][D], vv[kL][D], bb[kL][D];  // qt is not needed here
   const ChunkPos p = chunk_pos(a);
-  load_chunk<TI, D, kLT>(a, p, qt, kt, vv, bb, nullptr);
+  load_chunk<TI, D, kLT>(a, p, nullptr, kt, vv, bb, nullptr);
   const int tid = threadIdx.x;
   // kt <- kt e^{b_last - b}
   for (int i = tid; i < kL * D; i += kLT) {

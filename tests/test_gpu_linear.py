@@ -118,7 +118,7 @@ def test_linear_backward(B, H, T, D, dtype):
     check_linear_bwd(x, dtype)
 
 
-@pytest.mark.parametrize("gmax", [1e-3, 8.0])
+@pytest.mark.parametrize("gmax", [1e-3, 8.0, 80.0])
 def test_linear_backward_retention_range(gmax):
     x = _prep(1, 2, 200, 64, "f32", seed=1500, gmax=gmax)
     check_linear_bwd(x, "f32")
