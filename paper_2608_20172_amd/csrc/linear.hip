@@ -779,17 +779,46 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
 #pragma unroll
   for (int i = 0; i < QW; ++i) Dx[r][q0 + i] = db[i];
   __syncthreads();
-  // dg: reverse running sum of db down the chunk, with the last row's extra terms
-  if (tid < D) {
-    const int d = tid;
-    float extra = 0.0f, dgam = 0.0f;
-    for (int j = 0; j < kL; ++j) extra += tmp[j][d];
-    for (int e = 0; e < D; ++e) dgam = __builtin_fmaf(Gs[d][swz<D>(d, e)], C0s[d][e], dgam);
-    float accg = extra + dgam * fast_exp2(bb[kL - 1][swz<D>(kL - 1, d)] * kLog2e);
+  // dg: reverse running sum of db down the chunk, plus the last row's extra
+  // terms (column sums of dKd Kd, and dgamma e^{b_last}), which reach every row.
+  // Thread (channel d, segment sg of RS rows) sums its rows from the bottom and
+  // its shares of the extra terms; the partials meet in LDS (dy and vv are free).
+  {
+    constexpr int NSG = kLTG / D, RS = kL / NSG, ES = D / NSG;
+    static_assert(RS * NSG == kL && ES * NSG == D && 2 * kLTG <= kL * D, "segments split evenly");
+    const int d = tid % D, sg = tid / D;
+    float* PT = &dy[0][0];         // [NSG][D]: segment totals of db
+    float* PE = &dy[0][0] + kLTG;  // [NSG][D]: column sums of dKd Kd over the segment
+    float* PG = &vv[0][0];         // [NSG][D]: shares of dgamma = sum_e G C0
+    float suf[RS];
+    float acc_t = 0.0f, ex = 0.0f, gm = 0.0f;
+#pragma unroll
+    for (int i = RS - 1; i >= 0; --i) {
+      acc_t += Dx[sg * RS + i][d];
+      suf[i] = acc_t;
+      ex += tmp[sg * RS + i][d];
+    }
+#pragma unroll
+    for (int i = 0; i < ES; ++i) {
+      const int e = sg * ES + i;
+      gm = __builtin_fmaf(Gs[d][swz<D>(d, e)], C0s[d][e], gm);
+    }
+    PT[sg * D + d] = acc_t;
+    PE[sg * D + d] = ex;
+    PG[sg * D + d] = gm;
+    __syncthreads();
+    float extra = 0.0f, dgam = 0.0f, later = 0.0f;
+    for (int u = 0; u < NSG; ++u) {
+      extra += PE[u * D + d];
+      dgam += PG[u * D + d];
+      if (u > sg) later += PT[u * D + d];
+    }
+    const float base_g = extra + dgam * fast_exp2(bb[kL - 1][swz<D>(kL - 1, d)] * kLog2e) + later;
     float* dG = a.dg + (int64_t)p.n * a.T * D;
-    for (int j = kL - 1; j >= 0; --j) {
-      accg += Dx[j][d];
-      if (j < p.len) dG[(int64_t)(p.t0 + j) * D + d] = accg;
+#pragma unroll
+    for (int i = 0; i < RS; ++i) {
+      const int j = sg * RS + i;
+      if (j < p.len) dG[(int64_t)(p.t0 + j) * D + d] = base_g + suf[i];
     }
   }
   // through qt = S p1 / |p1|, kt = S p2 / |p2|, S = sigmoid(scale p1 . p2 / tau_S)
