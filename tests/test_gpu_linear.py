@@ -129,11 +129,23 @@ def test_linear_backward_long():
     check_linear_bwd(x, "bf16", heads=[(0, 1)])
 
 
-@pytest.mark.parametrize("T,gmax", [(1025, 0.02), (3000, 0.005)])
-def test_linear_backward_scan_segments(T, gmax):
+@pytest.mark.parametrize("T,D,gmax", [(1025, 64, 0.02), (3000, 64, 0.005), (2100, 32, 0.01)])
+def test_linear_backward_scan_segments(T, D, gmax):
     """Forward and reverse state scans across segments of 16 chunks."""
-    x = _prep(1, 1, T, 64, "f32", seed=1650 + T, gmax=gmax)
+    x = _prep(1, 1, T, D, "f32", seed=1650 + T + D, gmax=gmax)
     check_linear_bwd(x, "f32")
+
+
+def test_linear_backward_strided():
+    """Token-major tensors (strides of a [B, T, H, D] layout) give the same
+    gradients as contiguous ones."""
+    x = _prep(2, 3, 150, 64, "bf16", seed=1680)
+    a = R.relation_linear_bwd(x["p1"], x["p2"], x["v"], x["g"], x["dy"])
+    t = lambda z: z.transpose(1, 2).contiguous().transpose(1, 2)
+    b = R.relation_linear_bwd(t(x["p1"]), t(x["p2"]), t(x["v"]), x["g"], t(x["dy"]))
+    torch.cuda.synchronize()
+    for n in ("dp1", "dp2", "dv", "dg"):
+        assert torch.equal(a[n].contiguous(), b[n].contiguous()), n
 
 
 def test_linear_backward_repeatable():
