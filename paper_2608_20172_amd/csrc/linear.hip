@@ -50,6 +50,25 @@ __device__ __forceinline__ int swz(int r, int c) {
   return (((c >> 2) ^ (r & (D / 4 - 1))) << 2) | (c & 3);
 }
 
+// 16 bytes of a row (8 bf16 or 4 fp32 elements) as floats.
+template <typename TI> struct Vec16;
+template <> struct Vec16<bf16> {
+  static __device__ __forceinline__ void load(const bf16* p, float (&x)[8]) {
+    const uintx4 u = *reinterpret_cast<const uintx4*>(p);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      x[2 * t] = bf16_lo(u[t]);
+      x[2 * t + 1] = bf16_hi(u[t]);
+    }
+  }
+};
+template <> struct Vec16<float> {
+  static __device__ __forceinline__ void load(const float* p, float (&x)[4]) {
+    const float4 u = *reinterpret_cast<const float4*>(p);
+    x[0] = u.x; x[1] = u.y; x[2] = u.z; x[3] = u.w;
+  }
+};
+
 // Loads the chunk into LDS as fp32 and forms qt = S ^p1, kt = S ^p2 (rows past
 // the sequence are zero), v, optionally dY, and b = running sum of g (zero g
 // past the end, so b stays at its last value). SWZ_VD stores v and dY
@@ -70,6 +89,61 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
   const TI* V = (const TI*)a.v + hoff;
   const TI* DY = WITH_DY ? (const TI*)a.dy + hoff : nullptr;
   const float* G = a.g + (int64_t)p.n * a.T * D;
+  auto col = [&](bool swzd, int row, int c) { return swzd ? swz<D>(row, c) : c; };
+  if (a.vec16) {
+    // 16 bytes per lane: LPR lanes hold a row, a wave RPI rows per step. Rows
+    // past the sequence read its last row and then count as zero.
+    constexpr int EPL = 16 / (int)sizeof(TI), LPR = D / EPL, RPI = 64 / LPR, NW = NT / 64;
+    static_assert(LPR >= 2 && LPR <= 64 && EPL % 4 == 0, "a row is whole 16-byte chunks over a lane group");
+    constexpr int STEPS = (kL + NW * RPI - 1) / (NW * RPI);
+    const int cg = lane % LPR, c0 = cg * EPL;
+#pragma unroll
+    for (int st = 0; st < STEPS; ++st) {
+      const int r = st * NW * RPI + w * RPI + lane / LPR;
+      if (st * NW * RPI + w * RPI < kL) {  // wave-uniform: the wave's rows are all in the chunk
+        const int64_t row = (int64_t)min(p.t0 + r, a.T - 1);
+        float x1[EPL], x2[EPL], vx[EPL], gx[EPL], dx[EPL];
+        Vec16<TI>::load(P1 + row * a.st + c0, x1);
+        Vec16<TI>::load(P2 + row * a.st + c0, x2);
+        Vec16<TI>::load(V + row * a.st + c0, vx);
+        if constexpr (WITH_DY) Vec16<TI>::load(DY + row * a.st + c0, dx);
+#pragma unroll
+        for (int e = 0; e < EPL; e += 4) {
+          const float4 g4 = *reinterpret_cast<const float4*>(G + row * D + c0 + e);
+          gx[e] = g4.x; gx[e + 1] = g4.y; gx[e + 2] = g4.z; gx[e + 3] = g4.w;
+        }
+        const bool ok = r < p.len;
+        float s11 = 0.0f, s22 = 0.0f, s12 = 0.0f;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) {
+          if (!ok) x1[e] = x2[e] = vx[e] = gx[e] = dx[e] = 0.0f;
+          s11 += x1[e] * x1[e];
+          s22 += x2[e] * x2[e];
+          s12 += x1[e] * x2[e];
+        }
+        s11 = lane_group_sum<LPR>(s11);
+        s22 = lane_group_sum<LPR>(s22);
+        s12 = lane_group_sum<LPR>(s12);
+        const float S = ok ? 1.0f / (1.0f + expf(-s12 * a.scale * a.inv_tau)) : 0.0f;
+        const float i1 = ok && s11 > 0.0f ? S * rsqrtf(s11) : 0.0f;
+        const float i2 = ok && s22 > 0.0f ? S * rsqrtf(s22) : 0.0f;
+#pragma unroll
+        for (int e = 0; e < EPL; e += 4) {
+          const int c = c0 + e;
+          *reinterpret_cast<float4*>(&vv[r][col(SWZ_VD, r, c)]) = make_float4(vx[e], vx[e + 1], vx[e + 2], vx[e + 3]);
+          *reinterpret_cast<float4*>(&bb[r][col(SWZ_QKB, r, c)]) = make_float4(gx[e], gx[e + 1], gx[e + 2], gx[e + 3]);
+          if constexpr (WITH_DY)
+            *reinterpret_cast<float4*>(&dyl[r][col(SWZ_VD, r, c)]) = make_float4(dx[e], dx[e + 1], dx[e + 2], dx[e + 3]);
+          if (qt)
+            *reinterpret_cast<float4*>(&qt[r][col(SWZ_QKB, r, c)]) =
+                make_float4(x1[e] * i1, x1[e + 1] * i1, x1[e + 2] * i1, x1[e + 3] * i1);
+          *reinterpret_cast<float4*>(&kt[r][col(SWZ_QKB, r, c)]) =
+              make_float4(x2[e] * i2, x2[e + 1] * i2, x2[e + 2] * i2, x2[e + 3] * i2);
+        }
+        if (cg == 0 && Srow) Srow[r] = S;
+      }
+    }
+  } else {
   // rows in batches whose loads are issued together: the loads are
   // unconditional (rows past the sequence read its last row, then count as
   // zero) so that the compiler can hoist them over the reductions
@@ -133,27 +207,28 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
       if (lane == 0 && Srow) Srow[r] = S;
     }
   }
+  }
   __syncthreads();
   // running sum of g down the chunk: thread (channel, segment of SR rows) sums
   // its segment in place, then adds the totals of the segments above it
   constexpr int NSEG = NT / D, SR = kL / NSEG;
   const int d = tid % D, sg = tid / D;
-  auto col = [&](int row) { return SWZ_QKB ? swz<D>(row, d) : d; };
+  auto bcol = [&](int row) { return col(SWZ_QKB, row, d); };
   float x[SR];
   float acc = 0.0f;
 #pragma unroll
-  for (int i = 0; i < SR; ++i) x[i] = bb[sg * SR + i][col(sg * SR + i)];
+  for (int i = 0; i < SR; ++i) x[i] = bb[sg * SR + i][bcol(sg * SR + i)];
 #pragma unroll
   for (int i = 0; i < SR; ++i) x[i] = acc += x[i];
 #pragma unroll
-  for (int i = 0; i < SR; ++i) bb[sg * SR + i][col(sg * SR + i)] = x[i];
+  for (int i = 0; i < SR; ++i) bb[sg * SR + i][bcol(sg * SR + i)] = x[i];
   __syncthreads();
   float off = 0.0f;
-  for (int u = 0; u < sg; ++u) off += bb[u * SR + SR - 1][col(u * SR + SR - 1)];
+  for (int u = 0; u < sg; ++u) off += bb[u * SR + SR - 1][bcol(u * SR + SR - 1)];
   __syncthreads();  // every segment total read
   if (sg > 0) {
 #pragma unroll
-    for (int i = 0; i < SR; ++i) bb[sg * SR + i][col(sg * SR + i)] = x[i] + off;
+    for (int i = 0; i < SR; ++i) bb[sg * SR + i][bcol(sg * SR + i)] = x[i] + off;
   }
   __syncthreads();
 }

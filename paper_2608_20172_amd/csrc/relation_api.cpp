@@ -9,6 +9,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
+#include <initializer_list>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -1122,6 +1123,16 @@ static LinearPlan plan_linear(const rel_problem* p) {
   return L;
 }
 
+// The chunk loads move 16 bytes per lane when every row of p1, p2, v (and dY)
+// starts on a 16-byte boundary and g is 16-byte aligned.
+static int linear_vec16(const rel_problem* p, std::initializer_list<const void*> rows, const float* g) {
+  const int64_t epl = 16 / (int64_t)elem_size(p->dtype);
+  if (p->stride_b % epl || p->stride_h % epl || p->stride_t % epl || ((uintptr_t)g & 15)) return 0;
+  for (const void* x : rows)
+    if ((uintptr_t)x & 15) return 0;
+  return 1;
+}
+
 static void set_linear_workspace(rel::LinearArgs& a, const LinearPlan& L, char* ws, bool backward) {
   a.dstate = (float*)(ws + L.dstate);
   a.gamma = (float*)(ws + L.gamma);
@@ -1178,6 +1189,7 @@ rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void*
   a.inv_tau = 1.0f / p->tau_s;
   a.nchunks = linear_chunks(p);
   a.nseg = linear_segments(p);
+  a.vec16 = linear_vec16(p, {p1, p2, v}, g);
   set_linear_workspace(a, L, (char*)workspace, false);
   const hipError_t e = rel::launch_linear_fwd(a, p->dtype, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "Linear Relation launch");
@@ -1238,6 +1250,7 @@ rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void*
   a.inv_tau = 1.0f / p->tau_s;
   a.nchunks = linear_chunks(p);
   a.nseg = linear_segments(p);
+  a.vec16 = linear_vec16(p, {p1, p2, v, dout}, g);
   set_linear_workspace(a, L, (char*)workspace, true);
   const hipError_t e = rel::launch_linear_bwd(a, p->dtype, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "Linear Relation backward launch");

@@ -148,6 +148,25 @@ def test_linear_backward_strided():
         assert torch.equal(a[n].contiguous(), b[n].contiguous()), n
 
 
+def _misaligned(t):
+    """The same values in a view that starts one element past a 16-byte boundary."""
+    buf = torch.empty(t.numel() + 1, dtype=t.dtype, device=t.device)
+    v = buf[1:].view(t.shape)
+    v.copy_(t)
+    return v
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_linear_unaligned_rows(dtype):
+    """Rows that do not start on 16-byte boundaries take the element-wise chunk
+    loads; forward and backward against the oracle."""
+    x = _prep(1, 2, 200, 64, dtype, seed=1690)
+    for n in ("p1", "p2", "v", "dy", "g"):
+        x[n] = _misaligned(x[n])
+    check_linear_fwd(x, dtype)
+    check_linear_bwd(x, dtype)
+
+
 def test_linear_backward_repeatable():
     x = _prep(2, 2, 300, 64, "bf16", seed=1700)
     a = R.relation_linear_bwd(x["p1"], x["p2"], x["v"], x["g"], x["dy"])
