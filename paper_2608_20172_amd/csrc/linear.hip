@@ -10,9 +10,11 @@
 //             + sum_{j<t in chunk} [sum_a qt_{t,a} kt_{j,a} e^{b_{t,a} - b_{j,a}}] I~_j   (intra)
 //   C_end = Diag(e^{b_last}) C0 + sum_j (kt_j e^{b_last - b_j}) I~_j^T.
 // Every exponent is <= 0 (g <= 0), so nothing overflows, whatever the decay.
-// Three launches: per chunk the state contribution (dC, gamma = e^{b_last});
-// per head the scan over chunks (the state entering every chunk); per chunk the
-// output. All arithmetic is fp32 on the vector units.
+// Forward launches: per chunk the state contribution (dC, gamma = e^{b_last});
+// the scan over chunks in segments (the state entering every chunk); per chunk
+// the output. All arithmetic is fp32: dense products on the matrix cores
+// (fp32 MFMA), the decay weights and the diagonal sub-blocks of the intra-chunk
+// pairs on the vector units.
 #include "kernels.h"
 #include "lanes.h"
 
@@ -22,8 +24,7 @@ namespace {
 
 constexpr int kL = 64;      // tokens per chunk
 constexpr int kLT = 512;    // threads per workgroup of the state kernels
-constexpr int kTPR = 8;     // threads per token row in the output and gradient kernels
-constexpr int kLT2 = kL * kTPR;
+constexpr int kLT2 = 512;   // threads per workgroup of the output kernel (8 waves)
 constexpr int kTPRG = 16;   // threads per token row in the gradient kernel
 constexpr int kLTG = kL * kTPRG;
 constexpr int kRowsPerWave = 64 / kTPRG;
