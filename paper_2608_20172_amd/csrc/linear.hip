@@ -419,26 +419,40 @@ __device__ __forceinline__ void chunk_scores(const float (*qt)[D], const float (
     else A[t][swz<kL>(t, j)] = x;
   };
   if (w < NSB) {
-    // lane -> row t = SB w + lane / 4 and columns j = SB w + lane % 4 + 4 m
-    const int t = SB * w + (lane >> 2), jq = lane & 3;
-    float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    // the block's 120 pairs j < t, two per lane (slot s: pair lane + 64 s in
+    // row-major order); the rest of the block is zero
+    const int base = SB * w, t = base + (lane >> 2), jq = lane & 3;
+#pragma unroll
+    for (int m = 0; m < 4; ++m) put(t, base + jq + 4 * m, 0.0f);  // same wave: the pairs land after
+    int tt[2], jj[2];
+    bool live[2];
+#pragma unroll
+    for (int sl = 0; sl < 2; ++sl) {
+      const int idx = lane + 64 * sl;
+      live[sl] = idx < SB * (SB - 1) / 2;
+      int r = 1, rem = live[sl] ? idx : 0;
+      while (rem >= r) {  // row r (of the block) holds r pairs
+        rem -= r;
+        ++r;
+      }
+      tt[sl] = base + r;
+      jj[sl] = base + rem;
+    }
+    float acc[2] = {0.0f, 0.0f};
 #pragma unroll 2
     for (int c = 0; c < CH; ++c) {
-      const floatx4 q4 = ld4<D>(qt, t, c), bt4 = ld4<D>(bb, t, c);
 #pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        const int j = SB * w + jq + 4 * m;
-        const floatx4 k4 = ld4<D>(kt, j, c), bj4 = ld4<D>(bb, j, c);
+      for (int sl = 0; sl < 2; ++sl) {
+        const floatx4 q4 = ld4<D>(qt, tt[sl], c), bt4 = ld4<D>(bb, tt[sl], c);
+        const floatx4 k4 = ld4<D>(kt, jj[sl], c), bj4 = ld4<D>(bb, jj[sl], c);
 #pragma unroll
         for (int u = 0; u < 4; ++u)
-          acc[m] = __builtin_fmaf(q4[u] * k4[u], fast_exp2((bt4[u] - bj4[u]) * kLog2e), acc[m]);
+          acc[sl] = __builtin_fmaf(q4[u] * k4[u], fast_exp2((bt4[u] - bj4[u]) * kLog2e), acc[sl]);
       }
     }
 #pragma unroll
-    for (int m = 0; m < 4; ++m) {
-      const int j = SB * w + jq + 4 * m;
-      put(t, j, j < t ? acc[m] : 0.0f);  // above the diagonal: zero
-    }
+    for (int sl = 0; sl < 2; ++sl)
+      if (live[sl]) put(tt[sl], jj[sl], acc[sl]);
     // the blocks above the diagonal block's row band are zero
     for (int jb = w + 1; jb < NSB; ++jb) {
 #pragma unroll
