@@ -149,8 +149,8 @@ struct LinearArgs {
   void* dp2;
   void* dv;
   float* dg;             // [B, H, T, D] fp32, dense
-  // 1: p1, p2, v (and dy) rows start on 16-byte boundaries and g is 16-byte
-  // aligned, so the chunk loads move 16 bytes per lane
+  // 1: p1, p2, v (and dy, dp1, dp2, dv) rows start on 16-byte boundaries and
+  // g is 16-byte aligned, so the chunk loads move 16 bytes per lane
   int vec16;
   // state scans over segments of linear_scan_segment() chunks
   int nseg;

@@ -70,6 +70,32 @@ template <> struct Vec16<float> {
   }
 };
 
+// 4 consecutive elements (8 bytes of bf16, 16 of fp32), for rows that start
+// on 16-byte boundaries and offsets that are multiples of 4.
+template <typename TI> struct Vec4;
+template <> struct Vec4<bf16> {
+  static __device__ __forceinline__ void load(const bf16* p, float (&x)[4]) {
+    const uint2 u = *reinterpret_cast<const uint2*>(p);
+    x[0] = bf16_lo(u.x); x[1] = bf16_hi(u.x); x[2] = bf16_lo(u.y); x[3] = bf16_hi(u.y);
+  }
+  static __device__ __forceinline__ void store(bf16* p, const float (&x)[4]) {
+    typedef bf16 bf16x4 __attribute__((ext_vector_type(4)));
+    bf16x4 o;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) o[t] = (bf16)x[t];
+    *reinterpret_cast<bf16x4*>(p) = o;
+  }
+};
+template <> struct Vec4<float> {
+  static __device__ __forceinline__ void load(const float* p, float (&x)[4]) {
+    const float4 u = *reinterpret_cast<const float4*>(p);
+    x[0] = u.x; x[1] = u.y; x[2] = u.z; x[3] = u.w;
+  }
+  static __device__ __forceinline__ void store(float* p, const float (&x)[4]) {
+    *reinterpret_cast<float4*>(p) = make_float4(x[0], x[1], x[2], x[3]);
+  }
+};
+
 // Loads the chunk into LDS as fp32 and forms qt = S ^p1, kt = S ^p2 (rows past
 // the sequence are zero), v, optionally dY, and b = running sum of g (zero g
 // past the end, so b stays at its last value). SWZ_VD stores v and dY
@@ -821,10 +847,18 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
   const TI* P2 = (const TI*)a.p2 + hoff + prow * a.st;
   const bool ok = r < p.len;
   float x1[QW], x2[QW];
+  if constexpr (QW == 4) {
+    if (a.vec16) {
+      Vec4<TI>::load(P1 + q0, x1);
+      Vec4<TI>::load(P2 + q0, x2);
+    }
+  }
+  if (QW != 4 || !a.vec16) {
 #pragma unroll
-  for (int i = 0; i < QW; ++i) {
-    x1[i] = Elem<TI>::load(P1 + q0 + i);
-    x2[i] = Elem<TI>::load(P2 + q0 + i);
+    for (int i = 0; i < QW; ++i) {
+      x1[i] = Elem<TI>::load(P1 + q0 + i);
+      x2[i] = Elem<TI>::load(P2 + q0 + i);
+    }
   }
 #pragma unroll
   for (int i = 0; i < QW; ++i) {
@@ -940,14 +974,27 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
     TI* DP1 = (TI*)a.dp1 + hoff + (int64_t)(p.t0 + r) * a.st;
     TI* DP2 = (TI*)a.dp2 + hoff + (int64_t)(p.t0 + r) * a.st;
     TI* DV = (TI*)a.dv + hoff + (int64_t)(p.t0 + r) * a.st;
+    float g1[QW], g2[QW];
 #pragma unroll
     for (int i = 0; i < QW; ++i) {
       // d^p1 = S dqt; dp1 = dU p2 + (d^p1 - ^p1 (^p1 . d^p1)) / |p1|
-      const float g1 = dU * x2[i] + S * (dq[i] - x1[i] * in1 * h1d) * in1;
-      const float g2 = dU * x1[i] + S * (dk[i] - x2[i] * in2 * h2d) * in2;
-      Elem<TI>::store(DP1 + q0 + i, g1);
-      Elem<TI>::store(DP2 + q0 + i, g2);
-      Elem<TI>::store(DV + q0 + i, dv[i]);
+      g1[i] = dU * x2[i] + S * (dq[i] - x1[i] * in1 * h1d) * in1;
+      g2[i] = dU * x1[i] + S * (dk[i] - x2[i] * in2 * h2d) * in2;
+    }
+    if constexpr (QW == 4) {
+      if (a.vec16) {
+        Vec4<TI>::store(DP1 + q0, g1);
+        Vec4<TI>::store(DP2 + q0, g2);
+        Vec4<TI>::store(DV + q0, dv);
+      }
+    }
+    if (QW != 4 || !a.vec16) {
+#pragma unroll
+      for (int i = 0; i < QW; ++i) {
+        Elem<TI>::store(DP1 + q0 + i, g1[i]);
+        Elem<TI>::store(DP2 + q0 + i, g2[i]);
+        Elem<TI>::store(DV + q0 + i, dv[i]);
+      }
     }
   }
 }

@@ -1123,8 +1123,9 @@ static LinearPlan plan_linear(const rel_problem* p) {
   return L;
 }
 
-// The chunk loads move 16 bytes per lane when every row of p1, p2, v (and dY)
-// starts on a 16-byte boundary and g is 16-byte aligned.
+// The chunk loads (and the gradient stores) move 16 bytes per lane when every
+// row of p1, p2, v (and dY, dp1, dp2, dv) starts on a 16-byte boundary and g
+// is 16-byte aligned.
 static int linear_vec16(const rel_problem* p, std::initializer_list<const void*> rows, const float* g) {
   const int64_t epl = 16 / (int64_t)elem_size(p->dtype);
   if (p->stride_b % epl || p->stride_h % epl || p->stride_t % epl || ((uintptr_t)g & 15)) return 0;
@@ -1250,7 +1251,7 @@ rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void*
   a.inv_tau = 1.0f / p->tau_s;
   a.nchunks = linear_chunks(p);
   a.nseg = linear_segments(p);
-  a.vec16 = linear_vec16(p, {p1, p2, v, dout}, g);
+  a.vec16 = linear_vec16(p, {p1, p2, v, dout, dp1, dp2, dv}, g);
   set_linear_workspace(a, L, (char*)workspace, true);
   const hipError_t e = rel::launch_linear_bwd(a, p->dtype, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "Linear Relation backward launch");
