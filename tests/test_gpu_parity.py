@@ -12,8 +12,8 @@ import torch
 import oracle
 from paper_2608_20172_amd import inputs as I
 from paper_2608_20172_amd import binding as R
-from tests.gpu_helpers import (assert_close, assert_scalar_close, lam_value, log, oracle_heads,
-                               sample_heads, to_device)
+from tests import oracle_pool as OP
+from tests.gpu_helpers import assert_close, assert_scalar_close, lam_value, log, sample_heads, to_device
 
 pytestmark = pytest.mark.gpu
 
@@ -23,6 +23,8 @@ def _gpu():
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     R.load_library()
+    yield
+    OP.close_pool()
 
 
 def _prep(inp, dtype):
@@ -40,28 +42,35 @@ def _np(t):
 
 
 def check_forward(x, dtype, heads=None, rows=None, row_block=256, with_aux=True):
-    """Fused forward vs oracle on the given heads (default: all)."""
+    """Fused forward vs oracle on the given heads (default: all), the oracle
+    heads spread over a process pool."""
     B, H, T, D = x["q"].shape
     log(f"[fwd] B={B} H={H} T={T} D={D} {dtype} lam={x['lam']:.4f}")
     out = R.relation_fwd(x["q"], x["k"], x["v"], x["lam"], want_masses=with_aux, want_lse=with_aux)
     torch.cuda.synchronize()
     heads = heads or [(b, h) for b in range(B) for h in range(H)]
-    o = _np(out["o"])
-    for (b, h) in heads:
-        f = oracle.forward(x["qr"][b, h], x["kr"][b, h], x["vr"][b, h], x["lam"],
-                           want_matrices=False, row_block=row_block, rows=rows)
-        rr = f["rows"]
-        assert_close(f"o[{b},{h}]", o[b, h][rr], f["Y"], dtype)
-        # row statistics are fp32 in both dtypes; hold them to the same bar as the outputs
-        assert_close(f"M[{b},{h}]", _np(out["row_stat"])[b, h][rr], f["M"], dtype)
-        if with_aux:
-            assert_close(f"self_mass[{b},{h}]", _np(out["self_mass"])[b, h][rr], f["self_mass"], dtype)
-            assert_close(f"exch_mass[{b},{h}]", _np(out["exch_mass"])[b, h][rr], f["exch_mass"], dtype)
-            assert_close(f"exch_lse[{b},{h}]", _np(out["exch_lse"])[b, h][rr], f["LE"], dtype)
+    refs = OP.forward_heads(x["qr"], x["kr"], x["vr"], x["lam"], heads, rows=rows)
+    compare_forward(out, heads, refs, dtype, with_aux)
     return out
 
 
+def compare_forward(out, heads, refs, dtype, with_aux=True):
+    o, M = _np(out["o"]), _np(out["row_stat"])
+    aux = {n: _np(out[n]) for n in ("self_mass", "exch_mass", "exch_lse")} if with_aux else {}
+    for (b, h), f in zip(heads, refs):
+        rr = f["rows"]
+        assert_close(f"o[{b},{h}]", o[b, h][rr], f["Y"], dtype)
+        # row statistics are fp32 in both dtypes; hold them to the same bar as the outputs
+        assert_close(f"M[{b},{h}]", M[b, h][rr], f["M"], dtype)
+        if with_aux:
+            assert_close(f"self_mass[{b},{h}]", aux["self_mass"][b, h][rr], f["self_mass"], dtype)
+            assert_close(f"exch_mass[{b},{h}]", aux["exch_mass"][b, h][rr], f["exch_mass"], dtype)
+            assert_close(f"exch_lse[{b},{h}]", aux["exch_lse"][b, h][rr], f["LE"], dtype)
+
+
 def check_backward(x, dtype, fwd, heads=None, rows=None, row_block=256, key_from=0):
+    """Fused backward vs oracle on the given heads (default: all, and then dlambda
+    against the oracle's sum over heads)."""
     B, H, T, D = x["q"].shape
     log(f"[bwd] B={B} H={H} T={T} D={D} {dtype}")
     g = R.relation_bwd(x["q"], x["k"], x["v"], fwd["o"], x["do"], x["lam"], fwd["row_stat"],
@@ -69,12 +78,17 @@ def check_backward(x, dtype, fwd, heads=None, rows=None, row_block=256, key_from
     torch.cuda.synchronize()
     all_heads = heads is None
     heads = heads or [(b, h) for b in range(B) for h in range(H)]
+    refs = OP.backward_heads(x["qr"], x["kr"], x["vr"], x["lam"], x["dor"], heads, rows=rows)
+    compare_backward(g, heads, refs, dtype, key_from=key_from, check_dlambda=all_heads and rows is None)
+    return g
+
+
+def compare_backward(g, heads, refs, dtype, key_from=0, check_dlambda=False):
     dq, dk, dv, dself = _np(g["dq"]), _np(g["dk"]), _np(g["dv"]), _np(g["dself"])
+    T = dq.shape[2]
     dlam_gpu = float(g["dlambda"].item())
     dlam_ref, terms = 0.0, 0.0
-    for (b, h) in heads:
-        r = oracle.backward(x["qr"][b, h], x["kr"][b, h], x["vr"][b, h], x["lam"], x["dor"][b, h],
-                            row_block=row_block, rows=rows)
+    for (b, h), r in zip(heads, refs):
         rr = r["rows"]
         assert_close(f"dq[{b},{h}]", dq[b, h][rr], r["dq"], dtype)
         assert_close(f"dk[{b},{h}]", dk[b, h][key_from:], r["dk"][key_from:], dtype)
@@ -82,7 +96,7 @@ def check_backward(x, dtype, fwd, heads=None, rows=None, row_block=256, key_from
         assert_close(f"dself[{b},{h}]", dself[b, h][rr], r["dS"], dtype)
         dlam_ref += r["dlam"]
         terms += float(np.sum(np.abs(np.log(rr + 1.0) * r["dS"])))
-    if all_heads and rows is None:
+    if check_dlambda:
         assert_scalar_close("dlambda", dlam_gpu, dlam_ref, terms, dtype)
     # dlambda is the ln(i)-weighted sum of the Self credits over every head and row
     i1 = np.arange(1, T + 1, dtype=np.float64)
@@ -90,7 +104,6 @@ def check_backward(x, dtype, fwd, heads=None, rows=None, row_block=256, key_from
     tot_terms = float(np.sum(np.abs(np.log(i1)[None, None, :] * dself)))
     assert abs(via_dself - dlam_gpu) <= 1e-4 * max(tot_terms, 1e-30) + 1e-6, \
         f"dlambda {dlam_gpu} vs sum ln(i) dself {via_dself}"
-    return g
 
 
 def check_materialized_backward(x, dtype, heads=None):
@@ -318,44 +331,43 @@ def test_backward_repeatability():
 
 
 # ----------------------------------------------------------------------------
-# decoder-scale workloads at full size, in the benchmark's launch configuration
+# decoder-scale workloads at full size, in the benchmark's launch configuration:
+# every head against the oracle, and one whole head of the long-context layer
 # ----------------------------------------------------------------------------
 def test_workload_dec10m_forward_vs_materialized():
     w = I.WORKLOADS["dec10m_T512"]
     x = _prep(I.make_workload_inputs(w), "bf16")
-    out = check_forward(x, "bf16", heads=sample_heads(w.B, w.H, 4))
+    out = check_forward(x, "bf16")
     m = R.relation_fwd_materialized(x["q"], x["k"], x["v"], x["lam"], want_masses=True)
     torch.cuda.synchronize()
-    for b, h in sample_heads(w.B, w.H, 2):
-        f = oracle.forward(x["qr"][b, h], x["kr"][b, h], x["vr"][b, h], x["lam"], want_matrices=False,
-                           row_block=256)
-        assert_close(f"mat.o[{b},{h}]", _np(m["o"])[b, h], f["Y"], "bf16")
-        assert_close(f"mat.exch_mass[{b},{h}]", _np(m["exch_mass"])[b, h], f["exch_mass"], "bf16")
-    # every head: the fused and the materialised outputs agree
-    assert_close("flash vs materialised o", _np(out["o"]), _np(m["o"]), "bf16")
+    heads = [(b, h) for b in range(w.B) for h in range(w.H)]
+    refs = OP.forward_heads(x["qr"], x["kr"], x["vr"], x["lam"], heads)
+    mo, mm = _np(m["o"]), _np(m["exch_mass"])
+    for (b, h), f in zip(heads, refs):
+        assert_close(f"mat.o[{b},{h}]", mo[b, h], f["Y"], "bf16")
+        assert_close(f"mat.exch_mass[{b},{h}]", mm[b, h], f["exch_mass"], "bf16")
+    assert_close("flash vs materialised o", _np(out["o"]), mo, "bf16")
 
 
 def test_workload_dec30m_forward_backward():
     w = I.WORKLOADS["dec30m_T1024"]
     x = _prep(I.make_workload_inputs(w), "bf16")
-    heads = sample_heads(w.B, w.H, 3)
-    f = check_forward(x, "bf16", heads=heads)
-    check_backward(x, "bf16", f, heads=heads)
+    f = check_forward(x, "bf16")
+    check_backward(x, "bf16", f)
 
 
 def test_workload_dec100m_forward_backward():
     w = I.WORKLOADS["dec100m_T2048"]
     x = _prep(I.make_workload_inputs(w), "bf16")
-    # include a head that holds boosted rows
     mask = I.make_workload_inputs(w)["boost_mask"]
-    heads = sample_heads(w.B, w.H, 2)
+    assert mask.any(), "the workload must hold boosted query rows"
+    f = check_forward(x, "bf16")
+    g = check_backward(x, "bf16", f)
+    # the materialised backward on the same layer: oracle on two heads (one
+    # with boosted rows), and the fused gradients on every head
     bh = np.argwhere(mask.any(axis=2))[0]
-    heads.append((int(bh[0]), int(bh[1])))
-    f = check_forward(x, "bf16", heads=heads)
-    g = check_backward(x, "bf16", f, heads=heads)
-    # the materialised backward on the same layer: oracle on two heads, and the
-    # fused gradients on every head
-    m = check_materialized_backward(x, "bf16", heads=heads[:2])
+    heads = [(0, 0), (int(bh[0]), int(bh[1]))]
+    m = check_materialized_backward(x, "bf16", heads=heads)
     for n in ("dq", "dk", "dv"):
         assert_close(f"flash vs materialised {n}", _np(g[n]), _np(m[n]), "bf16")
     dl_f, dl_m = float(g["dlambda"].item()), float(m["dlambda"].item())
@@ -365,24 +377,41 @@ def test_workload_dec100m_forward_backward():
     assert abs(dl_f - dl_m) <= 2e-2 * max(abs(dl_f), 1e-3 * terms)
 
 
-def test_workload_long_context_sampled():
-    """T = 16384, D = 128: forward on sampled rows of two heads; backward on the
-    last 256 rows of one head, which completes dk, dv for the last 256 keys;
-    properties that hold at any size for everything else."""
+def test_workload_long_context_full_head():
+    """T = 16384, D = 128: one whole head, (0, 3), forward and backward against
+    the row-blocked oracle (every row of o, M, dq, dself; every key of dk, dv,
+    including the first keys, whose sums run over all 16384 query rows), and
+    that head's share of dlambda, sum_i ln(i) dself_i. Sampled rows of a second
+    head, and sum_j dV_j = sum_i dO_i on every head."""
     w = I.WORKLOADS["long_T16384"]
     x = _prep(I.make_workload_inputs(w), "bf16")
     T = w.T
+    out = R.relation_fwd(x["q"], x["k"], x["v"], x["lam"], want_masses=True, want_lse=True)
+    g = R.relation_bwd(x["q"], x["k"], x["v"], out["o"], x["do"], x["lam"], out["row_stat"], want_dself=True)
+    torch.cuda.synchronize()
+    b, h = 0, 3
+    log(f"[long] oracle forward of head ({b},{h}), all {T} rows")
+    f = OP.forward_split(x["qr"][b, h], x["kr"][b, h], x["vr"][b, h], x["lam"])
+    compare_forward(out, [(b, h)], [f], "bf16")
+    log(f"[long] oracle backward of head ({b},{h}), all {T} rows")
+    r = OP.backward_split(x["qr"][b, h], x["kr"][b, h], x["vr"][b, h], x["lam"], x["dor"][b, h])
+    assert np.array_equal(r["rows"], np.arange(T))
+    compare_backward(g, [(b, h)], [r], "bf16")
+    # this head's dlambda term, from the GPU's dself, against the oracle's
+    lnw = np.log(np.arange(1, T + 1, dtype=np.float64))
+    ds = _np(g["dself"])[b, h]
+    head_dlam = float(np.sum(lnw * ds))
+    assert_scalar_close(f"dlambda term of head ({b},{h})", head_dlam, r["dlam"],
+                        float(np.sum(np.abs(lnw * r["dS"]))), "bf16")
+    # a second head on sampled rows
     rows = np.unique(np.concatenate([np.arange(0, 8), np.linspace(8, T - 1, 56).astype(np.int64),
                                      np.arange(T - 8, T)]))
-    f = check_forward(x, "bf16", heads=[(0, 0), (0, w.H - 1)], rows=rows)
-    tail = np.arange(T - 256, T)
-    g = check_backward(x, "bf16", f, heads=[(0, 3)], rows=tail, key_from=T - 256)
+    hb = (0, w.H - 1)
+    ref2 = OP.forward_heads(x["qr"], x["kr"], x["vr"], x["lam"], [hb], rows=rows)
+    compare_forward(out, [hb], ref2, "bf16")
     # sum_j dV_j = sum_i dO_i, because every row of F sums to one
     dv = _np(g["dv"]).sum(axis=2)
     do = x["dor"].sum(axis=2)
     err = np.abs(dv - do).max() / np.abs(do).max()
     log(f"  sum dV vs sum dO: rel err {err:.3e}")
     assert err < 2e-2
-    sm = f["self_mass"]
-    assert sm is not None
-
