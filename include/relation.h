@@ -120,6 +120,27 @@ rel_status relation_bwd(const rel_problem* p, const void* q, const void* k, cons
                         const float* row_stat, void* dq, void* dk, void* dv, float* dlambda,
                         float* dself, void* workspace, size_t workspace_bytes, void* stream);
 
+/* Backward pass for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * relation_bwd with the same kernels and results, but no workspace argument.
+ * Its scratch (the two fp32 values per row and the dlambda partials that
+ * relation_bwd takes from its workspace) lives in a device array inside the
+ * library, one copy per GPU, allocated when the library's code is loaded on
+ * that GPU and held until the process ends. The call itself allocates
+ * nothing (no hipMalloc, hipFree or allocating library routine).
+ *   Limit: relation_bwd_workspace_bytes(p) must not exceed
+ *   relation_bwd_noalloc_max_scratch_bytes() (32 MiB, about 4 million rows
+ *   B*H*T); larger problems return REL_ERR_WORKSPACE without launching.
+ *   Every call on one GPU shares that GPU's array: calls that overlap in time
+ *   on one GPU (two streams, two host threads) race and give wrong results;
+ *   serialise them. The array's contents on entry are ignored.
+ * Other arguments, errors and outputs as relation_bwd. */
+size_t relation_bwd_noalloc_max_scratch_bytes(void);
+rel_status relation_bwd_noalloc(const rel_problem* p, const void* q, const void* k, const void* v,
+                                const void* o, const void* dout, const float* lambda,
+                                const float* row_stat, void* dq, void* dk, void* dv,
+                                float* dlambda, float* dself, void* stream);
+
 /* Materialised Full Relation: U = scale q k^T is written to HBM in full
  * (rocBLAS batched GEMM), a row kernel builds R and F = softmax(R) (eqs. 2-3),
  * and a second GEMM forms o = F v. The baseline the fused path is measured

@@ -3,7 +3,7 @@ step of the operator runs in the library's HIP kernels; torch provides device
 memory and the current stream.
 
 Functions carry the C-ABI names (relation_fwd, relation_bwd,
-relation_fwd_materialized, relation_bwd_materialized,
+relation_bwd_noalloc, relation_fwd_materialized, relation_bwd_materialized,
 relation_exchange_allocation, relation_layer_fwd, relation_layer_bwd,
 relation_decode, relation_decode_states, relation_decode_merge, ...). ``relation`` is the differentiable wrapper
 (torch.autograd.Function) over relation_fwd / relation_bwd.
@@ -51,6 +51,9 @@ _SIGS = {
     "relation_bwd_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(RelProblem)]),
     "relation_bwd": (ctypes.c_int, [ctypes.POINTER(RelProblem), _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                     _P, _P, _P, ctypes.c_size_t, _P]),
+    "relation_bwd_noalloc_max_scratch_bytes": (ctypes.c_size_t, []),
+    "relation_bwd_noalloc": (ctypes.c_int, [ctypes.POINTER(RelProblem), _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                            _P, _P, _P, _P]),
     "relation_fwd_materialized_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(RelProblem)]),
     "relation_fwd_materialized": (ctypes.c_int, [ctypes.POINTER(RelProblem), _P, _P, _P, _P, _P, _P, _P,
                                                  _P, _P, _P, _P, ctypes.c_size_t, _P]),
@@ -224,6 +227,29 @@ def relation_bwd(q, k, v, o, dout, lam, row_stat, *, tau_s: float = TAU_S,
                           _ptr(workspace), workspace.numel() * workspace.element_size(), _stream())
     _check(st, "relation_bwd")
     return {"dq": dq, "dk": dk, "dv": dv, "dlambda": dlam, "dself": dself}
+
+
+def relation_bwd_noalloc(q, k, v, o, dout, lam, row_stat, *, tau_s: float = TAU_S,
+                         scale: Optional[float] = None, want_dself: bool = False, out=None):
+    """relation_bwd through the entry point that allocates nothing on the device
+    (its scratch is the library's own per-device array). ``out`` may hold
+    preallocated dq, dk, dv, dlambda (and dself) tensors. Returns the same dict."""
+    lib = load_library()
+    k, v, o, dout = _same_layout(q, k, v, o, dout)
+    p = make_problem(q, tau_s, scale)
+    B, H, T, D = q.shape
+    dev = q.device
+    lam_t = _lam_tensor(lam, dev)
+    if out is None:
+        out = {"dq": _layout_like(q), "dk": _layout_like(q), "dv": _layout_like(q),
+               "dlambda": torch.empty((1,), dtype=torch.float32, device=dev),
+               "dself": torch.empty((B, H, T), dtype=torch.float32, device=dev) if want_dself else None}
+    rs = row_stat.contiguous()
+    st = lib.relation_bwd_noalloc(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(dout), _ptr(lam_t),
+                                  _ptr(rs), _ptr(out["dq"]), _ptr(out["dk"]), _ptr(out["dv"]), _ptr(out["dlambda"]),
+                                  _ptr(out.get("dself")), _stream())
+    _check(st, "relation_bwd_noalloc")
+    return out
 
 
 def relation_fwd_materialized_workspace_bytes(q, *, tau_s: float = TAU_S,

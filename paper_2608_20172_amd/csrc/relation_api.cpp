@@ -545,6 +545,66 @@ rel_status relation_bwd(const rel_problem* p, const void* q, const void* k, cons
                   workspace_bytes, stream, 0);
 }
 
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Scratch of the backward pass without a caller workspace: a file-scope device
+// array, one copy per GPU, held until the process ends. Host code never passes
+// the array's name to a kernel or a copy: it is a host-side stand-in. The
+// device address of each GPU's copy comes from hipGetSymbolAddress, taken once
+// per device with that device current, and only that address is used.
+// ---------------------------------------------------------------------------
+static constexpr size_t kNoAllocScratchBytes = 32u << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of the current device's copy of `scratch`.
+rel_status scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(REL_ERR_UNSUPPORTED, "device index %d >= %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!ptr) return fail(REL_ERR_HIP, "hipGetSymbolAddress(scratch) returned null");
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return REL_OK;
+}
+}  // namespace
+
+extern "C" {
+
+size_t relation_bwd_noalloc_max_scratch_bytes(void) { return kNoAllocScratchBytes; }
+
+rel_status relation_bwd_noalloc(const rel_problem* p, const void* q, const void* k, const void* v,
+                                const void* o, const void* dout, const float* lambda,
+                                const float* row_stat, void* dq, void* dk, void* dv, float* dlambda,
+                                float* dself, void* stream) {
+  // the same per-row scratch relation_bwd takes from its workspace; its
+  // contents on entry are ignored (every word read is written first)
+  const size_t need = relation_bwd_workspace_bytes(p);  // 0 for an empty or invalid problem
+  void* ws = nullptr;
+  if (need > 0) {
+    if (need > kNoAllocScratchBytes)
+      return fail(REL_ERR_WORKSPACE,
+                  "relation_bwd_noalloc: the problem needs %zu bytes of scratch, over the %zu bytes "
+                  "this entry point holds per device",
+                  need, kNoAllocScratchBytes);
+    REL_TRY(scratch_address(&ws));
+  }
+  return bwd_impl(p, q, k, v, o, dout, lambda, row_stat, dq, dk, dv, dlambda, dself, ws,
+                  need > 0 ? kNoAllocScratchBytes : 0, stream, 0);
+}
+
 size_t relation_fwd_materialized_workspace_bytes(const rel_problem* p) {
   bool empty = false;
   if (check_problem(p, &empty) != REL_OK) return 0;

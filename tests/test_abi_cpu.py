@@ -298,3 +298,22 @@ def test_decode_validation(lib):
     assert mg(0, None) == R.REL_ERR_HIP                   # no states: a pure Self row
     assert mg(-1, a[7]) == R.REL_ERR_INVALID_ARG
     assert mg(2, a[5]) == R.REL_ERR_INVALID_ARG           # states inside out
+
+
+def test_noalloc_backward_validates_before_any_hip_call(lib):
+    """The no-allocation backward rejects a problem whose scratch exceeds its
+    per-device array with REL_ERR_WORKSPACE, before touching the device; a
+    valid problem reaches the device (no GPU here: REL_ERR_HIP)."""
+    a = ptrs(12)
+    cap = lib.relation_bwd_noalloc_max_scratch_bytes()
+    assert cap == 32 << 20
+    big = prob(B=1, H=64, T=1 << 16, D=32)
+    assert lib.relation_bwd_workspace_bytes(ctypes.byref(big)) > cap
+    st = lib.relation_bwd_noalloc(ctypes.byref(big), *a[:11], None, None)
+    assert st == R.REL_ERR_WORKSPACE
+    assert b"scratch" in lib.relation_last_error()
+    small = prob()
+    assert lib.relation_bwd_workspace_bytes(ctypes.byref(small)) <= cap
+    assert lib.relation_bwd_noalloc(ctypes.byref(small), *a[:11], None, None) == R.REL_ERR_HIP
+    # an invalid problem is reported as such, whatever its size
+    assert lib.relation_bwd_noalloc(ctypes.byref(prob(D=48)), *a[:11], None, None) == R.REL_ERR_UNSUPPORTED
