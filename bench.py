@@ -538,8 +538,20 @@ def main() -> int:
     if w.backward:
         f_saved = R.relation_fwd(q, k, v, lam_t)
         bcall = lambda: R.relation_bwd(q, k, v, f_saved["o"], do, lam_t, f_saved["row_stat"], workspace=ws)
+        dcall = lambda: R.relation_bwd(q, k, v, f_saved["o"], do, lam_t, f_saved["row_stat"], workspace=ws,
+                                       deterministic=True)
+        fused = lib.relation_bwd_workspace_bytes(ctypes.byref(R.make_problem(q))) > 0 and w.dtype == "bf16" \
+            and w.D <= 64
+        per_kernel["bwd_path"] = "one kernel (dq by atomics)" if fused else "two kernels"
         per_kernel["bwd_dkdv_kernel_ms"] = kernel_ms("bwd_dkdv", bcall)
-        per_kernel["bwd_dq_kernel_ms"] = kernel_ms("bwd_dq", bcall)
+        if fused:
+            per_kernel["bwd_prep_kernel_ms"] = kernel_ms("bwd_prep", bcall)
+            per_kernel["bwd_convert_kernel_ms"] = kernel_ms("bwd_convert", bcall)
+            per_kernel["bwd_deterministic_ms"] = kernel_ms("bwd", dcall)
+            per_kernel["bwd_deterministic_dq_kernel_ms"] = kernel_ms("bwd_dq", dcall)
+            per_kernel["bwd_deterministic_dkdv_kernel_ms"] = kernel_ms("bwd_dkdv", dcall)
+        else:
+            per_kernel["bwd_dq_kernel_ms"] = kernel_ms("bwd_dq", bcall)
 
     # materialised baseline forward
     mat = {"status": "skipped"}
@@ -612,7 +624,7 @@ def main() -> int:
         "decode": decode,
         "linear": linear,
         "roofline": {
-            "kernel": "bwd_dkdv_kernel+bwd_dq_kernel" if w.backward else "fwd_kernel",
+            "kernel": ("relation_bwd (" + per_kernel.get("bwd_path", "") + ")") if w.backward else "fwd_kernel",
             "bound": "mfma",
             "achieved": achieved / 1e12,
             "peak": PEAK_BF16 / 1e12,

@@ -101,28 +101,41 @@ rel_status relation_exchange_allocation(const rel_problem* p, const void* q, con
 
 /* Backward pass: gradients of sum(dout * o) (App. A.1.7), recomputed tile by
  * tile from q, k, v, o and row_stat.
+ * relation_bwd runs one kernel for dk, dv and dq when dtype is bf16 and D is 32
+ * or 64 (a row pass before it and a dq pass after it): each workgroup of 256
+ * keys adds its dq partials into an fp32 accumulator with atomics, so dq is
+ * correct to fp32 rounding but not bitwise run-to-run repeatable; dk, dv,
+ * dlambda and dself are. Other problems, and relation_bwd_deterministic
+ * always, run the two-kernel backward (a query-major dq kernel, then a
+ * key-major dk/dv kernel), where every output is written exactly once and all
+ * results are bitwise repeatable.
  *   dq, dk, dv out [B,H,T,D] dtype
  *   dlambda    out device fp32 scalar: sum over b, h, i of ln(i) * dR_ii, which
  *              equals -sum g_i (1-g_i) c_i ln i of App. A.1.7. Reduced in a fixed
  *              order.
  *   dself      out [B,H,T] fp32, optional: dL/dS_i, the gradient reaching the
  *              Self logit R_ii = S_i (-g_i (1 - g_i) c_i in App. A.1.7).
- *   workspace  at least relation_bwd_workspace_bytes(p) bytes of device memory,
- *              16-byte aligned: two fp32 values per row (-D_i = -dout_i . o_i and
- *              M_i log2(e), passed from the dQ pass to the dK/dV pass) and one
- *              partial per dQ workgroup for the fixed-order dlambda reduction;
- *              contents on entry are ignored.
- *   Every output is written exactly once (no atomics): results are run-to-run
- *   identical. */
+ *   workspace  at least relation_bwd_workspace_bytes(p) bytes of device memory
+ *              (enough for either path), 16-byte aligned: two fp32 values per
+ *              row (-D_i = -dout_i . o_i and M_i log2(e), read by the dk/dv
+ *              kernel), one dlambda partial per workgroup for the fixed-order
+ *              reduction, and on the one-kernel path the fp32 dq accumulator
+ *              [B,H,T,D]; contents on entry are ignored. */
 size_t relation_bwd_workspace_bytes(const rel_problem* p);
 rel_status relation_bwd(const rel_problem* p, const void* q, const void* k, const void* v,
                         const void* o, const void* dout, const float* lambda,
                         const float* row_stat, void* dq, void* dk, void* dv, float* dlambda,
                         float* dself, void* workspace, size_t workspace_bytes, void* stream);
+rel_status relation_bwd_deterministic(const rel_problem* p, const void* q, const void* k,
+                                      const void* v, const void* o, const void* dout,
+                                      const float* lambda, const float* row_stat, void* dq, void* dk,
+                                      void* dv, float* dlambda, float* dself, void* workspace,
+                                      size_t workspace_bytes, void* stream);
 
 /* Backward pass for callers that cannot allocate device memory (code under
  * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
- * relation_bwd with the same kernels and results, but no workspace argument.
+ * relation_bwd_deterministic (the two-kernel backward, bitwise repeatable) with
+ * the same kernels and results, but no workspace argument.
  * Its scratch (the two fp32 values per row and the dlambda partials that
  * relation_bwd takes from its workspace) lives in a device array inside the
  * library, one copy per GPU, allocated when the library's code is loaded on

@@ -51,6 +51,8 @@ _SIGS = {
     "relation_bwd_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(RelProblem)]),
     "relation_bwd": (ctypes.c_int, [ctypes.POINTER(RelProblem), _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                     _P, _P, _P, ctypes.c_size_t, _P]),
+    "relation_bwd_deterministic": (ctypes.c_int, [ctypes.POINTER(RelProblem), _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                                  _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "relation_bwd_noalloc_max_scratch_bytes": (ctypes.c_size_t, []),
     "relation_bwd_noalloc": (ctypes.c_int, [ctypes.POINTER(RelProblem), _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                             _P, _P, _P, _P]),
@@ -207,8 +209,10 @@ def relation_bwd_workspace_bytes(q, *, tau_s: float = TAU_S, scale: Optional[flo
 
 
 def relation_bwd(q, k, v, o, dout, lam, row_stat, *, tau_s: float = TAU_S,
-                 scale: Optional[float] = None, want_dself: bool = False, workspace=None):
-    """Fused backward. Returns dict(dq, dk, dv, dlambda (1-element fp32 tensor), dself)."""
+                 scale: Optional[float] = None, want_dself: bool = False, workspace=None,
+                 deterministic: bool = False):
+    """Fused backward. Returns dict(dq, dk, dv, dlambda (1-element fp32 tensor), dself).
+    deterministic=True calls relation_bwd_deterministic (bitwise repeatable dq)."""
     lib = load_library()
     k, v, o, dout = _same_layout(q, k, v, o, dout)
     p = make_problem(q, tau_s, scale)
@@ -222,10 +226,11 @@ def relation_bwd(q, k, v, o, dout, lam, row_stat, *, tau_s: float = TAU_S,
     if workspace is None or workspace.numel() * workspace.element_size() < nbytes:
         workspace = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=dev)
     rs = row_stat.contiguous()
-    st = lib.relation_bwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(dout), _ptr(lam_t),
-                          _ptr(rs), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dlam), _ptr(dself),
-                          _ptr(workspace), workspace.numel() * workspace.element_size(), _stream())
-    _check(st, "relation_bwd")
+    fn = lib.relation_bwd_deterministic if deterministic else lib.relation_bwd
+    st = fn(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(dout), _ptr(lam_t),
+            _ptr(rs), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dlam), _ptr(dself),
+            _ptr(workspace), workspace.numel() * workspace.element_size(), _stream())
+    _check(st, "relation_bwd_deterministic" if deterministic else "relation_bwd")
     return {"dq": dq, "dk": dk, "dv": dv, "dlambda": dlam, "dself": dself}
 
 

@@ -26,6 +26,7 @@
 // dP_ij - D_i directly: in dK/dV the dP chains start from an accumulator
 // holding -D of each query row, in dQ one more product adds -D_i.
 #include "kernels.h"
+#include "lanes.h"
 
 #include <algorithm>
 #include <type_traits>
@@ -39,6 +40,7 @@ constexpr int kBQI = 64;   // query rows per dK/dV tile
 constexpr int kBQ = 128;   // query rows per dQ workgroup
 constexpr int kBK = 64;    // keys per dQ tile
 constexpr int kNT = 256;
+constexpr int kFusedWaves = 8;  // fused backward: 8 waves, 256 keys per workgroup
 #ifndef REL_DQ_WAVES_PER_SIMD
 #define REL_DQ_WAVES_PER_SIMD 3   // bf16, d <= 64
 #endif
@@ -428,43 +430,65 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
 // ---------------------------------------------------------------------------
 // dK / dV
 // ---------------------------------------------------------------------------
-template <class P, int D>
-__global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel(BwdArgs a) {
+// NW waves of 32 keys each. FQ (bf16, fused backward): the workgroup also
+// forms dQ. The dU tile of each query tile (keys x queries, bf16) goes to LDS;
+// after the next barrier, waves 0 .. 2 D/32 - 1 each take one 32 x 32 block of
+// the tile's dQ partial, dU[64 x NW*32] K[NW*32 x D] on the matrix cores (K of
+// the workgroup's keys is held in LDS), and add it to the fp32 dQ accumulator
+// with global atomics. The diagonal (Self) entry sits in dU, so dQ needs no
+// separate Self term; dself and the dlambda partials come from the diagonal
+// blocks here.
+template <class P, int D, int NW, bool FQ>
+__global__ __launch_bounds__(NW * 64, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel(BwdArgs a) {
   using E = typename P::T;
   using Op = typename P::Op;
+  using PU = PolBF16<64>;                       // layout of the dU tile: 64 query columns
+  constexpr int NT = NW * 64;
+  constexpr int KW = NW * 32;                   // keys per workgroup
   constexpr int KS = D / 16;
   constexpr int DB = D / 32;
   constexpr int TB = kBQI * P::ROWB;            // one tensor tile (Q or dO)
   constexpr int NSEG = TB / 1024;
-  constexpr int SEGW = 2 * NSEG / 4;
-  static_assert(SEGW >= 1 && 2 * NSEG % 4 == 0, "tile does not split over the waves");
+  constexpr int SEGW = 2 * NSEG / NW;
+  static_assert(SEGW >= 1 && 2 * NSEG % NW == 0, "tile does not split over the waves");
+  static_assert(!FQ || (sizeof(E) == 2 && KW % 64 == 0 && 2 * DB <= NW), "fused dQ: bf16, whole 64-key tiles");
   constexpr int BUF = 2 * TB + 2 * kBQI * 4;    // Q, dO, M log2(e), -D
-  // two tile buffers as distinct objects: the compiler can then see that
-  // reads of one do not wait for the loads in flight into the other
+  constexpr int DUT = PU::tile_bytes(kBQI);     // dU of 64 keys x 64 queries
+  constexpr int KQB = FQ ? (KW / 64) * TB : 16; // K of the workgroup's keys
+  constexpr int DUB = FQ ? (KW / 64) * DUT : 16;
+  // tile buffers as distinct objects: the compiler can then see that reads of
+  // one do not wait for the loads in flight into another
   __shared__ __attribute__((aligned(1024))) unsigned char bufA[BUF];
   __shared__ __attribute__((aligned(1024))) unsigned char bufB[BUF];
+  __shared__ __attribute__((aligned(1024))) unsigned char Kq[KQB];
+  __shared__ __attribute__((aligned(1024))) unsigned char dUA[DUB];
+  __shared__ __attribute__((aligned(1024))) unsigned char dUB[DUB];
+  __shared__ float red[NT];
 
   const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int lane = tid & 63;
   const Lane L(lane);
   const int n = L.n, g = L.g;
-  if (blockIdx.x == 0 && a.dlambda) {
+  if (!FQ && blockIdx.x == 0 && a.dlambda) {
     // dlambda: the dQ kernel (which ran before this one) left one partial per
     // workgroup; summed here in a fixed order, so the result is run-to-run
     // identical
-    __shared__ float red[kNT];
     float acc = 0.0f;
-    for (int i = tid; i < a.nparts; i += kNT) acc += a.dlam_part[i];
+    for (int i = tid; i < a.nparts; i += NT) acc += a.dlam_part[i];
     red[tid] = acc;
     __syncthreads();
-    for (int h = kNT / 2; h >= 1; h >>= 1) {
+    for (int h = NT / 2; h >= 1; h >>= 1) {
       if (tid < h) red[tid] += red[tid + h];
       __syncthreads();
     }
     if (tid == 0) *a.dlambda = red[0];
+    __syncthreads();
   }
   int head, kt;
-  if (!map_tile(a.map, blockIdx.x, head, kt, false)) return;
+  if (!map_tile(a.map, blockIdx.x, head, kt, false)) {
+    if (FQ && tid == 0) a.dlam_part[blockIdx.x] = 0.0f;
+    return;
+  }
   const int T = a.T;
   const int64_t st = a.st;
   const int64_t hoff = (int64_t)(head / a.H) * a.sb + (int64_t)(head % a.H) * a.sh;
@@ -475,7 +499,7 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
   const float c = a.scale * kLog2e;
   const float lam = *a.lambda;
 
-  const int j0 = kt * kBKW;
+  const int j0 = kt * KW;
   const int kw0 = j0 + 32 * w;        // first key of this wave
   const int kj = kw0 + n;             // this lane's key
   const bool wave_keys = kw0 < T;
@@ -499,6 +523,16 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
   const int nqt = (T + kBQI - 1) / kBQI;
   const int qt0 = j0 / kBQI;
   load_tile(qt0 * kBQI, bufA);
+  if constexpr (FQ) {
+    // K of the workgroup's keys, the second operand of dQ = dU K
+    const __amdgpu_buffer_rsrc_t krs = make_rsrc(k, T * row_bytes);
+#pragma unroll
+    for (int s = 0; s < (KW / 64) * NSEG / NW; ++s) {
+      const int seg = w * ((KW / 64) * NSEG / NW) + s;
+      dma_segment<P>(krs, Kq + (seg / NSEG) * TB, seg % NSEG, row_bytes, j0 + 64 * (seg / NSEG), lane);
+    }
+  }
+  if (FQ) red[tid] = 0.0f;  // fused: per-key dlambda terms, written in the diagonal blocks
 
   // B operands of U = Q K^T and dP = dO V^T: this lane's key row
   Op kop[KS], vop[KS];
@@ -576,7 +610,12 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
         }
       }
       if (holds_row(n, g)) {
-        const SelfGrad sg = self_grad(uself, dself, Mb[rs], a.scale, a.inv_tau, lam, logf((float)(kj + 1)), kj == 0);
+        const float ln_i = logf((float)(kj + 1));
+        const SelfGrad sg = self_grad(uself, dself, Mb[rs], a.scale, a.inv_tau, lam, ln_i, kj == 0);
+        if (FQ && kj < T) {
+          red[32 * w + n] = ln_i * sg.dR;  // this key's dlambda term (each key's diagonal is met once)
+          if (a.dself) a.dself[(int64_t)head * T + kj] = sg.dR;
+        }
         const float fself = a.exch_only ? 0.0f : sg.F;  // F_ii carries dO_i to v_i unless exchange-only
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
@@ -610,16 +649,65 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
       }
   };
 
+  // fused: dU of one query block (rows 32 qb .. of the tile) into the LDS dU
+  // tile, row = key, column = query
+  auto write_dU = [&](unsigned char* dUw, int qb, const Op (&uop)[2]) __attribute__((always_inline)) {
+    if constexpr (FQ) {
+      int kr = 32 * w + n;
+      asm volatile("" : "+v"(kr));  // formed here, not held in a register across the tile loop
+      unsigned char* t = dUw + (kr >> 6) * DUT;
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          *(uintx2*)(t + PU::off(kr & 63, 32 * qb + 16 * hh + 8 * h + 4 * g)) = half_of(uop[hh], h);
+    }
+  };
+  // fused: the dQ partial of query tile i0 .. i0+63 from its dU tile, one
+  // 32 x 32 block per wave, added to the fp32 accumulator
+  auto dq_tile = [&](const unsigned char* dUr, int i0) __attribute__((always_inline)) {
+    if constexpr (FQ) if (w < 2 * DB) {
+      const int qb = w / DB, db = w % DB;
+      floatx16 acc = {};
+#pragma unroll
+      for (int kq = 0; kq < KW / 16; ++kq) {
+        const Op ua = PU::col_op(dUr + (kq >> 2) * DUT, kq & 3, 32 * qb, L);
+        const Op kb = P::col_op(Kq + (kq >> 2) * TB, kq & 3, 32 * db, L);
+        acc = P::mma(ua, kb, acc);
+      }
+      // register r holds row acc_row(r, g) = 8 (r / 4) + 4 g + r % 4 of the block,
+      // column n: a uniform base, one lane offset and a constant per register
+      float* base = a.dq_acc + ((int64_t)head * T + i0 + 32 * qb) * D + 32 * db;
+      int off = 4 * g * D + n;
+      asm volatile("" : "+v"(off));  // formed here, not held in a register across the tile loop
+      const int lim = T - i0 - 32 * qb;  // rows of the block inside the sequence
+      if (lim >= 32) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) unsafeAtomicAdd(base + off + (8 * (r >> 2) + (r & 3)) * D, acc[r]);
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (8 * (r >> 2) + (r & 3) + 4 * g < lim) unsafeAtomicAdd(base + off + (8 * (r >> 2) + (r & 3)) * D, acc[r]);
+      }
+    }
+  };
+
   const int kfirst = wave_keys ? kw0 : (1 << 30);  // a wave past T meets no query
   // One query tile. A block before the wave's keys or past T contributes zero
   // F and dU, so the dV / dK products (and the accumulators) run on every
   // path. Order: evidence of block 0, its vector work, evidence of block 1,
   // then the products of block 0 (which run under the vector work of block 1).
-  auto step = [&](int qt, const unsigned char* buf, unsigned char* nxt) __attribute__((always_inline)) {
+  auto step = [&](int qt, const unsigned char* buf, unsigned char* nxt, unsigned char* dUw,
+                  const unsigned char* dUr) __attribute__((always_inline)) {
     const int i0 = qt * kBQI;
     wait_loads();
     __syncthreads();
     if (qt + 1 < nqt) load_tile(i0 + kBQI, nxt);
+    if (FQ && qt > qt0) {
+      __builtin_amdgcn_sched_barrier(0);
+      dq_tile(dUr, i0 - kBQI);
+      __builtin_amdgcn_sched_barrier(0);
+    }
     const int q0 = i0, q1 = i0 + 32;
     const bool live0 = q0 >= kfirst && q0 < T, live1 = q1 >= kfirst && q1 < T;
     floatx16 s0, dp0, s1, dp1;
@@ -632,22 +720,30 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
     if (live1) evid(buf, 1, s1, dp1);
     __builtin_amdgcn_sched_barrier(0);
     accum(buf, 0, f0, u0);
+    write_dU(dUw, 0, u0);
     __builtin_amdgcn_sched_barrier(0);
     if (live1) {
       if (q1 == kfirst) grads(buf, 1, s1, dp1, f1, u1, std::true_type{});
       else grads(buf, 1, s1, dp1, f1, u1, std::false_type{});
     }
     accum(buf, 1, f1, u1);
+    write_dU(dUw, 1, u1);
   };
   // A full tile (both blocks live and past every wave's diagonal) is one
   // basic block: the evidence of block 1 and then the products of block 0 are
   // interleaved with the vector work of blocks 0 and 1, so that one wave keeps
   // the matrix and the vector units busy together.
-  auto full = [&](int qt, const unsigned char* buf, unsigned char* nxt) __attribute__((always_inline)) {
+  auto full = [&](int qt, const unsigned char* buf, unsigned char* nxt, unsigned char* dUw,
+                  const unsigned char* dUr) __attribute__((always_inline)) {
     const int i0 = qt * kBQI;
     wait_loads();
     __syncthreads();
     if (qt + 1 < nqt) load_tile(i0 + kBQI, nxt);
+    if (FQ && qt > qt0) {
+      __builtin_amdgcn_sched_barrier(0);
+      dq_tile(dUr, i0 - kBQI);
+      __builtin_amdgcn_sched_barrier(0);
+    }
     floatx16 s0, dp0, s1, dp1;
     Op f0[2], u0[2], f1[2], u1[2];
     evid(buf, 0, s0, dp0);
@@ -657,28 +753,47 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
     if (REL_DKDV_INTERLEAVE) interleave<2 * KS, REL_DKDV_IL_VALU, 0>();
     __builtin_amdgcn_sched_barrier(0);
     accum(buf, 0, f0, u0);
+    write_dU(dUw, 0, u0);
     grads(buf, 1, s1, dp1, f1, u1, std::false_type{});
     if (REL_DKDV_INTERLEAVE) interleave<4 * DB, REL_DKDV_IL_VALU, 1>();
     __builtin_amdgcn_sched_barrier(0);
     accum(buf, 1, f1, u1);
+    write_dU(dUw, 1, u1);
   };
-  // tiles alternate between bufA and bufB, starting with bufA at qt0
+  // tiles alternate between bufA and bufB (and the dU tiles between dUA and
+  // dUB), starting with bufA at qt0
   auto run = [&](int qa, int qb, auto st) __attribute__((always_inline)) {
     int qt = qa;
     if (qt < qb && ((qt - qt0) & 1)) {
-      st(qt, bufB, bufA);
+      st(qt, bufB, bufA, dUB, dUA);
       ++qt;
     }
     for (; qt < qb; qt += 2) {
-      st(qt, bufA, bufB);
-      if (qt + 1 < qb) st(qt + 1, bufB, bufA);
+      st(qt, bufA, bufB, dUA, dUB);
+      if (qt + 1 < qb) st(qt + 1, bufB, bufA, dUB, dUA);
     }
   };
-  const int qf0 = min(qt0 + kBKW / kBQI, nqt);  // tiles with the workgroup's diagonals
-  const int qf1 = max(qf0, T / kBQI);             // full tiles end here
+  const int qf0 = min(qt0 + KW / kBQI, nqt);  // tiles with the workgroup's diagonals
+  const int qf1 = max(qf0, T / kBQI);           // full tiles end here
   run(qt0, qf0, step);
   run(qf0, qf1, full);
   run(qf1, nqt, step);
+  if constexpr (FQ) {
+    // the last tile's dQ, and this workgroup's dlambda partial in a fixed order
+    __syncthreads();
+    dq_tile(((nqt - 1 - qt0) & 1) ? dUB : dUA, (nqt - 1) * kBQI);
+    float t = tid < KW ? red[tid] : 0.0f;
+#pragma unroll
+    for (int s = 32; s >= 1; s >>= 1) t += __shfl_xor(t, s, 64);
+    __syncthreads();
+    if (lane == 0) red[w] = t;
+    __syncthreads();
+    if (tid == 0) {
+      float sum = 0.0f;
+      for (int i = 0; i < NW; ++i) sum += red[i];
+      a.dlam_part[blockIdx.x] = sum;
+    }
+  }
 
   if (kj < T) {
     E* dk = (E*)a.dk + hoff;
@@ -700,6 +815,75 @@ __global__ __launch_bounds__(kNT, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel
   }
 }
 
+// ---------------------------------------------------------------------------
+// Fused backward (bf16, D <= 64): the row pass before and the dQ pass after
+// the dK/dV/dQ kernel.
+// ---------------------------------------------------------------------------
+constexpr int kRowNT = 256;
+
+// Row r of the [N, T] row space: its head and the element offset of its row.
+__device__ __forceinline__ int64_t row_offset(const BwdArgs& a, int64_t r) {
+  const int head = (int)(r / a.T), t = (int)(r % a.T);
+  return (int64_t)(head / a.H) * a.sb + (int64_t)(head % a.H) * a.sh + (int64_t)t * a.st;
+}
+
+// D_i = dO_i . o_i (stored as -D_i), M_i log2(e), and the row's fp32 dQ
+// accumulator cleared. D/8 lanes per row, 16 bytes each.
+template <int D>
+__global__ __launch_bounds__(kRowNT) void bwd_prep_kernel(BwdArgs a) {
+  constexpr int LPR = D / 8, RPB = kRowNT / LPR;
+  const int tid = threadIdx.x, c = tid % LPR;
+  const int64_t r = (int64_t)blockIdx.x * RPB + tid / LPR;
+  const bool ok = r < (int64_t)a.map.N * a.T;
+  float part = 0.0f;
+  if (ok) {
+    const int64_t off = row_offset(a, r) + 8 * c;
+    part = PolBF16<D>::chunk_dot(*(const uintx4*)((const bf16*)a.o + off), *(const uintx4*)((const bf16*)a.dout + off));
+  }
+  const float Di = lane_group_sum<LPR>(part);  // every lane takes part
+  if (ok) {
+    if (c == 0) {
+      a.negd[r] = -Di;
+      a.m2[r] = a.row_stat[r] * kLog2e;
+    }
+    floatx4* acc = (floatx4*)(a.dq_acc + r * D + 8 * c);
+    acc[0] = floatx4{};
+    acc[1] = floatx4{};
+  }
+}
+
+// dq = scale * (fp32 accumulator) in bf16; block 0 first sums the dlambda
+// partials of the fused kernel (which ran before on the stream) in a fixed
+// order.
+template <int D>
+__global__ __launch_bounds__(kRowNT) void bwd_dq_convert_kernel(BwdArgs a) {
+  constexpr int LPR = D / 8, RPB = kRowNT / LPR;
+  const int tid = threadIdx.x, c = tid % LPR;
+  if (blockIdx.x == 0 && a.dlambda) {
+    __shared__ float red[kRowNT];
+    float acc = 0.0f;
+    for (int i = tid; i < a.nparts; i += kRowNT) acc += a.dlam_part[i];
+    red[tid] = acc;
+    __syncthreads();
+    for (int h = kRowNT / 2; h >= 1; h >>= 1) {
+      if (tid < h) red[tid] += red[tid + h];
+      __syncthreads();
+    }
+    if (tid == 0) *a.dlambda = red[0];
+  }
+  const int64_t r = (int64_t)blockIdx.x * RPB + tid / LPR;
+  if (r >= (int64_t)a.map.N * a.T) return;
+  const floatx4* acc = (const floatx4*)(a.dq_acc + r * D + 8 * c);
+  const floatx4 x0 = acc[0], x1 = acc[1];
+  bf16x8 y;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    y[t] = (bf16)(a.scale * x0[t]);
+    y[4 + t] = (bf16)(a.scale * x1[t]);
+  }
+  *(bf16x8*)((bf16*)a.dq + row_offset(a, r) + 8 * c) = y;
+}
+
 template <class P, int D>
 void launch_pair(const BwdArgs& a, const TileMap& mkv, const TileMap& mq, hipStream_t stream,
                  hipEvent_t* prof) {
@@ -716,21 +900,60 @@ void launch_pair(const BwdArgs& a, const TileMap& mkv, const TileMap& mq, hipStr
   b.map = mkv;
   const bool p_kv = !p_all && profile_slot("bwd_dkdv", &e0, &e1);
   if (p_kv) (void)hipEventRecord(e0, stream);
-  hipLaunchKernelGGL((bwd_dkdv_kernel<P, D>), dim3((unsigned)grid_size(mkv)), dim3(kNT), 0, stream, b);
+  hipLaunchKernelGGL((bwd_dkdv_kernel<P, D, 4, false>), dim3((unsigned)grid_size(mkv)), dim3(kNT), 0, stream, b);
   if (p_kv) (void)hipEventRecord(e1, stream);
+  if (p_all) (void)hipEventRecord(prof[1], stream);
+}
+
+// The fused backward: row pass, the dK/dV/dQ kernel (256 keys per workgroup),
+// dQ pass.
+template <int D>
+void launch_fused(const BwdArgs& a, hipStream_t stream, hipEvent_t* prof) {
+  constexpr int NW = kFusedWaves;
+  BwdArgs b = a;
+  const int64_t rows = (int64_t)a.map.N * a.T;
+  const unsigned row_blocks = (unsigned)((rows + kRowNT / (D / 8) - 1) / (kRowNT / (D / 8)));
+  hipEvent_t e0, e1;
+  const bool p_all = prof != nullptr;
+  if (p_all) (void)hipEventRecord(prof[0], stream);
+  const bool p_r = !p_all && profile_slot("bwd_prep", &e0, &e1);
+  if (p_r) (void)hipEventRecord(e0, stream);
+  hipLaunchKernelGGL((bwd_prep_kernel<D>), dim3(row_blocks), dim3(kRowNT), 0, stream, b);
+  if (p_r) (void)hipEventRecord(e1, stream);
+  b.map = make_tilemap(a.map.N, (a.T + 32 * NW - 1) / (32 * NW));
+  const bool p_kv = !p_all && profile_slot("bwd_dkdv", &e0, &e1);
+  if (p_kv) (void)hipEventRecord(e0, stream);
+  hipLaunchKernelGGL((bwd_dkdv_kernel<PolBF16<D>, D, NW, true>), dim3((unsigned)grid_size(b.map)), dim3(64 * NW), 0,
+                     stream, b);
+  if (p_kv) (void)hipEventRecord(e1, stream);
+  b.map = a.map;
+  const bool p_c = !p_all && profile_slot("bwd_convert", &e0, &e1);
+  if (p_c) (void)hipEventRecord(e0, stream);
+  hipLaunchKernelGGL((bwd_dq_convert_kernel<D>), dim3(row_blocks), dim3(kRowNT), 0, stream, b);
+  if (p_c) (void)hipEventRecord(e1, stream);
   if (p_all) (void)hipEventRecord(prof[1], stream);
 }
 
 }  // namespace
 
-int bwd_partials(int N, int T, int D, int dtype) {
+bool bwd_fused_supported(int D, int dtype) { return dtype == 1 && (D == 32 || D == 64); }
+
+int bwd_partials(int N, int T, int D, int dtype, bool fused) {
   (void)D;
   (void)dtype;
+  if (fused) return (int)grid_size(make_tilemap(N, (T + 32 * kFusedWaves - 1) / (32 * kFusedWaves)));
   return (int)grid_size(make_tilemap(N, (T + kBQ - 1) / kBQ));
 }
 
 hipError_t launch_bwd(const BwdArgs& a, int dtype, int D, hipStream_t stream) {
   const int N = a.map.N;
+  if (a.dq_acc) {
+    hipEvent_t ev[2];
+    const bool prof = profile_slot("bwd", &ev[0], &ev[1]);
+    if (D == 32) launch_fused<32>(a, stream, prof ? ev : nullptr);
+    else launch_fused<64>(a, stream, prof ? ev : nullptr);
+    return hipGetLastError();
+  }
   const TileMap mkv = make_tilemap(N, (a.T + kBKW - 1) / kBKW);
   const TileMap mq = make_tilemap(N, (a.T + kBQ - 1) / kBQ);
   hipEvent_t ev[2];

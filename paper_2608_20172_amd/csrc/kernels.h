@@ -45,6 +45,7 @@ struct BwdArgs {
   float* negd;       // -D_i = -dO_i . o_i, [N, T], written by the dQ kernel
   float* m2;         // M_i log2(e), [N, T], written by the dQ kernel
   float* dself;      // optional [N, T]
+  float* dq_acc;     // fused backward: fp32 dQ accumulator [N, T, D]; null selects the two-kernel backward
   int64_t sb, sh, st;
   int H, T;
   float scale;
@@ -165,7 +166,10 @@ bool profile_slot(const char* name, hipEvent_t* start, hipEvent_t* stop);
 
 hipError_t launch_fwd(const FwdArgs& a, int dtype, int D, hipStream_t stream);
 hipError_t launch_bwd(const BwdArgs& a, int dtype, int D, hipStream_t stream);
-int bwd_partials(int N, int T, int D, int dtype);
+// The fused backward (one kernel for dK, dV and dQ, dQ summed by atomics) covers
+// these problems; the two-kernel backward covers all.
+bool bwd_fused_supported(int D, int dtype);
+int bwd_partials(int N, int T, int D, int dtype, bool fused);
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t stream);
 hipError_t launch_allocation(const RowArgs& a, int dtype, int N, hipStream_t stream);
 // Layer passes. `vec` (8, 2 or 1 for bf16; 4, 2 or 1 for fp32) is the number

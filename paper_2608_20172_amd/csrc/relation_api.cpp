@@ -360,7 +360,7 @@ const char* relation_status_string(rel_status s) {
 const char* relation_last_error(void) { return g_last_error.c_str(); }
 
 rel_status relation_profile_arm(const char* kernel, void** events, int n_pairs) {
-  static const char* kNames[] = {"fwd", "bwd", "bwd_dkdv", "bwd_dq"};
+  static const char* kNames[] = {"fwd", "bwd", "bwd_dkdv", "bwd_dq", "bwd_prep", "bwd_convert"};
   bool known = false;
   for (const char* nm : kNames) known = known || (kernel && std::string(kernel) == nm);
   if (!known) return fail(REL_ERR_INVALID_ARG, "unknown kernel name for profiling");
@@ -458,20 +458,39 @@ rel_status relation_exchange_allocation(const rel_problem* p, const void* q, con
 }
 
 
+}  // extern "C"
+
+namespace {
+// Backward workspace of one path (valid, non-empty problem): -D_i and
+// M_i log2(e) per row, the dlambda partials, and for the fused path the fp32
+// dQ accumulator.
+size_t bwd_workspace(const rel_problem* p, bool fused) {
+  const size_t N = (size_t)(p->B * p->H), rows = N * (size_t)p->T;
+  size_t b = 2 * align256(rows * 4) +
+             align256((size_t)rel::bwd_partials((int)N, (int)p->T, (int)p->D, p->dtype, fused) * 4);
+  if (fused) b += align256(rows * (size_t)p->D * 4);
+  return b;
+}
+bool bwd_fused(const rel_problem* p) { return rel::bwd_fused_supported((int)p->D, p->dtype); }
+}  // namespace
+
+extern "C" {
+
 size_t relation_bwd_workspace_bytes(const rel_problem* p) {
   bool empty = false;
   if (check_problem(p, &empty) != REL_OK) return 0;
   if (empty) return 0;
-  const size_t N = (size_t)(p->B * p->H);
-  return 2 * align256(N * (size_t)p->T * 4) +
-         align256((size_t)rel::bwd_partials((int)N, (int)p->T, (int)p->D, p->dtype) * 4);
+  const size_t two = bwd_workspace(p, false);
+  return bwd_fused(p) ? std::max(two, bwd_workspace(p, true)) : two;
 }
 
+// fused: take the one-kernel backward where it covers the problem (dq summed
+// by atomics); otherwise, and with fused = false, the two-kernel backward.
 static rel_status bwd_impl(const rel_problem* p, const void* q, const void* k, const void* v,
                            const void* o, const void* dout, const float* lambda,
                            const float* row_stat, void* dq, void* dk, void* dv, float* dlambda,
                            float* dself, void* workspace, size_t workspace_bytes, void* stream,
-                           int exch_only) {
+                           int exch_only, bool fused) {
   bool empty = false;
   REL_TRY(check_problem(p, &empty));
   if (empty) {
@@ -495,7 +514,8 @@ static rel_status bwd_impl(const rel_problem* p, const void* q, const void* k, c
   REL_TRY(check_aligned(row_stat, 4, "row_stat", true));
   REL_TRY(check_aligned(dlambda, 4, "dlambda", true));
   REL_TRY(check_aligned(dself, 4, "dself", false));
-  const size_t need = relation_bwd_workspace_bytes(p);
+  fused = fused && bwd_fused(p);
+  const size_t need = bwd_workspace(p, fused);
   if (!workspace || workspace_bytes < need)
     return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
                 workspace ? workspace_bytes : (size_t)0);
@@ -521,16 +541,18 @@ static rel_status bwd_impl(const rel_problem* p, const void* q, const void* k, c
   a.q = q; a.k = k; a.v = v; a.o = o; a.dout = dout; a.lambda = lambda; a.row_stat = row_stat;
   a.dq = dq; a.dk = dk; a.dv = dv; a.dself = dself;
   const size_t rowv = align256(N * (size_t)p->T * 4);
+  const int nparts = rel::bwd_partials((int)N, (int)p->T, (int)p->D, p->dtype, fused);
   a.negd = (float*)workspace;
   a.m2 = (float*)((char*)workspace + rowv);
   a.dlam_part = (float*)((char*)workspace + 2 * rowv);
+  a.dq_acc = fused ? (float*)((char*)workspace + 2 * rowv + align256((size_t)nparts * 4)) : nullptr;
   a.sb = p->stride_b; a.sh = p->stride_h; a.st = p->stride_t;
   a.H = (int)p->H; a.T = (int)p->T;
   a.scale = eff_scale(p);
   a.exch_only = exch_only;
   a.inv_tau = 1.0f / p->tau_s;
   a.map = rel::make_tilemap((int)N, 1);
-  a.nparts = rel::bwd_partials((int)N, (int)p->T, (int)p->D, p->dtype);
+  a.nparts = nparts;
   a.dlambda = dlambda;
   hipError_t e = rel::launch_bwd(a, p->dtype, (int)p->D, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "relation_bwd launch");
@@ -542,7 +564,15 @@ rel_status relation_bwd(const rel_problem* p, const void* q, const void* k, cons
                         const float* row_stat, void* dq, void* dk, void* dv, float* dlambda,
                         float* dself, void* workspace, size_t workspace_bytes, void* stream) {
   return bwd_impl(p, q, k, v, o, dout, lambda, row_stat, dq, dk, dv, dlambda, dself, workspace,
-                  workspace_bytes, stream, 0);
+                  workspace_bytes, stream, 0, true);
+}
+
+rel_status relation_bwd_deterministic(const rel_problem* p, const void* q, const void* k, const void* v,
+                                      const void* o, const void* dout, const float* lambda,
+                                      const float* row_stat, void* dq, void* dk, void* dv, float* dlambda,
+                                      float* dself, void* workspace, size_t workspace_bytes, void* stream) {
+  return bwd_impl(p, q, k, v, o, dout, lambda, row_stat, dq, dk, dv, dlambda, dself, workspace,
+                  workspace_bytes, stream, 0, false);
 }
 
 }  // extern "C"
@@ -591,7 +621,8 @@ rel_status relation_bwd_noalloc(const rel_problem* p, const void* q, const void*
                                 float* dself, void* stream) {
   // the same per-row scratch relation_bwd takes from its workspace; its
   // contents on entry are ignored (every word read is written first)
-  const size_t need = relation_bwd_workspace_bytes(p);  // 0 for an empty or invalid problem
+  // 0 for an empty or invalid problem (bwd_impl then reports it)
+  const size_t need = relation_bwd_workspace_bytes(p) ? bwd_workspace(p, false) : 0;
   void* ws = nullptr;
   if (need > 0) {
     if (need > kNoAllocScratchBytes)
@@ -602,7 +633,7 @@ rel_status relation_bwd_noalloc(const rel_problem* p, const void* q, const void*
     REL_TRY(scratch_address(&ws));
   }
   return bwd_impl(p, q, k, v, o, dout, lambda, row_stat, dq, dk, dv, dlambda, dself, ws,
-                  need > 0 ? kNoAllocScratchBytes : 0, stream, 0);
+                  need > 0 ? kNoAllocScratchBytes : 0, stream, 0, false);
 }
 
 size_t relation_fwd_materialized_workspace_bytes(const rel_problem* p) {
@@ -971,7 +1002,7 @@ rel_status relation_layer_bwd(const rel_problem* p, const rel_layer_opts* opts, 
   char* ws = (char*)workspace;
   if (L.pass)
     return bwd_impl(&L.pp, q, k, v, out, dout, lambda, row_stat, dq, dk, dv, dlambda, nullptr, ws + L.bws,
-                    relation_bwd_workspace_bytes(&L.pp), stream, opts->transport);
+                    relation_bwd_workspace_bytes(&L.pp), stream, opts->transport, true);
   char* prep = saved ? (char*)saved : ws;
   char* scr = saved ? ws : ws + L.prep;
   const size_t tb = (size_t)extent_elems(p) * es, rb = (size_t)(p->B * p->H * p->T) * 4;
@@ -1014,7 +1045,7 @@ rel_status relation_layer_bwd(const rel_problem* p, const rel_layer_opts* opts, 
   a.dth_rows = giv ? (float*)(scr + L.dth) : nullptr;
   REL_TRY(bwd_impl(&L.pp, a.qr, a.kr, a.vt, y_direct ? out : prep + L.yp, do_direct ? dout : scr + L.dop,
                    lambda, row_stat, (void*)a.gq, (void*)a.gk, (void*)a.gv, dlambda, nullptr, scr + L.bws,
-                   relation_bwd_workspace_bytes(&L.pp), stream, opts->transport));
+                   relation_bwd_workspace_bytes(&L.pp), stream, opts->transport, true));
   if ((he = rel::launch_layer_epilogue(a, p->dtype, vec, s))) return hip_fail(he, "layer epilogue launch");
   if (giv && (he = rel::launch_segment_sum(a.dth_rows, (int)(p->H / 2), p->B * p->T, (float*)(scr + L.dpart),
                                            dtheta, s)))

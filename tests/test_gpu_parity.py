@@ -13,7 +13,8 @@ import oracle
 from paper_2608_20172_amd import inputs as I
 from paper_2608_20172_amd import binding as R
 from tests import oracle_pool as OP
-from tests.gpu_helpers import assert_close, assert_scalar_close, lam_value, log, sample_heads, to_device
+from tests.gpu_helpers import (assert_close, assert_order_close, assert_scalar_close, lam_value, log, sample_heads,
+                               to_device)
 
 pytestmark = pytest.mark.gpu
 
@@ -68,13 +69,13 @@ def compare_forward(out, heads, refs, dtype, with_aux=True):
             assert_close(f"exch_lse[{b},{h}]", aux["exch_lse"][b, h][rr], f["LE"], dtype)
 
 
-def check_backward(x, dtype, fwd, heads=None, rows=None, row_block=256, key_from=0):
+def check_backward(x, dtype, fwd, heads=None, rows=None, row_block=256, key_from=0, deterministic=False):
     """Fused backward vs oracle on the given heads (default: all, and then dlambda
-    against the oracle's sum over heads)."""
+    against the oracle's sum over heads). deterministic: the two-kernel path."""
     B, H, T, D = x["q"].shape
-    log(f"[bwd] B={B} H={H} T={T} D={D} {dtype}")
+    log(f"[bwd] B={B} H={H} T={T} D={D} {dtype}{' deterministic' if deterministic else ''}")
     g = R.relation_bwd(x["q"], x["k"], x["v"], fwd["o"], x["do"], x["lam"], fwd["row_stat"],
-                       want_dself=True)
+                       want_dself=True, deterministic=deterministic)
     torch.cuda.synchronize()
     all_heads = heads is None
     heads = heads or [(b, h) for b in range(B) for h in range(H)]
@@ -211,10 +212,32 @@ def test_forward_lambda_values(lam):
 
 
 @pytest.mark.parametrize("D", [32, 64, 96, 128])
-def test_backward_bf16_ragged(D):
+@pytest.mark.parametrize("deterministic", [False, True])
+def test_backward_bf16_ragged(D, deterministic):
     x = _prep(I.make_inputs(2, 2, 300, D, seed=11, qkv_std=1 / math.sqrt(D), lam=0.5), "bf16")
     f = check_forward(x, "bf16", with_aux=False)
-    check_backward(x, "bf16", f)
+    check_backward(x, "bf16", f, deterministic=deterministic)
+
+
+@pytest.mark.parametrize("T", [1, 2, 63, 64, 65, 255, 256, 257, 511, 513, 700])
+@pytest.mark.parametrize("D", [32, 64])
+def test_backward_one_kernel_matches_two_kernel(T, D):
+    """The one-kernel backward (256-key workgroups, dq by atomics) against the
+    two-kernel one on the same inputs, at lengths around its 64-row query tiles
+    and 256-key workgroups; the oracle on one head."""
+    x = _prep(I.make_inputs(2, 3, T, D, seed=200 + T + D, qkv_std=1 / math.sqrt(D), lam=0.3), "bf16")
+    f = R.relation_fwd(x["q"], x["k"], x["v"], x["lam"])
+    a = R.relation_bwd(x["q"], x["k"], x["v"], f["o"], x["do"], x["lam"], f["row_stat"], want_dself=True)
+    b = R.relation_bwd(x["q"], x["k"], x["v"], f["o"], x["do"], x["lam"], f["row_stat"], want_dself=True,
+                       deterministic=True)
+    torch.cuda.synchronize()
+    for n in ("dq", "dk", "dv", "dself"):
+        assert_close(f"one vs two kernels {n}", _np(a[n]), _np(b[n]), "bf16")
+    lnw = np.log(np.arange(1, T + 1, dtype=np.float64))
+    assert_scalar_close("one vs two kernels dlambda", float(a["dlambda"].item()), float(b["dlambda"].item()),
+                        float(np.abs(lnw * _np(b["dself"])).sum()), "bf16")
+    (r,) = OP.backward_heads(x["qr"], x["kr"], x["vr"], x["lam"], x["dor"], [(1, 2)])
+    compare_backward(a, [(1, 2)], [r], "bf16")
 
 
 @pytest.mark.parametrize("D", [32, 64, 128])
@@ -295,11 +318,16 @@ def test_strided_layout_matches_contiguous():
     assert qs.stride() != x["q"].stride()
     f2 = R.relation_fwd(qs, ks, vs, x["lam"])
     g2 = R.relation_bwd(qs, ks, vs, f2["o"], ds, x["lam"], f2["row_stat"])
+    d1 = R.relation_bwd(x["q"], x["k"], x["v"], f1["o"], x["do"], x["lam"], f1["row_stat"], deterministic=True)
+    d2 = R.relation_bwd(qs, ks, vs, f2["o"], ds, x["lam"], f2["row_stat"], deterministic=True)
     torch.cuda.synchronize()
     assert torch.equal(f1["o"], f2["o"].contiguous())
     assert torch.equal(f1["row_stat"], f2["row_stat"])
-    for n in ("dq", "dk", "dv"):
+    for n in ("dk", "dv"):
         assert torch.equal(g1[n], g2[n].contiguous()), n
+    assert_order_close("dq", _np(g1["dq"]), _np(g2["dq"].contiguous()))
+    for n in ("dq", "dk", "dv"):
+        assert torch.equal(d1[n], d2[n].contiguous()), n
 
 
 def test_autograd_wrapper():
@@ -314,20 +342,26 @@ def test_autograd_wrapper():
     g = R.relation_bwd(x["q"], x["k"], x["v"], f["o"], x["do"], x["lam"], f["row_stat"])
     torch.cuda.synchronize()
     assert torch.equal(y.detach(), f["o"])
-    assert torch.equal(q.grad, g["dq"]) and torch.equal(k.grad, g["dk"]) and torch.equal(v.grad, g["dv"])
+    assert torch.equal(k.grad, g["dk"]) and torch.equal(v.grad, g["dv"])
+    assert_order_close("dq", _np(q.grad), _np(g["dq"]))
     assert abs(lam.grad.item() - g["dlambda"].item()) <= 1e-6 * max(1.0, abs(g["dlambda"].item()))
 
 
 def test_backward_repeatability():
-    """Every gradient is written once, with fixed-order reductions: bitwise repeatable."""
-    x = _prep(I.make_inputs(2, 2, 400, 64, seed=23, qkv_std=0.125, lam=0.5), "bf16")
+    """The two-kernel backward writes every gradient once, with fixed-order
+    reductions: bitwise repeatable. The one-kernel backward is too, except dq,
+    whose atomic sums agree to rounding."""
+    x = _prep(I.make_inputs(2, 2, 1000, 64, seed=23, qkv_std=0.125, lam=0.5), "bf16")
     f = R.relation_fwd(x["q"], x["k"], x["v"], x["lam"])
-    runs = [R.relation_bwd(x["q"], x["k"], x["v"], f["o"], x["do"], x["lam"], f["row_stat"],
-                           want_dself=True) for _ in range(3)]
-    torch.cuda.synchronize()
-    for r in runs[1:]:
-        for n in ("dq", "dk", "dv", "dlambda", "dself"):
-            assert torch.equal(r[n], runs[0][n]), n
+    for det in (True, False):
+        runs = [R.relation_bwd(x["q"], x["k"], x["v"], f["o"], x["do"], x["lam"], f["row_stat"],
+                               want_dself=True, deterministic=det) for _ in range(3)]
+        torch.cuda.synchronize()
+        for r in runs[1:]:
+            for n in ("dk", "dv", "dlambda", "dself") + (("dq",) if det else ()):
+                assert torch.equal(r[n], runs[0][n]), n
+            if not det:
+                assert_order_close("dq", _np(r["dq"]), _np(runs[0]["dq"]))
 
 
 # ----------------------------------------------------------------------------
