@@ -420,6 +420,129 @@ def linear_leg(K: int) -> list:
     return out
 
 
+def mfma_peak_leg(lib, hip) -> dict:
+    """Achievable dense bf16 MFMA rate (relation_mfma_peak_probe: every SIMD
+    runs independent 32x32x16 chains) and the shader clock during it, from the
+    s_memtime / s_memrealtime differences of one wave (s_memrealtime runs at
+    100 MHz), cross-checked against the event time."""
+    import statistics
+    import torch
+    wg, iters = 256, 20000
+    sink = torch.empty(wg * 256, dtype=torch.float32, device="cuda")
+    clocks = torch.zeros(2, dtype=torch.int64, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    flops = float(lib.relation_mfma_peak_flops(wg, iters))
+    ms, mhz = [], []
+    for rep in range(6):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        if lib.relation_mfma_peak_probe(wg, iters, sink.data_ptr(), clocks.data_ptr(), stream) != 0:
+            raise RuntimeError(lib.relation_last_error().decode())
+        e1.record()
+        torch.cuda.synchronize()
+        if rep == 0:
+            continue  # first launch loads the code object
+        ms.append(e0.elapsed_time(e1))
+        t, r = (int(x) for x in clocks.cpu().tolist())
+        mhz.append(100.0 * t / r if r else float("nan"))
+    med = statistics.median(ms)
+    return {"tflops": flops / (med * 1e-3) / 1e12, "ms": med, "flops": flops,
+            "clock_mhz_memtime": statistics.median(mhz),
+            "note": "256 workgroups x 4 waves, 8 independent v_mfma_f32_32x32x16_bf16 chains per wave"}
+
+
+def time_steps(fwd_call, bwd_call, K: int, warmup: int) -> dict:
+    """Per-step event pairs around the forward and the backward call: means and
+    medians of forward, backward and whole-step times (ms)."""
+    import statistics
+    import torch
+    for _ in range(warmup):
+        f = fwd_call()
+        if bwd_call:
+            bwd_call(f)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3 * K)]
+    for s_ in range(K):
+        ev[3 * s_].record()
+        f = fwd_call()
+        ev[3 * s_ + 1].record()
+        if bwd_call:
+            bwd_call(f)
+        ev[3 * s_ + 2].record()
+    torch.cuda.synchronize()
+    fw = [ev[3 * i].elapsed_time(ev[3 * i + 1]) for i in range(K)]
+    bw = [ev[3 * i + 1].elapsed_time(ev[3 * i + 2]) for i in range(K)] if bwd_call else [0.0] * K
+    st = [a + b for a, b in zip(fw, bw)]
+    return {"fwd_ms_mean": sum(fw) / K, "fwd_ms_median": statistics.median(fw),
+            "bwd_ms_mean": sum(bw) / K, "bwd_ms_median": statistics.median(bw),
+            "step_ms_mean": sum(st) / K, "step_ms_median": statistics.median(st)}
+
+
+def workload_leg(name: str, K: int, warmup: int, peak_measured: float) -> dict:
+    """One of the other decoder-scale workloads: forward (+ backward) tokens/s,
+    TFLOP/s and fraction of the bf16 peaks (medians of per-step events), and
+    the materialised baseline where its T x T workspace fits the budget."""
+    import torch
+    from paper_2608_20172_amd import binding as R
+    w = WORKLOADS[name]
+    inp = make_workload_inputs(w)
+    dev = torch.device("cuda:0")
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    q, k, v = (torch.from_numpy(inp[n]).to(tdt).to(dev) for n in ("q", "k", "v"))
+    do = torch.from_numpy(inp["dout"]).to(tdt).to(dev) if w.backward else None
+    lam_t = torch.tensor([float(inp["lam"])], dtype=torch.float32, device=dev)
+    ws = torch.empty(max(1, R.relation_bwd_workspace_bytes(q)), dtype=torch.uint8, device=dev)
+    fwd_call = lambda: R.relation_fwd(q, k, v, lam_t)
+    bwd_call = (lambda f: R.relation_bwd(q, k, v, f["o"], do, lam_t, f["row_stat"], workspace=ws)) \
+        if w.backward else None
+    n = max(10, K)
+    t = time_steps(fwd_call, bwd_call, n, warmup)
+    fl_f = flops(w, "fwd")
+    fl_b = flops(w, "bwd") if w.backward else 0.0
+    step = t["step_ms_median"]
+    out = {"workload": w.name, "B": w.B, "H": w.H, "T": w.T, "D": w.D, "dtype": w.dtype,
+           "passes": "fwd+bwd" if w.backward else "fwd", "steps": n, **t,
+           "tokens_per_s": w.tokens / (step * 1e-3), "tflops": (fl_f + fl_b) / (step * 1e-3) / 1e12,
+           "mfma_peak_frac": (fl_f + fl_b) / (step * 1e-3) / PEAK_BF16,
+           "mfma_measured_peak_frac": (fl_f + fl_b) / (step * 1e-3) / (peak_measured * 1e12)
+           if peak_measured else None,
+           "fwd_tflops": fl_f / (t["fwd_ms_median"] * 1e-3) / 1e12}
+    if w.backward:
+        out["bwd_tflops"] = fl_b / (t["bwd_ms_median"] * 1e-3) / 1e12
+    need = R.relation_fwd_materialized_workspace_bytes(q)
+    if need > MATERIALIZED_BUDGET:
+        out["materialized"] = {"status": f"skipped: T x T workspace {need / 2**30:.1f} GiB exceeds the "
+                                         f"{MATERIALIZED_BUDGET / 2**30:.0f} GiB budget"}
+    else:
+        mws = torch.empty(need, dtype=torch.uint8, device=dev)
+        mf = lambda: R.relation_fwd_materialized(q, k, v, lam_t, workspace=mws)
+        mat = {"status": "ok"}
+        mt = time_steps(mf, None, n, warmup)
+        NTT = w.N * w.T * w.T
+        es = 2 if w.dtype == "bf16" else 4
+        mat["fwd_ms"] = mt["fwd_ms_median"]
+        mat["speedup_fwd"] = mt["fwd_ms_median"] / t["fwd_ms_median"]
+        mat["txt_hbm_GBps"] = NTT * (4 + 4 + es + es) / (mt["fwd_ms_median"] * 1e-3) / 1e9
+        del mws
+        if w.backward:
+            nb = R.relation_bwd_materialized_workspace_bytes(q)
+            if nb > MATERIALIZED_BUDGET:
+                mat["bwd_status"] = "skipped: exceeds budget"
+            else:
+                bws = torch.empty(nb, dtype=torch.uint8, device=dev)
+                mb = lambda: R.relation_bwd_materialized(q, k, v, do, lam_t, workspace=bws)
+                bt = time_steps(mb, None, n, warmup)
+                mat["bwd_ms"] = bt["fwd_ms_median"]
+                mat["speedup_bwd"] = bt["fwd_ms_median"] / t["bwd_ms_median"]
+                mat["speedup_step"] = (mat["fwd_ms"] + mat["bwd_ms"]) / step
+                mat["bwd_txt_hbm_GBps"] = NTT * (8 + 8 + 2 * es + 2 * es) / (bt["fwd_ms_median"] * 1e-3) / 1e9
+                del bws
+        out["materialized"] = mat
+    del q, k, v, do, ws
+    torch.cuda.empty_cache()
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -432,6 +555,7 @@ def main() -> int:
     ap.add_argument("--no-layer", action="store_true", help="skip the layer entry points leg")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode leg")
     ap.add_argument("--no-linear", action="store_true", help="skip the Linear Relation leg")
+    ap.add_argument("--no-workloads", action="store_true", help="skip the other decoder-scale workloads")
     ap.add_argument("--copy-bytes", type=int, default=0)
     ap.add_argument("--copy-kind", choices=("memcpy", "elementwise"), default="elementwise")
     ap.add_argument("--summarize-counters", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
@@ -506,19 +630,13 @@ def main() -> int:
     kern_ms = sum(hip.elapsed_ms(kev[2 * s], kev[2 * s + 1]) for s in range(recorded)) / max(recorded, 1)
     hip.destroy(kev)
 
-    # forward / backward split of a step (a separate pass: the extra events
-    # between the calls are kept out of the timed region)
-    split = [torch.cuda.Event(enable_timing=True) for _ in range(3 * K)]
-    for s in range(K):
-        split[3 * s].record()
-        f = R.relation_fwd(q, k, v, lam_t)
-        split[3 * s + 1].record()
-        if w.backward:
-            R.relation_bwd(q, k, v, f["o"], do, lam_t, f["row_stat"], workspace=ws)
-        split[3 * s + 2].record()
-    torch.cuda.synchronize()
-    fwd_ms = sum(split[3 * s].elapsed_time(split[3 * s + 1]) for s in range(K)) / K
-    bwd_ms = sum(split[3 * s + 1].elapsed_time(split[3 * s + 2]) for s in range(K)) / K
+    # forward / backward split of a step, means and medians of per-step events
+    # (a separate pass: the extra events between the calls are kept out of the
+    # timed region)
+    split = time_steps(lambda: R.relation_fwd(q, k, v, lam_t),
+                       (lambda f: R.relation_bwd(q, k, v, f["o"], do, lam_t, f["row_stat"], workspace=ws))
+                       if w.backward else None, K, 0)
+    fwd_ms, bwd_ms = split["fwd_ms_mean"], split["bwd_ms_mean"]
 
     # each fused kernel alone (further passes with the same launches)
     def kernel_ms(name, call):
@@ -540,8 +658,7 @@ def main() -> int:
         bcall = lambda: R.relation_bwd(q, k, v, f_saved["o"], do, lam_t, f_saved["row_stat"], workspace=ws)
         dcall = lambda: R.relation_bwd(q, k, v, f_saved["o"], do, lam_t, f_saved["row_stat"], workspace=ws,
                                        deterministic=True)
-        fused = lib.relation_bwd_workspace_bytes(ctypes.byref(R.make_problem(q))) > 0 and w.dtype == "bf16" \
-            and w.D <= 64
+        fused = w.dtype == "bf16" and w.D in (32, 64) and w.T >= 1536  # relation_bwd's one-kernel path
         per_kernel["bwd_path"] = "one kernel (dq by atomics)" if fused else "two kernels"
         per_kernel["bwd_dkdv_kernel_ms"] = kernel_ms("bwd_dkdv", bcall)
         if fused:
@@ -582,6 +699,11 @@ def main() -> int:
             if w.backward:
                 mat.update(materialized_backward(w, q, k, v, do, lam_t, fwd_ms, bwd_ms, mat_ms, K, args))
 
+    peak = mfma_peak_leg(lib, hip)
+    legs = {"status": "skipped"}
+    if not args.no_workloads:
+        legs = {n: workload_leg(n, K, args.warmup, peak["tflops"])
+                for n in ("dec10m_T512", "dec30m_T1024", "long_T16384") if n != w.name}
     layer = {"status": "skipped"}
     if not args.no_layer:
         layer = layer_leg(hip, lib, K, args.warmup)
@@ -617,12 +739,17 @@ def main() -> int:
         "mfma_peak_frac": (fl_f + fl_b) / (ms_step * 1e-3) / PEAK_BF16,
         "fwd_ms": fwd_ms,
         "bwd_ms": bwd_ms,
+        "step_split_ms": split,
+        "mfma_measured_peak": peak,
+        "mfma_measured_peak_frac": (fl_f + fl_b) / (ms_step * 1e-3) / (peak["tflops"] * 1e12),
+        "mfma_peak_frac_median_step": (fl_f + fl_b) / (split["step_ms_median"] * 1e-3) / PEAK_BF16,
         **per_kernel,
         "fwd_kernel_tflops": fl_f / (fwd_kern_ms * 1e-3) / 1e12,
         "materialized": mat,
         "layer": layer,
         "decode": decode,
         "linear": linear,
+        "workloads": legs,
         "roofline": {
             "kernel": ("relation_bwd (" + per_kernel.get("bwd_path", "") + ")") if w.backward else "fwd_kernel",
             "bound": "mfma",

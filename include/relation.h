@@ -101,8 +101,9 @@ rel_status relation_exchange_allocation(const rel_problem* p, const void* q, con
 
 /* Backward pass: gradients of sum(dout * o) (App. A.1.7), recomputed tile by
  * tile from q, k, v, o and row_stat.
- * relation_bwd runs one kernel for dk, dv and dq when dtype is bf16 and D is 32
- * or 64 (a row pass before it and a dq pass after it): each workgroup of 256
+ * relation_bwd runs one kernel for dk, dv and dq when dtype is bf16, D is 32
+ * or 64 and T >= 1536 (a row pass before it and a dq pass after it; at shorter
+ * T the two-kernel backward is faster): each workgroup of 256
  * keys adds its dq partials into an fp32 accumulator with atomics, so dq is
  * correct to fp32 rounding but not bitwise run-to-run repeatable; dk, dv,
  * dlambda and dself are. Other problems, and relation_bwd_deterministic
@@ -352,8 +353,10 @@ rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void*
                                void* workspace, size_t workspace_bytes, void* stream);
 
 /* Measurement aid. While armed, every launch of the named kernel ("fwd": the
- * fused forward kernel; "bwd_dkdv", "bwd_dq": the two backward kernels; "bwd":
- * both backward kernels, back to back) is bracketed by
+ * fused forward kernel; "bwd": all kernels of one relation_bwd call, back to
+ * back; "bwd_dkdv": the dk/dv kernel, or the one-kernel backward's main
+ * kernel; "bwd_dq": the two-kernel backward's dq kernel; "bwd_prep",
+ * "bwd_convert": the one-kernel backward's row pass and dq pass) is bracketed by
  * hipEventRecord on its launch stream, using the caller's events in pairs
  * (events[2i] before launch i, events[2i+1] after it) until n_pairs launches
  * have been recorded. The events are owned by the caller (hipEvent_t, created
@@ -362,6 +365,17 @@ rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void*
  * is process-wide and guarded by a mutex. */
 rel_status relation_profile_arm(const char* kernel, void** events, int n_pairs);
 int relation_profile_disarm(void);
+
+/* Measurement aid, not part of the operator: the achievable dense bf16 MFMA
+ * rate. Launches `workgroups` workgroups of 4 waves; every wave runs `iters`
+ * rounds of 8 independent v_mfma_f32_32x32x16_bf16 chains, in all
+ * relation_mfma_peak_flops(workgroups, iters) flop; time it with events on
+ * `stream`. sink: device fp32 [workgroups * 256] (results, so nothing is
+ * optimised away). clocks: device uint64 [2], wave 0 of workgroup 0's
+ * s_memtime and s_memrealtime differences over its loop. */
+int64_t relation_mfma_peak_flops(int workgroups, int iters);
+rel_status relation_mfma_peak_probe(int workgroups, int iters, float* sink, unsigned long long* clocks,
+                                    void* stream);
 
 const char* relation_status_string(rel_status s);
 const char* relation_last_error(void);

@@ -936,7 +936,10 @@ void launch_fused(const BwdArgs& a, hipStream_t stream, hipEvent_t* prof) {
 
 }  // namespace
 
-bool bwd_fused_supported(int D, int dtype) { return dtype == 1 && (D == 32 || D == 64); }
+// The one-kernel backward pays a fixed cost per row (the row pass and the dq
+// pass move about 5 D bytes per row) that the removed dq recompute, whose cost
+// grows with T, outweighs from T of about 1.6K on (measured at T = 1024 and 2048).
+bool bwd_fused_supported(int T, int D, int dtype) { return dtype == 1 && (D == 32 || D == 64) && T >= 1536; }
 
 int bwd_partials(int N, int T, int D, int dtype, bool fused) {
   (void)D;

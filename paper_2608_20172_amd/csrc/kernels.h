@@ -165,10 +165,13 @@ struct LinearArgs {
 bool profile_slot(const char* name, hipEvent_t* start, hipEvent_t* stop);
 
 hipError_t launch_fwd(const FwdArgs& a, int dtype, int D, hipStream_t stream);
+// Measurement aid: dense bf16 MFMA chains (4 waves per workgroup).
+int64_t mfma_peak_flops_per_launch(int workgroups, int iters);
+hipError_t launch_mfma_peak(int workgroups, int iters, float* sink, unsigned long long* clocks, hipStream_t stream);
 hipError_t launch_bwd(const BwdArgs& a, int dtype, int D, hipStream_t stream);
 // The fused backward (one kernel for dK, dV and dQ, dQ summed by atomics) covers
 // these problems; the two-kernel backward covers all.
-bool bwd_fused_supported(int D, int dtype);
+bool bwd_fused_supported(int T, int D, int dtype);
 int bwd_partials(int N, int T, int D, int dtype, bool fused);
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t stream);
 hipError_t launch_allocation(const RowArgs& a, int dtype, int N, hipStream_t stream);

@@ -373,6 +373,20 @@ rel_status relation_profile_arm(const char* kernel, void** events, int n_pairs) 
   return REL_OK;
 }
 
+int64_t relation_mfma_peak_flops(int workgroups, int iters) {
+  if (workgroups <= 0 || iters <= 0) return 0;
+  return rel::mfma_peak_flops_per_launch(workgroups, iters);
+}
+
+rel_status relation_mfma_peak_probe(int workgroups, int iters, float* sink, unsigned long long* clocks,
+                                    void* stream) {
+  if (workgroups <= 0 || iters <= 0) return fail(REL_ERR_INVALID_ARG, "workgroups and iters must be > 0");
+  if (!sink || !clocks) return fail(REL_ERR_INVALID_ARG, "sink and clocks are required");
+  hipError_t e = rel::launch_mfma_peak(workgroups, iters, sink, clocks, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "relation_mfma_peak_probe launch");
+  return REL_OK;
+}
+
 int relation_profile_disarm(void) {
   std::lock_guard<std::mutex> lock(g_prof_mu);
   const int n = g_prof_next;
@@ -471,7 +485,7 @@ size_t bwd_workspace(const rel_problem* p, bool fused) {
   if (fused) b += align256(rows * (size_t)p->D * 4);
   return b;
 }
-bool bwd_fused(const rel_problem* p) { return rel::bwd_fused_supported((int)p->D, p->dtype); }
+bool bwd_fused(const rel_problem* p) { return rel::bwd_fused_supported((int)p->T, (int)p->D, p->dtype); }
 }  // namespace
 
 extern "C" {

@@ -75,16 +75,16 @@ def check_layer(x, dtype, pairing, rope_base, transport="full"):
     assert_close("M", _np(f["row_stat"]), of["M"], dtype)
     # dlambda: summed over every head and row; its terms are ln(i) dR_ii
     lni = np.log(np.arange(1, T + 1, dtype=np.float64))
-    terms = float(np.sum(np.abs(lni[None, None, :] * ob["dS"])))
-    assert_scalar_close("dlambda", float(g["dlambda"].item()), ob["dlam"], terms, dtype)
+    assert_scalar_close("dlambda", float(g["dlambda"].item()), ob["dlam"], lni[None, None, :] * ob["dS"], dtype)
     if pairing:
         vt_grad = ob["dvt"]
         v = x["vr"]
         terms = []
         for p, (a, b) in enumerate(LO.givens_pairs(H, pairing)):
             c, s = math.cos(thr[p]), math.sin(thr[p])
-            terms.append(float(np.sum(np.abs(vt_grad[:, a] * (-s * v[:, a] - c * v[:, b])))
-                               + np.sum(np.abs(vt_grad[:, b] * (c * v[:, a] - s * v[:, b])))))
+            # the angle's gradient sums these per-element terms over (b, t, channel) of both heads
+            terms.append(np.concatenate([(vt_grad[:, a] * (-s * v[:, a] - c * v[:, b])).ravel(),
+                                         (vt_grad[:, b] * (c * v[:, a] - s * v[:, b])).ravel()]))
         _assert_vec("dtheta", _np(g["dtheta"]), ob["dtheta"], terms, dtype)
     else:
         assert g["dtheta"] is None
@@ -101,6 +101,14 @@ def test_layer_bf16(D, pairing, rope):
     check_layer(x, "bf16", pairing, rope)
 
 
+@pytest.mark.parametrize("D,pairing,rope", [(48, "A", 1.0e4), (60, "B", 1.0e4), (64, None, 0.0)])
+def test_layer_one_kernel_backward(D, pairing, rope):
+    """T = 1600: the layer's backward runs the one-kernel path (widths 48 and 60
+    padded to 64)."""
+    x = _prep(1, 4, 1600, D, "bf16", seed=350 + D)
+    check_layer(x, "bf16", pairing, rope)
+
+
 @pytest.mark.parametrize("D,pairing,rope", [(60, "A", 1.0e4), (80, "B", 1.0e4), (64, None, 1.0e4)])
 def test_layer_fp32(D, pairing, rope):
     x = _prep(1, 4, 190, D, "f32", seed=400 + D, std=1.0)
@@ -110,6 +118,7 @@ def test_layer_fp32(D, pairing, rope):
 @pytest.mark.parametrize("D,pairing,rope,dtype,T", [
     (64, None, 0.0, "bf16", 300), (80, "A", 1.0e4, "bf16", 300), (64, "B", 1.0e4, "f32", 190),
     (60, None, 0.0, "bf16", 1), (64, None, 0.0, "bf16", 2), (128, None, 0.0, "bf16", 129),
+    (64, "A", 1.0e4, "bf16", 1600),  # the one-kernel backward (T >= 1536)
 ])
 def test_layer_exchange_only(D, pairing, rope, dtype, T):
     """The exchange-only ablation (App. C): y_i = sum_{j<i} F_ij v~_j, forward and backward."""

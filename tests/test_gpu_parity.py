@@ -88,7 +88,7 @@ def compare_backward(g, heads, refs, dtype, key_from=0, check_dlambda=False):
     dq, dk, dv, dself = _np(g["dq"]), _np(g["dk"]), _np(g["dv"]), _np(g["dself"])
     T = dq.shape[2]
     dlam_gpu = float(g["dlambda"].item())
-    dlam_ref, terms = 0.0, 0.0
+    dlam_ref, terms = 0.0, []
     for (b, h), r in zip(heads, refs):
         rr = r["rows"]
         assert_close(f"dq[{b},{h}]", dq[b, h][rr], r["dq"], dtype)
@@ -96,9 +96,9 @@ def compare_backward(g, heads, refs, dtype, key_from=0, check_dlambda=False):
         assert_close(f"dv[{b},{h}]", dv[b, h][key_from:], r["dv"][key_from:], dtype)
         assert_close(f"dself[{b},{h}]", dself[b, h][rr], r["dS"], dtype)
         dlam_ref += r["dlam"]
-        terms += float(np.sum(np.abs(np.log(rr + 1.0) * r["dS"])))
+        terms.append(np.log(rr + 1.0) * r["dS"])
     if check_dlambda:
-        assert_scalar_close("dlambda", dlam_gpu, dlam_ref, terms, dtype)
+        assert_scalar_close("dlambda", dlam_gpu, dlam_ref, np.concatenate(terms), dtype)
     # dlambda is the ln(i)-weighted sum of the Self credits over every head and row
     i1 = np.arange(1, T + 1, dtype=np.float64)
     via_dself = float(np.sum(np.log(i1)[None, None, :] * dself))
@@ -116,7 +116,7 @@ def check_materialized_backward(x, dtype, heads=None):
     all_heads = heads is None
     heads = heads or [(b, h) for b in range(B) for h in range(H)]
     dq, dk, dv = _np(g["dq"]), _np(g["dk"]), _np(g["dv"])
-    dlam_ref, terms = 0.0, 0.0
+    dlam_ref, terms = 0.0, []
     for (b, h) in heads:
         r = oracle.backward(x["qr"][b, h], x["kr"][b, h], x["vr"][b, h], x["lam"], x["dor"][b, h],
                             row_block=256)
@@ -124,9 +124,9 @@ def check_materialized_backward(x, dtype, heads=None):
         assert_close(f"mat.dk[{b},{h}]", dk[b, h], r["dk"], dtype)
         assert_close(f"mat.dv[{b},{h}]", dv[b, h], r["dv"], dtype)
         dlam_ref += r["dlam"]
-        terms += float(np.sum(np.abs(np.log(r["rows"] + 1.0) * r["dS"])))
+        terms.append(np.log(r["rows"] + 1.0) * r["dS"])
     if all_heads:
-        assert_scalar_close("mat.dlambda", float(g["dlambda"].item()), dlam_ref, terms, dtype)
+        assert_scalar_close("mat.dlambda", float(g["dlambda"].item()), dlam_ref, np.concatenate(terms), dtype)
     return g
 
 
@@ -219,12 +219,13 @@ def test_backward_bf16_ragged(D, deterministic):
     check_backward(x, "bf16", f, deterministic=deterministic)
 
 
-@pytest.mark.parametrize("T", [1, 2, 63, 64, 65, 255, 256, 257, 511, 513, 700])
+@pytest.mark.parametrize("T", [1536, 1537, 1600, 1791, 1855, 2000, 2048, 2049, 2111])
 @pytest.mark.parametrize("D", [32, 64])
 def test_backward_one_kernel_matches_two_kernel(T, D):
-    """The one-kernel backward (256-key workgroups, dq by atomics) against the
-    two-kernel one on the same inputs, at lengths around its 64-row query tiles
-    and 256-key workgroups; the oracle on one head."""
+    """The one-kernel backward (256-key workgroups, dq by atomics; relation_bwd
+    takes it for bf16, D <= 64, T >= 1536) against the two-kernel one on the
+    same inputs, at lengths around its 64-row query tiles and 256-key
+    workgroups; the oracle on one head."""
     x = _prep(I.make_inputs(2, 3, T, D, seed=200 + T + D, qkv_std=1 / math.sqrt(D), lam=0.3), "bf16")
     f = R.relation_fwd(x["q"], x["k"], x["v"], x["lam"])
     a = R.relation_bwd(x["q"], x["k"], x["v"], f["o"], x["do"], x["lam"], f["row_stat"], want_dself=True)
@@ -235,7 +236,7 @@ def test_backward_one_kernel_matches_two_kernel(T, D):
         assert_close(f"one vs two kernels {n}", _np(a[n]), _np(b[n]), "bf16")
     lnw = np.log(np.arange(1, T + 1, dtype=np.float64))
     assert_scalar_close("one vs two kernels dlambda", float(a["dlambda"].item()), float(b["dlambda"].item()),
-                        float(np.abs(lnw * _np(b["dself"])).sum()), "bf16")
+                        lnw * _np(b["dself"]), "bf16")
     (r,) = OP.backward_heads(x["qr"], x["kr"], x["vr"], x["lam"], x["dor"], [(1, 2)])
     compare_backward(a, [(1, 2)], [r], "bf16")
 
@@ -309,7 +310,7 @@ def test_backward_no_count_calibration():
 
 def test_strided_layout_matches_contiguous():
     """[B, T, H, D] storage (head stride D) gives the same results as [B, H, T, D]."""
-    inp = I.make_inputs(2, 3, 150, 64, seed=21, qkv_std=0.125, lam=0.5)
+    inp = I.make_inputs(1, 3, 1600, 64, seed=21, qkv_std=0.125, lam=0.5)
     x = _prep(inp, "bf16")
     f1 = R.relation_fwd(x["q"], x["k"], x["v"], x["lam"])
     g1 = R.relation_bwd(x["q"], x["k"], x["v"], f1["o"], x["do"], x["lam"], f1["row_stat"])
@@ -331,7 +332,7 @@ def test_strided_layout_matches_contiguous():
 
 
 def test_autograd_wrapper():
-    x = _prep(I.make_inputs(1, 2, 130, 64, seed=22, qkv_std=0.125, lam=0.5), "bf16")
+    x = _prep(I.make_inputs(1, 2, 1600, 64, seed=22, qkv_std=0.125, lam=0.5), "bf16")
     q = x["q"].clone().requires_grad_(True)
     k = x["k"].clone().requires_grad_(True)
     v = x["v"].clone().requires_grad_(True)
@@ -351,7 +352,7 @@ def test_backward_repeatability():
     """The two-kernel backward writes every gradient once, with fixed-order
     reductions: bitwise repeatable. The one-kernel backward is too, except dq,
     whose atomic sums agree to rounding."""
-    x = _prep(I.make_inputs(2, 2, 1000, 64, seed=23, qkv_std=0.125, lam=0.5), "bf16")
+    x = _prep(I.make_inputs(2, 2, 1700, 64, seed=23, qkv_std=0.125, lam=0.5), "bf16")
     f = R.relation_fwd(x["q"], x["k"], x["v"], x["lam"])
     for det in (True, False):
         runs = [R.relation_bwd(x["q"], x["k"], x["v"], f["o"], x["do"], x["lam"], f["row_stat"],
@@ -407,8 +408,7 @@ def test_workload_dec100m_forward_backward():
     dl_f, dl_m = float(g["dlambda"].item()), float(m["dlambda"].item())
     log(f"  dlambda flash {dl_f:.6e} materialised {dl_m:.6e}")
     lnw = np.log(np.arange(1, w.T + 1, dtype=np.float64))
-    terms = float(np.abs(lnw[None, None, :] * _np(g["dself"])).sum())
-    assert abs(dl_f - dl_m) <= 2e-2 * max(abs(dl_f), 1e-3 * terms)
+    assert_scalar_close("flash vs materialised dlambda", dl_f, dl_m, lnw[None, None, :] * _np(g["dself"]), "bf16")
 
 
 def test_workload_long_context_full_head():
@@ -435,8 +435,7 @@ def test_workload_long_context_full_head():
     lnw = np.log(np.arange(1, T + 1, dtype=np.float64))
     ds = _np(g["dself"])[b, h]
     head_dlam = float(np.sum(lnw * ds))
-    assert_scalar_close(f"dlambda term of head ({b},{h})", head_dlam, r["dlam"],
-                        float(np.sum(np.abs(lnw * r["dS"]))), "bf16")
+    assert_scalar_close(f"dlambda term of head ({b},{h})", head_dlam, r["dlam"], lnw * r["dS"], "bf16")
     # a second head on sampled rows
     rows = np.unique(np.concatenate([np.arange(0, 8), np.linspace(8, T - 1, 56).astype(np.int64),
                                      np.arange(T - 8, T)]))
