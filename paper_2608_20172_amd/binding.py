@@ -11,7 +11,6 @@ relation_decode, relation_decode_states, relation_decode_merge, ...). ``relation
 from __future__ import annotations
 
 import ctypes
-import math
 import os
 from typing import Optional
 
@@ -80,6 +79,8 @@ _SIGS = {
     "relation_linear_bwd": (ctypes.c_int, [_PP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "relation_profile_arm": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]),
     "relation_profile_disarm": (ctypes.c_int, []),
+    "relation_mfma_peak_flops": (ctypes.c_int64, [ctypes.c_int, ctypes.c_int]),
+    "relation_mfma_peak_probe": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, _P, _P, _P]),
     "relation_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "relation_last_error": (ctypes.c_char_p, []),
     "relation_abi_version": (ctypes.c_int, []),
@@ -560,6 +561,3 @@ def relation(q, k, v, lam, tau_s: float = TAU_S, scale: Optional[float] = None) 
         lam = torch.tensor(float(lam), dtype=torch.float32, device=q.device)
     return _RelationFn.apply(q, k, v, lam, tau_s, scale)
 
-
-def default_scale(D: int) -> float:
-    return 1.0 / math.sqrt(D)

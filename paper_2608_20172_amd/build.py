@@ -19,7 +19,8 @@ LIB = os.path.join(HERE, "librelation.so")
 BUILD_DIR = os.path.join(HERE, "_build")
 
 ARCH = "gfx950"
-SOURCES = ["fwd.hip", "bwd.hip", "rows.hip", "layer.hip", "decode.hip", "linear.hip", "relation_api.cpp"]
+SOURCES = ["fwd.hip", "bwd.hip", "rows.hip", "layer.hip", "decode.hip", "linear.hip", "measure.hip",
+           "relation_api.cpp"]
 
 # Packed fp32 VALU instructions are disabled for all device code.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

@@ -41,41 +41,8 @@ constexpr int kBQ = 128;   // query rows per dQ workgroup
 constexpr int kBK = 64;    // keys per dQ tile
 constexpr int kNT = 256;
 constexpr int kFusedWaves = 8;  // fused backward: 8 waves, 256 keys per workgroup
-#ifndef REL_DQ_WAVES_PER_SIMD
-#define REL_DQ_WAVES_PER_SIMD 3   // bf16, d <= 64
-#endif
-#ifndef REL_DQ_WAVES_PER_SIMD_D128
-#define REL_DQ_WAVES_PER_SIMD_D128 2  // bf16, d = 128
-#endif
-#ifndef REL_DQ_NEGD_SEED
-#define REL_DQ_NEGD_SEED 2  // dQ: 1 = the dP chains start from -D_i (16 registers); 0 = subtract D_i per entry;
-                            // 2 = one more MFMA per block adds -D_i (bf16; 0 on the fp32 path)
-#endif
-#ifndef REL_DQ_PIPELINE
-#define REL_DQ_PIPELINE 0  // dQ: 1 = evidence of block 1 before the products of block 0 (needs 2 waves per SIMD)
-#endif
-#ifndef REL_DQ_OPERAND_BATCH
-#define REL_DQ_OPERAND_BATCH 1
-#endif
-#ifndef REL_DKDV_WAVES_PER_SIMD
-#define REL_DKDV_WAVES_PER_SIMD 2 // bf16, d <= 64
-#endif
-
-#ifndef REL_DQ_FULL_PATH
-#define REL_DQ_FULL_PATH 1
-#endif
-#ifndef REL_DQ_INTERLEAVE
-#define REL_DQ_INTERLEAVE 1
-#endif
-#ifndef REL_DQ_IL_VALU
-#define REL_DQ_IL_VALU 28
-#endif
-#ifndef REL_DKDV_INTERLEAVE
-#define REL_DKDV_INTERLEAVE 1
-#endif
-#ifndef REL_DKDV_IL_VALU
-#define REL_DKDV_IL_VALU 12  // vector instructions scheduled after each matrix instruction
-#endif
+constexpr int kDqIlValu = 28;    // dQ full tiles: vector instructions after each matrix instruction
+constexpr int kDkdvIlValu = 12;  // dK/dV full tiles: the same
 
 // Scheduling pattern for one basic block holding NM matrix instructions and
 // independent vector work: the LDS reads first, then each matrix instruction
@@ -90,14 +57,14 @@ __device__ __forceinline__ void interleave() {
   }
 }
 
+// Waves per SIMD the kernels are compiled for.
 template <class P, int D>
 constexpr int dq_occupancy() {
-  return sizeof(typename P::T) == 2 ? (D <= 64 ? REL_DQ_WAVES_PER_SIMD : REL_DQ_WAVES_PER_SIMD_D128)
-                                    : (D <= 32 ? 2 : 1);
+  return sizeof(typename P::T) == 2 ? (D <= 64 ? 3 : 2) : (D <= 32 ? 2 : 1);
 }
 template <class P, int D>
 constexpr int dkdv_occupancy() {
-  return sizeof(typename P::T) == 2 ? (D <= 64 ? REL_DKDV_WAVES_PER_SIMD : 1) : 1;
+  return sizeof(typename P::T) == 2 ? (D <= 64 ? 2 : 1) : 1;
 }
 
 __global__ void fill_zero_kernel(float* p, int64_t n) {
@@ -221,14 +188,10 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
     a.negd[(int64_t)head * T + qi] = -Di;
     a.m2[(int64_t)head * T + qi] = Mi2;
   }
-  // -D_i enters the dP chains: as their starting accumulator (mode 1), as one
-  // more product of a 0/1 column against -D_i split into two bf16 terms
-  // (mode 2: every key row of this lane's query gets -D_hi - D_lo), or by a
-  // subtraction per entry (mode 0)
-  constexpr int NDM = (REL_DQ_NEGD_SEED == 2 && sizeof(E) != 2) ? 0 : REL_DQ_NEGD_SEED;
-  floatx16 negD;
-#pragma unroll
-  for (int r = 0; r < 16; ++r) negD[r] = NDM == 1 ? -Di : 0.0f;
+  // -D_i enters the dP chains as one more product of a 0/1 column against -D_i
+  // split into two bf16 terms (bf16: every key row of this lane's query gets
+  // -D_hi - D_lo), or by a subtraction per entry (fp32)
+  constexpr int NDM = sizeof(E) == 2 ? 2 : 0;
   const float dsub = NDM == 0 ? Di : 0.0f;
   Op dcol{}, dval{};
   if constexpr (NDM == 2) {
@@ -251,21 +214,13 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
   auto evid = [&](const unsigned char* Ks, const unsigned char* Vs, int krow0, floatx16& s, floatx16& dp) {
     const int row = krow0 + n;
     s = floatx16{};
-    dp = negD;
-    constexpr int NB = REL_DQ_OPERAND_BATCH;  // K/V operand slices read per batch
+    dp = floatx16{};
 #pragma unroll
-    for (int k0 = 0; k0 < KS; k0 += NB) {
-      Op ka[NB], va[NB];
-#pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        ka[j] = P::row_op(Ks, row, k0 + j, L);
-        va[j] = P::row_op(Vs, row, k0 + j, L);
-      }
-#pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        s = P::mma(ka[j], qop[k0 + j], s);
-        dp = P::mma(va[j], doop[k0 + j], dp);  // dP - D
-      }
+    for (int k0 = 0; k0 < KS; ++k0) {
+      const Op ka = P::row_op(Ks, row, k0, L);
+      const Op va = P::row_op(Vs, row, k0, L);
+      s = P::mma(ka, qop[k0], s);
+      dp = P::mma(va, doop[k0], dp);
     }
     if constexpr (NDM == 2) dp = P::mma(dcol, dval, dp);
   };
@@ -324,40 +279,21 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
     __syncthreads();
     if (kt + 1 < nkt) load_tile((kt + 1) * kBK, nxt);
     const unsigned char* Vs = Ks + TB;
-    const int k0 = kt * kBK, k1 = k0 + 32;
-    if (!REL_DQ_PIPELINE) {
+    const int k0 = kt * kBK;
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        const int kb = k0 + 32 * b;
-        Op u[2] = {Op{}, Op{}};
-        floatx16 s, dp;
-        if (kb < qlast) {
-          evid(Ks, Vs, 32 * b, s, dp);
-          grads(s, dp, u, std::false_type{});
-        } else if (kb == qlast) {
-          evid(Ks, Vs, 32 * b, s, dp);
-          grads(s, dp, u, std::true_type{});
-        }
-        accum(Ks, b, u);
+    for (int b = 0; b < 2; ++b) {
+      const int kb = k0 + 32 * b;
+      Op u[2] = {Op{}, Op{}};
+      floatx16 s, dp;
+      if (kb < qlast) {
+        evid(Ks, Vs, 32 * b, s, dp);
+        grads(s, dp, u, std::false_type{});
+      } else if (kb == qlast) {
+        evid(Ks, Vs, 32 * b, s, dp);
+        grads(s, dp, u, std::true_type{});
       }
-      return;
+      accum(Ks, b, u);
     }
-    floatx16 s0, dp0, s1, dp1;
-    Op u0[2] = {Op{}, Op{}}, u1[2] = {Op{}, Op{}};
-    if (k0 <= qlast) {
-      evid(Ks, Vs, 0, s0, dp0);
-      if (k0 == qlast) grads(s0, dp0, u0, std::true_type{});
-      else grads(s0, dp0, u0, std::false_type{});
-    }
-    if (k1 <= qlast) evid(Ks, Vs, 32, s1, dp1);
-    __builtin_amdgcn_sched_barrier(0);
-    accum(Ks, 0, u0);
-    __builtin_amdgcn_sched_barrier(0);
-    if (k1 <= qlast) {
-      if (k1 == qlast) grads(s1, dp1, u1, std::true_type{});
-      else grads(s1, dp1, u1, std::false_type{});
-    }
-    accum(Ks, 1, u1);
   };
   // A full tile (both blocks below every wave's rows) runs without branches.
   auto full = [&](int kt, const unsigned char* Ks, unsigned char* nxt) __attribute__((always_inline)) {
@@ -365,30 +301,19 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
     __syncthreads();
     if (kt + 1 < nkt) load_tile((kt + 1) * kBK, nxt);
     const unsigned char* Vs = Ks + TB;
-    if (REL_DQ_INTERLEAVE) {
-      // the products of block 0 between the vector work of block 1
-      Op u0[2], u1[2];
-      floatx16 s, dp;
-      evid(Ks, Vs, 0, s, dp);
-      grads(s, dp, u0, std::false_type{});
-      __builtin_amdgcn_sched_barrier(0);
-      evid(Ks, Vs, 32, s, dp);
-      __builtin_amdgcn_sched_barrier(0);
-      accum(Ks, 0, u0);
-      grads(s, dp, u1, std::false_type{});
-      interleave<2 * DB, REL_DQ_IL_VALU, 0>();
-      __builtin_amdgcn_sched_barrier(0);
-      accum(Ks, 1, u1);
-      return;
-    }
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      Op u[2];
-      floatx16 s, dp;
-      evid(Ks, Vs, 32 * b, s, dp);
-      grads(s, dp, u, std::false_type{});
-      accum(Ks, b, u);
-    }
+    // the products of block 0 between the vector work of block 1
+    Op u0[2], u1[2];
+    floatx16 s, dp;
+    evid(Ks, Vs, 0, s, dp);
+    grads(s, dp, u0, std::false_type{});
+    __builtin_amdgcn_sched_barrier(0);
+    evid(Ks, Vs, 32, s, dp);
+    __builtin_amdgcn_sched_barrier(0);
+    accum(Ks, 0, u0);
+    grads(s, dp, u1, std::false_type{});
+    interleave<2 * DB, kDqIlValu, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+    accum(Ks, 1, u1);
   };
   // even tiles in bufA, odd ones in bufB
   auto run = [&](int ka, int kb, auto st) __attribute__((always_inline)) {
@@ -402,7 +327,7 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
       if (kt + 1 < kb) st(kt + 1, bufB, bufA);
     }
   };
-  const int kf = REL_DQ_FULL_PATH ? min(i0 / kBK, nkt) : 0;  // tiles below the workgroup's diagonal
+  const int kf = min(i0 / kBK, nkt);  // tiles below the workgroup's diagonal
   run(0, kf, full);
   run(kf, nkt, step);
 
@@ -750,12 +675,12 @@ __global__ __launch_bounds__(NW * 64, (dkdv_occupancy<P, D>())) void bwd_dkdv_ke
     __builtin_amdgcn_sched_barrier(0);
     evid(buf, 1, s1, dp1);
     grads(buf, 0, s0, dp0, f0, u0, std::false_type{});
-    if (REL_DKDV_INTERLEAVE) interleave<2 * KS, REL_DKDV_IL_VALU, 0>();
+    interleave<2 * KS, kDkdvIlValu, 0>();
     __builtin_amdgcn_sched_barrier(0);
     accum(buf, 0, f0, u0);
     write_dU(dUw, 0, u0);
     grads(buf, 1, s1, dp1, f1, u1, std::false_type{});
-    if (REL_DKDV_INTERLEAVE) interleave<4 * DB, REL_DKDV_IL_VALU, 1>();
+    interleave<4 * DB, kDkdvIlValu, 1>();
     __builtin_amdgcn_sched_barrier(0);
     accum(buf, 1, f1, u1);
     write_dU(dUw, 1, u1);

@@ -32,38 +32,15 @@ namespace {
 constexpr int kBQ = 128;  // query rows per workgroup
 constexpr float kRescale = 8.0f;
 constexpr float kSpecMax = 18446744073709551616.0f;  // 2^64
-#ifndef REL_FWD_BF16_WAVES_PER_SIMD
-#define REL_FWD_BF16_WAVES_PER_SIMD 3  // occupancy of the bf16 kernel for d <= 64
-#endif
-#ifndef REL_FWD_WAVES_PER_SIMD
-#define REL_FWD_WAVES_PER_SIMD 2  // occupancy of the fp32 kernel for d <= 64
-#endif
+
+constexpr int kIlValu = 28;  // vector instructions scheduled after each matrix instruction in full tiles
 
 // How the query operand carries c = scale log2(e):
-//   0: raw q; each evidence entry is multiplied by c
-//   1: q c in the operand (fp32)
-//   2: q c as bf16 hi + lo, two MFMAs per slice
-#ifndef REL_FWD_FULL_PATH
-#define REL_FWD_FULL_PATH 1  // branch-free fast steps for tiles below the workgroup's rows
-#endif
-#ifndef REL_FWD_SPECULATE
-#define REL_FWD_SPECULATE 1  // scan with the reference at 0 and check the row totals at the end
-#endif
-#ifndef REL_FWD_PIPE2
-#define REL_FWD_PIPE2 1  // full tiles: evidence of block 1 under the vector work of block 0
-#endif
-#ifndef REL_FWD_INTERLEAVE
-#define REL_FWD_INTERLEAVE 1
-#endif
-#ifndef REL_FWD_IL_VALU
-#define REL_FWD_IL_VALU 28
-#endif
-#ifndef REL_FWD_BF16_QMODE
-#define REL_FWD_BF16_QMODE 0
-#endif
+//   0 (bf16): raw q; each evidence entry is multiplied by c in fp32
+//   1 (fp32): q c in the operand
 template <class P, int D>
 constexpr int qmode() {
-  return sizeof(typename P::T) == 4 ? 1 : (D <= 64 ? REL_FWD_BF16_QMODE : 0);
+  return sizeof(typename P::T) == 4 ? 1 : 0;
 }
 
 // Exchange logits of one 32x32 block, in place: s[r] (U log2 e, or raw q.k in
@@ -133,9 +110,9 @@ __device__ __forceinline__ void scan_block(floatx16 s, floatx16 (&oacc)[D / 32],
 }
 
 // Evidence block: keys krow0 .. krow0+31 of the K tile against this lane's row.
-template <class P, int KS, int QM>
-__device__ __forceinline__ floatx16 evidence(const unsigned char* Ks, int krow0, const typename P::Op (&qhi)[KS],
-                                             const typename P::Op (&qlo)[KS], const Lane& L) {
+template <class P, int KS>
+__device__ __forceinline__ floatx16 evidence(const unsigned char* Ks, int krow0, const typename P::Op (&qop)[KS],
+                                             const Lane& L) {
   floatx16 s = {};
 #pragma unroll
   for (int k0 = 0; k0 < KS; k0 += 2) {  // operands two slices at a time
@@ -143,25 +120,19 @@ __device__ __forceinline__ floatx16 evidence(const unsigned char* Ks, int krow0,
 #pragma unroll
     for (int j = 0; j < 2; ++j) ka[j] = P::row_op(Ks, krow0 + L.n, k0 + j, L);
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      s = P::mma(ka[j], qhi[k0 + j], s);
-      if (QM == 2) s = P::mma(ka[j], qlo[k0 + j], s);
-    }
+    for (int j = 0; j < 2; ++j) s = P::mma(ka[j], qop[k0 + j], s);
   }
   return s;
 }
 
-// Common-case block: the logits of the block, then, if none exceeds the
-// running reference by more than kRescale, the packed weights P of its two
-// 16-key halves and their sum into l. Returns false (and changes neither l nor
-// pop) when the reference has to be raised first.
-template <class P, int D, int QM, bool DIAG, bool CHECK>
-__device__ __forceinline__ bool fast_block(floatx16 s, float m, float& l, float& uii, typename P::Op (&pop)[2],
+// A block of the scan with the reference m held fixed: the logits of the block,
+// the packed weights P of its two 16-key halves and their sum into l.
+template <class P, int D, int QM, bool DIAG>
+__device__ __forceinline__ void fast_block(floatx16 s, float m, float& l, float& uii, typename P::Op (&pop)[2],
                                            const Lane& L, float c) {
   if (DIAG && holds_row(L.n, L.g)) uii = pick(s, row_reg(L.n));  // the Self evidence
   float mx = kNegInf;
-  exchange_logits<DIAG, QM, CHECK>(s, L, c, m, mx);
-  if (CHECK && wave_any(mx > kRescale)) return false;
+  exchange_logits<DIAG, QM, false>(s, L, c, m, mx);
   // l sums the fp32 p (not the bf16-rounded MFMA operand), so that L^E and the
   // saved statistic M carry no operand rounding
 #pragma unroll
@@ -174,19 +145,17 @@ __device__ __forceinline__ bool fast_block(floatx16 s, float m, float& l, float&
     }
     pop[hh] = P::pack(p);
   }
-  return true;
 }
 
 // The 64 keys krow0 .. krow0+63 of a tile (two 32-key blocks, the first at
-// global key kglob) for a wave whose rows start at qr0, without moving the
-// running reference. A block above the wave's rows contributes zero weights,
-// so the P V products (and the accumulators) run on every path. Returns -1,
-// or the first block that needs the reference raised (not accumulated).
-template <class P, int D, int QM, bool FULL, bool CHECK>
-__device__ __forceinline__ int fast_keys64(const unsigned char* Ks, const unsigned char* Vs, int krow0, int kglob,
-                                           int qr0, const typename P::Op (&qhi)[D / 16],
-                                           const typename P::Op (&qlo)[D / 16], floatx16 (&oacc)[D / 32], float m,
-                                           float& l, float& uii, const Lane& L, float c) {
+// global key kglob) for a wave whose rows start at qr0, with the reference
+// held fixed. A block above the wave's rows contributes zero weights, so the
+// P V products (and the accumulators) run on every path. FULL: both blocks lie
+// below every row of the wave.
+template <class P, int D, int QM, bool FULL>
+__device__ __forceinline__ void fast_keys64(const unsigned char* Ks, const unsigned char* Vs, int krow0, int kglob,
+                                            int qr0, const typename P::Op (&qop)[D / 16], floatx16 (&oacc)[D / 32],
+                                            float m, float& l, float& uii, const Lane& L, float c) {
   constexpr int KS = D / 16, DB = D / 32;
   using Op = typename P::Op;
   auto pv = [&](int b, const Op (&pop)[2]) {
@@ -196,89 +165,64 @@ __device__ __forceinline__ int fast_keys64(const unsigned char* Ks, const unsign
       for (int db = 0; db < DB; ++db)
         oacc[db] = P::mma(P::col_op(Vs, krow0 / 16 + 2 * b + hh, 32 * db, L), pop[hh], oacc[db]);
   };
-  // order: evidence of block 0, its vector work, evidence of block 1, then the
-  // P V products of block 0 (which run under the vector work of block 1)
   const int k0 = kglob, k1 = kglob + 32;
   Op p0[2] = {Op{}, Op{}}, p1[2] = {Op{}, Op{}};
   floatx16 s1;
-  if (FULL && !CHECK && REL_FWD_PIPE2) {
-    // both blocks below the wave's rows and no checks: one basic block, the
-    // evidence of block 1 under the vector work of block 0, the P V products
-    // of block 0 under that of block 1
-    const floatx16 s0 = evidence<P, KS, QM>(Ks, krow0, qhi, qlo, L);
+  if (FULL) {
+    // one basic block: the evidence of block 1 under the vector work of block
+    // 0, the P V products of block 0 under that of block 1
+    const floatx16 s0 = evidence<P, KS>(Ks, krow0, qop, L);
     __builtin_amdgcn_sched_barrier(0);
-    s1 = evidence<P, KS, QM>(Ks, krow0 + 32, qhi, qlo, L);
-    fast_block<P, D, QM, false, CHECK>(s0, m, l, uii, p0, L, c);
+    s1 = evidence<P, KS>(Ks, krow0 + 32, qop, L);
+    fast_block<P, D, QM, false>(s0, m, l, uii, p0, L, c);
     __builtin_amdgcn_sched_group_barrier(0x100, 64, 0);
 #pragma unroll
-    for (int i = 0; i < (QM == 2 ? 2 : 1) * KS; ++i) {
+    for (int i = 0; i < KS; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, REL_FWD_IL_VALU, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, kIlValu, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
     pv(0, p0);
-    fast_block<P, D, QM, false, CHECK>(s1, m, l, uii, p1, L, c);
+    fast_block<P, D, QM, false>(s1, m, l, uii, p1, L, c);
     __builtin_amdgcn_sched_group_barrier(0x100, 64, 1);
 #pragma unroll
     for (int i = 0; i < 2 * DB; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
-      __builtin_amdgcn_sched_group_barrier(0x002, REL_FWD_IL_VALU, 1);
+      __builtin_amdgcn_sched_group_barrier(0x002, kIlValu, 1);
     }
     __builtin_amdgcn_sched_barrier(0);
     pv(1, p1);
-    return -1;
+    return;
   }
-  if (FULL) {  // both blocks below the wave's rows
-    const floatx16 s0 = evidence<P, KS, QM>(Ks, krow0, qhi, qlo, L);
-    if (!fast_block<P, D, QM, false, CHECK>(s0, m, l, uii, p0, L, c)) return 0;
-    s1 = evidence<P, KS, QM>(Ks, krow0 + 32, qhi, qlo, L);
-    __builtin_amdgcn_sched_barrier(0);
-    pv(0, p0);
-    if (!REL_FWD_INTERLEAVE) __builtin_amdgcn_sched_barrier(0);
-    const bool ok = fast_block<P, D, QM, false, CHECK>(s1, m, l, uii, p1, L, c);
-    if (REL_FWD_INTERLEAVE) {  // the P V products of block 0 between the vector work of block 1
-      __builtin_amdgcn_sched_group_barrier(0x100, 64, 0);
-#pragma unroll
-      for (int i = 0; i < 2 * DB; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, REL_FWD_IL_VALU, 0);
-      }
-    }
-    if (!ok) return 1;
-    pv(1, p1);
-    return -1;
-  }
+  // order: evidence of block 0, its vector work, evidence of block 1, then the
+  // P V products of block 0 (which run under the vector work of block 1)
   if (k0 <= qr0) {
-    const floatx16 s0 = evidence<P, KS, QM>(Ks, krow0, qhi, qlo, L);
-    const bool ok = k0 == qr0 ? fast_block<P, D, QM, true, CHECK>(s0, m, l, uii, p0, L, c)
-                              : fast_block<P, D, QM, false, CHECK>(s0, m, l, uii, p0, L, c);
-    if (!ok) return 0;
+    const floatx16 s0 = evidence<P, KS>(Ks, krow0, qop, L);
+    if (k0 == qr0) fast_block<P, D, QM, true>(s0, m, l, uii, p0, L, c);
+    else fast_block<P, D, QM, false>(s0, m, l, uii, p0, L, c);
   }
-  if (k1 <= qr0) s1 = evidence<P, KS, QM>(Ks, krow0 + 32, qhi, qlo, L);
+  if (k1 <= qr0) s1 = evidence<P, KS>(Ks, krow0 + 32, qop, L);
   __builtin_amdgcn_sched_barrier(0);
   pv(0, p0);
   __builtin_amdgcn_sched_barrier(0);
   if (k1 <= qr0) {
-    const bool ok = k1 == qr0 ? fast_block<P, D, QM, true, CHECK>(s1, m, l, uii, p1, L, c)
-                              : fast_block<P, D, QM, false, CHECK>(s1, m, l, uii, p1, L, c);
-    if (!ok) return 1;
+    if (k1 == qr0) fast_block<P, D, QM, true>(s1, m, l, uii, p1, L, c);
+    else fast_block<P, D, QM, false>(s1, m, l, uii, p1, L, c);
   }
   pv(1, p1);
-  return -1;
 }
 
-// The same 64 keys from block b0 on, raising the running reference as needed
-// (taken once a block has exceeded it; rare).
+// The same 64 keys, raising the running reference as needed (the rescan of a
+// wave whose fixed-reference scan failed its row-total check; rare).
 template <class P, int D, int QM>
 __device__ __forceinline__ void slow_keys64(const unsigned char* Ks, const unsigned char* Vs, int krow0, int kglob,
-                                            int qr0, int b0, const typename P::Op (&qhi)[D / 16],
-                                            const typename P::Op (&qlo)[D / 16], floatx16 (&oacc)[D / 32], float& m,
-                                            float& l, float& uii, const Lane& L, float c) {
+                                            int qr0, const typename P::Op (&qop)[D / 16], floatx16 (&oacc)[D / 32],
+                                            float& m, float& l, float& uii, const Lane& L, float c) {
   constexpr int KS = D / 16;
-  for (int b = b0; b < 2; ++b) {
+  for (int b = 0; b < 2; ++b) {
     const int kb0 = kglob + 32 * b;
     if (kb0 > qr0) break;
-    const floatx16 s = evidence<P, KS, QM>(Ks, krow0 + 32 * b, qhi, qlo, L);
+    const floatx16 s = evidence<P, KS>(Ks, krow0 + 32 * b, qop, L);
     if (kb0 == qr0) scan_block<P, D, QM, true>(s, oacc, m, l, uii, Vs, krow0 / 16 + 2 * b, L, c);
     else scan_block<P, D, QM, false>(s, oacc, m, l, uii, Vs, krow0 / 16 + 2 * b, L, c);
   }
@@ -351,17 +295,20 @@ __device__ __forceinline__ void finish_row(const FwdArgs& a, typename P::T* o, c
   }
 }
 
-// The query operand of this lane's row (times c unless mode 0).
+// The query operand of this lane's row (times c in mode 1).
 template <class P, int KS, int QM>
 __device__ __forceinline__ void load_query(const typename P::T* q, int64_t st, int qi, int T, const Lane& L, float c,
-                                           typename P::Op (&qhi)[KS], typename P::Op (&qlo)[KS]) {
+                                           typename P::Op (&qop)[KS]) {
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
-    qhi[ks] = typename P::Op{};
-    qlo[ks] = typename P::Op{};
+    qop[ks] = typename P::Op{};
     if (qi < T) {
-      if (QM == 0) qhi[ks] = P::row_op_g(q + qi * st, ks, L);
-      else P::row_op_scaled(q + qi * st, ks, L, c, qhi[ks], qlo[ks]);
+      if (QM == 0) {
+        qop[ks] = P::row_op_g(q + qi * st, ks, L);
+      } else {
+        typename P::Op unused;
+        P::row_op_scaled(q + qi * st, ks, L, c, qop[ks], unused);
+      }
     }
   }
 }
@@ -371,8 +318,7 @@ constexpr int kNT = 256;  // threads per workgroup
 
 template <class P, int D>
 constexpr int fwd_occupancy() {
-  return sizeof(typename P::T) == 2 ? (D <= 64 ? REL_FWD_BF16_WAVES_PER_SIMD : 2)
-                                    : (D <= 64 ? REL_FWD_WAVES_PER_SIMD : 1);
+  return sizeof(typename P::T) == 2 ? (D <= 64 ? 3 : 2) : (D <= 64 ? 2 : 1);  // waves per SIMD
 }
 
 template <class P, int D>
@@ -422,8 +368,8 @@ __global__ __launch_bounds__(kNT, (fwd_occupancy<P, D>())) void fwd_kernel(FwdAr
     }
   };
 
-  Op qhi[KS], qlo[KS];
-  load_query<P, KS, QM>(q, st, qi, T, L, c, qhi, qlo);
+  Op qop[KS];
+  load_query<P, KS, QM>(q, st, qi, T, L, c, qop);
 
   float m = 0.0f, l = 0.0f, uii = 0.0f;
   floatx16 oacc[DB];
@@ -432,86 +378,54 @@ __global__ __launch_bounds__(kNT, (fwd_occupancy<P, D>())) void fwd_kernel(FwdAr
 
   const int kmax = min(i0 + kBQ, T) - 1;  // the diagonal of the last row is included
   const int nkt = kmax / kBK + 1;
-  // Tiles alternate between the buffers: even ones in KA/VA, odd ones in
-  // KB/VB. A fast step returns the block that needs the running reference
-  // raised, or -1.
+  // Tiles alternate between the buffers: even ones in KA/VA, odd ones in KB/VB.
   const int qlast = wave_live ? qr0 : -1;  // rows of a wave past T meet no key
-  constexpr bool SPEC = REL_FWD_SPECULATE;  // no per-block check; the row totals are checked at the end
   auto fast_step = [&](auto full, int kt, const unsigned char* Ks, const unsigned char* Vs, unsigned char* Kn,
                        unsigned char* Vn) __attribute__((always_inline)) {
     wait_loads();      // this wave's part of tile kt is in LDS
     __syncthreads();   // ... and every wave's; tile kt-1 is no longer read
     if (kt + 1 < nkt) load_tile((kt + 1) * kBK, Kn, Vn);
-    return fast_keys64<P, D, QM, decltype(full)::value, !SPEC>(Ks, Vs, 0, kt * kBK, qlast, qhi, qlo, oacc, m, l,
-                                                                uii, L, c);
+    fast_keys64<P, D, QM, decltype(full)::value>(Ks, Vs, 0, kt * kBK, qlast, qop, oacc, m, l, uii, L, c);
   };
-  // fast steps over tiles ka .. kb-1; returns the block that needs the
-  // reference raised (kt then names its tile), or -1
-  int kt = 0;
   auto run_fast = [&](int ka, int kb, auto full) __attribute__((always_inline)) {
-    kt = ka;
+    int kt = ka;
     if (kt < kb && (kt & 1)) {
-      const int r = fast_step(full, kt, KB, VB, KA, VA);
-      if (r >= 0) return r;
+      fast_step(full, kt, KB, VB, KA, VA);
       ++kt;
     }
     for (; kt < kb; kt += 2) {
-      int r = fast_step(full, kt, KA, VA, KB, VB);
-      if (r >= 0) return r;
-      if (kt + 1 < kb) {
-        r = fast_step(full, kt + 1, KB, VB, KA, VA);
-        if (r >= 0) {
-          ++kt;
-          return r;
-        }
-      }
+      fast_step(full, kt, KA, VA, KB, VB);
+      if (kt + 1 < kb) fast_step(full, kt + 1, KB, VB, KA, VA);
     }
-    return -1;
   };
   load_tile(0, KA, VA);
   // tiles below the workgroup's first row have both blocks below every wave's rows
-  const int kf = REL_FWD_FULL_PATH ? min(i0 / kBK, nkt) : 0;
-  int resume = run_fast(0, kf, std::true_type{});
-  if (resume < 0) resume = run_fast(kf, nkt, std::false_type{});
-  if (SPEC) {
-    // The scan ran with the reference fixed at 0. Every weight is at most the
-    // row total l, so l <= 2^64 bounds every weight and |z| <= l max|v|: then
-    // nothing overflowed and the result is exact. Otherwise (or on inf / NaN)
-    // the wave's rows are scanned again with the rescaling loop; the whole
-    // workgroup passes the tiles again for the barriers.
-    const float lt = l + xor32(l);
-    const bool bad = wave_live && !(lt <= kSpecMax);
-    if (__syncthreads_or(bad ? 1 : 0)) {
-      const bool redo = wave_any(bad);
-      if (redo) {
-        m = 0.0f;
-        l = 0.0f;
-        uii = 0.0f;
+  const int kf = min(i0 / kBK, nkt);
+  run_fast(0, kf, std::true_type{});
+  run_fast(kf, nkt, std::false_type{});
+  // The scan ran with the reference fixed at 0. Every weight is at most the row
+  // total l, so l <= 2^64 bounds every weight and |z| <= l max|v|: then nothing
+  // overflowed and the result is exact. Otherwise (or on inf / NaN) the wave's
+  // rows are scanned again with the rescaling loop; the whole workgroup passes
+  // the tiles again for the barriers.
+  const float lt = l + xor32(l);
+  const bool bad = wave_live && !(lt <= kSpecMax);
+  if (__syncthreads_or(bad ? 1 : 0)) {
+    const bool redo = wave_any(bad);
+    if (redo) {
+      m = 0.0f;
+      l = 0.0f;
+      uii = 0.0f;
 #pragma unroll
-        for (int db = 0; db < DB; ++db) oacc[db] = floatx16{};
-      }
-      load_tile(0, KA, VA);
-      for (kt = 0; kt < nkt; ++kt) {
-        const bool odd = kt & 1;
-        wait_loads();
-        __syncthreads();
-        if (kt + 1 < nkt) load_tile((kt + 1) * kBK, odd ? KA : KB, odd ? VA : VB);
-        if (redo)
-          slow_keys64<P, D, QM>(odd ? KB : KA, odd ? VB : VA, 0, kt * kBK, qlast, 0, qhi, qlo, oacc, m, l, uii, L,
-                                c);
-      }
+      for (int db = 0; db < DB; ++db) oacc[db] = floatx16{};
     }
-  } else if (resume >= 0) {
-    // a block exceeded the running reference: finish the scan with rescaling,
-    // passing the same barriers as the rest of the workgroup
-    slow_keys64<P, D, QM>((kt & 1) ? KB : KA, (kt & 1) ? VB : VA, 0, kt * kBK, qlast, resume, qhi, qlo, oacc, m,
-                          l, uii, L, c);
-    for (++kt; kt < nkt; ++kt) {
+    load_tile(0, KA, VA);
+    for (int kt = 0; kt < nkt; ++kt) {
       const bool odd = kt & 1;
       wait_loads();
       __syncthreads();
       if (kt + 1 < nkt) load_tile((kt + 1) * kBK, odd ? KA : KB, odd ? VA : VB);
-      slow_keys64<P, D, QM>(odd ? KB : KA, odd ? VB : VA, 0, kt * kBK, qlast, 0, qhi, qlo, oacc, m, l, uii, L, c);
+      if (redo) slow_keys64<P, D, QM>(odd ? KB : KA, odd ? VB : VA, 0, kt * kBK, qlast, qop, oacc, m, l, uii, L, c);
     }
   }
   if (!wave_live) return;
