@@ -53,7 +53,11 @@ typedef enum rel_status {
   REL_ERR_UNSUPPORTED = -2, /* dtype, head dimension or causal flag this build has no kernel for,
                                T > 2^24, B*H > 2^30, or T * stride_t * element size >= 2^31 bytes */
   REL_ERR_WORKSPACE = -3,   /* workspace pointer null or smaller than the query result */
-  REL_ERR_HIP = -4          /* a HIP/rocBLAS call failed; see relation_last_error() */
+  REL_ERR_HIP = -4,         /* a HIP/rocBLAS call failed; see relation_last_error() */
+  /* Widens the enumeration to every int32 value, so that any status code a C
+   * caller passes (relation_status_string) is a valid value of the type in C++
+   * as well; never returned. */
+  REL_STATUS_MAX_ENUM = 0x7fffffff
 } rel_status;
 
 typedef enum rel_dtype {
@@ -238,7 +242,12 @@ rel_status relation_bwd_materialized(const rel_problem* p, const void* q, const 
  *               in the padded layout, relation_bwd's own workspace, one fp32
  *               dtheta term per (pair, b, t) and their partial sums.
  *               16-byte aligned, contents ignored on entry.
- *   out (backward) must be the tensor the forward call wrote.
+ *   out (backward) must be the tensor the forward call wrote, at the same
+ *               address: from its address and layout the backward pass
+ *               decides whether the forward's output sits there or in the
+ *               saved buffer (a copy elsewhere, with a different 16-byte
+ *               alignment, would make it read a region the forward did not
+ *               write).
  * The backward pass returns dq, dk, dv with respect to the unrotated, unmixed
  * inputs, dlambda as relation_bwd, and dtheta [H/2] fp32 (required when
  * givens != NONE, each angle's gradient summed over batch, positions and
@@ -287,7 +296,10 @@ rel_status relation_layer_bwd(const rel_problem* p, const rel_layer_opts* opts, 
  *   q          [B,H,D] dtype, dense: the new token's relation query.
  *   k_cache, v_cache  [B,H,Tmax,D] dtype with the problem's strides.
  *   lengths    device int32 [B]: entries of the cache in use, new token
- *              included; values outside 1..Tmax are clamped into it.
+ *              included. They are device data, so the host cannot check
+ *              them: for an entry outside 1..Tmax the kernels read only
+ *              inside the cache and that entry's rows of out and row_stat
+ *              are written as NaN.
  *   out        [B,H,D] dtype, dense: y_i.   row_stat  [B,H] fp32, optional:
  *              M_i = ln Z_i + lambda ln i.
  *   workspace  relation_decode_workspace_bytes(p) bytes, 16-byte aligned: the

@@ -63,5 +63,54 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+# Host code under AddressSanitizer and UndefinedBehaviorSanitizer: the C-ABI
+# layer (argument validation, overlap tests, workspace arithmetic) compiled with
+# the sanitizers on the host side only; the device code of the other sources is
+# linked as built by build(). The library is loaded in a process that preloads
+# the ASan runtime (tests/test_abi_sanitized.py); it is for CPU-side checks and
+# launches no kernel.
+HOST_SANITIZE = "-Xarch_host -fsanitize=address -Xarch_host -fsanitize=undefined".split() + \
+    "-Xarch_host -fno-sanitize-recover=undefined -Xarch_host -fno-omit-frame-pointer".split()
+LIB_HOST_SANITIZED = os.path.join(BUILD_DIR, "librelation_host_sanitized.so")
+
+
+def build_host_sanitized(verbose: bool = False) -> str:
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    objs = []
+    for src in SOURCES:
+        if src == "relation_api.cpp":
+            obj = os.path.join(BUILD_DIR, "relation_api_host_sanitized.o")
+            cmd = [hipcc(), *COMMON, *DEVICE_FLAGS, *HOST_SANITIZE, "-x", "hip", "-c", os.path.join(CSRC, src),
+                   "-o", obj]
+            r = subprocess.run(cmd, capture_output=True, text=True)
+            if r.returncode != 0:
+                raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+        else:
+            obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
+            if not os.path.exists(obj):
+                obj = _compile(src)
+        objs.append(obj)
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *HOST_SANITIZE, "-o", LIB_HOST_SANITIZED, *objs,
+           "-L/opt/rocm/lib", "-lrocblas", "-Wl,-rpath,/opt/rocm/lib"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    if verbose:
+        print(f"built {LIB_HOST_SANITIZED}")
+    return LIB_HOST_SANITIZED
+
+
+def asan_runtime() -> str:
+    """Path of the AddressSanitizer runtime of the compiler that built the library."""
+    clang = os.path.join(os.path.dirname(os.path.realpath(hipcc())), "..", "lib", "llvm", "bin", "clang")
+    for cand in (clang, "/opt/rocm/llvm/bin/clang", shutil.which("clang") or ""):
+        if cand and os.path.exists(cand):
+            r = subprocess.run([cand, "-print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True, text=True)
+            path = r.stdout.strip()
+            if r.returncode == 0 and os.path.isabs(path) and os.path.exists(path):
+                return path
+    raise RuntimeError("AddressSanitizer runtime not found")
+
+
 if __name__ == "__main__":
     build(verbose=True)

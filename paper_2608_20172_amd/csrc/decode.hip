@@ -52,9 +52,15 @@ struct Row<float, 4> {
 
 __device__ __forceinline__ float sigm(float x) { return fast_rcp(1.0f + fast_exp2(-x * kLog2e)); }
 
+// The cache length of batch entry b, clamped to 1 .. Tmax so that every read
+// stays inside the cache; the merge writes NaN for an entry outside that range.
 __device__ __forceinline__ int clamp_len(const int32_t* lengths, int b, int Tmax) {
   const int n = lengths[b];
   return n < 1 ? 1 : (n > Tmax ? Tmax : n);
+}
+__device__ __forceinline__ bool len_valid(const int32_t* lengths, int b, int Tmax) {
+  const int n = lengths[b];
+  return n >= 1 && n <= Tmax;
 }
 
 // Merges state (mo, lo, zo) into (m, l, z); an empty state has m = -inf, l = 0.
@@ -258,10 +264,14 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
     zr1 = z1 * il;
     lnZ = fmaxf(S, A) + log1pf(expf(-fabsf(S - A)));
   }
+  // an entry whose cache length lies outside 1 .. Tmax gets NaN: the error is
+  // visible in the output instead of a result at a clamped position
+  const bool valid = len_valid(a.lengths, b, a.Tmax);
+  const float nan = __builtin_nanf("");
   TI* o = (TI*)a.out + (int64_t)n * a.D;
-  if (lane < a.D) Elem<TI>::store(o + lane, omg * vi0 + g * zr0);
-  if (lane + 64 < a.D) Elem<TI>::store(o + lane + 64, omg * vi1 + g * zr1);
-  if (lane == 0 && a.row_stat) a.row_stat[n] = lnZ + lam * ln_i;
+  if (lane < a.D) Elem<TI>::store(o + lane, valid ? omg * vi0 + g * zr0 : nan);
+  if (lane + 64 < a.D) Elem<TI>::store(o + lane + 64, valid ? omg * vi1 + g * zr1 : nan);
+  if (lane == 0 && a.row_stat) a.row_stat[n] = valid ? lnZ + lam * ln_i : nan;
 }
 
 template <typename TI, int VEC>

@@ -353,6 +353,7 @@ const char* relation_status_string(rel_status s) {
     case REL_ERR_UNSUPPORTED: return "unsupported problem";
     case REL_ERR_WORKSPACE: return "workspace too small";
     case REL_ERR_HIP: return "HIP error";
+    case REL_STATUS_MAX_ENUM: break;
   }
   return "unknown status";
 }

@@ -68,12 +68,19 @@ def test_decode_parity(D, dtype):
     assert np.array_equal(_np(r["o"])[0], x["vr"][0, :, 0])
 
 
-def test_decode_lengths_are_clamped():
-    x = _prep(2, 2, 64, 64, "bf16", seed=810, lengths=[0, 99])
+def test_decode_out_of_range_lengths_give_nan():
+    """Cache lengths outside 1..Tmax (0 and Tmax + 1 here) give NaN rows in y
+    and M for those batch entries only; the valid entries match the oracle."""
+    x = _prep(4, 2, 64, 64, "bf16", seed=810, lengths=[0, 64, 65, 17])
     r = R.relation_decode(x["q"], x["k"], x["v"], x["len"], x["lam"])
     torch.cuda.synchronize()
-    Y, M = _oracle_rows(x, lengths=[1, 64])
-    assert_close("y", _np(r["o"]), Y, "bf16")
+    o, M = _np(r["o"]), _np(r["row_stat"])
+    for b in (0, 2):
+        assert np.all(np.isnan(o[b])) and np.all(np.isnan(M[b])), f"entry {b} must be NaN"
+    Y, MR = _oracle_rows(x, lengths=[1, 64, 1, 17])
+    for b in (1, 3):
+        assert_close(f"y[{b}]", o[b], Y[b], "bf16")
+        assert_close(f"M[{b}]", M[b], MR[b], "bf16")
 
 
 def test_decode_is_the_forward_last_row():
