@@ -188,27 +188,41 @@ def _counter_rows(path: str) -> dict:
     return {k: sum(v) / len(v) for k, v in acc.items()}
 
 
+# kernels of the 100M-scale layer's step (bf16, D = 64), by the parts of their names
+STEP_KERNELS = {
+    "fwd_kernel": ("fwd_kernel<", "PolBF16<64>"),
+    "bwd_prep_kernel": ("bwd_prep_kernel<64>",),
+    "bwd_fused_kernel": ("bwd_dkdv_kernel<", "PolBF16<64>", "8, true"),
+    "bwd_dq_convert_kernel": ("bwd_dq_convert_kernel<64>",),
+    "bwd_dq_kernel": ("bwd_dq_kernel<", "PolBF16<64>"),
+    "bwd_dkdv_kernel": ("bwd_dkdv_kernel<", "PolBF16<64>", "4, false"),
+}
+ONE_KERNEL_BWD = ("bwd_prep_kernel", "bwd_fused_kernel", "bwd_dq_convert_kernel")
+TWO_KERNEL_BWD = ("bwd_dq_kernel", "bwd_dkdv_kernel")
+
+
 def summarize_counters(paths, copy_bytes: int) -> dict:
-    """HBM bytes per launch of each fused kernel from FETCH_SIZE and WRITE_SIZE
-    (KiB per dispatch), each scaled by what the same counter reads for a plain
-    device copy of ``copy_bytes`` bytes (read once, written once)."""
+    """HBM bytes per launch of each kernel of the step from FETCH_SIZE and
+    WRITE_SIZE (KiB per dispatch), each scaled by what the same counter reads
+    for a plain device copy of ``copy_bytes`` bytes (read once, written once)."""
     fetch, write, cfetch, cwrite = (_counter_rows(p) for p in paths)
     copy_name = max(cfetch, key=cfetch.get)
     f_scale = copy_bytes / (cfetch[copy_name] * 1024.0)
     w_scale = copy_bytes / (cwrite[max(cwrite, key=cwrite.get)] * 1024.0)
     per = {}
-    for short in ("fwd_kernel", "bwd_dq_kernel", "bwd_dkdv_kernel"):
-        names = [n for n in fetch if short + "<" in n and "PolBF16<64>" in n]
+    for short, parts in STEP_KERNELS.items():
+        names = [n for n in fetch if all(x in n for x in parts)]
         if not names:
             continue
         n = names[0]
         fb = fetch[n] * 1024.0 * f_scale
         wb = write.get(n, 0.0) * 1024.0 * w_scale
-        per[short] = {"fetch_kib_raw": fetch[n], "write_kib_raw": write.get(n, 0.0),
+        per[short] = {"name": n, "fetch_kib_raw": fetch[n], "write_kib_raw": write.get(n, 0.0),
                       "read_bytes": fb, "write_bytes": wb, "bytes": fb + wb}
-    bwd = per["bwd_dq_kernel"]["bytes"] + per["bwd_dkdv_kernel"]["bytes"]
+    one = sum(per[k]["bytes"] for k in ONE_KERNEL_BWD) if all(k in per for k in ONE_KERNEL_BWD) else None
+    two = sum(per[k]["bytes"] for k in TWO_KERNEL_BWD) if all(k in per for k in TWO_KERNEL_BWD) else None
     return {"sources_hash": sources_hash(), "workload": "dec100m_T2048",
-            "bytes_per_launch": bwd, "per_kernel": per,
+            "bytes_per_launch": one, "bytes_per_launch_two_kernel": two, "per_kernel": per,
             "calibration": {"copy_bytes": copy_bytes, "copy_kernel": copy_name,
                             "fetch_factor": f_scale, "write_factor": w_scale}}
 

@@ -575,7 +575,11 @@ __global__ __launch_bounds__(NW * 64, (dkdv_occupancy<P, D>())) void bwd_dkdv_ke
   };
 
   // fused: dU of one query block (rows 32 qb .. of the tile) into the LDS dU
-  // tile, row = key, column = query
+  // tile, row = key, column = query position. Positions within each block are
+  // the queries with bits 2 and 3 of their index swapped, so that the 8 queries
+  // of a lane's operand half (16 hh + 4 g + 0..3 and 16 hh + 8 + 4 g + 0..3) are
+  // one 16-byte chunk: one write per half, and the 16 lanes of each write phase
+  // meet distinct banks.
   auto write_dU = [&](unsigned char* dUw, int qb, const Op (&uop)[2]) __attribute__((always_inline)) {
     if constexpr (FQ) {
       int kr = 32 * w + n;
@@ -583,36 +587,45 @@ __global__ __launch_bounds__(NW * 64, (dkdv_occupancy<P, D>())) void bwd_dkdv_ke
       unsigned char* t = dUw + (kr >> 6) * DUT;
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-          *(uintx2*)(t + PU::off(kr & 63, 32 * qb + 16 * hh + 8 * h + 4 * g)) = half_of(uop[hh], h);
+        *(uintx4*)(t + PU::off(kr & 63, 32 * qb + 16 * hh + 8 * g)) = __builtin_bit_cast(uintx4, uop[hh]);
     }
   };
   // fused: the dQ partial of query tile i0 .. i0+63 from its dU tile, one
-  // 32 x 32 block per wave, added to the fp32 accumulator
+  // 32 x 32 block per wave (waves 0 .. 2 D/32 - 1), added to the fp32
+  // accumulator. (A 16x16x32 split over all eight waves was slower: its
+  // atomics touch four 64-byte row pieces per instruction instead of two
+  // 128-byte rows.)
   auto dq_tile = [&](const unsigned char* dUr, int i0) __attribute__((always_inline)) {
     if constexpr (FQ) if (w < 2 * DB) {
       const int qb = w / DB, db = w % DB;
-      floatx16 acc = {};
+      // two independent accumulation chains (even and odd key slices), so that
+      // consecutive products do not wait on each other's result
+      floatx16 acc = {}, acc2 = {};
 #pragma unroll
-      for (int kq = 0; kq < KW / 16; ++kq) {
+      for (int kq = 0; kq < KW / 16; kq += 2) {
         const Op ua = PU::col_op(dUr + (kq >> 2) * DUT, kq & 3, 32 * qb, L);
         const Op kb = P::col_op(Kq + (kq >> 2) * TB, kq & 3, 32 * db, L);
+        const Op ua2 = PU::col_op(dUr + ((kq + 1) >> 2) * DUT, (kq + 1) & 3, 32 * qb, L);
+        const Op kb2 = P::col_op(Kq + ((kq + 1) >> 2) * TB, (kq + 1) & 3, 32 * db, L);
         acc = P::mma(ua, kb, acc);
+        acc2 = P::mma(ua2, kb2, acc2);
       }
-      // register r holds row acc_row(r, g) = 8 (r / 4) + 4 g + r % 4 of the block,
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[r] += acc2[r];
+      // register r holds position acc_row(r, g) = 8 (r / 4) + 4 g + r % 4 of the
+      // block, that is query 16 (r / 8) + 8 g + r % 8 (bits 2 and 3 swapped back),
       // column n: a uniform base, one lane offset and a constant per register
       float* base = a.dq_acc + ((int64_t)head * T + i0 + 32 * qb) * D + 32 * db;
-      int off = 4 * g * D + n;
+      int off = 8 * g * D + n;
       asm volatile("" : "+v"(off));  // formed here, not held in a register across the tile loop
       const int lim = T - i0 - 32 * qb;  // rows of the block inside the sequence
       if (lim >= 32) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) unsafeAtomicAdd(base + off + (8 * (r >> 2) + (r & 3)) * D, acc[r]);
+        for (int r = 0; r < 16; ++r) unsafeAtomicAdd(base + off + (16 * (r >> 3) + (r & 7)) * D, acc[r]);
       } else {
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-          if (8 * (r >> 2) + (r & 3) + 4 * g < lim) unsafeAtomicAdd(base + off + (8 * (r >> 2) + (r & 3)) * D, acc[r]);
+          if (16 * (r >> 3) + (r & 7) + 8 * g < lim) unsafeAtomicAdd(base + off + (16 * (r >> 3) + (r & 7)) * D, acc[r]);
       }
     }
   };
