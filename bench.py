@@ -384,10 +384,12 @@ def decode_leg(K: int) -> list:
     return out
 
 
-LINEAR_SHAPES = [  # (B, H, T, D): one Linear Relation layer, 8 heads of width 64 (the paper's 60, padded)
-    (1, 8, 4096, 64),
+LINEAR_SHAPES = [  # (B, H, T, D): one Linear Relation layer of 8 heads, width 64 (the paper's 48 and 60,
+    (1, 8, 4096, 64),  # padded) and 128 (the paper's 80, padded)
     (1, 8, 16384, 64),
     (1, 8, 32768, 64),
+    (1, 8, 4096, 128),
+    (1, 8, 32768, 128),
 ]
 
 

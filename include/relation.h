@@ -353,12 +353,20 @@ rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void*
 
 /* Linear Relation backward: gradients of sum(dout * y) with respect to p1,
  * p2, v (dtype, the problem's strides) and g (fp32, dense [B,H,T,D]). The
- * chunk states are recomputed from the inputs. D in {32, 64} (a chunk of 64
- * tokens and its gradients stay in LDS), else REL_ERR_UNSUPPORTED.
+ * chunk states are recomputed from the inputs. D in {32, 64, 128}. At D = 128
+ * the state is taken as four 64 x 64 blocks (halves of the relation and of
+ * the information channels), each of which evolves on its own, and the
+ * gradient is the sum of the four blocks' terms; the result matches the
+ * one-block computation up to fp32 rounding order. Head widths between these
+ * (the paper's 48, 60, 80) run zero-padded to the next one, with an explicit
+ * scale of 1/sqrt(true width).
  *   workspace  relation_linear_bwd_workspace_bytes(p) bytes, 16-byte aligned:
  *              the forward workspace plus, per chunk, the D x D products that
  *              the reverse scan over chunks reads and the state gradients it
- *              writes, and per segment of 16 chunks the reverse summary. */
+ *              writes, and per segment of 16 chunks the reverse summary. At
+ *              D = 128 the chunk states are those of 4 B H heads of width 64,
+ *              plus S ^p1 and S ^p2 of every row and eight fp32 [B,H,T,128]
+ *              planes of partial gradients (5 KiB per token and head). */
 size_t relation_linear_bwd_workspace_bytes(const rel_problem* p);
 rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
                                const float* g, const void* dout, void* dp1, void* dp2, void* dv, float* dg,

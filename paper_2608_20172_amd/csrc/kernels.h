@@ -158,6 +158,17 @@ struct LinearArgs {
   float* segc;           // [N, nseg, D, D]: each segment's forward result from a zero start
   float* segg;           // [N, nseg, D]: each segment's retention product
   float* segp;           // [N, nseg, D, D]: each segment's reverse (gradient) result from a zero start
+  // The D = 128 backward runs as four 64-channel sub-problems: relation half A
+  // (state rows: channels 64 A .. of qt, kt and g) times information half E
+  // (state columns: channels 64 E .. of v and dY), each a D = 64 problem on
+  // virtual head 4 n + 2 A + E with its own chunk states. A row pass forms qt
+  // and kt over all 128 channels first; another sums the sub-problems' partial
+  // gradients and takes them through S and the normalisation.
+  int split;             // 1: D = 64 sub-problem kernels of a D = 128 backward
+  float* qn;             // [N, T, 128] fp32 (split): qt = S ^p1
+  float* kn;             // [N, T, 128] fp32 (split): kt = S ^p2
+  float* part;           // [8][N, T, 128] fp32 (split): dqt from E = 0, 1; dkt from E = 0, 1;
+                         // dv from A = 0, 1 (A = 0 holds the dY of Y = I~ + E); dg from E = 0, 1
 };
 
 // Measurement aid: if armed for kernel `name`, returns the event pair to record

@@ -42,6 +42,38 @@ __device__ __forceinline__ ChunkPos chunk_pos(const LinearArgs& a) {
   return p;
 }
 
+// Virtual heads: with SPLIT (the D = 128 backward cut into four problems of
+// D channels) virtual head nv is sub-problem (A, E) = ((nv >> 1) & 1, nv & 1)
+// of head nv >> 2; otherwise it is the head itself.
+__host__ __device__ __forceinline__ int virtual_heads(const LinearArgs& a) { return a.B * a.H * (a.split ? 4 : 1); }
+
+struct HeadRef {
+  int n;         // head (b * H + h)
+  int64_t hoff;  // element offset of its [T, D] slice in p1, p2, v, dY and their gradients
+  int pa, pe;    // first relation channel (qt, kt, g) and first information channel (v, dY)
+};
+
+template <bool SPLIT, int D>
+__device__ __forceinline__ HeadRef head_ref(const LinearArgs& a, int nv) {
+  HeadRef r;
+  r.n = SPLIT ? nv >> 2 : nv;
+  r.pa = SPLIT ? ((nv >> 1) & 1) * D : 0;
+  r.pe = SPLIT ? (nv & 1) * D : 0;
+  r.hoff = (int64_t)(r.n / a.H) * a.sb + (int64_t)(r.n % a.H) * a.sh;
+  return r;
+}
+
+// K consecutive fp32 values from a 16-byte aligned address.
+template <int K>
+__device__ __forceinline__ void load_f32(const float* p, float (&x)[K]) {
+  static_assert(K % 4 == 0, "whole 16-byte chunks");
+#pragma unroll
+  for (int i = 0; i < K; i += 4) {
+    const float4 u = *reinterpret_cast<const float4*>(p + i);
+    x[i] = u.x; x[i + 1] = u.y; x[i + 2] = u.z; x[i + 3] = u.w;
+  }
+}
+
 // Column of element (r, c) of a row-major [kL][D] array stored with its
 // 16-byte chunks XOR-swizzled by row: rows read together at one column (lanes
 // over rows) then hit different banks, and four consecutive columns from a
@@ -100,22 +132,26 @@ template <> struct Vec4<float> {
 // the sequence are zero), v, optionally dY, and b = running sum of g (zero g
 // past the end, so b stays at its last value). SWZ_VD stores v and dY
 // swizzled (swz), SWZ_QKB qt, kt and b; qt may be null (not stored). One wave
-// per row for the norms and S.
-template <typename TI, int D, int NT, bool SWZ_VD = false, bool WITH_DY = false, bool SWZ_QKB = false>
+// per row for the norms and S. SPLIT: qt and kt are read as formed (fp32, from
+// qn and kn) and the chunk holds the sub-problem's halves of the channels.
+template <typename TI, int D, int NT, bool SWZ_VD = false, bool WITH_DY = false, bool SWZ_QKB = false,
+          bool SPLIT = false>
 __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& p, float (*qt)[D], float (*kt)[D],
                                            float (*vv)[D], float (*bb)[D], float* Srow,
                                            float (*dyl)[D] = nullptr) {
   static_assert(NT % 64 == 0 && kL % (NT / 64) == 0 && NT % D == 0, "rows and channels split evenly");
   constexpr int RPW = kL / (NT / 64);  // rows per wave
   constexpr int U = (D + 63) / 64;     // channels per lane
+  constexpr int GW = SPLIT ? 2 * D : D;  // row length of g, qn and kn
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
-  const int b = p.n / a.H, h = p.n % a.H;
-  const int64_t hoff = (int64_t)b * a.sb + (int64_t)h * a.sh;
-  const TI* P1 = (const TI*)a.p1 + hoff;
-  const TI* P2 = (const TI*)a.p2 + hoff;
-  const TI* V = (const TI*)a.v + hoff;
-  const TI* DY = WITH_DY ? (const TI*)a.dy + hoff : nullptr;
-  const float* G = a.g + (int64_t)p.n * a.T * D;
+  const HeadRef hr = head_ref<SPLIT, D>(a, p.n);
+  const TI* P1 = (const TI*)a.p1 + hr.hoff;
+  const TI* P2 = (const TI*)a.p2 + hr.hoff;
+  const float* Q1 = SPLIT ? a.qn + (int64_t)hr.n * a.T * GW + hr.pa : nullptr;
+  const float* Q2 = SPLIT ? a.kn + (int64_t)hr.n * a.T * GW + hr.pa : nullptr;
+  const TI* V = (const TI*)a.v + hr.hoff + hr.pe;
+  const TI* DY = WITH_DY ? (const TI*)a.dy + hr.hoff + hr.pe : nullptr;
+  const float* G = a.g + (int64_t)hr.n * a.T * GW + hr.pa;
   auto col = [&](bool swzd, int row, int c) { return swzd ? swz<D>(row, c) : c; };
   if (a.vec16) {
     // 16 bytes per lane: LPR lanes hold a row, a wave RPI rows per step. Rows
@@ -130,15 +166,16 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
       if (st * NW * RPI + w * RPI < kL) {  // wave-uniform: the wave's rows are all in the chunk
         const int64_t row = (int64_t)min(p.t0 + r, a.T - 1);
         float x1[EPL], x2[EPL], vx[EPL], gx[EPL], dx[EPL];
-        Vec16<TI>::load(P1 + row * a.st + c0, x1);
-        Vec16<TI>::load(P2 + row * a.st + c0, x2);
+        if constexpr (SPLIT) {
+          load_f32<EPL>(Q1 + row * GW + c0, x1);
+          load_f32<EPL>(Q2 + row * GW + c0, x2);
+        } else {
+          Vec16<TI>::load(P1 + row * a.st + c0, x1);
+          Vec16<TI>::load(P2 + row * a.st + c0, x2);
+        }
         Vec16<TI>::load(V + row * a.st + c0, vx);
         if constexpr (WITH_DY) Vec16<TI>::load(DY + row * a.st + c0, dx);
-#pragma unroll
-        for (int e = 0; e < EPL; e += 4) {
-          const float4 g4 = *reinterpret_cast<const float4*>(G + row * D + c0 + e);
-          gx[e] = g4.x; gx[e + 1] = g4.y; gx[e + 2] = g4.z; gx[e + 3] = g4.w;
-        }
+        load_f32<EPL>(G + row * GW + c0, gx);
         const bool ok = r < p.len;
         float s11 = 0.0f, s22 = 0.0f, s12 = 0.0f;
 #pragma unroll
@@ -148,12 +185,15 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
           s22 += x2[e] * x2[e];
           s12 += x1[e] * x2[e];
         }
-        s11 = lane_group_sum<LPR>(s11);
-        s22 = lane_group_sum<LPR>(s22);
-        s12 = lane_group_sum<LPR>(s12);
-        const float S = ok ? 1.0f / (1.0f + expf(-s12 * a.scale * a.inv_tau)) : 0.0f;
-        const float i1 = ok && s11 > 0.0f ? S * rsqrtf(s11) : 0.0f;
-        const float i2 = ok && s22 > 0.0f ? S * rsqrtf(s22) : 0.0f;
+        float S = 1.0f, i1 = 1.0f, i2 = 1.0f;  // SPLIT: qt and kt as read
+        if constexpr (!SPLIT) {
+          s11 = lane_group_sum<LPR>(s11);
+          s22 = lane_group_sum<LPR>(s22);
+          s12 = lane_group_sum<LPR>(s12);
+          S = ok ? 1.0f / (1.0f + expf(-s12 * a.scale * a.inv_tau)) : 0.0f;
+          i1 = ok && s11 > 0.0f ? S * rsqrtf(s11) : 0.0f;
+          i2 = ok && s22 > 0.0f ? S * rsqrtf(s22) : 0.0f;
+        }
 #pragma unroll
         for (int e = 0; e < EPL; e += 4) {
           const int c = c0 + e;
@@ -185,10 +225,10 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int d = min(lane + 64 * u, D - 1);
-        x1[kb][u] = Elem<TI>::load(P1 + row * a.st + d);
-        x2[kb][u] = Elem<TI>::load(P2 + row * a.st + d);
+        x1[kb][u] = SPLIT ? Q1[row * GW + d] : Elem<TI>::load(P1 + row * a.st + d);
+        x2[kb][u] = SPLIT ? Q2[row * GW + d] : Elem<TI>::load(P2 + row * a.st + d);
         vx[kb][u] = Elem<TI>::load(V + row * a.st + d);
-        gx[kb][u] = G[row * D + d];
+        gx[kb][u] = G[row * GW + d];
         dx[kb][u] = WITH_DY ? Elem<TI>::load(DY + row * a.st + d) : 0.0f;
       }
     }
@@ -211,17 +251,15 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
         s22 += x2[kb][u] * x2[kb][u];
         s12 += x1[kb][u] * x2[kb][u];
       }
-      s11 = group_sum<16>(s11);
-      s22 = group_sum<16>(s22);
-      s12 = group_sum<16>(s12);
-      for (int o = 16; o <= 32; o <<= 1) {
-        s11 += __shfl_xor(s11, o, 64);
-        s22 += __shfl_xor(s22, o, 64);
-        s12 += __shfl_xor(s12, o, 64);
+      float S = 1.0f, i1 = 1.0f, i2 = 1.0f;  // SPLIT: qt and kt as read
+      if constexpr (!SPLIT) {
+        s11 = lane_group_sum<64>(s11);
+        s22 = lane_group_sum<64>(s22);
+        s12 = lane_group_sum<64>(s12);
+        S = ok ? 1.0f / (1.0f + expf(-s12 * a.scale * a.inv_tau)) : 0.0f;
+        i1 = ok && s11 > 0.0f ? S * rsqrtf(s11) : 0.0f;
+        i2 = ok && s22 > 0.0f ? S * rsqrtf(s22) : 0.0f;
       }
-      const float S = ok ? 1.0f / (1.0f + expf(-s12 * a.scale * a.inv_tau)) : 0.0f;
-      const float i1 = ok && s11 > 0.0f ? S * rsqrtf(s11) : 0.0f;
-      const float i2 = ok && s22 > 0.0f ? S * rsqrtf(s22) : 0.0f;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int d = lane + 64 * u;
@@ -377,7 +415,7 @@ __global__ __launch_bounds__(256) void linear_seg_apply_kernel(LinearArgs a, int
 }
 
 hipError_t launch_state_scan(const LinearArgs& a, int reverse, hipStream_t stream) {
-  const dim3 grid((unsigned)((a.D * a.D + 255) / 256), (unsigned)a.nseg, (unsigned)(a.B * a.H));
+  const dim3 grid((unsigned)((a.D * a.D + 255) / 256), (unsigned)a.nseg, (unsigned)virtual_heads(a));
   if (a.nseg > 1) {
     hipLaunchKernelGGL(linear_seg_kernel, grid, dim3(256), 0, stream, a, reverse);
     const hipError_t e = hipGetLastError();
@@ -607,11 +645,11 @@ __global__ __launch_bounds__(kLT2) void linear_out_kernel(LinearArgs a) {
 // ---------------------------------------------------------------------------
 
 // Per chunk: the state contribution (as in the forward pass) and P = Qe^T dY.
-template <typename TI, int D>
+template <typename TI, int D, bool SPLIT = false>
 __global__ __launch_bounds__(kLT) void linear_bstate_kernel(LinearArgs a) {
   __shared__ float qt[kL][D], kt[kL][D], vv[kL][D], bb[kL][D], dy[kL][D];
   const ChunkPos p = chunk_pos(a);
-  load_chunk<TI, D, kLT, false, true>(a, p, qt, kt, vv, bb, nullptr, dy);
+  load_chunk<TI, D, kLT, false, true, false, SPLIT>(a, p, qt, kt, vv, bb, nullptr, dy);
   const int tid = threadIdx.x;
   for (int i = tid; i < kL * D; i += kLT) {
     const int r = i / D, d = i % D;
@@ -659,7 +697,9 @@ __device__ __forceinline__ floatx4 tile_product(const float (*X)[W], int r0, int
 //   query block; k side: the last row of the key block), both factors <= 1;
 //   the diagonal blocks term by term on the vector units.
 // The three inter-chunk products are dense (kL x D by D x D), 32 x 32 blocks.
-template <typename TI, int D>
+// SPLIT: a sub-problem of the D = 128 backward; it ends at dqt, dkt, dv and
+// dg, its partials of the head's gradients, stored in fp32.
+template <typename TI, int D, bool SPLIT = false>
 __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
   static_assert(D == 32 || D == 64, "the backward kernel keeps the chunk of D <= 64 channels in LDS");
   constexpr int SB = 16, NSB = kL / SB, NE = D / 16;
@@ -685,14 +725,17 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
     c0r[k] = a.cprev[base * D * D + tid + k * kLTG];
     gr[k] = a.gout[base * D * D + tid + k * kLTG];
   }
-  load_chunk<TI, D, kLTG, true, true, true>(a, p, qt, kt, vv, bb, Srow, dy);
+  load_chunk<TI, D, kLTG, true, true, true, SPLIT>(a, p, qt, kt, vv, bb, SPLIT ? nullptr : Srow, dy);
 #pragma unroll
   for (int k = 0; k < NCG; ++k) {
     const int e = tid + k * kLTG;
     C0s[e / D][e % D] = c0r[k];
   }
-  const int b = p.n / a.H, h = p.n % a.H;
-  const int64_t hoff = (int64_t)b * a.sb + (int64_t)h * a.sh;
+  const HeadRef hr = head_ref<SPLIT, D>(a, p.n);
+  const int64_t hoff = hr.hoff;
+  constexpr int GW = SPLIT ? 2 * D : D;  // row length of g, dg and the partial gradients
+  const int64_t plane = (int64_t)a.B * a.H * a.T * GW;
+  const int ia = hr.pa ? 1 : 0, ie = hr.pe ? 1 : 0;
   const int r = tid / kTPRG, q0 = (tid % kTPRG) * QW;
   const int qs = swz<D>(r, q0);  // this thread's channels in a swizzled row r (contiguous)
   const int wrow = w * kRowsPerWave;
@@ -773,7 +816,7 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
     kself[i] = kt[r][qs + i];
     bself[i] = bb[r][qs + i];
     dq[i] = dk[i] = 0.0f;
-    dv[i] = dy[r][qs + i];  // Y = I~ + E
+    dv[i] = SPLIT && ia ? 0.0f : dy[r][qs + i];  // Y = I~ + E (once over the halves A)
   }
   {
     const int blo = (wrow / SB) * SB;  // the wave's rows share one 16-row block
@@ -847,23 +890,25 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
   const TI* P2 = (const TI*)a.p2 + hoff + prow * a.st;
   const bool ok = r < p.len;
   float x1[QW], x2[QW];
-  if constexpr (QW == 4) {
-    if (a.vec16) {
-      Vec4<TI>::load(P1 + q0, x1);
-      Vec4<TI>::load(P2 + q0, x2);
+  if constexpr (!SPLIT) {
+    if constexpr (QW == 4) {
+      if (a.vec16) {
+        Vec4<TI>::load(P1 + q0, x1);
+        Vec4<TI>::load(P2 + q0, x2);
+      }
     }
-  }
-  if (QW != 4 || !a.vec16) {
+    if (QW != 4 || !a.vec16) {
+#pragma unroll
+      for (int i = 0; i < QW; ++i) {
+        x1[i] = Elem<TI>::load(P1 + q0 + i);
+        x2[i] = Elem<TI>::load(P2 + q0 + i);
+      }
+    }
 #pragma unroll
     for (int i = 0; i < QW; ++i) {
-      x1[i] = Elem<TI>::load(P1 + q0 + i);
-      x2[i] = Elem<TI>::load(P2 + q0 + i);
+      x1[i] = ok ? x1[i] : 0.0f;
+      x2[i] = ok ? x2[i] : 0.0f;
     }
-  }
-#pragma unroll
-  for (int i = 0; i < QW; ++i) {
-    x1[i] = ok ? x1[i] : 0.0f;
-    x2[i] = ok ? x2[i] : 0.0f;
   }
   __syncthreads();
   // ---- inter-chunk terms: wave w < 3 NB takes block w % NB of
@@ -938,12 +983,22 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
       if (u > sg) later += PT[u * D + d];
     }
     const float base_g = extra + dgam * fast_exp2(bb[kL - 1][swz<D>(kL - 1, d)] * kLog2e) + later;
-    float* dG = a.dg + (int64_t)p.n * a.T * D;
+    float* dG = SPLIT ? a.part + (6 + ie) * plane + (int64_t)hr.n * a.T * GW + hr.pa : a.dg + (int64_t)p.n * a.T * D;
 #pragma unroll
     for (int i = 0; i < RS; ++i) {
       const int j = sg * RS + i;
-      if (j < p.len) dG[(int64_t)(p.t0 + j) * D + d] = base_g + suf[i];
+      if (j < p.len) dG[(int64_t)(p.t0 + j) * GW + d] = base_g + suf[i];
     }
+  }
+  if constexpr (SPLIT) {
+    static_assert(QW == 4, "a thread's channels are one 16-byte chunk");
+    if (ok) {
+      const int64_t row = ((int64_t)hr.n * a.T + p.t0 + r) * GW;
+      Vec4<float>::store(a.part + ie * plane + row + hr.pa + q0, dq);
+      Vec4<float>::store(a.part + (2 + ie) * plane + row + hr.pa + q0, dk);
+      Vec4<float>::store(a.part + (4 + ia) * plane + row + hr.pe + q0, dv);
+    }
+    return;
   }
   // through qt = S p1 / |p1|, kt = S p2 / |p2|, S = sigmoid(scale p1 . p2 / tau_S)
   float s11 = 0.0f, s22 = 0.0f, s12 = 0.0f;
@@ -999,15 +1054,171 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
   }
 }
 
-template <typename TI, int D>
+template <typename TI, int D, bool SPLIT = false>
 hipError_t launch_bwd_d(const LinearArgs& a, hipStream_t stream) {
-  const dim3 grid((unsigned)a.nchunks, (unsigned)(a.B * a.H));
-  hipLaunchKernelGGL((linear_bstate_kernel<TI, D>), grid, dim3(kLT), 0, stream, a);
+  const dim3 grid((unsigned)a.nchunks, (unsigned)virtual_heads(a));
+  hipLaunchKernelGGL((linear_bstate_kernel<TI, D, SPLIT>), grid, dim3(kLT), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   e = launch_state_scan(a, 1, stream);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((linear_grad_kernel<TI, D>), grid, dim3(kLTG), 0, stream, a);
+  hipLaunchKernelGGL((linear_grad_kernel<TI, D, SPLIT>), grid, dim3(kLTG), 0, stream, a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// D = 128 backward. The state's rows evolve with their own retention and its
+// columns do not mix, so the state splits into four 64 x 64 blocks (relation
+// half A, information half E), each a recurrence of its own driven by
+// kt[A], v[E], alpha[A] and read by qt[A]. The scores of the intra-chunk
+// pairs and their gradients split the same way: a score is the sum of its
+// two relation halves, dA the sum of the information halves of dY . v. So
+// every gradient is the sum over the other half of the four problems' terms.
+// Only qt = S ^p1 and kt = S ^p2 (S and the norms over all 128 channels) do
+// not split: a row pass forms them before, and another takes the summed dqt,
+// dkt through S and the normalisation after.
+// ---------------------------------------------------------------------------
+constexpr int kSW = 128;            // channels
+constexpr int kSLanes = kSW / 4;    // lanes per row, 4 channels each
+constexpr int kSRows = 256 / kSLanes;
+
+// The row of flat index row (n * T + t) that this lane's group works on, its
+// first channel, and whether the row exists (rows past the end are clamped
+// to the last one and then not stored, so that every lane takes part in the
+// lane sums).
+struct SplitRow {
+  int64_t nt;
+  int c0;
+  bool ok;
+  int64_t off;  // element offset of the row in p1, p2, v, dY and their gradients
+};
+
+__device__ __forceinline__ SplitRow split_row(const LinearArgs& a) {
+  SplitRow s;
+  const int64_t rows = (int64_t)a.B * a.H * a.T;
+  const int64_t nt = (int64_t)blockIdx.x * kSRows + threadIdx.x / kSLanes;
+  s.ok = nt < rows;
+  s.nt = s.ok ? nt : rows - 1;
+  s.c0 = (threadIdx.x % kSLanes) * 4;
+  const int64_t n = s.nt / a.T, t = s.nt % a.T;
+  s.off = (n / a.H) * a.sb + (n % a.H) * a.sh + t * a.st + s.c0;
+  return s;
+}
+
+template <typename TI>
+__device__ __forceinline__ void load4(const LinearArgs& a, const TI* p, float (&x)[4]) {
+  if (a.vec16) {
+    Vec4<TI>::load(p, x);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) x[i] = Elem<TI>::load(p + i);
+  }
+}
+
+template <typename TI>
+__device__ __forceinline__ void store4(const LinearArgs& a, TI* p, const float (&x)[4]) {
+  if (a.vec16) {
+    Vec4<TI>::store(p, x);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) Elem<TI>::store(p + i, x[i]);
+  }
+}
+
+// S, 1/|p1| and 1/|p2| of a row held as 4 channels per lane over kSLanes lanes.
+__device__ __forceinline__ void row_self(const LinearArgs& a, const float (&x1)[4], const float (&x2)[4], float& S,
+                                        float& in1, float& in2) {
+  float s11 = 0.0f, s22 = 0.0f, s12 = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    s11 += x1[i] * x1[i];
+    s22 += x2[i] * x2[i];
+    s12 += x1[i] * x2[i];
+  }
+  s11 = lane_group_sum<kSLanes>(s11);
+  s22 = lane_group_sum<kSLanes>(s22);
+  s12 = lane_group_sum<kSLanes>(s12);
+  S = 1.0f / (1.0f + expf(-s12 * a.scale * a.inv_tau));
+  in1 = s11 > 0.0f ? rsqrtf(s11) : 0.0f;
+  in2 = s22 > 0.0f ? rsqrtf(s22) : 0.0f;
+}
+
+// qn = S ^p1, kn = S ^p2 per row.
+template <typename TI>
+__global__ __launch_bounds__(256) void linear_split_prep_kernel(LinearArgs a) {
+  const SplitRow w = split_row(a);
+  float x1[4], x2[4], S, in1, in2;
+  load4<TI>(a, (const TI*)a.p1 + w.off, x1);
+  load4<TI>(a, (const TI*)a.p2 + w.off, x2);
+  row_self(a, x1, x2, S, in1, in2);
+  if (w.ok) {
+    float q[4], k[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      q[i] = x1[i] * (S * in1);
+      k[i] = x2[i] * (S * in2);
+    }
+    Vec4<float>::store(a.qn + w.nt * kSW + w.c0, q);
+    Vec4<float>::store(a.kn + w.nt * kSW + w.c0, k);
+  }
+}
+
+// Sums the four problems' partials and takes dqt, dkt through
+// qt = S p1 / |p1|, kt = S p2 / |p2|, S = sigmoid(scale p1 . p2 / tau_S).
+template <typename TI>
+__global__ __launch_bounds__(256) void linear_split_combine_kernel(LinearArgs a) {
+  const SplitRow w = split_row(a);
+  const int64_t plane = (int64_t)a.B * a.H * a.T * kSW, at = w.nt * kSW + w.c0;
+  float x1[4], x2[4], S, in1, in2;
+  load4<TI>(a, (const TI*)a.p1 + w.off, x1);
+  load4<TI>(a, (const TI*)a.p2 + w.off, x2);
+  float pr[8][4];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) Vec4<float>::load(a.part + k * plane + at, pr[k]);
+  row_self(a, x1, x2, S, in1, in2);
+  float dq[4], dk[4], dv[4], dg[4];
+  float ds = 0.0f, h1d = 0.0f, h2d = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    dq[i] = pr[0][i] + pr[1][i];
+    dk[i] = pr[2][i] + pr[3][i];
+    dv[i] = pr[4][i] + pr[5][i];
+    dg[i] = pr[6][i] + pr[7][i];
+    ds += dq[i] * x1[i] * in1 + dk[i] * x2[i] * in2;
+    h1d += x1[i] * in1 * dq[i];
+    h2d += x2[i] * in2 * dk[i];
+  }
+  ds = lane_group_sum<kSLanes>(ds);
+  h1d = lane_group_sum<kSLanes>(h1d);
+  h2d = lane_group_sum<kSLanes>(h2d);
+  if (w.ok) {
+    const float dU = ds * S * (1.0f - S) * a.scale * a.inv_tau;
+    float g1[4], g2[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      g1[i] = dU * x2[i] + S * (dq[i] - x1[i] * in1 * h1d) * in1;
+      g2[i] = dU * x1[i] + S * (dk[i] - x2[i] * in2 * h2d) * in2;
+    }
+    store4<TI>(a, (TI*)a.dp1 + w.off, g1);
+    store4<TI>(a, (TI*)a.dp2 + w.off, g2);
+    store4<TI>(a, (TI*)a.dv + w.off, dv);
+    Vec4<float>::store(a.dg + at, dg);
+  }
+}
+
+template <typename TI>
+hipError_t launch_bwd_split(const LinearArgs& a, hipStream_t stream) {
+  const int64_t rows = (int64_t)a.B * a.H * a.T;
+  const dim3 rgrid((unsigned)((rows + kSRows - 1) / kSRows));
+  hipLaunchKernelGGL((linear_split_prep_kernel<TI>), rgrid, dim3(256), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  LinearArgs s = a;
+  s.D = kSW / 2;
+  s.split = 1;
+  e = launch_bwd_d<TI, kSW / 2, true>(s, stream);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((linear_split_combine_kernel<TI>), rgrid, dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -1016,6 +1227,7 @@ hipError_t launch_bwd_t(const LinearArgs& a, hipStream_t stream) {
   switch (a.D) {
     case 32: return launch_bwd_d<TI, 32>(a, stream);
     case 64: return launch_bwd_d<TI, 64>(a, stream);
+    case kSW: return launch_bwd_split<TI>(a, stream);
     default: return hipErrorInvalidValue;
   }
 }

@@ -1206,15 +1206,22 @@ static int linear_segments(const rel_problem* p) {
 // Forward workspace: per chunk its state contribution, retention product and
 // entering state; per segment of chunks the scan summaries. The backward adds
 // per chunk the gradient contribution and the gradient of the leaving state,
-// and per segment the reverse summaries.
+// and per segment the reverse summaries. The D = 128 backward runs as four
+// problems of 64 channels per head (split): its chunk states are those of
+// 4 B H heads of width 64, and it adds qt and kt of every row and eight
+// planes of partial gradients (fp32, [B H, T, 128] each).
 struct LinearPlan {
   size_t dstate, gamma, cprev, segc, segg, total;  // forward
   size_t pstate, gout, segp, total_bwd;            // backward
+  size_t qn, kn, part;                             // split backward
 };
 
-static LinearPlan plan_linear(const rel_problem* p) {
+static bool linear_split(const rel_problem* p) { return p->D == 128; }
+
+static LinearPlan plan_linear(const rel_problem* p, bool split) {
   LinearPlan L{};
-  const size_t N = (size_t)(p->B * p->H), nc = (size_t)linear_chunks(p), D = (size_t)p->D;
+  const size_t N = (size_t)(p->B * p->H) * (split ? 4 : 1), nc = (size_t)linear_chunks(p);
+  const size_t D = split ? (size_t)p->D / 2 : (size_t)p->D;
   const size_t ns = (size_t)linear_segments(p);
   L.dstate = 0;
   L.gamma = align256(N * nc * D * D * 4);
@@ -1226,6 +1233,13 @@ static LinearPlan plan_linear(const rel_problem* p) {
   L.gout = L.pstate + align256(N * nc * D * D * 4);
   L.segp = L.gout + align256(N * nc * D * D * 4);
   L.total_bwd = L.segp + align256(N * ns * D * D * 4);
+  if (split) {
+    const size_t plane = (size_t)(p->B * p->H) * (size_t)p->T * (size_t)p->D * 4;
+    L.qn = L.total_bwd;
+    L.kn = L.qn + align256(plane);
+    L.part = L.kn + align256(plane);
+    L.total_bwd = L.part + 8 * align256(plane);
+  }
   return L;
 }
 
@@ -1251,12 +1265,17 @@ static void set_linear_workspace(rel::LinearArgs& a, const LinearPlan& L, char* 
     a.gout = (float*)(ws + L.gout);
     a.segp = (float*)(ws + L.segp);
   }
+  if (L.part) {
+    a.qn = (float*)(ws + L.qn);
+    a.kn = (float*)(ws + L.kn);
+    a.part = (float*)(ws + L.part);
+  }
 }
 
 size_t relation_linear_fwd_workspace_bytes(const rel_problem* p) {
   bool empty = false;
   if (check_linear(p, &empty) != REL_OK || empty) return 0;
-  return plan_linear(p).total;
+  return plan_linear(p, false).total;
 }
 
 rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
@@ -1272,7 +1291,7 @@ rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void*
   REL_TRY(check_aligned(g, 4, "g", true));
   REL_TRY(check_aligned(out, es, "out", true));
   REL_TRY(check_aligned(state_out, 4, "state_out", false));
-  const LinearPlan L = plan_linear(p);
+  const LinearPlan L = plan_linear(p, false);
   if (!workspace || workspace_bytes < L.total)
     return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
                 workspace ? workspace_bytes : (size_t)0);
@@ -1305,8 +1324,8 @@ rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void*
 
 size_t relation_linear_bwd_workspace_bytes(const rel_problem* p) {
   bool empty = false;
-  if (check_linear(p, &empty) != REL_OK || empty || p->D > 64) return 0;
-  return plan_linear(p).total_bwd;
+  if (check_linear(p, &empty) != REL_OK || empty) return 0;
+  return plan_linear(p, linear_split(p)).total_bwd;
 }
 
 rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
@@ -1315,9 +1334,6 @@ rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void*
   bool empty = false;
   REL_TRY(check_linear(p, &empty));
   if (empty) return REL_OK;
-  if (p->D > 64)
-    return fail(REL_ERR_UNSUPPORTED, "the Linear Relation backward keeps a chunk in LDS: D <= 64 (got %lld)",
-                (long long)p->D);
   const size_t es = elem_size(p->dtype);
   REL_TRY(check_aligned(p1, es, "p1", true));
   REL_TRY(check_aligned(p2, es, "p2", true));
@@ -1347,7 +1363,7 @@ rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void*
                             {dg, gb, false, true, "dg"},
                             {workspace, need, false, true, "workspace"}}));
   if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected by RELATION_TEST_FAIL_LAUNCH");
-  const LinearPlan L = plan_linear(p);
+  const LinearPlan L = plan_linear(p, linear_split(p));
   rel::LinearArgs a{};
   a.p1 = p1; a.p2 = p2; a.v = v; a.g = g; a.dy = dout;
   a.dp1 = dp1; a.dp2 = dp2; a.dv = dv; a.dg = dg;

@@ -317,3 +317,30 @@ def test_noalloc_backward_validates_before_any_hip_call(lib):
     assert lib.relation_bwd_noalloc(ctypes.byref(small), *a[:11], None, None) == R.REL_ERR_HIP
     # an invalid problem is reported as such, whatever its size
     assert lib.relation_bwd_noalloc(ctypes.byref(prob(D=48)), *a[:11], None, None) == R.REL_ERR_UNSUPPORTED
+
+
+def test_linear_widths_and_workspace(lib):
+    """Linear Relation takes widths 32, 64 and 128 forward and backward (128
+    as four 64-channel problems, whose backward workspace holds at least qt,
+    kt and eight partial-gradient planes of fp32 per token); other widths are
+    refused before any device work, and valid calls reach the launch."""
+    a = ptrs(10)
+    for D in (32, 64, 128):
+        p = prob(B=2, H=3, T=300, D=D)
+        fws = lib.relation_linear_fwd_workspace_bytes(ctypes.byref(p))
+        bws = lib.relation_linear_bwd_workspace_bytes(ctypes.byref(p))
+        assert fws > 0 and bws > fws
+        if D == 128:
+            assert bws >= 10 * 2 * 3 * 300 * 128 * 4
+        st = lib.relation_linear_bwd(ctypes.byref(p), a[0], a[1], a[2], a[3], a[4], a[5], a[6], a[7], a[8],
+                                     a[9], bws, None)
+        assert st == R.REL_ERR_HIP
+        st = lib.relation_linear_bwd(ctypes.byref(p), a[0], a[1], a[2], a[3], a[4], a[5], a[6], a[7], a[8],
+                                     a[9], bws - 1, None)
+        assert st == R.REL_ERR_WORKSPACE
+    for D in (48, 80, 96):
+        p = prob(B=1, H=1, T=64, D=D)
+        assert lib.relation_linear_bwd_workspace_bytes(ctypes.byref(p)) == 0
+        st = lib.relation_linear_bwd(ctypes.byref(p), a[0], a[1], a[2], a[3], a[4], a[5], a[6], a[7], a[8],
+                                     a[9], 1 << 20, None)
+        assert st == R.REL_ERR_UNSUPPORTED

@@ -112,15 +112,18 @@ def check_linear_bwd(x, dtype, heads=None):
 @pytest.mark.parametrize("B,H,T,D,dtype", [
     (2, 2, 300, 64, "bf16"), (1, 2, 190, 32, "f32"), (1, 3, 64, 64, "f32"), (1, 2, 1, 64, "bf16"),
     (1, 2, 65, 32, "bf16"), (1, 2, 129, 64, "f32"),
+    # width 128: four 64-channel problems per head, summed
+    (1, 2, 200, 128, "bf16"), (2, 2, 129, 128, "f32"), (1, 1, 1, 128, "bf16"), (1, 3, 64, 128, "f32"),
 ])
 def test_linear_backward(B, H, T, D, dtype):
     x = _prep(B, H, T, D, dtype, seed=1400 + T + D)
     check_linear_bwd(x, dtype)
 
 
+@pytest.mark.parametrize("D", [64, 128])
 @pytest.mark.parametrize("gmax", [1e-3, 8.0, 80.0])
-def test_linear_backward_retention_range(gmax):
-    x = _prep(1, 2, 200, 64, "f32", seed=1500, gmax=gmax)
+def test_linear_backward_retention_range(gmax, D):
+    x = _prep(1, 2, 200, D, "f32", seed=1500 + D, gmax=gmax)
     check_linear_bwd(x, "f32")
 
 
@@ -129,17 +132,18 @@ def test_linear_backward_long():
     check_linear_bwd(x, "bf16", heads=[(0, 1)])
 
 
-@pytest.mark.parametrize("T,D,gmax", [(1025, 64, 0.02), (3000, 64, 0.005), (2100, 32, 0.01)])
+@pytest.mark.parametrize("T,D,gmax", [(1025, 64, 0.02), (3000, 64, 0.005), (2100, 32, 0.01), (2100, 128, 0.01)])
 def test_linear_backward_scan_segments(T, D, gmax):
     """Forward and reverse state scans across segments of 16 chunks."""
     x = _prep(1, 1, T, D, "f32", seed=1650 + T + D, gmax=gmax)
     check_linear_bwd(x, "f32")
 
 
-def test_linear_backward_strided():
+@pytest.mark.parametrize("D", [64, 128])
+def test_linear_backward_strided(D):
     """Token-major tensors (strides of a [B, T, H, D] layout) give the same
     gradients as contiguous ones."""
-    x = _prep(2, 3, 150, 64, "bf16", seed=1680)
+    x = _prep(2, 3, 150, D, "bf16", seed=1680 + D)
     a = R.relation_linear_bwd(x["p1"], x["p2"], x["v"], x["g"], x["dy"])
     t = lambda z: z.transpose(1, 2).contiguous().transpose(1, 2)
     b = R.relation_linear_bwd(t(x["p1"]), t(x["p2"]), t(x["v"]), x["g"], t(x["dy"]))
@@ -156,21 +160,54 @@ def _misaligned(t):
     return v
 
 
+@pytest.mark.parametrize("D", [64, 128])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_linear_unaligned_rows(dtype):
+def test_linear_unaligned_rows(dtype, D):
     """Rows that do not start on 16-byte boundaries take the element-wise chunk
     loads; forward and backward against the oracle."""
-    x = _prep(1, 2, 200, 64, dtype, seed=1690)
+    x = _prep(1, 2, 200, D, dtype, seed=1690 + D)
     for n in ("p1", "p2", "v", "dy", "g"):
         x[n] = _misaligned(x[n])
     check_linear_fwd(x, dtype)
     check_linear_bwd(x, dtype)
 
 
-def test_linear_backward_repeatable():
-    x = _prep(2, 2, 300, 64, "bf16", seed=1700)
+@pytest.mark.parametrize("D", [64, 128])
+def test_linear_backward_repeatable(D):
+    x = _prep(2, 2, 300, D, "bf16", seed=1700 + D)
     a = R.relation_linear_bwd(x["p1"], x["p2"], x["v"], x["g"], x["dy"])
     b = R.relation_linear_bwd(x["p1"], x["p2"], x["v"], x["g"], x["dy"])
     torch.cuda.synchronize()
     for n in ("dp1", "dp2", "dv", "dg"):
         assert torch.equal(a[n], b[n]), n
+
+
+def _pad(t, width):
+    return torch.nn.functional.pad(t, (0, width - t.shape[-1]))
+
+
+@pytest.mark.parametrize("width,padded,T,dtype", [(80, 128, 300, "bf16"), (80, 128, 130, "f32"),
+                                                   (48, 64, 200, "bf16"), (60, 64, 129, "f32")])
+def test_linear_padded_head_width(width, padded, T, dtype):
+    """The paper's head widths (48, 60, 80) run zero-padded to a supported one
+    with the scale of the true width: p1, p2, v, dY and g padded with zeros
+    (alpha = 1 on the padded channels, whose state rows and columns stay
+    zero). y and every gradient match the oracle at the true width on the
+    first channels and are zero on the padding."""
+    x = _prep(1, 2, T, width, dtype, seed=1800 + width + T)
+    pad = {n: _pad(x[n], padded).contiguous() for n in ("p1", "p2", "v", "dy", "g")}
+    scale = 1.0 / math.sqrt(width)
+    log(f"[linear padded] width {width} -> {padded}, T={T} {dtype}")
+    f = R.relation_linear_fwd(pad["p1"], pad["p2"], pad["v"], pad["g"], scale=scale)
+    r = R.relation_linear_bwd(pad["p1"], pad["p2"], pad["v"], pad["g"], pad["dy"], scale=scale)
+    torch.cuda.synchronize()
+    for h in range(2):
+        ref_f = LO.forward(x["p1r"][0, h], x["p2r"][0, h], x["vr"][0, h], x["gr"][0, h])
+        ref_b = LO.backward(x["p1r"][0, h], x["p2r"][0, h], x["vr"][0, h], x["gr"][0, h], x["dyr"][0, h])
+        y = _np(f["o"])[0, h]
+        assert_close(f"y[0,{h}]", y[:, :width], ref_f["Y"], dtype)
+        assert not np.any(y[:, width:])
+        for n in ("dp1", "dp2", "dv", "dg"):
+            got = _np(r[n])[0, h]
+            assert_close(f"{n}[0,{h}]", got[:, :width], ref_b[n], dtype)
+            assert not np.any(got[:, width:]), f"{n}: padding channels non-zero"
