@@ -16,10 +16,14 @@ One head, tokens t = 1..T, inputs after RoPE (App. B):
 The oracle runs this recurrence token by token (``forward``) and its exact
 adjoint token by token in reverse (``backward``).
 
+The retention gate of eq. 9 (``kda_gate``) maps the pre-activation r_t and
+the per-channel parameters A_log, dt_bias to g_t = log alpha_t; ``forward``
+and ``backward`` take g_t itself, and ``kda_gate_backward`` carries dg on to
+r, A_log and dt_bias.
+
 Readings where the paper leaves a choice (listed in the design notes):
-  * The operator takes the log-retention g_t = log alpha_t (<= 0, one value per
-    channel and token) as its input; how g_t is parameterised (the KDA gate of
-    eq. 9: -exp(A_log) softplus(r_t + dt_bias)) is the caller's elementwise map.
+  * A_log and dt_bias hold one value per channel of the head (the width of
+    r_t and alpha_t), shared by every token and batch entry.
   * The state's rows are indexed by the relation channel (the ^p1 / ^p2 side)
     and its columns by the information channel, as written in App. A.4.
   * The scale inside S_t is 1/sqrt(d_h) unless given.
@@ -31,7 +35,7 @@ import math
 import numpy as np
 from scipy.special import expit
 
-__all__ = ["forward", "backward", "forward_unrolled", "TAU_S"]
+__all__ = ["forward", "backward", "forward_unrolled", "kda_gate", "kda_gate_backward", "TAU_S"]
 
 TAU_S = 2.0
 
@@ -119,3 +123,24 @@ def backward(p1, p2, v, g, dY, *, tau_s: float = TAU_S, scale=None) -> dict:
         dp1[t] += (dh1 - h1[t] * float(h1[t] @ dh1)) / n1[t]
         dp2[t] += (dh2 - h2[t] * float(h2[t] @ dh2)) / n2[t]
     return {"dp1": dp1, "dp2": dp2, "dv": dv, "dg": dg}
+
+
+def kda_gate(r, a_log, dt_bias) -> np.ndarray:
+    """Log-retention of eq. 9: g_t = -exp(A_log) * softplus(r_t + dt_bias)
+    elementwise, r of shape [..., D] and A_log, dt_bias of shape [D]. Since
+    exp > 0 and softplus > 0, g < 0 and alpha = exp(g) lies in (0, 1]."""
+    r, a_log, dt_bias = (np.asarray(x, np.float64) for x in (r, a_log, dt_bias))
+    softplus = np.logaddexp(0.0, r + dt_bias)                  # log(1 + e^x)
+    return -np.exp(a_log) * softplus
+
+
+def kda_gate_backward(r, a_log, dt_bias, dg) -> dict:
+    """Gradients through eq. 9 given dg = dL/dg_t (shape of r): softplus' is
+    the logistic sigmoid, so dr = dg * (-exp(A_log) sigmoid(r + dt_bias));
+    dt_bias enters as r does, so d dt_bias is dr summed over every axis but
+    the channel; and d g / d A_log = g, so d A_log sums dg * g the same way."""
+    r, a_log, dt_bias, dg = (np.asarray(x, np.float64) for x in (r, a_log, dt_bias, dg))
+    dr = dg * (-np.exp(a_log) * expit(r + dt_bias))
+    lead = tuple(range(r.ndim - 1))
+    return {"dr": dr, "da_log": np.sum(dg * kda_gate(r, a_log, dt_bias), axis=lead),
+            "ddt_bias": np.sum(dr, axis=lead)}

@@ -93,7 +93,55 @@ def check_gradients_fd(lo):
             assert np.allclose(r[name], num, atol=3e-8), f"{name} vs FD"
 
 
-ALL_CHECKS = [check_unrolled, check_closed_forms, check_strictly_historical, check_gradients_fd]
+def check_gate_closed_forms(lo):
+    """Eq. 9 at points where softplus is known: softplus(0) = ln 2, softplus(x)
+    tends to x for large x and to e^x for very negative x; g < 0 everywhere
+    and alpha = exp(g) in (0, 1]; A_log scales g by e^A_log."""
+    D = 4
+    a = np.array([0.0, 1.0, -2.0, 0.5])
+    b = np.array([0.3, -0.3, 1.5, -1.5])
+    r0 = np.tile(-b, (3, 1))                                 # r + dt_bias = 0
+    assert np.allclose(lo.kda_gate(r0, a, b), -np.exp(a) * math.log(2.0), atol=1e-15), "softplus(0)"
+    big = np.full((1, D), 40.0) - b
+    assert np.allclose(lo.kda_gate(big, a, b), -np.exp(a) * 40.0, rtol=1e-15), "softplus(40) = 40"
+    small = np.full((1, D), -40.0) - b
+    assert np.allclose(lo.kda_gate(small, a, b), -np.exp(a) * math.exp(-40.0), rtol=1e-12), "softplus(-40)"
+    rng = np.random.default_rng(60)
+    r = rng.standard_normal((50, D)) * 5.0
+    g = lo.kda_gate(r, a, b)
+    assert np.all(g < 0.0) and np.all(np.exp(g) <= 1.0), "g < 0, alpha in (0, 1]"
+    assert np.allclose(lo.kda_gate(r, a + 1.0, b), math.e * g, rtol=1e-14), "A_log scales by e^A_log"
+
+
+def check_gate_gradients_fd(lo):
+    """The chain through eq. 9 and the recurrence: dr, dA_log and ddt_bias from
+    kda_gate_backward (fed dg from the recurrence's adjoint) against central
+    differences of sum(dY * Y) with g = kda_gate(r, A_log, dt_bias)."""
+    h = 1e-6
+    T, D = 6, 3
+    p1, p2, v, _, dY = _inputs(T, D, 70)
+    rng = np.random.default_rng(71)
+    r = rng.standard_normal((T, D))
+    a = rng.standard_normal(D) * 0.5
+    b = rng.standard_normal(D) * 0.5
+    dg = lo.backward(p1, p2, v, lo.kda_gate(r, a, b), dY)["dg"]
+    got = lo.kda_gate_backward(r, a, b, dg)
+    loss = lambda: float(np.sum(dY * lo.forward(p1, p2, v, lo.kda_gate(r, a, b))["Y"]))
+    for name, X in (("dr", r), ("da_log", a), ("ddt_bias", b)):
+        num = np.empty_like(X)
+        for idx in np.ndindex(X.shape):
+            old = X[idx]
+            X[idx] = old + h
+            lp = loss()
+            X[idx] = old - h
+            lm = loss()
+            X[idx] = old
+            num[idx] = (lp - lm) / (2 * h)
+        assert np.allclose(got[name], num, atol=3e-8), f"{name} vs FD"
+
+
+ALL_CHECKS = [check_unrolled, check_closed_forms, check_strictly_historical, check_gradients_fd,
+              check_gate_closed_forms, check_gate_gradients_fd]
 
 
 @pytest.mark.parametrize("check", ALL_CHECKS, ids=lambda c: c.__name__)
@@ -114,6 +162,12 @@ MUTATIONS = [
     ("adjoint_norm_projection", "        dp1[t] += (dh1 - h1[t] * float(h1[t] @ dh1)) / n1[t]",
      "        dp1[t] += dh1 / n1[t]"),
     ("adjoint_write_transposed", "        dv[t] = S[t] * (dC.T @ h2[t]) + dY[t]", "        dv[t] = S[t] * (dC @ h2[t]) + dY[t]"),
+    ("gate_drops_bias", "    softplus = np.logaddexp(0.0, r + dt_bias)", "    softplus = np.logaddexp(0.0, r)"),
+    ("gate_exp_of_softplus", "    return -np.exp(a_log) * softplus", "    return -np.exp(a_log * softplus)"),
+    ("gate_adjoint_softplus_for_sigmoid", "    dr = dg * (-np.exp(a_log) * expit(r + dt_bias))",
+     "    dr = dg * (-np.exp(a_log) * np.logaddexp(0.0, r + dt_bias))"),
+    ("gate_adjoint_alog_drops_dg", "np.sum(dg * kda_gate(r, a_log, dt_bias), axis=lead)",
+     "np.sum(kda_gate(r, a_log, dt_bias), axis=lead)"),
 ]
 
 
