@@ -372,6 +372,31 @@ rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void*
                                const float* g, const void* dout, void* dp1, void* dp2, void* dv, float* dg,
                                void* workspace, size_t workspace_bytes, void* stream);
 
+/* Linear Relation with the retention gate of eq. 9 formed inside the kernels:
+ *   g_t = -exp(A_log) * softplus(r_t + dt_bias),  alpha_t = exp(g_t) in (0, 1]
+ * in place of a caller-made g (Sec. 5.2, App. A.4).
+ *   r          [B,H,T,D] fp32, dense: the gate's pre-activation (the caller's
+ *              low-rank projection of the token's input).
+ *   a_log,     [H,D] fp32, dense: one value per head and channel, shared by
+ *   dt_bias    every batch entry and token.
+ * Forward: as relation_linear_fwd, with the same workspace
+ * (relation_linear_fwd_workspace_bytes). Backward: as relation_linear_bwd, with
+ *   dr         [B,H,T,D] fp32, dense: dL/dr (in place of dg);
+ *   da_log,    [H,D] fp32: dL/dA_log and dL/d dt_bias, each summed over batch
+ *   ddt_bias   entries and tokens in a fixed order (run-to-run identical);
+ *   workspace  relation_linear_gated_bwd_workspace_bytes(p) bytes: the
+ *              ungated backward's plus per head and segment of 256 tokens the
+ *              two sums (fp32).
+ * Missing a_log or dt_bias: REL_ERR_INVALID_ARG. */
+rel_status relation_linear_gated_fwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
+                                     const float* r, const float* a_log, const float* dt_bias, void* out,
+                                     float* state_out, void* workspace, size_t workspace_bytes, void* stream);
+size_t relation_linear_gated_bwd_workspace_bytes(const rel_problem* p);
+rel_status relation_linear_gated_bwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
+                                     const float* r, const float* a_log, const float* dt_bias, const void* dout,
+                                     void* dp1, void* dp2, void* dv, float* dr, float* da_log, float* ddt_bias,
+                                     void* workspace, size_t workspace_bytes, void* stream);
+
 /* Measurement aid. While armed, every launch of the named kernel ("fwd": the
  * fused forward kernel; "bwd": all kernels of one relation_bwd call, back to
  * back; "bwd_dkdv": the dk/dv kernel, or the one-kernel backward's main

@@ -77,6 +77,10 @@ _SIGS = {
     "relation_linear_fwd": (ctypes.c_int, [_PP, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "relation_linear_bwd_workspace_bytes": (ctypes.c_size_t, [_PP]),
     "relation_linear_bwd": (ctypes.c_int, [_PP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "relation_linear_gated_fwd": (ctypes.c_int, [_PP, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "relation_linear_gated_bwd_workspace_bytes": (ctypes.c_size_t, [_PP]),
+    "relation_linear_gated_bwd": (ctypes.c_int, [_PP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                                 ctypes.c_size_t, _P]),
     "relation_profile_arm": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]),
     "relation_profile_disarm": (ctypes.c_int, []),
     "relation_mfma_peak_flops": (ctypes.c_int64, [ctypes.c_int, ctypes.c_int]),
@@ -522,6 +526,61 @@ def relation_linear_bwd(p1, p2, v, g, dout, *, tau_s: float = TAU_S, scale: Opti
                                  _ptr(dp2), _ptr(dv), _ptr(dg), _ptr(ws), _nbytes(ws), _stream())
     _check(st, "relation_linear_bwd")
     return {"dp1": dp1, "dp2": dp2, "dv": dv, "dg": dg}
+
+
+def _gate_params(a_log, dt_bias, p1):
+    H, D = p1.shape[1], p1.shape[3]
+    out = []
+    for name, x in (("a_log", a_log), ("dt_bias", dt_bias)):
+        x = x.to(device=p1.device, dtype=torch.float32).contiguous()
+        if tuple(x.shape) != (H, D):
+            raise ValueError(f"{name} must have shape [H, D] = [{H}, {D}]")
+        out.append(x)
+    return out
+
+
+def relation_linear_gated_fwd(p1, p2, v, r, a_log, dt_bias, *, tau_s: float = TAU_S,
+                              scale: Optional[float] = None, want_state: bool = False, workspace=None):
+    """Linear Relation forward with the retention gate of eq. 9 formed in the
+    kernels from r ([B, H, T, D] fp32) and a_log, dt_bias ([H, D] fp32).
+    Returns dict(o, state)."""
+    lib = load_library()
+    p2, v = _same_layout(p1, p2, v)
+    p = make_problem(p1, tau_s, scale)
+    dev = p1.device
+    r = r.to(device=dev, dtype=torch.float32).contiguous()
+    if r.shape != p1.shape:
+        raise ValueError("r must have the shape of p1")
+    a_log, dt_bias = _gate_params(a_log, dt_bias, p1)
+    o = _layout_like(p1)
+    B, H, T, D = p1.shape
+    state = torch.empty((B, H, D, D), dtype=torch.float32, device=dev) if want_state else None
+    ws = _workspace(max(1, int(lib.relation_linear_fwd_workspace_bytes(ctypes.byref(p)))), workspace, dev)
+    st = lib.relation_linear_gated_fwd(ctypes.byref(p), _ptr(p1), _ptr(p2), _ptr(v), _ptr(r), _ptr(a_log),
+                                       _ptr(dt_bias), _ptr(o), _ptr(state), _ptr(ws), _nbytes(ws), _stream())
+    _check(st, "relation_linear_gated_fwd")
+    return {"o": o, "state": state}
+
+
+def relation_linear_gated_bwd(p1, p2, v, r, a_log, dt_bias, dout, *, tau_s: float = TAU_S,
+                              scale: Optional[float] = None, workspace=None):
+    """Backward of relation_linear_gated_fwd. Returns dict(dp1, dp2, dv, dr
+    (fp32), da_log, ddt_bias ([H, D] fp32))."""
+    lib = load_library()
+    p2, v, dout = _same_layout(p1, p2, v, dout)
+    p = make_problem(p1, tau_s, scale)
+    dev = p1.device
+    r = r.to(device=dev, dtype=torch.float32).contiguous()
+    a_log, dt_bias = _gate_params(a_log, dt_bias, p1)
+    dp1, dp2, dv = _layout_like(p1), _layout_like(p1), _layout_like(p1)
+    dr = torch.empty(p1.shape, dtype=torch.float32, device=dev)
+    da_log, ddt_bias = torch.empty_like(a_log), torch.empty_like(dt_bias)
+    ws = _workspace(max(1, int(lib.relation_linear_gated_bwd_workspace_bytes(ctypes.byref(p)))), workspace, dev)
+    st = lib.relation_linear_gated_bwd(ctypes.byref(p), _ptr(p1), _ptr(p2), _ptr(v), _ptr(r), _ptr(a_log),
+                                       _ptr(dt_bias), _ptr(dout), _ptr(dp1), _ptr(dp2), _ptr(dv), _ptr(dr),
+                                       _ptr(da_log), _ptr(ddt_bias), _ptr(ws), _nbytes(ws), _stream())
+    _check(st, "relation_linear_gated_bwd")
+    return {"dp1": dp1, "dp2": dp2, "dv": dv, "dr": dr, "da_log": da_log, "ddt_bias": ddt_bias}
 
 
 def relation_profile_arm(kernel: str, events: list) -> None:

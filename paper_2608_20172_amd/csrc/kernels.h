@@ -164,6 +164,15 @@ struct LinearArgs {
   // virtual head 4 n + 2 A + E with its own chunk states. A row pass forms qt
   // and kt over all 128 channels first; another sums the sub-problems' partial
   // gradients and takes them through S and the normalisation.
+  // The retention gate of eq. 9 inside the kernels: with a_log set, g holds
+  // the gate's pre-activation r and the chunk loads form
+  // g = -exp(A_log) softplus(r + dt_bias); the backward's dg then goes on to
+  // dr (in place), dA_log and d dt_bias.
+  const float* a_log;    // [H, D] fp32, or null: g is the log-retention itself
+  const float* dt_bias;  // [H, D] fp32
+  float* gpart;          // [B H, ceil(T / 256), 2, D] fp32: per token segment, the sums of dg g and dr
+  float* da_log;         // [H, D] fp32: d A_log
+  float* ddt_bias;       // [H, D] fp32: d dt_bias
   int split;             // 1: D = 64 sub-problem kernels of a D = 128 backward
   float* qn;             // [N, T, 128] fp32 (split): qt = S ^p1
   float* kn;             // [N, T, 128] fp32 (split): kt = S ^p2
@@ -193,6 +202,7 @@ int linear_chunk();
 int linear_scan_segment();  // chunks per segment of the state scans
 hipError_t launch_linear_fwd(const LinearArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_linear_bwd(const LinearArgs& a, int dtype, hipStream_t stream);
+int linear_gate_segment();  // tokens per segment of the gate's parameter-gradient sums
 int decode_slice_keys();
 hipError_t launch_decode_states(const DecodeArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_decode_merge(const DecodeArgs& a, int dtype, hipStream_t stream);

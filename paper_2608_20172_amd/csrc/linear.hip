@@ -63,6 +63,13 @@ __device__ __forceinline__ HeadRef head_ref(const LinearArgs& a, int nv) {
   return r;
 }
 
+// The retention gate of eq. 9: g = -exp(A_log) softplus(r + dt_bias), with
+// softplus(x) = max(x, 0) + log(1 + e^-|x|) (no overflow for any x).
+__device__ __forceinline__ float kda_gate(float r, float ea, float dtb) {
+  const float x = r + dtb;
+  return -ea * (fmaxf(x, 0.0f) + log1pf(expf(-fabsf(x))));
+}
+
 // K consecutive fp32 values from a 16-byte aligned address.
 template <int K>
 __device__ __forceinline__ void load_f32(const float* p, float (&x)[K]) {
@@ -176,6 +183,11 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
         Vec16<TI>::load(V + row * a.st + c0, vx);
         if constexpr (WITH_DY) Vec16<TI>::load(DY + row * a.st + c0, dx);
         load_f32<EPL>(G + row * GW + c0, gx);
+        if (a.a_log) {
+          const int64_t pc = (int64_t)(hr.n % a.H) * GW + hr.pa + c0;
+#pragma unroll
+          for (int e = 0; e < EPL; ++e) gx[e] = kda_gate(gx[e], expf(a.a_log[pc + e]), a.dt_bias[pc + e]);
+        }
         const bool ok = r < p.len;
         float s11 = 0.0f, s22 = 0.0f, s12 = 0.0f;
 #pragma unroll
@@ -229,6 +241,10 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
         x2[kb][u] = SPLIT ? Q2[row * GW + d] : Elem<TI>::load(P2 + row * a.st + d);
         vx[kb][u] = Elem<TI>::load(V + row * a.st + d);
         gx[kb][u] = G[row * GW + d];
+        if (a.a_log) {
+          const int64_t pc = (int64_t)(hr.n % a.H) * GW + hr.pa + d;
+          gx[kb][u] = kda_gate(gx[kb][u], expf(a.a_log[pc]), a.dt_bias[pc]);
+        }
         dx[kb][u] = WITH_DY ? Elem<TI>::load(DY + row * a.st + d) : 0.0f;
       }
     }
@@ -1222,6 +1238,83 @@ hipError_t launch_bwd_split(const LinearArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Backward through the retention gate of eq. 9, after the chunk kernels have
+// left dg in a.dg: per element dr = dg (-exp(A_log) sigmoid(r + dt_bias)),
+// written over dg; per head, token segment and channel the sums of dg g
+// (d A_log, since dg/dA_log = g) and of dr (d dt_bias); then per head and
+// channel the sum of those over batch entries and segments, in a fixed order.
+// ---------------------------------------------------------------------------
+constexpr int kGateSeg = 256;  // tokens per segment
+
+template <int D>
+__global__ __launch_bounds__(256) void linear_gate_bwd_kernel(LinearArgs a) {
+  constexpr int RG = 256 / D;  // rows in flight per step
+  __shared__ float red[2][RG][D];
+  const int n = blockIdx.y, seg = blockIdx.x;
+  const int c = threadIdx.x % D, rg = threadIdx.x / D;
+  const int64_t pc = (int64_t)(n % a.H) * D + c;
+  const float ea = expf(a.a_log[pc]), dtb = a.dt_bias[pc];
+  const int t0 = seg * kGateSeg, t1 = min(a.T, t0 + kGateSeg);
+  const float* R = a.g + (int64_t)n * a.T * D;
+  float* DG = a.dg + (int64_t)n * a.T * D;
+  float sa = 0.0f, sd = 0.0f;
+  for (int t = t0 + rg; t < t1; t += RG) {
+    const int64_t i = (int64_t)t * D + c;
+    const float x = R[i] + dtb, dg = DG[i];
+    const float sp = fmaxf(x, 0.0f) + log1pf(expf(-fabsf(x)));
+    const float dr = dg * (-ea / (1.0f + expf(-x)));
+    sa = __builtin_fmaf(dg, -ea * sp, sa);
+    sd += dr;
+    DG[i] = dr;
+  }
+  red[0][rg][c] = sa;
+  red[1][rg][c] = sd;
+  __syncthreads();
+  if (rg == 0) {
+    for (int k = 1; k < RG; ++k) {
+      sa += red[0][k][c];
+      sd += red[1][k][c];
+    }
+    float* P = a.gpart + (((int64_t)n * gridDim.x + seg) * 2) * D;
+    P[c] = sa;
+    P[D + c] = sd;
+  }
+}
+
+// One thread per (head, channel): the batch entries' segment sums in order.
+__global__ __launch_bounds__(256) void linear_gate_reduce_kernel(LinearArgs a, int nseg) {
+  const int idx = blockIdx.x * 256 + threadIdx.x;
+  if (idx >= a.H * a.D) return;
+  const int h = idx / a.D, c = idx % a.D;
+  float sa = 0.0f, sd = 0.0f;
+  for (int b = 0; b < a.B; ++b) {
+    const float* P = a.gpart + ((int64_t)(b * a.H + h) * nseg * 2) * a.D + c;
+    for (int s = 0; s < nseg; ++s) {
+      sa += P[(2 * s) * a.D];
+      sd += P[(2 * s + 1) * a.D];
+    }
+  }
+  a.da_log[idx] = sa;
+  a.ddt_bias[idx] = sd;
+}
+
+hipError_t launch_gate_bwd(const LinearArgs& a, hipStream_t stream) {
+  const int nseg = (a.T + kGateSeg - 1) / kGateSeg;
+  const dim3 grid((unsigned)nseg, (unsigned)(a.B * a.H));
+  switch (a.D) {
+    case 32: hipLaunchKernelGGL(linear_gate_bwd_kernel<32>, grid, dim3(256), 0, stream, a); break;
+    case 64: hipLaunchKernelGGL(linear_gate_bwd_kernel<64>, grid, dim3(256), 0, stream, a); break;
+    case 128: hipLaunchKernelGGL(linear_gate_bwd_kernel<128>, grid, dim3(256), 0, stream, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(linear_gate_reduce_kernel, dim3((unsigned)((a.H * a.D + 255) / 256)), dim3(256), 0, stream, a,
+                     nseg);
+  return hipGetLastError();
+}
+
 template <typename TI>
 hipError_t launch_bwd_t(const LinearArgs& a, hipStream_t stream) {
   switch (a.D) {
@@ -1264,7 +1357,11 @@ hipError_t launch_linear_fwd(const LinearArgs& a, int dtype, hipStream_t stream)
 }
 
 hipError_t launch_linear_bwd(const LinearArgs& a, int dtype, hipStream_t stream) {
-  return dtype == 1 ? launch_bwd_t<bf16>(a, stream) : launch_bwd_t<float>(a, stream);
+  const hipError_t e = dtype == 1 ? launch_bwd_t<bf16>(a, stream) : launch_bwd_t<float>(a, stream);
+  if (e != hipSuccess || !a.a_log) return e;
+  return launch_gate_bwd(a, stream);
 }
+
+int linear_gate_segment() { return kGateSeg; }
 
 }  // namespace rel

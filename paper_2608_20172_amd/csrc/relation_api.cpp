@@ -1214,6 +1214,7 @@ struct LinearPlan {
   size_t dstate, gamma, cprev, segc, segg, total;  // forward
   size_t pstate, gout, segp, total_bwd;            // backward
   size_t qn, kn, part;                             // split backward
+  size_t gpart, total_gated;                       // gated backward: the gate's segment sums
 };
 
 static bool linear_split(const rel_problem* p) { return p->D == 128; }
@@ -1240,6 +1241,9 @@ static LinearPlan plan_linear(const rel_problem* p, bool split) {
     L.part = L.kn + align256(plane);
     L.total_bwd = L.part + 8 * align256(plane);
   }
+  const size_t gseg = (size_t)((p->T + rel::linear_gate_segment() - 1) / rel::linear_gate_segment());
+  L.gpart = L.total_bwd;
+  L.total_gated = L.gpart + align256((size_t)(p->B * p->H) * gseg * 2 * (size_t)p->D * 4);
   return L;
 }
 
@@ -1278,9 +1282,10 @@ size_t relation_linear_fwd_workspace_bytes(const rel_problem* p) {
   return plan_linear(p, false).total;
 }
 
-rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
-                               const float* g, void* out, float* state_out, void* workspace,
-                               size_t workspace_bytes, void* stream) {
+// g: the log-retention, or with a_log set the gate's pre-activation r.
+static rel_status linear_fwd_impl(const rel_problem* p, const void* p1, const void* p2, const void* v, const float* g,
+                                  const float* a_log, const float* dt_bias, void* out, float* state_out,
+                                  void* workspace, size_t workspace_bytes, void* stream) {
   bool empty = false;
   REL_TRY(check_linear(p, &empty));
   if (empty) return REL_OK;
@@ -1288,7 +1293,9 @@ rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void*
   REL_TRY(check_aligned(p1, es, "p1", true));
   REL_TRY(check_aligned(p2, es, "p2", true));
   REL_TRY(check_aligned(v, es, "v", true));
-  REL_TRY(check_aligned(g, 4, "g", true));
+  REL_TRY(check_aligned(g, 4, a_log ? "r" : "g", true));
+  REL_TRY(check_aligned(a_log, 4, "a_log", false));
+  REL_TRY(check_aligned(dt_bias, 4, "dt_bias", false));
   REL_TRY(check_aligned(out, es, "out", true));
   REL_TRY(check_aligned(state_out, 4, "state_out", false));
   const LinearPlan L = plan_linear(p, false);
@@ -1299,16 +1306,20 @@ rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void*
   const size_t tb = (size_t)extent_elems(p) * es;
   const size_t N = (size_t)(p->B * p->H);
   const size_t gb = N * (size_t)p->T * (size_t)p->D * 4;
+  const size_t pb = a_log ? (size_t)p->H * (size_t)p->D * 4 : 0;
   REL_TRY(check_buffers(p, {{p1, tb, true, false, "p1"},
                             {p2, tb, true, false, "p2"},
                             {v, tb, true, false, "v"},
-                            {g, gb, false, false, "g"},
+                            {g, gb, false, false, a_log ? "r" : "g"},
+                            {a_log, pb, false, false, "a_log"},
+                            {dt_bias, pb, false, false, "dt_bias"},
                             {out, tb, true, true, "out"},
                             {state_out, N * (size_t)(p->D * p->D) * 4, false, true, "state_out"},
                             {workspace, L.total, false, true, "workspace"}}));
   if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected by RELATION_TEST_FAIL_LAUNCH");
   rel::LinearArgs a{};
   a.p1 = p1; a.p2 = p2; a.v = v; a.g = g; a.out = out; a.state_out = state_out;
+  a.a_log = a_log; a.dt_bias = dt_bias;
   a.sb = p->stride_b; a.sh = p->stride_h; a.st = p->stride_t;
   a.B = (int)p->B; a.H = (int)p->H; a.T = (int)p->T; a.D = (int)p->D;
   a.scale = eff_scale(p);
@@ -1322,29 +1333,56 @@ rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void*
   return REL_OK;
 }
 
-size_t relation_linear_bwd_workspace_bytes(const rel_problem* p) {
-  bool empty = false;
-  if (check_linear(p, &empty) != REL_OK || empty) return 0;
-  return plan_linear(p, linear_split(p)).total_bwd;
+rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
+                               const float* g, void* out, float* state_out, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+  return linear_fwd_impl(p, p1, p2, v, g, nullptr, nullptr, out, state_out, workspace, workspace_bytes, stream);
 }
 
-rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
-                               const float* g, const void* dout, void* dp1, void* dp2, void* dv, float* dg,
-                               void* workspace, size_t workspace_bytes, void* stream) {
+rel_status relation_linear_gated_fwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
+                                     const float* r, const float* a_log, const float* dt_bias, void* out,
+                                     float* state_out, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!a_log || !dt_bias) return fail(REL_ERR_INVALID_ARG, "a_log and dt_bias are required");
+  return linear_fwd_impl(p, p1, p2, v, r, a_log, dt_bias, out, state_out, workspace, workspace_bytes, stream);
+}
+
+static size_t linear_bwd_ws(const rel_problem* p, bool gated) {
   bool empty = false;
+  if (check_linear(p, &empty) != REL_OK || empty) return 0;
+  const LinearPlan L = plan_linear(p, linear_split(p));
+  return gated ? L.total_gated : L.total_bwd;
+}
+
+size_t relation_linear_bwd_workspace_bytes(const rel_problem* p) { return linear_bwd_ws(p, false); }
+size_t relation_linear_gated_bwd_workspace_bytes(const rel_problem* p) { return linear_bwd_ws(p, true); }
+
+// g: the log-retention, or with a_log set the gate's pre-activation r; dg is
+// then dr, and da_log, ddt_bias receive the parameters' gradients.
+static rel_status linear_bwd_impl(const rel_problem* p, const void* p1, const void* p2, const void* v, const float* g,
+                                  const float* a_log, const float* dt_bias, const void* dout, void* dp1, void* dp2,
+                                  void* dv, float* dg, float* da_log, float* ddt_bias, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  bool empty = false;
+  const bool gated = a_log != nullptr;
   REL_TRY(check_linear(p, &empty));
   if (empty) return REL_OK;
   const size_t es = elem_size(p->dtype);
   REL_TRY(check_aligned(p1, es, "p1", true));
   REL_TRY(check_aligned(p2, es, "p2", true));
   REL_TRY(check_aligned(v, es, "v", true));
-  REL_TRY(check_aligned(g, 4, "g", true));
+  REL_TRY(check_aligned(g, 4, gated ? "r" : "g", true));
   REL_TRY(check_aligned(dout, es, "dout", true));
   REL_TRY(check_aligned(dp1, es, "dp1", true));
   REL_TRY(check_aligned(dp2, es, "dp2", true));
   REL_TRY(check_aligned(dv, es, "dv", true));
-  REL_TRY(check_aligned(dg, 4, "dg", true));
-  const size_t need = relation_linear_bwd_workspace_bytes(p);
+  REL_TRY(check_aligned(dg, 4, gated ? "dr" : "dg", true));
+  if (gated) {
+    REL_TRY(check_aligned(a_log, 4, "a_log", true));
+    REL_TRY(check_aligned(dt_bias, 4, "dt_bias", true));
+    REL_TRY(check_aligned(da_log, 4, "da_log", true));
+    REL_TRY(check_aligned(ddt_bias, 4, "ddt_bias", true));
+  }
+  const size_t need = linear_bwd_ws(p, gated);
   if (!workspace || workspace_bytes < need)
     return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
                 workspace ? workspace_bytes : (size_t)0);
@@ -1352,15 +1390,20 @@ rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void*
   const size_t tb = (size_t)extent_elems(p) * es;
   const size_t N = (size_t)(p->B * p->H);
   const size_t gb = N * (size_t)p->T * (size_t)p->D * 4;
+  const size_t pb = gated ? (size_t)p->H * (size_t)p->D * 4 : 0;
   REL_TRY(check_buffers(p, {{p1, tb, true, false, "p1"},
                             {p2, tb, true, false, "p2"},
                             {v, tb, true, false, "v"},
-                            {g, gb, false, false, "g"},
+                            {g, gb, false, false, gated ? "r" : "g"},
+                            {a_log, pb, false, false, "a_log"},
+                            {dt_bias, pb, false, false, "dt_bias"},
                             {dout, tb, true, false, "dout"},
                             {dp1, tb, true, true, "dp1"},
                             {dp2, tb, true, true, "dp2"},
                             {dv, tb, true, true, "dv"},
-                            {dg, gb, false, true, "dg"},
+                            {dg, gb, false, true, gated ? "dr" : "dg"},
+                            {da_log, pb, false, true, "da_log"},
+                            {ddt_bias, pb, false, true, "ddt_bias"},
                             {workspace, need, false, true, "workspace"}}));
   if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected by RELATION_TEST_FAIL_LAUNCH");
   const LinearPlan L = plan_linear(p, linear_split(p));
@@ -1375,9 +1418,30 @@ rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void*
   a.nseg = linear_segments(p);
   a.vec16 = linear_vec16(p, {p1, p2, v, dout, dp1, dp2, dv}, g);
   set_linear_workspace(a, L, (char*)workspace, true);
+  if (gated) {
+    a.a_log = a_log; a.dt_bias = dt_bias;
+    a.gpart = (float*)((char*)workspace + L.gpart);
+    a.da_log = da_log; a.ddt_bias = ddt_bias;
+  }
   const hipError_t e = rel::launch_linear_bwd(a, p->dtype, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "Linear Relation backward launch");
   return REL_OK;
+}
+
+rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
+                               const float* g, const void* dout, void* dp1, void* dp2, void* dv, float* dg,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  return linear_bwd_impl(p, p1, p2, v, g, nullptr, nullptr, dout, dp1, dp2, dv, dg, nullptr, nullptr, workspace,
+                         workspace_bytes, stream);
+}
+
+rel_status relation_linear_gated_bwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
+                                     const float* r, const float* a_log, const float* dt_bias, const void* dout,
+                                     void* dp1, void* dp2, void* dv, float* dr, float* da_log, float* ddt_bias,
+                                     void* workspace, size_t workspace_bytes, void* stream) {
+  if (!a_log || !dt_bias) return fail(REL_ERR_INVALID_ARG, "a_log and dt_bias are required");
+  return linear_bwd_impl(p, p1, p2, v, r, a_log, dt_bias, dout, dp1, dp2, dv, dr, da_log, ddt_bias, workspace,
+                         workspace_bytes, stream);
 }
 
 }  // extern "C"

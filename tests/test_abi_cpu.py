@@ -344,3 +344,27 @@ def test_linear_widths_and_workspace(lib):
         st = lib.relation_linear_bwd(ctypes.byref(p), a[0], a[1], a[2], a[3], a[4], a[5], a[6], a[7], a[8],
                                      a[9], 1 << 20, None)
         assert st == R.REL_ERR_UNSUPPORTED
+
+
+def test_linear_gated_validation(lib):
+    """The gated Linear Relation entry points need a_log and dt_bias, reject an
+    output that overlaps r, and take a larger backward workspace than the
+    ungated backward (the gate's segment sums)."""
+    a = ptrs(14)
+    p = prob(B=2, H=3, T=300, D=64)
+    ws = lib.relation_linear_gated_bwd_workspace_bytes(ctypes.byref(p))
+    assert ws > lib.relation_linear_bwd_workspace_bytes(ctypes.byref(p))
+    fws = lib.relation_linear_fwd_workspace_bytes(ctypes.byref(p))
+    fwd = lambda alog, dtb: lib.relation_linear_gated_fwd(ctypes.byref(p), a[0], a[1], a[2], a[3], alog, dtb, a[6],
+                                                         None, a[13], fws, None)
+    assert fwd(a[4], a[5]) == R.REL_ERR_HIP
+    assert fwd(None, a[5]) == R.REL_ERR_INVALID_ARG
+    assert fwd(a[4], None) == R.REL_ERR_INVALID_ARG
+    bwd = lambda dr: lib.relation_linear_gated_bwd(ctypes.byref(p), a[0], a[1], a[2], a[3], a[4], a[5], a[6], a[7],
+                                                   a[8], a[9], dr, a[11], a[12], a[13], ws, None)
+    assert bwd(a[10]) == R.REL_ERR_HIP
+    assert bwd(a[3]) == R.REL_ERR_INVALID_ARG  # dr over r
+    assert b"overlaps" in lib.relation_last_error()
+    st = lib.relation_linear_gated_bwd(ctypes.byref(p), a[0], a[1], a[2], a[3], None, a[5], a[6], a[7], a[8], a[9],
+                                       a[10], a[11], a[12], a[13], ws, None)
+    assert st == R.REL_ERR_INVALID_ARG

@@ -211,3 +211,81 @@ def test_linear_padded_head_width(width, padded, T, dtype):
             got = _np(r[n])[0, h]
             assert_close(f"{n}[0,{h}]", got[:, :width], ref_b[n], dtype)
             assert not np.any(got[:, width:]), f"{n}: padding channels non-zero"
+
+
+def _gate_params(H, D, seed, a_mean=0.0):
+    rng = np.random.default_rng(seed + 7919)
+    a_log = (a_mean + 0.5 * rng.standard_normal((H, D))).astype(np.float32)
+    dt_bias = rng.standard_normal((H, D)).astype(np.float32)
+    return a_log, dt_bias
+
+
+def _assert_param_grad(name, x, ref, terms, dtype):
+    """A per-(head, channel) sum over batch entries and tokens: each entry's
+    error against the bar times the larger of |ref| and the l2 norm of its
+    terms (bf16), or max-abs against the larger of 1e-4 and 1e-5 of the sum of
+    |terms| (fp32)."""
+    err = np.abs(np.asarray(x, np.float64) - ref)
+    t = np.abs(terms)
+    if dtype == "f32":
+        lim = np.maximum(1e-4, 1e-5 * t.sum(axis=(0, 2)))
+    else:
+        lim = 2e-2 * np.maximum(np.abs(ref), np.sqrt(np.sum(t * t, axis=(0, 2))))
+    zero = lim == 0.0  # no terms (T = 1 has no history): the sum must be zero
+    assert np.all(err[zero] == 0.0), f"{name}: non-zero where every term is zero"
+    worst = float(np.max(err[~zero] / lim[~zero])) if np.any(~zero) else 0.0
+    log(f"  {name}: worst error / allowance {worst:.3e}")
+    assert worst <= 1.0, f"{name}: error {worst:.3e} of the allowance"
+
+
+@pytest.mark.parametrize("B,H,T,D,dtype,a_mean", [
+    (2, 2, 300, 64, "bf16", 0.0), (1, 2, 190, 32, "f32", 0.0), (1, 2, 200, 128, "bf16", 0.0),
+    (2, 1, 129, 128, "f32", -1.0), (1, 2, 1, 64, "bf16", 0.0), (1, 1, 600, 64, "f32", -4.0),
+])
+def test_linear_gated(B, H, T, D, dtype, a_mean):
+    """The retention gate of eq. 9 formed in the kernels: y and the state, then
+    dp1, dp2, dv, dr and the per-channel dA_log, d dt_bias, against the oracle's
+    gate composed with its recurrence (the gate's adjoint fed the recurrence's
+    dg)."""
+    x = _prep(B, H, T, D, dtype, seed=1900 + T + D, with_dout=True)
+    rng = np.random.default_rng(1950 + T)
+    r = (2.0 * rng.standard_normal((B, H, T, D))).astype(np.float32)
+    a_log, dt_bias = _gate_params(H, D, 1960 + T, a_mean)
+    rt, at, bt = (torch.from_numpy(z).cuda() for z in (r, a_log, dt_bias))
+    log(f"[linear gated] B={B} H={H} T={T} D={D} {dtype} A_log mean {a_mean}")
+    f = R.relation_linear_gated_fwd(x["p1"], x["p2"], x["v"], rt, at, bt, want_state=True)
+    o = R.relation_linear_gated_bwd(x["p1"], x["p2"], x["v"], rt, at, bt, x["dy"])
+    torch.cuda.synchronize()
+    da_terms = np.zeros((B, H, T, D))
+    dt_terms = np.zeros((B, H, T, D))
+    da_ref = np.zeros((H, D))
+    dt_ref = np.zeros((H, D))
+    for b in range(B):
+        for h in range(H):
+            g = LO.kda_gate(r[b, h], a_log[h], dt_bias[h])
+            ref_f = LO.forward(x["p1r"][b, h], x["p2r"][b, h], x["vr"][b, h], g)
+            assert_close(f"y[{b},{h}]", _np(f["o"])[b, h], ref_f["Y"], dtype)
+            assert_close(f"state[{b},{h}]", _np(f["state"])[b, h], ref_f["C"], dtype)
+            ref_b = LO.backward(x["p1r"][b, h], x["p2r"][b, h], x["vr"][b, h], g, x["dyr"][b, h])
+            gb = LO.kda_gate_backward(r[b, h], a_log[h], dt_bias[h], ref_b["dg"])
+            for n in ("dp1", "dp2", "dv"):
+                assert_close(f"{n}[{b},{h}]", _np(o[n])[b, h], ref_b[n], dtype)
+            assert_close(f"dr[{b},{h}]", _np(o["dr"])[b, h], gb["dr"], dtype)
+            da_terms[b, h] = ref_b["dg"] * g
+            dt_terms[b, h] = gb["dr"]
+            da_ref[h] += gb["da_log"]
+            dt_ref[h] += gb["ddt_bias"]
+    _assert_param_grad("da_log", _np(o["da_log"]), da_ref, da_terms, dtype)
+    _assert_param_grad("ddt_bias", _np(o["ddt_bias"]), dt_ref, dt_terms, dtype)
+
+
+def test_linear_gated_repeatable():
+    x = _prep(2, 2, 700, 64, "bf16", seed=1990)
+    rng = np.random.default_rng(1991)
+    r = torch.from_numpy(rng.standard_normal((2, 2, 700, 64)).astype(np.float32)).cuda()
+    a_log, dt_bias = (torch.from_numpy(z).cuda() for z in _gate_params(2, 64, 1992))
+    a = R.relation_linear_gated_bwd(x["p1"], x["p2"], x["v"], r, a_log, dt_bias, x["dy"])
+    b = R.relation_linear_gated_bwd(x["p1"], x["p2"], x["v"], r, a_log, dt_bias, x["dy"])
+    torch.cuda.synchronize()
+    for n in ("dp1", "dp2", "dv", "dr", "da_log", "ddt_bias"):
+        assert torch.equal(a[n], b[n]), n
