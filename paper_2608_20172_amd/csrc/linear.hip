@@ -63,12 +63,17 @@ __device__ __forceinline__ HeadRef head_ref(const LinearArgs& a, int nv) {
   return r;
 }
 
-// The retention gate of eq. 9: g = -exp(A_log) softplus(r + dt_bias), with
-// softplus(x) = max(x, 0) + log(1 + e^-|x|) (no overflow for any x).
-__device__ __forceinline__ float kda_gate(float r, float ea, float dtb) {
-  const float x = r + dtb;
-  return -ea * (fmaxf(x, 0.0f) + log1pf(expf(-fabsf(x))));
+// softplus(x) = max(x, 0) + ln(1 + e^-|x|): no overflow for any x; the
+// logarithm's argument lies in (1, 2], where the hardware log2 is accurate
+// (for x below about -17 the e^-|x| term is lost against 1 and softplus
+// comes out 0: g then differs from the exact value by less than 1e-7 e^A_log).
+__device__ __forceinline__ float softplus_f(float x) {
+  return fmaxf(x, 0.0f) + kLn2 * __builtin_amdgcn_logf(1.0f + fast_exp2(-fabsf(x) * kLog2e));
 }
+
+// The retention gate of eq. 9: g = -exp(A_log) softplus(r + dt_bias), with
+// ea = exp(A_log) of the channel.
+__device__ __forceinline__ float kda_gate(float r, float ea, float dtb) { return -ea * softplus_f(r + dtb); }
 
 // K consecutive fp32 values from a 16-byte aligned address.
 template <int K>
@@ -167,6 +172,15 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
     static_assert(LPR >= 2 && LPR <= 64 && EPL % 4 == 0, "a row is whole 16-byte chunks over a lane group");
     constexpr int STEPS = (kL + NW * RPI - 1) / (NW * RPI);
     const int cg = lane % LPR, c0 = cg * EPL;
+    float ea[EPL], dtb[EPL];  // the gate's parameters of this lane's channels
+    if (a.a_log) {
+      const int64_t pc = (int64_t)(hr.n % a.H) * GW + hr.pa + c0;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) {
+        ea[e] = fast_exp2(a.a_log[pc + e] * kLog2e);
+        dtb[e] = a.dt_bias[pc + e];
+      }
+    }
 #pragma unroll
     for (int st = 0; st < STEPS; ++st) {
       const int r = st * NW * RPI + w * RPI + lane / LPR;
@@ -184,9 +198,8 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
         if constexpr (WITH_DY) Vec16<TI>::load(DY + row * a.st + c0, dx);
         load_f32<EPL>(G + row * GW + c0, gx);
         if (a.a_log) {
-          const int64_t pc = (int64_t)(hr.n % a.H) * GW + hr.pa + c0;
 #pragma unroll
-          for (int e = 0; e < EPL; ++e) gx[e] = kda_gate(gx[e], expf(a.a_log[pc + e]), a.dt_bias[pc + e]);
+          for (int e = 0; e < EPL; ++e) gx[e] = kda_gate(gx[e], ea[e], dtb[e]);
         }
         const bool ok = r < p.len;
         float s11 = 0.0f, s22 = 0.0f, s12 = 0.0f;
@@ -243,7 +256,7 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
         gx[kb][u] = G[row * GW + d];
         if (a.a_log) {
           const int64_t pc = (int64_t)(hr.n % a.H) * GW + hr.pa + d;
-          gx[kb][u] = kda_gate(gx[kb][u], expf(a.a_log[pc]), a.dt_bias[pc]);
+          gx[kb][u] = kda_gate(gx[kb][u], fast_exp2(a.a_log[pc] * kLog2e), a.dt_bias[pc]);
         }
         dx[kb][u] = WITH_DY ? Elem<TI>::load(DY + row * a.st + d) : 0.0f;
       }
@@ -1254,7 +1267,7 @@ __global__ __launch_bounds__(256) void linear_gate_bwd_kernel(LinearArgs a) {
   const int n = blockIdx.y, seg = blockIdx.x;
   const int c = threadIdx.x % D, rg = threadIdx.x / D;
   const int64_t pc = (int64_t)(n % a.H) * D + c;
-  const float ea = expf(a.a_log[pc]), dtb = a.dt_bias[pc];
+  const float ea = fast_exp2(a.a_log[pc] * kLog2e), dtb = a.dt_bias[pc];
   const int t0 = seg * kGateSeg, t1 = min(a.T, t0 + kGateSeg);
   const float* R = a.g + (int64_t)n * a.T * D;
   float* DG = a.dg + (int64_t)n * a.T * D;
@@ -1262,9 +1275,8 @@ __global__ __launch_bounds__(256) void linear_gate_bwd_kernel(LinearArgs a) {
   for (int t = t0 + rg; t < t1; t += RG) {
     const int64_t i = (int64_t)t * D + c;
     const float x = R[i] + dtb, dg = DG[i];
-    const float sp = fmaxf(x, 0.0f) + log1pf(expf(-fabsf(x)));
-    const float dr = dg * (-ea / (1.0f + expf(-x)));
-    sa = __builtin_fmaf(dg, -ea * sp, sa);
+    const float dr = dg * (-ea * fast_rcp(1.0f + fast_exp2(-x * kLog2e)));  // softplus' = sigmoid
+    sa = __builtin_fmaf(dg, -ea * softplus_f(x), sa);
     sd += dr;
     DG[i] = dr;
   }
