@@ -491,19 +491,65 @@ __device__ __forceinline__ floatx4 ld4(const float (*X)[D], int r, int c) {
   return *reinterpret_cast<const floatx4*>(&X[r][(c ^ (r & (D / 4 - 1))) << 2]);
 }
 
+// Largest decay (log2 units) over a 16-row block of the chunk for which the
+// diagonal blocks are factored at a reference row like the blocks below: the
+// factors then lie in [2^-kFactLim, 2^kFactLim], far inside the fp32 range.
+constexpr float kFactLim = 64.0f;
+
+// True when on every channel the decay across each 16-row block, from the
+// row before the block (the first row for the first block) to its last row,
+// is at most 2^kFactLim (false for any NaN). Every wave checks all of them
+// itself (no barrier, no LDS of its own), so the result is the same in every
+// wave of the workgroup.
+template <int D>
+__device__ __forceinline__ bool diag_factorable(const float (*bb)[D]) {
+  bool over = false;
+  for (int i = threadIdx.x & 63; i < 4 * D; i += 64) {
+    const int blk = i / D, c = i % D;
+    const int r0 = blk ? 16 * blk - 1 : 0, r1 = 16 * blk + 15;
+    over |= !((bb[r0][swz<D>(r0, c)] - bb[r1][swz<D>(r1, c)]) * kLog2e <= kFactLim);
+  }
+  return !wave_any(over);
+}
+
 // Intra-chunk scores A[t][j] = sum_a qt_{t,a} kt_{j,a} e^{b_{t,a} - b_{j,a}}
 // (j < t) into the swizzled A, in 16 x 16 sub-blocks. qt, kt and b are
 // swizzled. Below the diagonal, block (tb, jb) factors the decay at the last
 // row rf of key block jb: e^{b_t - b_j} = e^{b_t - b_rf} e^{b_rf - b_j}, both
 // factors <= 1 (b does not increase down the chunk), so the block is a plain
 // product of qt e^{b - b_rf} and kt e^{b_rf - b} on the matrix cores
-// (16x16x4 fp32 steps, the operands formed in registers). The four diagonal
-// blocks are summed term by term on the vector units. Waves 0-3 of the
-// workgroup: diagonal block w; waves 4-7: blocks w - 4 and w (of the six below
-// the diagonal). With TRANS the scores go to A as A^T (A[j][t]).
+// (16x16x4 fp32 steps, the operands formed in registers). A diagonal block is
+// the same product factored at its first row when FACT (diag_factorable: the
+// key factor e^{b_rf - b_j} >= 1 stays below 2^kFactLim), with the pairs
+// j >= t set to zero; otherwise it is summed term by term on the vector units.
+// Waves 0-3 of the workgroup: diagonal block w; waves 4-7: blocks w - 4 and w
+// (of the six below the diagonal). With TRANS the scores go to A as A^T (A[j][t]).
+template <int D>
+__device__ __forceinline__ floatx4 scaled_block(const float (*qt)[D], const float (*kt)[D], const float (*bb)[D],
+                                                int tb, int jb, int rf) {
+  constexpr int CH = D / 4;
+  const int lane = threadIdx.x & 63, i = lane & 15, g = lane >> 4;
+  const int tr = 16 * tb + i, jr = 16 * jb + i;
+  floatx4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+  // lane group g takes the channel chunks CH/4 g .. CH/4 g + CH/4 - 1
+#pragma unroll 2
+  for (int c0 = 0; c0 < CH / 4; ++c0) {
+    const int c = (CH / 4) * g + c0;
+    const floatx4 q4 = ld4<D>(qt, tr, c), bt4 = ld4<D>(bb, tr, c), br4 = ld4<D>(bb, rf, c);
+    const floatx4 k4 = ld4<D>(kt, jr, c), bj4 = ld4<D>(bb, jr, c);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float qa = q4[u] * fast_exp2((bt4[u] - br4[u]) * kLog2e);
+      const float kb = k4[u] * fast_exp2((br4[u] - bj4[u]) * kLog2e);
+      acc = mfma16f(qa, kb, acc);
+    }
+  }
+  return acc;
+}
+
 template <int D, bool TRANS = false>
 __device__ __forceinline__ void chunk_scores(const float (*qt)[D], const float (*kt)[D], const float (*bb)[D],
-                                             float (*A)[kL]) {
+                                             float (*A)[kL], bool fact) {
   constexpr int SB = 16, NSB = kL / SB, CH = D / 4;
   static_assert(NSB == 4, "four diagonal blocks, six below");
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
@@ -511,7 +557,16 @@ __device__ __forceinline__ void chunk_scores(const float (*qt)[D], const float (
     if (TRANS) A[j][swz<kL>(j, t)] = x;
     else A[t][swz<kL>(t, j)] = x;
   };
-  if (w < NSB) {
+  if (w < NSB && fact) {
+    const int i = lane & 15, g = lane >> 4;
+    const floatx4 acc = scaled_block<D>(qt, kt, bb, w, w, SB * w);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) put(SB * w + 4 * g + v, SB * w + i, i < 4 * g + v ? acc[v] : 0.0f);
+    for (int jb = w + 1; jb < NSB; ++jb) {  // the blocks above the diagonal in the row band are zero
+#pragma unroll
+      for (int v = 0; v < 4; ++v) put(SB * w + 4 * g + v, SB * jb + i, 0.0f);
+    }
+  } else if (w < NSB) {
     // the block's 120 pairs j < t, two per lane (slot s: pair lane + 64 s in
     // row-major order); the rest of the block is zero
     const int base = SB * w, t = base + (lane >> 2), jq = lane & 3;
@@ -559,21 +614,7 @@ __device__ __forceinline__ void chunk_scores(const float (*qt)[D], const float (
       // blocks below the diagonal, bi = 0..5: (1,0) (2,0) (3,0) (2,1) (3,1) (3,2)
       const int jb = bi < 3 ? 0 : bi < 5 ? 1 : 2;
       const int tb = jb + 1 + (bi < 3 ? bi : bi < 5 ? bi - 3 : 0);
-      const int rf = SB * jb + SB - 1, tr = SB * tb + i, jr = SB * jb + i;
-      floatx4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-      // lane group g takes the channel chunks CH/4 g .. CH/4 g + CH/4 - 1
-#pragma unroll 2
-      for (int c0 = 0; c0 < CH / 4; ++c0) {
-        const int c = (CH / 4) * g + c0;
-        const floatx4 q4 = ld4<D>(qt, tr, c), bt4 = ld4<D>(bb, tr, c), br4 = ld4<D>(bb, rf, c);
-        const floatx4 k4 = ld4<D>(kt, jr, c), bj4 = ld4<D>(bb, jr, c);
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const float qa = q4[u] * fast_exp2((bt4[u] - br4[u]) * kLog2e);
-          const float kb = k4[u] * fast_exp2((br4[u] - bj4[u]) * kLog2e);
-          acc = mfma16f(qa, kb, acc);
-        }
-      }
+      const floatx4 acc = scaled_block<D>(qt, kt, bb, tb, jb, SB * jb + SB - 1);
       // register v of lane (i, g): row 4 g + v, column i of the block
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
@@ -606,7 +647,7 @@ __global__ __launch_bounds__(kLT2) void linear_out_kernel(LinearArgs a) {
     for (int k = 0; k < NC0; ++k) c0r[k] = C0[tid + k * kLT2];
   }
   load_chunk<TI, D, kLT2, false, false, true>(a, p, qt, kt, vv, bb, nullptr);
-  chunk_scores<D>(qt, kt, bb, A);
+  chunk_scores<D>(qt, kt, bb, A, diag_factorable<D>(bb));
   __syncthreads();
   // Qe = qt e^{b} (the inter read's query), over kt; all three swizzled alike
   for (int i = tid; i < kL * D; i += kLT2) {
@@ -724,7 +765,9 @@ __device__ __forceinline__ floatx4 tile_product(const float (*X)[W], int r0, int
 //   dv_intra = A^T dY; dq_intra, dk_intra below the diagonal as products with
 //   the decay factored at a block boundary (q side: the row before the
 //   query block; k side: the last row of the key block), both factors <= 1;
-//   the diagonal blocks term by term on the vector units.
+//   the diagonal blocks in the same products when the chunk's decay allows
+//   (diag_factorable: the factors past the boundary stay below 2^kFactLim),
+//   else term by term on the vector units.
 // The three inter-chunk products are dense (kL x D by D x D), 32 x 32 blocks.
 // SPLIT: a sub-problem of the D = 128 backward; it ends at dqt, dkt, dv and
 // dg, its partials of the head's gradients, stored in fp32.
@@ -768,9 +811,13 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
   const int r = tid / kTPRG, q0 = (tid % kTPRG) * QW;
   const int qs = swz<D>(r, q0);  // this thread's channels in a swizzled row r (contiguous)
   const int wrow = w * kRowsPerWave;
+  // FACT: the diagonal blocks are factored at a reference row and join the
+  // matrix-core products (the score blocks, and the dq and dk tiles below take
+  // one more 16-row block); otherwise they are summed term by term
+  const bool fact = diag_factorable<D>(bb);
   // ---- scores and dA: waves 0-7 the scores (to M0 as A^T), waves 8-15 dA
   if (w < 8) {
-    chunk_scores<D, true>(qt, kt, bb, M0);
+    chunk_scores<D, true>(qt, kt, bb, M0, fact);
   } else {
     // the ten blocks (tb, jb) with jb <= tb; wave 8 + i takes blocks i and i + 8
     const int i = lane & 15, g = lane >> 4;
@@ -791,12 +838,17 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
     }
   }
   __syncthreads();
-  // ---- intra products below the diagonal: 16 x 16 tiles, wave w takes tiles w, w + 16, w + 32
+  // ---- intra products as 16 x 16 tiles, wave w takes tiles w, w + 16, w + 32
   //   type 0 (4 NE tiles): dv_intra[j][e] = sum_{t >= 16 jb} A^T[j][t] dY[t][e]
-  //   type 1 (3 NE): dq_intra[t][d] = e^{b_t - b_rf} sum_{j < 16 tb} dA[t][j] kt[j][d] e^{b_rf - b_j}, rf = 16 tb - 1
-  //   type 2 (3 NE): dk_intra[j][d] = e^{b_rf - b_j} sum_{t > rf} dA^T[j][t] qt[t][d] e^{b_t - b_rf}, rf = 16 jb + 15
-  constexpr int NT0 = NSB * NE, NT1 = (NSB - 1) * NE, NTT = NT0 + 2 * NT1;
+  //   type 1 (3 NE, 4 NE with FACT): dq_intra[t][d] = e^{b_t - b_rf} sum_j dA[t][j] kt[j][d] e^{b_rf - b_j},
+  //     rf = 16 tb - 1 (0 for tb = 0), over j < 16 tb (below the diagonal) or j < 16 tb + 16 (FACT)
+  //   type 2 (3 NE, 4 NE with FACT): dk_intra[j][d] = e^{b_rf - b_j} sum_t dA^T[j][t] qt[t][d] e^{b_t - b_rf},
+  //     rf = 16 jb + 15, over t > rf or t >= 16 jb (FACT)
+  // dA is zero for j >= t, so the diagonal blocks' upper triangles add nothing.
+  constexpr int NT0 = NSB * NE, NTT = NT0 + 2 * NSB * NE;
   constexpr int MAXT = (NTT + 15) / 16;
+  const int nt1 = fact ? NSB * NE : (NSB - 1) * NE, tb1 = fact ? 0 : 1;
+  const int ntt = NT0 + 2 * nt1;
   floatx4 res[MAXT];
 #pragma unroll
   for (int m = 0; m < MAXT; ++m) {
@@ -806,11 +858,11 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
       const int jb = tau / NE, eb = tau % NE;
       res[m] = tile_product<kL>(M0, SB * jb, SB * eb, SB * jb, kL - SB * jb,
                                 [&](int k, int e) { return dy[k][swz<D>(k, e)]; });
-    } else if (tau < NT0 + NT1) {
-      const int tb = 1 + (tau - NT0) / NE, db = (tau - NT0) % NE;
-      const int rf = SB * tb - 1, col = SB * db + (lane & 15);
+    } else if (tau < NT0 + nt1) {
+      const int tb = tb1 + (tau - NT0) / NE, db = (tau - NT0) % NE;
+      const int rf = tb ? SB * tb - 1 : 0, col = SB * db + (lane & 15);
       const float brf = bb[rf][swz<D>(rf, col)];
-      floatx4 acc = tile_product<kL>(M1, SB * tb, SB * db, 0, SB * tb, [&](int k, int d) {
+      floatx4 acc = tile_product<kL>(M1, SB * tb, SB * db, 0, SB * tb + (fact ? SB : 0), [&](int k, int d) {
         const int c = swz<D>(k, d);
         return kt[k][c] * fast_exp2((brf - bb[k][c]) * kLog2e);
       });
@@ -820,11 +872,12 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
         acc[v] *= fast_exp2((bb[t][swz<D>(t, col)] - brf) * kLog2e);
       }
       res[m] = acc;
-    } else if (tau < NTT) {
-      const int jb = (tau - NT0 - NT1) / NE, db = (tau - NT0 - NT1) % NE;
+    } else if (tau < ntt) {
+      const int jb = (tau - NT0 - nt1) / NE, db = (tau - NT0 - nt1) % NE;
       const int rf = SB * jb + SB - 1, col = SB * db + (lane & 15);
       const float brf = bb[rf][swz<D>(rf, col)];
-      floatx4 acc = tile_product<kL>(M2, SB * jb, SB * db, rf + 1, kL - rf - 1, [&](int k, int d) {
+      const int k0 = fact ? SB * jb : rf + 1;
+      floatx4 acc = tile_product<kL>(M2, SB * jb, SB * db, k0, kL - k0, [&](int k, int d) {
         const int c = swz<D>(k, d);
         return qt[k][c] * fast_exp2((bb[k][c] - brf) * kLog2e);
       });
@@ -836,7 +889,7 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
       res[m] = acc;
     }
   }
-  // ---- diagonal blocks on the vector units, in the thread's row and channels
+  // ---- diagonal blocks on the vector units (unless FACT), in the thread's row and channels
   float dq[QW], dk[QW], dv[QW], db[QW];
   float qself[QW], kself[QW], bself[QW];
 #pragma unroll
@@ -847,7 +900,7 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
     dq[i] = dk[i] = 0.0f;
     dv[i] = SPLIT && ia ? 0.0f : dy[r][qs + i];  // Y = I~ + E (once over the halves A)
   }
-  {
+  if (!fact) {
     const int blo = (wrow / SB) * SB;  // the wave's rows share one 16-row block
     // dq: j in [blo, r)
     for (int j = blo; j < wrow + kRowsPerWave - 1; ++j) {
@@ -878,10 +931,10 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
 #pragma unroll
     for (int m = 0; m < MAXT; ++m) {
       const int tau = w + 16 * m;
-      if (tau < NTT) {
-        const int ty = tau < NT0 ? 0 : tau < NT0 + NT1 ? 1 : 2;
-        const int u = tau - (ty == 0 ? 0 : ty == 1 ? NT0 : NT0 + NT1);
-        const int rb = ty == 1 ? SB * (1 + u / NE) : SB * (u / NE), cb = SB * (u % NE);
+      if (tau < ntt) {
+        const int ty = tau < NT0 ? 0 : tau < NT0 + nt1 ? 1 : 2;
+        const int u = tau - (ty == 0 ? 0 : ty == 1 ? NT0 : NT0 + nt1);
+        const int rb = ty == 1 ? SB * (tb1 + u / NE) : SB * (u / NE), cb = SB * (u % NE);
         float(*R)[D] = ty == 0 ? R0 : ty == 1 ? R1 : R2;
 #pragma unroll
         for (int v = 0; v < 4; ++v) R[rb + 4 * (lane >> 4) + v][cb + (lane & 15)] = res[m][v];
@@ -891,8 +944,8 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
 #pragma unroll
     for (int i = 0; i < QW; ++i) {
       dv[i] += R0[r][q0 + i];
-      if (r >= SB) dq[i] += R1[r][q0 + i];
-      if (r < kL - SB) dk[i] += R2[r][q0 + i];
+      if (fact || r >= SB) dq[i] += R1[r][q0 + i];
+      if (fact || r < kL - SB) dk[i] += R2[r][q0 + i];
       db[i] = qself[i] * dq[i] - kself[i] * dk[i];
     }
   }

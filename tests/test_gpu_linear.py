@@ -289,3 +289,20 @@ def test_linear_gated_repeatable():
     torch.cuda.synchronize()
     for n in ("dp1", "dp2", "dv", "dr", "da_log", "ddt_bias"):
         assert torch.equal(a[n], b[n]), n
+
+
+@pytest.mark.parametrize("D,dtype", [(64, "f32"), (32, "bf16"), (128, "f32")])
+def test_linear_mixed_decay_chunks(D, dtype):
+    """Chunks whose decay inside a 16-token block is mild take the factored
+    diagonal blocks on the matrix cores, chunks with steep decay (here up to
+    e^-20 per token) the term-by-term path; one sequence with both kinds,
+    forward and backward against the oracle."""
+    T = 64 * 5 + 17
+    x = _prep(1, 2, T, D, dtype, seed=2100 + D)
+    rng = np.random.default_rng(2101)
+    gmax = np.where((np.arange(T) // 64) % 2 == 1, 20.0, 0.05)[None, None, :, None]
+    g = (-rng.uniform(0.0, 1.0, (1, 2, T, D)) * gmax).astype(np.float32)
+    x["g"] = torch.from_numpy(g).cuda()
+    x["gr"] = g.astype(np.float64)
+    check_linear_fwd(x, dtype)
+    check_linear_bwd(x, dtype)
