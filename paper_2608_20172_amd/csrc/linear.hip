@@ -1347,21 +1347,28 @@ __global__ __launch_bounds__(256) void linear_gate_bwd_kernel(LinearArgs a) {
   }
 }
 
-// One thread per (head, channel): the batch entries' segment sums in order.
+// One wave per (head, channel): lane l sums the (batch entry, segment) items
+// l, l + 64, ... in order, then the 64 lane sums meet in a fixed butterfly, so
+// the result does not depend on timing.
 __global__ __launch_bounds__(256) void linear_gate_reduce_kernel(LinearArgs a, int nseg) {
-  const int idx = blockIdx.x * 256 + threadIdx.x;
-  if (idx >= a.H * a.D) return;
+  const int idx = blockIdx.x * 4 + (int)(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (idx >= a.H * a.D) return;  // wave-uniform
   const int h = idx / a.D, c = idx % a.D;
   float sa = 0.0f, sd = 0.0f;
-  for (int b = 0; b < a.B; ++b) {
-    const float* P = a.gpart + ((int64_t)(b * a.H + h) * nseg * 2) * a.D + c;
-    for (int s = 0; s < nseg; ++s) {
-      sa += P[(2 * s) * a.D];
-      sd += P[(2 * s + 1) * a.D];
-    }
+  for (int it = lane; it < a.B * nseg; it += 64) {
+    const int b = it / nseg, sg = it % nseg;
+    const float* P = a.gpart + (((int64_t)(b * a.H + h) * nseg + sg) * 2) * a.D + c;
+    sa += P[0];
+    sd += P[a.D];
   }
-  a.da_log[idx] = sa;
-  a.ddt_bias[idx] = sd;
+  for (int o = 32; o >= 1; o >>= 1) {
+    sa += __shfl_xor(sa, o, 64);
+    sd += __shfl_xor(sd, o, 64);
+  }
+  if (lane == 0) {
+    a.da_log[idx] = sa;
+    a.ddt_bias[idx] = sd;
+  }
 }
 
 hipError_t launch_gate_bwd(const LinearArgs& a, hipStream_t stream) {
@@ -1375,8 +1382,7 @@ hipError_t launch_gate_bwd(const LinearArgs& a, hipStream_t stream) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(linear_gate_reduce_kernel, dim3((unsigned)((a.H * a.D + 255) / 256)), dim3(256), 0, stream, a,
-                     nseg);
+  hipLaunchKernelGGL(linear_gate_reduce_kernel, dim3((unsigned)((a.H * a.D + 3) / 4)), dim3(256), 0, stream, a, nseg);
   return hipGetLastError();
 }
 
