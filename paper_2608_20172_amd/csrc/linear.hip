@@ -1066,10 +1066,47 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
     }
     const float base_g = extra + dgam * fast_exp2(bb[kL - 1][swz<D>(kL - 1, d)] * kLog2e) + later;
     float* dG = SPLIT ? a.part + (6 + ie) * plane + (int64_t)hr.n * a.T * GW + hr.pa : a.dg + (int64_t)p.n * a.T * D;
+    if (!SPLIT && a.a_log) {
+      // the retention gate of eq. 9 (g = -exp(A_log) softplus(r + dt_bias)):
+      // dr = dg (-exp(A_log) sigmoid(r + dt_bias)) goes out in place of dg, and
+      // the chunk's per-channel sums of dg g and dr (its shares of dA_log and
+      // d dt_bias) meet over the segments in LDS, in a fixed order
+      const int64_t pc = (int64_t)(p.n % a.H) * D + d;
+      const float ea = fast_exp2(a.a_log[pc] * kLog2e), dtb = a.dt_bias[pc];
+      const float* Rg = a.g + (int64_t)p.n * a.T * D;
+      float sa = 0.0f, sd = 0.0f;
 #pragma unroll
-    for (int i = 0; i < RS; ++i) {
-      const int j = sg * RS + i;
-      if (j < p.len) dG[(int64_t)(p.t0 + j) * GW + d] = base_g + suf[i];
+      for (int i = 0; i < RS; ++i) {
+        const int j = sg * RS + i;
+        if (j < p.len) {
+          const int64_t at = (int64_t)(p.t0 + j) * D + d;
+          const float dgv = base_g + suf[i], x = Rg[at] + dtb;
+          const float dr = dgv * (-ea * fast_rcp(1.0f + fast_exp2(-x * kLog2e)));
+          sa = __builtin_fmaf(dgv, -ea * softplus_f(x), sa);
+          sd += dr;
+          dG[at] = dr;
+        }
+      }
+      __syncthreads();  // every read of PT and PE done
+      PT[sg * D + d] = sa;
+      PE[sg * D + d] = sd;
+      __syncthreads();
+      if (sg == 0) {
+        float ta = 0.0f, td = 0.0f;
+        for (int u = 0; u < NSG; ++u) {
+          ta += PT[u * D + d];
+          td += PE[u * D + d];
+        }
+        float* P = a.gpart + ((int64_t)p.n * a.nchunks + p.c) * 2 * D;
+        P[d] = ta;
+        P[D + d] = td;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < RS; ++i) {
+        const int j = sg * RS + i;
+        if (j < p.len) dG[(int64_t)(p.t0 + j) * GW + d] = base_g + suf[i];
+      }
     }
   }
   if constexpr (SPLIT) {
@@ -1305,11 +1342,13 @@ hipError_t launch_bwd_split(const LinearArgs& a, hipStream_t stream) {
 }
 
 // ---------------------------------------------------------------------------
-// Backward through the retention gate of eq. 9, after the chunk kernels have
-// left dg in a.dg: per element dr = dg (-exp(A_log) sigmoid(r + dt_bias)),
-// written over dg; per head, token segment and channel the sums of dg g
-// (d A_log, since dg/dA_log = g) and of dr (d dt_bias); then per head and
-// channel the sum of those over batch entries and segments, in a fixed order.
+// Backward through the retention gate of eq. 9 at width 128, after the
+// combine pass has left dg in a.dg: per element dr = dg (-exp(A_log)
+// sigmoid(r + dt_bias)), written over dg; per head, token segment and channel
+// the sums of dg g (d A_log, since dg/dA_log = g) and of dr (d dt_bias). Then,
+// at every width, per head and channel the sum of those (per segment, or per
+// chunk as the gradient kernel leaves them) over batch entries, in a fixed
+// order.
 // ---------------------------------------------------------------------------
 constexpr int kGateSeg = 256;  // tokens per segment
 
@@ -1371,17 +1410,17 @@ __global__ __launch_bounds__(256) void linear_gate_reduce_kernel(LinearArgs a, i
   }
 }
 
+// The gradient kernel (D <= 64) forms dr and per-chunk sums itself; the
+// width-128 backward (its dg comes from the combine pass) takes the row pass.
 hipError_t launch_gate_bwd(const LinearArgs& a, hipStream_t stream) {
-  const int nseg = (a.T + kGateSeg - 1) / kGateSeg;
-  const dim3 grid((unsigned)nseg, (unsigned)(a.B * a.H));
-  switch (a.D) {
-    case 32: hipLaunchKernelGGL(linear_gate_bwd_kernel<32>, grid, dim3(256), 0, stream, a); break;
-    case 64: hipLaunchKernelGGL(linear_gate_bwd_kernel<64>, grid, dim3(256), 0, stream, a); break;
-    case 128: hipLaunchKernelGGL(linear_gate_bwd_kernel<128>, grid, dim3(256), 0, stream, a); break;
-    default: return hipErrorInvalidValue;
+  int nseg = a.nchunks;
+  if (a.D == 128) {
+    nseg = (a.T + kGateSeg - 1) / kGateSeg;
+    hipLaunchKernelGGL(linear_gate_bwd_kernel<128>, dim3((unsigned)nseg, (unsigned)(a.B * a.H)), dim3(256), 0,
+                       stream, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
   }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(linear_gate_reduce_kernel, dim3((unsigned)((a.H * a.D + 3) / 4)), dim3(256), 0, stream, a, nseg);
   return hipGetLastError();
 }

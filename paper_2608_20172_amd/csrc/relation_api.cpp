@@ -1241,7 +1241,8 @@ static LinearPlan plan_linear(const rel_problem* p, bool split) {
     L.part = L.kn + align256(plane);
     L.total_bwd = L.part + 8 * align256(plane);
   }
-  const size_t gseg = (size_t)((p->T + rel::linear_gate_segment() - 1) / rel::linear_gate_segment());
+  // the gate's sums: per chunk (D <= 64) or per segment of tokens (D = 128), a chunk being the shorter
+  const size_t gseg = std::max((size_t)nc, (size_t)((p->T + rel::linear_gate_segment() - 1) / rel::linear_gate_segment()));
   L.gpart = L.total_bwd;
   L.total_gated = L.gpart + align256((size_t)(p->B * p->H) * gseg * 2 * (size_t)p->D * 4);
   return L;
