@@ -159,9 +159,11 @@ def arm(lib, kernel: str, evs):
     return arr
 
 
-def traffic_for(kernel_hash: str):
-    """HBM bytes per launch of the backward kernel, from the committed counter
-    summary, if it was taken on the current kernel source."""
+def traffic_for(kernel_hash: str, kernel=None):
+    """HBM bytes per launch of one kernel of the backward (``kernel``: its key
+    in the summary's per_kernel table), or of the whole one-kernel backward,
+    from the committed counter summary, if it was taken on the current kernel
+    source."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
@@ -169,6 +171,8 @@ def traffic_for(kernel_hash: str):
         return None
     if t.get("sources_hash") != kernel_hash:
         return None
+    if kernel is not None:
+        return t.get("per_kernel", {}).get(kernel, {}).get("bytes")
     return t.get("bytes_per_launch")
 
 
@@ -643,8 +647,12 @@ def main() -> int:
 
     K = args.steps
     # timed region: K whole steps; the library records HIP events on the launch
-    # stream around the dominant kernels of every step (the backward pair)
-    main_kernel = "bwd" if w.backward else "fwd"
+    # stream around the dominant kernel of every step: the fused dK/dV/dQ kernel
+    # on the one-kernel backward (it does every product of the backward; the row
+    # pass before it and the dq pass after it are O(T D) passes), the whole
+    # two-kernel backward otherwise, the forward kernel for a forward-only workload
+    fused = w.backward and w.dtype == "bf16" and w.D in (32, 64) and w.T >= 1536  # relation_bwd's one-kernel path
+    main_kernel = ("bwd_dkdv" if fused else "bwd") if w.backward else "fwd"
     kev = hip.events(2 * K)
     keep = arm(lib, main_kernel, kev)
     t0 = torch.cuda.Event(enable_timing=True)
@@ -689,7 +697,6 @@ def main() -> int:
         bcall = lambda: R.relation_bwd(q, k, v, f_saved["o"], do, lam_t, f_saved["row_stat"], workspace=ws)
         dcall = lambda: R.relation_bwd(q, k, v, f_saved["o"], do, lam_t, f_saved["row_stat"], workspace=ws,
                                        deterministic=True)
-        fused = w.dtype == "bf16" and w.D in (32, 64) and w.T >= 1536  # relation_bwd's one-kernel path
         per_kernel["bwd_path"] = "one kernel (dq by atomics)" if fused else "two kernels"
         per_kernel["bwd_dkdv_kernel_ms"] = kernel_ms("bwd_dkdv", bcall)
         if fused:
@@ -749,7 +756,7 @@ def main() -> int:
     kern_flops = fl_b if w.backward else fl_f
     achieved = kern_flops / (kern_ms * 1e-3)
     khash = sources_hash()
-    traffic = traffic_for(khash) if w.backward else None
+    traffic = traffic_for(khash, "bwd_fused_kernel" if fused else None) if w.backward else None
     out = {
         "metric": METRIC,
         "value": w.tokens / (ms_step * 1e-3),
@@ -782,7 +789,8 @@ def main() -> int:
         "linear": linear,
         "workloads": legs,
         "roofline": {
-            "kernel": ("relation_bwd (" + per_kernel.get("bwd_path", "") + ")") if w.backward else "fwd_kernel",
+            "kernel": (("bwd_dkdv_kernel<PolBF16<%d>, %d, 8, true> (one-kernel backward: dK, dV and dQ)" % (w.D, w.D))
+                       if fused else "relation_bwd (two kernels)") if w.backward else "fwd_kernel",
             "bound": "mfma",
             "achieved": achieved / 1e12,
             "peak": PEAK_BF16 / 1e12,
@@ -792,6 +800,9 @@ def main() -> int:
             "launches_timed": int(recorded),
             "kernel_ms": kern_ms,
             "sources_hash": khash,
+            # the whole relation_bwd call (with the row pass and the dq pass) over the same flops
+            "relation_bwd_ms": split["bwd_ms_median"] if w.backward else None,
+            "relation_bwd_frac": (kern_flops / (split["bwd_ms_median"] * 1e-3) / PEAK_BF16) if w.backward else None,
         },
         "cpu_baseline": cpu,
     }
