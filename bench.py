@@ -400,8 +400,8 @@ LINEAR_SHAPES = [  # (B, H, T, D): one Linear Relation layer of 8 heads, width 6
 def linear_leg(K: int) -> list:
     """relation_linear_fwd + relation_linear_bwd on bf16 Gaussians and
     log-retention -U(0, 0.05): time per step, tokens/s, the forward alone, and
-    the step with the retention gate formed in the kernels (the gated entry
-    points, pre-activation r ~ N(0, 1))."""
+    the step with the retention gate formed in the kernels and RoPE on p1, p2
+    (the gated entry points, pre-activation r ~ N(0, 1))."""
     import torch
     from paper_2608_20172_amd import binding as R
 
@@ -423,16 +423,21 @@ def linear_leg(K: int) -> list:
             fwd()
             R.relation_linear_bwd(p1, p2, v, g, dy, workspace=bws)
 
-        # the same step with the retention gate of eq. 9 formed in the kernels
+        # the same step as the paper's layer runs it: the retention gate of eq. 9
+        # formed in the kernels and RoPE on p1, p2 (over the paper's width 80
+        # when the heads are 80 padded to 128)
+        rope_dim = 80 if D == 128 else D
         r = torch.randn(B, H, T, D, device=dev, generator=gen)
         a_log = torch.full((H, D), -4.0, device=dev)   # -exp(-4) softplus(r - 3): alpha of about 0.999
         dt_bias = torch.full((H, D), -3.0, device=dev)
         gws = torch.empty(max(1, int(R.load_library().relation_linear_gated_bwd_workspace_bytes(
-            ctypes.byref(R.make_problem(p1))))), dtype=torch.uint8, device=dev)
+            ctypes.byref(R.make_problem(p1)), rope_dim))), dtype=torch.uint8, device=dev)
+        gfws = torch.empty(max(1, int(R.load_library().relation_linear_gated_fwd_workspace_bytes(
+            ctypes.byref(R.make_problem(p1)), rope_dim))), dtype=torch.uint8, device=dev)
 
         def gated_step():
-            R.relation_linear_gated_fwd(p1, p2, v, r, a_log, dt_bias, workspace=fws)
-            R.relation_linear_gated_bwd(p1, p2, v, r, a_log, dt_bias, dy, workspace=gws)
+            R.relation_linear_gated_fwd(p1, p2, v, r, a_log, dt_bias, rope_dim=rope_dim, workspace=gfws)
+            R.relation_linear_gated_bwd(p1, p2, v, r, a_log, dt_bias, dy, rope_dim=rope_dim, workspace=gws)
 
         for _ in range(3):
             step()
@@ -451,7 +456,7 @@ def linear_leg(K: int) -> list:
             res[name] = e0.elapsed_time(e1) / n
         out.append({"B": B, "H": H, "T": T, "D": D, "ms_fwd_bwd": res["fwd_bwd"], "ms_fwd": res["fwd"],
                     "tokens_per_s": B * T / (res["fwd_bwd"] * 1e-3), "ms_gated_fwd_bwd": res["gated_fwd_bwd"]})
-        del p1, p2, v, dy, g, fws, bws, r, a_log, dt_bias, gws
+        del p1, p2, v, dy, g, fws, bws, r, a_log, dt_bias, gws, gfws
     return out
 
 

@@ -372,30 +372,44 @@ rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void*
                                const float* g, const void* dout, void* dp1, void* dp2, void* dv, float* dg,
                                void* workspace, size_t workspace_bytes, void* stream);
 
-/* Linear Relation with the retention gate of eq. 9 formed inside the kernels:
- *   g_t = -exp(A_log) * softplus(r_t + dt_bias),  alpha_t = exp(g_t) in (0, 1]
- * in place of a caller-made g (Sec. 5.2, App. A.4).
+/* Linear Relation as the paper's layer runs it (Sec. 5.2, App. A.4), with the
+ * retention gate of eq. 9 formed inside the kernels,
+ *   g_t = -exp(A_log) * softplus(r_t + dt_bias),  alpha_t = exp(g_t) in (0, 1],
+ * in place of a caller-made g, and optionally the RoPE of Sec. 3.1 on p1 and p2
+ * before S_t and the normalised coordinates are formed.
  *   r          [B,H,T,D] fp32, dense: the gate's pre-activation (the caller's
  *              low-rank projection of the token's input).
  *   a_log,     [H,D] fp32, dense: one value per head and channel, shared by
  *   dt_bias    every batch entry and token.
- * Forward: as relation_linear_fwd, with the same workspace
- * (relation_linear_fwd_workspace_bytes). Backward: as relation_linear_bwd, with
+ *   rope_dim   0: p1, p2 as given. Else the rotated width, even and <= D (a
+ *              multiple of 8 at D = 128): channel j < rope_dim/2 turns with
+ *              channel j + rope_dim/2 by t * rope_base^(-2j/rope_dim) at the
+ *              zero-based position t; channels from rope_dim on are not turned
+ *              (a head of width 80 zero-padded to 128 takes rope_dim = 80).
+ *   rope_base  the base, finite and > 0 (the paper's 10^4) when rope_dim > 0.
+ * Forward: as relation_linear_fwd, with workspace
+ * relation_linear_gated_fwd_workspace_bytes(p, rope_dim) (the ungated
+ * forward's plus the [T, rope_dim/2] table of (cos, sin)). Backward: as
+ * relation_linear_bwd, the gradients with respect to the unrotated p1, p2, with
  *   dr         [B,H,T,D] fp32, dense: dL/dr (in place of dg);
  *   da_log,    [H,D] fp32: dL/dA_log and dL/d dt_bias, each summed over batch
  *   ddt_bias   entries and tokens in a fixed order (run-to-run identical);
- *   workspace  relation_linear_gated_bwd_workspace_bytes(p) bytes: the
- *              ungated backward's plus per head and segment of 256 tokens the
- *              two sums (fp32).
- * Missing a_log or dt_bias: REL_ERR_INVALID_ARG. */
+ *   workspace  relation_linear_gated_bwd_workspace_bytes(p, rope_dim) bytes:
+ *              the ungated backward's plus the two sums per head and chunk (or
+ *              segment of 256 tokens) and the RoPE table.
+ * Missing a_log or dt_bias, a bad rope_dim or rope_base: REL_ERR_INVALID_ARG
+ * (REL_ERR_UNSUPPORTED for a rope_dim at D = 128 that is not a multiple of 8). */
+size_t relation_linear_gated_fwd_workspace_bytes(const rel_problem* p, int32_t rope_dim);
 rel_status relation_linear_gated_fwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
-                                     const float* r, const float* a_log, const float* dt_bias, void* out,
-                                     float* state_out, void* workspace, size_t workspace_bytes, void* stream);
-size_t relation_linear_gated_bwd_workspace_bytes(const rel_problem* p);
+                                     const float* r, const float* a_log, const float* dt_bias, int32_t rope_dim,
+                                     float rope_base, void* out, float* state_out, void* workspace,
+                                     size_t workspace_bytes, void* stream);
+size_t relation_linear_gated_bwd_workspace_bytes(const rel_problem* p, int32_t rope_dim);
 rel_status relation_linear_gated_bwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
-                                     const float* r, const float* a_log, const float* dt_bias, const void* dout,
-                                     void* dp1, void* dp2, void* dv, float* dr, float* da_log, float* ddt_bias,
-                                     void* workspace, size_t workspace_bytes, void* stream);
+                                     const float* r, const float* a_log, const float* dt_bias, int32_t rope_dim,
+                                     float rope_base, const void* dout, void* dp1, void* dp2, void* dv, float* dr,
+                                     float* da_log, float* ddt_bias, void* workspace, size_t workspace_bytes,
+                                     void* stream);
 
 /* Measurement aid. While armed, every launch of the named kernel ("fwd": the
  * fused forward kernel; "bwd": all kernels of one relation_bwd call, back to

@@ -77,10 +77,12 @@ _SIGS = {
     "relation_linear_fwd": (ctypes.c_int, [_PP, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "relation_linear_bwd_workspace_bytes": (ctypes.c_size_t, [_PP]),
     "relation_linear_bwd": (ctypes.c_int, [_PP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
-    "relation_linear_gated_fwd": (ctypes.c_int, [_PP, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
-    "relation_linear_gated_bwd_workspace_bytes": (ctypes.c_size_t, [_PP]),
-    "relation_linear_gated_bwd": (ctypes.c_int, [_PP, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
-                                                 ctypes.c_size_t, _P]),
+    "relation_linear_gated_fwd_workspace_bytes": (ctypes.c_size_t, [_PP, ctypes.c_int32]),
+    "relation_linear_gated_fwd": (ctypes.c_int, [_PP, _P, _P, _P, _P, _P, _P, ctypes.c_int32, ctypes.c_float, _P,
+                                                 _P, _P, ctypes.c_size_t, _P]),
+    "relation_linear_gated_bwd_workspace_bytes": (ctypes.c_size_t, [_PP, ctypes.c_int32]),
+    "relation_linear_gated_bwd": (ctypes.c_int, [_PP, _P, _P, _P, _P, _P, _P, ctypes.c_int32, ctypes.c_float, _P,
+                                                 _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "relation_profile_arm": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]),
     "relation_profile_disarm": (ctypes.c_int, []),
     "relation_mfma_peak_flops": (ctypes.c_int64, [ctypes.c_int, ctypes.c_int]),
@@ -539,10 +541,12 @@ def _gate_params(a_log, dt_bias, p1):
     return out
 
 
-def relation_linear_gated_fwd(p1, p2, v, r, a_log, dt_bias, *, tau_s: float = TAU_S,
-                              scale: Optional[float] = None, want_state: bool = False, workspace=None):
+def relation_linear_gated_fwd(p1, p2, v, r, a_log, dt_bias, *, rope_dim: int = 0, rope_base: float = 1.0e4,
+                              tau_s: float = TAU_S, scale: Optional[float] = None, want_state: bool = False,
+                              workspace=None):
     """Linear Relation forward with the retention gate of eq. 9 formed in the
-    kernels from r ([B, H, T, D] fp32) and a_log, dt_bias ([H, D] fp32).
+    kernels from r ([B, H, T, D] fp32) and a_log, dt_bias ([H, D] fp32), and
+    RoPE over the first rope_dim channels of p1, p2 (0: none).
     Returns dict(o, state)."""
     lib = load_library()
     p2, v = _same_layout(p1, p2, v)
@@ -555,15 +559,17 @@ def relation_linear_gated_fwd(p1, p2, v, r, a_log, dt_bias, *, tau_s: float = TA
     o = _layout_like(p1)
     B, H, T, D = p1.shape
     state = torch.empty((B, H, D, D), dtype=torch.float32, device=dev) if want_state else None
-    ws = _workspace(max(1, int(lib.relation_linear_fwd_workspace_bytes(ctypes.byref(p)))), workspace, dev)
+    ws = _workspace(max(1, int(lib.relation_linear_gated_fwd_workspace_bytes(ctypes.byref(p), rope_dim))),
+                    workspace, dev)
     st = lib.relation_linear_gated_fwd(ctypes.byref(p), _ptr(p1), _ptr(p2), _ptr(v), _ptr(r), _ptr(a_log),
-                                       _ptr(dt_bias), _ptr(o), _ptr(state), _ptr(ws), _nbytes(ws), _stream())
+                                       _ptr(dt_bias), rope_dim, rope_base, _ptr(o), _ptr(state), _ptr(ws),
+                                       _nbytes(ws), _stream())
     _check(st, "relation_linear_gated_fwd")
     return {"o": o, "state": state}
 
 
-def relation_linear_gated_bwd(p1, p2, v, r, a_log, dt_bias, dout, *, tau_s: float = TAU_S,
-                              scale: Optional[float] = None, workspace=None):
+def relation_linear_gated_bwd(p1, p2, v, r, a_log, dt_bias, dout, *, rope_dim: int = 0, rope_base: float = 1.0e4,
+                              tau_s: float = TAU_S, scale: Optional[float] = None, workspace=None):
     """Backward of relation_linear_gated_fwd. Returns dict(dp1, dp2, dv, dr
     (fp32), da_log, ddt_bias ([H, D] fp32))."""
     lib = load_library()
@@ -575,10 +581,12 @@ def relation_linear_gated_bwd(p1, p2, v, r, a_log, dt_bias, dout, *, tau_s: floa
     dp1, dp2, dv = _layout_like(p1), _layout_like(p1), _layout_like(p1)
     dr = torch.empty(p1.shape, dtype=torch.float32, device=dev)
     da_log, ddt_bias = torch.empty_like(a_log), torch.empty_like(dt_bias)
-    ws = _workspace(max(1, int(lib.relation_linear_gated_bwd_workspace_bytes(ctypes.byref(p)))), workspace, dev)
+    ws = _workspace(max(1, int(lib.relation_linear_gated_bwd_workspace_bytes(ctypes.byref(p), rope_dim))),
+                    workspace, dev)
     st = lib.relation_linear_gated_bwd(ctypes.byref(p), _ptr(p1), _ptr(p2), _ptr(v), _ptr(r), _ptr(a_log),
-                                       _ptr(dt_bias), _ptr(dout), _ptr(dp1), _ptr(dp2), _ptr(dv), _ptr(dr),
-                                       _ptr(da_log), _ptr(ddt_bias), _ptr(ws), _nbytes(ws), _stream())
+                                       _ptr(dt_bias), rope_dim, rope_base, _ptr(dout), _ptr(dp1), _ptr(dp2),
+                                       _ptr(dv), _ptr(dr), _ptr(da_log), _ptr(ddt_bias), _ptr(ws), _nbytes(ws),
+                                       _stream())
     _check(st, "relation_linear_gated_bwd")
     return {"dp1": dp1, "dp2": dp2, "dv": dv, "dr": dr, "da_log": da_log, "ddt_bias": ddt_bias}
 

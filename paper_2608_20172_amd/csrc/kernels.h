@@ -173,6 +173,12 @@ struct LinearArgs {
   float* gpart;          // [B H, ceil(T / 256), 2, D] fp32: per token segment, the sums of dg g and dr
   float* da_log;         // [H, D] fp32: d A_log
   float* ddt_bias;       // [H, D] fp32: d dt_bias
+  // RoPE on p1 and p2 (the rotation of Sec. 3.1, applied before S and the
+  // normalised coordinates are formed): channel j with channel j + rope_half
+  // (j < rope_half) by the angle of the token's position, from a [T, rope_half]
+  // table of (cos, sin). Null: no rotation. The norms and p1 . p2 do not change.
+  const float2* rope;
+  int rope_half;
   int split;             // 1: D = 64 sub-problem kernels of a D = 128 backward
   float* qn;             // [N, T, 128] fp32 (split): qt = S ^p1
   float* kn;             // [N, T, 128] fp32 (split): kt = S ^p2

@@ -303,6 +303,24 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
   }
   }
   __syncthreads();
+  if (!SPLIT && a.rope) {
+    // RoPE on the chunk's qt and kt (scaled, not yet rotated): pairs (j, j + h)
+    // of every row; S and the norms above are the same before and after
+    const int h = a.rope_half;
+    for (int i = tid; i < kL * h; i += NT) {
+      const int r = i / h, j = i % h;
+      const float2 cs = a.rope[(int64_t)min(p.t0 + r, a.T - 1) * h + j];
+      const int c1 = col(SWZ_QKB, r, j), c2 = col(SWZ_QKB, r, j + h);
+      if (qt) {
+        const float x = qt[r][c1], y = qt[r][c2];
+        qt[r][c1] = x * cs.x - y * cs.y;
+        qt[r][c2] = x * cs.y + y * cs.x;
+      }
+      const float x = kt[r][c1], y = kt[r][c2];
+      kt[r][c1] = x * cs.x - y * cs.y;
+      kt[r][c2] = x * cs.y + y * cs.x;
+    }
+  }
   // running sum of g down the chunk: thread (channel, segment of SR rows) sums
   // its segment in place, then adds the totals of the segments above it
   constexpr int NSEG = NT / D, SR = kL / NSEG;
@@ -1132,6 +1150,36 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
   s12 = group_sum<kTPRG>(s12);
   const float S = Srow[r];
   const float in1 = s11 > 0.0f ? rsqrtf(s11) : 0.0f, in2 = s22 > 0.0f ? rsqrtf(s22) : 0.0f;
+  // with RoPE the projections below take the rotated p1, p2 (a channel's
+  // partner lives in another thread: the exchange goes through the free qt and
+  // kt arrays, plain layout), and the result goes back through the rotation's
+  // transpose the same way
+  float(*X1)[D] = qt;
+  float(*X2)[D] = kt;
+  const int64_t trow = (int64_t)min(p.t0 + r, a.T - 1) * a.rope_half;
+  auto rotate = [&](float(&u1)[QW], float(&u2)[QW], bool transpose) {
+#pragma unroll
+    for (int i = 0; i < QW; ++i) {
+      X1[r][q0 + i] = u1[i];
+      X2[r][q0 + i] = u2[i];
+    }
+    __syncthreads();
+    const int h = a.rope_half;
+#pragma unroll
+    for (int i = 0; i < QW; ++i) {
+      const int c = q0 + i;
+      if (c < 2 * h) {
+        const bool lo = c < h;
+        const int j = lo ? c : c - h, pc = lo ? c + h : c - h;
+        const float2 cs = a.rope[trow + j];
+        const float sn = transpose ? -cs.y : cs.y;  // R^T: the angle negated
+        u1[i] = lo ? u1[i] * cs.x - X1[r][pc] * sn : X1[r][pc] * sn + u1[i] * cs.x;
+        u2[i] = lo ? u2[i] * cs.x - X2[r][pc] * sn : X2[r][pc] * sn + u2[i] * cs.x;
+      }
+    }
+    __syncthreads();
+  };
+  if (a.rope) rotate(x1, x2, false);
   // dS = dqt . ^p1 + dkt . ^p2; ^p . d^p for the projections
   float ds = 0.0f, h1d = 0.0f, h2d = 0.0f;
 #pragma unroll
@@ -1143,18 +1191,19 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
   ds = group_sum<kTPRG>(ds);
   h1d = group_sum<kTPRG>(h1d);
   h2d = group_sum<kTPRG>(h2d);
+  const float dU = ds * S * (1.0f - S) * a.scale * a.inv_tau;
+  float g1[QW], g2[QW];
+#pragma unroll
+  for (int i = 0; i < QW; ++i) {
+    // d^p1 = S dqt; dp1 = dU p2 + (d^p1 - ^p1 (^p1 . d^p1)) / |p1|
+    g1[i] = dU * x2[i] + S * (dq[i] - x1[i] * in1 * h1d) * in1;
+    g2[i] = dU * x1[i] + S * (dk[i] - x2[i] * in2 * h2d) * in2;
+  }
+  if (a.rope) rotate(g1, g2, true);
   if (ok) {
-    const float dU = ds * S * (1.0f - S) * a.scale * a.inv_tau;
     TI* DP1 = (TI*)a.dp1 + hoff + (int64_t)(p.t0 + r) * a.st;
     TI* DP2 = (TI*)a.dp2 + hoff + (int64_t)(p.t0 + r) * a.st;
     TI* DV = (TI*)a.dv + hoff + (int64_t)(p.t0 + r) * a.st;
-    float g1[QW], g2[QW];
-#pragma unroll
-    for (int i = 0; i < QW; ++i) {
-      // d^p1 = S dqt; dp1 = dU p2 + (d^p1 - ^p1 (^p1 . d^p1)) / |p1|
-      g1[i] = dU * x2[i] + S * (dq[i] - x1[i] * in1 * h1d) * in1;
-      g2[i] = dU * x1[i] + S * (dk[i] - x2[i] * in2 * h2d) * in2;
-    }
     if constexpr (QW == 4) {
       if (a.vec16) {
         Vec4<TI>::store(DP1 + q0, g1);
@@ -1262,7 +1311,29 @@ __device__ __forceinline__ void row_self(const LinearArgs& a, const float (&x1)[
   in2 = s22 > 0.0f ? rsqrtf(s22) : 0.0f;
 }
 
-// qn = S ^p1, kn = S ^p2 per row.
+// RoPE of a row held as 4 channels per lane over kSLanes lanes (pairs (j,
+// j + h) with h a multiple of 4, so a lane's partner chunk is one lane):
+// transpose = false rotates, true applies the transposed rotation. Every lane
+// of the wave takes part (the exchange is a lane shuffle).
+__device__ __forceinline__ void rope_row(const LinearArgs& a, int64_t t, int c0, float (&u)[4], bool transpose) {
+  const int h = a.rope_half, lane = threadIdx.x & 63;
+  const bool lo = c0 < h, on = c0 < 2 * h;
+  const int src = on ? (lo ? lane + h / 4 : lane - h / 4) : lane;
+  float pv[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) pv[e] = __shfl(u[e], src, 64);
+  if (on) {
+    const int j0 = lo ? c0 : c0 - h;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float2 cs = a.rope[t * h + j0 + e];
+      const float sn = transpose ? -cs.y : cs.y;
+      u[e] = lo ? u[e] * cs.x - pv[e] * sn : pv[e] * sn + u[e] * cs.x;
+    }
+  }
+}
+
+// qn = S ^p1, kn = S ^p2 per row (rotated with RoPE).
 template <typename TI>
 __global__ __launch_bounds__(256) void linear_split_prep_kernel(LinearArgs a) {
   const SplitRow w = split_row(a);
@@ -1270,6 +1341,10 @@ __global__ __launch_bounds__(256) void linear_split_prep_kernel(LinearArgs a) {
   load4<TI>(a, (const TI*)a.p1 + w.off, x1);
   load4<TI>(a, (const TI*)a.p2 + w.off, x2);
   row_self(a, x1, x2, S, in1, in2);
+  if (a.rope) {
+    rope_row(a, w.nt % a.T, w.c0, x1, false);
+    rope_row(a, w.nt % a.T, w.c0, x2, false);
+  }
   if (w.ok) {
     float q[4], k[4];
 #pragma unroll
@@ -1295,6 +1370,10 @@ __global__ __launch_bounds__(256) void linear_split_combine_kernel(LinearArgs a)
 #pragma unroll
   for (int k = 0; k < 8; ++k) Vec4<float>::load(a.part + k * plane + at, pr[k]);
   row_self(a, x1, x2, S, in1, in2);
+  if (a.rope) {  // the projections take the rotated coordinates
+    rope_row(a, w.nt % a.T, w.c0, x1, false);
+    rope_row(a, w.nt % a.T, w.c0, x2, false);
+  }
   float dq[4], dk[4], dv[4], dg[4];
   float ds = 0.0f, h1d = 0.0f, h2d = 0.0f;
 #pragma unroll
@@ -1310,14 +1389,18 @@ __global__ __launch_bounds__(256) void linear_split_combine_kernel(LinearArgs a)
   ds = lane_group_sum<kSLanes>(ds);
   h1d = lane_group_sum<kSLanes>(h1d);
   h2d = lane_group_sum<kSLanes>(h2d);
-  if (w.ok) {
-    const float dU = ds * S * (1.0f - S) * a.scale * a.inv_tau;
-    float g1[4], g2[4];
+  const float dU = ds * S * (1.0f - S) * a.scale * a.inv_tau;
+  float g1[4], g2[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      g1[i] = dU * x2[i] + S * (dq[i] - x1[i] * in1 * h1d) * in1;
-      g2[i] = dU * x1[i] + S * (dk[i] - x2[i] * in2 * h2d) * in2;
-    }
+  for (int i = 0; i < 4; ++i) {
+    g1[i] = dU * x2[i] + S * (dq[i] - x1[i] * in1 * h1d) * in1;
+    g2[i] = dU * x1[i] + S * (dk[i] - x2[i] * in2 * h2d) * in2;
+  }
+  if (a.rope) {  // back through the rotation
+    rope_row(a, w.nt % a.T, w.c0, g1, true);
+    rope_row(a, w.nt % a.T, w.c0, g2, true);
+  }
+  if (w.ok) {
     store4<TI>(a, (TI*)a.dp1 + w.off, g1);
     store4<TI>(a, (TI*)a.dp2 + w.off, g2);
     store4<TI>(a, (TI*)a.dv + w.off, dv);
@@ -1335,6 +1418,7 @@ hipError_t launch_bwd_split(const LinearArgs& a, hipStream_t stream) {
   LinearArgs s = a;
   s.D = kSW / 2;
   s.split = 1;
+  s.rope = nullptr;  // qn and kn are rotated already
   e = launch_bwd_d<TI, kSW / 2, true>(s, stream);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((linear_split_combine_kernel<TI>), rgrid, dim3(256), 0, stream, a);

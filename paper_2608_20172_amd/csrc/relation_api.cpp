@@ -1283,12 +1283,52 @@ size_t relation_linear_fwd_workspace_bytes(const rel_problem* p) {
   return plan_linear(p, false).total;
 }
 
+// RoPE of the gated entry points: rope_dim 0 (none), or an even width up to D
+// whose channels j < rope_dim / 2 turn with j + rope_dim / 2; at D = 128 (the
+// four-block backward, whose row passes hold 4 channels per lane) a multiple of 8.
+static rel_status check_rope(const rel_problem* p, int32_t rope_dim, float rope_base) {
+  if (rope_dim == 0) return REL_OK;
+  if (rope_dim < 0 || rope_dim % 2 || rope_dim > p->D)
+    return fail(REL_ERR_INVALID_ARG, "rope_dim %d must be 0 or an even width <= D = %lld", (int)rope_dim,
+                (long long)p->D);
+  if (p->D == 128 && rope_dim % 8)
+    return fail(REL_ERR_UNSUPPORTED, "at D = 128 rope_dim must be a multiple of 8 (got %d)", (int)rope_dim);
+  if (!(std::isfinite(rope_base) && rope_base > 0.0f))
+    return fail(REL_ERR_INVALID_ARG, "rope_base must be finite and > 0");
+  return REL_OK;
+}
+
+static size_t rope_table_bytes(const rel_problem* p, int32_t rope_dim) {
+  return rope_dim > 0 ? align256((size_t)p->T * (size_t)(rope_dim / 2) * 8) : 0;
+}
+
+size_t relation_linear_gated_fwd_workspace_bytes(const rel_problem* p, int32_t rope_dim) {
+  bool empty = false;
+  if (check_linear(p, &empty) != REL_OK || empty || check_rope(p, rope_dim, 1.0f) != REL_OK) return 0;
+  return plan_linear(p, false).total + rope_table_bytes(p, rope_dim);
+}
+
+// The RoPE table [T, rope_dim / 2] of (cos, sin) at workspace offset off, and
+// the kernels' view of it.
+static rel_status set_rope(rel::LinearArgs& a, const rel_problem* p, int32_t rope_dim, float rope_base, char* ws,
+                           size_t off, hipStream_t stream) {
+  if (rope_dim == 0) return REL_OK;
+  float2* tab = (float2*)(ws + off);
+  const hipError_t e = rel::launch_rope_table(tab, (int)p->T, (int)rope_dim, (double)rope_base, stream);
+  if (e != hipSuccess) return hip_fail(e, "RoPE table launch");
+  a.rope = tab;
+  a.rope_half = rope_dim / 2;
+  return REL_OK;
+}
+
 // g: the log-retention, or with a_log set the gate's pre-activation r.
 static rel_status linear_fwd_impl(const rel_problem* p, const void* p1, const void* p2, const void* v, const float* g,
-                                  const float* a_log, const float* dt_bias, void* out, float* state_out,
-                                  void* workspace, size_t workspace_bytes, void* stream) {
+                                  const float* a_log, const float* dt_bias, int32_t rope_dim, float rope_base,
+                                  void* out, float* state_out, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
   bool empty = false;
   REL_TRY(check_linear(p, &empty));
+  REL_TRY(check_rope(p, rope_dim, rope_base));
   if (empty) return REL_OK;
   const size_t es = elem_size(p->dtype);
   REL_TRY(check_aligned(p1, es, "p1", true));
@@ -1300,8 +1340,9 @@ static rel_status linear_fwd_impl(const rel_problem* p, const void* p1, const vo
   REL_TRY(check_aligned(out, es, "out", true));
   REL_TRY(check_aligned(state_out, 4, "state_out", false));
   const LinearPlan L = plan_linear(p, false);
-  if (!workspace || workspace_bytes < L.total)
-    return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
+  const size_t need = L.total + rope_table_bytes(p, rope_dim);
+  if (!workspace || workspace_bytes < need)
+    return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
                 workspace ? workspace_bytes : (size_t)0);
   REL_TRY(check_aligned(workspace, 16, "workspace", true));
   const size_t tb = (size_t)extent_elems(p) * es;
@@ -1316,7 +1357,7 @@ static rel_status linear_fwd_impl(const rel_problem* p, const void* p1, const vo
                             {dt_bias, pb, false, false, "dt_bias"},
                             {out, tb, true, true, "out"},
                             {state_out, N * (size_t)(p->D * p->D) * 4, false, true, "state_out"},
-                            {workspace, L.total, false, true, "workspace"}}));
+                            {workspace, need, false, true, "workspace"}}));
   if (test_fail_launch()) return fail(REL_ERR_HIP, "launch failure injected by RELATION_TEST_FAIL_LAUNCH");
   rel::LinearArgs a{};
   a.p1 = p1; a.p2 = p2; a.v = v; a.g = g; a.out = out; a.state_out = state_out;
@@ -1329,6 +1370,7 @@ static rel_status linear_fwd_impl(const rel_problem* p, const void* p1, const vo
   a.nseg = linear_segments(p);
   a.vec16 = linear_vec16(p, {p1, p2, v}, g);
   set_linear_workspace(a, L, (char*)workspace, false);
+  REL_TRY(set_rope(a, p, rope_dim, rope_base, (char*)workspace, L.total, (hipStream_t)stream));
   const hipError_t e = rel::launch_linear_fwd(a, p->dtype, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "Linear Relation launch");
   return REL_OK;
@@ -1337,35 +1379,41 @@ static rel_status linear_fwd_impl(const rel_problem* p, const void* p1, const vo
 rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
                                const float* g, void* out, float* state_out, void* workspace,
                                size_t workspace_bytes, void* stream) {
-  return linear_fwd_impl(p, p1, p2, v, g, nullptr, nullptr, out, state_out, workspace, workspace_bytes, stream);
+  return linear_fwd_impl(p, p1, p2, v, g, nullptr, nullptr, 0, 0.0f, out, state_out, workspace, workspace_bytes,
+                         stream);
 }
 
 rel_status relation_linear_gated_fwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
-                                     const float* r, const float* a_log, const float* dt_bias, void* out,
-                                     float* state_out, void* workspace, size_t workspace_bytes, void* stream) {
+                                     const float* r, const float* a_log, const float* dt_bias, int32_t rope_dim,
+                                     float rope_base, void* out, float* state_out, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
   if (!a_log || !dt_bias) return fail(REL_ERR_INVALID_ARG, "a_log and dt_bias are required");
-  return linear_fwd_impl(p, p1, p2, v, r, a_log, dt_bias, out, state_out, workspace, workspace_bytes, stream);
+  return linear_fwd_impl(p, p1, p2, v, r, a_log, dt_bias, rope_dim, rope_base, out, state_out, workspace,
+                         workspace_bytes, stream);
 }
 
-static size_t linear_bwd_ws(const rel_problem* p, bool gated) {
+static size_t linear_bwd_ws(const rel_problem* p, bool gated, int32_t rope_dim) {
   bool empty = false;
-  if (check_linear(p, &empty) != REL_OK || empty) return 0;
+  if (check_linear(p, &empty) != REL_OK || empty || check_rope(p, rope_dim, 1.0f) != REL_OK) return 0;
   const LinearPlan L = plan_linear(p, linear_split(p));
-  return gated ? L.total_gated : L.total_bwd;
+  return (gated ? L.total_gated : L.total_bwd) + rope_table_bytes(p, rope_dim);
 }
 
-size_t relation_linear_bwd_workspace_bytes(const rel_problem* p) { return linear_bwd_ws(p, false); }
-size_t relation_linear_gated_bwd_workspace_bytes(const rel_problem* p) { return linear_bwd_ws(p, true); }
+size_t relation_linear_bwd_workspace_bytes(const rel_problem* p) { return linear_bwd_ws(p, false, 0); }
+size_t relation_linear_gated_bwd_workspace_bytes(const rel_problem* p, int32_t rope_dim) {
+  return linear_bwd_ws(p, true, rope_dim);
+}
 
 // g: the log-retention, or with a_log set the gate's pre-activation r; dg is
 // then dr, and da_log, ddt_bias receive the parameters' gradients.
 static rel_status linear_bwd_impl(const rel_problem* p, const void* p1, const void* p2, const void* v, const float* g,
-                                  const float* a_log, const float* dt_bias, const void* dout, void* dp1, void* dp2,
-                                  void* dv, float* dg, float* da_log, float* ddt_bias, void* workspace,
-                                  size_t workspace_bytes, void* stream) {
+                                  const float* a_log, const float* dt_bias, int32_t rope_dim, float rope_base,
+                                  const void* dout, void* dp1, void* dp2, void* dv, float* dg, float* da_log,
+                                  float* ddt_bias, void* workspace, size_t workspace_bytes, void* stream) {
   bool empty = false;
   const bool gated = a_log != nullptr;
   REL_TRY(check_linear(p, &empty));
+  REL_TRY(check_rope(p, rope_dim, rope_base));
   if (empty) return REL_OK;
   const size_t es = elem_size(p->dtype);
   REL_TRY(check_aligned(p1, es, "p1", true));
@@ -1383,7 +1431,7 @@ static rel_status linear_bwd_impl(const rel_problem* p, const void* p1, const vo
     REL_TRY(check_aligned(da_log, 4, "da_log", true));
     REL_TRY(check_aligned(ddt_bias, 4, "ddt_bias", true));
   }
-  const size_t need = linear_bwd_ws(p, gated);
+  const size_t need = linear_bwd_ws(p, gated, rope_dim);
   if (!workspace || workspace_bytes < need)
     return fail(REL_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
                 workspace ? workspace_bytes : (size_t)0);
@@ -1424,6 +1472,8 @@ static rel_status linear_bwd_impl(const rel_problem* p, const void* p1, const vo
     a.gpart = (float*)((char*)workspace + L.gpart);
     a.da_log = da_log; a.ddt_bias = ddt_bias;
   }
+  REL_TRY(set_rope(a, p, rope_dim, rope_base, (char*)workspace, gated ? L.total_gated : L.total_bwd,
+                   (hipStream_t)stream));
   const hipError_t e = rel::launch_linear_bwd(a, p->dtype, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "Linear Relation backward launch");
   return REL_OK;
@@ -1432,17 +1482,18 @@ static rel_status linear_bwd_impl(const rel_problem* p, const void* p1, const vo
 rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
                                const float* g, const void* dout, void* dp1, void* dp2, void* dv, float* dg,
                                void* workspace, size_t workspace_bytes, void* stream) {
-  return linear_bwd_impl(p, p1, p2, v, g, nullptr, nullptr, dout, dp1, dp2, dv, dg, nullptr, nullptr, workspace,
-                         workspace_bytes, stream);
+  return linear_bwd_impl(p, p1, p2, v, g, nullptr, nullptr, 0, 0.0f, dout, dp1, dp2, dv, dg, nullptr, nullptr,
+                         workspace, workspace_bytes, stream);
 }
 
 rel_status relation_linear_gated_bwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
-                                     const float* r, const float* a_log, const float* dt_bias, const void* dout,
-                                     void* dp1, void* dp2, void* dv, float* dr, float* da_log, float* ddt_bias,
-                                     void* workspace, size_t workspace_bytes, void* stream) {
+                                     const float* r, const float* a_log, const float* dt_bias, int32_t rope_dim,
+                                     float rope_base, const void* dout, void* dp1, void* dp2, void* dv, float* dr,
+                                     float* da_log, float* ddt_bias, void* workspace, size_t workspace_bytes,
+                                     void* stream) {
   if (!a_log || !dt_bias) return fail(REL_ERR_INVALID_ARG, "a_log and dt_bias are required");
-  return linear_bwd_impl(p, p1, p2, v, r, a_log, dt_bias, dout, dp1, dp2, dv, dr, da_log, ddt_bias, workspace,
-                         workspace_bytes, stream);
+  return linear_bwd_impl(p, p1, p2, v, r, a_log, dt_bias, rope_dim, rope_base, dout, dp1, dp2, dv, dr, da_log,
+                         ddt_bias, workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

@@ -348,23 +348,38 @@ def test_linear_widths_and_workspace(lib):
 
 def test_linear_gated_validation(lib):
     """The gated Linear Relation entry points need a_log and dt_bias, reject an
-    output that overlaps r, and take a larger backward workspace than the
-    ungated backward (the gate's segment sums)."""
+    output that overlaps r and a bad RoPE width or base, and take a larger
+    backward workspace than the ungated backward (the gate's sums) and a larger
+    workspace again with RoPE (its table)."""
     a = ptrs(14)
     p = prob(B=2, H=3, T=300, D=64)
-    ws = lib.relation_linear_gated_bwd_workspace_bytes(ctypes.byref(p))
+    ws = lib.relation_linear_gated_bwd_workspace_bytes(ctypes.byref(p), 0)
     assert ws > lib.relation_linear_bwd_workspace_bytes(ctypes.byref(p))
-    fws = lib.relation_linear_fwd_workspace_bytes(ctypes.byref(p))
-    fwd = lambda alog, dtb: lib.relation_linear_gated_fwd(ctypes.byref(p), a[0], a[1], a[2], a[3], alog, dtb, a[6],
-                                                         None, a[13], fws, None)
+    assert lib.relation_linear_gated_bwd_workspace_bytes(ctypes.byref(p), 60) > ws
+    fws = lib.relation_linear_gated_fwd_workspace_bytes(ctypes.byref(p), 0)
+    assert fws == lib.relation_linear_fwd_workspace_bytes(ctypes.byref(p))
+    assert lib.relation_linear_gated_fwd_workspace_bytes(ctypes.byref(p), 64) > fws
+    fwd = lambda alog, dtb, rd=0, rb=0.0, pp=p, n=fws: lib.relation_linear_gated_fwd(
+        ctypes.byref(pp), a[0], a[1], a[2], a[3], alog, dtb, rd, rb, a[6], None, a[13], n, None)
     assert fwd(a[4], a[5]) == R.REL_ERR_HIP
     assert fwd(None, a[5]) == R.REL_ERR_INVALID_ARG
     assert fwd(a[4], None) == R.REL_ERR_INVALID_ARG
-    bwd = lambda dr: lib.relation_linear_gated_bwd(ctypes.byref(p), a[0], a[1], a[2], a[3], a[4], a[5], a[6], a[7],
-                                                   a[8], a[9], dr, a[11], a[12], a[13], ws, None)
+    big = 1 << 22
+    assert fwd(a[4], a[5], 60, 1e4, n=big) == R.REL_ERR_HIP       # width 60 of 64
+    assert fwd(a[4], a[5], 61, 1e4, n=big) == R.REL_ERR_INVALID_ARG
+    assert fwd(a[4], a[5], 66, 1e4, n=big) == R.REL_ERR_INVALID_ARG
+    assert fwd(a[4], a[5], 64, 0.0, n=big) == R.REL_ERR_INVALID_ARG
+    assert fwd(a[4], a[5], 64, 1e4) == R.REL_ERR_WORKSPACE        # the table does not fit
+    p128 = prob(B=1, H=2, T=100, D=128)
+    assert fwd(a[4], a[5], 80, 1e4, pp=p128, n=big) == R.REL_ERR_HIP
+    assert fwd(a[4], a[5], 60, 1e4, pp=p128, n=big) == R.REL_ERR_UNSUPPORTED
+    bwd = lambda dr, rd=0: lib.relation_linear_gated_bwd(ctypes.byref(p), a[0], a[1], a[2], a[3], a[4], a[5], rd,
+                                                         1e4, a[6], a[7], a[8], a[9], dr, a[11], a[12], a[13],
+                                                         big, None)
     assert bwd(a[10]) == R.REL_ERR_HIP
+    assert bwd(a[10], 48) == R.REL_ERR_HIP
     assert bwd(a[3]) == R.REL_ERR_INVALID_ARG  # dr over r
     assert b"overlaps" in lib.relation_last_error()
-    st = lib.relation_linear_gated_bwd(ctypes.byref(p), a[0], a[1], a[2], a[3], None, a[5], a[6], a[7], a[8], a[9],
-                                       a[10], a[11], a[12], a[13], ws, None)
+    st = lib.relation_linear_gated_bwd(ctypes.byref(p), a[0], a[1], a[2], a[3], None, a[5], 0, 0.0, a[6], a[7], a[8],
+                                       a[9], a[10], a[11], a[12], a[13], ws, None)
     assert st == R.REL_ERR_INVALID_ARG

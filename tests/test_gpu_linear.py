@@ -306,3 +306,50 @@ def test_linear_mixed_decay_chunks(D, dtype):
     x["gr"] = g.astype(np.float64)
     check_linear_fwd(x, dtype)
     check_linear_bwd(x, dtype)
+
+
+@pytest.mark.parametrize("width,padded,T,dtype", [(64, 64, 300, "bf16"), (32, 32, 190, "f32"), (128, 128, 200, "bf16"),
+                                                   (80, 128, 260, "f32"), (60, 64, 129, "f32"), (48, 64, 200, "bf16")])
+def test_linear_gated_rope(width, padded, T, dtype):
+    """RoPE (base 1e4) on p1, p2 inside the gated kernels, over the true width
+    of a head zero-padded to a kernel width: y, dp1, dp2, dv, dr, dA_log and
+    d dt_bias against the oracle's RoPE (the layer oracle's rotate-half)
+    composed with the gate and the recurrence at the true width, and zeros on
+    the padding."""
+    from oracle import layer_oracle as LR
+    B, H = 1, 2
+    x = _prep(B, H, T, width, dtype, seed=2200 + width + T)
+    rng = np.random.default_rng(2201 + T)
+    r = (2.0 * rng.standard_normal((B, H, T, width))).astype(np.float32)
+    a_log, dt_bias = _gate_params(H, width, 2202 + T)
+    pad = {n: _pad(x[n], padded).contiguous() for n in ("p1", "p2", "v", "dy")}
+    rt = _pad(torch.from_numpy(r), padded).contiguous().cuda()
+    at, bt = (_pad(torch.from_numpy(z), padded).contiguous().cuda() for z in (a_log, dt_bias))
+    scale = 1.0 / math.sqrt(width)
+    log(f"[linear gated rope] width {width} -> {padded}, T={T} {dtype}")
+    f = R.relation_linear_gated_fwd(pad["p1"], pad["p2"], pad["v"], rt, at, bt, rope_dim=width, rope_base=1e4,
+                                    scale=scale)
+    o = R.relation_linear_gated_bwd(pad["p1"], pad["p2"], pad["v"], rt, at, bt, pad["dy"], rope_dim=width,
+                                    rope_base=1e4, scale=scale)
+    torch.cuda.synchronize()
+    da_ref, dt_ref = np.zeros((H, width)), np.zeros((H, width))
+    da_terms, dt_terms = np.zeros((B, H, T, width)), np.zeros((B, H, T, width))
+    for h in range(H):
+        p1r, p2r = LR.rope(x["p1r"][0, h], 1e4), LR.rope(x["p2r"][0, h], 1e4)
+        g = LO.kda_gate(r[0, h], a_log[h], dt_bias[h])
+        ref_f = LO.forward(p1r, p2r, x["vr"][0, h], g)
+        y = _np(f["o"])[0, h]
+        assert_close(f"y[0,{h}]", y[:, :width], ref_f["Y"], dtype)
+        assert not np.any(y[:, width:])
+        ref_b = LO.backward(p1r, p2r, x["vr"][0, h], g, x["dyr"][0, h])
+        gb = LO.kda_gate_backward(r[0, h], a_log[h], dt_bias[h], ref_b["dg"])
+        want = {"dp1": LR.rope_transpose(ref_b["dp1"], 1e4), "dp2": LR.rope_transpose(ref_b["dp2"], 1e4),
+                "dv": ref_b["dv"], "dr": gb["dr"]}
+        for n, ref in want.items():
+            got = _np(o[n])[0, h]
+            assert_close(f"{n}[0,{h}]", got[:, :width], ref, dtype)
+            assert not np.any(got[:, width:]), f"{n}: padding channels non-zero"
+        da_ref[h], dt_ref[h] = gb["da_log"], gb["ddt_bias"]
+        da_terms[0, h], dt_terms[0, h] = ref_b["dg"] * g, gb["dr"]
+    _assert_param_grad("da_log", _np(o["da_log"])[:, :width], da_ref, da_terms, dtype)
+    _assert_param_grad("ddt_bias", _np(o["ddt_bias"])[:, :width], dt_ref, dt_terms, dtype)
