@@ -389,7 +389,8 @@ rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void*
  *   rope_base  the base, finite and > 0 (the paper's 10^4) when rope_dim > 0.
  * Forward: as relation_linear_fwd, with workspace
  * relation_linear_gated_fwd_workspace_bytes(p, rope_dim) (the ungated
- * forward's plus the [T, rope_dim/2] table of (cos, sin)). Backward: as
+ * forward's plus a table of (cos, sin) at the 64-token chunk starts and at
+ * the offsets inside a chunk, ((T + 63)/64 + 64) x rope_dim/2). Backward: as
  * relation_linear_bwd, the gradients with respect to the unrotated p1, p2, with
  *   dr         [B,H,T,D] fp32, dense: dL/dr (in place of dg);
  *   da_log,    [H,D] fp32: dL/dA_log and dL/d dt_bias, each summed over batch

@@ -175,8 +175,9 @@ struct LinearArgs {
   float* ddt_bias;       // [H, D] fp32: d dt_bias
   // RoPE on p1 and p2 (the rotation of Sec. 3.1, applied before S and the
   // normalised coordinates are formed): channel j with channel j + rope_half
-  // (j < rope_half) by the angle of the token's position, from a [T, rope_half]
-  // table of (cos, sin). Null: no rotation. The norms and p1 . p2 do not change.
+  // (j < rope_half) by the angle of the token's position, from a table of
+  // (cos, sin) at the chunk starts and the offsets inside a chunk
+  // (launch_linear_rope_table). Null: no rotation. The norms and p1 . p2 do not change.
   const float2* rope;
   int rope_half;
   int split;             // 1: D = 64 sub-problem kernels of a D = 128 backward
@@ -209,6 +210,8 @@ int linear_scan_segment();  // chunks per segment of the state scans
 hipError_t launch_linear_fwd(const LinearArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_linear_bwd(const LinearArgs& a, int dtype, hipStream_t stream);
 int linear_gate_segment();  // tokens per segment of the gate's parameter-gradient sums
+// RoPE table of the Linear Relation kernels: (linear_chunk() + chunks) x rope_dim/2 (cos, sin)
+hipError_t launch_linear_rope_table(float2* tab, int T, int rope_dim, double base, hipStream_t stream);
 int decode_slice_keys();
 hipError_t launch_decode_states(const DecodeArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_decode_merge(const DecodeArgs& a, int dtype, hipStream_t stream);

@@ -71,6 +71,17 @@ __device__ __forceinline__ float softplus_f(float x) {
   return fmaxf(x, 0.0f) + kLn2 * __builtin_amdgcn_logf(1.0f + fast_exp2(-fabsf(x) * kLog2e));
 }
 
+// RoPE angle of position t, channel pair j: the table holds (cos, sin) of the
+// angle at every chunk start (rows 0 .. nchunks - 1) and at every offset
+// inside a chunk (rows nchunks .. nchunks + kL - 1); the angle at t is their
+// sum (a few kB instead of a [T, rope_half] table read by every head).
+__device__ __forceinline__ float2 rope_cs(const LinearArgs& a, int64_t t, int j) {
+  const int h = a.rope_half;
+  const float2 A = a.rope[(t / kL) * h + j];
+  const float2 B = a.rope[(int64_t)(a.nchunks + t % kL) * h + j];
+  return make_float2(A.x * B.x - A.y * B.y, A.y * B.x + A.x * B.y);
+}
+
 // The retention gate of eq. 9: g = -exp(A_log) softplus(r + dt_bias), with
 // ea = exp(A_log) of the channel.
 __device__ __forceinline__ float kda_gate(float r, float ea, float dtb) { return -ea * softplus_f(r + dtb); }
@@ -309,7 +320,7 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
     const int h = a.rope_half;
     for (int i = tid; i < kL * h; i += NT) {
       const int r = i / h, j = i % h;
-      const float2 cs = a.rope[(int64_t)min(p.t0 + r, a.T - 1) * h + j];
+      const float2 cs = rope_cs(a, min(p.t0 + r, a.T - 1), j);
       const int c1 = col(SWZ_QKB, r, j), c2 = col(SWZ_QKB, r, j + h);
       if (qt) {
         const float x = qt[r][c1], y = qt[r][c2];
@@ -990,6 +1001,15 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
   const TI* P2 = (const TI*)a.p2 + hoff + prow * a.st;
   const bool ok = r < p.len;
   float x1[QW], x2[QW];
+  float2 rq[QW];  // RoPE (cos, sin) of this thread's channels, read now for the last step
+  if (!SPLIT && a.rope) {
+    const int h = a.rope_half;
+#pragma unroll
+    for (int i = 0; i < QW; ++i) {
+      const int c = q0 + i;
+      rq[i] = c < 2 * h ? rope_cs(a, min(p.t0 + r, a.T - 1), c < h ? c : c - h) : make_float2(1.0f, 0.0f);
+    }
+  }
   if constexpr (!SPLIT) {
     if constexpr (QW == 4) {
       if (a.vec16) {
@@ -1156,7 +1176,6 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
   // transpose the same way
   float(*X1)[D] = qt;
   float(*X2)[D] = kt;
-  const int64_t trow = (int64_t)min(p.t0 + r, a.T - 1) * a.rope_half;
   auto rotate = [&](float(&u1)[QW], float(&u2)[QW], bool transpose) {
 #pragma unroll
     for (int i = 0; i < QW; ++i) {
@@ -1170,8 +1189,8 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
       const int c = q0 + i;
       if (c < 2 * h) {
         const bool lo = c < h;
-        const int j = lo ? c : c - h, pc = lo ? c + h : c - h;
-        const float2 cs = a.rope[trow + j];
+        const int pc = lo ? c + h : c - h;
+        const float2 cs = rq[i];
         const float sn = transpose ? -cs.y : cs.y;  // R^T: the angle negated
         u1[i] = lo ? u1[i] * cs.x - X1[r][pc] * sn : X1[r][pc] * sn + u1[i] * cs.x;
         u2[i] = lo ? u2[i] * cs.x - X2[r][pc] * sn : X2[r][pc] * sn + u2[i] * cs.x;
@@ -1326,7 +1345,7 @@ __device__ __forceinline__ void rope_row(const LinearArgs& a, int64_t t, int c0,
     const int j0 = lo ? c0 : c0 - h;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const float2 cs = a.rope[t * h + j0 + e];
+      const float2 cs = rope_cs(a, t, j0 + e);
       const float sn = transpose ? -cs.y : cs.y;
       u[e] = lo ? u[e] * cs.x - pv[e] * sn : pv[e] * sn + u[e] * cs.x;
     }
@@ -1543,7 +1562,28 @@ hipError_t launch_fwd_t(const LinearArgs& a, hipStream_t stream) {
 
 }  // namespace
 
+// The RoPE table of rope_cs: (cos, sin) of t * base^(-2j/rope_dim) for t at
+// the chunk starts and the offsets inside a chunk, evaluated in fp64.
+__global__ __launch_bounds__(256) void linear_rope_table_kernel(float2* tab, int nch, int rope_dim, double log_base) {
+  const int h = rope_dim / 2;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)(nch + kL) * h) return;
+  const int row = (int)(idx / h), j = (int)(idx % h);
+  const double t = row < nch ? (double)row * kL : (double)(row - nch);
+  double sn, cs;
+  sincos(t * exp(-2.0 * (double)j / (double)rope_dim * log_base), &sn, &cs);
+  tab[idx] = make_float2((float)cs, (float)sn);
+}
+
 int linear_chunk() { return kL; }
+
+hipError_t launch_linear_rope_table(float2* tab, int T, int rope_dim, double base, hipStream_t stream) {
+  const int nch = (T + kL - 1) / kL;
+  const int64_t n = (int64_t)(nch + kL) * (rope_dim / 2);
+  hipLaunchKernelGGL(linear_rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, tab, nch,
+                     rope_dim, log(base));
+  return hipGetLastError();
+}
 int linear_scan_segment() { return kSegChunks; }
 
 hipError_t launch_linear_fwd(const LinearArgs& a, int dtype, hipStream_t stream) {

@@ -1299,7 +1299,8 @@ static rel_status check_rope(const rel_problem* p, int32_t rope_dim, float rope_
 }
 
 static size_t rope_table_bytes(const rel_problem* p, int32_t rope_dim) {
-  return rope_dim > 0 ? align256((size_t)p->T * (size_t)(rope_dim / 2) * 8) : 0;
+  const size_t rows = (size_t)linear_chunks(p) + (size_t)rel::linear_chunk();
+  return rope_dim > 0 ? align256(rows * (size_t)(rope_dim / 2) * 8) : 0;
 }
 
 size_t relation_linear_gated_fwd_workspace_bytes(const rel_problem* p, int32_t rope_dim) {
@@ -1308,13 +1309,13 @@ size_t relation_linear_gated_fwd_workspace_bytes(const rel_problem* p, int32_t r
   return plan_linear(p, false).total + rope_table_bytes(p, rope_dim);
 }
 
-// The RoPE table [T, rope_dim / 2] of (cos, sin) at workspace offset off, and
-// the kernels' view of it.
+// The RoPE table (cos, sin at the chunk starts and at the offsets inside a
+// chunk) at workspace offset off, and the kernels' view of it.
 static rel_status set_rope(rel::LinearArgs& a, const rel_problem* p, int32_t rope_dim, float rope_base, char* ws,
                            size_t off, hipStream_t stream) {
   if (rope_dim == 0) return REL_OK;
   float2* tab = (float2*)(ws + off);
-  const hipError_t e = rel::launch_rope_table(tab, (int)p->T, (int)rope_dim, (double)rope_base, stream);
+  const hipError_t e = rel::launch_linear_rope_table(tab, (int)p->T, (int)rope_dim, (double)rope_base, stream);
   if (e != hipSuccess) return hip_fail(e, "RoPE table launch");
   a.rope = tab;
   a.rope_half = rope_dim / 2;
