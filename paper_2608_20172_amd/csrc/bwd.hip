@@ -363,15 +363,23 @@ __global__ __launch_bounds__(kNT, (dq_occupancy<P, D>())) void bwd_dq_kernel(Bwd
 // with global atomics. The diagonal (Self) entry sits in dU, so dQ needs no
 // separate Self term; dself and the dlambda partials come from the diagonal
 // blocks here.
-template <class P, int D, int NW, bool FQ>
-__global__ __launch_bounds__(NW * 64, (dkdv_occupancy<P, D>())) void bwd_dkdv_kernel(BwdArgs a) {
+// CS = 2 (channel split, two-kernel path at D = 128): two waves share each 32
+// keys. Each forms U, dP, F and dU of one of the tile's two 32-query blocks,
+// the pair swap their packed F and dU through LDS, and each accumulates dK and
+// dV for half of the channels over both blocks. So a wave holds half of the
+// 128 accumulator registers of its keys, and two waves per SIMD fit where one
+// did (at one wave per SIMD a wave issues vector work at half the SIMD's rate).
+template <class P, int D, int NW, bool FQ, int CS = 1>
+__global__ __launch_bounds__(NW * 64, (CS == 2 ? 2 : dkdv_occupancy<P, D>())) void bwd_dkdv_kernel(BwdArgs a) {
   using E = typename P::T;
   using Op = typename P::Op;
   using PU = PolBF16<64>;                       // layout of the dU tile: 64 query columns
   constexpr int NT = NW * 64;
-  constexpr int KW = NW * 32;                   // keys per workgroup
+  constexpr int KW = NW * 32 / CS;              // keys per workgroup
   constexpr int KS = D / 16;
   constexpr int DB = D / 32;
+  constexpr int DBH = DB / CS;                  // 32-channel blocks of dK and dV per wave
+  static_assert(CS == 1 || (CS == 2 && !FQ && DB % 2 == 0), "channel split: two-kernel path, even channel blocks");
   constexpr int TB = kBQI * P::ROWB;            // one tensor tile (Q or dO)
   constexpr int NSEG = TB / 1024;
   constexpr int SEGW = 2 * NSEG / NW;
@@ -388,6 +396,10 @@ __global__ __launch_bounds__(NW * 64, (dkdv_occupancy<P, D>())) void bwd_dkdv_ke
   __shared__ __attribute__((aligned(1024))) unsigned char Kq[KQB];
   __shared__ __attribute__((aligned(1024))) unsigned char dUA[DUB];
   __shared__ __attribute__((aligned(1024))) unsigned char dUB[DUB];
+  // CS: per key group and query block, the packed F and dU operands (two
+  // 16-row halves each) of the wave that formed them, one 16-byte lane slot each
+  constexpr int XCH = CS == 2 ? (KW / 32) * 2 * 4 * 64 * 16 : 16;
+  __shared__ __attribute__((aligned(1024))) unsigned char Xch[XCH];
   __shared__ float red[NT];
 
   const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
@@ -425,7 +437,8 @@ __global__ __launch_bounds__(NW * 64, (dkdv_occupancy<P, D>())) void bwd_dkdv_ke
   const float lam = *a.lambda;
 
   const int j0 = kt * KW;
-  const int kw0 = j0 + 32 * w;        // first key of this wave
+  const int kgw = w / CS, chw = w % CS;  // key group; with CS, the query block and channel half of the wave
+  const int kw0 = j0 + 32 * kgw;      // first key of this wave
   const int kj = kw0 + n;             // this lane's key
   const bool wave_keys = kw0 < T;
 
@@ -467,9 +480,9 @@ __global__ __launch_bounds__(NW * 64, (dkdv_occupancy<P, D>())) void bwd_dkdv_ke
     vop[ks] = kj < T ? P::row_op_g(v + kj * st, ks, L) : Op{};
   }
 
-  floatx16 dKt[DB], dVt[DB];
+  floatx16 dKt[DBH], dVt[DBH];
 #pragma unroll
-  for (int db = 0; db < DB; ++db) {
+  for (int db = 0; db < DBH; ++db) {
     dKt[db] = floatx16{};
     dVt[db] = floatx16{};
   }
@@ -561,18 +574,23 @@ __global__ __launch_bounds__(NW * 64, (dkdv_occupancy<P, D>())) void bwd_dkdv_ke
       uop[hh] = P::pack(u8);
     }
   };
-  // dV += F^T dO and dK += dU^T Q for query block qb
-  auto accum = [&](const unsigned char* buf, int qb, const Op (&fop)[2], const Op (&uop)[2]) {
+  // dV += F^T dO and dK += dU^T Q for 16-row half hh of query block qb (the wave's channels)
+  auto accum_half = [&](const unsigned char* buf, int qb, int hh, const Op& fop, const Op& uop) {
     const unsigned char* Qs = buf;
     const unsigned char* dOs = buf + TB;
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        dVt[db] = P::mma(P::col_op(dOs, 2 * qb + hh, 32 * db, L), fop[hh], dVt[db]);
-        dKt[db] = P::mma(P::col_op(Qs, 2 * qb + hh, 32 * db, L), uop[hh], dKt[db]);
-      }
+    for (int db = 0; db < DBH; ++db) {
+      const int c0 = 32 * (db + chw * DBH);
+      dVt[db] = P::mma(P::col_op(dOs, 2 * qb + hh, c0, L), fop, dVt[db]);
+      dKt[db] = P::mma(P::col_op(Qs, 2 * qb + hh, c0, L), uop, dKt[db]);
+    }
   };
+  auto accum = [&](const unsigned char* buf, int qb, const Op (&fop)[2], const Op (&uop)[2]) {
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) accum_half(buf, qb, hh, fop[hh], uop[hh]);
+  };
+  // CS: slot of operand k (0, 1: F halves; 2, 3: dU halves) of query block qb of the wave's key group
+  auto xslot = [&](int qb, int k) { return (uintx4*)(Xch + ((((kgw * 2 + qb) * 4 + k) * 64) + lane) * 16); };
 
   // fused: dU of one query block (rows 32 qb .. of the tile) into the LDS dU
   // tile, row = key, column = query position. Positions within each block are
@@ -646,6 +664,31 @@ __global__ __launch_bounds__(NW * 64, (dkdv_occupancy<P, D>())) void bwd_dkdv_ke
       dq_tile(dUr, i0 - kBQI);
       __builtin_amdgcn_sched_barrier(0);
     }
+    if constexpr (CS == 2) {
+      // this wave's query block: its F and dU, swapped with the partner's
+      const int qm = i0 + 32 * chw;
+      floatx16 sm, dpm;
+      Op fm[2] = {Op{}, Op{}}, um[2] = {Op{}, Op{}};
+      if (qm >= kfirst && qm < T) {
+        evid(buf, chw, sm, dpm);
+        if (qm == kfirst) grads(buf, chw, sm, dpm, fm, um, std::true_type{});
+        else grads(buf, chw, sm, dpm, fm, um, std::false_type{});
+      }
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        *xslot(chw, hh) = __builtin_bit_cast(uintx4, fm[hh]);
+        *xslot(chw, 2 + hh) = __builtin_bit_cast(uintx4, um[hh]);
+      }
+      accum(buf, chw, fm, um);  // its own block first: these products run while the partner catches up
+      __syncthreads();
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {  // the partner's block, one 16-row half at a time
+        const Op fo = __builtin_bit_cast(Op, *xslot(1 - chw, hh));
+        const Op uo = __builtin_bit_cast(Op, *xslot(1 - chw, 2 + hh));
+        accum_half(buf, 1 - chw, hh, fo, uo);
+      }
+      return;
+    }
     const int q0 = i0, q1 = i0 + 32;
     const bool live0 = q0 >= kfirst && q0 < T, live1 = q1 >= kfirst && q1 < T;
     floatx16 s0, dp0, s1, dp1;
@@ -713,9 +756,13 @@ __global__ __launch_bounds__(NW * 64, (dkdv_occupancy<P, D>())) void bwd_dkdv_ke
   };
   const int qf0 = min(qt0 + KW / kBQI, nqt);  // tiles with the workgroup's diagonals
   const int qf1 = max(qf0, T / kBQI);           // full tiles end here
-  run(qt0, qf0, step);
-  run(qf0, qf1, full);
-  run(qf1, nqt, step);
+  if constexpr (CS == 2) {
+    run(qt0, nqt, step);
+  } else {
+    run(qt0, qf0, step);
+    run(qf0, qf1, full);
+    run(qf1, nqt, step);
+  }
   if constexpr (FQ) {
     // the last tile's dQ, and this workgroup's dlambda partial in a fixed order
     __syncthreads();
@@ -737,10 +784,10 @@ __global__ __launch_bounds__(NW * 64, (dkdv_occupancy<P, D>())) void bwd_dkdv_ke
     E* dk = (E*)a.dk + hoff;
     E* dv = (E*)a.dv + hoff;
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
+    for (int db = 0; db < DBH; ++db)
 #pragma unroll
       for (int rq = 0; rq < 4; ++rq) {
-        const int d0 = 32 * db + 8 * rq + 4 * g;
+        const int d0 = 32 * (db + chw * DBH) + 8 * rq + 4 * g;
         floatx4 kk, vv;
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
@@ -822,6 +869,12 @@ __global__ __launch_bounds__(kRowNT) void bwd_dq_convert_kernel(BwdArgs a) {
   *(bf16x8*)((bf16*)a.dq + row_offset(a, r) + 8 * c) = y;
 }
 
+// The two-kernel dK/dV kernel runs with its channels split over wave pairs
+// (CS = 2, 8 waves for 128 keys) at bf16 D = 128, where one wave's dK and dV
+// accumulators would take 128 registers.
+template <class P, int D>
+constexpr bool kSplitChannels = sizeof(typename P::T) == 2 && D == 128;
+
 template <class P, int D>
 void launch_pair(const BwdArgs& a, const TileMap& mkv, const TileMap& mq, hipStream_t stream,
                  hipEvent_t* prof) {
@@ -838,7 +891,11 @@ void launch_pair(const BwdArgs& a, const TileMap& mkv, const TileMap& mq, hipStr
   b.map = mkv;
   const bool p_kv = !p_all && profile_slot("bwd_dkdv", &e0, &e1);
   if (p_kv) (void)hipEventRecord(e0, stream);
-  hipLaunchKernelGGL((bwd_dkdv_kernel<P, D, 4, false>), dim3((unsigned)grid_size(mkv)), dim3(kNT), 0, stream, b);
+  if constexpr (kSplitChannels<P, D>) {
+    hipLaunchKernelGGL((bwd_dkdv_kernel<P, D, 8, false, 2>), dim3((unsigned)grid_size(mkv)), dim3(512), 0, stream, b);
+  } else {
+    hipLaunchKernelGGL((bwd_dkdv_kernel<P, D, 4, false>), dim3((unsigned)grid_size(mkv)), dim3(kNT), 0, stream, b);
+  }
   if (p_kv) (void)hipEventRecord(e1, stream);
   if (p_all) (void)hipEventRecord(prof[1], stream);
 }
