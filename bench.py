@@ -423,7 +423,7 @@ def linear_leg(K: int) -> list:
             fwd()
             R.relation_linear_bwd(p1, p2, v, g, dy, workspace=bws)
 
-        # the same step as the paper's layer runs it: the retention gate of eq. 9
+        # the same step as the paper's layer runs it: the retention gate of eq. 15
         # formed in the kernels and RoPE on p1, p2 (over the paper's width 80
         # when the heads are 80 padded to 128)
         rope_dim = 80 if D == 128 else D

@@ -337,7 +337,7 @@ rel_status relation_decode_merge(const rel_problem* p, int32_t nstates, const fl
  *   p1, p2     [B,H,T,D] dtype: the two relation coordinates after RoPE.
  *   v          [B,H,T,D] dtype: the information state I~.
  *   g          [B,H,T,D] fp32, dense: log-retention g_t = log alpha_t <= 0 (the
- *              gate of eq. 9 is the caller's elementwise map; positive values
+ *              gate of eq. 15 is the caller's elementwise map; positive values
  *              are not checked and grow the state).
  *   out        [B,H,T,D] dtype: y.
  *   state_out  [B,H,D,D] fp32, optional: C_T, the decode state after the last
@@ -373,7 +373,7 @@ rel_status relation_linear_bwd(const rel_problem* p, const void* p1, const void*
                                void* workspace, size_t workspace_bytes, void* stream);
 
 /* Linear Relation as the paper's layer runs it (Sec. 5.2, App. A.4), with the
- * retention gate of eq. 9 formed inside the kernels,
+ * retention gate of eq. 15 formed inside the kernels,
  *   g_t = -exp(A_log) * softplus(r_t + dt_bias),  alpha_t = exp(g_t) in (0, 1],
  * in place of a caller-made g, and optionally the RoPE of Sec. 3.1 on p1 and p2
  * before S_t and the normalised coordinates are formed.

@@ -16,7 +16,7 @@ One head, tokens t = 1..T, inputs after RoPE (App. B):
 The oracle runs this recurrence token by token (``forward``) and its exact
 adjoint token by token in reverse (``backward``).
 
-The retention gate of eq. 9 (``kda_gate``) maps the pre-activation r_t and
+The retention gate of eq. 15 (``kda_gate``) maps the pre-activation r_t and
 the per-channel parameters A_log, dt_bias to g_t = log alpha_t; ``forward``
 and ``backward`` take g_t itself, and ``kda_gate_backward`` carries dg on to
 r, A_log and dt_bias.
@@ -126,7 +126,7 @@ def backward(p1, p2, v, g, dY, *, tau_s: float = TAU_S, scale=None) -> dict:
 
 
 def kda_gate(r, a_log, dt_bias) -> np.ndarray:
-    """Log-retention of eq. 9: g_t = -exp(A_log) * softplus(r_t + dt_bias)
+    """Log-retention of eq. 15: g_t = -exp(A_log) * softplus(r_t + dt_bias)
     elementwise, r of shape [..., D] and A_log, dt_bias of shape [D]. Since
     exp > 0 and softplus > 0, g < 0 and alpha = exp(g) lies in (0, 1]."""
     r, a_log, dt_bias = (np.asarray(x, np.float64) for x in (r, a_log, dt_bias))
@@ -135,7 +135,7 @@ def kda_gate(r, a_log, dt_bias) -> np.ndarray:
 
 
 def kda_gate_backward(r, a_log, dt_bias, dg) -> dict:
-    """Gradients through eq. 9 given dg = dL/dg_t (shape of r): softplus' is
+    """Gradients through eq. 15 given dg = dL/dg_t (shape of r): softplus' is
     the logistic sigmoid, so dr = dg * (-exp(A_log) sigmoid(r + dt_bias));
     dt_bias enters as r does, so d dt_bias is dr summed over every axis but
     the channel; and d g / d A_log = g, so d A_log sums dg * g the same way."""

@@ -544,7 +544,7 @@ def _gate_params(a_log, dt_bias, p1):
 def relation_linear_gated_fwd(p1, p2, v, r, a_log, dt_bias, *, rope_dim: int = 0, rope_base: float = 1.0e4,
                               tau_s: float = TAU_S, scale: Optional[float] = None, want_state: bool = False,
                               workspace=None):
-    """Linear Relation forward with the retention gate of eq. 9 formed in the
+    """Linear Relation forward with the retention gate of eq. 15 formed in the
     kernels from r ([B, H, T, D] fp32) and a_log, dt_bias ([H, D] fp32), and
     RoPE over the first rope_dim channels of p1, p2 (0: none).
     Returns dict(o, state)."""

@@ -164,7 +164,7 @@ struct LinearArgs {
   // virtual head 4 n + 2 A + E with its own chunk states. A row pass forms qt
   // and kt over all 128 channels first; another sums the sub-problems' partial
   // gradients and takes them through S and the normalisation.
-  // The retention gate of eq. 9 inside the kernels: with a_log set, g holds
+  // The retention gate of eq. 15 inside the kernels: with a_log set, g holds
   // the gate's pre-activation r and the chunk loads form
   // g = -exp(A_log) softplus(r + dt_bias); the backward's dg then goes on to
   // dr (in place), dA_log and d dt_bias.

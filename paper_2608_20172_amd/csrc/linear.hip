@@ -13,8 +13,11 @@
 // Forward launches: per chunk the state contribution (dC, gamma = e^{b_last});
 // the scan over chunks in segments (the state entering every chunk); per chunk
 // the output. All arithmetic is fp32: dense products on the matrix cores
-// (fp32 MFMA), the decay weights and the diagonal sub-blocks of the intra-chunk
-// pairs on the vector units.
+// (fp32 MFMA), the decay weights on the vector units, and the diagonal
+// sub-blocks of the intra-chunk pairs on the matrix cores where the chunk's
+// decay lets them be factored, else term by term on the vector units. With
+// the gated entry points the kernels also form g from the KDA gate and rotate
+// p1, p2 with RoPE as they load a chunk (and take both back in the gradient).
 #include "kernels.h"
 #include "lanes.h"
 
@@ -82,7 +85,7 @@ __device__ __forceinline__ float2 rope_cs(const LinearArgs& a, int64_t t, int j)
   return make_float2(A.x * B.x - A.y * B.y, A.y * B.x + A.x * B.y);
 }
 
-// The retention gate of eq. 9: g = -exp(A_log) softplus(r + dt_bias), with
+// The retention gate of eq. 15: g = -exp(A_log) softplus(r + dt_bias), with
 // ea = exp(A_log) of the channel.
 __device__ __forceinline__ float kda_gate(float r, float ea, float dtb) { return -ea * softplus_f(r + dtb); }
 
@@ -155,8 +158,11 @@ template <> struct Vec4<float> {
 // the sequence are zero), v, optionally dY, and b = running sum of g (zero g
 // past the end, so b stays at its last value). SWZ_VD stores v and dY
 // swizzled (swz), SWZ_QKB qt, kt and b; qt may be null (not stored). One wave
-// per row for the norms and S. SPLIT: qt and kt are read as formed (fp32, from
-// qn and kn) and the chunk holds the sub-problem's halves of the channels.
+// per row for the norms and S. With a.a_log the g read is the gate's
+// pre-activation r and g = kda_gate(r); with a.rope qt and kt are rotated
+// after S and the norms are formed (neither changes under the rotation).
+// SPLIT: qt and kt are read as formed (fp32, from qn and kn, already rotated)
+// and the chunk holds the sub-problem's halves of the channels.
 template <typename TI, int D, int NT, bool SWZ_VD = false, bool WITH_DY = false, bool SWZ_QKB = false,
           bool SPLIT = false>
 __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& p, float (*qt)[D], float (*kt)[D],
@@ -1105,7 +1111,7 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
     const float base_g = extra + dgam * fast_exp2(bb[kL - 1][swz<D>(kL - 1, d)] * kLog2e) + later;
     float* dG = SPLIT ? a.part + (6 + ie) * plane + (int64_t)hr.n * a.T * GW + hr.pa : a.dg + (int64_t)p.n * a.T * D;
     if (!SPLIT && a.a_log) {
-      // the retention gate of eq. 9 (g = -exp(A_log) softplus(r + dt_bias)):
+      // the retention gate of eq. 15 (g = -exp(A_log) softplus(r + dt_bias)):
       // dr = dg (-exp(A_log) sigmoid(r + dt_bias)) goes out in place of dg, and
       // the chunk's per-channel sums of dg g and dr (its shares of dA_log and
       // d dt_bias) meet over the segments in LDS, in a fixed order
@@ -1445,7 +1451,7 @@ hipError_t launch_bwd_split(const LinearArgs& a, hipStream_t stream) {
 }
 
 // ---------------------------------------------------------------------------
-// Backward through the retention gate of eq. 9 at width 128, after the
+// Backward through the retention gate of eq. 15 at width 128, after the
 // combine pass has left dg in a.dg: per element dr = dg (-exp(A_log)
 // sigmoid(r + dt_bias)), written over dg; per head, token segment and channel
 // the sums of dg g (d A_log, since dg/dA_log = g) and of dr (d dt_bias). Then,

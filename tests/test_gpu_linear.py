@@ -243,7 +243,7 @@ def _assert_param_grad(name, x, ref, terms, dtype):
     (2, 1, 129, 128, "f32", -1.0), (1, 2, 1, 64, "bf16", 0.0), (1, 1, 600, 64, "f32", -4.0),
 ])
 def test_linear_gated(B, H, T, D, dtype, a_mean):
-    """The retention gate of eq. 9 formed in the kernels: y and the state, then
+    """The retention gate of eq. 15 formed in the kernels: y and the state, then
     dp1, dp2, dv, dr and the per-channel dA_log, d dt_bias, against the oracle's
     gate composed with its recurrence (the gate's adjoint fed the recurrence's
     dg)."""

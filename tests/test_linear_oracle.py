@@ -94,7 +94,7 @@ def check_gradients_fd(lo):
 
 
 def check_gate_closed_forms(lo):
-    """Eq. 9 at points where softplus is known: softplus(0) = ln 2, softplus(x)
+    """Eq. 15 at points where softplus is known: softplus(0) = ln 2, softplus(x)
     tends to x for large x and to e^x for very negative x; g < 0 everywhere
     and alpha = exp(g) in (0, 1]; A_log scales g by e^A_log."""
     D = 4
@@ -114,7 +114,7 @@ def check_gate_closed_forms(lo):
 
 
 def check_gate_gradients_fd(lo):
-    """The chain through eq. 9 and the recurrence: dr, dA_log and ddt_bias from
+    """The chain through eq. 15 and the recurrence: dr, dA_log and ddt_bias from
     kda_gate_backward (fed dg from the recurrence's adjoint) against central
     differences of sum(dY * Y) with g = kda_gate(r, A_log, dt_bias)."""
     h = 1e-6
