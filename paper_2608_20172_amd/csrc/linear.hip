@@ -12,10 +12,12 @@
 // Every exponent is <= 0 (g <= 0), so nothing overflows, whatever the decay.
 // Forward launches: per chunk the state contribution (dC, gamma = e^{b_last});
 // the scan over chunks in segments (the state entering every chunk); per chunk
-// the output. All arithmetic is fp32: dense products on the matrix cores
-// (fp32 MFMA), the decay weights on the vector units, and the diagonal
-// sub-blocks of the intra-chunk pairs on the matrix cores where the chunk's
-// decay lets them be factored, else term by term on the vector units. With
+// the output. Dense products run on the matrix cores (fp32 MFMA for fp32
+// inputs; for bf16 inputs bf16 MFMA with fp32 accumulation, except in the
+// backward's products that reach the decay gradient), the decay weights on
+// the vector units in fp32, and the diagonal sub-blocks of the intra-chunk
+// pairs on the matrix cores where the chunk's decay lets them be factored,
+// else term by term on the vector units. With
 // the gated entry points the kernels also form g from the KDA gate and rotate
 // p1, p2 with RoPE as they load a chunk (and take both back in the gradient).
 #include "kernels.h"
@@ -362,19 +364,74 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
   __syncthreads();
 }
 
+// Matrix-core operands. With fp32 inputs every product runs on fp32 MFMA
+// steps. With bf16 inputs (BF) the operands, formed in fp32, are rounded to
+// bf16 and the products run on bf16 MFMA steps with fp32 accumulation, eight
+// fp32 steps' worth of contraction per instruction. A lane supplies the values
+// of its row of the left operand and of its column of the right operand at the
+// same contraction indices; which indices go to which lane and slot does not
+// matter to the sum, so each lane keeps the index range it has on the fp32 path.
+// The backward keeps fp32 steps for every product that reaches the gradient
+// of the decay (dq, dk, and the states C0 and G): that gradient is a small
+// difference of large terms (the scores depend on b only through b_t - b_j,
+// so the intra-chunk parts of qt dq and kt dk cancel over a chunk), and
+// operands rounded to bf16 leave a residual of their rounding in it that adds
+// up coherently over the tokens in dA_log.
+template <typename TI> constexpr bool kBF = sizeof(TI) == 2;
+
+template <int N>
+__device__ __forceinline__ void pack_bf16(const float* x, __bf16 __attribute__((ext_vector_type(N))) & o) {
+#pragma unroll
+  for (int t = 0; t < N; ++t) o[t] = (bf16)x[t];
+}
+__device__ __forceinline__ floatx4 mfma16b(const float (&a)[8], const float (&b)[8], const floatx4& c) {
+  bf16x8 x, y;
+  pack_bf16<8>(a, x);
+  pack_bf16<8>(b, y);
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(x, y, c, 0, 0, 0);
+}
+__device__ __forceinline__ floatx4 mfma16b4(const float (&a)[4], const float (&b)[4], const floatx4& c) {
+  bf16x4 x, y;
+  pack_bf16<4>(a, x);
+  pack_bf16<4>(b, y);
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(shortx4, x), __builtin_bit_cast(shortx4, y), c,
+                                                   0, 0, 0);
+}
+__device__ __forceinline__ floatx16 mfma32b(const float (&a)[8], const float (&b)[8], const floatx16& c) {
+  bf16x8 x, y;
+  pack_bf16<8>(a, x);
+  pack_bf16<8>(b, y);
+  return mfma32(x, y, c);
+}
+
 // One 32 x 32 block (rows ab.., columns eb..) of X^T Y, the contraction over
 // the kL rows of the chunk (X, Y plain [kL][D] arrays), on the matrix cores
-// (32x32x2 fp32 steps; lane group g takes the rows of parity g).
-template <int D>
+// (lane group g takes the rows of parity g: 32x32x2 fp32 steps, or 32x32x16
+// bf16 steps of eight such rows with BF).
+template <int D, bool BF = false>
 __device__ __forceinline__ floatx16 gram_block(const float (*X)[D], const float (*Y)[D], int ab, int eb) {
   const int lane = threadIdx.x & 63, ln = lane & 31, lg = lane >> 5;
   floatx16 acc;
 #pragma unroll
   for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
+  if constexpr (BF) {
+#pragma unroll
+    for (int s = 0; s < kL / 16; ++s) {
+      float x[8], y[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int r = 16 * s + 2 * u + lg;
+        x[u] = X[r][ab + ln];
+        y[u] = Y[r][eb + ln];
+      }
+      acc = mfma32b(x, y, acc);
+    }
+  } else {
 #pragma unroll 8
-  for (int s2 = 0; s2 < kL / 2; ++s2) {
-    const int r = 2 * s2 + lg;
-    acc = mfma32f(X[r][ab + ln], Y[r][eb + ln], acc);
+    for (int s2 = 0; s2 < kL / 2; ++s2) {
+      const int r = 2 * s2 + lg;
+      acc = mfma32f(X[r][ab + ln], Y[r][eb + ln], acc);
+    }
   }
   return acc;
 }
@@ -406,7 +463,7 @@ __global__ __launch_bounds__(kLT) void linear_state_kernel(LinearArgs a) {
   constexpr int NBE = D / 32;
   for (int bk = __builtin_amdgcn_readfirstlane(tid >> 6); bk < NBE * NBE; bk += kLT / 64) {
     const int ab = 32 * (bk / NBE), eb = 32 * (bk % NBE);
-    store_block<D>(a.dstate + base * D * D, gram_block<D>(kt, vv, ab, eb), ab, eb);
+    store_block<D>(a.dstate + base * D * D, gram_block<D, kBF<TI>>(kt, vv, ab, eb), ab, eb);
   }
 }
 
@@ -491,20 +548,40 @@ hipError_t launch_state_scan(const LinearArgs& a, int reverse, hipStream_t strea
 
 // acc += one 32 x 32 block (rows rb.., columns cb..) of a product X B whose
 // contraction runs over the K columns of X, on the matrix cores (32x32x2 fp32
-// steps). X is a swizzled (swz) row-major [kL][K] array; B(k, j) gives the
-// column operand. Lane group g takes the contraction indices K/2 g ..
-// K/2 g + K/2 - 1 in order, four per 16-byte read of its row of X.
-template <int K, typename ColOp>
+// steps, or 32x32x16 bf16 steps with BF). X is a swizzled (swz) row-major
+// [kL][K] array; B(k, j) gives the column operand. Lane group g takes the
+// contraction indices K/2 g .. K/2 g + K/2 - 1 in order, four per 16-byte read
+// of its row of X.
+template <int K, bool BF = false, typename ColOp>
 __device__ __forceinline__ floatx16 block_product(const float (*X)[K], int rb, int cb, floatx16 acc, ColOp B) {
   constexpr int KH = K / 2;
   const int lane = threadIdx.x & 63, ln = lane & 31, lg = lane >> 5;
   const int xr = rb + ln;
+  if constexpr (BF) {
+    static_assert(KH % 8 == 0, "whole bf16 steps");
 #pragma unroll 2
-  for (int s0 = 0; s0 < KH; s0 += 4) {
-    const int kk = KH * lg + s0;
-    const floatx4 xa = *reinterpret_cast<const floatx4*>(&X[xr][swz<K>(xr, kk)]);
+    for (int s0 = 0; s0 < KH; s0 += 8) {
+      const int kk = KH * lg + s0;
+      const floatx4 x0 = *reinterpret_cast<const floatx4*>(&X[xr][swz<K>(xr, kk)]);
+      const floatx4 x1 = *reinterpret_cast<const floatx4*>(&X[xr][swz<K>(xr, kk + 4)]);
+      float xa[8], xb[8];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) acc = mfma32f(xa[u], B(kk + u, cb + ln), acc);
+      for (int u = 0; u < 4; ++u) {
+        xa[u] = x0[u];
+        xa[4 + u] = x1[u];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) xb[u] = B(kk + u, cb + ln);
+      acc = mfma32b(xa, xb, acc);
+    }
+  } else {
+#pragma unroll 2
+    for (int s0 = 0; s0 < KH; s0 += 4) {
+      const int kk = KH * lg + s0;
+      const floatx4 xa = *reinterpret_cast<const floatx4*>(&X[xr][swz<K>(xr, kk)]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc = mfma32f(xa[u], B(kk + u, cb + ln), acc);
+    }
   }
   return acc;
 }
@@ -559,30 +636,46 @@ __device__ __forceinline__ bool diag_factorable(const float (*bb)[D]) {
 // j >= t set to zero; otherwise it is summed term by term on the vector units.
 // Waves 0-3 of the workgroup: diagonal block w; waves 4-7: blocks w - 4 and w
 // (of the six below the diagonal). With TRANS the scores go to A as A^T (A[j][t]).
-template <int D>
+template <int D, bool BF = false>
 __device__ __forceinline__ floatx4 scaled_block(const float (*qt)[D], const float (*kt)[D], const float (*bb)[D],
                                                 int tb, int jb, int rf) {
   constexpr int CH = D / 4;
   const int lane = threadIdx.x & 63, i = lane & 15, g = lane >> 4;
   const int tr = 16 * tb + i, jr = 16 * jb + i;
   floatx4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-  // lane group g takes the channel chunks CH/4 g .. CH/4 g + CH/4 - 1
-#pragma unroll 2
-  for (int c0 = 0; c0 < CH / 4; ++c0) {
-    const int c = (CH / 4) * g + c0;
+  // the scaled operands of channel chunk c (4 channels)
+  auto operands = [&](int c, float* qa, float* kb) {
     const floatx4 q4 = ld4<D>(qt, tr, c), bt4 = ld4<D>(bb, tr, c), br4 = ld4<D>(bb, rf, c);
     const floatx4 k4 = ld4<D>(kt, jr, c), bj4 = ld4<D>(bb, jr, c);
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const float qa = q4[u] * fast_exp2((bt4[u] - br4[u]) * kLog2e);
-      const float kb = k4[u] * fast_exp2((br4[u] - bj4[u]) * kLog2e);
-      acc = mfma16f(qa, kb, acc);
+      qa[u] = q4[u] * fast_exp2((bt4[u] - br4[u]) * kLog2e);
+      kb[u] = k4[u] * fast_exp2((br4[u] - bj4[u]) * kLog2e);
+    }
+  };
+  // lane group g takes the channel chunks CH/4 g .. CH/4 g + CH/4 - 1
+  if constexpr (BF) {
+    static_assert(CH % 8 == 0, "two chunks per bf16 step");
+#pragma unroll 2
+    for (int c0 = 0; c0 < CH / 4; c0 += 2) {
+      float qa[8], kb[8];
+      operands((CH / 4) * g + c0, qa, kb);
+      operands((CH / 4) * g + c0 + 1, qa + 4, kb + 4);
+      acc = mfma16b(qa, kb, acc);
+    }
+  } else {
+#pragma unroll 2
+    for (int c0 = 0; c0 < CH / 4; ++c0) {
+      float qa[4], kb[4];
+      operands((CH / 4) * g + c0, qa, kb);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc = mfma16f(qa[u], kb[u], acc);
     }
   }
   return acc;
 }
 
-template <int D, bool TRANS = false>
+template <int D, bool TRANS = false, bool BF = false>
 __device__ __forceinline__ void chunk_scores(const float (*qt)[D], const float (*kt)[D], const float (*bb)[D],
                                              float (*A)[kL], bool fact) {
   constexpr int SB = 16, NSB = kL / SB, CH = D / 4;
@@ -594,7 +687,7 @@ __device__ __forceinline__ void chunk_scores(const float (*qt)[D], const float (
   };
   if (w < NSB && fact) {
     const int i = lane & 15, g = lane >> 4;
-    const floatx4 acc = scaled_block<D>(qt, kt, bb, w, w, SB * w);
+    const floatx4 acc = scaled_block<D, BF>(qt, kt, bb, w, w, SB * w);
 #pragma unroll
     for (int v = 0; v < 4; ++v) put(SB * w + 4 * g + v, SB * w + i, i < 4 * g + v ? acc[v] : 0.0f);
     for (int jb = w + 1; jb < NSB; ++jb) {  // the blocks above the diagonal in the row band are zero
@@ -649,7 +742,7 @@ __device__ __forceinline__ void chunk_scores(const float (*qt)[D], const float (
       // blocks below the diagonal, bi = 0..5: (1,0) (2,0) (3,0) (2,1) (3,1) (3,2)
       const int jb = bi < 3 ? 0 : bi < 5 ? 1 : 2;
       const int tb = jb + 1 + (bi < 3 ? bi : bi < 5 ? bi - 3 : 0);
-      const floatx4 acc = scaled_block<D>(qt, kt, bb, tb, jb, SB * jb + SB - 1);
+      const floatx4 acc = scaled_block<D, BF>(qt, kt, bb, tb, jb, SB * jb + SB - 1);
       // register v of lane (i, g): row 4 g + v, column i of the block
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
@@ -682,7 +775,7 @@ __global__ __launch_bounds__(kLT2) void linear_out_kernel(LinearArgs a) {
     for (int k = 0; k < NC0; ++k) c0r[k] = C0[tid + k * kLT2];
   }
   load_chunk<TI, D, kLT2, false, false, true>(a, p, qt, kt, vv, bb, nullptr);
-  chunk_scores<D>(qt, kt, bb, A, diag_factorable<D>(bb));
+  chunk_scores<D, false, kBF<TI>>(qt, kt, bb, A, diag_factorable<D>(bb));
   __syncthreads();
   // Qe = qt e^{b} (the inter read's query), over kt; all three swizzled alike
   for (int i = tid; i < kL * D; i += kLT2) {
@@ -709,9 +802,9 @@ __global__ __launch_bounds__(kLT2) void linear_out_kernel(LinearArgs a) {
   const int rb = 32 * (blk / NBC), cb = 32 * (blk % NBC);
   const bool busy = w < (SPLIT ? 2 * NB : NB);
   floatx16 acc = zero16();
-  if (busy && part == 0) acc = block_product<kL>(A, rb, cb, acc, [&](int k, int j) { return vv[k][j]; });
+  if (busy && part == 0) acc = block_product<kL, kBF<TI>>(A, rb, cb, acc, [&](int k, int j) { return vv[k][j]; });
   if (busy && (!SPLIT || part == 1))
-    acc = block_product<D>(kt, rb, cb, acc, [&](int k, int j) { return C0s[k * D + j]; });
+    acc = block_product<D, kBF<TI>>(kt, rb, cb, acc, [&](int k, int j) { return C0s[k * D + j]; });
   float* Ap = &A[0][0];
   if constexpr (SPLIT) {
     __syncthreads();  // every operand of A read
@@ -769,26 +862,56 @@ __global__ __launch_bounds__(kLT) void linear_bstate_kernel(LinearArgs a) {
   constexpr int NBE = D / 32, NBB = NBE * NBE;
   for (int bk = __builtin_amdgcn_readfirstlane(tid >> 6); bk < 2 * NBB; bk += kLT / 64) {
     const int ab = 32 * ((bk % NBB) / NBE), eb = 32 * (bk % NBE);
+    // fp32 steps at any input type: C0 and G reach the decay gradient
     if (bk < NBB) store_block<D>(a.dstate + base * D * D, gram_block<D>(kt, vv, ab, eb), ab, eb);
     else store_block<D>(a.pstate + base * D * D, gram_block<D>(qt, dy, ab, eb), ab, eb);
   }
 }
 
-// One 16 x 16 tile of a product on the matrix cores (16x16x4 fp32 steps):
+// One 16 x 16 tile of a product on the matrix cores (16x16x4 fp32 steps; with
+// BF, 16x16x32 bf16 steps and a 16x16x16 one for a remainder of four indices):
 // acc[v] of lane (i, g) = sum over k in [k0, k0 + K) of X[r0 + i][k] B(k, c0 + ...)
 // for output row r0 + 4 g + v and column c0 + i. X is a swizzled [kL][W]
 // array; B(k, j) gives the column operand. K is a multiple of 16 and k0 of 4;
 // lane group g takes the indices k0 + K/4 g .. k0 + K/4 g + K/4 - 1.
-template <int W, typename ColOp>
+template <int W, bool BF = false, typename ColOp>
 __device__ __forceinline__ floatx4 tile_product(const float (*X)[W], int r0, int c0, int k0, int K, ColOp B) {
   const int lane = threadIdx.x & 63, i = lane & 15, g = lane >> 4;
   const int kq = K >> 2, xr = r0 + i;
   floatx4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-  for (int s0 = 0; s0 < kq; s0 += 4) {
-    const int k = k0 + kq * g + s0;
-    const floatx4 xa = ld4<W>(X, xr, k >> 2);
+  if constexpr (BF) {
+    int s0 = 0;
+    for (; s0 + 8 <= kq; s0 += 8) {
+      const int k = k0 + kq * g + s0;
+      const floatx4 x0 = ld4<W>(X, xr, k >> 2), x1 = ld4<W>(X, xr, (k >> 2) + 1);
+      float xa[8], xb[8];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) acc = mfma16f(xa[u], B(k + u, c0 + i), acc);
+      for (int u = 0; u < 4; ++u) {
+        xa[u] = x0[u];
+        xa[4 + u] = x1[u];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) xb[u] = B(k + u, c0 + i);
+      acc = mfma16b(xa, xb, acc);
+    }
+    if (s0 < kq) {  // four indices left (K / 4 is a multiple of 4)
+      const int k = k0 + kq * g + s0;
+      const floatx4 x0 = ld4<W>(X, xr, k >> 2);
+      float xa[4], xb[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        xa[u] = x0[u];
+        xb[u] = B(k + u, c0 + i);
+      }
+      acc = mfma16b4(xa, xb, acc);
+    }
+  } else {
+    for (int s0 = 0; s0 < kq; s0 += 4) {
+      const int k = k0 + kq * g + s0;
+      const floatx4 xa = ld4<W>(X, xr, k >> 2);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc = mfma16f(xa[u], B(k + u, c0 + i), acc);
+    }
   }
   return acc;
 }
@@ -852,7 +975,7 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
   const bool fact = diag_factorable<D>(bb);
   // ---- scores and dA: waves 0-7 the scores (to M0 as A^T), waves 8-15 dA
   if (w < 8) {
-    chunk_scores<D, true>(qt, kt, bb, M0, fact);
+    chunk_scores<D, true, kBF<TI>>(qt, kt, bb, M0, fact);
   } else {
     // the ten blocks (tb, jb) with jb <= tb; wave 8 + i takes blocks i and i + 8
     const int i = lane & 15, g = lane >> 4;
@@ -862,7 +985,7 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
         jb -= tb + 1;
         ++tb;
       }
-      const floatx4 acc = tile_product<D>(dy, SB * tb, SB * jb, 0, D, [&](int k, int j) { return vv[j][swz<D>(j, k)]; });
+      const floatx4 acc = tile_product<D, kBF<TI>>(dy, SB * tb, SB * jb, 0, D, [&](int k, int j) { return vv[j][swz<D>(j, k)]; });
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int t = SB * tb + 4 * g + v, j = SB * jb + i;
@@ -880,6 +1003,7 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
   //   type 2 (3 NE, 4 NE with FACT): dk_intra[j][d] = e^{b_rf - b_j} sum_t dA^T[j][t] qt[t][d] e^{b_t - b_rf},
   //     rf = 16 jb + 15, over t > rf or t >= 16 jb (FACT)
   // dA is zero for j >= t, so the diagonal blocks' upper triangles add nothing.
+  // Types 1 and 2 reach the decay gradient: fp32 steps at any input type.
   constexpr int NT0 = NSB * NE, NTT = NT0 + 2 * NSB * NE;
   constexpr int MAXT = (NTT + 15) / 16;
   const int nt1 = fact ? NSB * NE : (NSB - 1) * NE, tb1 = fact ? 0 : 1;
@@ -891,7 +1015,7 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
     res[m] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
     if (tau < NT0) {
       const int jb = tau / NE, eb = tau % NE;
-      res[m] = tile_product<kL>(M0, SB * jb, SB * eb, SB * jb, kL - SB * jb,
+      res[m] = tile_product<kL, kBF<TI>>(M0, SB * jb, SB * eb, SB * jb, kL - SB * jb,
                                 [&](int k, int e) { return dy[k][swz<D>(k, e)]; });
     } else if (tau < NT0 + nt1) {
       const int tb = tb1 + (tau - NT0) / NE, db = (tau - NT0) % NE;
@@ -1044,12 +1168,12 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
   const int prod = w / NB, blk = w % NB;
   const int rb = 32 * (blk / NBC), cb = 32 * (blk % NBC);
   floatx16 acc;
-  if (prod == 0) {
+  if (prod == 0) {  // dQe and dKd reach the decay gradient: fp32 steps at any input type
     acc = block_product<D>(dy, rb, cb, zero16(), [&](int k, int j) { return C0s[j][k]; });
   } else if (prod == 1) {
     acc = block_product<D>(vv, rb, cb, zero16(), [&](int k, int j) { return Gs[j][swz<D>(j, k)]; });
   } else if (prod == 2) {
-    acc = block_product<D>(Kd, rb, cb, zero16(), [&](int k, int j) { return Gs[k][swz<D>(k, j)]; });
+    acc = block_product<D, kBF<TI>>(Kd, rb, cb, zero16(), [&](int k, int j) { return Gs[k][swz<D>(k, j)]; });
   }
   __syncthreads();  // every operand read: dy, vv, M2 take the three results (plain)
   float(*Dx)[D] = reinterpret_cast<float(*)[D]>(&M2[0][0]);

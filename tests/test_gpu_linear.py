@@ -241,6 +241,9 @@ def _assert_param_grad(name, x, ref, terms, dtype):
 @pytest.mark.parametrize("B,H,T,D,dtype,a_mean", [
     (2, 2, 300, 64, "bf16", 0.0), (1, 2, 190, 32, "f32", 0.0), (1, 2, 200, 128, "bf16", 0.0),
     (2, 1, 129, 128, "f32", -1.0), (1, 2, 1, 64, "bf16", 0.0), (1, 1, 600, 64, "f32", -4.0),
+    # long sequences: dA_log and d dt_bias sum over every token, so an error in
+    # dg that is coherent over the tokens would outgrow the allowance here
+    (1, 2, 8192, 64, "bf16", 0.0), (1, 1, 2048, 128, "bf16", 0.0),
 ])
 def test_linear_gated(B, H, T, D, dtype, a_mean):
     """The retention gate of eq. 15 formed in the kernels: y and the state, then
