@@ -768,7 +768,7 @@ __global__ __launch_bounds__(kLT2) void linear_out_kernel(LinearArgs a) {
   const int tid = threadIdx.x;
   const float* C0 = a.cprev + ((int64_t)p.n * a.nchunks + p.c) * D * D;
   constexpr int NC0 = D * D / kLT2;  // elements of C0 per thread
-  constexpr bool PREFETCH = NC0 <= 8;
+  constexpr bool PREFETCH = NC0 <= 32;  // 32 registers at D = 128 (two waves per SIMD: LDS-bound)
   float c0r[PREFETCH ? NC0 : 1];
   if constexpr (PREFETCH) {
 #pragma unroll
