@@ -1300,33 +1300,51 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
   s12 = group_sum<kTPRG>(s12);
   const float S = Srow[r];
   const float in1 = s11 > 0.0f ? rsqrtf(s11) : 0.0f, in2 = s22 > 0.0f ? rsqrtf(s22) : 0.0f;
-  // with RoPE the projections below take the rotated p1, p2 (a channel's
-  // partner lives in another thread: the exchange goes through the free qt and
-  // kt arrays, plain layout), and the result goes back through the rotation's
-  // transpose the same way
+  // with RoPE the projections below take the rotated p1, p2, and the result
+  // goes back through the rotation's transpose. A channel's partner lives in
+  // another thread of the row (the row's kTPRG threads are one lane group of
+  // a wave): when it is the same element of that thread (h a multiple of
+  // QW) it comes by a lane shuffle, else through the free qt and kt arrays
+  // (plain layout) between two barriers.
   float(*X1)[D] = qt;
   float(*X2)[D] = kt;
   auto rotate = [&](float(&u1)[QW], float(&u2)[QW], bool transpose) {
-#pragma unroll
-    for (int i = 0; i < QW; ++i) {
-      X1[r][q0 + i] = u1[i];
-      X2[r][q0 + i] = u2[i];
-    }
-    __syncthreads();
     const int h = a.rope_half;
+    float y1[QW], y2[QW];  // the partners' values
+    if (h % QW == 0) {
+      const bool lo = q0 < h;
+      const int src = q0 < 2 * h ? lane + (lo ? h / QW : -(h / QW)) : lane;
+#pragma unroll
+      for (int i = 0; i < QW; ++i) {
+        y1[i] = __shfl(u1[i], src, 64);
+        y2[i] = __shfl(u2[i], src, 64);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < QW; ++i) {
+        X1[r][q0 + i] = u1[i];
+        X2[r][q0 + i] = u2[i];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < QW; ++i) {
+        const int c = q0 + i, pc = c < h ? c + h : c < 2 * h ? c - h : c;
+        y1[i] = X1[r][pc];
+        y2[i] = X2[r][pc];
+      }
+      __syncthreads();
+    }
 #pragma unroll
     for (int i = 0; i < QW; ++i) {
       const int c = q0 + i;
       if (c < 2 * h) {
         const bool lo = c < h;
-        const int pc = lo ? c + h : c - h;
         const float2 cs = rq[i];
         const float sn = transpose ? -cs.y : cs.y;  // R^T: the angle negated
-        u1[i] = lo ? u1[i] * cs.x - X1[r][pc] * sn : X1[r][pc] * sn + u1[i] * cs.x;
-        u2[i] = lo ? u2[i] * cs.x - X2[r][pc] * sn : X2[r][pc] * sn + u2[i] * cs.x;
+        u1[i] = lo ? u1[i] * cs.x - y1[i] * sn : y1[i] * sn + u1[i] * cs.x;
+        u2[i] = lo ? u2[i] * cs.x - y2[i] * sn : y2[i] * sn + u2[i] * cs.x;
       }
     }
-    __syncthreads();
   };
   if (a.rope) rotate(x1, x2, false);
   // dS = dqt . ^p1 + dkt . ^p2; ^p . d^p for the projections
