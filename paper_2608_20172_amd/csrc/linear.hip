@@ -354,8 +354,12 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
 #pragma unroll
   for (int i = 0; i < SR; ++i) bb[sg * SR + i][bcol(sg * SR + i)] = x[i];
   __syncthreads();
-  float off = 0.0f;
-  for (int u = 0; u < sg; ++u) off += bb[u * SR + SR - 1][bcol(u * SR + SR - 1)];
+  float off = 0.0f;  // the totals of the segments above, added in order (reads issued together)
+#pragma unroll
+  for (int u = 0; u < NSEG - 1; ++u) {
+    const float t = bb[u * SR + SR - 1][bcol(u * SR + SR - 1)];
+    if (u < sg) off += t;
+  }
   __syncthreads();  // every segment total read
   if (sg > 0) {
 #pragma unroll
@@ -582,6 +586,46 @@ __device__ __forceinline__ floatx16 block_product(const float (*X)[K], int rb, i
 #pragma unroll
       for (int u = 0; u < 4; ++u) acc = mfma32f(xa[u], B(kk + u, cb + ln), acc);
     }
+  }
+  return acc;
+}
+
+// acc += one 32 x 32 block of X B as block_product, for a row operand X whose
+// values are bf16 numbers (the bf16 inputs, held in fp32) and any fp32 column
+// operand: B is split as b = hi + mid + lo, three bf16 numbers that carry its
+// 24 significant bits, and the block takes three 32x32x16 bf16 steps per 16
+// contraction indices, with the products exact and fp32 accumulation, where
+// fp32 steps take eight.
+template <int K, typename ColOp>
+__device__ __forceinline__ floatx16 block_product_split3(const float (*X)[K], int rb, int cb, floatx16 acc, ColOp B) {
+  constexpr int KH = K / 2;
+  static_assert(KH % 8 == 0, "whole bf16 steps");
+  const int lane = threadIdx.x & 63, ln = lane & 31, lg = lane >> 5;
+  const int xr = rb + ln;
+#pragma unroll 1
+  for (int s0 = 0; s0 < KH; s0 += 8) {
+    const int kk = KH * lg + s0;
+    const floatx4 x0 = *reinterpret_cast<const floatx4*>(&X[xr][swz<K>(xr, kk)]);
+    const floatx4 x1 = *reinterpret_cast<const floatx4*>(&X[xr][swz<K>(xr, kk + 4)]);
+    bf16x8 xv, hv, mv, lv;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      xv[u] = (bf16)x0[u];
+      xv[4 + u] = (bf16)x1[u];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const float b = B(kk + u, cb + ln);
+      const bf16 h = (bf16)b;
+      const float r1 = b - (float)h;
+      const bf16 m = (bf16)r1;
+      hv[u] = h;
+      mv[u] = m;
+      lv[u] = (bf16)(r1 - (float)m);
+    }
+    acc = mfma32(xv, hv, acc);
+    acc = mfma32(xv, mv, acc);
+    acc = mfma32(xv, lv, acc);
   }
   return acc;
 }
@@ -1168,10 +1212,17 @@ __global__ __launch_bounds__(kLTG) void linear_grad_kernel(LinearArgs a) {
   const int prod = w / NB, blk = w % NB;
   const int rb = 32 * (blk / NBC), cb = 32 * (blk % NBC);
   floatx16 acc;
-  if (prod == 0) {  // dQe and dKd reach the decay gradient: fp32 steps at any input type
-    acc = block_product<D>(dy, rb, cb, zero16(), [&](int k, int j) { return C0s[j][k]; });
+  // dQe and dKd reach the decay gradient: fp32 steps, or with bf16 inputs
+  // (dY and v exact in bf16) bf16 steps on C0 and G split in three, which
+  // give the fp32 products
+  auto c0t = [&](int k, int j) { return C0s[j][k]; };
+  auto gt = [&](int k, int j) { return Gs[j][swz<D>(j, k)]; };
+  if (prod == 0) {
+    if constexpr (kBF<TI>) acc = block_product_split3<D>(dy, rb, cb, zero16(), c0t);
+    else acc = block_product<D>(dy, rb, cb, zero16(), c0t);
   } else if (prod == 1) {
-    acc = block_product<D>(vv, rb, cb, zero16(), [&](int k, int j) { return Gs[j][swz<D>(j, k)]; });
+    if constexpr (kBF<TI>) acc = block_product_split3<D>(vv, rb, cb, zero16(), gt);
+    else acc = block_product<D>(vv, rb, cb, zero16(), gt);
   } else if (prod == 2) {
     acc = block_product<D, kBF<TI>>(Kd, rb, cb, zero16(), [&](int k, int j) { return Gs[k][swz<D>(k, j)]; });
   }
