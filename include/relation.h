@@ -260,7 +260,7 @@ typedef enum rel_givens {
 
 typedef enum rel_transport {
   REL_TRANSPORT_FULL = 0,     /* y_i = sum_{j <= i} F_ij v~_j (eq. 3) */
-  REL_TRANSPORT_EXCHANGE = 1  /* exchange-only ablation (App. C): y_i = sum_{j < i} F_ij v~_j,
+  REL_TRANSPORT_EXCHANGE = 1  /* exchange-only ablation (App. D): y_i = sum_{j < i} F_ij v~_j,
                                  the same F, historical weights not renormalised */
 } rel_transport;
 

@@ -72,7 +72,7 @@ def forward(q, k, v, lam, *, tau_s: float = TAU_S, scale: float | None = None,
             transport: str = "full") -> dict:
     """Full Relation forward for one head. q, k, v: [T, D] fp64 arrays.
 
-    ``transport="exchange"`` is the exchange-only ablation (App. C, ablation
+    ``transport="exchange"`` is the exchange-only ablation (App. D, ablation
     definitions): the same F, but Y_i = sum_{j<i} F_ij I~_j, without the Self
     term and without renormalising the historical weights.
 

@@ -297,7 +297,7 @@ def check_row_blocking(orc):
 
 
 # ---------------------------------------------------------------------------
-# 7. Exchange-only transport (App. C, ablation definitions): the same flow F,
+# 7. Exchange-only transport (App. D, ablation definitions): the same flow F,
 #    Y_i = sum_{j<i} F_ij I~_j, historical weights not renormalised
 # ---------------------------------------------------------------------------
 def check_exchange_only(orc):

@@ -121,7 +121,7 @@ def test_layer_fp32(D, pairing, rope):
     (64, "A", 1.0e4, "bf16", 1600),  # the one-kernel backward (T >= 1536)
 ])
 def test_layer_exchange_only(D, pairing, rope, dtype, T):
-    """The exchange-only ablation (App. C): y_i = sum_{j<i} F_ij v~_j, forward and backward."""
+    """The exchange-only ablation (App. D): y_i = sum_{j<i} F_ij v~_j, forward and backward."""
     std = 1.0 if dtype == "f32" else None
     x = _prep(1 if dtype == "f32" else 2, 4, T, D, dtype, seed=900 + D + T, std=std)
     f, g = check_layer(x, dtype, pairing, rope, transport="exchange")
