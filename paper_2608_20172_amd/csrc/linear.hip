@@ -440,6 +440,38 @@ __device__ __forceinline__ floatx16 gram_block(const float (*X)[D], const float 
   return acc;
 }
 
+// gram_block for a right operand Y whose values are bf16 numbers (the bf16
+// inputs, held in fp32): X is split as hi + mid + lo, three bf16 numbers that
+// carry its 24 significant bits, so the three 32x32x16 bf16 steps per 16 rows
+// give exact products with fp32 accumulation, as the fp32 steps would.
+template <int D>
+__device__ __forceinline__ floatx16 gram_block_split3(const float (*X)[D], const float (*Y)[D], int ab, int eb) {
+  const int lane = threadIdx.x & 63, ln = lane & 31, lg = lane >> 5;
+  floatx16 acc;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
+#pragma unroll 1
+  for (int s = 0; s < kL / 16; ++s) {
+    bf16x8 hv, mv, lv, yv;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int r = 16 * s + 2 * u + lg;
+      const float x = X[r][ab + ln];
+      const bf16 h = (bf16)x;
+      const float r1 = x - (float)h;
+      const bf16 m = (bf16)r1;
+      hv[u] = h;
+      mv[u] = m;
+      lv[u] = (bf16)(r1 - (float)m);
+      yv[u] = (bf16)Y[r][eb + ln];
+    }
+    acc = mfma32(hv, yv, acc);
+    acc = mfma32(mv, yv, acc);
+    acc = mfma32(lv, yv, acc);
+  }
+  return acc;
+}
+
 // Stores a 32 x 32 accumulator block at (ab, eb) of a dense D x D matrix.
 template <int D>
 __device__ __forceinline__ void store_block(float* out, const floatx16& acc, int ab, int eb) {
@@ -906,9 +938,12 @@ __global__ __launch_bounds__(kLT) void linear_bstate_kernel(LinearArgs a) {
   constexpr int NBE = D / 32, NBB = NBE * NBE;
   for (int bk = __builtin_amdgcn_readfirstlane(tid >> 6); bk < 2 * NBB; bk += kLT / 64) {
     const int ab = 32 * ((bk % NBB) / NBE), eb = 32 * (bk % NBE);
-    // fp32 steps at any input type: C0 and G reach the decay gradient
-    if (bk < NBB) store_block<D>(a.dstate + base * D * D, gram_block<D>(kt, vv, ab, eb), ab, eb);
-    else store_block<D>(a.pstate + base * D * D, gram_block<D>(qt, dy, ab, eb), ab, eb);
+    // C0 and G reach the decay gradient: fp32 steps, or with bf16 inputs
+    // (v and dY exact in bf16) bf16 steps on Kd and Qe split in three
+    floatx16 acc;
+    if constexpr (kBF<TI>) acc = bk < NBB ? gram_block_split3<D>(kt, vv, ab, eb) : gram_block_split3<D>(qt, dy, ab, eb);
+    else acc = bk < NBB ? gram_block<D>(kt, vv, ab, eb) : gram_block<D>(qt, dy, ab, eb);
+    store_block<D>((bk < NBB ? a.dstate : a.pstate) + base * D * D, acc, ab, eb);
   }
 }
 
