@@ -127,6 +127,15 @@ def test_linear_backward_retention_range(gmax, D):
     check_linear_bwd(x, "f32")
 
 
+@pytest.mark.parametrize("D,gmax", [(64, 1e-3), (64, 8.0), (64, 80.0), (128, 80.0)])
+def test_linear_backward_retention_range_bf16(D, gmax):
+    """The same retention range with bf16 inputs, where the chunk products
+    take bf16 operands: decay factors down to underflow inside the operands."""
+    x = _prep(1, 2, 200, D, "bf16", seed=1550 + D, gmax=gmax)
+    check_linear_fwd(x, "bf16")
+    check_linear_bwd(x, "bf16")
+
+
 def test_linear_backward_long():
     x = _prep(1, 2, 2048, 64, "bf16", seed=1600, gmax=0.05)
     check_linear_bwd(x, "bf16", heads=[(0, 1)])
@@ -312,7 +321,8 @@ def test_linear_mixed_decay_chunks(D, dtype):
 
 
 @pytest.mark.parametrize("width,padded,T,dtype", [(64, 64, 300, "bf16"), (32, 32, 190, "f32"), (128, 128, 200, "bf16"),
-                                                   (80, 128, 260, "f32"), (60, 64, 129, "f32"), (48, 64, 200, "bf16")])
+                                                   (80, 128, 260, "f32"), (60, 64, 129, "f32"), (48, 64, 200, "bf16"),
+                                                   (80, 128, 300, "bf16")])
 def test_linear_gated_rope(width, padded, T, dtype):
     """RoPE (base 1e4) on p1, p2 inside the gated kernels, over the true width
     of a head zero-padded to a kernel width: y, dp1, dp2, dv, dr, dA_log and
