@@ -516,6 +516,22 @@ constexpr int kSegChunks = 16;
 __device__ __forceinline__ int seg_begin(int s) { return s * kSegChunks; }
 __device__ __forceinline__ int seg_end(const LinearArgs& a, int s) { return min(a.nchunks, (s + 1) * kSegChunks); }
 
+// The retention row and one state element of every chunk of segment [c0, c1)
+// (in reverse order with REV), all loads issued before any is used: the walk
+// over the chunks is a dependent chain, and loading inside it left one
+// round trip per step. Slots past the segment repeat its last (first) chunk
+// and are not used.
+template <bool REV>
+__device__ __forceinline__ void load_segment(const float* gamma, const float* st, int64_t hb, int c0, int c1, int D,
+                                             int ar, int64_t idx, float (&gv)[kSegChunks], float (&sv)[kSegChunks]) {
+#pragma unroll
+  for (int k = 0; k < kSegChunks; ++k) {
+    const int c = REV ? max(c1 - 1 - k, c0) : min(c0 + k, c1 - 1);
+    gv[k] = gamma[(hb + c) * D + ar];
+    sv[k] = st[(hb + c) * D * D + idx];
+  }
+}
+
 __global__ __launch_bounds__(256) void linear_seg_kernel(LinearArgs a, int reverse) {
   const int D = a.D;
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -524,20 +540,25 @@ __global__ __launch_bounds__(256) void linear_seg_kernel(LinearArgs a, int rever
   const int ar = (int)(idx / D);
   const int c0 = seg_begin(s), c1 = seg_end(a, s);
   const int64_t hb = (int64_t)n * a.nchunks;
+  float gv[kSegChunks], sv[kSegChunks];
+  load_segment<false>(a.gamma, a.dstate, hb, c0, c1, D, ar, idx, gv, sv);
   float C = 0.0f, prod = 1.0f;
-#pragma unroll 4
-  for (int c = c0; c < c1; ++c) {
-    const float gm = a.gamma[(hb + c) * D + ar];
-    C = gm * C + a.dstate[(hb + c) * D * D + idx];
-    prod *= gm;
+#pragma unroll
+  for (int k = 0; k < kSegChunks; ++k) {
+    if (c0 + k < c1) {
+      C = gv[k] * C + sv[k];
+      prod *= gv[k];
+    }
   }
   const int64_t sb = (int64_t)n * a.nseg + s;
   a.segc[sb * D * D + idx] = C;
   if (idx % D == 0) a.segg[sb * D + ar] = prod;
   if (reverse) {
+    load_segment<true>(a.gamma, a.pstate, hb, c0, c1, D, ar, idx, gv, sv);
     float G = 0.0f;
-#pragma unroll 4
-    for (int c = c1 - 1; c >= c0; --c) G = a.gamma[(hb + c) * D + ar] * G + a.pstate[(hb + c) * D * D + idx];
+#pragma unroll
+    for (int k = 0; k < kSegChunks; ++k)
+      if (c1 - 1 - k >= c0) G = gv[k] * G + sv[k];
     a.segp[sb * D * D + idx] = G;
   }
 }
@@ -550,23 +571,30 @@ __global__ __launch_bounds__(256) void linear_seg_apply_kernel(LinearArgs a, int
   const int ar = (int)(idx / D);
   const int c0 = seg_begin(s), c1 = seg_end(a, s);
   const int64_t hb = (int64_t)n * a.nchunks, sh = (int64_t)n * a.nseg;
+  float gv[kSegChunks], sv[kSegChunks];
+  load_segment<false>(a.gamma, a.dstate, hb, c0, c1, D, ar, idx, gv, sv);
   float C = 0.0f;
 #pragma unroll 4
   for (int u = 0; u < s; ++u) C = a.segg[(sh + u) * D + ar] * C + a.segc[(sh + u) * D * D + idx];
-#pragma unroll 4
-  for (int c = c0; c < c1; ++c) {
-    a.cprev[(hb + c) * D * D + idx] = C;
-    C = a.gamma[(hb + c) * D + ar] * C + a.dstate[(hb + c) * D * D + idx];
+#pragma unroll
+  for (int k = 0; k < kSegChunks; ++k) {
+    if (c0 + k < c1) {
+      a.cprev[(hb + c0 + k) * D * D + idx] = C;
+      C = gv[k] * C + sv[k];
+    }
   }
   if (a.state_out && s == a.nseg - 1) a.state_out[(int64_t)n * D * D + idx] = C;
   if (reverse) {
+    load_segment<true>(a.gamma, a.pstate, hb, c0, c1, D, ar, idx, gv, sv);
     float G = 0.0f;
 #pragma unroll 4
     for (int u = a.nseg - 1; u > s; --u) G = a.segg[(sh + u) * D + ar] * G + a.segp[(sh + u) * D * D + idx];
-#pragma unroll 4
-    for (int c = c1 - 1; c >= c0; --c) {
-      a.gout[(hb + c) * D * D + idx] = G;
-      G = a.gamma[(hb + c) * D + ar] * G + a.pstate[(hb + c) * D * D + idx];
+#pragma unroll
+    for (int k = 0; k < kSegChunks; ++k) {
+      if (c1 - 1 - k >= c0) {
+        a.gout[(hb + c1 - 1 - k) * D * D + idx] = G;
+        G = gv[k] * G + sv[k];
+      }
     }
   }
 }
