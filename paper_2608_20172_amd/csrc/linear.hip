@@ -375,12 +375,14 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
 // of its row of the left operand and of its column of the right operand at the
 // same contraction indices; which indices go to which lane and slot does not
 // matter to the sum, so each lane keeps the index range it has on the fp32 path.
-// The backward keeps fp32 steps for every product that reaches the gradient
-// of the decay (dq, dk, and the states C0 and G): that gradient is a small
-// difference of large terms (the scores depend on b only through b_t - b_j,
-// so the intra-chunk parts of qt dq and kt dk cancel over a chunk), and
-// operands rounded to bf16 leave a residual of their rounding in it that adds
-// up coherently over the tokens in dA_log.
+// The backward keeps fp32 accuracy in every product that reaches the
+// gradient of the decay (dq, dk, and the states C0 and G): fp32 steps, or,
+// where one operand is a bf16 input, bf16 steps with the other split in three
+// bf16 parts (exact products). That gradient is a small difference of large
+// terms (the scores depend on b only through b_t - b_j, so the intra-chunk
+// parts of qt dq and kt dk cancel over a chunk), and operands rounded to bf16
+// leave a residual of their rounding in it that adds up coherently over the
+// tokens in dA_log.
 template <typename TI> constexpr bool kBF = sizeof(TI) == 2;
 
 template <int N>
