@@ -5,9 +5,11 @@ MI355X: forward + backward tokens/s on the 100M-decoder-scale layer
 
 One step = relation_fwd + relation_bwd over the whole batch, inputs resident
 in HBM. Prints one JSON line. Extra legs: the materialised baseline's forward
-(for the speedup), per-kernel durations from HIP events recorded around the
-fused kernels inside the timed region, and the fp64 oracle on a bounded sample
-of heads on the host cores.
+and backward (for the speedups), per-kernel durations from HIP events
+recorded around the fused kernels inside the timed region, the measured MFMA
+peak, the other decoder-scale and long-context workloads, the layer entry
+points at the paper's 100M geometry, decode steps, Linear Relation, and the
+fp64 oracle on a bounded sample of heads on the host cores.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
   python bench.py --copy-bytes N   # plain device copy of N bytes (counter calibration)
