@@ -191,15 +191,10 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
     static_assert(LPR >= 2 && LPR <= 64 && EPL % 4 == 0, "a row is whole 16-byte chunks over a lane group");
     constexpr int STEPS = (kL + NW * RPI - 1) / (NW * RPI);
     const int cg = lane % LPR, c0 = cg * EPL;
-    float ea[EPL], dtb[EPL];  // the gate's parameters of this lane's channels
-    if (a.a_log) {
-      const int64_t pc = (int64_t)(hr.n % a.H) * GW + hr.pa + c0;
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) {
-        ea[e] = fast_exp2(a.a_log[pc + e] * kLog2e);
-        dtb[e] = a.dt_bias[pc + e];
-      }
-    }
+    // the gate's parameters of this lane's channels: read with the rows (their
+    // loads issued before anything waits), A_log turned into exp(A_log) at use
+    const float* AL = a.a_log ? a.a_log + (int64_t)(hr.n % a.H) * GW + hr.pa + c0 : nullptr;
+    const float* DB = a.a_log ? a.dt_bias + (int64_t)(hr.n % a.H) * GW + hr.pa + c0 : nullptr;
 #pragma unroll
     for (int st = 0; st < STEPS; ++st) {
       const int r = st * NW * RPI + w * RPI + lane / LPR;
@@ -216,9 +211,12 @@ __device__ __forceinline__ void load_chunk(const LinearArgs& a, const ChunkPos& 
         Vec16<TI>::load(V + row * a.st + c0, vx);
         if constexpr (WITH_DY) Vec16<TI>::load(DY + row * a.st + c0, dx);
         load_f32<EPL>(G + row * GW + c0, gx);
-        if (a.a_log) {
+        if (AL) {
+          float al[EPL], dtb[EPL];
+          load_f32<EPL>(AL, al);
+          load_f32<EPL>(DB, dtb);
 #pragma unroll
-          for (int e = 0; e < EPL; ++e) gx[e] = kda_gate(gx[e], ea[e], dtb[e]);
+          for (int e = 0; e < EPL; ++e) gx[e] = kda_gate(gx[e], fast_exp2(al[e] * kLog2e), dtb[e]);
         }
         const bool ok = r < p.len;
         float s11 = 0.0f, s22 = 0.0f, s12 = 0.0f;

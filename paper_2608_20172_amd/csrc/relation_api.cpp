@@ -1250,7 +1250,7 @@ static LinearPlan plan_linear(const rel_problem* p, bool split) {
 
 // The chunk loads (and the gradient stores) move 16 bytes per lane when every
 // row of p1, p2, v (and dY, dp1, dp2, dv) starts on a 16-byte boundary and g
-// is 16-byte aligned.
+// (with the gate: r, A_log and dt_bias) is 16-byte aligned.
 static int linear_vec16(const rel_problem* p, std::initializer_list<const void*> rows, const float* g) {
   const int64_t epl = 16 / (int64_t)elem_size(p->dtype);
   if (p->stride_b % epl || p->stride_h % epl || p->stride_t % epl || ((uintptr_t)g & 15)) return 0;
@@ -1369,7 +1369,7 @@ static rel_status linear_fwd_impl(const rel_problem* p, const void* p1, const vo
   a.inv_tau = 1.0f / p->tau_s;
   a.nchunks = linear_chunks(p);
   a.nseg = linear_segments(p);
-  a.vec16 = linear_vec16(p, {p1, p2, v}, g);
+  a.vec16 = linear_vec16(p, {p1, p2, v, a_log, dt_bias}, g);
   set_linear_workspace(a, L, (char*)workspace, false);
   REL_TRY(set_rope(a, p, rope_dim, rope_base, (char*)workspace, L.total, (hipStream_t)stream));
   const hipError_t e = rel::launch_linear_fwd(a, p->dtype, (hipStream_t)stream);
@@ -1466,7 +1466,7 @@ static rel_status linear_bwd_impl(const rel_problem* p, const void* p1, const vo
   a.inv_tau = 1.0f / p->tau_s;
   a.nchunks = linear_chunks(p);
   a.nseg = linear_segments(p);
-  a.vec16 = linear_vec16(p, {p1, p2, v, dout, dp1, dp2, dv}, g);
+  a.vec16 = linear_vec16(p, {p1, p2, v, dout, dp1, dp2, dv, gated ? a_log : nullptr, gated ? dt_bias : nullptr}, g);
   set_linear_workspace(a, L, (char*)workspace, true);
   if (gated) {
     a.a_log = a_log; a.dt_bias = dt_bias;

@@ -291,6 +291,36 @@ def test_linear_gated(B, H, T, D, dtype, a_mean):
     _assert_param_grad("ddt_bias", _np(o["ddt_bias"]), dt_ref, dt_terms, dtype)
 
 
+def test_linear_gated_unaligned_params():
+    """A_log and dt_bias at addresses that are not 16-byte aligned (views one
+    element into a buffer) take the element-wise chunk loads; y, the state and
+    every gradient agree with the oracle as with aligned parameters."""
+    B, H, T, D = 1, 2, 150, 64
+    x = _prep(B, H, T, D, "bf16", seed=1970, with_dout=True)
+    rng = np.random.default_rng(1971)
+    r = (2.0 * rng.standard_normal((B, H, T, D))).astype(np.float32)
+    a_log, dt_bias = _gate_params(H, D, 1972)
+    rt = torch.from_numpy(r).cuda()
+    abuf = torch.zeros(H * D + 1, dtype=torch.float32, device="cuda")
+    bbuf = torch.zeros(H * D + 1, dtype=torch.float32, device="cuda")
+    abuf[1:] = torch.from_numpy(a_log.ravel()).cuda()
+    bbuf[1:] = torch.from_numpy(dt_bias.ravel()).cuda()
+    at, bt = abuf[1:].view(H, D), bbuf[1:].view(H, D)
+    assert at.data_ptr() % 16 and bt.data_ptr() % 16
+    f = R.relation_linear_gated_fwd(x["p1"], x["p2"], x["v"], rt, at, bt, want_state=True)
+    o = R.relation_linear_gated_bwd(x["p1"], x["p2"], x["v"], rt, at, bt, x["dy"])
+    torch.cuda.synchronize()
+    for h in range(H):
+        g = LO.kda_gate(r[0, h], a_log[h], dt_bias[h])
+        ref_f = LO.forward(x["p1r"][0, h], x["p2r"][0, h], x["vr"][0, h], g)
+        assert_close(f"y[0,{h}]", _np(f["o"])[0, h], ref_f["Y"], "bf16")
+        ref_b = LO.backward(x["p1r"][0, h], x["p2r"][0, h], x["vr"][0, h], g, x["dyr"][0, h])
+        gb = LO.kda_gate_backward(r[0, h], a_log[h], dt_bias[h], ref_b["dg"])
+        for n in ("dp1", "dp2", "dv"):
+            assert_close(f"{n}[0,{h}]", _np(o[n])[0, h], ref_b[n], "bf16")
+        assert_close(f"dr[0,{h}]", _np(o["dr"])[0, h], gb["dr"], "bf16")
+
+
 def test_linear_gated_repeatable():
     x = _prep(2, 2, 700, 64, "bf16", seed=1990)
     rng = np.random.default_rng(1991)
