@@ -345,7 +345,11 @@ rel_status relation_decode_merge(const rel_problem* p, int32_t nstates, const fl
  *   workspace  relation_linear_fwd_workspace_bytes(p) bytes, 16-byte aligned:
  *              per chunk of 64 tokens its state contribution and retention
  *              product, and the state entering it; per segment of 16 chunks
- *              the scan's summary (fp32). */
+ *              the scan's summary (fp32).
+ * Precision: fp32 inputs run every product in fp32. bf16 inputs take the
+ * chunk products on bf16 operands with fp32 accumulation, except that the
+ * backward keeps fp32 accuracy in the products that reach dg (and so dr,
+ * dA_log, d dt_bias); decay weights, state scans and statistics are fp32. */
 size_t relation_linear_fwd_workspace_bytes(const rel_problem* p);
 rel_status relation_linear_fwd(const rel_problem* p, const void* p1, const void* p2, const void* v,
                                const float* g, void* out, float* state_out, void* workspace,
